@@ -1,0 +1,407 @@
+"""AATC oracle: calibration, encoding and exact decode attention (NumPy, fp64).
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).  Citations name the paper's
+sections, equations, algorithms and tables ("KV Cache Compression Through the Lens of
+Transform Coding").
+
+What is computed, step by step
+------------------------------
+Calibration (Alg. 1, offline part; Sec. 5.1 and 5.2), per KV head and tensor (K or V):
+  1. Sigma = X^T X / n, the uncentered empirical covariance of the calibration
+     samples (Sec. 5.1).
+  2. Its eigendecomposition, sorted by decreasing eigenvalue.  The PCA basis P is the
+     decorrelating transform.  The Proposition of App. D shows it spans the same
+     channels as the whitening-based SVD; the two differ only by a per-channel scale,
+     which changes neither the codes nor the products w_c * sigma_c^2 used by the
+     allocation.
+  3. Attention-aware channel weights (eq. waterfilling-keys and its GQA remark in
+     App. B for keys; the value weight of Sec. 5.2).  w = 1 when no queries / W_O are
+     given ("AATC var-only", Sec. 6).
+  4. Integer reverse water-filling: minimize sum_c W_c 2^(-2 b_c) with W_c =
+     w_c sigma_c^2, subject to sum_c b_c = B and b_c in {0..b_max} (eq.
+     waterfilling-keys; Alg. 1).
+  5. Per-channel scale s_c = 99th percentile of |h_c| over the calibration tokens
+     (Sec. 5.2, "The right scaling").
+Encoding (Alg. 1, online part; Sec. 5.2), per token and head:
+  6. h = T^T x (eq. transformed-cache), computed by the canonical fixed-point
+     arithmetic below.
+  7. alpha = max_c |h_c / s_c| over the stored channels; the signed uniform quantizer
+     with step Delta_c = 2 alpha s_c / 2^b_c (Sec. 5.2).
+  8. Bit packing of the codes (layout defined below; the paper is silent on it).
+Decode attention (Alg. 1, online part; Def. 1):
+  9. Reconstruct K = H^ T^T and V = H^ T^T, then o = softmax(q K^T / sqrt(d)) V in fp64.
+
+Readings where the paper is silent or ambiguous (each listed in the design doc)
+----------------------------------------------------------------------------
+* The integer allocation (the paper names an unspecified "dynamic program"): greedy
+  marginal allocation, one bit at a time to argmax_c W_c 4^(-b_c) among channels
+  below b_max, ties to the lowest eigen index.  This is exactly optimal for the
+  separable convex problem and spends exactly B = round(avg_bits * d) bits.
+* Var-only weights are w = 1 on the orthonormal PCA coefficients (W_c = eigenvalue),
+  the reconstruction-error criterion the paper equates with per-layer KVTC.
+* alpha is taken over the stored channels only (zero-bit channels are not cached).
+* Canonical arithmetic, so that codes are reproducible bit for bit: the transform is
+  evaluated exactly in integers on a per-token fixed-point x (13 fractional bits below
+  the token's leading bit) and a fixed-point T (14 fractional bits); the quantizer is
+  the fp32 sequence of ``quantize``.  alpha and s_c are stored as fp16.
+* Storage order of channels: stable sort by bit width, widest first (eigen order
+  breaks ties), so dropped channels form a suffix.
+
+Parity unpinned (spec choices with no value in the paper to check against): the
+percentile interpolation (linear between order statistics), the storage order and
+the packing layout.  The tests pin them to worked examples of this spec.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import numpy as np
+
+# Canonical fixed-point transform parameters (see module docstring).
+X_LEAD_BIT = 13      # the largest |x_j| of a token maps into [2^13, 2^14)
+T_FRAC_BITS = 14     # T entries are multiples of 2^-14
+TILE_TOKENS = 64     # tokens per tile of the value-cache layout
+FP16_MAX = 65504.0
+
+
+# --------------------------------------------------------------------------------------
+# Calibration
+# --------------------------------------------------------------------------------------
+def covariance(x: np.ndarray) -> np.ndarray:
+    """Uncentered empirical covariance Sigma = X^T X / n (Sec. 5.1)."""
+    x = np.asarray(x, dtype=np.float64)
+    return x.T @ x / x.shape[0]
+
+
+def pca_basis(sigma: np.ndarray):
+    """Eigenvectors of Sigma by decreasing eigenvalue, sign-canonicalized.
+
+    Returns (P, lam): columns of P are orthonormal eigenvectors; lam the eigenvalues
+    (the channel variances sigma_c^2 of Sec. 5.1 / App. B).  The sign of each column
+    makes its largest-magnitude entry positive (the lowest row index wins a tie).
+    """
+    lam, vec = np.linalg.eigh(sigma)
+    order = np.argsort(-lam, kind="stable")
+    lam = lam[order]
+    vec = vec[:, order]
+    for c in range(vec.shape[1]):
+        col = vec[:, c]
+        j = int(np.argmax(np.abs(col)))   # first index of the maximum magnitude
+        if col[j] < 0:
+            vec[:, c] = -col
+    return vec, lam
+
+
+def key_weights(p: np.ndarray, q_calib: np.ndarray, group: int) -> np.ndarray:
+    """w_c = (1/T) sum over the group's query heads and tokens of (P_c^T q)^2.
+
+    eq. waterfilling-keys, with the GQA remark of App. B (sum over the query heads
+    that share this KV head).  ``q_calib`` stacks the group's calibration queries,
+    [group * T, d].
+    """
+    proj = np.asarray(q_calib, dtype=np.float64) @ p
+    t = q_calib.shape[0] // group
+    return (proj ** 2).sum(axis=0) / t
+
+
+def value_weights(p: np.ndarray, w_o: np.ndarray) -> np.ndarray:
+    """w_c = || (P^T W_O)_c ||^2, the value weight of Sec. 5.2 (W_O rows of this head)."""
+    m = p.T @ np.asarray(w_o, dtype=np.float64)
+    return (m ** 2).sum(axis=1)
+
+
+def rwf_continuous(var: np.ndarray, avg_bits: float):
+    """Classical reverse water-filling, closed form (Sec. 3.1, eq. bit-allocation).
+
+    b_i = max(0, 1/2 log2(var_i / lam)) with the water level lam set so that the mean
+    of b equals avg_bits.  Returns (lam, b).  The active set is found by trying the k
+    largest variances, k = d .. 1.
+    """
+    var = np.asarray(var, dtype=np.float64)
+    d = var.size
+    order = np.argsort(-var, kind="stable")
+    v = var[order]
+    for k in range(d, 0, -1):
+        # sum_{i<k} 1/2 log2(v_i / lam) = d * avg_bits
+        log2_lam = (np.sum(np.log2(v[:k])) - 2.0 * d * avg_bits) / k
+        lam = 2.0 ** log2_lam
+        if v[k - 1] > lam and (k == d or v[k] <= lam):
+            b = np.zeros(d)
+            b[order[:k]] = 0.5 * np.log2(v[:k] / lam)
+            return lam, b
+    raise ValueError("no water level found")
+
+
+def allocate_bits(w_var: np.ndarray, budget: int, b_max: int) -> np.ndarray:
+    """Integer reverse water-filling by greedy marginal allocation (reading of Sec. 5.2).
+
+    Each of the ``budget`` bits goes to argmax_c W_c 4^(-b_c) over channels with
+    b_c < b_max (first index on ties).  Adding a bit to channel c lowers the objective
+    sum_c W_c 2^(-2 b_c) by 3/4 W_c 4^(-b_c); those gains shrink geometrically per
+    channel, so the greedy result is a global optimum of the separable problem.
+    """
+    w_var = np.asarray(w_var, dtype=np.float64)
+    d = w_var.size
+    if budget > d * b_max or budget < 0:
+        raise ValueError("budget outside [0, d * b_max]")
+    b = np.zeros(d, dtype=np.int64)
+    for _ in range(budget):
+        gain = np.where(b < b_max, np.ldexp(w_var, -2 * b), -np.inf)
+        c = int(np.argmax(gain))
+        b[c] += 1
+    return b
+
+
+def allocation_objective(w_var: np.ndarray, bits: np.ndarray) -> float:
+    """sum_c W_c 2^(-2 b_c) (eq. waterfilling-keys)."""
+    return float(np.sum(np.ldexp(np.asarray(w_var, dtype=np.float64), -2 * np.asarray(bits))))
+
+
+def to_f16(x) -> np.ndarray:
+    """Round to fp16 (nearest, ties to even), saturating at the largest finite value."""
+    x = np.asarray(x, dtype=np.float64)
+    return np.clip(x, -FP16_MAX, FP16_MAX).astype(np.float16)
+
+
+@dataclasses.dataclass
+class Calibration:
+    """Calibration artifact of one (KV head, K or V); channels in storage order."""
+
+    d: int
+    budget: int               # B = sum of bits
+    record_bytes: int         # R = 4 * ceil(B / 32)
+    d_active: int             # channels with at least one bit
+    bits: np.ndarray          # [d] int64, storage order, non-increasing
+    perm: np.ndarray          # [d] eigen index of each storage channel
+    T64: np.ndarray           # [d, d] fp64, column c = eigenvector of storage channel c
+    T32: np.ndarray           # [d, d] fp32 rounding of T64 (the transform the path uses)
+    s16: np.ndarray           # [d] fp16 per-channel scales (0 for dropped channels)
+    sigma2: np.ndarray        # [d] eigenvalues, eigen order
+    weight: np.ndarray        # [d] channel weights, eigen order
+    bits_eig: np.ndarray      # [d] bits, eigen order
+
+
+def calibrate(x_calib: np.ndarray, avg_bits: float, b_max: int = 8,
+              percentile: float = 0.99, q_calib: Optional[np.ndarray] = None,
+              group: int = 1, w_o: Optional[np.ndarray] = None) -> Calibration:
+    """Alg. 1 (calibration) for one KV head and one tensor.
+
+    ``q_calib`` (keys) or ``w_o`` (values) select the attention-aware weights; with
+    neither, w = 1 (var-only).  The budget is B = round(avg_bits * d) bits per token.
+    """
+    x = np.asarray(x_calib, dtype=np.float64)
+    n, d = x.shape
+    if n < 2:
+        raise ValueError("need at least 2 calibration samples")
+    budget = int(np.floor(avg_bits * d + 0.5))
+    p, lam = pca_basis(covariance(x))
+    if q_calib is not None:
+        w = key_weights(p, q_calib, group)
+    elif w_o is not None:
+        w = value_weights(p, w_o)
+    else:
+        w = np.ones(d)
+    w_var = w * lam
+    bits_eig = allocate_bits(w_var, budget, b_max)
+    perm = np.argsort(-bits_eig, kind="stable")
+    bits = bits_eig[perm]
+    t64 = p[:, perm]
+    t32 = t64.astype(np.float32)
+    # Per-channel scale: 99th percentile of |h_c| over the calibration tokens.
+    h = x @ t64
+    s = np.zeros(d)
+    for c in range(d):
+        if bits[c] > 0:
+            s[c] = np.percentile(np.abs(h[:, c]), 100.0 * percentile)
+    s16 = to_f16(s)
+    s16[bits == 0] = 0
+    return Calibration(d=d, budget=budget, record_bytes=4 * ((budget + 31) // 32),
+                       d_active=int(np.count_nonzero(bits)), bits=bits, perm=perm,
+                       T64=t64, T32=t32, s16=s16, sigma2=lam, weight=w,
+                       bits_eig=bits_eig)
+
+
+# --------------------------------------------------------------------------------------
+# Encoding
+# --------------------------------------------------------------------------------------
+def fixed_point_transform(x32: np.ndarray, t32: np.ndarray) -> np.ndarray:
+    """h = T^T x per token (eq. transformed-cache) in canonical fixed-point arithmetic.
+
+    x is scaled per token by 2^S so its largest magnitude lies in [2^13, 2^14) and
+    rounded to integers (ties to even); T is rounded to multiples of 2^-14.  The
+    integer dot products are exact; the result is rounded once to fp32 (ties to even).
+    """
+    x = np.asarray(x32, dtype=np.float32).astype(np.float64)
+    m = np.max(np.abs(x), axis=1) if x.shape[1] else np.zeros(x.shape[0])
+    e = np.frexp(m)[1].astype(np.int64) - 1          # floor(log2 m) for m > 0
+    shift = np.where(m > 0, X_LEAD_BIT - e, 0)
+    xi = np.rint(np.ldexp(x, shift[:, None])).astype(np.int64)
+    ti = np.rint(np.ldexp(np.asarray(t32, dtype=np.float32).astype(np.float64),
+                          T_FRAC_BITS)).astype(np.int64)
+    hi = xi @ ti
+    return np.ldexp(hi.astype(np.float64), -(shift + T_FRAC_BITS)[:, None]).astype(np.float32)
+
+
+def inverse_f32(v: np.ndarray) -> np.ndarray:
+    """fp32 1/v rounded to nearest, and 0 where v == 0."""
+    v = np.asarray(v, dtype=np.float32)
+    safe = np.where(v != 0, v, np.float32(1))
+    return np.where(v != 0, np.float32(1) / safe, np.float32(0)).astype(np.float32)
+
+
+def quantize(h32: np.ndarray, bits: np.ndarray, s16: np.ndarray):
+    """Signed uniform quantizer with per-token scale alpha (Sec. 5.2).
+
+    For each token: alpha = max_c |h_c / s_c| over channels with b_c >= 1; with
+    Delta_c = 2 alpha s_c / 2^b_c the code is clamp(floor(h_c / Delta_c + 1/2),
+    -2^(b-1), 2^(b-1) - 1), stored unsigned as u = code + 2^(b-1).
+    The canonical fp32 evaluation is r = h * (1/s), alpha16 = fp16(max |r|),
+    y = r * (1/alpha16), x = y * 2^(b-1), code = floor(x + 1/2) taken exactly.
+    Returns (u [n, d] int64 with 0 for dropped channels, alpha16 [n] fp16).
+    """
+    h = np.asarray(h32, dtype=np.float32)
+    bits = np.asarray(bits, dtype=np.int64)
+    keep = bits > 0
+    inv_s = inverse_f32(np.asarray(s16, dtype=np.float16).astype(np.float32))
+    r = (h * inv_s[None, :]).astype(np.float32)
+    if np.any(keep):
+        alpha = np.max(np.abs(r[:, keep]), axis=1)
+    else:
+        alpha = np.zeros(h.shape[0], dtype=np.float32)
+    alpha16 = to_f16(alpha)
+    inv_a = inverse_f32(alpha16.astype(np.float32))
+    y = (r * inv_a[:, None]).astype(np.float32)
+    x = np.ldexp(y, np.maximum(bits - 1, 0)[None, :]).astype(np.float32)
+    f = np.floor(x)
+    code = f + ((x - f) >= np.float32(0.5))
+    half = np.left_shift(1, np.maximum(bits - 1, 0))
+    lo = np.where(keep, -half, 0)
+    hi = np.where(keep, half - 1, 0)
+    code = np.clip(code.astype(np.int64), lo[None, :], hi[None, :])
+    u = np.where(keep[None, :], code + half[None, :], 0)
+    return u.astype(np.int64), alpha16
+
+
+def dequantize(u: np.ndarray, alpha16: np.ndarray, bits: np.ndarray,
+               s16: np.ndarray) -> np.ndarray:
+    """h^_c = Delta_c * code = alpha s_c 2^(1-b_c) (u_c - 2^(b_c-1)); 0 for b_c = 0."""
+    bits = np.asarray(bits, dtype=np.int64)
+    keep = bits > 0
+    s = np.asarray(s16, dtype=np.float16).astype(np.float64)
+    a = np.asarray(alpha16, dtype=np.float16).astype(np.float64)
+    half = np.where(keep, np.ldexp(1.0, np.maximum(bits - 1, 0)), 0.0)
+    step = np.where(keep, s * np.ldexp(1.0, 1 - bits), 0.0)
+    return a[:, None] * step[None, :] * (np.asarray(u, dtype=np.float64) - half[None, :])
+
+
+# --------------------------------------------------------------------------------------
+# Packing (the paper does not specify one; this is the layout the path defines)
+# --------------------------------------------------------------------------------------
+def pack_records(u: np.ndarray, bits: np.ndarray) -> np.ndarray:
+    """Token-major records: the codes of one token as one LSB-first bit string.
+
+    Channel c (storage order) occupies bits [o_c, o_c + b_c) with o_c = sum of the
+    earlier widths, least significant bit first; bit i of the record is bit i % 8 of
+    byte i // 8.  The record is zero-padded to R = 4 * ceil(B / 32) bytes.
+    """
+    u = np.asarray(u, dtype=np.int64)
+    bits = np.asarray(bits, dtype=np.int64)
+    n = u.shape[0]
+    budget = int(bits.sum())
+    rbytes = 4 * ((budget + 31) // 32)
+    flat = np.zeros((n, 8 * rbytes), dtype=np.uint8)
+    off = 0
+    for c, b in enumerate(bits):
+        for k in range(int(b)):
+            flat[:, off + k] = (u[:, c] >> k) & 1
+        off += int(b)
+    return np.packbits(flat, axis=1, bitorder="little")
+
+
+def unpack_records(rec: np.ndarray, bits: np.ndarray) -> np.ndarray:
+    """Inverse of ``pack_records``: codes u [n, d]."""
+    bits = np.asarray(bits, dtype=np.int64)
+    flat = np.unpackbits(np.asarray(rec, dtype=np.uint8), axis=1, bitorder="little")
+    u = np.zeros((rec.shape[0], bits.size), dtype=np.int64)
+    off = 0
+    for c, b in enumerate(bits):
+        for k in range(int(b)):
+            u[:, c] |= flat[:, off + k].astype(np.int64) << k
+        off += int(b)
+    return u
+
+
+def records_to_tiles(rec: np.ndarray) -> np.ndarray:
+    """Value-cache layout: tiles of 64 tokens, bit-transposed.
+
+    Record bit v of the 64 tokens of tile j is stored as two little-endian 32-bit
+    words, word (j, v, half) holding, at bit t, record bit v of token
+    64 j + 32 half + t.  A tile is 8R words x 2 = 64 R bytes, the same bytes as its 64
+    records.  The token count must be a multiple of 64.  Returns uint8
+    [n_tiles, 64 R].
+    """
+    rec = np.asarray(rec, dtype=np.uint8)
+    n, rbytes = rec.shape
+    if n % TILE_TOKENS:
+        raise ValueError("token count must be a multiple of 64")
+    flat = np.unpackbits(rec, axis=1, bitorder="little")              # [n, 8R]
+    nt = n // TILE_TOKENS
+    b = flat.reshape(nt, 2, 32, 8 * rbytes).transpose(0, 3, 1, 2)    # [nt, 8R, 2, 32]
+    return np.packbits(b, axis=-1, bitorder="little").reshape(nt, 64 * rbytes)
+
+
+def tiles_to_records(tiles: np.ndarray, rbytes: int) -> np.ndarray:
+    """Inverse of ``records_to_tiles``: records [64 * n_tiles, R]."""
+    tiles = np.asarray(tiles, dtype=np.uint8)
+    nt = tiles.shape[0]
+    b = np.unpackbits(tiles.reshape(nt, 8 * rbytes, 2, 4), axis=-1, bitorder="little")
+    flat = b.transpose(0, 2, 3, 1).reshape(nt * TILE_TOKENS, 8 * rbytes)
+    return np.packbits(flat, axis=1, bitorder="little")
+
+
+def encode(x32: np.ndarray, cal: Calibration):
+    """Encode tokens [n, d] of one head: (records [n, R] uint8, alpha16 [n], u [n, d])."""
+    h = fixed_point_transform(x32, cal.T32)
+    u, alpha16 = quantize(h, cal.bits, cal.s16)
+    return pack_records(u, cal.bits), alpha16, u
+
+
+def decode_tokens(rec: np.ndarray, alpha16: np.ndarray, cal: Calibration) -> np.ndarray:
+    """Reconstructed tokens [n, d] in the original coordinates: x^ = T h^ (fp64)."""
+    h = dequantize(unpack_records(rec, cal.bits), alpha16, cal.bits, cal.s16)
+    return h @ cal.T64.T
+
+
+# --------------------------------------------------------------------------------------
+# Decode attention
+# --------------------------------------------------------------------------------------
+def softmax_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float) -> np.ndarray:
+    """One decode row per query: o = softmax(q k^T * scale) v, fp64 (Def. 1, no mask
+    inside the cache: the decode row attends to every cached token)."""
+    q = np.asarray(q, dtype=np.float64)
+    s = (q @ np.asarray(k, dtype=np.float64).T) * scale
+    s = s - s.max(axis=-1, keepdims=True)
+    p = np.exp(s)
+    p /= p.sum(axis=-1, keepdims=True)
+    return p @ np.asarray(v, dtype=np.float64)
+
+
+def decode_attention(q32: np.ndarray, cal_k, cal_v, k_rec, k_alpha, v_rec, v_alpha,
+                     seq_len: int, scale: Optional[float] = None) -> np.ndarray:
+    """Attention of one sequence's queries over its compressed cache (Alg. 1, online).
+
+    q32: [H_q, d] fp32 queries; cal_k / cal_v: per-KV-head Calibration lists;
+    k_rec / v_rec: per-head records [>= seq_len, R]; k_alpha / v_alpha: per-head fp16
+    token scales.  Query head j reads KV head j // (H_q / H_kv).  Returns [H_q, d] fp64.
+    """
+    hq, d = q32.shape
+    hkv = len(cal_k)
+    g = hq // hkv
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    out = np.zeros((hq, d))
+    for h in range(hkv):
+        kh = decode_tokens(k_rec[h][:seq_len], k_alpha[h][:seq_len], cal_k[h])
+        vh = decode_tokens(v_rec[h][:seq_len], v_alpha[h][:seq_len], cal_v[h])
+        out[h * g:(h + 1) * g] = softmax_attention(q32[h * g:(h + 1) * g], kh, vh, scale)
+    return out
