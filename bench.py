@@ -1,0 +1,261 @@
+"""Benchmark of the AATC hot path on one MI355X.
+
+Step (the whole hot path once, Llama-3.1-8B-shaped layer, decode batch 1):
+  1. aatc_encode of one new token's keys and values (8 KV heads) into the packed
+     caches (records for K, bit-transposed tiles for V), at the last cached position;
+  2. aatc_decode_attention of 32 query heads (GQA 4:1) over 32768 cached tokens per KV
+     head packed at 2.75 bits per channel.
+The cache stays at 32768 tokens: every step rewrites the last token.  To measure HBM
+rather than the 256 MB Infinity Cache, the steps rotate over enough cache copies to
+exceed 512 MB.
+
+value = packed-cache bytes read per step (codes + fp16 token scales of K and V) /
+wall time per step.  roofline = the same bytes / the decode kernel's average duration
+(HIP events on the launch stream) against 8 TB/s.  Encode throughput of a 65536-token
+prefill (8 KV heads, K and V) is reported alongside.  cpu_baseline = the NumPy oracle's
+decode attention on a bounded token sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def bf16_tensor(arr, device="cuda"):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16).to(device)
+
+
+def setup_decode(cfg_id=2):
+    import torch
+    import paper_2608_14191_amd as P
+    from kvsynth import workload
+
+    w = workload(cfg_id)
+    H, HQ, L, B = w.n_kv_heads, w.n_q_heads, w.n_tokens, w.batch
+    avg = w.cfg["avg_bits"][0]
+    qw = w.cfg["query_weighted_k"]
+    t0 = time.time()
+    cal_k = [P.aatc_calibrate(w.calib(h, "k"), avg, q_calib=w.calib_queries(h) if qw else None,
+                              q_group=w.group) for h in range(H)]
+    cal_v = [P.aatc_calibrate(w.calib(h, "v"), avg) for h in range(H)]
+    _log(f"[setup] calibrated {2 * H} tensors in {time.time() - t0:.1f}s")
+    pk = torch.from_numpy(P.aatc_params_pack(cal_k)).cuda()
+    pv = torch.from_numpy(P.aatc_params_pack(cal_v)).cuda()
+    rk, rv = cal_k[0].record_bytes, cal_v[0].record_bytes
+    cap = L
+    kc = torch.zeros((B, H, cap, rk), dtype=torch.uint8, device="cuda")
+    vc = torch.zeros((B, H, cap // 64, 64 * rv), dtype=torch.uint8, device="cuda")
+    ka = torch.zeros((B, H, cap), dtype=torch.int16, device="cuda")
+    va = torch.zeros((B, H, cap), dtype=torch.int16, device="cuda")
+    t0 = time.time()
+    last_tok = []
+    for b in range(B):
+        for kind, codes, alpha, params, layout in (("k", kc, ka, pk, P.LAYOUT_RECORDS),
+                                                   ("v", vc, va, pv, P.LAYOUT_TILES)):
+            x = bf16_tensor(np.stack([w.cache(b, h, kind) for h in range(H)], axis=1))
+            P.aatc_encode(params, H, x, L, H * 128, layout, codes[b], alpha[b], cap, 0)
+            last_tok.append(x[L - 1:L].clone())
+            del x
+    torch.cuda.synchronize()
+    _log(f"[setup] encoded the {B}x{H}x{L}-token caches in {time.time() - t0:.1f}s")
+    q = bf16_tensor(np.stack([w.queries(b) for b in range(B)]))
+    return dict(w=w, P=P, pk=pk, pv=pv, kc=kc, vc=vc, ka=ka, va=va, q=q, cap=cap, L=L,
+                rk=rk, rv=rv, last_tok=last_tok, cal_k=cal_k, cal_v=cal_v)
+
+
+def decode_bytes(s) -> int:
+    w = s["w"]
+    return w.batch * w.n_kv_heads * s["L"] * (s["rk"] + s["rv"] + 4)
+
+
+def run_decode_bench(s, steps, warmup):
+    import torch
+    P, w = s["P"], s["w"]
+    H, HQ, B, L, cap = w.n_kv_heads, w.n_q_heads, w.batch, s["L"], s["cap"]
+    per_copy = sum(t.numel() for t in (s["kc"], s["vc"])) + 2 * (s["ka"].numel() + s["va"].numel())
+    n_copies = max(2, math.ceil(512e6 / per_copy))
+    copies = [(s["kc"], s["ka"], s["vc"], s["va"])]
+    for _ in range(n_copies - 1):
+        copies.append(tuple(t.clone() for t in copies[0]))
+    lens = torch.full((B,), L, dtype=torch.int32, device="cuda")
+    out = torch.zeros((B, HQ, 128), dtype=torch.float32, device="cuda")
+    ws = torch.zeros(P.aatc_decode_workspace_bytes(B, HQ, H, cap), dtype=torch.uint8,
+                     device="cuda")
+    scale = 128 ** -0.5
+    xk, xv = s["last_tok"][0], s["last_tok"][1]
+
+    def step(i, ev=None):
+        kc, ka, vc, va = copies[i % n_copies]
+        P.aatc_encode(s["pk"], H, xk, 1, H * 128, P.LAYOUT_RECORDS, kc[0], ka[0], cap, L - 1)
+        P.aatc_encode(s["pv"], H, xv, 1, H * 128, P.LAYOUT_TILES, vc[0], va[0], cap, L - 1)
+        if ev is not None:
+            ev[0].record()
+        P.aatc_decode_attention(s["pk"], s["pv"], B, HQ, H, s["q"], kc, ka, vc, va, lens, cap,
+                                scale, out, ws)
+        if ev is not None:
+            ev[1].record()
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    return elapsed, kern_ms, n_copies, out
+
+
+def run_encode_bench(avg_bits, reps=3):
+    """Prefill encode of 65536 tokens x 8 KV heads (K records + V tiles)."""
+    import torch
+    import paper_2608_14191_amd as P
+    from kvsynth import workload
+    w = workload(4)
+    H, L = w.n_kv_heads, w.n_tokens
+    cal_k = [P.aatc_calibrate(w.calib(h, "k"), avg_bits) for h in range(H)]
+    cal_v = [P.aatc_calibrate(w.calib(h, "v"), avg_bits) for h in range(H)]
+    pk = torch.from_numpy(P.aatc_params_pack(cal_k)).cuda()
+    pv = torch.from_numpy(P.aatc_params_pack(cal_v)).cuda()
+    rk, rv = cal_k[0].record_bytes, cal_v[0].record_bytes
+    xk = bf16_tensor(np.stack([w.cache(0, h, "k") for h in range(H)], axis=1))
+    xv = bf16_tensor(np.stack([w.cache(0, h, "v") for h in range(H)], axis=1))
+    kc = torch.zeros((H, L, rk), dtype=torch.uint8, device="cuda")
+    vc = torch.zeros((H, L // 64, 64 * rv), dtype=torch.uint8, device="cuda")
+    ka = torch.zeros((H, L), dtype=torch.int16, device="cuda")
+    va = torch.zeros((H, L), dtype=torch.int16, device="cuda")
+
+    def once():
+        P.aatc_encode(pk, H, xk, L, H * 128, P.LAYOUT_RECORDS, kc, ka, L, 0)
+        P.aatc_encode(pv, H, xv, L, H * 128, P.LAYOUT_TILES, vc, va, L, 0)
+
+    once()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        once()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    return dict(avg_bits=avg_bits, tokens=L, seconds=dt, tokens_per_s=L / dt,
+                bytes=int(L * H * (2 * 128 * 2 + rk + rv + 4)))
+
+
+def cpu_baseline(s, target_seconds=15.0):
+    """The oracle's decode attention over a bounded token sample of the same workload."""
+    from oracle import aatc as ora
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    w = s["w"]
+    H = w.n_kv_heads
+
+    def ocal(c):
+        bits = c.bits_np
+        return ora.Calibration(d=128, budget=c.budget_bits, record_bytes=c.record_bytes,
+                               d_active=c.d_active, bits=bits, perm=np.arange(128),
+                               T64=c.T.astype(np.float64), T32=c.T, s16=c.s16,
+                               sigma2=np.ones(128), weight=np.ones(128), bits_eig=bits)
+    ck = [ocal(c) for c in s["cal_k"]]
+    cv = [ocal(c) for c in s["cal_v"]]
+    n = 4096
+    krec = [s["kc"][0, h, :n].cpu().numpy() for h in range(H)]
+    vrec = [ora.tiles_to_records(s["vc"][0, h, :n // 64].cpu().numpy(), s["rv"]) for h in range(H)]
+    ka = [s["ka"][0, h, :n].cpu().numpy().view(np.float16) for h in range(H)]
+    va = [s["va"][0, h, :n].cpu().numpy().view(np.float16) for h in range(H)]
+    q32 = w.as_f32(w.queries(0))
+    reps, t_total = 0, 0.0
+    while t_total < target_seconds and reps < 50:
+        t0 = time.perf_counter()
+        ora.decode_attention(q32, ck, cv, krec, ka, vrec, va, n)
+        t_total += time.perf_counter() - t0
+        reps += 1
+    per = t_total / reps
+    nbytes = H * n * (s["rk"] + s["rv"] + 4)
+    return {"value": nbytes / per / 1e9, "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"oracle decode attention of 32 query heads over the first {n} of the "
+                      f"32768 cached tokens (8 KV heads), {reps} runs, {per:.2f} s each; "
+                      f"GB/s over the same packed-cache bytes as the GPU metric"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-encode", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the decode path shards by KV head with no communication; see DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    s = setup_decode(2)
+    nbytes = decode_bytes(s)
+    elapsed, kern_ms, n_copies, _ = run_decode_bench(s, args.steps, args.warmup)
+    ms_per_step = elapsed / args.steps * 1e3
+    value = nbytes / (elapsed / args.steps) / 1e9
+    achieved = nbytes / (kern_ms * 1e-3) / 1e9
+    _log(f"[decode] {ms_per_step * 1e3:.1f} us/step, kernel {kern_ms * 1e3:.1f} us, "
+         f"{value:.0f} GB/s step, {achieved:.0f} GB/s kernel ({n_copies} cache copies)")
+    enc = []
+    if not args.no_encode:
+        for avg in (2.75, 4.0):
+            r = run_encode_bench(avg)
+            enc.append(r)
+            _log(f"[encode] {avg} bits: {r['seconds'] * 1e3:.2f} ms, {r['tokens_per_s']:.3e} tok/s")
+    line = {
+        "metric": "decode-attention HBM GB/s (% of peak) on packed KV; encode tokens/sec",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int-codes/f32",
+        "data": "synthetic",
+        "config": {"workload": "llama31_8b_decode_b1_32k: 1 layer, batch 1, 32 q heads, 8 kv "
+                               "heads, head_dim 128, 32768 cached tokens, 2.75 avg bits, bf16 "
+                               "q/k/v; step = append 1 token + decode attention",
+                   "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+                   "bytes_per_step": nbytes, "cache_copies": n_copies},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None},
+        "encode": [{"workload": f"llama31_8b_prefill_64k at {r['avg_bits']} bits",
+                    "tokens_per_s": round(r["tokens_per_s"], 1),
+                    "ms": round(r["seconds"] * 1e3, 3)} for r in enc],
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(s)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

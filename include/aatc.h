@@ -1,0 +1,198 @@
+/*
+ * aatc.h -- C ABI of the Attention-Aware Transform Coding (AATC) hot path on MI355X.
+ *
+ * AATC ("KV Cache Compression Through the Lens of Transform Coding") stores each key
+ * and value vector of a KV head in a calibrated decorrelated basis, quantizing every
+ * transformed channel with its own bit width (0 bits drops the channel), and runs
+ * decode attention directly on the packed cache.
+ *
+ * Conventions shared by every entry point:
+ *   - Head dimension d is 128 (v1); other values return AATC_E_UNSUPPORTED.
+ *   - Channel widths are 0..8 bits (b_max <= 8).
+ *   - "Device" pointers are HIP device memory owned by the caller; "host" pointers are
+ *     ordinary host memory.  The library allocates no device memory, never frees
+ *     caller memory and never synchronizes a stream.
+ *   - Every call validates its arguments on the host and returns AATC_E_INVALID
+ *     (or AATC_E_UNSUPPORTED) before launching anything.  Launch failures return
+ *     AATC_E_DEVICE.  No C++ exception crosses this interface.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Kernels are enqueued on
+ *     it and run asynchronously.
+ *   - The library is stateless and thread-safe.
+ *
+ * Cache layouts (per sequence; B_b = sum of a tensor's channel widths, the "budget",
+ * R = 4 * ceil(B_b / 32) bytes per token):
+ *   - RECORDS (used for keys): [n_kv_heads][cap][R] bytes.  Token t's codes are one
+ *     LSB-first bit string: storage channel c occupies bits [o_c, o_c + b_c), o_c the
+ *     sum of the earlier widths; bit i is bit (i % 8) of byte (i / 8); zero padded.
+ *   - TILES (used for values): [n_kv_heads][cap / 64][64 * R] bytes.  Tile j holds
+ *     tokens 64 j .. 64 j + 63 bit-transposed: record bit v of token 64 j + 32 h + t
+ *     is bit t of the little-endian 32-bit word (v, h) of the tile, word index
+ *     2 v + h.  cap must be a multiple of 64.
+ *   - Token scales alpha: [n_kv_heads][cap] fp16 bit patterns, for either layout.
+ */
+#ifndef AATC_H_
+#define AATC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AATC_HEAD_DIM 128
+#define AATC_MAX_BITS 8
+#define AATC_TILE_TOKENS 64
+
+typedef enum {
+  AATC_OK = 0,
+  AATC_E_INVALID = 1,      /* bad pointer, size, alignment or combination */
+  AATC_E_UNSUPPORTED = 2,  /* valid request outside what v1 implements (d != 128) */
+  AATC_E_NUMERIC = 3,      /* non-finite input or eigensolver failure */
+  AATC_E_DEVICE = 4,       /* a HIP call or kernel launch failed */
+  AATC_E_WORKSPACE = 5     /* workspace too small */
+} aatc_status;
+
+typedef enum { AATC_F32 = 0, AATC_BF16 = 1, AATC_F16 = 2 } aatc_dtype;
+
+typedef enum { AATC_LAYOUT_RECORDS = 0, AATC_LAYOUT_TILES = 1 } aatc_layout;
+
+/*
+ * Calibration artifact of one (KV head, tensor), channels in storage order (widest
+ * first; eigen order breaks ties, so zero-bit channels form a suffix).
+ */
+typedef struct {
+  int32_t d;                    /* head dimension (128) */
+  int32_t budget_bits;          /* B = sum of bits */
+  int32_t record_bytes;         /* R = 4 * ceil(B / 32) */
+  int32_t d_active;             /* channels with >= 1 bit */
+  float transform[AATC_HEAD_DIM * AATC_HEAD_DIM]; /* row-major [j][c] = T_jc: column c
+                                   is the unit eigenvector of storage channel c */
+  uint8_t bits[AATC_HEAD_DIM];  /* width of storage channel c, non-increasing */
+  uint16_t scale_f16[AATC_HEAD_DIM]; /* s_c as fp16 bits (0 for dropped channels) */
+  int32_t perm[AATC_HEAD_DIM];  /* eigen index (by decreasing eigenvalue) of channel c */
+  double sigma2[AATC_HEAD_DIM]; /* eigenvalues, decreasing (eigen order) */
+  double weight[AATC_HEAD_DIM]; /* attention-aware channel weights w (eigen order) */
+  uint8_t bits_eig[AATC_HEAD_DIM]; /* widths in eigen order */
+} aatc_calibration;
+
+/*
+ * aatc_calibrate -- offline calibration of one (KV head, tensor) on the host.
+ *
+ * Follows Algorithm 1 (calibration part) with Sec. 5.1 (decorrelating transform) and
+ * Sec. 5.2 (attention-aware reverse water-filling, "The right scaling"):
+ *   Sigma = X^T X / n (uncentered, fp64); eigenvectors by decreasing eigenvalue, each
+ *   signed so its largest-magnitude entry is positive (the PCA form of the whitening
+ *   SVD, App. D); weights w_c = (1/T) sum over the group's query heads and tokens of
+ *   (P_c^T q)^2 when q_calib is given (eq. waterfilling-keys and its GQA remark,
+ *   App. B), w_c = ||P_c^T W_O||^2 when w_o is given (value weights, Sec. 5.2), else 1
+ *   ("var-only", Sec. 6); integer widths minimizing sum_c w_c sigma_c^2 2^(-2 b_c)
+ *   with sum_c b_c = round(avg_bits * d) and 0 <= b_c <= b_max, by exact greedy
+ *   marginal allocation (ties to the lower eigen index); s_c = fp16 of the
+ *   `percentile` quantile (linear interpolation) of |h_c| over the calibration tokens.
+ *
+ * x_calib  host [n_calib][d] fp32 calibration samples of this head (n_calib >= 2).
+ * q_calib  host [n_q][d] fp32 calibration queries of the q_group query heads that
+ *          share this KV head, stacked (n_q a multiple of q_group), or NULL.
+ * w_o      host [d][d_out] fp32 rows of W_O that read this head's values, or NULL.
+ *          At most one of q_calib / w_o may be non-NULL.
+ * avg_bits average bits per channel, 0 < avg_bits * d <= d * b_max.
+ * b_max    1..8.
+ * percentile in (0, 1], 0.99 in the paper.
+ * out      host, caller-allocated, fully written on success.
+ * Errors: AATC_E_INVALID for NULL/size/range problems, AATC_E_UNSUPPORTED for
+ * d != 128, AATC_E_NUMERIC for non-finite inputs or no eigensolver convergence.
+ */
+aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int32_t d,
+                           const float* q_calib, int64_t n_q, int32_t q_group,
+                           const float* w_o, int32_t d_out,
+                           double avg_bits, int32_t b_max, double percentile,
+                           aatc_calibration* out);
+
+/*
+ * aatc_params_bytes / aatc_params_pack -- build the device parameter block of one
+ * tensor (K or V) for n_kv_heads heads from their calibrations (host only).
+ *
+ * The block holds, per head, the fp32 transform, its fixed-point copy used by the
+ * encoder (rint(T * 2^14)), widths, bit offsets, fp16 scales and their fp32
+ * reciprocals, and bit-to-channel tables for the decoder.  All heads of a tensor
+ * must have the same budget (so the same record size).  The caller copies the
+ * `bytes` written to `host_buf` into device memory (16-byte aligned) and passes that
+ * device pointer to aatc_encode / aatc_decode_attention.
+ * Errors: AATC_E_INVALID (NULL, n_kv_heads < 1, bytes too small, budgets differ,
+ * malformed calibration).
+ */
+size_t aatc_params_bytes(int32_t n_kv_heads);
+aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_t n_kv_heads,
+                             void* host_buf, size_t bytes);
+
+/*
+ * aatc_encode -- append n_tok tokens of one sequence to a compressed cache.
+ *
+ * Algorithm 1 (inference part: project and append quantized codes) with Sec. 5.2:
+ * per token and head, h = T^T x (eq. transformed-cache) in exact fixed-point
+ * arithmetic (x scaled per token so max |x_j| lies in [2^13, 2^14) and rounded to
+ * integers; T rounded to multiples of 2^-14; one final fp32 rounding); r_c = h_c *
+ * (1/s_c); alpha = fp16(max over stored channels of |r_c|); code_c = clamp(floor(
+ * r_c * (1/alpha) * 2^(b_c - 1) + 1/2), -2^(b_c-1), 2^(b_c-1) - 1) stored as
+ * u_c = code_c + 2^(b_c - 1), packed in `layout`.
+ *
+ * dev_params   device block from aatc_params_pack (this tensor, n_kv_heads heads).
+ * x            device [n_tok] tokens, token t at x + t * x_tok_stride elements, each
+ *              [n_kv_heads][d] contiguous, of type x_dtype (F32 or BF16).
+ * codes        device cache of this sequence in `layout` (see top of file).
+ * alpha        device [n_kv_heads][cap] fp16 token scales.
+ * cap, pos     cache capacity in tokens and first token written; pos + n_tok <= cap.
+ *              TILES needs cap % 64 == 0; tokens of a partly written tile that lie
+ *              outside [pos, pos + n_tok) keep their bits.
+ * n_tok == 0 is a no-op.  Errors: AATC_E_INVALID.
+ */
+aatc_status aatc_encode(const void* dev_params, int32_t n_kv_heads, int32_t d,
+                        const void* x, aatc_dtype x_dtype, int64_t n_tok,
+                        int64_t x_tok_stride, aatc_layout layout, void* codes,
+                        uint16_t* alpha, int64_t cap, int64_t pos, void* stream);
+
+/*
+ * aatc_decode_attention -- one decode step of attention over packed caches.
+ *
+ * Algorithm 1 (inference: reconstruct, softmax, output) evaluated in the transformed
+ * domain (App. B: effective query q~ = T_K^T q): for query head j of sequence b,
+ * reading KV head j / (n_q_heads / n_kv_heads),
+ *   o = T_V * sum_i softmax_i(scale * q~ . h^K_i) h^V_i,
+ * with h^_c = alpha_i s_c 2^(1-b_c) (u_ic - 2^(b_c-1)) and no mask inside
+ * [0, seq_len[b]).  Online softmax over token splits; the inverse transform T_V is
+ * applied once to each output.
+ *
+ * dev_params_k / _v  device parameter blocks of the key and value tensors.
+ * q          device [batch][n_q_heads][d], q_dtype F32 or BF16.
+ * k_codes    device RECORDS layout, [batch][n_kv_heads][cap][R_K].
+ * k_alpha    device [batch][n_kv_heads][cap] fp16.
+ * v_codes    device TILES layout, [batch][n_kv_heads][cap / 64][64 * R_V].
+ * v_alpha    device [batch][n_kv_heads][cap] fp16.
+ * seq_len    device [batch] int32, 0 <= seq_len[b] <= cap (0 gives a zero output).
+ * cap        tokens per sequence in the caches, a multiple of 64.
+ * softmax_scale  logit scale, 1/sqrt(d) for standard attention.
+ * out        device [batch][n_q_heads][d] fp32.
+ * workspace  device scratch of at least aatc_decode_workspace_bytes(...) bytes,
+ *            zero-filled once after allocation; every call leaves it reusable.
+ * Errors: AATC_E_INVALID, AATC_E_WORKSPACE, AATC_E_DEVICE.
+ */
+size_t aatc_decode_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                   int64_t cap);
+aatc_status aatc_decode_attention(const void* dev_params_k, const void* dev_params_v,
+                                  int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                  int32_t d, const void* q, aatc_dtype q_dtype,
+                                  const void* k_codes, const uint16_t* k_alpha,
+                                  const void* v_codes, const uint16_t* v_alpha,
+                                  const int32_t* seq_len, int64_t cap, float softmax_scale,
+                                  float* out, void* workspace, size_t ws_bytes,
+                                  void* stream);
+
+/* Human-readable name of a status code (static string). */
+const char* aatc_status_string(aatc_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AATC_H_ */

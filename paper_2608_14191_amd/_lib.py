@@ -1,0 +1,185 @@
+"""ctypes binding of libaatc.so: the C ABI of include/aatc.h, argument marshalling only.
+
+Every function here has the name of the C entry point it calls.  Device buffers are
+torch tensors on a HIP device; their pointers and the current HIP stream are handed to
+the library, which does all the work.  If libaatc.so is missing, importing this module
+raises ImportError: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+
+from .build import LIB
+
+HEAD_DIM = 128
+MAX_BITS = 8
+TILE_TOKENS = 64
+
+OK, E_INVALID, E_UNSUPPORTED, E_NUMERIC, E_DEVICE, E_WORKSPACE = range(6)
+F32, BF16, F16 = 0, 1, 2
+LAYOUT_RECORDS, LAYOUT_TILES = 0, 1
+
+
+class AatcError(RuntimeError):
+    def __init__(self, func: str, status: int):
+        super().__init__(f"{func}: {_status_string(status)} (status {status})")
+        self.status = status
+
+
+class Calibration(ctypes.Structure):
+    """Mirror of aatc_calibration (include/aatc.h)."""
+
+    _fields_ = [
+        ("d", ctypes.c_int32),
+        ("budget_bits", ctypes.c_int32),
+        ("record_bytes", ctypes.c_int32),
+        ("d_active", ctypes.c_int32),
+        ("transform", ctypes.c_float * (HEAD_DIM * HEAD_DIM)),
+        ("bits", ctypes.c_uint8 * HEAD_DIM),
+        ("scale_f16", ctypes.c_uint16 * HEAD_DIM),
+        ("perm", ctypes.c_int32 * HEAD_DIM),
+        ("sigma2", ctypes.c_double * HEAD_DIM),
+        ("weight", ctypes.c_double * HEAD_DIM),
+        ("bits_eig", ctypes.c_uint8 * HEAD_DIM),
+    ]
+
+    # numpy views (copies) for convenience
+    @property
+    def T(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self.transform).reshape(HEAD_DIM, HEAD_DIM).copy()
+
+    @property
+    def bits_np(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self.bits).astype(np.int64)
+
+    @property
+    def s16(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self.scale_f16).copy().view(np.float16)
+
+
+if not os.path.exists(LIB):
+    raise ImportError(f"{LIB} is not built; call __graft_entry__.build() first")
+_L = ctypes.CDLL(LIB)
+
+_vp, _i32, _i64, _sz, _f32, _f64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                    ctypes.c_size_t, ctypes.c_float, ctypes.c_double)
+_L.aatc_status_string.restype = ctypes.c_char_p
+_L.aatc_status_string.argtypes = [ctypes.c_int]
+_L.aatc_calibrate.restype = ctypes.c_int
+_L.aatc_calibrate.argtypes = [_vp, _i64, _i32, _vp, _i64, _i32, _vp, _i32, _f64, _i32, _f64,
+                              ctypes.POINTER(Calibration)]
+_L.aatc_params_bytes.restype = _sz
+_L.aatc_params_bytes.argtypes = [_i32]
+_L.aatc_params_pack.restype = ctypes.c_int
+_L.aatc_params_pack.argtypes = [ctypes.POINTER(Calibration), _i32, _vp, _sz]
+_L.aatc_encode.restype = ctypes.c_int
+_L.aatc_encode.argtypes = [_vp, _i32, _i32, _vp, ctypes.c_int, _i64, _i64, ctypes.c_int, _vp,
+                           _vp, _i64, _i64, _vp]
+_L.aatc_decode_workspace_bytes.restype = _sz
+_L.aatc_decode_workspace_bytes.argtypes = [_i32, _i32, _i32, _i64]
+_L.aatc_decode_attention.restype = ctypes.c_int
+_L.aatc_decode_attention.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32, _vp, ctypes.c_int,
+                                     _vp, _vp, _vp, _vp, _vp, _i64, _f32, _vp, _vp, _sz, _vp]
+
+
+def library() -> ctypes.CDLL:
+    return _L
+
+
+def exported_symbols_declared_in_header(header_path: str):
+    """Names of the functions include/aatc.h declares."""
+    text = open(header_path).read()
+    return sorted(set(re.findall(r"\b(aatc_[a-z_0-9]+)\s*\(", text)))
+
+
+def _status_string(status: int) -> str:
+    return _L.aatc_status_string(int(status)).decode()
+
+
+aatc_status_string = _status_string
+
+
+def _check(func: str, status: int):
+    if status != OK:
+        raise AatcError(func, status)
+
+
+def _np_ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def aatc_calibrate(x_calib, avg_bits: float, b_max: int = 8, percentile: float = 0.99,
+                   q_calib=None, q_group: int = 1, w_o=None) -> Calibration:
+    """Host calibration of one (KV head, tensor); arrays are float32 numpy arrays."""
+    x = np.ascontiguousarray(x_calib, dtype=np.float32)
+    q = None if q_calib is None else np.ascontiguousarray(q_calib, dtype=np.float32)
+    wo = None if w_o is None else np.ascontiguousarray(w_o, dtype=np.float32)
+    out = Calibration()
+    st = _L.aatc_calibrate(_np_ptr(x), x.shape[0], x.shape[1] if x.ndim == 2 else 0,
+                           _np_ptr(q), 0 if q is None else q.shape[0], int(q_group),
+                           _np_ptr(wo), 0 if wo is None else wo.shape[1],
+                           float(avg_bits), int(b_max), float(percentile), ctypes.byref(out))
+    _check("aatc_calibrate", st)
+    return out
+
+
+def aatc_params_bytes(n_kv_heads: int) -> int:
+    return int(_L.aatc_params_bytes(int(n_kv_heads)))
+
+
+def aatc_params_pack(calibrations) -> np.ndarray:
+    """Host parameter block (uint8 numpy array) for a list of per-head Calibration."""
+    n = len(calibrations)
+    arr = (Calibration * n)(*calibrations)
+    buf = np.zeros(aatc_params_bytes(n), dtype=np.uint8)
+    _check("aatc_params_pack", _L.aatc_params_pack(arr, n, _np_ptr(buf), buf.nbytes))
+    return buf
+
+
+def _stream(stream):
+    if stream is not None:
+        return ctypes.c_void_p(int(stream))
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def aatc_encode(dev_params, n_kv_heads: int, x, n_tok: int, x_tok_stride: int, layout: int,
+                codes, alpha, cap: int, pos: int, stream=None):
+    """Append n_tok tokens of x ([n_tok, n_kv_heads, 128] view) to a sequence's cache."""
+    st = _L.aatc_encode(_dptr(dev_params), int(n_kv_heads), HEAD_DIM, _dptr(x), _dtype_code(x),
+                        int(n_tok), int(x_tok_stride), int(layout), _dptr(codes), _dptr(alpha),
+                        int(cap), int(pos), _stream(stream))
+    _check("aatc_encode", st)
+
+
+def aatc_decode_workspace_bytes(batch: int, n_q_heads: int, n_kv_heads: int, cap: int) -> int:
+    return int(_L.aatc_decode_workspace_bytes(int(batch), int(n_q_heads), int(n_kv_heads),
+                                              int(cap)))
+
+
+def aatc_decode_attention(dev_params_k, dev_params_v, batch: int, n_q_heads: int,
+                          n_kv_heads: int, q, k_codes, k_alpha, v_codes, v_alpha, seq_len,
+                          cap: int, softmax_scale: float, out, workspace, stream=None):
+    st = _L.aatc_decode_attention(
+        _dptr(dev_params_k), _dptr(dev_params_v), int(batch), int(n_q_heads), int(n_kv_heads),
+        HEAD_DIM, _dptr(q), _dtype_code(q), _dptr(k_codes), _dptr(k_alpha), _dptr(v_codes),
+        _dptr(v_alpha), _dptr(seq_len), int(cap), float(softmax_scale), _dptr(out),
+        _dptr(workspace), int(workspace.numel() * workspace.element_size()), _stream(stream))
+    _check("aatc_decode_attention", st)

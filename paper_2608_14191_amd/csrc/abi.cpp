@@ -1,0 +1,156 @@
+// C ABI entry points: argument validation, parameter-block packing and dispatch to
+// the HIP launchers.  No exception crosses the boundary.
+#include <cmath>
+#include <cstring>
+
+#include "aatc.h"
+#include "launch.h"
+#include "params.h"
+
+using namespace aatc;
+
+namespace {
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool calibration_ok(const aatc_calibration& c) {
+  if (c.d != kD) return false;
+  int sum = 0, active = 0, prev = kMaxBits;
+  for (int i = 0; i < kD; ++i) {
+    if (c.bits[i] > kMaxBits || c.bits[i] > prev) return false;   // non-increasing
+    prev = c.bits[i];
+    sum += c.bits[i];
+    if (c.bits[i]) ++active;
+  }
+  return sum == c.budget_bits && active == c.d_active && sum > 0 &&
+         c.record_bytes == 4 * ((sum + 31) / 32);
+}
+
+}  // namespace
+
+extern "C" const char* aatc_status_string(aatc_status s) {
+  switch (s) {
+    case AATC_OK: return "ok";
+    case AATC_E_INVALID: return "invalid argument";
+    case AATC_E_UNSUPPORTED: return "unsupported configuration";
+    case AATC_E_NUMERIC: return "numerical failure";
+    case AATC_E_DEVICE: return "device error";
+    case AATC_E_WORKSPACE: return "workspace too small";
+  }
+  return "unknown status";
+}
+
+extern "C" size_t aatc_params_bytes(int32_t n_kv_heads) {
+  if (n_kv_heads < 1) return 0;
+  return params_bytes(n_kv_heads);
+}
+
+extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_t n_kv_heads,
+                                        void* host_buf, size_t bytes) {
+  try {
+    if (!per_head || !host_buf || n_kv_heads < 1) return AATC_E_INVALID;
+    if (bytes < params_bytes(n_kv_heads)) return AATC_E_INVALID;
+    for (int h = 0; h < n_kv_heads; ++h) {
+      if (!calibration_ok(per_head[h])) return AATC_E_INVALID;
+      if (per_head[h].budget_bits != per_head[0].budget_bits) return AATC_E_INVALID;
+    }
+    std::memset(host_buf, 0, params_bytes(n_kv_heads));
+    auto* hdr = static_cast<TensorHeader*>(host_buf);
+    hdr->magic = kMagic;
+    hdr->n_heads = n_kv_heads;
+    hdr->budget = per_head[0].budget_bits;
+    hdr->record_bytes = per_head[0].record_bytes;
+    for (int h = 0; h < n_kv_heads; ++h) {
+      const aatc_calibration& c = per_head[h];
+      auto* hp = const_cast<HeadParams*>(head_params(host_buf, h));
+      std::memcpy(hp->T, c.transform, sizeof(hp->T));
+      for (int i = 0; i < kD * kD; ++i)
+        hp->Tq[i] = (int16_t)std::nearbyint(std::ldexp((double)c.transform[i], kTFrac));
+      int off = 0;
+      for (int ch = 0; ch < kD; ++ch) {
+        const int b = c.bits[ch];
+        hp->bits[ch] = (uint8_t)b;
+        hp->bit_off[ch] = (uint16_t)off;
+        hp->s16[ch] = c.scale_f16[ch];
+        const double s = b ? f16_bits_to_f64(c.scale_f16[ch]) : 0.0;
+        hp->s[ch] = (float)s;
+        // fp32 1/s correctly rounded: the fp64 quotient of an 11-bit divisor rounds
+        // to fp32 without a double-rounding error.
+        hp->inv_s[ch] = (b && s > 0.0) ? (float)(1.0 / s) : 0.0f;
+        for (int k = 0; k < b; ++k) {
+          hp->virt_chan[off + k] = (uint8_t)ch;
+          hp->virt_bit[off + k] = (uint8_t)k;
+        }
+        off += b;
+      }
+      hp->d_active = c.d_active;
+      hp->budget = c.budget_bits;
+      hp->record_bytes = c.record_bytes;
+    }
+    return AATC_OK;
+  } catch (...) {
+    return AATC_E_INVALID;
+  }
+}
+
+extern "C" aatc_status aatc_encode(const void* dev_params, int32_t n_kv_heads, int32_t d,
+                                   const void* x, aatc_dtype x_dtype, int64_t n_tok,
+                                   int64_t x_tok_stride, aatc_layout layout, void* codes,
+                                   uint16_t* alpha, int64_t cap, int64_t pos, void* stream) {
+  try {
+    if (d != kD) return AATC_E_UNSUPPORTED;
+    if (!dev_params || !x || !codes || !alpha) return AATC_E_INVALID;
+    if (n_kv_heads < 1 || n_tok < 0 || cap < 1 || pos < 0 || pos + n_tok > cap)
+      return AATC_E_INVALID;
+    if (x_dtype != AATC_F32 && x_dtype != AATC_BF16) return AATC_E_INVALID;
+    if (layout != AATC_LAYOUT_RECORDS && layout != AATC_LAYOUT_TILES) return AATC_E_INVALID;
+    if (layout == AATC_LAYOUT_TILES && cap % kTile != 0) return AATC_E_INVALID;
+    if (x_tok_stride < (int64_t)n_kv_heads * d) return AATC_E_INVALID;
+    if (!aligned(dev_params, 16) || !aligned(codes, 16) || !aligned(alpha, 2) ||
+        !aligned(x, x_dtype == AATC_F32 ? 4 : 2))
+      return AATC_E_INVALID;
+    if (n_tok == 0) return AATC_OK;
+    return launch_encode(dev_params, n_kv_heads, x, x_dtype, n_tok, x_tok_stride, layout,
+                         codes, alpha, cap, pos, stream);
+  } catch (...) {
+    return AATC_E_INVALID;
+  }
+}
+
+extern "C" size_t aatc_decode_workspace_bytes(int32_t batch, int32_t n_q_heads,
+                                              int32_t n_kv_heads, int64_t cap) {
+  if (batch < 1 || n_q_heads < 1 || n_kv_heads < 1 || cap < 0) return 0;
+  return decode_workspace_bytes(batch, n_q_heads, n_kv_heads, cap);
+}
+
+extern "C" aatc_status aatc_decode_attention(
+    const void* dev_params_k, const void* dev_params_v, int32_t batch, int32_t n_q_heads,
+    int32_t n_kv_heads, int32_t d, const void* q, aatc_dtype q_dtype, const void* k_codes,
+    const uint16_t* k_alpha, const void* v_codes, const uint16_t* v_alpha,
+    const int32_t* seq_len, int64_t cap, float softmax_scale, float* out, void* workspace,
+    size_t ws_bytes, void* stream) {
+  try {
+    if (d != kD) return AATC_E_UNSUPPORTED;
+    if (!dev_params_k || !dev_params_v || !q || !k_codes || !k_alpha || !v_codes ||
+        !v_alpha || !seq_len || !out || !workspace)
+      return AATC_E_INVALID;
+    if (batch < 1 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0)
+      return AATC_E_INVALID;
+    if (n_q_heads / n_kv_heads > kMaxGroup) return AATC_E_UNSUPPORTED;
+    if (cap < kTile || cap % kTile != 0) return AATC_E_INVALID;
+    if (q_dtype != AATC_F32 && q_dtype != AATC_BF16) return AATC_E_INVALID;
+    if (!std::isfinite(softmax_scale)) return AATC_E_INVALID;
+    if (!aligned(dev_params_k, 16) || !aligned(dev_params_v, 16) || !aligned(k_codes, 16) ||
+        !aligned(v_codes, 16) || !aligned(k_alpha, 4) || !aligned(v_alpha, 4) ||
+        !aligned(seq_len, 4) || !aligned(out, 16) || !aligned(workspace, 256) ||
+        !aligned(q, q_dtype == AATC_F32 ? 4 : 2))
+      return AATC_E_INVALID;
+    if (ws_bytes < decode_workspace_bytes(batch, n_q_heads, n_kv_heads, cap))
+      return AATC_E_WORKSPACE;
+    return launch_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads, q, q_dtype,
+                         k_codes, k_alpha, v_codes, v_alpha, seq_len, cap, softmax_scale, out,
+                         workspace, stream);
+  } catch (...) {
+    return AATC_E_INVALID;
+  }
+}

@@ -1,0 +1,285 @@
+// Host-side calibration of one (KV head, tensor): Algorithm 1 (calibration part),
+// Sec. 5.1 (decorrelating transform, PCA form of App. D) and Sec. 5.2 (attention-aware
+// reverse water-filling and per-channel scales).  Pure C++17, fp64.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <numeric>
+#include <vector>
+
+#include "aatc.h"
+#include "params.h"
+
+// The percentile interpolation and the scale reciprocals are defined as separate
+// IEEE operations; keep the compiler from fusing them.
+#pragma clang fp contract(off)
+
+namespace aatc {
+
+// Round a double to fp16 bits, nearest-even, saturating at +-65504.
+uint16_t f64_to_f16_bits(double v) {
+  uint16_t sign = std::signbit(v) ? 0x8000 : 0;
+  double a = std::fabs(v);
+  if (std::isnan(v)) return 0x7e00;
+  if (a >= 65504.0) return sign | 0x7bff;
+  if (a == 0.0) return sign;
+  int e;
+  double m = std::frexp(a, &e);          // a = m * 2^e, m in [0.5, 1)
+  int exp16 = e - 1 + 15;                // biased exponent of a normal fp16
+  double scaled;
+  if (exp16 >= 1) {
+    scaled = std::ldexp(m, 11);          // 11 significant bits: [1024, 2048)
+  } else {
+    scaled = std::ldexp(a, 24);          // subnormal: units of 2^-24
+    exp16 = 0;
+  }
+  double fl = std::floor(scaled);
+  double frac = scaled - fl;
+  uint32_t q = (uint32_t)fl;
+  if (frac > 0.5 || (frac == 0.5 && (q & 1u))) q += 1;
+  if (exp16 == 0) {
+    // subnormal (q <= 1024; q == 1024 is the smallest normal)
+    return sign | (uint16_t)q;
+  }
+  if (q == 2048) {                       // rounding carried into the next binade
+    q = 1024;
+    exp16 += 1;
+  }
+  if (exp16 >= 31) return sign | 0x7bff;
+  return sign | (uint16_t)((exp16 << 10) | (q - 1024));
+}
+
+double f16_bits_to_f64(uint16_t h) {
+  int e = (h >> 10) & 0x1f;
+  int m = h & 0x3ff;
+  double v;
+  if (e == 0) v = std::ldexp((double)m, -24);
+  else if (e == 31) v = m ? NAN : INFINITY;
+  else v = std::ldexp((double)(m | 0x400), e - 25);
+  return (h & 0x8000) ? -v : v;
+}
+
+namespace {
+
+// Cyclic Jacobi eigendecomposition of a symmetric n x n matrix (row-major, destroyed).
+// On success: w = eigenvalues (unsorted), V columns = orthonormal eigenvectors.
+bool jacobi_eigen(std::vector<double>& a, int n, std::vector<double>& v,
+                  std::vector<double>& w) {
+  v.assign((size_t)n * n, 0.0);
+  for (int i = 0; i < n; ++i) v[(size_t)i * n + i] = 1.0;
+  bool converged = false;
+  for (int sweep = 0; sweep < 100; ++sweep) {
+    double off = 0.0, diag = 0.0;
+    for (int p = 0; p < n; ++p) {
+      diag += a[(size_t)p * n + p] * a[(size_t)p * n + p];
+      for (int q = p + 1; q < n; ++q) off += a[(size_t)p * n + q] * a[(size_t)p * n + q];
+    }
+    if (off <= 1e-32 * diag || off == 0.0) {
+      converged = true;
+      break;
+    }
+    for (int p = 0; p < n - 1; ++p) {
+      for (int q = p + 1; q < n; ++q) {
+        double apq = a[(size_t)p * n + q];
+        if (apq == 0.0) continue;
+        double app = a[(size_t)p * n + p], aqq = a[(size_t)q * n + q];
+        double theta = (aqq - app) / (2.0 * apq);
+        double t = (theta >= 0 ? 1.0 : -1.0) / (std::fabs(theta) + std::sqrt(theta * theta + 1.0));
+        double c = 1.0 / std::sqrt(t * t + 1.0), s = t * c;
+        for (int k = 0; k < n; ++k) {        // A <- A J
+          double akp = a[(size_t)k * n + p], akq = a[(size_t)k * n + q];
+          a[(size_t)k * n + p] = c * akp - s * akq;
+          a[(size_t)k * n + q] = s * akp + c * akq;
+        }
+        for (int k = 0; k < n; ++k) {        // A <- J^T A
+          double apk = a[(size_t)p * n + k], aqk = a[(size_t)q * n + k];
+          a[(size_t)p * n + k] = c * apk - s * aqk;
+          a[(size_t)q * n + k] = s * apk + c * aqk;
+        }
+        a[(size_t)p * n + q] = 0.0;
+        a[(size_t)q * n + p] = 0.0;
+        for (int k = 0; k < n; ++k) {        // V <- V J
+          double vkp = v[(size_t)k * n + p], vkq = v[(size_t)k * n + q];
+          v[(size_t)k * n + p] = c * vkp - s * vkq;
+          v[(size_t)k * n + q] = s * vkp + c * vkq;
+        }
+      }
+    }
+  }
+  w.resize(n);
+  for (int i = 0; i < n; ++i) w[i] = a[(size_t)i * n + i];
+  return converged;
+}
+
+// numpy's "linear" percentile of an ascending array: virtual index (n-1) q, then
+// lerp(a, b, t) = a + (b-a) t for t < 1/2, b - (b-a)(1-t) otherwise.
+double percentile_linear(const std::vector<double>& sorted, double q) {
+  size_t n = sorted.size();
+  double vi = (double)(n - 1) * q;
+  double lo = std::floor(vi);
+  size_t i = (size_t)lo;
+  if (i >= n - 1) return sorted[n - 1];
+  double t = vi - lo;
+  double a = sorted[i], b = sorted[i + 1];
+  double diff = b - a;
+  if (t >= 0.5) {
+    double u = diff * (1.0 - t);
+    return b - u;
+  }
+  double u = diff * t;
+  return a + u;
+}
+
+}  // namespace
+}  // namespace aatc
+
+using namespace aatc;
+
+extern "C" aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int32_t d,
+                                      const float* q_calib, int64_t n_q, int32_t q_group,
+                                      const float* w_o, int32_t d_out, double avg_bits,
+                                      int32_t b_max, double percentile,
+                                      aatc_calibration* out) {
+  try {
+    if (!x_calib || !out) return AATC_E_INVALID;
+    if (d != AATC_HEAD_DIM) return AATC_E_UNSUPPORTED;
+    if (n_calib < 2 || b_max < 1 || b_max > AATC_MAX_BITS) return AATC_E_INVALID;
+    if (!(percentile > 0.0 && percentile <= 1.0)) return AATC_E_INVALID;
+    if (!(avg_bits > 0.0) || !std::isfinite(avg_bits)) return AATC_E_INVALID;
+    if (q_calib && w_o) return AATC_E_INVALID;
+    if (q_calib && (q_group < 1 || n_q < q_group || n_q % q_group != 0)) return AATC_E_INVALID;
+    if (w_o && d_out < 1) return AATC_E_INVALID;
+    const int64_t budget = (int64_t)std::floor(avg_bits * d + 0.5);
+    if (budget < 1 || budget > (int64_t)d * b_max) return AATC_E_INVALID;
+
+    const size_t n = (size_t)n_calib;
+    for (size_t i = 0; i < n * d; ++i)
+      if (!std::isfinite(x_calib[i])) return AATC_E_NUMERIC;
+
+    // 1. Sigma = X^T X / n (fp64, uncentered).
+    std::vector<double> sigma((size_t)d * d, 0.0);
+    {
+      std::vector<double> row(d);
+      for (size_t i = 0; i < n; ++i) {
+        for (int j = 0; j < d; ++j) row[j] = x_calib[i * d + j];
+        for (int j = 0; j < d; ++j) {
+          double xj = row[j];
+          double* s = &sigma[(size_t)j * d];
+          for (int k = j; k < d; ++k) s[k] += xj * row[k];
+        }
+      }
+      for (int j = 0; j < d; ++j)
+        for (int k = j; k < d; ++k) {
+          double v = sigma[(size_t)j * d + k] / (double)n;
+          sigma[(size_t)j * d + k] = v;
+          sigma[(size_t)k * d + j] = v;
+        }
+    }
+
+    // 2. Eigendecomposition, decreasing eigenvalues, canonical signs.
+    std::vector<double> vec, lam_raw;
+    if (!jacobi_eigen(sigma, d, vec, lam_raw)) return AATC_E_NUMERIC;
+    std::vector<int> order(d);
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int a, int b) { return lam_raw[a] > lam_raw[b]; });
+    std::vector<double> p((size_t)d * d), lam(d);   // p[j*d + c]
+    for (int c = 0; c < d; ++c) {
+      int src = order[c];
+      lam[c] = lam_raw[src];
+      int jmax = 0;
+      double amax = -1.0;
+      for (int j = 0; j < d; ++j) {
+        double a = std::fabs(vec[(size_t)j * d + src]);
+        if (a > amax) { amax = a; jmax = j; }
+      }
+      double sgn = vec[(size_t)jmax * d + src] < 0 ? -1.0 : 1.0;
+      for (int j = 0; j < d; ++j) p[(size_t)j * d + c] = sgn * vec[(size_t)j * d + src];
+    }
+
+    // 3. Channel weights.
+    std::vector<double> w(d, 1.0);
+    if (q_calib) {
+      for (int64_t i = 0; i < n_q * d; ++i)
+        if (!std::isfinite(q_calib[i])) return AATC_E_NUMERIC;
+      std::fill(w.begin(), w.end(), 0.0);
+      const double t = (double)(n_q / q_group);
+      for (int64_t i = 0; i < n_q; ++i) {
+        const float* q = q_calib + i * d;
+        for (int c = 0; c < d; ++c) {
+          double acc = 0.0;
+          for (int j = 0; j < d; ++j) acc += (double)q[j] * p[(size_t)j * d + c];
+          w[c] += acc * acc;
+        }
+      }
+      for (int c = 0; c < d; ++c) w[c] /= t;
+    } else if (w_o) {
+      for (int64_t i = 0; i < (int64_t)d * d_out; ++i)
+        if (!std::isfinite(w_o[i])) return AATC_E_NUMERIC;
+      for (int c = 0; c < d; ++c) {
+        double acc2 = 0.0;
+        for (int o = 0; o < d_out; ++o) {
+          double acc = 0.0;
+          for (int j = 0; j < d; ++j) acc += p[(size_t)j * d + c] * (double)w_o[(size_t)j * d_out + o];
+          acc2 += acc * acc;
+        }
+        w[c] = acc2;
+      }
+    }
+
+    // 4. Integer reverse water-filling: greedy marginal allocation.
+    std::vector<double> wv(d);
+    for (int c = 0; c < d; ++c) wv[c] = w[c] * lam[c];
+    std::vector<int> b_eig(d, 0);
+    for (int64_t step = 0; step < budget; ++step) {
+      int best = -1;
+      double gbest = 0.0;
+      for (int c = 0; c < d; ++c) {
+        if (b_eig[c] >= b_max) continue;
+        double g = std::ldexp(wv[c], -2 * b_eig[c]);
+        if (best < 0 || g > gbest) { best = c; gbest = g; }
+      }
+      b_eig[best] += 1;
+    }
+
+    // 5. Storage order: widest first, eigen order on ties.
+    std::vector<int> perm(d);
+    std::iota(perm.begin(), perm.end(), 0);
+    std::stable_sort(perm.begin(), perm.end(),
+                     [&](int a, int b) { return b_eig[a] > b_eig[b]; });
+
+    std::memset(out, 0, sizeof(*out));
+    out->d = d;
+    out->budget_bits = (int32_t)budget;
+    out->record_bytes = (int32_t)(4 * ((budget + 31) / 32));
+    int d_active = 0;
+    for (int c = 0; c < d; ++c) {
+      int e = perm[c];
+      out->perm[c] = e;
+      out->bits[c] = (uint8_t)b_eig[e];
+      if (b_eig[e] > 0) ++d_active;
+      out->sigma2[c] = lam[c];
+      out->weight[c] = w[c];
+      out->bits_eig[c] = (uint8_t)b_eig[c];
+      for (int j = 0; j < d; ++j) out->transform[(size_t)j * d + c] = (float)p[(size_t)j * d + e];
+    }
+    out->d_active = d_active;
+
+    // 6. Per-channel scales: percentile of |h_c| over the calibration tokens, fp16.
+    std::vector<double> col(n);
+    for (int c = 0; c < d; ++c) {
+      if (out->bits[c] == 0) { out->scale_f16[c] = 0; continue; }
+      int e = perm[c];
+      for (size_t i = 0; i < n; ++i) {
+        double acc = 0.0;
+        for (int j = 0; j < d; ++j) acc += (double)x_calib[i * d + j] * p[(size_t)j * d + e];
+        col[i] = std::fabs(acc);
+      }
+      std::sort(col.begin(), col.end());
+      out->scale_f16[c] = f64_to_f16_bits(percentile_linear(col, percentile));
+    }
+    return AATC_OK;
+  } catch (...) {
+    return AATC_E_INVALID;
+  }
+}

@@ -1,0 +1,147 @@
+// AATC encode on gfx950: transform, per-token scale, quantize, pack (Algorithm 1,
+// inference part; Sec. 5.2).  Exact VALU kernel: the transform is evaluated as an exact
+// integer dot product on fixed-point operands, so every code is reproducible bit for
+// bit.  Works for any token count; one workgroup per (64-token tile, KV head).
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include "launch.h"
+#include "params.h"
+
+namespace aatc {
+namespace {
+
+constexpr int kEncThreads = 256;                 // two tokens in flight, 128 lanes each
+constexpr int kRecWords = kMaxBudget / 32;       // words of the largest record
+
+__device__ inline float load_elem(const void* x, int dtype, int64_t idx) {
+  if (dtype == AATC_BF16) {
+    uint32_t b = static_cast<const uint16_t*>(x)[idx];
+    return __uint_as_float(b << 16);
+  }
+  return static_cast<const float*>(x)[idx];
+}
+
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Quantize one transformed coefficient (canonical fp32 sequence).
+__device__ inline uint32_t quantize_code(float r, float inv_a, int b) {
+  float y = r * inv_a;
+  float xq = ldexpf(y, b - 1);
+  float f = floorf(xq);
+  int code = (int)f + ((xq - f) >= 0.5f ? 1 : 0);
+  const int half = 1 << (b - 1);
+  code = min(max(code, -half), half - 1);
+  return (uint32_t)(code + half);
+}
+
+__global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
+    const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
+    int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
+    int64_t cap, int64_t pos) {
+  __shared__ int16_t tq[kD * kD];                 // fixed-point transform of this head
+  __shared__ uint32_t rec[kTile][kRecWords];      // records of the tile's tokens
+  __shared__ int xs[2][kD];
+  __shared__ float red_x[4], red_a[4];
+
+  const int head = blockIdx.y;
+  const HeadParams* hp = head_params(params, head);
+  const int rbytes = hp->record_bytes;
+  const int rwords = rbytes / 4;
+  const int64_t tile = pos / kTile + blockIdx.x;
+  const int64_t tile_base = tile * kTile;
+  const int64_t t_begin = max(tile_base, pos);
+  const int64_t t_end = min(tile_base + kTile, pos + n_tok);
+
+  const int tid = threadIdx.x;
+  const int slot = tid >> 7;
+  const int c = tid & (kD - 1);
+  const int wave = tid >> 6;
+
+  for (int i = tid; i < kD * kD / 2; i += kEncThreads)
+    reinterpret_cast<uint32_t*>(tq)[i] = reinterpret_cast<const uint32_t*>(hp->Tq)[i];
+  for (int i = tid; i < kTile * kRecWords; i += kEncThreads) (&rec[0][0])[i] = 0u;
+  const int b = hp->bits[c];
+  const int off = hp->bit_off[c];
+  const float inv_s = hp->inv_s[c];
+  __syncthreads();
+
+  for (int64_t t0 = t_begin; t0 < t_end; t0 += 2) {
+    const int64_t t = t0 + slot;
+    const bool valid = t < t_end;
+    const float xv = valid ? load_elem(x, dtype, (t - pos) * x_stride + (int64_t)head * kD + c) : 0.f;
+    // Per-token fixed-point scale: max |x_j| goes to [2^13, 2^14).
+    float m = wave_max(fabsf(xv));
+    if ((tid & 63) == 0) red_x[wave] = m;
+    __syncthreads();
+    m = fmaxf(red_x[2 * slot], red_x[2 * slot + 1]);
+    int e = 0;
+    frexpf(m, &e);                                  // m = f * 2^e, f in [0.5, 1)
+    const int shift = (m > 0.f) ? (kXLead - (e - 1)) : 0;
+    xs[slot][c] = (int)rintf(ldexpf(xv, shift));
+    __syncthreads();
+    // Exact integer transform h_c = sum_j X_j Tq_jc (|sum| < 2^36).
+    long long acc = 0;
+#pragma unroll 8
+    for (int j = 0; j < kD; ++j) acc += (long long)xs[slot][j] * (long long)tq[j * kD + c];
+    const float h = (float)ldexp((double)acc, -(shift + kTFrac));
+    const float r = h * inv_s;
+    float a = wave_max(b > 0 ? fabsf(r) : 0.f);
+    if ((tid & 63) == 0) red_a[wave] = a;
+    __syncthreads();
+    a = fmaxf(red_a[2 * slot], red_a[2 * slot + 1]);
+    const __half a16 = __float2half_rn(fminf(a, 65504.f));
+    const float a32 = __half2float(a16);
+    // fp32 1/alpha correctly rounded (11-bit divisor: no double-rounding error).
+    const float inv_a = (a32 > 0.f) ? (float)(1.0 / (double)a32) : 0.f;
+    if (valid && b > 0) {
+      const uint32_t u = quantize_code(r, inv_a, b);
+      const int li = (int)(t - tile_base);
+      atomicOr(&rec[li][off >> 5], u << (off & 31));
+      if ((off & 31) + b > 32) atomicOr(&rec[li][(off >> 5) + 1], u >> (32 - (off & 31)));
+    }
+    if (valid && c == 0) alpha[(int64_t)head * cap + t] = __half_as_ushort(a16);
+    __syncthreads();
+  }
+
+  const int lo = (int)(t_begin - tile_base), hi = (int)(t_end - tile_base);
+  if (layout == AATC_LAYOUT_RECORDS) {
+    uint32_t* out = reinterpret_cast<uint32_t*>(codes) + ((int64_t)head * cap + tile_base) * rwords;
+    for (int i = lo * rwords + tid; i < hi * rwords; i += kEncThreads)
+      out[i] = rec[i / rwords][i % rwords];
+  } else {
+    // Bit-transposed tile: word 2v + h holds record bit v of tokens 32h .. 32h + 31.
+    uint32_t* out = reinterpret_cast<uint32_t*>(codes) +
+                    ((int64_t)head * (cap / kTile) + tile) * (16 * rbytes);
+    for (int wi = tid; wi < 16 * rbytes; wi += kEncThreads) {
+      const int v = wi >> 1, hh = wi & 1;
+      const int a0 = max(lo - 32 * hh, 0), a1 = min(hi - 32 * hh, 32);
+      if (a0 >= a1) continue;
+      const uint32_t mask = (a1 - a0 == 32) ? 0xffffffffu : (((1u << (a1 - a0)) - 1u) << a0);
+      uint32_t nw = 0;
+      for (int k = a0; k < a1; ++k) nw |= ((rec[32 * hh + k][v >> 5] >> (v & 31)) & 1u) << k;
+      const uint32_t old = (mask == 0xffffffffu) ? 0u : out[wi];
+      out[wi] = (old & ~mask) | (nw & mask);
+    }
+  }
+}
+
+}  // namespace
+
+aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_dtype x_dtype,
+                          int64_t n_tok, int64_t x_tok_stride, aatc_layout layout,
+                          void* codes, uint16_t* alpha, int64_t cap, int64_t pos,
+                          void* stream) {
+  const int64_t first = pos / kTile, last = (pos + n_tok - 1) / kTile;
+  dim3 grid((unsigned)(last - first + 1), (unsigned)n_heads);
+  hipLaunchKernelGGL(encode_exact_kernel, grid, dim3(kEncThreads), 0, (hipStream_t)stream,
+                     params, x, (int)x_dtype, n_tok, x_tok_stride, (int)layout,
+                     static_cast<uint8_t*>(codes), alpha, cap, pos);
+  return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
+}
+
+}  // namespace aatc

@@ -1,0 +1,29 @@
+// Host launchers implemented next to their kernels (encode.hip, decode.hip).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "aatc.h"
+
+namespace aatc {
+
+constexpr int kMaxGroup = 16;     // query heads per KV head handled by one workgroup
+
+uint16_t f64_to_f16_bits(double v);
+double f16_bits_to_f64(uint16_t h);
+
+aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_dtype x_dtype,
+                          int64_t n_tok, int64_t x_tok_stride, aatc_layout layout,
+                          void* codes, uint16_t* alpha, int64_t cap, int64_t pos,
+                          void* stream);
+
+size_t decode_workspace_bytes(int batch, int n_q_heads, int n_kv_heads, int64_t cap);
+
+aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
+                          int n_q_heads, int n_kv_heads, const void* q, aatc_dtype q_dtype,
+                          const void* k_codes, const uint16_t* k_alpha, const void* v_codes,
+                          const uint16_t* v_alpha, const int32_t* seq_len, int64_t cap,
+                          float softmax_scale, float* out, void* workspace, void* stream);
+
+}  // namespace aatc

@@ -1,0 +1,54 @@
+// Device parameter block of one tensor (keys or values): a header followed by one
+// HeadParams per KV head.  Built on the host by aatc_params_pack, read by the
+// encode and decode kernels.  Shared between host and device code.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace aatc {
+
+constexpr int kD = 128;                   // head dimension
+constexpr int kMaxBits = 8;               // widest channel code
+constexpr int kMaxBudget = kD * kMaxBits; // most bits per token record
+constexpr int kTile = 64;                 // tokens per value-cache tile
+constexpr int kTFrac = 14;                // fixed-point fraction bits of T
+constexpr int kXLead = 13;                // per-token x scaled into [2^13, 2^14)
+constexpr uint32_t kMagic = 0x43544141u;  // "AATC"
+
+struct alignas(256) HeadParams {
+  float T[kD * kD];               // [j][c] transform, storage channels (fp32)
+  int16_t Tq[kD * kD];            // [j][c] rint(T * 2^14), |Tq| <= 2^14
+  float inv_s[kD];                // fp32 1/s_c (0 for dropped or zero-scale channels)
+  float s[kD];                    // s_c as fp32 (exact value of the fp16 scale)
+  uint16_t s16[kD];               // s_c fp16 bits
+  uint8_t bits[kD];               // width of storage channel c
+  uint16_t bit_off[kD];           // first record bit of channel c
+  uint8_t virt_chan[kMaxBudget];  // record bit v -> storage channel
+  uint8_t virt_bit[kMaxBudget];   // record bit v -> bit index inside that channel's code
+  int32_t d_active;
+  int32_t budget;
+  int32_t record_bytes;
+  int32_t pad_;
+};
+
+struct alignas(256) TensorHeader {
+  uint32_t magic;
+  int32_t n_heads;
+  int32_t budget;
+  int32_t record_bytes;
+};
+
+inline constexpr size_t params_bytes(int n_heads) {
+  return sizeof(TensorHeader) + sizeof(HeadParams) * (size_t)n_heads;
+}
+
+#if defined(__HIPCC__)
+__host__ __device__
+#endif
+inline const HeadParams* head_params(const void* block, int head) {
+  return reinterpret_cast<const HeadParams*>(static_cast<const char*>(block) +
+                                             sizeof(TensorHeader)) + head;
+}
+
+}  // namespace aatc

@@ -1,0 +1,204 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bar: bit-exact packed codes and fp16 token scales; decode attention within 2e-3
+relative L2 of the oracle's exact fp64 attention over the decoded cache.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_14191_amd as P
+from kvsynth import workload
+from oracle import aatc as ora
+
+from helpers import (alpha_cache, device_params, oracle_tiles, record_cache, rel_l2,
+                     stored_to_torch, tile_cache)
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-3
+
+
+def _log(msg):
+    print(msg, flush=True)
+
+
+class Case:
+    """Calibrations, stored tokens and queries of a (reduced) workload."""
+
+    def __init__(self, cfg, n_tokens, batch=1, lens=None, avg_bits=None):
+        self.w = workload(cfg, n_tokens=n_tokens, batch=batch)
+        w = self.w
+        self.avg = w.cfg["avg_bits"][0] if avg_bits is None else avg_bits
+        self.lens = [n_tokens] * batch if lens is None else lens
+        self.cap = max(64, -(-max(self.lens + [1]) // 64) * 64)
+        qw = w.cfg["query_weighted_k"]
+        self.cal_k = [ora.calibrate(w.calib(h, "k"), self.avg,
+                                    q_calib=w.calib_queries(h) if qw else None,
+                                    group=w.group) for h in range(w.n_kv_heads)]
+        self.cal_v = [ora.calibrate(w.calib(h, "v"), self.avg) for h in range(w.n_kv_heads)]
+        self.k = [[w.cache(b, h, "k", n=self.lens[b]) for h in range(w.n_kv_heads)]
+                  for b in range(batch)]
+        self.v = [[w.cache(b, h, "v", n=self.lens[b]) for h in range(w.n_kv_heads)]
+                  for b in range(batch)]
+        self.q = [w.queries(b) for b in range(batch)]
+
+    def x_tokens(self, b, kind):
+        """torch [len, H_kv, 128] (fp32 or bf16) of sequence b."""
+        parts = self.k[b] if kind == "k" else self.v[b]
+        arr = np.stack(parts, axis=1)
+        return stored_to_torch(arr).cuda()
+
+    def oracle_encode(self, b, h, kind):
+        cal = (self.cal_k if kind == "k" else self.cal_v)[h]
+        x = self.w.as_f32((self.k if kind == "k" else self.v)[b][h])
+        rec, a16, _ = ora.encode(x, cal)
+        return rec, a16
+
+
+def _gpu_caches(case, params_k=None, params_v=None):
+    w = case.w
+    H, B, cap = w.n_kv_heads, w.batch, case.cap
+    pk = device_params(case.cal_k) if params_k is None else params_k
+    pv = device_params(case.cal_v) if params_v is None else params_v
+    kc = record_cache(H, cap, case.cal_k[0].record_bytes, batch=B)
+    ka = alpha_cache(H, cap, batch=B)
+    vc = tile_cache(H, cap, case.cal_v[0].record_bytes, batch=B)
+    va = alpha_cache(H, cap, batch=B)
+    for b in range(B):
+        n = case.lens[b]
+        if n == 0:
+            continue
+        xk, xv = case.x_tokens(b, "k"), case.x_tokens(b, "v")
+        P.aatc_encode(pk, H, xk, n, H * 128, P.LAYOUT_RECORDS, kc[b], ka[b], cap, 0)
+        P.aatc_encode(pv, H, xv, n, H * 128, P.LAYOUT_TILES, vc[b], va[b], cap, 0)
+    torch.cuda.synchronize()
+    return pk, pv, kc, ka, vc, va
+
+
+def _check_codes(case, kc, ka, vc, va):
+    for b in range(case.w.batch):
+        n = case.lens[b]
+        for h in range(case.w.n_kv_heads):
+            rk, ak = case.oracle_encode(b, h, "k")
+            rv, av = case.oracle_encode(b, h, "v")
+            got = kc[b, h, :n].cpu().numpy()
+            bad = np.argwhere(np.any(got != rk, axis=1))
+            assert bad.size == 0, f"seq {b} head {h}: key records differ at tokens {bad[:5].ravel()}"
+            np.testing.assert_array_equal(ka[b, h, :n].cpu().numpy().view(np.uint16),
+                                          ak.view(np.uint16))
+            np.testing.assert_array_equal(vc[b, h].cpu().numpy(), oracle_tiles(rv, case.cap))
+            np.testing.assert_array_equal(va[b, h, :n].cpu().numpy().view(np.uint16),
+                                          av.view(np.uint16))
+
+
+def _decode(case, pk, pv, kc, ka, vc, va):
+    w = case.w
+    B, H, HQ = w.batch, w.n_kv_heads, w.n_q_heads
+    q = stored_to_torch(np.stack(case.q)).cuda()
+    lens = torch.tensor(case.lens, dtype=torch.int32, device="cuda")
+    out = torch.full((B, HQ, 128), float("nan"), dtype=torch.float32, device="cuda")
+    ws = torch.zeros(P.aatc_decode_workspace_bytes(B, HQ, H, case.cap), dtype=torch.uint8,
+                     device="cuda")
+    P.aatc_decode_attention(pk, pv, B, HQ, H, q, kc, ka, vc, va, lens, case.cap,
+                            1 / np.sqrt(128), out, ws)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), ws
+
+
+def _oracle_decode(case):
+    outs = []
+    for b in range(case.w.batch):
+        n = case.lens[b]
+        q32 = case.w.as_f32(case.q[b])
+        if n == 0:
+            outs.append(np.zeros_like(q32, dtype=np.float64))
+            continue
+        enc_k = [case.oracle_encode(b, h, "k") for h in range(case.w.n_kv_heads)]
+        enc_v = [case.oracle_encode(b, h, "v") for h in range(case.w.n_kv_heads)]
+        outs.append(ora.decode_attention(q32, case.cal_k, case.cal_v, [e[0] for e in enc_k],
+                                         [e[1] for e in enc_k], [e[0] for e in enc_v],
+                                         [e[1] for e in enc_v], n))
+    return np.stack(outs)
+
+
+CASES = {
+    "cfg1_single_head_512": dict(cfg=1, n_tokens=512),
+    "cfg2_llama_ragged_1000": dict(cfg=2, n_tokens=1000),
+    "cfg3_qwen_b2_ragged": dict(cfg=3, n_tokens=700, batch=2, lens=[700, 333]),
+    "cfg5_long_qweighted_zero_bits": dict(cfg=5, n_tokens=1100, batch=2, lens=[1100, 65]),
+    "cfg4_llama_4bit_300": dict(cfg=4, n_tokens=300, avg_bits=4.0),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_encode_bit_exact_and_decode_parity(name):
+    _log(f"[case] {name}")
+    case = Case(**CASES[name])
+    pk, pv, kc, ka, vc, va = _gpu_caches(case)
+    _check_codes(case, kc, ka, vc, va)
+    out, _ = _decode(case, pk, pv, kc, ka, vc, va)
+    ref = _oracle_decode(case)
+    for b in range(case.w.batch):
+        err = rel_l2(out[b], ref[b])
+        _log(f"  seq {b} len {case.lens[b]} rel_l2 {err:.3e}")
+        assert err <= TOL
+
+
+def test_encode_incremental_appends_match_bulk():
+    """Decode-step appends (1 token, odd chunks, partial tiles) give the same caches."""
+    case = Case(cfg=2, n_tokens=300)
+    H, cap = case.w.n_kv_heads, case.cap
+    pk, pv = device_params(case.cal_k), device_params(case.cal_v)
+    xk, xv = case.x_tokens(0, "k"), case.x_tokens(0, "v")
+    kc = record_cache(H, cap, case.cal_k[0].record_bytes)
+    vc = tile_cache(H, cap, case.cal_v[0].record_bytes)
+    ka, va = alpha_cache(H, cap), alpha_cache(H, cap)
+    vc.fill_(0xA5)          # stale bytes beyond the written tokens must not matter
+    pos = 0
+    for n in [1, 1, 5, 57, 1, 64, 3, 100, 68]:
+        P.aatc_encode(pk, H, xk[pos:], n, H * 128, P.LAYOUT_RECORDS, kc, ka, cap, pos)
+        P.aatc_encode(pv, H, xv[pos:], n, H * 128, P.LAYOUT_TILES, vc, va, cap, pos)
+        pos += n
+    assert pos == 300
+    torch.cuda.synchronize()
+    for h in range(H):
+        rk, ak = case.oracle_encode(0, h, "k")
+        rv, av = case.oracle_encode(0, h, "v")
+        np.testing.assert_array_equal(kc[h, :300].cpu().numpy(), rk)
+        got = ora.tiles_to_records(vc[h].cpu().numpy(), rv.shape[1])
+        np.testing.assert_array_equal(got[:300], rv)
+        np.testing.assert_array_equal(va[h, :300].cpu().numpy().view(np.uint16), av.view(np.uint16))
+
+
+def test_decode_edge_lengths():
+    """Empty, single-token, tile-edge and ragged lengths in one batch."""
+    lens = [0, 1, 63, 64, 65, 511, 512, 513]
+    case = Case(cfg=2, n_tokens=513, batch=len(lens), lens=lens)
+    pk, pv, kc, ka, vc, va = _gpu_caches(case)
+    out, _ = _decode(case, pk, pv, kc, ka, vc, va)
+    ref = _oracle_decode(case)
+    assert np.all(out[0] == 0)
+    for b in range(1, len(lens)):
+        assert rel_l2(out[b], ref[b]) <= TOL, (b, lens[b])
+
+
+def test_decode_repeatable_and_workspace_reusable():
+    case = Case(cfg=3, n_tokens=640, batch=1)
+    pk, pv, kc, ka, vc, va = _gpu_caches(case)
+    o1, ws = _decode(case, pk, pv, kc, ka, vc, va)
+    o2, _ = _decode(case, pk, pv, kc, ka, vc, va)
+    np.testing.assert_array_equal(o1, o2)
+
+
+def test_end_to_end_with_host_calibration():
+    """aatc_calibrate (host C++) -> encode -> decode against the oracle pipeline."""
+    case = Case(cfg=5, n_tokens=800)
+    w = case.w
+    abi_k = [P.aatc_calibrate(w.calib(h, "k"), case.avg, q_calib=w.calib_queries(h),
+                              q_group=w.group) for h in range(w.n_kv_heads)]
+    abi_v = [P.aatc_calibrate(w.calib(h, "v"), case.avg) for h in range(w.n_kv_heads)]
+    pk, pv = device_params(abi_k), device_params(abi_v)
+    pk_, pv_, kc, ka, vc, va = _gpu_caches(case, pk, pv)
+    out, _ = _decode(case, pk, pv, kc, ka, vc, va)
+    ref = _oracle_decode(case)
+    assert rel_l2(out[0], ref[0]) <= TOL

@@ -1,0 +1,155 @@
+"""Host-side checks of libaatc.so that need no GPU: exports, argument validation,
+host calibration parity with the oracle, parameter packing."""
+import ctypes
+import os
+
+import numpy as np
+import pytest
+
+import paper_2608_14191_amd as P
+from kvsynth import workload
+from oracle import aatc as ora
+
+from helpers import abi_calibration
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "aatc.h")
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2608_14191_amd._lib import exported_symbols_declared_in_header
+    names = exported_symbols_declared_in_header(HEADER)
+    assert {"aatc_calibrate", "aatc_encode", "aatc_decode_attention"} <= set(names)
+    lib = P.library()
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    assert P.aatc_status_string(0) == "ok"
+    assert "workspace" in P.aatc_status_string(5)
+
+
+def _calib_cases():
+    return [(1, 0, "k"), (1, 0, "v"), (2, 3, "k"), (2, 5, "v"), (3, 1, "k"), (5, 2, "k")]
+
+
+@pytest.mark.parametrize("cfg,head,kind", _calib_cases())
+def test_host_calibration_matches_oracle(cfg, head, kind):
+    w = workload(cfg, n_tokens=64)
+    x = w.calib(head, kind)
+    avg = w.cfg["avg_bits"][0]
+    qc = w.calib_queries(head) if (kind == "k" and w.cfg["query_weighted_k"]) else None
+    g = w.group if qc is not None else 1
+    c = P.aatc_calibrate(x, avg, q_calib=qc, q_group=g)
+    o = ora.calibrate(x, avg, q_calib=qc, group=g)
+    np.testing.assert_array_equal(c.bits_np, o.bits)
+    np.testing.assert_array_equal(np.ctypeslib.as_array(c.perm), o.perm)
+    np.testing.assert_array_equal(np.ctypeslib.as_array(c.bits_eig), o.bits_eig)
+    np.testing.assert_array_equal(c.s16.view(np.uint16), o.s16.view(np.uint16))
+    assert (c.budget_bits, c.record_bytes, c.d_active) == (o.budget, o.record_bytes, o.d_active)
+    np.testing.assert_allclose(c.T, o.T32, rtol=0, atol=1e-6)
+    np.testing.assert_allclose(np.ctypeslib.as_array(c.sigma2), o.sigma2, rtol=1e-9,
+                               atol=1e-12 * o.sigma2[0])
+    np.testing.assert_allclose(np.ctypeslib.as_array(c.weight), o.weight, rtol=1e-9)
+
+
+def test_host_calibration_value_weights_match_oracle():
+    w = workload(2, n_tokens=64)
+    x = w.calib(0, "v")
+    w_o = np.random.default_rng(0).standard_normal((128, 96)).astype(np.float32)
+    c = P.aatc_calibrate(x, 2.75, w_o=w_o)
+    o = ora.calibrate(x, 2.75, w_o=w_o)
+    np.testing.assert_array_equal(c.bits_np, o.bits)
+    np.testing.assert_allclose(np.ctypeslib.as_array(c.weight), o.weight, rtol=1e-9)
+
+
+def test_host_calibration_worked_rwf_example():
+    """Diagonal covariance with variances 4, 1, 1/4, 1/16 repeated: the integer
+    allocation follows the tie rule exactly (Sec. 5.2; see test_oracle_allocation)."""
+    d = 128
+    var = np.tile([4.0, 1.0, 0.25, 0.0625], d // 4) * np.repeat(4.0 ** -np.arange(32), 4)
+    rng = np.random.default_rng(1)
+    z, _ = np.linalg.qr(rng.standard_normal((512, d)))
+    x = (z * np.sqrt(512) * np.sqrt(var)[None, :]).astype(np.float32)
+    c = P.aatc_calibrate(x, 1.0)
+    o = ora.calibrate(x, 1.0)
+    np.testing.assert_array_equal(c.bits_np, o.bits)
+
+
+@pytest.mark.parametrize("bad", ["d", "n", "bits", "pct", "both"])
+def test_calibrate_validation(bad):
+    x = np.zeros((16, 128), dtype=np.float32)
+    kwargs = dict(avg_bits=2.0)
+    if bad == "d":
+        with pytest.raises(P.AatcError) as e:
+            P.aatc_calibrate(np.zeros((16, 64), dtype=np.float32), 2.0)
+        assert e.value.status == 2
+        return
+    if bad == "n":
+        x = x[:1]
+    if bad == "bits":
+        kwargs = dict(avg_bits=9.0)
+    if bad == "pct":
+        kwargs = dict(avg_bits=2.0, percentile=1.5)
+    if bad == "both":
+        kwargs = dict(avg_bits=2.0, q_calib=np.ones((4, 128), np.float32),
+                      w_o=np.ones((128, 4), np.float32))
+    with pytest.raises(P.AatcError) as e:
+        P.aatc_calibrate(x, **kwargs)
+    assert e.value.status == 1
+
+
+def test_calibrate_rejects_non_finite():
+    x = np.ones((16, 128), dtype=np.float32)
+    x[3, 7] = np.nan
+    with pytest.raises(P.AatcError) as e:
+        P.aatc_calibrate(x, 2.0)
+    assert e.value.status == 3
+
+
+def test_params_pack_validation():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((256, 128)).astype(np.float32)
+    a = abi_calibration(ora.calibrate(x, 2.0))
+    b = abi_calibration(ora.calibrate(x, 3.0))
+    P.aatc_params_pack([a, a])
+    with pytest.raises(P.AatcError):
+        P.aatc_params_pack([a, b])                      # budgets differ
+    bad = abi_calibration(ora.calibrate(x, 2.0))
+    bad.bits[5], bad.bits[6] = bad.bits[6], bad.bits[5] + 1   # not non-increasing
+    with pytest.raises(P.AatcError):
+        P.aatc_params_pack([bad])
+
+
+def _fake(addr=4096):
+    return ctypes.c_void_p(addr)
+
+
+def test_encode_and_decode_validate_before_launch():
+    """Invalid requests are rejected on the host; nothing reaches the device."""
+    L = P.library()
+    p = _fake()
+    # d != 128
+    assert L.aatc_encode(p, 1, 64, p, 0, 1, 128, 0, p, p, 64, 0, None) == 2
+    # pos + n_tok > cap
+    assert L.aatc_encode(p, 1, 128, p, 0, 10, 128, 0, p, p, 64, 60, None) == 1
+    # tiles need cap % 64 == 0
+    assert L.aatc_encode(p, 1, 128, p, 0, 1, 128, 1, p, p, 100, 0, None) == 1
+    # null codes
+    assert L.aatc_encode(p, 1, 128, p, 0, 1, 128, 0, None, p, 64, 0, None) == 1
+    # misaligned codes
+    assert L.aatc_encode(p, 1, 128, p, 0, 1, 128, 0, _fake(4097), p, 64, 0, None) == 1
+    # n_tok = 0 is a no-op
+    assert L.aatc_encode(p, 1, 128, p, 0, 0, 128, 0, p, p, 64, 0, None) == 0
+    ws = P.aatc_decode_workspace_bytes(1, 32, 8, 4096)
+    assert ws > 0
+    args = [p, p, 1, 32, 8, 128, p, 1, p, p, p, p, p, 4096, 0.088, p, p, ws, None]
+    bad = list(args); bad[4] = 6                     # 32 % 6 != 0
+    assert L.aatc_decode_attention(*bad) == 1
+    bad = list(args); bad[13] = 100                  # cap not a multiple of 64
+    assert L.aatc_decode_attention(*bad) == 1
+    bad = list(args); bad[17] = ws - 1               # workspace too small
+    assert L.aatc_decode_attention(*bad) == 5
+    bad = list(args); bad[5] = 64
+    assert L.aatc_decode_attention(*bad) == 2
