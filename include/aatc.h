@@ -10,7 +10,8 @@
  *   - Head dimension d is 128 (v1); other values return AATC_E_UNSUPPORTED.
  *   - Channel widths are 0..8 bits (b_max <= 8).
  *   - "Device" pointers are HIP device memory owned by the caller; "host" pointers are
- *     ordinary host memory.  The library allocates no device memory, never frees
+ *     ordinary host memory.  Device buffers are 16-byte aligned unless stated
+ *     otherwise.  The library allocates no device memory, never frees
  *     caller memory and never synchronizes a stream.
  *   - Every call validates its arguments on the host and returns AATC_E_INVALID
  *     (or AATC_E_UNSUPPORTED) before launching anything.  Launch failures return
@@ -166,11 +167,15 @@ aatc_status aatc_encode(const void* dev_params, int32_t n_kv_heads, int32_t d,
  * dev_params_k / _v  device parameter blocks of the key and value tensors.
  * q          device [batch][n_q_heads][d], q_dtype F32 or BF16.
  * k_codes    device RECORDS layout, [batch][n_kv_heads][cap][R_K].
- * k_alpha    device [batch][n_kv_heads][cap] fp16.
+ * k_alpha    device [batch][n_kv_heads][cap] fp16, 16-byte aligned (as v_alpha).
  * v_codes    device TILES layout, [batch][n_kv_heads][cap / 64][64 * R_V].
  * v_alpha    device [batch][n_kv_heads][cap] fp16.
- * seq_len    device [batch] int32, 0 <= seq_len[b] <= cap (0 gives a zero output).
+ * seq_len    device [batch] int32, 0 <= seq_len[b] <= cap (0 gives a zero output;
+ *            values outside [0, cap] are clamped).
  * cap        tokens per sequence in the caches, a multiple of 64.
+ * k_record_bytes, v_record_bytes  R of the key and value tensors, as in their
+ *            calibrations (the sizes the caches were allocated with).  If they differ
+ *            from the parameter blocks, the outputs are NaN.
  * softmax_scale  logit scale, 1/sqrt(d) for standard attention.
  * out        device [batch][n_q_heads][d] fp32.
  * workspace  device scratch of at least aatc_decode_workspace_bytes(...) bytes,
@@ -184,9 +189,10 @@ aatc_status aatc_decode_attention(const void* dev_params_k, const void* dev_para
                                   int32_t d, const void* q, aatc_dtype q_dtype,
                                   const void* k_codes, const uint16_t* k_alpha,
                                   const void* v_codes, const uint16_t* v_alpha,
-                                  const int32_t* seq_len, int64_t cap, float softmax_scale,
-                                  float* out, void* workspace, size_t ws_bytes,
-                                  void* stream);
+                                  const int32_t* seq_len, int64_t cap,
+                                  int32_t k_record_bytes, int32_t v_record_bytes,
+                                  float softmax_scale, float* out, void* workspace,
+                                  size_t ws_bytes, void* stream);
 
 /* Human-readable name of a status code (static string). */
 const char* aatc_status_string(aatc_status s);

@@ -192,9 +192,10 @@ class Workload:
 
 
 def workload(config_id: int, n_tokens: Optional[int] = None,
-             batch: Optional[int] = None) -> Workload:
-    """Workload of a configuration, optionally with fewer cached tokens or sequences."""
-    cfg = CONFIGS[config_id]
+             batch: Optional[int] = None, **overrides) -> Workload:
+    """Workload of a configuration, optionally with fewer cached tokens or sequences, or
+    other fields of the configuration replaced (e.g. n_q_heads)."""
+    cfg = dict(CONFIGS[config_id], **overrides)
     return Workload(config_id=config_id, cfg=cfg,
                     n_tokens=cfg["n_tokens"] if n_tokens is None else n_tokens,
                     batch=cfg["batch"] if batch is None else batch)

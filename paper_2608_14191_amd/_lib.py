@@ -61,9 +61,10 @@ class Calibration(ctypes.Structure):
         return np.ctypeslib.as_array(self.scale_f16).copy().view(np.float16)
 
 
-if not os.path.exists(LIB):
-    raise ImportError(f"{LIB} is not built; call __graft_entry__.build() first")
-_L = ctypes.CDLL(LIB)
+LIB_PATH = os.environ.get("AATC_LIBRARY", LIB)   # optional override of the built library
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; call __graft_entry__.build() first")
+_L = ctypes.CDLL(LIB_PATH)
 
 _vp, _i32, _i64, _sz, _f32, _f64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
                                     ctypes.c_size_t, ctypes.c_float, ctypes.c_double)
@@ -83,7 +84,8 @@ _L.aatc_decode_workspace_bytes.restype = _sz
 _L.aatc_decode_workspace_bytes.argtypes = [_i32, _i32, _i32, _i64]
 _L.aatc_decode_attention.restype = ctypes.c_int
 _L.aatc_decode_attention.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32, _vp, ctypes.c_int,
-                                     _vp, _vp, _vp, _vp, _vp, _i64, _f32, _vp, _vp, _sz, _vp]
+                                     _vp, _vp, _vp, _vp, _vp, _i64, _i32, _i32, _f32, _vp, _vp,
+                                     _sz, _vp]
 
 
 def library() -> ctypes.CDLL:
@@ -176,10 +178,12 @@ def aatc_decode_workspace_bytes(batch: int, n_q_heads: int, n_kv_heads: int, cap
 
 def aatc_decode_attention(dev_params_k, dev_params_v, batch: int, n_q_heads: int,
                           n_kv_heads: int, q, k_codes, k_alpha, v_codes, v_alpha, seq_len,
-                          cap: int, softmax_scale: float, out, workspace, stream=None):
+                          cap: int, k_record_bytes: int, v_record_bytes: int,
+                          softmax_scale: float, out, workspace, stream=None):
     st = _L.aatc_decode_attention(
         _dptr(dev_params_k), _dptr(dev_params_v), int(batch), int(n_q_heads), int(n_kv_heads),
         HEAD_DIM, _dptr(q), _dtype_code(q), _dptr(k_codes), _dptr(k_alpha), _dptr(v_codes),
-        _dptr(v_alpha), _dptr(seq_len), int(cap), float(softmax_scale), _dptr(out),
-        _dptr(workspace), int(workspace.numel() * workspace.element_size()), _stream(stream))
+        _dptr(v_alpha), _dptr(seq_len), int(cap), int(k_record_bytes), int(v_record_bytes),
+        float(softmax_scale), _dptr(out), _dptr(workspace),
+        int(workspace.numel() * workspace.element_size()), _stream(stream))
     _check("aatc_decode_attention", st)

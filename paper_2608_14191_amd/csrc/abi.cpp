@@ -64,6 +64,8 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
       const aatc_calibration& c = per_head[h];
       auto* hp = const_cast<HeadParams*>(head_params(host_buf, h));
       std::memcpy(hp->T, c.transform, sizeof(hp->T));
+      for (int j = 0; j < kD; ++j)
+        for (int ch = 0; ch < kD; ++ch) hp->Tt[ch * kD + j] = c.transform[j * kD + ch];
       for (int i = 0; i < kD * kD; ++i)
         hp->Tq[i] = (int16_t)std::nearbyint(std::ldexp((double)c.transform[i], kTFrac));
       int off = 0;
@@ -127,8 +129,8 @@ extern "C" aatc_status aatc_decode_attention(
     const void* dev_params_k, const void* dev_params_v, int32_t batch, int32_t n_q_heads,
     int32_t n_kv_heads, int32_t d, const void* q, aatc_dtype q_dtype, const void* k_codes,
     const uint16_t* k_alpha, const void* v_codes, const uint16_t* v_alpha,
-    const int32_t* seq_len, int64_t cap, float softmax_scale, float* out, void* workspace,
-    size_t ws_bytes, void* stream) {
+    const int32_t* seq_len, int64_t cap, int32_t k_record_bytes, int32_t v_record_bytes,
+    float softmax_scale, float* out, void* workspace, size_t ws_bytes, void* stream) {
   try {
     if (d != kD) return AATC_E_UNSUPPORTED;
     if (!dev_params_k || !dev_params_v || !q || !k_codes || !k_alpha || !v_codes ||
@@ -138,18 +140,21 @@ extern "C" aatc_status aatc_decode_attention(
       return AATC_E_INVALID;
     if (n_q_heads / n_kv_heads > kMaxGroup) return AATC_E_UNSUPPORTED;
     if (cap < kTile || cap % kTile != 0) return AATC_E_INVALID;
+    if (k_record_bytes < 4 || k_record_bytes > kMaxBudget / 8 || k_record_bytes % 4 != 0 ||
+        v_record_bytes < 4 || v_record_bytes > kMaxBudget / 8 || v_record_bytes % 4 != 0)
+      return AATC_E_INVALID;
     if (q_dtype != AATC_F32 && q_dtype != AATC_BF16) return AATC_E_INVALID;
     if (!std::isfinite(softmax_scale)) return AATC_E_INVALID;
     if (!aligned(dev_params_k, 16) || !aligned(dev_params_v, 16) || !aligned(k_codes, 16) ||
-        !aligned(v_codes, 16) || !aligned(k_alpha, 4) || !aligned(v_alpha, 4) ||
+        !aligned(v_codes, 16) || !aligned(k_alpha, 16) || !aligned(v_alpha, 16) ||
         !aligned(seq_len, 4) || !aligned(out, 16) || !aligned(workspace, 256) ||
         !aligned(q, q_dtype == AATC_F32 ? 4 : 2))
       return AATC_E_INVALID;
     if (ws_bytes < decode_workspace_bytes(batch, n_q_heads, n_kv_heads, cap))
       return AATC_E_WORKSPACE;
     return launch_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads, q, q_dtype,
-                         k_codes, k_alpha, v_codes, v_alpha, seq_len, cap, softmax_scale, out,
-                         workspace, stream);
+                         k_codes, k_alpha, v_codes, v_alpha, seq_len, cap, k_record_bytes,
+                         v_record_bytes, softmax_scale, out, workspace, stream);
   } catch (...) {
     return AATC_E_INVALID;
   }

@@ -24,6 +24,7 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
                           int n_q_heads, int n_kv_heads, const void* q, aatc_dtype q_dtype,
                           const void* k_codes, const uint16_t* k_alpha, const void* v_codes,
                           const uint16_t* v_alpha, const int32_t* seq_len, int64_t cap,
-                          float softmax_scale, float* out, void* workspace, void* stream);
+                          int k_record_bytes, int v_record_bytes, float softmax_scale,
+                          float* out, void* workspace, void* stream);
 
 }  // namespace aatc

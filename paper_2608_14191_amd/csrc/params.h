@@ -18,6 +18,7 @@ constexpr uint32_t kMagic = 0x43544141u;  // "AATC"
 
 struct alignas(256) HeadParams {
   float T[kD * kD];               // [j][c] transform, storage channels (fp32)
+  float Tt[kD * kD];              // [c][j] the same transform, transposed
   int16_t Tq[kD * kD];            // [j][c] rint(T * 2^14), |Tq| <= 2^14
   float inv_s[kD];                // fp32 1/s_c (0 for dropped or zero-scale channels)
   float s[kD];                    // s_c as fp32 (exact value of the fp16 scale)

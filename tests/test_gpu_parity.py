@@ -25,8 +25,8 @@ def _log(msg):
 class Case:
     """Calibrations, stored tokens and queries of a (reduced) workload."""
 
-    def __init__(self, cfg, n_tokens, batch=1, lens=None, avg_bits=None):
-        self.w = workload(cfg, n_tokens=n_tokens, batch=batch)
+    def __init__(self, cfg, n_tokens, batch=1, lens=None, avg_bits=None, **overrides):
+        self.w = workload(cfg, n_tokens=n_tokens, batch=batch, **overrides)
         w = self.w
         self.avg = w.cfg["avg_bits"][0] if avg_bits is None else avg_bits
         self.lens = [n_tokens] * batch if lens is None else lens
@@ -100,6 +100,7 @@ def _decode(case, pk, pv, kc, ka, vc, va):
     ws = torch.zeros(P.aatc_decode_workspace_bytes(B, HQ, H, case.cap), dtype=torch.uint8,
                      device="cuda")
     P.aatc_decode_attention(pk, pv, B, HQ, H, q, kc, ka, vc, va, lens, case.cap,
+                            case.cal_k[0].record_bytes, case.cal_v[0].record_bytes,
                             1 / np.sqrt(128), out, ws)
     torch.cuda.synchronize()
     return out.cpu().numpy(), ws
@@ -127,6 +128,9 @@ CASES = {
     "cfg3_qwen_b2_ragged": dict(cfg=3, n_tokens=700, batch=2, lens=[700, 333]),
     "cfg5_long_qweighted_zero_bits": dict(cfg=5, n_tokens=1100, batch=2, lens=[1100, 65]),
     "cfg4_llama_4bit_300": dict(cfg=4, n_tokens=300, avg_bits=4.0),
+    # outside the MFMA kernel's range: the generic kernel runs these
+    "generic_gqa16": dict(cfg=2, n_tokens=700, n_q_heads=32, n_kv_heads=2),
+    "generic_6bit": dict(cfg=4, n_tokens=400, avg_bits=6.0),
 }
 
 

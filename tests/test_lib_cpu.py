@@ -144,12 +144,16 @@ def test_encode_and_decode_validate_before_launch():
     assert L.aatc_encode(p, 1, 128, p, 0, 0, 128, 0, p, p, 64, 0, None) == 0
     ws = P.aatc_decode_workspace_bytes(1, 32, 8, 4096)
     assert ws > 0
-    args = [p, p, 1, 32, 8, 128, p, 1, p, p, p, p, p, 4096, 0.088, p, p, ws, None]
+    args = [p, p, 1, 32, 8, 128, p, 1, p, p, p, p, p, 4096, 44, 44, 0.088, p, p, ws, None]
     bad = list(args); bad[4] = 6                     # 32 % 6 != 0
     assert L.aatc_decode_attention(*bad) == 1
     bad = list(args); bad[13] = 100                  # cap not a multiple of 64
     assert L.aatc_decode_attention(*bad) == 1
-    bad = list(args); bad[17] = ws - 1               # workspace too small
+    bad = list(args); bad[14] = 42                   # record size not a multiple of 4
+    assert L.aatc_decode_attention(*bad) == 1
+    bad = list(args); bad[15] = 132                  # record larger than 1024 bits
+    assert L.aatc_decode_attention(*bad) == 1
+    bad = list(args); bad[19] = ws - 1               # workspace too small
     assert L.aatc_decode_attention(*bad) == 5
     bad = list(args); bad[5] = 64
     assert L.aatc_decode_attention(*bad) == 2
