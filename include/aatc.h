@@ -26,9 +26,11 @@
  *     LSB-first bit string: storage channel c occupies bits [o_c, o_c + b_c), o_c the
  *     sum of the earlier widths; bit i is bit (i % 8) of byte (i / 8); zero padded.
  *   - TILES (used for values): [n_kv_heads][cap / 64][64 * R] bytes.  Tile j holds
- *     tokens 64 j .. 64 j + 63 bit-transposed: record bit v of token 64 j + 32 h + t
- *     is bit t of the little-endian 32-bit word (v, h) of the tile, word index
- *     2 v + h.  cap must be a multiple of 64.
+ *     tokens 64 j .. 64 j + 63 bit-transposed: record bit v of token 64 j + t, with
+ *     t = 16 d + 4 g + i (d, g, i in 0..3), is bit 8 i + 2 g + (d mod 2) of the
+ *     little-endian 32-bit word 2 v + d / 2 of the tile.  cap must be a multiple of
+ *     64.  (This order makes the decode kernel's value operands line up with its
+ *     score outputs.)
  *   - Token scales alpha: [n_kv_heads][cap] fp16 bit patterns, for either layout.
  */
 #ifndef AATC_H_

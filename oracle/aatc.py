@@ -332,14 +332,24 @@ def unpack_records(rec: np.ndarray, bits: np.ndarray) -> np.ndarray:
     return u
 
 
+def _tile_token_of_bit() -> np.ndarray:
+    """Token (0..63) of each (word W, bit p) position of a value tile: t = 16 d + 4 g + i
+    is stored in word W = d // 2 at bit p = 8 i + 2 g + d % 2."""
+    tok = np.zeros((2, 32), dtype=np.int64)
+    for t in range(TILE_TOKENS):
+        d, g, i = t // 16, (t // 4) % 4, t % 4
+        tok[d // 2, 8 * i + 2 * g + d % 2] = t
+    return tok
+
+
 def records_to_tiles(rec: np.ndarray) -> np.ndarray:
     """Value-cache layout: tiles of 64 tokens, bit-transposed.
 
-    Record bit v of the 64 tokens of tile j is stored as two little-endian 32-bit
-    words, word (j, v, half) holding, at bit t, record bit v of token
-    64 j + 32 half + t.  A tile is 8R words x 2 = 64 R bytes, the same bytes as its 64
-    records.  The token count must be a multiple of 64.  Returns uint8
-    [n_tiles, 64 R].
+    Record bit v of the 64 tokens of tile j is stored in two little-endian 32-bit words
+    (j, v, W), W = 0, 1.  Token t = 16 d + 4 g + i of the tile (d, g, i in 0..3) sits
+    in word W = d // 2 at bit 8 i + 2 g + d % 2.  A tile is 8R words x 2 = 64 R bytes,
+    the same bytes as its 64 records.  The token count must be a multiple of 64.
+    Returns uint8 [n_tiles, 64 R].
     """
     rec = np.asarray(rec, dtype=np.uint8)
     n, rbytes = rec.shape
@@ -347,7 +357,9 @@ def records_to_tiles(rec: np.ndarray) -> np.ndarray:
         raise ValueError("token count must be a multiple of 64")
     flat = np.unpackbits(rec, axis=1, bitorder="little")              # [n, 8R]
     nt = n // TILE_TOKENS
-    b = flat.reshape(nt, 2, 32, 8 * rbytes).transpose(0, 3, 1, 2)    # [nt, 8R, 2, 32]
+    tok = _tile_token_of_bit()                                        # [2, 32]
+    b = flat.reshape(nt, TILE_TOKENS, 8 * rbytes)[:, tok, :]          # [nt, 2, 32, 8R]
+    b = b.transpose(0, 3, 1, 2)                                       # [nt, 8R, 2, 32]
     return np.packbits(b, axis=-1, bitorder="little").reshape(nt, 64 * rbytes)
 
 
@@ -356,8 +368,10 @@ def tiles_to_records(tiles: np.ndarray, rbytes: int) -> np.ndarray:
     tiles = np.asarray(tiles, dtype=np.uint8)
     nt = tiles.shape[0]
     b = np.unpackbits(tiles.reshape(nt, 8 * rbytes, 2, 4), axis=-1, bitorder="little")
-    flat = b.transpose(0, 2, 3, 1).reshape(nt * TILE_TOKENS, 8 * rbytes)
-    return np.packbits(flat, axis=1, bitorder="little")
+    b = b.transpose(0, 2, 3, 1)                                       # [nt, 2, 32, 8R]
+    flat = np.zeros((nt, TILE_TOKENS, 8 * rbytes), dtype=np.uint8)
+    flat[:, _tile_token_of_bit(), :] = b
+    return np.packbits(flat.reshape(nt * TILE_TOKENS, 8 * rbytes), axis=1, bitorder="little")
 
 
 def encode(x32: np.ndarray, cal: Calibration):

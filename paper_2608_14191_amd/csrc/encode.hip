@@ -114,18 +114,23 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
     for (int i = lo * rwords + tid; i < hi * rwords; i += kEncThreads)
       out[i] = rec[i / rwords][i % rwords];
   } else {
-    // Bit-transposed tile: word 2v + h holds record bit v of tokens 32h .. 32h + 31.
+    // Bit-transposed tile: word 2 v + W holds record bit v of the tile's tokens
+    // t = 16 d + 4 g + i with d / 2 = W, at bit 8 i + 2 g + d % 2.
     uint32_t* out = reinterpret_cast<uint32_t*>(codes) +
                     ((int64_t)head * (cap / kTile) + tile) * (16 * rbytes);
     for (int wi = tid; wi < 16 * rbytes; wi += kEncThreads) {
-      const int v = wi >> 1, hh = wi & 1;
-      const int a0 = max(lo - 32 * hh, 0), a1 = min(hi - 32 * hh, 32);
-      if (a0 >= a1) continue;
-      const uint32_t mask = (a1 - a0 == 32) ? 0xffffffffu : (((1u << (a1 - a0)) - 1u) << a0);
-      uint32_t nw = 0;
-      for (int k = a0; k < a1; ++k) nw |= ((rec[32 * hh + k][v >> 5] >> (v & 31)) & 1u) << k;
+      const int v = wi >> 1, W = wi & 1;
+      uint32_t mask = 0, nw = 0;
+      for (int p = 0; p < 32; ++p) {
+        const int t = 16 * (2 * W + (p & 1)) + 4 * ((p >> 1) & 3) + (p >> 3);
+        if (t >= lo && t < hi) {
+          mask |= 1u << p;
+          nw |= ((rec[t][v >> 5] >> (v & 31)) & 1u) << p;
+        }
+      }
+      if (!mask) continue;
       const uint32_t old = (mask == 0xffffffffu) ? 0u : out[wi];
-      out[wi] = (old & ~mask) | (nw & mask);
+      out[wi] = (old & ~mask) | nw;
     }
   }
 }

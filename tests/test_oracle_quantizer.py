@@ -146,17 +146,28 @@ def test_record_roundtrip_and_padding():
 
 
 def test_tile_layout_single_bit():
-    """One set bit (token 64*1 + 32 + 5, record bit 13) lands at word (1, 13, 1), bit 5."""
+    """One set bit (token 64*1 + 37, record bit 13) lands at word (1, 13, 1), bit 10:
+    t = 37 = 16*2 + 4*1 + 1, so W = 2 // 2 = 1 and p = 8*1 + 2*1 + 2 % 2 = 10."""
     rbytes = 8
     rec = np.zeros((128, rbytes), dtype=np.uint8)
-    rec[64 + 32 + 5, 13 // 8] = 1 << (13 % 8)
+    rec[64 + 37, 13 // 8] = 1 << (13 % 8)
     tiles = aatc.records_to_tiles(rec)
     assert tiles.shape == (2, 64 * rbytes)
     words = tiles.view("<u4").reshape(2, 8 * rbytes, 2)
     nz = np.argwhere(words)
     assert nz.tolist() == [[1, 13, 1]]
-    assert words[1, 13, 1] == 1 << 5
+    assert words[1, 13, 1] == 1 << 10
     np.testing.assert_array_equal(aatc.tiles_to_records(tiles, rbytes), rec)
+
+
+def test_tile_layout_is_a_permutation_of_tokens():
+    """Each token of a tile owns exactly one bit position per record bit."""
+    rbytes = 4
+    for t in range(64):
+        rec = np.zeros((64, rbytes), dtype=np.uint8)
+        rec[t, 0] = 1
+        words = aatc.records_to_tiles(rec).view("<u4").reshape(8 * rbytes, 2)
+        assert np.count_nonzero(words) == 1 and bin(int(words.sum())).count("1") == 1
 
 
 def test_tile_roundtrip_random():
