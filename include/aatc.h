@@ -22,6 +22,7 @@
  *
  * Cache layouts (per sequence; B_b = sum of a tensor's channel widths, the "budget",
  * R = 4 * ceil(B_b / 32) bytes per token):
+ *   - Codes are stored as b_c-bit two's complement patterns.
  *   - RECORDS (used for keys): [n_kv_heads][cap][R] bytes.  Token t's codes are one
  *     LSB-first bit string: storage channel c occupies bits [o_c, o_c + b_c), o_c the
  *     sum of the earlier widths; bit i is bit (i % 8) of byte (i / 8); zero padded.
@@ -137,8 +138,8 @@ aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_t n_kv_head
  * arithmetic (x scaled per token so max |x_j| lies in [2^13, 2^14) and rounded to
  * integers; T rounded to multiples of 2^-14; one final fp32 rounding); r_c = h_c *
  * (1/s_c); alpha = fp16(max over stored channels of |r_c|); code_c = clamp(floor(
- * r_c * (1/alpha) * 2^(b_c - 1) + 1/2), -2^(b_c-1), 2^(b_c-1) - 1) stored as
- * u_c = code_c + 2^(b_c - 1), packed in `layout`.
+ * r_c * (1/alpha) * 2^(b_c - 1) + 1/2), -2^(b_c-1), 2^(b_c-1) - 1) stored as its
+ * b_c-bit two's complement pattern, packed in `layout`.
  *
  * dev_params   device block from aatc_params_pack (this tensor, n_kv_heads heads).
  * x            device [n_tok] tokens, token t at x + t * x_tok_stride elements, each

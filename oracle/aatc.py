@@ -255,10 +255,10 @@ def quantize(h32: np.ndarray, bits: np.ndarray, s16: np.ndarray):
 
     For each token: alpha = max_c |h_c / s_c| over channels with b_c >= 1; with
     Delta_c = 2 alpha s_c / 2^b_c the code is clamp(floor(h_c / Delta_c + 1/2),
-    -2^(b-1), 2^(b-1) - 1), stored unsigned as u = code + 2^(b-1).
+    -2^(b-1), 2^(b-1) - 1).
     The canonical fp32 evaluation is r = h * (1/s), alpha16 = fp16(max |r|),
     y = r * (1/alpha16), x = y * 2^(b-1), code = floor(x + 1/2) taken exactly.
-    Returns (u [n, d] int64 with 0 for dropped channels, alpha16 [n] fp16).
+    Returns (code [n, d] int64 with 0 for dropped channels, alpha16 [n] fp16).
     """
     h = np.asarray(h32, dtype=np.float32)
     bits = np.asarray(bits, dtype=np.int64)
@@ -279,57 +279,62 @@ def quantize(h32: np.ndarray, bits: np.ndarray, s16: np.ndarray):
     lo = np.where(keep, -half, 0)
     hi = np.where(keep, half - 1, 0)
     code = np.clip(code.astype(np.int64), lo[None, :], hi[None, :])
-    u = np.where(keep[None, :], code + half[None, :], 0)
-    return u.astype(np.int64), alpha16
+    return code.astype(np.int64), alpha16
 
 
-def dequantize(u: np.ndarray, alpha16: np.ndarray, bits: np.ndarray,
+def dequantize(code: np.ndarray, alpha16: np.ndarray, bits: np.ndarray,
                s16: np.ndarray) -> np.ndarray:
-    """h^_c = Delta_c * code = alpha s_c 2^(1-b_c) (u_c - 2^(b_c-1)); 0 for b_c = 0."""
+    """h^_c = Delta_c * code_c = alpha s_c 2^(1-b_c) code_c; 0 for b_c = 0."""
     bits = np.asarray(bits, dtype=np.int64)
     keep = bits > 0
     s = np.asarray(s16, dtype=np.float16).astype(np.float64)
     a = np.asarray(alpha16, dtype=np.float16).astype(np.float64)
-    half = np.where(keep, np.ldexp(1.0, np.maximum(bits - 1, 0)), 0.0)
     step = np.where(keep, s * np.ldexp(1.0, 1 - bits), 0.0)
-    return a[:, None] * step[None, :] * (np.asarray(u, dtype=np.float64) - half[None, :])
+    return a[:, None] * step[None, :] * np.asarray(code, dtype=np.float64)
 
 
 # --------------------------------------------------------------------------------------
 # Packing (the paper does not specify one; this is the layout the path defines)
 # --------------------------------------------------------------------------------------
-def pack_records(u: np.ndarray, bits: np.ndarray) -> np.ndarray:
+def pack_records(code: np.ndarray, bits: np.ndarray) -> np.ndarray:
     """Token-major records: the codes of one token as one LSB-first bit string.
 
     Channel c (storage order) occupies bits [o_c, o_c + b_c) with o_c = sum of the
-    earlier widths, least significant bit first; bit i of the record is bit i % 8 of
-    byte i // 8.  The record is zero-padded to R = 4 * ceil(B / 32) bytes.
+    earlier widths and holds the b_c-bit two's complement pattern of its code, least
+    significant bit first; bit i of the record is bit i % 8 of byte i // 8.  The record
+    is zero-padded to R = 4 * ceil(B / 32) bytes.
     """
-    u = np.asarray(u, dtype=np.int64)
+    code = np.asarray(code, dtype=np.int64)
     bits = np.asarray(bits, dtype=np.int64)
-    n = u.shape[0]
+    n = code.shape[0]
     budget = int(bits.sum())
     rbytes = 4 * ((budget + 31) // 32)
     flat = np.zeros((n, 8 * rbytes), dtype=np.uint8)
     off = 0
     for c, b in enumerate(bits):
+        pattern = np.mod(code[:, c], 1 << int(b))           # two's complement, b bits
         for k in range(int(b)):
-            flat[:, off + k] = (u[:, c] >> k) & 1
+            flat[:, off + k] = (pattern >> k) & 1
         off += int(b)
     return np.packbits(flat, axis=1, bitorder="little")
 
 
 def unpack_records(rec: np.ndarray, bits: np.ndarray) -> np.ndarray:
-    """Inverse of ``pack_records``: codes u [n, d]."""
+    """Inverse of ``pack_records``: signed codes [n, d] (0 for dropped channels)."""
     bits = np.asarray(bits, dtype=np.int64)
     flat = np.unpackbits(np.asarray(rec, dtype=np.uint8), axis=1, bitorder="little")
-    u = np.zeros((rec.shape[0], bits.size), dtype=np.int64)
+    code = np.zeros((rec.shape[0], bits.size), dtype=np.int64)
     off = 0
     for c, b in enumerate(bits):
-        for k in range(int(b)):
-            u[:, c] |= flat[:, off + k].astype(np.int64) << k
-        off += int(b)
-    return u
+        b = int(b)
+        if b == 0:
+            continue
+        u = np.zeros(rec.shape[0], dtype=np.int64)
+        for k in range(b):
+            u |= flat[:, off + k].astype(np.int64) << k
+        code[:, c] = np.where(u >= (1 << (b - 1)), u - (1 << b), u)
+        off += b
+    return code
 
 
 def _tile_token_of_bit() -> np.ndarray:
@@ -375,10 +380,10 @@ def tiles_to_records(tiles: np.ndarray, rbytes: int) -> np.ndarray:
 
 
 def encode(x32: np.ndarray, cal: Calibration):
-    """Encode tokens [n, d] of one head: (records [n, R] uint8, alpha16 [n], u [n, d])."""
+    """Encode tokens [n, d] of one head: (records [n, R] uint8, alpha16 [n], codes [n, d])."""
     h = fixed_point_transform(x32, cal.T32)
-    u, alpha16 = quantize(h, cal.bits, cal.s16)
-    return pack_records(u, cal.bits), alpha16, u
+    code, alpha16 = quantize(h, cal.bits, cal.s16)
+    return pack_records(code, cal.bits), alpha16, code
 
 
 def decode_tokens(rec: np.ndarray, alpha16: np.ndarray, cal: Calibration) -> np.ndarray:

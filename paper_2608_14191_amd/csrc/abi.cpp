@@ -80,8 +80,11 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
         // to fp32 without a double-rounding error.
         hp->inv_s[ch] = (b && s > 0.0) ? (float)(1.0 / s) : 0.0f;
         for (int k = 0; k < b; ++k) {
-          hp->virt_chan[off + k] = (uint8_t)ch;
-          hp->virt_bit[off + k] = (uint8_t)k;
+          const int v = off + k;
+          hp->virt_chan[v] = (uint8_t)ch;
+          hp->virt_bit[v] = (uint8_t)k;
+          hp->bit_desc[((v >> 5) * 8 + (v & 7)) * 4 + ((v >> 3) & 3)] =
+              (uint16_t)(0x8000 | (k == b - 1 ? 0x4000 : 0) | ((8 + k + 1 - b) << 8) | ch);
         }
         off += b;
       }

@@ -2,15 +2,19 @@
 // transformed domain of App. B: q~ = T_K^T q; the inverse transform T_V is applied once
 // to each output).
 //
-// Grid: (token split, KV head, sequence).  Each workgroup scores its split's tokens for
-// the G query heads of its KV head, runs a split-local softmax and accumulates the
-// value codes into a partial (m, l, o~).  The last workgroup of each (sequence, KV
-// head) to finish merges the partials and applies T_V.
+// Grid: one workgroup per (sequence, KV head, token split).  Each workgroup scores its
+// split's tokens for the G query heads of its KV head, runs a split-local softmax and
+// accumulates the value codes into a partial (m, l, o~) in the workspace.  The last
+// workgroup of each (sequence, KV head) to finish merges the partials and applies T_V.
 //
 // Two kernels share that structure:
-//  * decode_mfma_kernel: G <= 8 and budgets <= 512 bits per token; both contractions
-//    on int8 MFMA over the bits of the packed codes (see the comment above it);
+//  * decode_mfma_kernel: G <= 8 and records of at most 64 bytes (budgets <= 512 bits);
+//    both contractions run on int8 MFMA over the bits of the packed codes;
 //  * decode_split_kernel: any G <= 16 and budget; plain VALU.
+//
+// Codes are b-bit two's complement patterns, code = sum_{k < b-1} 2^k bit_k -
+// 2^(b-1) bit_(b-1): every record bit is a virtual channel whose weight is its
+// channel's weight times +-2^k, and sums over bits need no offset term.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -22,16 +26,45 @@
 namespace aatc {
 namespace {
 
-constexpr int kDecThreads = 256;
+constexpr int kThreads = 256;                    // generic kernel: four waves
 constexpr int kSplit = 512;                      // tokens per workgroup, generic kernel
 constexpr int kMinSplit = 256;                   // smallest split of either kernel
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kMaxPairs = 4;     // record dword quads per key record (<= 512 bits)
-constexpr int kMaxNH = 8;        // head slots of the MFMA kernel (G <= 8)
-constexpr int kSpinLimit = 1000; // polls (~0.3 us each) for the published query planes
+constexpr int kMaxNH = 8;                        // head slots of the MFMA kernel
+constexpr int kRsrcWord3 = 0x00020000;           // raw buffer descriptor word 3 (gfx950)
+constexpr int kCoherent = 16;                    // cache policy sc1: device-coherent access
+constexpr int kMergeU = 8;                       // split partials in flight per merging thread
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v2f __attribute__((ext_vector_type(2)));
+
+struct alignas(16) Partial {   // per (sequence, KV head, split, head-in-group)
+  float m;                     // split max of the log2-domain logits
+  float l;                     // sum of 2^(z - m)
+  float pad_[2];
+  float o[kD];                 // sum of 2^(z - m) h^V (transformed domain, storage channels)
+};
+
+struct DecodeArgs {
+  const void* params_k;
+  const void* params_v;
+  const void* q;
+  const uint8_t* k_codes;
+  const uint16_t* k_alpha;
+  const uint8_t* v_codes;
+  const uint16_t* v_alpha;
+  const int32_t* seq_len;
+  float* out;
+  unsigned* counters;
+  Partial* partials;
+  int64_t cap;
+  int n_q_heads, n_kv_heads, G, q_dtype;
+  int n_splits, n_blocks;         // splits per (sequence, KV head); rows x splits
+  int rk, rv;                     // record bytes
+  float scale_log2e;
+  int off_v, off_ak, off_av, off_ql, off_pb, off_ob, ob_stride;   // dynamic LDS layout
+};
 
 __device__ inline float load_q(const void* q, int dtype, int64_t idx) {
   if (dtype == AATC_BF16) {
@@ -45,6 +78,38 @@ __device__ inline float half_bits_to_float(uint16_t h) {
   return __half2float(__ushort_as_half(h));
 }
 
+// Buffer descriptors: loads past `bytes` return 0, stores past it are dropped.
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           kRsrcWord3);
+}
+template <int AUX>
+__device__ inline v4i buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return (v4i)__builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, AUX);
+}
+__device__ inline v2f buf_load8_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return (v2f)__builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, kCoherent);
+}
+__device__ inline void buf_store16_coherent(v4f v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b128((v4i)v, r, (int)off, 0, kCoherent);
+}
+__device__ inline void buf_store4_coherent(float v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_int(v), r, (int)off, 0, kCoherent);
+}
+
+// Device-coherent scalar store: a relaxed agent-scope atomic is performed where every
+// compute unit of the device sees it (it bypasses the per-XCD caches).
+__device__ inline void st_dev(float* p, float v) {
+  __hip_atomic_store(reinterpret_cast<unsigned*>(p), __float_as_uint(v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
 __device__ inline float block_reduce(float v, bool is_max, float* scratch) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
@@ -56,178 +121,219 @@ __device__ inline float block_reduce(float v, bool is_max, float* scratch) {
   if ((threadIdx.x & 63) == 0) scratch[wave] = v;
   __syncthreads();
   float r = scratch[0];
-  for (int i = 1; i < kDecThreads / 64; ++i) r = is_max ? fmaxf(r, scratch[i]) : r + scratch[i];
+  for (int i = 1; i < kThreads / 64; ++i) r = is_max ? fmaxf(r, scratch[i]) : r + scratch[i];
   return r;
 }
 
-struct alignas(16) Partial {   // per (sequence, KV head, split, head-in-group)
-  float m;                     // split max of the log2-domain logits
-  float l;                     // sum of 2^(z - m)
-  float pad_[2];
-  float o[kD];                 // sum of 2^(z - m) h^V (transformed domain, storage channels)
-};
+// Lane-quad data movement (lanes 4k .. 4k + 3): xor 1 and xor 2 within the quad.
+__device__ inline uint32_t quad_xor1(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+}
+__device__ inline uint32_t quad_xor2(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+}
+__device__ inline float quad_xor1(float v) { return __uint_as_float(quad_xor1(__float_as_uint(v))); }
+__device__ inline float quad_xor2(float v) { return __uint_as_float(quad_xor2(__float_as_uint(v))); }
 
-// Query bit weights of one (sequence, KV head), published by split 0 of the MFMA kernel.
-struct alignas(256) QPlanes {
-  uint8_t ql[4 * kMaxNH * 2 * kMaxPairs * 64];   // [limb][head][K-step][64 bytes]
-  int cofs[kMaxNH][4];                           // key offset per head and limb
-  int fexp[kMaxNH];                              // fixed-point exponent per head
-};
+// Reduce-scatter over the quad: lane L of the quad returns sum over the quad's lanes of
+// their x[L].
+__device__ inline float quad_reduce_scatter(const float x[4], int L) {
+  const bool o1 = L & 1, o2 = L & 2;
+  const float k0 = o1 ? x[1] : x[0], s0 = o1 ? x[0] : x[1];
+  const float k1 = o1 ? x[3] : x[2], s1 = o1 ? x[2] : x[3];
+  const float y0 = k0 + quad_xor1(s0), y1 = k1 + quad_xor1(s1);
+  const float keep = o2 ? y1 : y0, send = o2 ? y0 : y1;
+  return keep + quad_xor2(send);
+}
 
+__device__ inline float quad_max(float v) {
+  v = fmaxf(v, quad_xor1(v));
+  return fmaxf(v, quad_xor2(v));
+}
+__device__ inline float quad_sum(float v) {
+  v += quad_xor1(v);
+  return v + quad_xor2(v);
+}
+
+// Four balanced int8 limbs of a 32-bit value |x| < 2^30, packed in one dword (limb L in
+// byte L, two's complement): x = sum_L limb_L 256^L.
+__device__ inline uint32_t pack_limbs(int x) {
+  return ((uint32_t)x + 0x80808080u) ^ 0x80808080u;
+}
+
+__device__ inline v4i mfma_i8(v4i a, v4i b, v4i c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------------------------------
+// Workspace: arrival counters per (sequence, KV head), then the split partials.
+// ---------------------------------------------------------------------------------------
 struct WsLayout {
-  size_t counters, flags, planes, partials, total;
+  size_t counters, partials, total;
 };
 
 __host__ __device__ inline size_t round256(size_t x) { return (x + 255) / 256 * 256; }
 
-__host__ __device__ inline WsLayout ws_layout(int batch, int n_q_heads, int n_kv_heads,
-                                              int64_t cap) {
+inline WsLayout ws_layout(int batch, int n_q_heads, int n_kv_heads, int64_t cap) {
   const size_t rows = (size_t)batch * n_kv_heads;
   const size_t n_splits = (size_t)((cap + kMinSplit - 1) / kMinSplit);
   WsLayout w;
   w.counters = 0;
-  w.flags = round256(rows * sizeof(unsigned));
-  w.planes = w.flags + round256(rows * sizeof(unsigned));
-  w.partials = w.planes + rows * sizeof(QPlanes);
+  w.partials = round256(rows * sizeof(unsigned));
   w.total = w.partials + (size_t)batch * n_q_heads * n_splits * sizeof(Partial);
   return w;
 }
 
-// Device-coherent accesses: relaxed agent-scope atomics are performed at the level all
-// compute units of the device see (they bypass the per-XCD L2), so publishing a few
-// values costs neither an L2 writeback nor an invalidate.
-__device__ inline void st_dev(float* p, float v) {
-  __hip_atomic_store(reinterpret_cast<unsigned*>(p), __float_as_uint(v), __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline void st_dev(int* p, int v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline unsigned ld_dev(const unsigned* p) {
-  return __hip_atomic_load(const_cast<unsigned*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Bytes of LDS the merge of an NTHR-thread workgroup needs (at the start of the dynamic
+// LDS).
+constexpr size_t merge_lds_bytes(int G, int NTHR) {
+  return (size_t)(6 * NTHR + G * kD + (NTHR / 32) * G * kD) * sizeof(float);
 }
 
-// Called by every workgroup after it stored its partial (m, l, o~) with st_dev.  The
-// last workgroup of a (sequence, KV head) to arrive merges the split partials of its G
-// query heads and applies the inverse transform o = T_V o~ / l; it also resets the
-// arrival counter and the query-plane flag for the next call.  `lds` must hold
-// (9 G + 4) kD + 4 kDecThreads floats.
-__device__ void merge_if_last(const void* params_v, int n_q_heads, int kvh, int seq,
-                              int64_t kv_row, int G, float* out, unsigned* counters,
-                              unsigned* flags, const Partial* partials, int n_splits,
-                              float* lds) {
-  __shared__ unsigned last_flag;
-  __shared__ float mm[kMaxGroup], ll[kMaxGroup];
+// Called by every workgroup after it stored its partial with device-coherent stores.
+// The last workgroup of the (sequence, KV head) `row` to arrive merges the split
+// partials of its G query heads, applies o = T_V o~ / l and resets the arrival counter.
+// A NaN split maximum (records that do not match the parameters) makes the output NaN.
+template <int NTHR>
+__device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int64_t row, int G,
+                                              int n_splits, const Partial* partials,
+                                              unsigned* counters, float* out_rows, float* lds) {
+  constexpr int NCB = NTHR / 32;          // column blocks of the T_V product
+  constexpr int CW = kD / NCB;            // columns per block
+  __shared__ unsigned last_s;
   const int tid = threadIdx.x;
   __builtin_amdgcn_s_waitcnt(0);          // this thread's partial stores have completed
   __syncthreads();
   if (tid == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(&counters[kv_row], 1u, __ATOMIC_RELAXED,
+    const unsigned prev = __hip_atomic_fetch_add(&counters[row], 1u, __ATOMIC_RELAXED,
                                                  __HIP_MEMORY_SCOPE_AGENT);
-    last_flag = (prev == (unsigned)n_splits - 1u) ? 1u : 0u;
+    last_s = (prev == (unsigned)n_splits - 1u) ? 1u : 0u;
   }
   __syncthreads();
-  if (!last_flag) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // drop stale lines of this L2 once
+  if (!last_s) return;
 
+  // (a) T_V rows 4 j4 .. 4 j4 + 3 at columns CW cb .. CW cb + CW - 1 per thread, in
+  //     flight together with the partials.
   const HeadParams* hv = head_params(params_v, kvh);
-  const Partial* all = partials + kv_row * n_splits * G;
-  float* osum = lds;                                       // [G][kD]
-  v4f* part4 = reinterpret_cast<v4f*>(osum + G * kD);      // [kDecThreads]
-  float* ored = reinterpret_cast<float*>(part4 + kDecThreads);  // [8][G][kD]
-  // (a) T_V rows 4 j4 .. 4 j4 + 3, columns 16 cq .. 16 cq + 15: 16 vector loads per
-  //     thread, issued before the partials are read.
-  const int j4 = tid & 31, cq = tid >> 5;
-  v4f tr[4][4];
+  const int j4 = tid & 31, cb = tid >> 5;
+  v4f tv[4][CW / 4];
 #pragma unroll
   for (int jj = 0; jj < 4; ++jj)
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
-      tr[jj][k] = reinterpret_cast<const v4f*>(hv->T)[(4 * j4 + jj) * (kD / 4) + 4 * cq + k];
-  // (b) global max and normalizer per head
-  if (tid < G) {
-    float m = -INFINITY;
-    for (int s = 0; s < n_splits; ++s) m = fmaxf(m, all[s * G + tid].m);
-    float l = 0.f;
-    for (int s = 0; s < n_splits; ++s) {
-      const float ms = all[s * G + tid].m;
-      l += (ms == -INFINITY) ? 0.f : exp2f(ms - m) * all[s * G + tid].l;
-    }
-    mm[tid] = m;
-    ll[tid] = l;
-  }
-  __syncthreads();
-  // (c) o~ = sum_s 2^(m_s - m) o~_s / l over float4 columns; the splits are strided
-  // over thread groups when the columns do not fill the workgroup.
+    for (int k = 0; k < CW / 4; ++k)
+      tv[jj][k] = reinterpret_cast<const v4f*>(hv->T)[(4 * j4 + jj) * (kD / 4) + (CW / 4) * cb + k];
+
+  float* cm = lds;                                         // [NTHR] group maxima
+  float* cl = cm + NTHR;                                   // [NTHR] group sums
+  v4f* cacc = reinterpret_cast<v4f*>(cl + NTHR);           // [NTHR]
+  float* osum = reinterpret_cast<float*>(cacc + NTHR);     // [G][kD]
+  float* ored = osum + G * kD;                             // [NCB][G][kD]
+  const __amdgpu_buffer_rsrc_t prs =
+      make_rsrc(partials + row * n_splits * G, (uint32_t)(n_splits * G * sizeof(Partial)));
+
+  // (b) Online merge over the splits: slot (head, float4 column) per thread; groups of
+  //     threads take interleaved splits and combine at the end.
   const int slots = G * (kD / 4);
-  for (int base = 0; base < slots; base += kDecThreads) {
-    const int width = min(slots - base, kDecThreads);
-    const int ngroups = kDecThreads / width;
+  for (int base = 0; base < slots; base += NTHR) {
+    const int width = min(slots - base, NTHR);
+    const int ngroups = NTHR / width;
     const int slot = base + tid % width, grp = tid / width;
+    const int h = slot >> 5, c4 = slot & 31;
+    float M = -INFINITY, Ls = 0.f;
+    v4f acc = {0.f, 0.f, 0.f, 0.f};
+    bool bad = false;
     if (grp < ngroups) {
-      const int h = slot / (kD / 4), c4 = slot % (kD / 4);
-      const float m = mm[h];
-      v4f acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 16
-      for (int s = grp; s < n_splits; s += ngroups) {
-        const float ms = all[s * G + h].m;
-        const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - m);
-        acc += w * reinterpret_cast<const v4f*>(all[s * G + h].o)[c4];
+      for (int s0 = grp; s0 < n_splits; s0 += kMergeU * ngroups) {
+        v2f hd[kMergeU];
+        v4f ov[kMergeU];
+#pragma unroll
+        for (int u = 0; u < kMergeU; ++u) {        // past the last split the loads read 0
+          const uint32_t off = (uint32_t)(((s0 + u * ngroups) * G + h) * sizeof(Partial));
+          hd[u] = buf_load8_coherent(prs, off);
+          ov[u] = (v4f)__builtin_amdgcn_raw_buffer_load_b128(prs, (int)(off + 16 + 16 * c4), 0,
+                                                            kCoherent);
+        }
+#pragma unroll
+        for (int u = 0; u < kMergeU; ++u) {
+          const float ms = (s0 + u * ngroups < n_splits) ? hd[u].x : -INFINITY;
+          bad |= (ms != ms);
+          if (ms > -INFINITY) {
+            const float mn = fmaxf(M, ms);
+            const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
+            acc = acc * sa + ov[u] * sb;
+            Ls = Ls * sa + hd[u].y * sb;
+            M = mn;
+          }
+        }
       }
-      part4[tid] = acc;
     }
+    cm[tid] = bad ? NAN : M;
+    cl[tid] = Ls;
+    cacc[tid] = acc;
     __syncthreads();
     if (tid < width) {
-      const int h = (base + tid) / (kD / 4), c4 = (base + tid) % (kD / 4);
-      v4f acc = part4[tid];
-      for (int g = 1; g < ngroups; ++g) acc += part4[g * width + tid];
-      const float inv_l = ll[h] > 0.f ? 1.f / ll[h] : 0.f;
+      M = cm[tid];
+      Ls = cl[tid];
+      acc = cacc[tid];
+      bad = M != M;
+      for (int q = 1; q < ngroups; ++q) {
+        const float ms = cm[q * width + tid];
+        bad |= (ms != ms);
+        if (ms > -INFINITY) {
+          const float mn = fmaxf(M, ms);
+          const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
+          acc = acc * sa + cacc[q * width + tid] * sb;
+          Ls = Ls * sa + cl[q * width + tid] * sb;
+          M = mn;
+        }
+      }
+      const float inv_l = bad ? NAN : (Ls > 0.f ? 1.f / Ls : 0.f);
       reinterpret_cast<v4f*>(osum)[h * (kD / 4) + c4] = acc * inv_l;
     }
     __syncthreads();
   }
-  // (d) o_j = sum_c T_V[j][c] o~_c: partial sums over this thread's 16 columns, then
-  //     over the 8 column blocks.
+  // (c) o_j = sum_c T_V[j][c] o~_c: partial sums over this thread's columns, then over
+  //     the column blocks.
   for (int h = 0; h < G; ++h) {
-    const v4f* oh = reinterpret_cast<const v4f*>(osum + h * kD) + 4 * cq;
-    const v4f o0 = oh[0], o1 = oh[1], o2 = oh[2], o3 = oh[3];
+    const v4f* oh = reinterpret_cast<const v4f*>(osum + h * kD) + (CW / 4) * cb;
+    v4f ov4[CW / 4];
+#pragma unroll
+    for (int k = 0; k < CW / 4; ++k) ov4[k] = oh[k];
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-      const v4f p = tr[jj][0] * o0 + tr[jj][1] * o1 + tr[jj][2] * o2 + tr[jj][3] * o3;
-      ored[(cq * G + h) * kD + 4 * j4 + jj] = p.x + p.y + p.z + p.w;
+      v4f p = tv[jj][0] * ov4[0];
+#pragma unroll
+      for (int k = 1; k < CW / 4; ++k) p += tv[jj][k] * ov4[k];
+      ored[(cb * G + h) * kD + 4 * j4 + jj] = p.x + p.y + p.z + p.w;
     }
   }
   __syncthreads();
-  for (int i = tid; i < G * kD; i += kDecThreads) {
+  for (int i = tid; i < G * kD; i += NTHR) {
     const int h = i / kD, j = i % kD;
     float acc = 0.f;
 #pragma unroll
-    for (int b = 0; b < 8; ++b) acc += ored[(b * G + h) * kD + j];
-    out[((int64_t)seq * n_q_heads + kvh * G + h) * kD + j] = acc;
+    for (int b = 0; b < NCB; ++b) acc += ored[(b * G + h) * kD + j];
+    out_rows[(int64_t)h * kD + j] = acc;
   }
-  if (tid == 0) {
-    counters[kv_row] = 0u;
-    flags[kv_row] = 0u;
-  }
+  if (tid == 0) counters[row] = 0u;
 }
 
 // ---------------------------------------------------------------------------------------
 // Generic VALU kernel (any G <= 16, any budget).
 // ---------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
+__global__ __launch_bounds__(kThreads) void decode_split_kernel(
     const void* __restrict__ params_k, const void* __restrict__ params_v, int n_q_heads,
     int n_kv_heads, const void* __restrict__ q, int q_dtype,
     const uint8_t* __restrict__ k_codes, const uint16_t* __restrict__ k_alpha,
     const uint8_t* __restrict__ v_codes, const uint16_t* __restrict__ v_alpha,
     const int32_t* __restrict__ seq_len, int64_t cap, float scale, float* __restrict__ out,
-    unsigned* __restrict__ counters, unsigned* __restrict__ flags,
-    Partial* __restrict__ partials, int n_splits, int rk, int rv) {
+    unsigned* __restrict__ counters, Partial* __restrict__ partials, int n_splits, int rk,
+    int rv) {
   extern __shared__ float dyn[];
   __shared__ float qs[kMaxGroup][kD];
   __shared__ float qp[kMaxGroup][kD];
-  __shared__ float cterm[kMaxGroup];
-  __shared__ float red[kDecThreads / 64];
-  __shared__ float mh[kMaxGroup], lh[kMaxGroup], pah[kMaxGroup];
+  __shared__ float red[kThreads / 64];
+  __shared__ float mh[kMaxGroup], lh[kMaxGroup];
 
   const int split = blockIdx.x, kvh = blockIdx.y, seq = blockIdx.z;
   const int G = n_q_heads / n_kv_heads;
@@ -244,10 +350,10 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
   const int nt = layout_ok ? max(0, min(kSplit, len - t0)) : 0;
 
   // Queries of the group, then q'_c = (T_K^T q)_c * s_c * 2^(1-b_c) * scale * log2(e).
-  for (int i = tid; i < G * kD; i += kDecThreads)
+  for (int i = tid; i < G * kD; i += kThreads)
     qs[i / kD][i % kD] = load_q(q, q_dtype, ((int64_t)seq * n_q_heads + kvh * G) * kD + i);
   __syncthreads();
-  for (int i = tid; i < G * kD; i += kDecThreads) {
+  for (int i = tid; i < G * kD; i += kThreads) {
     const int h = i / kD, c = i % kD;
     float acc = 0.f;
 #pragma unroll 16
@@ -256,21 +362,18 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
     qp[h][c] = b ? acc * hk->s[c] * ldexpf(1.f, 1 - b) * scale * kLog2e : 0.f;
   }
   __syncthreads();
-  if (tid < G) {
-    float acc = 0.f;
-    for (int c = 0; c < kD; ++c)
-      if (hk->bits[c]) acc += qp[tid][c] * ldexpf(1.f, hk->bits[c] - 1);
-    cterm[tid] = acc;
-  }
-  for (int i = tid; i < G * bk; i += kDecThreads) {
+  // Weight of record bit v: q'_c 2^k, negated for the sign bit k = b_c - 1.
+  for (int i = tid; i < G * bk; i += kThreads) {
     const int h = i / bk, v = i % bk;
-    vq[h * kMaxBudget + v] = ldexpf(qp[h][hk->virt_chan[v]], hk->virt_bit[v]);
+    const int c = hk->virt_chan[v], k = hk->virt_bit[v];
+    const float w = ldexpf(qp[h][c], k);
+    vq[h * kMaxBudget + v] = (k == hk->bits[c] - 1) ? -w : w;
   }
   __syncthreads();
 
-  // Scores z = alpha^K (sum_v Q_v bit_v - C) in the log2 domain.
+  // Scores z = alpha^K sum_v Q_v bit_v in the log2 domain.
   const int64_t kv_row = (int64_t)seq * n_kv_heads + kvh;
-  for (int tl = tid; tl < kSplit; tl += kDecThreads) {
+  for (int tl = tid; tl < kSplit; tl += kThreads) {
     float acc[kMaxGroup];
 #pragma unroll
     for (int h = 0; h < kMaxGroup; ++h) acc[h] = 0.f;
@@ -290,7 +393,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
       const float ak = half_bits_to_float(k_alpha[kv_row * cap + t]);
 #pragma unroll
       for (int h = 0; h < kMaxGroup; ++h)
-        if (h < G) sc[h * kSplit + tl] = ak * (acc[h] - cterm[h]);
+        if (h < G) sc[h * kSplit + tl] = ak * acc[h];
     } else {
       for (int h = 0; h < G; ++h) sc[h * kSplit + tl] = -INFINITY;
     }
@@ -300,22 +403,19 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
   // Split-local softmax statistics per head; weights become 2^(z - m) * alpha^V.
   for (int h = 0; h < G; ++h) {
     float m = -INFINITY;
-    for (int tl = tid; tl < kSplit; tl += kDecThreads) m = fmaxf(m, sc[h * kSplit + tl]);
+    for (int tl = tid; tl < kSplit; tl += kThreads) m = fmaxf(m, sc[h * kSplit + tl]);
     m = block_reduce(m, true, red);
-    float l = 0.f, pa = 0.f;
-    for (int tl = tid; tl < kSplit; tl += kDecThreads) {
+    float l = 0.f;
+    for (int tl = tid; tl < kSplit; tl += kThreads) {
       float p = (tl < nt) ? exp2f(sc[h * kSplit + tl] - m) : 0.f;
       float w = (tl < nt) ? p * half_bits_to_float(v_alpha[kv_row * cap + t0 + tl]) : 0.f;
       sc[h * kSplit + tl] = w;
       l += p;
-      pa += w;
     }
     l = block_reduce(l, false, red);
-    pa = block_reduce(pa, false, red);
     if (tid == 0) {
       mh[h] = m;
       lh[h] = l;
-      pah[h] = pa;
     }
   }
   __syncthreads();
@@ -323,7 +423,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
   // Value bits: sum over tokens of w_t * bit_v(t), one thread per record bit.
   const uint32_t* vt = reinterpret_cast<const uint32_t*>(v_codes) +
                        (kv_row * (cap / kTile) + t0 / kTile) * (16 * rv);
-  for (int v = tid; v < bv; v += kDecThreads) {
+  for (int v = tid; v < bv; v += kThreads) {
     float acc[kMaxGroup];
 #pragma unroll
     for (int h = 0; h < kMaxGroup; ++h) acc[h] = 0.f;
@@ -348,16 +448,19 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
   }
   __syncthreads();
 
-  // Partial o~_c = s_c 2^(1-b_c) (sum_k 2^k S_(c,k) - 2^(b_c-1) sum_t w_t).
+  // Partial o~_c = s_c 2^(1-b_c) (sum_{k < b-1} 2^k S_(c,k) - 2^(b-1) S_(c,b-1)).
   Partial* part = partials + (kv_row * n_splits + split) * G;
-  for (int i = tid; i < G * kD; i += kDecThreads) {
+  for (int i = tid; i < G * kD; i += kThreads) {
     const int h = i / kD, c = i % kD;
     const int b = hv->bits[c];
     float o = 0.f;
     if (b && nt > 0) {
       float acc = 0.f;
-      for (int k = 0; k < b; ++k) acc += ldexpf(vq[h * kMaxBudget + hv->bit_off[c] + k], k);
-      o = hv->s[c] * ldexpf(1.f, 1 - b) * (acc - ldexpf(pah[h], b - 1));
+      for (int k = 0; k < b; ++k) {
+        const float t = ldexpf(vq[h * kMaxBudget + hv->bit_off[c] + k], k);
+        acc += (k == b - 1) ? -t : t;
+      }
+      o = hv->s[c] * ldexpf(acc, 1 - b);
     }
     st_dev(&part[h].o[c], o);
   }
@@ -365,314 +468,279 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
     st_dev(&part[tid].m, !layout_ok ? NAN : (nt > 0) ? mh[tid] : -INFINITY);
     st_dev(&part[tid].l, !layout_ok ? NAN : (nt > 0) ? lh[tid] : 0.f);
   }
-  merge_if_last(params_v, n_q_heads, kvh, seq, kv_row, G, out, counters, flags, partials,
-                n_splits, dyn);
+  merge_if_last<kThreads>(params_v, kvh, kv_row, G, n_splits, partials, counters,
+                          out + ((int64_t)seq * n_q_heads + kvh * G) * kD, dyn);
 }
 
 // ---------------------------------------------------------------------------------------
-// MFMA decode kernel (G <= 8 query heads per KV head, record budgets <= 512 bits).
+// MFMA decode kernel (G <= 8 query heads per KV head, records of at most 64 bytes).
 //
-// Both contractions run on v_mfma_i32_16x16x64_i8 over the bits of the codes: a code
-// u_c = sum_k 2^k bit_k, so every record bit is a virtual channel whose weight is the
-// channel's weight times 2^k.
+// Both contractions run on v_mfma_i32_16x16x64_i8 over the bits of the codes.
 //  * Keys: D[token, (head, limb)] = sum_bits bit(token) * Qlimb[bit, (head, limb)].
 //    One record dword w (32 bits of one token) expands to MFMA bytes by
 //    r_d = w & (0x01010101 << d): byte j of r_d is 2^d * bit (8j + d).  The factor 2^d
 //    (and the sign of int8 0x80 for d = 7) is folded into the query weights, which are
 //    32-bit fixed point split into four int8 limbs: four heads times four limbs fill
 //    the 16 MFMA columns.  Lane (column (h, L), row group g) of the result holds limb L
-//    of the scores of tokens 4g .. 4g + 3; a DPP sum over the lane quad recombines the
-//    limbs.
+//    of the scores of tokens 4g .. 4g + 3; a reduce-scatter over the lane quad leaves
+//    lane L with the full score of token 4g + L.
 //  * Values: D[bit, (head, limb)] = sum_tokens bit(token) * Plimb[token, (head, limb)]
-//    with P = 2^(z - m) alpha^V in 32-bit fixed point.  The value tiles store the bit of
-//    token 16 d + 4 g + i at bit 8 i + 2 g + d % 2 of word d / 2, so a lane of row
-//    group g expands its two words with two masks into exactly the tokens whose
-//    scores it computed: each lane's softmax weights are its own MFMA operand.
-// The four waves of a workgroup work on disjoint quarters of the split and meet once,
-// to combine their (m, l, o~) into the workgroup partial.  Integer accumulation is
-// exact; limbs are recombined in fp32.
+//    with P = 2^(z - m) alpha^V in 32-bit fixed point (one exponent per workgroup).
+//    The value tiles store the bit of token 16 d + 4 g + i at bit 8 i + 2 g + d % 2 of
+//    word d / 2, so a lane of row group g expands its two words with two masks into
+//    exactly the tokens whose scores its quad computed; a byte transpose inside the quad
+//    turns (one token, four limbs) per lane into (four tokens, one limb).
+// Each wave scores and weights its own share of the split; the value bits are then
+// split across the waves, over all tokens of the split.  Integer accumulation is exact;
+// limbs are recombined in fp32.
 //
-// The query bit weights of a (sequence, KV head) are computed once, by the workgroup
-// of split 0, and published in the workspace; the other splits poll a flag a bounded
-// number of times while their cache loads are in flight, and compute the weights
-// themselves if the flag does not appear.
+// Every workgroup derives its query bit weights itself, while its cache loads are in
+// flight: q~ = T_K^T q (fp32), then per bit the 32-bit fixed-point limbs.
 // ---------------------------------------------------------------------------------------
-constexpr int kMaxLoads = 6;     // 16-byte loads per thread per cache region
+template <int NT, int NTILE, int NP, int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const DecodeArgs a) {
+  constexpr int NTHR = 64 * NW;       // threads per workgroup
+  constexpr int NH = 4 * NT;          // head slots: 4 per column tile
+  constexpr int TW = 16 * NTILE;      // tokens per wave
+  constexpr int S = NW * TW;          // tokens per workgroup
+  constexpr int NCH = S / 64;         // 64-token chunks per workgroup
+  constexpr int CPW = NTILE / 4;      // chunks per wave
+  constexpr int NLD = S * 64 / 16 / NTHR;   // 16-byte loads per thread per cache (64-byte records)
+  constexpr int NJQ = NTHR / 32;      // row blocks of the query transform
+  constexpr int RJ = kD / NJQ;        // rows per block
+  constexpr int AL = S / 8;           // 16-byte loads of one alpha array (one per thread)
+  constexpr int NR = NH * kD / NTHR;  // (head, channel) items per thread
+  constexpr int NPI = (NH * 4 * NP * 8 + NTHR - 1) / NTHR;   // plane items per thread
+  static_assert(NTILE % 4 == 0, "a wave owns whole 64-token chunks");
+  static_assert(AL <= NTHR && NR >= 1, "thread mapping");
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ unsigned qmx[NH];
+  __shared__ int fexp_s[NH];
+  __shared__ float wmax[NW][NH], wsum[NW][NH], wav[NW];
 
-__device__ inline v4i mfma_i8(v4i a, v4i b, v4i c) {
-  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
-}
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 15, g = lane >> 4, hc = n >> 2, L = n & 3;
+  // XCD-aware order: workgroups are dealt to the 8 XCDs round robin, so consecutive
+  // splits of a (sequence, KV head) are given block ids that land on one XCD.
+  const int lb = (int)(blockIdx.x & 7) * (int)(gridDim.x >> 3) + (int)(blockIdx.x >> 3);
+  if (lb >= a.n_blocks) return;
+  const int64_t row = lb / a.n_splits;
+  const int split = lb % a.n_splits;
+  const int seq = (int)(row / a.n_kv_heads), kvh = (int)(row % a.n_kv_heads);
+  const int G = a.G, RK = a.rk, RV = a.rv;
+  const int RWK = RK >> 2;
+  const HeadParams* hk = head_params(a.params_k, kvh);
+  const HeadParams* hv = head_params(a.params_v, kvh);
+  const int t0 = split * S;
 
-// Four balanced int8 limbs of a 32-bit value |x| < 2^30, packed in one dword (limb L in
-// byte L, two's complement): x = sum_L limb_L 256^L.
-__device__ inline uint32_t pack_limbs(int x) {
-  return ((uint32_t)x + 0x80808080u) ^ 0x80808080u;
-}
-
-// Sum over the lane quad (lanes 4k .. 4k + 3); every lane of the quad gets the sum.
-__device__ inline float quad_sum(float v) {
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
-  return v;
-}
-
-// Query bit weights in MFMA operand order (limb planes), their offsets C and exponents,
-// into LDS.  scratch: >= 8 * NH * kD floats of LDS not otherwise in use.
-template <int NH>
-__device__ void query_planes(const HeadParams* hk, const void* q, int q_dtype, int64_t qbase,
-                             int G, float scale, int BK, int NP, float* scratch, uint8_t* ql,
-                             int (*cofs)[4], int* fexp) {
-  __shared__ float qs[NH][kD];
-  __shared__ float qp[NH][kD];
-  __shared__ unsigned qmax_bits[NH];
-  __shared__ uint8_t tbits[kD];
-  __shared__ float tscale[kD];
-  __shared__ uint8_t vchan[kMaxBudget / 2], vbit[kMaxBudget / 2];
-  const int tid = threadIdx.x;
-  const int c4 = tid & 31, jq = tid >> 5;
-  // One round of loads: T rows 16 jq .. 16 jq + 15 (columns 4 c4 ..), q, small tables.
-  v4f tr[16];
-  const v4f* t4 = reinterpret_cast<const v4f*>(hk->T);
+  // (0) Loads that need nothing: T_K rows RJ jq .. RJ jq + RJ - 1 at columns 4 c4 .. + 3,
+  //     the channel tables, the queries.
+  const int c4 = tid & 31, jq = tid >> 5, cq = tid & (kD - 1);
+  v4f tr[RJ];
 #pragma unroll
-  for (int jj = 0; jj < 16; ++jj) tr[jj] = t4[(16 * jq + jj) * (kD / 4) + c4];
-  for (int i = tid; i < NH * kD; i += kDecThreads) {
-    const int h = i / kD;
-    qs[h][i % kD] = (h < G) ? load_q(q, q_dtype, qbase + i) : 0.f;
+  for (int jj = 0; jj < RJ; ++jj)
+    tr[jj] = reinterpret_cast<const v4f*>(hk->T)[(RJ * jq + jj) * (kD / 4) + c4];
+  const int kb = hk->bits[cq], koff = hk->bit_off[cq];
+  const float ks = hk->s[cq];
+  const int vbc = hv->bits[cq], voc = hv->bit_off[cq];
+  const float vsc = hv->s[cq];
+  // Plane items (head, record dword D, bit d of each byte): the 4 record bits 32 D +
+  // 8 j + d, j = 0..3, of one head.
+  // (Every load here is unconditional, with clamped indices: the wait counters then stay
+  // exact, and waiting for these does not wait for the cache loads issued after them.)
+  uint2 desc[NPI];
+#pragma unroll
+  for (int r = 0; r < NPI; ++r) {
+    const int dd = (r * NTHR + tid) % (8 * RWK);                 // < 128: in the table
+    desc[r] = reinterpret_cast<const uint2*>(hk->bit_desc)[dd];
   }
-  for (int i = tid; i < BK; i += kDecThreads) {
-    vchan[i] = hk->virt_chan[i];
-    vbit[i] = hk->virt_bit[i];
+  // Queries, element r NTHR + tid, read as the aligned dword that holds the element
+  // (either type, no branch; the dword never leaves the element's page).
+  typedef const __attribute__((address_space(1))) uint32_t* gdword;
+  const bool q_bf = a.q_dtype == AATC_BF16;
+  uint32_t qraw[NR];
+  bool qhi[NR];
+  {
+    const int64_t qb = ((int64_t)seq * a.n_q_heads + kvh * G) * kD;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const int64_t i = qb + min(r * NTHR + tid, G * kD - 1);
+      const uintptr_t ad = reinterpret_cast<uintptr_t>(a.q) + (q_bf ? 2 * i : 4 * i);
+      qraw[r] = *reinterpret_cast<gdword>(ad & ~(uintptr_t)3);
+      qhi[r] = (ad & 2) != 0;
+    }
   }
-  if (tid < kD) {
-    tbits[tid] = hk->bits[tid];
-    tscale[tid] = hk->s[tid];
+  if (tid < NH) qmx[tid] = 0u;
+
+  Partial* parts = a.partials + row * a.n_splits * G;
+  float* out_rows = a.out + ((int64_t)seq * a.n_q_heads + kvh * G) * kD;
+  const int len = (int)min<int64_t>(max(a.seq_len[seq], 0), a.cap);
+  const int nt = max(0, min(S, len - t0));
+
+  // (1) This split's packed cache, into registers (loads past the capacity read 0).  The
+  //     layout check below gates the compute, not these loads.
+  const int n_load = min(S, (nt + kTile - 1) / kTile * kTile);
+  const int nk16 = n_load * RK / 16, nv16 = n_load * RV / 16, na16 = n_load / 8;
+  const __amdgpu_buffer_rsrc_t krs = make_rsrc(a.k_codes + row * a.cap * RK, (uint32_t)(a.cap * RK));
+  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(a.v_codes + row * a.cap * RV, (uint32_t)(a.cap * RV));
+  // Loads a thread does not need get an offset past the descriptor (they return 0).
+  constexpr uint32_t kNone = 0x80000000u;
+  v4i rk[NLD], rv[NLD], rak, rav;
+#pragma unroll
+  for (int i = 0; i < NLD; ++i) {
+    const int idx = tid + i * NTHR;
+    rk[i] = buf_load16<0>(krs, idx < nk16 ? (uint32_t)(t0 * RK + 16 * idx) : kNone);
   }
-  for (int i = tid; i < 4 * NH * 2 * NP * 64 / 4; i += kDecThreads)
-    reinterpret_cast<uint32_t*>(ql)[i] = 0u;
-  if (tid < NH) qmax_bits[tid] = 0u;
-  if (tid < NH * 4) cofs[tid / 4][tid % 4] = 0;
-  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < NLD; ++i) {
+    const int idx = tid + i * NTHR;
+    rv[i] = buf_load16<0>(vrs, idx < nv16 ? (uint32_t)(t0 * RV + 16 * idx) : kNone);
+  }
+  {
+    const uint32_t aoff = (tid < na16) ? (uint32_t)(2 * t0 + 16 * tid) : kNone;
+    rak = buf_load16<0>(make_rsrc(a.k_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
+    rav = buf_load16<0>(make_rsrc(a.v_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
+  }
+  // Keep the compiler from moving work that waits on the early loads above the cache loads.
+  __builtin_amdgcn_sched_barrier(0);
+  // No branch on the split's contents: an empty split computes on masked tokens and
+  // stores (m, l, o~) = (-inf, 0, 0); records that do not match the parameters store a
+  // NaN maximum (the value budget is clamped to the record so LDS accesses stay in range).
+  const bool layout_ok = (hk->record_bytes == RK) & (hv->record_bytes == RV);
+  const __amdgpu_buffer_rsrc_t prs =
+      make_rsrc(parts, (uint32_t)(a.n_splits * G * sizeof(Partial)));
+  // Only now wait for the queries (issued before the cache, so the cache stays in flight).
+  float* qs = reinterpret_cast<float*>(smem) + NJQ * NH * kD;     // [NH][kD]
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const uint32_t w = qraw[r];
+    const float qv = q_bf ? __uint_as_float((qhi[r] ? (w >> 16) : (w & 0xffffu)) << 16)
+                          : __uint_as_float(w);
+    qs[r * NTHR + tid] = ((r * NTHR + tid) / kD < G) ? qv : 0.f;
+  }
+  __syncthreads();                                   // qs, qmx
+
+  // (2) q~ = T_K^T q: RJ-row partial sums per thread, then over the NJQ row blocks.
+  float* scr = reinterpret_cast<float*>(smem);       // [NJQ][NH][kD]
   {
     v4f acc[NH];
 #pragma unroll
     for (int h = 0; h < NH; ++h) acc[h] = (v4f){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int jj = 0; jj < 16; ++jj)
+    for (int jj = 0; jj < RJ; jj += 4)
 #pragma unroll
-      for (int h = 0; h < NH; ++h) acc[h] += tr[jj] * qs[h][16 * jq + jj];
+      for (int h = 0; h < NH; ++h) {
+        const v4f qv = *reinterpret_cast<const v4f*>(qs + h * kD + RJ * jq + jj);
+        acc[h] += tr[jj] * qv.x + tr[jj + 1] * qv.y + tr[jj + 2] * qv.z + tr[jj + 3] * qv.w;
+      }
 #pragma unroll
-    for (int h = 0; h < NH; ++h)
-      reinterpret_cast<v4f*>(scratch)[(jq * NH + h) * (kD / 4) + c4] = acc[h];
+    for (int h = 0; h < NH; ++h) reinterpret_cast<v4f*>(scr)[(jq * NH + h) * (kD / 4) + c4] = acc[h];
   }
   __syncthreads();
-  for (int i = tid; i < NH * kD; i += kDecThreads) {
-    const int h = i / kD, c = i % kD;
-    float acc = 0.f;
+  // Channel weight Q_c = q~_c s_c scale log2(e) (the weight of the code's sign bit up to
+  // sign), kept in LDS; the largest |Q_c| of a head sets its fixed-point exponent.
+  float* qcl = qs;                                   // [NH][kD], over the consumed queries
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc += scratch[(j * NH + h) * kD + c];
-    const int b = tbits[c];
-    float qv = 0.f;
-    if (h < G && b) {
-      qv = acc * tscale[c] * ldexpf(1.f, 1 - b) * scale * kLog2e;
-      atomicMax(&qmax_bits[h], __float_as_uint(ldexpf(fabsf(qv), b - 1)));
-    }
-    qp[h][c] = qv;
+  for (int r = 0; r < NR; ++r) {
+    const int h = (r * NTHR + tid) / kD;
+    float qq = 0.f;
+#pragma unroll
+    for (int j = 0; j < NJQ; ++j) qq += scr[(j * NH + h) * kD + cq];
+    const float qc = (h < G && kb > 0) ? qq * ks * a.scale_log2e : 0.f;
+    qcl[h * kD + cq] = qc;
+    const float m = wave_max(fabsf(qc));
+    if (lane == 0) atomicMax(&qmx[h], __float_as_uint(m));
   }
   __syncthreads();
   if (tid < NH) {
     int e = 0;
-    frexpf(__uint_as_float(qmax_bits[tid]), &e);
-    fexp[tid] = qmax_bits[tid] ? 30 - e : 0;
+    frexpf(__uint_as_float(qmx[tid]), &e);
+    fexp_s[tid] = qmx[tid] ? 30 - e : 0;
   }
-  __syncthreads();
-  // Record bit v = 32 D + 8 j + d  ->  K-step 2 (D / 4) + d / 4, lane group D % 4,
-  // byte 4 (d % 4) + j.  Weight 2^(k - d) q'_c, negated for d = 7 (int8 0x80 = -128).
-  for (int i = tid; i < NH * BK; i += kDecThreads) {
-    const int h = i / BK, v = i % BK;
-    if (h >= G) continue;
-    const int c = vchan[v], k = vbit[v];
-    const int D = v >> 5, p = v & 31, j = p >> 3, d = p & 7;
-    int fx = (int)rintf(ldexpf(qp[h][c], k - d + fexp[h]));
-    if (d == 7) fx = -fx;
-    const uint32_t limbs = pack_limbs(fx);
-    const int s = 2 * (D >> 2) + (d >> 2);
-    const int pos = ((D & 3) << 4) + ((d & 3) << 2) + j;
+  // Record bit v = 32 D + 8 j + d  ->  K-step 2 (D % NP) + d / 4, lane group D / NP,
+  // byte 4 (d % 4) + j of the 16-byte operand; dwords RWK .. 4 NP - 1 get weight 0.  Weight 2^(k + 1 - b) Q_c / 2^d, negated
+  // for the sign bit and for d = 7 (int8 0x80 = -128); the four limbs of the four bits
+  // j = 0..3 are transposed into one dword per limb plane.
+  uint8_t* ql = smem + a.off_ql;                     // [4][NH][2 NP][64]
+  for (int i = tid; i < 4 * NH * 2 * 4 * (4 * NP - RWK); i += NTHR) {
+    const int D = RWK + i / (4 * NH * 2 * 4), rest = i % (4 * NH * 2 * 4);
+    const int plane = rest / 8, st = 2 * (D % NP) + ((rest >> 2) & 1);
+    *reinterpret_cast<uint32_t*>(ql + (plane * 2 * NP + st) * 64 + ((D / NP) << 4) +
+                                 4 * (rest & 3)) = 0u;
+  }
 #pragma unroll
-    for (int L = 0; L < 4; ++L)
-      ql[((L * NH + h) * 2 * NP + s) * 64 + pos] = (uint8_t)(limbs >> (8 * L));
-    if (k == tbits[c] - 1) {                    // offset C = sum_c Q(c, msb)
-      const int bv = (d == 7) ? -128 : (1 << d);
+  for (int r = 0; r < NPI; ++r) {
+    const int i = r * NTHR + tid;
+    const int h = i / (8 * RWK), dd = i % (8 * RWK), D = dd >> 3, d = dd & 7;
+    if (h < G) {
+      int e = 0;
+      const unsigned qm = qmx[h];
+      frexpf(__uint_as_float(qm), &e);
+      const int fe = qm ? 30 - e : 0;
+      uint32_t x[4];
 #pragma unroll
-      for (int L = 0; L < 4; ++L)
-        atomicAdd(&cofs[h][L], (int)(int8_t)(limbs >> (8 * L)) * bv);
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t ent = ((j < 2 ? desc[r].x : desc[r].y) >> (16 * (j & 1))) & 0xffffu;
+        const float qv = qcl[h * kD + (ent & 127)];
+        int fx = (int)rintf(ldexpf(qv, (int)((ent >> 8) & 15) - 8 + fe - d));
+        if ((((ent >> 14) & 1) != 0) != (d == 7)) fx = -fx;
+        x[j] = (ent & 0x8000u) ? pack_limbs(fx) : 0u;
+      }
+      // x[j] = (limb 0..3 of bit j)  ->  y[L] = (limb L of bits 0..3)
+      const uint32_t t0 = __builtin_amdgcn_perm(x[1], x[0], 0x05010400u);
+      const uint32_t t1 = __builtin_amdgcn_perm(x[3], x[2], 0x05010400u);
+      const uint32_t t2 = __builtin_amdgcn_perm(x[1], x[0], 0x07030602u);
+      const uint32_t t3 = __builtin_amdgcn_perm(x[3], x[2], 0x07030602u);
+      const uint32_t y[4] = {__builtin_amdgcn_perm(t1, t0, 0x05040100u),
+                             __builtin_amdgcn_perm(t1, t0, 0x07060302u),
+                             __builtin_amdgcn_perm(t3, t2, 0x05040100u),
+                             __builtin_amdgcn_perm(t3, t2, 0x07060302u)};
+      const int st = 2 * (D % NP) + (d >> 2);
+      const int pos = ((D / NP) << 4) + ((d & 3) << 2);
+#pragma unroll
+      for (int l4 = 0; l4 < 4; ++l4)
+        *reinterpret_cast<uint32_t*>(ql + ((l4 * NH + h) * 2 * NP + st) * 64 + pos) = y[l4];
     }
   }
   __syncthreads();
-}
+  v4i bq[NT][2 * NP];
+  int fex[NT];
+#pragma unroll
+  for (int rt = 0; rt < NT; ++rt) {
+    const int h = 4 * rt + hc;
+#pragma unroll
+    for (int s = 0; s < 2 * NP; ++s)
+      bq[rt][s] = *reinterpret_cast<const v4i*>(ql + ((L * NH + h) * 2 * NP + s) * 64 + 16 * g);
+    fex[rt] = fexp_s[h];
+  }
 
-template <int NT, int S>
-__global__ __launch_bounds__(kDecThreads, 2) void decode_mfma_kernel(
-    const void* __restrict__ params_k, const void* __restrict__ params_v, int n_q_heads,
-    int n_kv_heads, const void* __restrict__ q, int q_dtype,
-    const uint8_t* __restrict__ k_codes, const uint16_t* __restrict__ k_alpha,
-    const uint8_t* __restrict__ v_codes, const uint16_t* __restrict__ v_alpha,
-    const int32_t* __restrict__ seq_len, int64_t cap, float scale, float* __restrict__ out,
-    unsigned* __restrict__ counters, unsigned* __restrict__ flags,
-    QPlanes* __restrict__ planes, Partial* __restrict__ partials, int n_splits, int RK, int RV,
-    int ob_base, int ob_wstride, int ql_base) {
-  constexpr int NH = 4 * NT;          // head slots: 4 per column tile
-  constexpr int TW = S / 4;           // tokens per wave
-  constexpr int NTILE = TW / 16;      // 16-token key tiles per wave
-  constexpr int NCH = TW / 64;        // 64-token value chunks per wave
-  constexpr int VTP = 16 / NT;        // value-bit tiles per pass
-  extern __shared__ __align__(16) uint8_t smem[];
-  __shared__ int cofs_s[NH][4];
-  __shared__ int fexp_s[NH];
-  __shared__ unsigned ready;
-  __shared__ float mw[4][NH], lw[4][NH];
-  __shared__ double paw[4][NH];
-  __shared__ float mfin[NH], lfin[NH], pafin[NH];
-
-  const int G = n_q_heads / n_kv_heads;
-  const int split = blockIdx.x, kvh = blockIdx.y, seq = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n = lane & 15, g = lane >> 4, hc = n >> 2, L = n & 3;
-  const HeadParams* hk = head_params(params_k, kvh);
-  const HeadParams* hv = head_params(params_v, kvh);
-  const int64_t kv_row = (int64_t)seq * n_kv_heads + kvh;
-  const int len = (int)min<int64_t>(max(seq_len[seq], 0), cap);
-  const int t0 = split * S;
-  const int nt = max(0, min(S, len - t0));
-  const int n_load = min(S, (nt + kTile - 1) / kTile * kTile);
-
-  // Dynamic LDS: key records | value tiles | alpha^K | alpha^V | [Q limb planes]
-  // [O' per wave, or inside each wave's own key records once they are consumed].
-  // The front (records + tiles) also serves as prologue and merge scratch.
+  // (3) Land the cache in LDS (over the query-transform scratch).
   uint8_t* kbuf = smem;
-  uint8_t* vbuf = kbuf + S * RK + 16;
-  uint16_t* akb = reinterpret_cast<uint16_t*>(vbuf + S * RV);
-  uint16_t* avb = akb + S;
-  uint8_t* ql = smem + ql_base;                                // [4][NH][2 NP][64]
-
-  Partial* part = partials + (kv_row * n_splits + split) * G;
-  const bool layout_ok = hk->record_bytes == RK && hv->record_bytes == RV;
-  if (nt == 0 || !layout_ok) {
-    for (int i = tid; i < G * kD; i += kDecThreads) st_dev(&part[i / kD].o[i % kD], 0.f);
-    if (tid < G) {
-      st_dev(&part[tid].m, layout_ok ? -INFINITY : NAN);
-      st_dev(&part[tid].l, layout_ok ? 0.f : NAN);
-    }
-    merge_if_last(params_v, n_q_heads, kvh, seq, kv_row, G, out, counters, flags, partials,
-                  n_splits, reinterpret_cast<float*>(smem));
-    return;
-  }
-  const int BK = hk->budget, BV = hv->budget;
-  const int RWK = RK / 4;
-  const int NP = (RWK + 3) / 4;
-  const int NVT = (BV + 15) / 16;
-
-  // (1) Issue the loads of this split's packed cache (kept in registers for now).
-  const v4i* gk = reinterpret_cast<const v4i*>(k_codes + (kv_row * cap + t0) * RK);
-  const v4i* gv = reinterpret_cast<const v4i*>(v_codes + (kv_row * cap + t0) * RV);
-  const int nk16 = n_load * RK / 16, nv16 = n_load * RV / 16, na16 = n_load * 2 / 16;
-  v4i rk[kMaxLoads], rv[kMaxLoads], ra = {0, 0, 0, 0};
+  uint8_t* vbuf = smem + a.off_v;
+  uint16_t* akb = reinterpret_cast<uint16_t*>(smem + a.off_ak);
+  uint16_t* avb = reinterpret_cast<uint16_t*>(smem + a.off_av);
 #pragma unroll
-  for (int i = 0; i < kMaxLoads; ++i) rk[i] = rv[i] = (v4i){0, 0, 0, 0};
-#pragma unroll
-  for (int i = 0; i < kMaxLoads; ++i) {
-    const int idx = tid + i * kDecThreads;
-    if (idx < nk16) rk[i] = gk[idx];
-  }
-#pragma unroll
-  for (int i = 0; i < kMaxLoads; ++i) {
-    const int idx = tid + i * kDecThreads;
-    if (idx < nv16) rv[i] = gv[idx];
-  }
-  {
-    const uint16_t* src = (tid < 64) ? k_alpha : v_alpha;
-    const int idx = tid & 63;
-    if (tid < 128 && idx < na16)
-      ra = reinterpret_cast<const v4i*>(src + kv_row * cap + t0)[idx];
-  }
-
-  // (2) Query operands (MFMA B for keys) while the loads are in flight.
-  v4i bq[NT][2 * kMaxPairs];
-  int cof[NT], fex[NT];
-  bool have = false;
-  QPlanes* qpl = planes + kv_row;
-  if (split != 0) {
-    if (tid == 0) {
-      unsigned ok = 0u;
-      for (int it = 0; it < kSpinLimit && !ok; ++it) {
-        ok = ld_dev(&flags[kv_row]);
-        if (!ok) __builtin_amdgcn_s_sleep(4);
-      }
-      ready = ok;
-    }
-    __syncthreads();
-    have = ready != 0u;
-    if (have) {
-#pragma unroll
-      for (int rt = 0; rt < NT; ++rt) {
-        const int h = 4 * rt + hc;
-#pragma unroll
-        for (int s = 0; s < 2 * kMaxPairs; ++s) {
-          if (s < 2 * NP) {
-            const unsigned* src = reinterpret_cast<const unsigned*>(
-                qpl->ql + ((L * NH + h) * 2 * NP + s) * 64 + g * 16);
-            bq[rt][s] = (v4i){(int)ld_dev(src), (int)ld_dev(src + 1), (int)ld_dev(src + 2),
-                              (int)ld_dev(src + 3)};
-          }
-        }
-        cof[rt] = (int)ld_dev(reinterpret_cast<const unsigned*>(&qpl->cofs[h][L]));
-        fex[rt] = (int)ld_dev(reinterpret_cast<const unsigned*>(&qpl->fexp[h]));
-      }
-    }
-  }
-  if (!have) {
-    query_planes<NH>(hk, q, q_dtype, ((int64_t)seq * n_q_heads + kvh * G) * kD, G, scale, BK,
-                     NP, reinterpret_cast<float*>(smem), ql, cofs_s, fexp_s);
-    if (split == 0) {
-      const int words = 4 * NH * 2 * NP * 64 / 4;
-      for (int i = tid; i < words; i += kDecThreads)
-        st_dev(reinterpret_cast<int*>(qpl->ql) + i, reinterpret_cast<const int*>(ql)[i]);
-      if (tid < NH * 4) st_dev(&qpl->cofs[tid / 4][tid % 4], cofs_s[tid / 4][tid % 4]);
-      if (tid < NH) st_dev(&qpl->fexp[tid], fexp_s[tid]);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      if (tid == 0)
-        __hip_atomic_store(&flags[kv_row], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-#pragma unroll
-    for (int rt = 0; rt < NT; ++rt) {
-      const int h = 4 * rt + hc;
-#pragma unroll
-      for (int s = 0; s < 2 * kMaxPairs; ++s)
-        if (s < 2 * NP)
-          bq[rt][s] = *reinterpret_cast<const v4i*>(ql + ((L * NH + h) * 2 * NP + s) * 64 + g * 16);
-      cof[rt] = cofs_s[h][L];
-      fex[rt] = fexp_s[h];
-    }
-    __syncthreads();                    // prologue scratch (the front) is reused below
-  }
-
-  // (3) Land the cache in LDS.
-#pragma unroll
-  for (int i = 0; i < kMaxLoads; ++i) {
-    const int idx = tid + i * kDecThreads;
+  for (int i = 0; i < NLD; ++i) {
+    const int idx = tid + i * NTHR;
     if (idx < nk16) reinterpret_cast<v4i*>(kbuf)[idx] = rk[i];
   }
 #pragma unroll
-  for (int i = 0; i < kMaxLoads; ++i) {
-    const int idx = tid + i * kDecThreads;
+  for (int i = 0; i < NLD; ++i) {
+    const int idx = tid + i * NTHR;
     if (idx < nv16) reinterpret_cast<v4i*>(vbuf)[idx] = rv[i];
   }
-  if (tid < 128 && (tid & 63) < na16) reinterpret_cast<v4i*>(tid < 64 ? akb : avb)[tid & 63] = ra;
+  if (tid < na16) {
+    reinterpret_cast<v4i*>(akb)[tid] = rak;
+    reinterpret_cast<v4i*>(avb)[tid] = rav;
+  }
   __syncthreads();
 
-  // (4) Key scores of this wave's tokens.
+  // (4) Key scores of this wave's tokens: lane L of a quad ends with token 4 g + L.
   const int wb = wave * TW;
-  float z[NTILE][NT][4];
+  const float lw = (float)(1 << (8 * L));            // weight of this lane's limb
+  float zr[NTILE][NT];
+  float avt[NTILE];
+  float amax = 0.f;
 #pragma unroll
   for (int tt = 0; tt < NTILE; ++tt) {
     const int tok0 = wb + 16 * tt;
@@ -680,197 +748,165 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_mfma_kernel(
     v4i acc[NT];
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) acc[rt] = (v4i){0, 0, 0, 0};
+    // Lane group g holds record dwords g NP .. g NP + NP - 1; dwords past the record
+    // (they belong to the next token) meet zero query weights.
+    uint32_t wd[NP];
 #pragma unroll
-    for (int P = 0; P < kMaxPairs; ++P) {
-      if (P < NP) {
-        const int D = 4 * P + g;
-        const uint32_t w = (D < RWK) ? *reinterpret_cast<const uint32_t*>(rec + 4 * D) : 0u;
-        const v4i a0 = {(int)(w & 0x01010101u), (int)(w & 0x02020202u),
-                        (int)(w & 0x04040404u), (int)(w & 0x08080808u)};
-        const v4i a1 = {(int)(w & 0x10101010u), (int)(w & 0x20202020u),
-                        (int)(w & 0x40404040u), (int)(w & 0x80808080u)};
+    for (int P = 0; P < NP; ++P) wd[P] = *reinterpret_cast<const uint32_t*>(rec + 4 * (g * NP + P));
 #pragma unroll
-        for (int rt = 0; rt < NT; ++rt) {
-          acc[rt] = mfma_i8(a0, bq[rt][2 * P], acc[rt]);
-          acc[rt] = mfma_i8(a1, bq[rt][2 * P + 1], acc[rt]);
-        }
+    for (int P = 0; P < NP; ++P) {
+      const uint32_t w = wd[P];
+      const v4i a0 = {(int)(w & 0x01010101u), (int)(w & 0x02020202u),
+                      (int)(w & 0x04040404u), (int)(w & 0x08080808u)};
+      const v4i a1 = {(int)(w & 0x10101010u), (int)(w & 0x20202020u),
+                      (int)(w & 0x40404040u), (int)(w & 0x80808080u)};
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) {
+        acc[rt] = mfma_i8(a0, bq[rt][2 * P], acc[rt]);
+        acc[rt] = mfma_i8(a1, bq[rt][2 * P + 1], acc[rt]);
       }
     }
-    const uint2 akw = *reinterpret_cast<const uint2*>(akb + tok0 + 4 * g);
-    const float ak[4] = {half_bits_to_float((uint16_t)(akw.x & 0xffff)),
-                         half_bits_to_float((uint16_t)(akw.x >> 16)),
-                         half_bits_to_float((uint16_t)(akw.y & 0xffff)),
-                         half_bits_to_float((uint16_t)(akw.y >> 16))};
+    const int tok = tok0 + 4 * g + L;
+    const bool tok_ok = tok < nt;
+    const float ak = half_bits_to_float(akb[tok]);
+    const float av = half_bits_to_float(avb[tok]);
+    avt[tt] = tok_ok ? av : 0.f;
+    amax = fmaxf(amax, fabsf(avt[tt]));
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) {
-      const bool head_ok = 4 * rt + hc < G;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float f = quad_sum(ldexpf((float)(acc[rt][i] - cof[rt]), 8 * L));
-        z[tt][rt][i] = (tok0 + 4 * g + i < nt && head_ok) ? ak[i] * ldexpf(f, -fex[rt])
-                                                          : -INFINITY;
-      }
+      const float x[4] = {(float)acc[rt][0] * lw, (float)acc[rt][1] * lw, (float)acc[rt][2] * lw,
+                          (float)acc[rt][3] * lw};
+      const float f = quad_reduce_scatter(x, L);
+      zr[tt][rt] = (tok_ok && 4 * rt + hc < G) ? ldexpf(f * ak, -fex[rt]) : -INFINITY;
     }
   }
 
-  // (5) Per-wave softmax: m, l, and the value-side operands P (fixed point, limb L).
-  float av[NTILE][4];
-  float am = 0.f;
-#pragma unroll
-  for (int tt = 0; tt < NTILE; ++tt) {
-    const int tok0 = wb + 16 * tt;
-    const uint2 avw = *reinterpret_cast<const uint2*>(avb + tok0 + 4 * g);
-    av[tt][0] = half_bits_to_float((uint16_t)(avw.x & 0xffff));
-    av[tt][1] = half_bits_to_float((uint16_t)(avw.x >> 16));
-    av[tt][2] = half_bits_to_float((uint16_t)(avw.y & 0xffff));
-    av[tt][3] = half_bits_to_float((uint16_t)(avw.y >> 16));
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (tok0 + 4 * g + i >= nt) av[tt][i] = 0.f;
-      am = fmaxf(am, fabsf(av[tt][i]));
-    }
-  }
-  am = fmaxf(am, __shfl_xor(am, 16, 64));
-  am = fmaxf(am, __shfl_xor(am, 32, 64));
-  int fv = 0;
-  {
-    int e = 0;
-    frexpf(am, &e);
-    fv = am > 0.f ? 30 - e : 0;    // P <= max alpha^V < 2^e, so P 2^fv < 2^30
-  }
-  uint32_t pdw[NT][NTILE];
+  // (5) Softmax: one maximum per head over the workgroup, and one fixed-point exponent
+  //     for P from the largest alpha^V.
 #pragma unroll
   for (int rt = 0; rt < NT; ++rt) {
     float m = -INFINITY;
 #pragma unroll
-    for (int tt = 0; tt < NTILE; ++tt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) m = fmaxf(m, z[tt][rt][i]);
+    for (int tt = 0; tt < NTILE; ++tt) m = fmaxf(m, zr[tt][rt]);
+    m = quad_max(m);
     m = fmaxf(m, __shfl_xor(m, 16, 64));
     m = fmaxf(m, __shfl_xor(m, 32, 64));
+    if (g == 0 && L == 0) wmax[wave][4 * rt + hc] = m;
+  }
+  amax = wave_max(amax);
+  if (lane == 0) wav[wave] = amax;
+  __syncthreads();
+  float mh[NT];
+#pragma unroll
+  for (int rt = 0; rt < NT; ++rt) {
+    mh[rt] = wmax[0][4 * rt + hc];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) mh[rt] = fmaxf(mh[rt], wmax[w][4 * rt + hc]);
+  }
+  int fv = 0;
+  {
+    float am = wav[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) am = fmaxf(am, wav[w]);
+    int e = 0;
+    frexpf(am, &e);
+    fv = am > 0.f ? 30 - e : 0;           // P <= max alpha^V < 2^e, so P 2^fv < 2^30
+  }
+  // Token 16 q + 4 g + L of a chunk sits at bit d = 2 g + q % 2 of its value byte.
+  const float sc_even = ldexpf(1.f, fv - 2 * g);
+  const float sc_odd = (g == 3 ? -1.f : 1.f) * ldexpf(1.f, fv - 2 * g - 1);
+  const uint32_t sel_a = (L & 2) ? 0x03020706u : 0x05040100u;
+  const uint32_t sel_b = (L & 1) ? 0x03070105u : 0x06020400u;
+  v4i* pb = reinterpret_cast<v4i*>(smem + a.off_pb);  // [NCH][NT][64] value operands
+#pragma unroll
+  for (int rt = 0; rt < NT; ++rt) {
     float lsum = 0.f;
-    double pa = 0.0;
 #pragma unroll
-    for (int tt = 0; tt < NTILE; ++tt) {
-      const int d = 2 * g + (tt & 1);     // bit of this lane's tokens inside the value bytes
-      uint32_t dw = 0u;
+    for (int ch = 0; ch < CPW; ++ch) {
+      uint32_t y[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = (z[tt][rt][i] == -INFINITY) ? 0.f : exp2f(z[tt][rt][i] - m);
+      for (int qd = 0; qd < 4; ++qd) {
+        const int tt = 4 * ch + qd;
+        const float z = zr[tt][rt];
+        const float p = (z == -INFINITY) ? 0.f : exp2f(z - mh[rt]);
         lsum += p;
-        int fx = (int)rintf(ldexpf(p * av[tt][i], fv - d));
-        pa += ldexp((double)fx, d);
-        if (d == 7) fx = -fx;
-        dw |= ((pack_limbs(fx) >> (8 * L)) & 0xffu) << (8 * i);
+        const int fx = (int)rintf(p * avt[tt] * ((qd & 1) ? sc_odd : sc_even));
+        uint32_t x = pack_limbs(fx);
+        // quad byte transpose: (token L, limbs 0..3) -> (limb L, tokens 0..3)
+        x = __builtin_amdgcn_perm(quad_xor2(x), x, sel_a);
+        y[qd] = __builtin_amdgcn_perm(quad_xor1(x), x, sel_b);
       }
-      pdw[rt][tt] = dw;
+      pb[((wave * CPW + ch) * NT + rt) * 64 + lane] =
+          (v4i){(int)y[0], (int)y[1], (int)y[2], (int)y[3]};
     }
+    lsum = quad_sum(lsum);
     lsum += __shfl_xor(lsum, 16, 64);
     lsum += __shfl_xor(lsum, 32, 64);
-    pa += __shfl_xor(pa, 16, 64);
-    pa += __shfl_xor(pa, 32, 64);
-    if (g == 0 && L == 0) {
-      mw[wave][4 * rt + hc] = m;
-      lw[wave][4 * rt + hc] = lsum;
-      paw[wave][4 * rt + hc] = ldexp(pa, -fv);
-    }
+    if (g == 0 && L == 0) wsum[wave][4 * rt + hc] = lsum;
   }
+  __syncthreads();
 
-  // (6) Value bits x P limbs, in passes of VTP value-bit tiles.
-  const uint32_t mask0 = 0x01010101u << (2 * g), mask1 = mask0 << 1;
-  float* obw = reinterpret_cast<float*>(smem + ob_base + wave * ob_wstride);   // [NH][BV]
-  for (int vb = 0; vb < NVT; vb += VTP) {
-    v4i accv[VTP][NT];
+  // (6) Value bits x P limbs over all chunks of the split; value-bit tiles are dealt to
+  //     the waves round robin.  O'(v) goes to LDS (over the consumed key records).
+  const int BV = min(hv->budget, 8 * RV);
+  const int NVT = (BV + 15) >> 4;
+  const uint32_t m0 = 0x01010101u << (2 * g), m1 = m0 << 1;
+  float* ob = reinterpret_cast<float*>(smem + a.off_ob);   // [NH][ob_stride]
+  for (int vt = wave; vt < NVT; vt += NW) {
+    v4i acc[NT], acc2[NT];                          // even / odd chunks: two MFMA chains
 #pragma unroll
-    for (int k = 0; k < VTP; ++k)
+    for (int rt = 0; rt < NT; ++rt) acc[rt] = acc2[rt] = (v4i){0, 0, 0, 0};
 #pragma unroll
-      for (int rt = 0; rt < NT; ++rt) accv[k][rt] = (v4i){0, 0, 0, 0};
+    for (int ch = 0; ch < NCH; ++ch) {
+      const uint2 ww = *reinterpret_cast<const uint2*>(vbuf + ch * kTile * RV + 8 * (16 * vt + n));
+      const v4i av4 = {(int)(ww.x & m0), (int)(ww.x & m1), (int)(ww.y & m0), (int)(ww.y & m1)};
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      v4i bp[NT];
-#pragma unroll
-      for (int rt = 0; rt < NT; ++rt)
-        bp[rt] = (v4i){(int)pdw[rt][4 * c], (int)pdw[rt][4 * c + 1], (int)pdw[rt][4 * c + 2],
-                       (int)pdw[rt][4 * c + 3]};
-      const uint8_t* tile = vbuf + ((wb >> 6) + c) * (kTile * RV);
-#pragma unroll
-      for (int k = 0; k < VTP; ++k) {
-        if (vb + k < NVT) {
-          const int v = 16 * (vb + k) + n;
-          const uint2 ww = *reinterpret_cast<const uint2*>(tile + 8 * v);
-          const v4i a = {(int)(ww.x & mask0), (int)(ww.x & mask1), (int)(ww.y & mask0),
-                         (int)(ww.y & mask1)};
-#pragma unroll
-          for (int rt = 0; rt < NT; ++rt) accv[k][rt] = mfma_i8(a, bp[rt], accv[k][rt]);
-        }
+      for (int rt = 0; rt < NT; ++rt) {
+        if (ch & 1)
+          acc2[rt] = mfma_i8(av4, pb[(ch * NT + rt) * 64 + lane], acc2[rt]);
+        else
+          acc[rt] = mfma_i8(av4, pb[(ch * NT + rt) * 64 + lane], acc[rt]);
       }
     }
-    if (vb == 0) __builtin_amdgcn_wave_barrier();   // key records of this wave are consumed
 #pragma unroll
-    for (int k = 0; k < VTP; ++k) {
-      if (vb + k < NVT) {
-#pragma unroll
-        for (int rt = 0; rt < NT; ++rt) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float f = quad_sum(ldexpf((float)accv[k][rt][i], 8 * L));
-            const int v = 16 * (vb + k) + 4 * g + i;
-            if (L == 0 && v < BV) obw[(4 * rt + hc) * BV + v] = ldexpf(f, -fv);
-          }
-        }
-      }
+    for (int rt = 0; rt < NT; ++rt) {
+      acc[rt] += acc2[rt];
+      const float x[4] = {(float)acc[rt][0] * lw, (float)acc[rt][1] * lw, (float)acc[rt][2] * lw,
+                          (float)acc[rt][3] * lw};
+      ob[(4 * rt + hc) * a.ob_stride + 16 * vt + 4 * g + L] = quad_reduce_scatter(x, L);
     }
   }
   __syncthreads();
 
-  // (7) Workgroup partial: merge the four waves, then per channel
-  //     o~_c = s_c 2^(1-b_c) (sum_k 2^k O'(c,k) - 2^(b_c-1) sum_t P_t).
-  if (tid < NH) {
-    float m = -INFINITY;
+  // (7) Partial: o~_c = s_c 2^(1-b_c-fv) (sum_{k < b-1} 2^k O'(c,k) - 2^(b-1) O'(c,b-1)),
+  //     one (head, channel) per thread.
 #pragma unroll
-    for (int w = 0; w < 4; ++w) m = fmaxf(m, mw[w][tid]);
-    float l = 0.f;
-    double pa = 0.0;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float sw = (mw[w][tid] == -INFINITY) ? 0.f : exp2f(mw[w][tid] - m);
-      l += sw * lw[w][tid];
-      pa += (double)sw * paw[w][tid];
-    }
-    mfin[tid] = m;
-    lfin[tid] = l;
-    pafin[tid] = (float)pa;
-  }
-  __syncthreads();
-  for (int i = tid; i < G * kD; i += kDecThreads) {
-    const int h = i / kD, c = i % kD;
-    const int b = hv->bits[c];
-    float o = 0.f;
-    if (b) {
-      float sw[4];
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-        sw[w] = (mw[w][h] == -INFINITY) ? 0.f : exp2f(mw[w][h] - mfin[h]);
-      const int off = hv->bit_off[c];
+  for (int r = 0; r < NR; ++r) {
+    const int h = (r * NTHR + tid) / kD;
+    if (h < G) {
+      const float* oh = ob + h * a.ob_stride;
       float acc = 0.f;
-      for (int k = 0; k < b; ++k) {
-        float ok = 0.f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w)
-          ok += sw[w] * reinterpret_cast<const float*>(smem + ob_base + w * ob_wstride)[h * BV + off + k];
-        acc += ldexpf(ok, k);
+      for (int k = 0; k < kMaxBits; ++k) {
+        const float t = ldexpf(oh[min(voc + k, 8 * RV - 1)], k);
+        acc += (k < vbc) ? ((k == vbc - 1) ? -t : t) : 0.f;
       }
-      o = hv->s[c] * ldexpf(1.f, 1 - b) * (acc - ldexpf(pafin[h], b - 1));
+      const float o = vbc ? ldexpf(vsc * acc, 1 - vbc - fv) : 0.f;
+      buf_store4_coherent(o, prs, (uint32_t)((split * G + h) * sizeof(Partial) + 16 + 4 * cq));
     }
-    st_dev(&part[h].o[c], o);
   }
   if (tid < G) {
-    st_dev(&part[tid].m, mfin[tid]);
-    st_dev(&part[tid].l, lfin[tid]);
+    float m = wmax[0][tid], l = wsum[0][tid];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) {
+      m = fmaxf(m, wmax[w][tid]);
+      l += wsum[w][tid];
+    }
+    buf_store16_coherent((v4f){layout_ok ? m : NAN, l, 0.f, 0.f}, prs,
+                         (uint32_t)((split * G + tid) * sizeof(Partial)));
   }
-  __syncthreads();
-  merge_if_last(params_v, n_q_heads, kvh, seq, kv_row, G, out, counters, flags, partials,
-                n_splits, reinterpret_cast<float*>(smem));
+  merge_if_last<NTHR>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters, out_rows,
+                      reinterpret_cast<float*>(smem));
 }
 
 }  // namespace
@@ -879,47 +915,66 @@ size_t decode_workspace_bytes(int batch, int n_q_heads, int n_kv_heads, int64_t 
   return ws_layout(batch, n_q_heads, n_kv_heads, cap).total;
 }
 
-template <int NT, int S>
-static aatc_status launch_mfma(const void* params_k, const void* params_v, int batch,
-                               int n_q_heads, int n_kv_heads, const void* q, aatc_dtype q_dtype,
-                               const void* k_codes, const uint16_t* k_alpha,
-                               const void* v_codes, const uint16_t* v_alpha,
-                               const int32_t* seq_len, int64_t cap, int rk, int rv,
-                               float softmax_scale, float* out, unsigned* ctr, unsigned* flg,
-                               QPlanes* pln, Partial* parts, size_t merge_lds, hipStream_t st) {
-  constexpr int NH = 4 * NT, TW = S / 4;
-  const int n_splits = (int)((cap + S - 1) / S);
-  const int bv_max = 8 * rv;                           // value budget <= 8 R
-  const size_t front = std::max((size_t)S * (rk + rv) + 16, (size_t)8 * NH * kD * 4);
-  size_t off = front + 4 * (size_t)S;                  // alpha^K, alpha^V
-  const int ql_base = (int)off;
-  off += (size_t)4 * NH * 2 * kMaxPairs * 64;
-  int ob_base, ob_wstride;
-  if ((size_t)NH * bv_max * 4 <= (size_t)TW * rk) {    // O' fits in each wave's key records
-    ob_base = 0;
-    ob_wstride = TW * rk;
+template <int NT, int NTILE, int NP, int NW>
+static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
+  constexpr int NH = 4 * NT, NTHR = 64 * NW, S = NW * 16 * NTILE;
+  a.n_splits = (int)((a.cap + S - 1) / S);
+  const int64_t rows = (int64_t)batch * a.n_kv_heads;
+  if (rows * a.n_splits > (1 << 30)) return AATC_E_UNSUPPORTED;
+  a.n_blocks = (int)(rows * a.n_splits);
+  // LDS: key records | value tiles | alpha^K | alpha^V   (front, also the query-transform
+  // and merge scratch) | query limb planes | value operands | [O' if it does not fit
+  // over the key records].
+  a.off_v = S * a.rk;
+  a.off_ak = a.off_v + S * a.rv;
+  a.off_av = a.off_ak + 2 * S;
+  size_t front = (size_t)a.off_av + 2 * S;
+  front = std::max(front, (size_t)(NTHR / 32 + 1) * NH * kD * sizeof(float));
+  front = std::max(front, merge_lds_bytes(a.G, NTHR));
+  front = round256(front);
+  a.off_ql = (int)front;
+  a.off_pb = a.off_ql + 4 * NH * 2 * NP * 64;
+  size_t off = (size_t)a.off_pb + (size_t)(S / 64) * NT * 64 * 16;
+  a.ob_stride = 8 * a.rv;
+  if ((size_t)NH * a.ob_stride * 4 <= (size_t)S * a.rk) {
+    a.off_ob = 0;
   } else {
-    ob_base = (int)off;
-    ob_wstride = NH * bv_max * 4;
-    off += (size_t)4 * ob_wstride;
+    a.off_ob = (int)off;
+    off += (size_t)NH * a.ob_stride * 4;
   }
-  const size_t lds = std::max(off, merge_lds);
-  if (lds > 160 * 1024 - 24 * 1024) return AATC_E_UNSUPPORTED;
+  const size_t lds = off;
+  if (lds > 160 * 1024 - 4 * 1024) return AATC_E_UNSUPPORTED;
   static size_t set_lds = 0;
   if (lds > set_lds) {
-    if (hipFuncSetAttribute((const void*)decode_mfma_kernel<NT, S>,
+    if (hipFuncSetAttribute((const void*)decode_mfma_kernel<NT, NTILE, NP, NW>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
       return AATC_E_DEVICE;
     set_lds = lds;
   }
-  dim3 grid((unsigned)n_splits, (unsigned)n_kv_heads, (unsigned)batch);
-  hipLaunchKernelGGL((decode_mfma_kernel<NT, S>), grid, dim3(kDecThreads), lds, st, params_k,
-                     params_v, n_q_heads, n_kv_heads, q, (int)q_dtype,
-                     static_cast<const uint8_t*>(k_codes), k_alpha,
-                     static_cast<const uint8_t*>(v_codes), v_alpha, seq_len, cap,
-                     softmax_scale, out, ctr, flg, pln, parts, n_splits, rk, rv, ob_base,
-                     ob_wstride, ql_base);
+  const unsigned grid = (unsigned)((a.n_blocks + 7) / 8 * 8);
+  hipLaunchKernelGGL((decode_mfma_kernel<NT, NTILE, NP, NW>), dim3(grid), dim3(NTHR), lds, st, a);
   return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
+}
+
+template <int NT, int NTILE, int NW>
+static aatc_status launch_mfma_np(const DecodeArgs& a, int batch, hipStream_t st) {
+  switch ((a.rk / 4 + 3) / 4) {
+    case 1: return launch_mfma<NT, NTILE, 1, NW>(a, batch, st);
+    case 2: return launch_mfma<NT, NTILE, 2, NW>(a, batch, st);
+    case 3: return launch_mfma<NT, NTILE, 3, NW>(a, batch, st);
+    default: return launch_mfma<NT, NTILE, 4, NW>(a, batch, st);
+  }
+}
+
+// Split size: 1024 tokens on eight waves while that still gives every compute unit a
+// workgroup, else 512 on four; records over 96 bytes in all halve both (LDS).
+template <int NT>
+static aatc_status launch_mfma_nt(const DecodeArgs& a, int batch, hipStream_t st) {
+  const bool big = a.rk + a.rv > 96;
+  const int64_t rows = (int64_t)batch * a.n_kv_heads;
+  const int64_t wide = rows * ((a.cap + (big ? 511 : 1023)) / (big ? 512 : 1024));
+  if (wide >= 256) return big ? launch_mfma_np<NT, 4, 8>(a, batch, st) : launch_mfma_np<NT, 8, 8>(a, batch, st);
+  return big ? launch_mfma_np<NT, 4, 4>(a, batch, st) : launch_mfma_np<NT, 8, 4>(a, batch, st);
 }
 
 aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
@@ -932,23 +987,37 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
   const WsLayout wl = ws_layout(batch, n_q_heads, n_kv_heads, cap);
   char* ws = static_cast<char*>(workspace);
   auto* ctr = reinterpret_cast<unsigned*>(ws + wl.counters);
-  auto* flg = reinterpret_cast<unsigned*>(ws + wl.flags);
-  auto* pln = reinterpret_cast<QPlanes*>(ws + wl.planes);
   auto* parts = reinterpret_cast<Partial*>(ws + wl.partials);
   const hipStream_t st = (hipStream_t)stream;
-  const size_t merge_lds = ((9 * (size_t)G + 4) * kD + 4 * kDecThreads) * sizeof(float);
+  // Buffer descriptors address at most 2^31 bytes of one (sequence, KV head).
+  if (cap * std::max(rk, rv) >= ((int64_t)1 << 31)) return AATC_E_UNSUPPORTED;
+  if ((cap / kMinSplit + 1) * G * (int64_t)sizeof(Partial) >= ((int64_t)1 << 31))
+    return AATC_E_UNSUPPORTED;
   if (G <= kMaxNH && rk <= 64 && rv <= 64) {
-    const bool big = rk > 48 || rv > 48;
-#define AATC_MFMA(NT, S)                                                                   \
-  launch_mfma<NT, S>(params_k, params_v, batch, n_q_heads, n_kv_heads, q, q_dtype, k_codes, \
-                     k_alpha, v_codes, v_alpha, seq_len, cap, rk, rv, softmax_scale, out, ctr, \
-                     flg, pln, parts, merge_lds, st)
-    if (G <= 4) return big ? AATC_MFMA(1, 256) : AATC_MFMA(1, 512);
-    return big ? AATC_MFMA(2, 256) : AATC_MFMA(2, 512);
-#undef AATC_MFMA
+    DecodeArgs a{};
+    a.params_k = params_k;
+    a.params_v = params_v;
+    a.q = q;
+    a.k_codes = static_cast<const uint8_t*>(k_codes);
+    a.k_alpha = k_alpha;
+    a.v_codes = static_cast<const uint8_t*>(v_codes);
+    a.v_alpha = v_alpha;
+    a.seq_len = seq_len;
+    a.out = out;
+    a.counters = ctr;
+    a.partials = parts;
+    a.cap = cap;
+    a.n_q_heads = n_q_heads;
+    a.n_kv_heads = n_kv_heads;
+    a.G = G;
+    a.q_dtype = (int)q_dtype;
+    a.rk = rk;
+    a.rv = rv;
+    a.scale_log2e = softmax_scale * kLog2e;
+    return G <= 4 ? launch_mfma_nt<1>(a, batch, st) : launch_mfma_nt<2>(a, batch, st);
   }
   const int n_splits = (int)((cap + kSplit - 1) / kSplit);
-  size_t lds = std::max((size_t)G * (kSplit + kMaxBudget) * sizeof(float), merge_lds);
+  size_t lds = std::max((size_t)G * (kSplit + kMaxBudget) * sizeof(float), merge_lds_bytes(G, kThreads));
   if (lds > 160 * 1024 - 24 * 1024) return AATC_E_UNSUPPORTED;
   static size_t set_lds0 = 0;
   if (lds > set_lds0) {
@@ -958,11 +1027,11 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
     set_lds0 = lds;
   }
   dim3 grid((unsigned)n_splits, (unsigned)n_kv_heads, (unsigned)batch);
-  hipLaunchKernelGGL(decode_split_kernel, grid, dim3(kDecThreads), lds, st, params_k, params_v,
+  hipLaunchKernelGGL(decode_split_kernel, grid, dim3(kThreads), lds, st, params_k, params_v,
                      n_q_heads, n_kv_heads, q, (int)q_dtype,
                      static_cast<const uint8_t*>(k_codes), k_alpha,
                      static_cast<const uint8_t*>(v_codes), v_alpha, seq_len, cap,
-                     softmax_scale, out, ctr, flg, parts, n_splits, rk, rv);
+                     softmax_scale, out, ctr, parts, n_splits, rk, rv);
   return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
 }
 

@@ -28,7 +28,8 @@ __device__ inline float wave_max(float v) {
   return v;
 }
 
-// Quantize one transformed coefficient (canonical fp32 sequence).
+// Quantize one transformed coefficient (canonical fp32 sequence); returns the b-bit two's
+// complement pattern of the code.
 __device__ inline uint32_t quantize_code(float r, float inv_a, int b) {
   float y = r * inv_a;
   float xq = ldexpf(y, b - 1);
@@ -36,7 +37,7 @@ __device__ inline uint32_t quantize_code(float r, float inv_a, int b) {
   int code = (int)f + ((xq - f) >= 0.5f ? 1 : 0);
   const int half = 1 << (b - 1);
   code = min(max(code, -half), half - 1);
-  return (uint32_t)(code + half);
+  return (uint32_t)code & ((1u << b) - 1u);
 }
 
 __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(

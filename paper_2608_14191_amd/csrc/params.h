@@ -27,11 +27,22 @@ struct alignas(256) HeadParams {
   uint16_t bit_off[kD];           // first record bit of channel c
   uint8_t virt_chan[kMaxBudget];  // record bit v -> storage channel
   uint8_t virt_bit[kMaxBudget];   // record bit v -> bit index inside that channel's code
+  // Record bit v = 32 D + 8 j + d described at [(8 D + d) * 4 + j]: storage channel c
+  // (bits 0-6), 8 + k + 1 - b_c for bit k of a b_c-bit code (bits 8-11), sign bit of
+  // the code (bit 14), bit in use (bit 15).
+  uint16_t bit_desc[kMaxBudget];
   int32_t d_active;
   int32_t budget;
   int32_t record_bytes;
   int32_t pad_;
 };
+
+// The decode kernel reads these fields with 16-, 8- and 4-byte vector loads.
+static_assert(offsetof(HeadParams, T) % 16 == 0, "T alignment");
+static_assert(offsetof(HeadParams, s) % 16 == 0, "s alignment");
+static_assert(offsetof(HeadParams, bit_off) % 8 == 0, "bit_off alignment");
+static_assert(offsetof(HeadParams, bits) % 4 == 0, "bits alignment");
+static_assert(offsetof(HeadParams, bit_desc) % 8 == 0, "bit_desc alignment");
 
 struct alignas(256) TensorHeader {
   uint32_t magic;

@@ -23,24 +23,26 @@ def test_quantizer_worked_example_two_bits():
     g = _golden("quantizer_worked_example.json")["two_bit"]
     h = np.array([g["h"]], dtype=np.float32)
     bits = np.array(g["bits"])
-    u, a16 = aatc.quantize(h, bits, _f16(g["s"]))
+    c, a16 = aatc.quantize(h, bits, _f16(g["s"]))
     assert float(a16[0]) == g["alpha"]
-    assert u[0].tolist() == g["u"]
-    assert (u[0] - 2).tolist() == g["codes"]
-    rec = aatc.pack_records(u, bits)
+    assert c[0].tolist() == g["codes"]
+    assert (c[0] % 4).tolist() == g["stored"]
+    rec = aatc.pack_records(c, bits)
     assert rec[0].tobytes().hex() == g["record_bytes_hex"]
-    hh = aatc.dequantize(u, a16, bits, _f16(g["s"]))
+    hh = aatc.dequantize(c, a16, bits, _f16(g["s"]))
     np.testing.assert_allclose(hh[0], g["h_hat"], atol=0)
-    np.testing.assert_array_equal(aatc.unpack_records(rec, bits), u)
+    np.testing.assert_array_equal(aatc.unpack_records(rec, bits), c)
 
 
 def test_quantizer_worked_example_one_bit():
     g = _golden("quantizer_worked_example.json")["one_bit"]
     h = np.array([g["h"]], dtype=np.float32)
     bits = np.array(g["bits"])
-    u, a16 = aatc.quantize(h, bits, _f16(g["s"]))
-    assert u[0].tolist() == g["u"]
-    hh = aatc.dequantize(u, a16, bits, _f16(g["s"]))
+    c, a16 = aatc.quantize(h, bits, _f16(g["s"]))
+    assert c[0].tolist() == g["codes"]
+    rec = aatc.pack_records(c, bits)
+    assert (np.unpackbits(rec[0], bitorder="little")[:2]).tolist() == g["stored"]
+    hh = aatc.dequantize(c, a16, bits, _f16(g["s"]))
     np.testing.assert_allclose(hh[0], g["h_hat"], atol=1e-3)   # alpha is stored as fp16
 
 
@@ -60,14 +62,14 @@ def test_quantizer_error_within_half_step(seed):
     the overload, so clamped elements stay within one step (plus the fp16 rounding of
     alpha)."""
     h, bits, s16 = _random_case(seed)
-    u, a16 = aatc.quantize(h, bits, s16)
-    hh = aatc.dequantize(u, a16, bits, s16)
+    c, a16 = aatc.quantize(h, bits, s16)
+    hh = aatc.dequantize(c, a16, bits, s16)
     keep = bits > 0
     s = s16.astype(np.float64)
     a = a16.astype(np.float64)
     delta = 2 * a[:, None] * s[None, :] * 2.0 ** (-bits[None, :].astype(float))
     err = np.abs(h.astype(np.float64) - hh)
-    top = u == (1 << bits)[None, :] - 1
+    top = c == (1 << np.maximum(bits - 1, 0))[None, :] - 1
     inner = keep[None, :] & ~top
     assert np.all(err[inner] <= delta[inner] * (0.5 + 1e-5))
     alpha = np.max(np.abs(h[:, keep].astype(np.float64) / s[keep]), axis=1)
@@ -75,7 +77,8 @@ def test_quantizer_error_within_half_step(seed):
     over = keep[None, :] & top
     assert np.all(err[over] <= (delta + slack)[over] * (1 + 1e-5))
     assert np.all(hh[:, ~keep] == 0)
-    assert np.all((u >= 0) & (u < (1 << bits)[None, :]))
+    half = np.where(keep, 1 << np.maximum(bits - 1, 0), 0)[None, :]
+    assert np.all((c >= -half) & (c < np.maximum(half, 1)))
 
 
 def test_quantizer_is_round_half_up_of_the_fp32_ratio():
@@ -85,8 +88,8 @@ def test_quantizer_is_round_half_up_of_the_fp32_ratio():
     # alpha = 1 (first token element), x = h * 8 exactly representable.
     vals = np.array([-8.0, -7.5, -2.5, -0.5, 0.0, 0.5, 1.5, 2.5, 7.49, 7.5, 8.0]) / 8.0
     h = np.stack([np.full_like(vals, 1.0), vals], axis=1).astype(np.float32)
-    u, _ = aatc.quantize(h, np.array([4, 4]), _f16([1.0, 1.0]))
-    codes = u[:, 1] - 8
+    c, _ = aatc.quantize(h, np.array([4, 4]), _f16([1.0, 1.0]))
+    codes = c[:, 1]
     assert codes.tolist() == [-8, -7, -2, 0, 0, 1, 2, 3, 7, 7, 7]
 
 
@@ -102,8 +105,8 @@ def test_noise_variance_closed_form_and_decay_with_bits():
     for b in range(1, 17):
         h = np.stack([np.ones(n), rng.uniform(-1, 1, n)], axis=1).astype(np.float32)
         bits = np.array([b, b])
-        u, a16 = aatc.quantize(h, bits, _f16([1.0, 1.0]))
-        hh = aatc.dequantize(u, a16, bits, _f16([1.0, 1.0]))
+        c, a16 = aatc.quantize(h, bits, _f16([1.0, 1.0]))
+        hh = aatc.dequantize(c, a16, bits, _f16([1.0, 1.0]))
         mse = np.mean((h[:, 1].astype(np.float64) - hh[:, 1]) ** 2)
         delta = 2.0 ** (1 - b)
         assert mse == pytest.approx(delta ** 2 / 12 * (1 + 3 * 2.0 ** -b), rel=0.01)
@@ -126,21 +129,23 @@ def test_zero_and_saturating_tokens():
     bits = np.array([3, 2, 0])
     s16 = _f16([1.0, 0.5, 0])
     h = np.array([[0, 0, 5], [1e6, -3e5, 0]], dtype=np.float32)
-    u, a16 = aatc.quantize(h, bits, s16)
-    assert u[0].tolist() == [4, 2, 0] and float(a16[0]) == 0.0
+    c, a16 = aatc.quantize(h, bits, s16)
+    assert c[0].tolist() == [0, 0, 0] and float(a16[0]) == 0.0
     assert float(a16[1]) == 65504.0
-    hh = aatc.dequantize(u, a16, bits, s16)
+    hh = aatc.dequantize(c, a16, bits, s16)
     assert np.all(hh[0] == 0)
 
 
 def test_record_roundtrip_and_padding():
     rng = np.random.default_rng(12)
     bits = np.sort(rng.integers(0, 9, size=128))[::-1]
-    u = rng.integers(0, 1 << 8, size=(70, 128)) & ((1 << bits) - 1)[None, :]
-    rec = aatc.pack_records(u, bits)
+    half = np.where(bits > 0, 1 << np.maximum(bits - 1, 0), 0)
+    c = rng.integers(-128, 128, size=(70, 128))
+    c = np.clip(c, -half[None, :], np.maximum(half - 1, 0)[None, :])
+    rec = aatc.pack_records(c, bits)
     budget = int(bits.sum())
     assert rec.shape == (70, 4 * ((budget + 31) // 32))
-    np.testing.assert_array_equal(aatc.unpack_records(rec, bits), u)
+    np.testing.assert_array_equal(aatc.unpack_records(rec, bits), c)
     pad = np.unpackbits(rec, axis=1, bitorder="little")[:, budget:]
     assert not pad.any()
 
