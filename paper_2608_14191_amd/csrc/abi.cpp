@@ -68,6 +68,8 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
         for (int ch = 0; ch < kD; ++ch) hp->Tt[ch * kD + j] = c.transform[j * kD + ch];
       for (int i = 0; i < kD * kD; ++i)
         hp->Tq[i] = (int16_t)std::nearbyint(std::ldexp((double)c.transform[i], kTFrac));
+      for (int j = 0; j < kD; ++j)
+        for (int ch = 0; ch < kD; ++ch) hp->Tqt[ch * kD + j] = hp->Tq[j * kD + ch];
       int off = 0;
       for (int ch = 0; ch < kD; ++ch) {
         const int b = c.bits[ch];

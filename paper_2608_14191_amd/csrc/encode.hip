@@ -13,6 +13,7 @@ namespace {
 
 constexpr int kEncThreads = 256;                 // two tokens in flight, 128 lanes each
 constexpr int kRecWords = kMaxBudget / 32;       // words of the largest record
+constexpr int kSmallBatch = 16;                  // appends up to this many tokens: per-token kernel
 
 __device__ inline float load_elem(const void* x, int dtype, int64_t idx) {
   if (dtype == AATC_BF16) {
@@ -136,12 +137,114 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
   }
 }
 
+// One workgroup per (token, KV head), for appends of a few tokens: the same canonical
+// arithmetic as encode_exact_kernel, with the exact dot product split over two halves
+// of j and the transposed fixed-point transform read straight from global memory.
+// Tile bits are set and cleared with device atomics, so tokens that share a tile word
+// may be encoded by different workgroups.
+__global__ __launch_bounds__(kEncThreads) void encode_token_kernel(
+    const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t x_stride,
+    int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha, int64_t cap,
+    int64_t pos) {
+  __shared__ __align__(16) int xs[kD];
+  __shared__ long long part[kD];
+  __shared__ uint32_t rec[kRecWords];
+  __shared__ float red_x[4], red_a[4];
+
+  const int64_t t = pos + blockIdx.x;
+  const int head = blockIdx.y;
+  const HeadParams* hp = head_params(params, head);
+  const int tid = threadIdx.x, c = tid & (kD - 1), half = tid >> 7, wave = tid >> 6;
+  // Loads: row c of the transposed transform, columns 64 half .. 64 half + 63; the
+  // channel tables; the token.
+  uint4 tq[8];
+  const uint4* trow = reinterpret_cast<const uint4*>(hp->Tqt + c * kD + 64 * half);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) tq[k] = trow[k];
+  const int b = hp->bits[c], off = hp->bit_off[c];
+  const float inv_s = hp->inv_s[c];
+  const int rbytes = hp->record_bytes;
+  const float xv = (tid < kD) ? load_elem(x, dtype, (int64_t)blockIdx.x * x_stride +
+                                                        (int64_t)head * kD + tid)
+                              : 0.f;
+  if (tid < kRecWords) rec[tid] = 0u;
+  // Per-token fixed-point scale: max |x_j| goes to [2^13, 2^14).
+  float m = wave_max(fabsf(xv));
+  if ((tid & 63) == 0) red_x[wave] = m;
+  __syncthreads();
+  m = fmaxf(red_x[0], red_x[1]);
+  int e = 0;
+  frexpf(m, &e);
+  const int shift = (m > 0.f) ? (kXLead - (e - 1)) : 0;
+  if (tid < kD) xs[tid] = (int)rintf(ldexpf(xv, shift));
+  __syncthreads();
+  // Exact integer transform h_c = sum_j X_j Tq_jc.
+  long long acc = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int4 x0 = reinterpret_cast<const int4*>(xs + 64 * half + 8 * k)[0];
+    const int4 x1 = reinterpret_cast<const int4*>(xs + 64 * half + 8 * k)[1];
+    const int xv8[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+    const uint32_t tw[4] = {tq[k].x, tq[k].y, tq[k].z, tq[k].w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc += (long long)xv8[2 * i] * (long long)(int16_t)(tw[i] & 0xffffu);
+      acc += (long long)xv8[2 * i + 1] * (long long)(int16_t)(tw[i] >> 16);
+    }
+  }
+  if (half) part[c] = acc;
+  __syncthreads();
+  float r = 0.f;
+  if (!half) {
+    acc += part[c];
+    const float h = (float)ldexp((double)acc, -(shift + kTFrac));
+    r = h * inv_s;
+  }
+  float a = wave_max((!half && b > 0) ? fabsf(r) : 0.f);
+  if ((tid & 63) == 0) red_a[wave] = a;
+  __syncthreads();
+  a = fmaxf(red_a[0], red_a[1]);
+  const __half a16 = __float2half_rn(fminf(a, 65504.f));
+  const float a32 = __half2float(a16);
+  const float inv_a = (a32 > 0.f) ? (float)(1.0 / (double)a32) : 0.f;
+  if (!half && b > 0) {
+    const uint32_t u = quantize_code(r, inv_a, b);
+    atomicOr(&rec[off >> 5], u << (off & 31));
+    if ((off & 31) + b > 32) atomicOr(&rec[(off >> 5) + 1], u >> (32 - (off & 31)));
+  }
+  if (tid == 0) alpha[(int64_t)head * cap + t] = __half_as_ushort(a16);
+  __syncthreads();
+
+  if (layout == AATC_LAYOUT_RECORDS) {
+    uint32_t* out = reinterpret_cast<uint32_t*>(codes + ((int64_t)head * cap + t) * rbytes);
+    for (int i = tid; i < rbytes / 4; i += kEncThreads) out[i] = rec[i];
+  } else {
+    // Token p = 16 d + 4 g + i of its tile: bit 8 i + 2 g + d % 2 of word 2 v + d / 2.
+    const int p = (int)(t % kTile), d = p >> 4;
+    const uint32_t bit = 1u << (8 * (p & 3) + 2 * ((p >> 2) & 3) + (d & 1));
+    uint32_t* tw = reinterpret_cast<uint32_t*>(codes) +
+                   ((int64_t)head * (cap / kTile) + t / kTile) * (16 * rbytes) + (d >> 1);
+    for (int v = tid; v < 8 * rbytes; v += kEncThreads) {
+      if ((rec[v >> 5] >> (v & 31)) & 1u)
+        __hip_atomic_fetch_or(tw + 2 * v, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      else
+        __hip_atomic_fetch_and(tw + 2 * v, ~bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
 }  // namespace
 
 aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_dtype x_dtype,
                           int64_t n_tok, int64_t x_tok_stride, aatc_layout layout,
                           void* codes, uint16_t* alpha, int64_t cap, int64_t pos,
                           void* stream) {
+  if (n_tok <= kSmallBatch) {
+    hipLaunchKernelGGL(encode_token_kernel, dim3((unsigned)n_tok, (unsigned)n_heads),
+                       dim3(kEncThreads), 0, (hipStream_t)stream, params, x, (int)x_dtype,
+                       x_tok_stride, (int)layout, static_cast<uint8_t*>(codes), alpha, cap, pos);
+    return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
+  }
   const int64_t first = pos / kTile, last = (pos + n_tok - 1) / kTile;
   dim3 grid((unsigned)(last - first + 1), (unsigned)n_heads);
   hipLaunchKernelGGL(encode_exact_kernel, grid, dim3(kEncThreads), 0, (hipStream_t)stream,

@@ -20,6 +20,7 @@ struct alignas(256) HeadParams {
   float T[kD * kD];               // [j][c] transform, storage channels (fp32)
   float Tt[kD * kD];              // [c][j] the same transform, transposed
   int16_t Tq[kD * kD];            // [j][c] rint(T * 2^14), |Tq| <= 2^14
+  int16_t Tqt[kD * kD];           // [c][j] the same, transposed
   float inv_s[kD];                // fp32 1/s_c (0 for dropped or zero-scale channels)
   float s[kD];                    // s_c as fp32 (exact value of the fp16 scale)
   uint16_t s16[kD];               // s_c fp16 bits
@@ -39,6 +40,7 @@ struct alignas(256) HeadParams {
 
 // The decode kernel reads these fields with 16-, 8- and 4-byte vector loads.
 static_assert(offsetof(HeadParams, T) % 16 == 0, "T alignment");
+static_assert(offsetof(HeadParams, Tqt) % 16 == 0, "Tqt alignment");
 static_assert(offsetof(HeadParams, s) % 16 == 0, "s alignment");
 static_assert(offsetof(HeadParams, bit_off) % 8 == 0, "bit_off alignment");
 static_assert(offsetof(HeadParams, bits) % 4 == 0, "bits alignment");

@@ -159,7 +159,7 @@ def test_encode_incremental_appends_match_bulk():
     ka, va = alpha_cache(H, cap), alpha_cache(H, cap)
     vc.fill_(0xA5)          # stale bytes beyond the written tokens must not matter
     pos = 0
-    for n in [1, 1, 5, 57, 1, 64, 3, 100, 68]:
+    for n in [1, 1, 5, 16, 41, 1, 64, 3, 100, 68]:      # 16: largest per-token append
         P.aatc_encode(pk, H, xk[pos:], n, H * 128, P.LAYOUT_RECORDS, kc, ka, cap, pos)
         P.aatc_encode(pv, H, xv[pos:], n, H * 128, P.LAYOUT_TILES, vc, va, cap, pos)
         pos += n
