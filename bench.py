@@ -1,18 +1,20 @@
 """Benchmark of the AATC hot path on one MI355X.
 
-Step (the whole hot path once, Llama-3.1-8B-shaped layer, decode batch 1):
-  1. aatc_encode of one new token's keys and values (8 KV heads) into the packed
-     caches (records for K, bit-transposed tiles for V), at the last cached position;
-  2. aatc_decode_attention of 32 query heads (GQA 4:1) over 32768 cached tokens per KV
-     head packed at 2.75 bits per channel.
+Step (the whole hot path once, Llama-3.1-8B-shaped layer, decode batch 1): one
+aatc_append_decode_attention call, which
+  1. encodes one new token's keys and values (8 KV heads) into the packed caches (records
+     for K, bit-transposed tiles for V) at the last cached position, and
+  2. runs decode attention of 32 query heads (GQA 4:1) over the 32768 cached tokens per
+     KV head packed at 2.75 bits per channel,
+in a single kernel launch.
 The cache stays at 32768 tokens: every step rewrites the last token.  To measure HBM
 rather than the 256 MB Infinity Cache, the steps rotate over enough cache copies to
 exceed 512 MB.  The steps are captured in HIP graphs (one step per cache copy) so the
 measurement is of the GPU, not of Python launch overhead.
 
 value = packed-cache bytes read per step (codes + fp16 token scales of K and V) /
-wall time per step.  roofline = the same bytes / the decode kernel's average duration
-(HIP events on the launch stream) against 8 TB/s.  Encode throughput of a 65536-token
+wall time per step.  roofline = the same bytes / that kernel's average duration (HIP
+events on the launch stream) against 8 TB/s.  Encode throughput of a 65536-token
 prefill (8 KV heads, K and V) is reported alongside.  cpu_baseline = the NumPy oracle's
 decode attention on a bounded token sample of the same workload.
 """
@@ -102,20 +104,15 @@ def run_decode_bench(s, steps, warmup):
     scale = 128 ** -0.5
     xk, xv = s["last_tok"][0], s["last_tok"][1]
 
-    def encode_new_token(i):
-        kc, ka, vc, va = copies[i % n_copies]
-        for b in range(B):
-            P.aatc_encode(s["pk"], H, xk, 1, H * 128, P.LAYOUT_RECORDS, kc[b], ka[b], cap, L - 1)
-            P.aatc_encode(s["pv"], H, xv, 1, H * 128, P.LAYOUT_TILES, vc[b], va[b], cap, L - 1)
-
-    def decode(i):
-        kc, ka, vc, va = copies[i % n_copies]
-        P.aatc_decode_attention(s["pk"], s["pv"], B, HQ, H, s["q"], kc, ka, vc, va, lens, cap,
-                                s["rk"], s["rv"], scale, out, ws)
+    x_new_k = xk.reshape(1, H, 128).expand(B, H, 128).contiguous()
+    x_new_v = xv.reshape(1, H, 128).expand(B, H, 128).contiguous()
 
     def step(i):
-        encode_new_token(i)
-        decode(i)
+        """Append the step's token (position L - 1) to K and V and decode: one launch."""
+        kc, ka, vc, va = copies[i % n_copies]
+        P.aatc_append_decode_attention(s["pk"], s["pv"], B, HQ, H, s["q"], x_new_k, x_new_v,
+                                       kc, ka, vc, va, lens, cap, s["rk"], s["rv"], scale, out,
+                                       ws)
 
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -135,9 +132,7 @@ def run_decode_bench(s, steps, warmup):
     g_full = capture(n_copies, step)
     rest = steps % n_copies
     g_rest = capture(rest, step) if rest else None
-    g_dec = capture(n_copies, decode)
-    for g in (g_full, g_dec):          # replay once untimed
-        g.replay()
+    g_full.replay()                    # replay once untimed
     torch.cuda.synchronize()
 
     t0 = time.perf_counter()
@@ -148,12 +143,12 @@ def run_decode_bench(s, steps, warmup):
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
-    # Decode kernel alone: HIP events around graph replays of back-to-back decodes.
+    # The step's one kernel: HIP events (on the stream the graphs run on) around replays.
     reps = max(1, min(20, steps // n_copies))
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(reps):
-        g_dec.replay()
+        g_full.replay()
     e1.record()
     torch.cuda.synchronize()
     kern_ms = e0.elapsed_time(e1) / (reps * n_copies)
@@ -263,8 +258,9 @@ def counted_traffic():
 
 
 def counters_run(s, n_decode=6, copy_mib=256):
-    """Eager launches for `rocprofv3 --pmc` (one counter per run): decodes over rotating
-    cache copies, then a plain device copy of known size that calibrates the counters."""
+    """Eager launches for `rocprofv3 --pmc` (one counter per run): decode steps (append +
+    decode, one launch each) over rotating cache copies, then a plain device copy of known
+    size that calibrates the counters."""
     import torch
     P, w = s["P"], s["w"]
     H, HQ, B, L, cap = w.n_kv_heads, w.n_q_heads, w.batch, s["L"], s["cap"]
@@ -275,10 +271,12 @@ def counters_run(s, n_decode=6, copy_mib=256):
     out = torch.zeros((B, HQ, 128), dtype=torch.float32, device="cuda")
     ws = torch.zeros(P.aatc_decode_workspace_bytes(B, HQ, H, cap), dtype=torch.uint8,
                      device="cuda")
+    xk = s["last_tok"][0].reshape(1, H, 128).expand(B, H, 128).contiguous()
+    xv = s["last_tok"][1].reshape(1, H, 128).expand(B, H, 128).contiguous()
     for i in range(n_decode):
         kc, ka, vc, va = copies[i % len(copies)]
-        P.aatc_decode_attention(s["pk"], s["pv"], B, HQ, H, s["q"], kc, ka, vc, va, lens, cap,
-                                s["rk"], s["rv"], 128 ** -0.5, out, ws)
+        P.aatc_append_decode_attention(s["pk"], s["pv"], B, HQ, H, s["q"], xk, xv, kc, ka, vc,
+                                       va, lens, cap, s["rk"], s["rv"], 128 ** -0.5, out, ws)
     torch.cuda.synchronize()
     src = torch.ones(copy_mib << 20, dtype=torch.uint8, device="cuda")
     dst = torch.empty_like(src)

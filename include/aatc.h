@@ -163,7 +163,7 @@ aatc_status aatc_encode(const void* dev_params, int32_t n_kv_heads, int32_t d,
  * domain (App. B: effective query q~ = T_K^T q): for query head j of sequence b,
  * reading KV head j / (n_q_heads / n_kv_heads),
  *   o = T_V * sum_i softmax_i(scale * q~ . h^K_i) h^V_i,
- * with h^_c = alpha_i s_c 2^(1-b_c) (u_ic - 2^(b_c-1)) and no mask inside
+ * with h^_c = alpha_i s_c 2^(1-b_c) code_ic and no mask inside
  * [0, seq_len[b]).  Online softmax over token splits; the inverse transform T_V is
  * applied once to each output.
  *
@@ -196,6 +196,32 @@ aatc_status aatc_decode_attention(const void* dev_params_k, const void* dev_para
                                   int32_t k_record_bytes, int32_t v_record_bytes,
                                   float softmax_scale, float* out, void* workspace,
                                   size_t ws_bytes, void* stream);
+
+/*
+ * aatc_append_decode_attention -- one decode step that also appends the step's new token.
+ *
+ * Equivalent to aatc_encode of x_k into (k_codes, k_alpha) and of x_v into (v_codes,
+ * v_alpha) at position seq_len[b] - 1 of every sequence b (Alg. 1: the new key and value
+ * are projected, quantized and appended), followed by aatc_decode_attention with the
+ * same arguments; codes, scales and outputs are identical to that sequence of calls.
+ * Sequences with seq_len[b] = 0 append nothing.  One launch where the decode kernel
+ * takes the append into the workgroup that reads the new token's split.
+ *
+ * x_k, x_v   device [batch][n_kv_heads][d] new key / value token of each sequence,
+ *            x_dtype F32 or BF16.
+ * k_codes, k_alpha, v_codes, v_alpha  as in aatc_decode_attention; written at the new
+ *            token's position.
+ * Other arguments and errors as in aatc_decode_attention.
+ */
+aatc_status aatc_append_decode_attention(const void* dev_params_k, const void* dev_params_v,
+                                         int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                         int32_t d, const void* q, aatc_dtype q_dtype,
+                                         const void* x_k, const void* x_v, aatc_dtype x_dtype,
+                                         void* k_codes, uint16_t* k_alpha, void* v_codes,
+                                         uint16_t* v_alpha, const int32_t* seq_len, int64_t cap,
+                                         int32_t k_record_bytes, int32_t v_record_bytes,
+                                         float softmax_scale, float* out, void* workspace,
+                                         size_t ws_bytes, void* stream);
 
 /* Human-readable name of a status code (static string). */
 const char* aatc_status_string(aatc_status s);

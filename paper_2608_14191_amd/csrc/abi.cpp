@@ -130,6 +130,40 @@ extern "C" size_t aatc_decode_workspace_bytes(int32_t batch, int32_t n_q_heads,
   return decode_workspace_bytes(batch, n_q_heads, n_kv_heads, cap);
 }
 
+namespace {
+
+aatc_status check_decode(const void* dev_params_k, const void* dev_params_v, int32_t batch,
+                         int32_t n_q_heads, int32_t n_kv_heads, int32_t d, const void* q,
+                         aatc_dtype q_dtype, const void* k_codes, const uint16_t* k_alpha,
+                         const void* v_codes, const uint16_t* v_alpha, const int32_t* seq_len,
+                         int64_t cap, int32_t k_record_bytes, int32_t v_record_bytes,
+                         float softmax_scale, const float* out, const void* workspace,
+                         size_t ws_bytes) {
+  if (d != kD) return AATC_E_UNSUPPORTED;
+  if (!dev_params_k || !dev_params_v || !q || !k_codes || !k_alpha || !v_codes || !v_alpha ||
+      !seq_len || !out || !workspace)
+    return AATC_E_INVALID;
+  if (batch < 1 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0)
+    return AATC_E_INVALID;
+  if (n_q_heads / n_kv_heads > kMaxGroup) return AATC_E_UNSUPPORTED;
+  if (cap < kTile || cap % kTile != 0) return AATC_E_INVALID;
+  if (k_record_bytes < 4 || k_record_bytes > kMaxBudget / 8 || k_record_bytes % 4 != 0 ||
+      v_record_bytes < 4 || v_record_bytes > kMaxBudget / 8 || v_record_bytes % 4 != 0)
+    return AATC_E_INVALID;
+  if (q_dtype != AATC_F32 && q_dtype != AATC_BF16) return AATC_E_INVALID;
+  if (!std::isfinite(softmax_scale)) return AATC_E_INVALID;
+  if (!aligned(dev_params_k, 16) || !aligned(dev_params_v, 16) || !aligned(k_codes, 16) ||
+      !aligned(v_codes, 16) || !aligned(k_alpha, 16) || !aligned(v_alpha, 16) ||
+      !aligned(seq_len, 4) || !aligned(out, 16) || !aligned(workspace, 256) ||
+      !aligned(q, q_dtype == AATC_F32 ? 4 : 2))
+    return AATC_E_INVALID;
+  if (ws_bytes < decode_workspace_bytes(batch, n_q_heads, n_kv_heads, cap))
+    return AATC_E_WORKSPACE;
+  return AATC_OK;
+}
+
+}  // namespace
+
 extern "C" aatc_status aatc_decode_attention(
     const void* dev_params_k, const void* dev_params_v, int32_t batch, int32_t n_q_heads,
     int32_t n_kv_heads, int32_t d, const void* q, aatc_dtype q_dtype, const void* k_codes,
@@ -137,29 +171,40 @@ extern "C" aatc_status aatc_decode_attention(
     const int32_t* seq_len, int64_t cap, int32_t k_record_bytes, int32_t v_record_bytes,
     float softmax_scale, float* out, void* workspace, size_t ws_bytes, void* stream) {
   try {
-    if (d != kD) return AATC_E_UNSUPPORTED;
-    if (!dev_params_k || !dev_params_v || !q || !k_codes || !k_alpha || !v_codes ||
-        !v_alpha || !seq_len || !out || !workspace)
-      return AATC_E_INVALID;
-    if (batch < 1 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0)
-      return AATC_E_INVALID;
-    if (n_q_heads / n_kv_heads > kMaxGroup) return AATC_E_UNSUPPORTED;
-    if (cap < kTile || cap % kTile != 0) return AATC_E_INVALID;
-    if (k_record_bytes < 4 || k_record_bytes > kMaxBudget / 8 || k_record_bytes % 4 != 0 ||
-        v_record_bytes < 4 || v_record_bytes > kMaxBudget / 8 || v_record_bytes % 4 != 0)
-      return AATC_E_INVALID;
-    if (q_dtype != AATC_F32 && q_dtype != AATC_BF16) return AATC_E_INVALID;
-    if (!std::isfinite(softmax_scale)) return AATC_E_INVALID;
-    if (!aligned(dev_params_k, 16) || !aligned(dev_params_v, 16) || !aligned(k_codes, 16) ||
-        !aligned(v_codes, 16) || !aligned(k_alpha, 16) || !aligned(v_alpha, 16) ||
-        !aligned(seq_len, 4) || !aligned(out, 16) || !aligned(workspace, 256) ||
-        !aligned(q, q_dtype == AATC_F32 ? 4 : 2))
-      return AATC_E_INVALID;
-    if (ws_bytes < decode_workspace_bytes(batch, n_q_heads, n_kv_heads, cap))
-      return AATC_E_WORKSPACE;
+    const aatc_status e = check_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads,
+                                       d, q, q_dtype, k_codes, k_alpha, v_codes, v_alpha,
+                                       seq_len, cap, k_record_bytes, v_record_bytes,
+                                       softmax_scale, out, workspace, ws_bytes);
+    if (e != AATC_OK) return e;
     return launch_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads, q, q_dtype,
                          k_codes, k_alpha, v_codes, v_alpha, seq_len, cap, k_record_bytes,
                          v_record_bytes, softmax_scale, out, workspace, stream);
+  } catch (...) {
+    return AATC_E_INVALID;
+  }
+}
+
+extern "C" aatc_status aatc_append_decode_attention(
+    const void* dev_params_k, const void* dev_params_v, int32_t batch, int32_t n_q_heads,
+    int32_t n_kv_heads, int32_t d, const void* q, aatc_dtype q_dtype, const void* x_k,
+    const void* x_v, aatc_dtype x_dtype, void* k_codes, uint16_t* k_alpha, void* v_codes,
+    uint16_t* v_alpha, const int32_t* seq_len, int64_t cap, int32_t k_record_bytes,
+    int32_t v_record_bytes, float softmax_scale, float* out, void* workspace, size_t ws_bytes,
+    void* stream) {
+  try {
+    const aatc_status e = check_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads,
+                                       d, q, q_dtype, k_codes, k_alpha, v_codes, v_alpha,
+                                       seq_len, cap, k_record_bytes, v_record_bytes,
+                                       softmax_scale, out, workspace, ws_bytes);
+    if (e != AATC_OK) return e;
+    if (!x_k || !x_v) return AATC_E_INVALID;
+    if (x_dtype != AATC_F32 && x_dtype != AATC_BF16) return AATC_E_INVALID;
+    const size_t xa = x_dtype == AATC_F32 ? 4 : 2;
+    if (!aligned(x_k, xa) || !aligned(x_v, xa)) return AATC_E_INVALID;
+    return launch_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads, q, q_dtype,
+                         k_codes, k_alpha, v_codes, v_alpha, seq_len, cap, k_record_bytes,
+                         v_record_bytes, softmax_scale, out, workspace, stream, x_k, x_v,
+                         x_dtype);
   } catch (...) {
     return AATC_E_INVALID;
   }

@@ -20,6 +20,7 @@
 
 #include <algorithm>
 
+#include "encode_core.h"
 #include "launch.h"
 #include "params.h"
 
@@ -50,11 +51,14 @@ struct DecodeArgs {
   const void* params_k;
   const void* params_v;
   const void* q;
-  const uint8_t* k_codes;
-  const uint16_t* k_alpha;
-  const uint8_t* v_codes;
-  const uint16_t* v_alpha;
+  uint8_t* k_codes;               // written only by the fused append
+  uint16_t* k_alpha;
+  uint8_t* v_codes;
+  uint16_t* v_alpha;
   const int32_t* seq_len;
+  const void* x_k;                // fused append: new token [batch][n_kv_heads][d], or null
+  const void* x_v;
+  int x_dtype;
   float* out;
   unsigned* counters;
   Partial* partials;
@@ -497,7 +501,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
 // Every workgroup derives its query bit weights itself, while its cache loads are in
 // flight: q~ = T_K^T q (fp32), then per bit the 32-bit fixed-point limbs.
 // ---------------------------------------------------------------------------------------
-template <int NT, int NTILE, int NP, int NW>
+template <int NT, int NTILE, int NP, int NW, bool APPEND>
 __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const DecodeArgs a) {
   constexpr int NTHR = 64 * NW;       // threads per workgroup
   constexpr int NH = 4 * NT;          // head slots: 4 per column tile
@@ -513,6 +517,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   constexpr int NPI = (NH * 4 * NP * 8 + NTHR - 1) / NTHR;   // plane items per thread
   static_assert(NTILE % 4 == 0, "a wave owns whole 64-token chunks");
   static_assert(AL <= NTHR && NR >= 1, "thread mapping");
+  static_assert(!APPEND || NW == 8, "the fused append maps one tensor to 256 threads");
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ unsigned qmx[NH];
   __shared__ int fexp_s[NH];
@@ -600,6 +605,26 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     const uint32_t aoff = (tid < na16) ? (uint32_t)(2 * t0 + 16 * tid) : kNone;
     rak = buf_load16<0>(make_rsrc(a.k_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
     rav = buf_load16<0>(make_rsrc(a.v_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
+  }
+  // Fused append: the workgroup whose split holds token len - 1 encodes it (K with
+  // threads 0..255, V with 256..511; two halves of j per channel), exactly as the encode
+  // kernels do, and patches its copy of the cache.  Its loads go out here.
+  const int p_loc = len - 1 - t0;
+  const bool is_app = APPEND && len > 0 && p_loc < S;          // p_loc >= 0 follows from nt > 0
+  const int et = tid >> 8, ec = tid & (kD - 1), ejp = (tid >> 7) & 1;
+  uint4 etq[8];
+  float ex = 0.f, e_inv_s = 0.f;
+  if constexpr (APPEND) {
+    if (is_app && nt > 0) {
+      const HeadParams* eh = et ? hv : hk;
+      const uint4* trow = reinterpret_cast<const uint4*>(eh->Tqt + ec * kD + 64 * ejp);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) etq[k] = trow[k];
+      e_inv_s = eh->inv_s[ec];
+      if (!ejp)
+        ex = load_elem(et ? a.x_v : a.x_k, a.x_dtype,
+                       ((int64_t)seq * a.n_kv_heads + kvh) * kD + ec);
+    }
   }
   // Keep the compiler from moving work that waits on the early loads above the cache loads.
   __builtin_amdgcn_sched_barrier(0);
@@ -714,6 +739,51 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     fex[rt] = fexp_s[h];
   }
 
+  // (2b) Fused append: encode the new token of both tensors into LDS records.
+  __shared__ int exs[2][kD];
+  __shared__ long long epart[2][kD];
+  __shared__ uint32_t erec[2][kMaxBudget / 32];
+  __shared__ float ered[8];
+  __shared__ uint16_t ea16[2];
+  if constexpr (APPEND) {
+    if (is_app && nt > 0) {
+      if (tid < 2 * (kMaxBudget / 32)) (&erec[0][0])[tid] = 0u;
+      const int eb = et ? vbc : kb, eoff = et ? voc : koff;
+      float m = wave_max(fabsf(ex));
+      if (lane == 0) ered[wave] = m;
+      __syncthreads();
+      const int shift = token_shift(fmaxf(ered[4 * et], ered[4 * et + 1]));
+      if (!ejp) exs[et][ec] = (int)rintf(ldexpf(ex, shift));
+      __syncthreads();
+      long long acc = 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int* xr = &exs[et][64 * ejp + 8 * k];
+        const uint32_t tw[4] = {etq[k].x, etq[k].y, etq[k].z, etq[k].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          acc += (long long)xr[2 * i] * (long long)(int16_t)(tw[i] & 0xffffu);
+          acc += (long long)xr[2 * i + 1] * (long long)(int16_t)(tw[i] >> 16);
+        }
+      }
+      if (ejp) epart[et][ec] = acc;
+      __syncthreads();
+      float r = 0.f;
+      if (!ejp) r = fixed_point_result(acc + epart[et][ec], shift) * e_inv_s;
+      const float am = wave_max((!ejp && eb > 0) ? fabsf(r) : 0.f);
+      if (lane == 0) ered[wave] = am;
+      __syncthreads();
+      const __half a16 = token_alpha(fmaxf(ered[4 * et], ered[4 * et + 1]));
+      const float inv_a = inverse_alpha(a16);
+      if (!ejp && eb > 0) {
+        const uint32_t u = quantize_code(r, inv_a, eb);
+        atomicOr(&erec[et][eoff >> 5], u << (eoff & 31));
+        if ((eoff & 31) + eb > 32) atomicOr(&erec[et][(eoff >> 5) + 1], u >> (32 - (eoff & 31)));
+      }
+      if (ec == 0 && !ejp) ea16[et] = __half_as_ushort(a16);
+    }
+  }
+
   // (3) Land the cache in LDS (over the query-transform scratch).
   uint8_t* kbuf = smem;
   uint8_t* vbuf = smem + a.off_v;
@@ -734,6 +804,34 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     reinterpret_cast<v4i*>(avb)[tid] = rav;
   }
   __syncthreads();
+  if constexpr (APPEND) {
+    // Patch the landed cache with the new token and write it back: its key record and
+    // scales, and the value-tile words that hold its bits (whole words from LDS: the
+    // tile is resident, and no other workgroup touches it).
+    if (is_app && nt > 0) {
+      const int64_t tg = row * a.cap + t0 + p_loc;
+      for (int i = tid; i < RK / 4; i += NTHR) {
+        reinterpret_cast<uint32_t*>(kbuf + p_loc * RK)[i] = erec[0][i];
+        reinterpret_cast<uint32_t*>(a.k_codes + tg * RK)[i] = erec[0][i];
+      }
+      if (tid == 0) {
+        akb[p_loc] = a.k_alpha[tg] = ea16[0];
+        avb[p_loc] = a.v_alpha[tg] = ea16[1];
+      }
+      const int tp = p_loc & (kTile - 1);
+      const uint32_t bit = 1u << tile_bit(tp);
+      uint32_t* lt = reinterpret_cast<uint32_t*>(vbuf + (p_loc / kTile) * kTile * RV) + tile_word(tp);
+      uint32_t* gt = reinterpret_cast<uint32_t*>(a.v_codes + (row * a.cap + t0) * RV +
+                                                 (int64_t)(p_loc / kTile) * kTile * RV) +
+                     tile_word(tp);
+      for (int v = tid; v < 8 * RV; v += NTHR) {
+        const uint32_t w = (lt[2 * v] & ~bit) | (((erec[1][v >> 5] >> (v & 31)) & 1u) ? bit : 0u);
+        lt[2 * v] = w;
+        gt[2 * v] = w;
+      }
+    }
+    __syncthreads();
+  }
 
   // (4) Key scores of this wave's tokens: lane L of a quad ends with token 4 g + L.
   const int wb = wave * TW;
@@ -915,7 +1013,7 @@ size_t decode_workspace_bytes(int batch, int n_q_heads, int n_kv_heads, int64_t 
   return ws_layout(batch, n_q_heads, n_kv_heads, cap).total;
 }
 
-template <int NT, int NTILE, int NP, int NW>
+template <int NT, int NTILE, int NP, int NW, bool APPEND>
 static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
   constexpr int NH = 4 * NT, NTHR = 64 * NW, S = NW * 16 * NTILE;
   a.n_splits = (int)((a.cap + S - 1) / S);
@@ -946,35 +1044,41 @@ static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
   if (lds > 160 * 1024 - 4 * 1024) return AATC_E_UNSUPPORTED;
   static size_t set_lds = 0;
   if (lds > set_lds) {
-    if (hipFuncSetAttribute((const void*)decode_mfma_kernel<NT, NTILE, NP, NW>,
+    if (hipFuncSetAttribute((const void*)decode_mfma_kernel<NT, NTILE, NP, NW, APPEND>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
       return AATC_E_DEVICE;
     set_lds = lds;
   }
   const unsigned grid = (unsigned)((a.n_blocks + 7) / 8 * 8);
-  hipLaunchKernelGGL((decode_mfma_kernel<NT, NTILE, NP, NW>), dim3(grid), dim3(NTHR), lds, st, a);
+  hipLaunchKernelGGL((decode_mfma_kernel<NT, NTILE, NP, NW, APPEND>), dim3(grid), dim3(NTHR), lds,
+                     st, a);
   return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
 }
 
-template <int NT, int NTILE, int NW>
+template <int NT, int NTILE, int NW, bool APPEND>
 static aatc_status launch_mfma_np(const DecodeArgs& a, int batch, hipStream_t st) {
   switch ((a.rk / 4 + 3) / 4) {
-    case 1: return launch_mfma<NT, NTILE, 1, NW>(a, batch, st);
-    case 2: return launch_mfma<NT, NTILE, 2, NW>(a, batch, st);
-    case 3: return launch_mfma<NT, NTILE, 3, NW>(a, batch, st);
-    default: return launch_mfma<NT, NTILE, 4, NW>(a, batch, st);
+    case 1: return launch_mfma<NT, NTILE, 1, NW, APPEND>(a, batch, st);
+    case 2: return launch_mfma<NT, NTILE, 2, NW, APPEND>(a, batch, st);
+    case 3: return launch_mfma<NT, NTILE, 3, NW, APPEND>(a, batch, st);
+    default: return launch_mfma<NT, NTILE, 4, NW, APPEND>(a, batch, st);
   }
 }
 
 // Split size: 1024 tokens on eight waves while that still gives every compute unit a
-// workgroup, else 512 on four; records over 96 bytes in all halve both (LDS).
+// workgroup (and always with a fused append), else 512 on four; records over 96 bytes in
+// all halve both (LDS).
 template <int NT>
 static aatc_status launch_mfma_nt(const DecodeArgs& a, int batch, hipStream_t st) {
   const bool big = a.rk + a.rv > 96;
+  if (a.x_k) return big ? launch_mfma_np<NT, 4, 8, true>(a, batch, st)
+                        : launch_mfma_np<NT, 8, 8, true>(a, batch, st);
   const int64_t rows = (int64_t)batch * a.n_kv_heads;
   const int64_t wide = rows * ((a.cap + (big ? 511 : 1023)) / (big ? 512 : 1024));
-  if (wide >= 256) return big ? launch_mfma_np<NT, 4, 8>(a, batch, st) : launch_mfma_np<NT, 8, 8>(a, batch, st);
-  return big ? launch_mfma_np<NT, 4, 4>(a, batch, st) : launch_mfma_np<NT, 8, 4>(a, batch, st);
+  if (wide >= 256) return big ? launch_mfma_np<NT, 4, 8, false>(a, batch, st)
+                              : launch_mfma_np<NT, 8, 8, false>(a, batch, st);
+  return big ? launch_mfma_np<NT, 4, 4, false>(a, batch, st)
+             : launch_mfma_np<NT, 8, 4, false>(a, batch, st);
 }
 
 aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
@@ -982,7 +1086,7 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
                           const void* k_codes, const uint16_t* k_alpha, const void* v_codes,
                           const uint16_t* v_alpha, const int32_t* seq_len, int64_t cap,
                           int rk, int rv, float softmax_scale, float* out, void* workspace,
-                          void* stream) {
+                          void* stream, const void* x_k, const void* x_v, aatc_dtype x_dtype) {
   const int G = n_q_heads / n_kv_heads;
   const WsLayout wl = ws_layout(batch, n_q_heads, n_kv_heads, cap);
   char* ws = static_cast<char*>(workspace);
@@ -998,11 +1102,14 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
     a.params_k = params_k;
     a.params_v = params_v;
     a.q = q;
-    a.k_codes = static_cast<const uint8_t*>(k_codes);
-    a.k_alpha = k_alpha;
-    a.v_codes = static_cast<const uint8_t*>(v_codes);
-    a.v_alpha = v_alpha;
+    a.k_codes = static_cast<uint8_t*>(const_cast<void*>(k_codes));
+    a.k_alpha = const_cast<uint16_t*>(k_alpha);
+    a.v_codes = static_cast<uint8_t*>(const_cast<void*>(v_codes));
+    a.v_alpha = const_cast<uint16_t*>(v_alpha);
     a.seq_len = seq_len;
+    a.x_k = x_k;
+    a.x_v = x_v;
+    a.x_dtype = (int)x_dtype;
     a.out = out;
     a.counters = ctr;
     a.partials = parts;
@@ -1015,6 +1122,16 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
     a.rv = rv;
     a.scale_log2e = softmax_scale * kLog2e;
     return G <= 4 ? launch_mfma_nt<1>(a, batch, st) : launch_mfma_nt<2>(a, batch, st);
+  }
+  if (x_k) {                // generic path: append with the per-token encode kernel first
+    aatc_status e = launch_encode_last(params_k, n_kv_heads, batch, x_k, x_dtype,
+                                       AATC_LAYOUT_RECORDS, const_cast<void*>(k_codes),
+                                       const_cast<uint16_t*>(k_alpha), cap, rk, seq_len, stream);
+    if (e == AATC_OK)
+      e = launch_encode_last(params_v, n_kv_heads, batch, x_v, x_dtype, AATC_LAYOUT_TILES,
+                             const_cast<void*>(v_codes), const_cast<uint16_t*>(v_alpha), cap, rv,
+                             seq_len, stream);
+    if (e != AATC_OK) return e;
   }
   const int n_splits = (int)((cap + kSplit - 1) / kSplit);
   size_t lds = std::max((size_t)G * (kSplit + kMaxBudget) * sizeof(float), merge_lds_bytes(G, kThreads));

@@ -5,6 +5,7 @@
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include "encode_core.h"
 #include "launch.h"
 #include "params.h"
 
@@ -15,30 +16,10 @@ constexpr int kEncThreads = 256;                 // two tokens in flight, 128 la
 constexpr int kRecWords = kMaxBudget / 32;       // words of the largest record
 constexpr int kSmallBatch = 16;                  // appends up to this many tokens: per-token kernel
 
-__device__ inline float load_elem(const void* x, int dtype, int64_t idx) {
-  if (dtype == AATC_BF16) {
-    uint32_t b = static_cast<const uint16_t*>(x)[idx];
-    return __uint_as_float(b << 16);
-  }
-  return static_cast<const float*>(x)[idx];
-}
-
 __device__ inline float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
   return v;
-}
-
-// Quantize one transformed coefficient (canonical fp32 sequence); returns the b-bit two's
-// complement pattern of the code.
-__device__ inline uint32_t quantize_code(float r, float inv_a, int b) {
-  float y = r * inv_a;
-  float xq = ldexpf(y, b - 1);
-  float f = floorf(xq);
-  int code = (int)f + ((xq - f) >= 0.5f ? 1 : 0);
-  const int half = 1 << (b - 1);
-  code = min(max(code, -half), half - 1);
-  return (uint32_t)code & ((1u << b) - 1u);
 }
 
 __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
@@ -81,25 +62,20 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
     if ((tid & 63) == 0) red_x[wave] = m;
     __syncthreads();
     m = fmaxf(red_x[2 * slot], red_x[2 * slot + 1]);
-    int e = 0;
-    frexpf(m, &e);                                  // m = f * 2^e, f in [0.5, 1)
-    const int shift = (m > 0.f) ? (kXLead - (e - 1)) : 0;
+    const int shift = token_shift(m);
     xs[slot][c] = (int)rintf(ldexpf(xv, shift));
     __syncthreads();
     // Exact integer transform h_c = sum_j X_j Tq_jc (|sum| < 2^36).
     long long acc = 0;
 #pragma unroll 8
     for (int j = 0; j < kD; ++j) acc += (long long)xs[slot][j] * (long long)tq[j * kD + c];
-    const float h = (float)ldexp((double)acc, -(shift + kTFrac));
-    const float r = h * inv_s;
+    const float r = fixed_point_result(acc, shift) * inv_s;
     float a = wave_max(b > 0 ? fabsf(r) : 0.f);
     if ((tid & 63) == 0) red_a[wave] = a;
     __syncthreads();
     a = fmaxf(red_a[2 * slot], red_a[2 * slot + 1]);
-    const __half a16 = __float2half_rn(fminf(a, 65504.f));
-    const float a32 = __half2float(a16);
-    // fp32 1/alpha correctly rounded (11-bit divisor: no double-rounding error).
-    const float inv_a = (a32 > 0.f) ? (float)(1.0 / (double)a32) : 0.f;
+    const __half a16 = token_alpha(a);
+    const float inv_a = inverse_alpha(a16);
     if (valid && b > 0) {
       const uint32_t u = quantize_code(r, inv_a, b);
       const int li = (int)(t - tile_base);
@@ -142,16 +118,26 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
 // of j and the transposed fixed-point transform read straight from global memory.
 // Tile bits are set and cleared with device atomics, so tokens that share a tile word
 // may be encoded by different workgroups.
+// With `seq_len` set, block x is a sequence instead: it encodes token seq_len[b] - 1 of
+// sequence b (nothing for an empty sequence) into caches `codes_bstride` bytes and
+// `alpha_bstride` scales apart.
 __global__ __launch_bounds__(kEncThreads) void encode_token_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t x_stride,
     int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha, int64_t cap,
-    int64_t pos) {
+    int64_t pos, const int32_t* __restrict__ seq_len, int64_t codes_bstride,
+    int64_t alpha_bstride) {
   __shared__ __align__(16) int xs[kD];
   __shared__ long long part[kD];
   __shared__ uint32_t rec[kRecWords];
   __shared__ float red_x[4], red_a[4];
 
-  const int64_t t = pos + blockIdx.x;
+  int64_t t = pos + blockIdx.x;
+  if (seq_len) {
+    t = min<int64_t>(max(seq_len[blockIdx.x], 0), cap) - 1;
+    if (t < 0) return;
+    codes += blockIdx.x * codes_bstride;
+    alpha += blockIdx.x * alpha_bstride;
+  }
   const int head = blockIdx.y;
   const HeadParams* hp = head_params(params, head);
   const int tid = threadIdx.x, c = tid & (kD - 1), half = tid >> 7, wave = tid >> 6;
@@ -173,9 +159,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_token_kernel(
   if ((tid & 63) == 0) red_x[wave] = m;
   __syncthreads();
   m = fmaxf(red_x[0], red_x[1]);
-  int e = 0;
-  frexpf(m, &e);
-  const int shift = (m > 0.f) ? (kXLead - (e - 1)) : 0;
+  const int shift = token_shift(m);
   if (tid < kD) xs[tid] = (int)rintf(ldexpf(xv, shift));
   __syncthreads();
   // Exact integer transform h_c = sum_j X_j Tq_jc.
@@ -197,16 +181,14 @@ __global__ __launch_bounds__(kEncThreads) void encode_token_kernel(
   float r = 0.f;
   if (!half) {
     acc += part[c];
-    const float h = (float)ldexp((double)acc, -(shift + kTFrac));
-    r = h * inv_s;
+    r = fixed_point_result(acc, shift) * inv_s;
   }
   float a = wave_max((!half && b > 0) ? fabsf(r) : 0.f);
   if ((tid & 63) == 0) red_a[wave] = a;
   __syncthreads();
   a = fmaxf(red_a[0], red_a[1]);
-  const __half a16 = __float2half_rn(fminf(a, 65504.f));
-  const float a32 = __half2float(a16);
-  const float inv_a = (a32 > 0.f) ? (float)(1.0 / (double)a32) : 0.f;
+  const __half a16 = token_alpha(a);
+  const float inv_a = inverse_alpha(a16);
   if (!half && b > 0) {
     const uint32_t u = quantize_code(r, inv_a, b);
     atomicOr(&rec[off >> 5], u << (off & 31));
@@ -219,11 +201,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_token_kernel(
     uint32_t* out = reinterpret_cast<uint32_t*>(codes + ((int64_t)head * cap + t) * rbytes);
     for (int i = tid; i < rbytes / 4; i += kEncThreads) out[i] = rec[i];
   } else {
-    // Token p = 16 d + 4 g + i of its tile: bit 8 i + 2 g + d % 2 of word 2 v + d / 2.
-    const int p = (int)(t % kTile), d = p >> 4;
-    const uint32_t bit = 1u << (8 * (p & 3) + 2 * ((p >> 2) & 3) + (d & 1));
+    const int p = (int)(t % kTile);
+    const uint32_t bit = 1u << tile_bit(p);
     uint32_t* tw = reinterpret_cast<uint32_t*>(codes) +
-                   ((int64_t)head * (cap / kTile) + t / kTile) * (16 * rbytes) + (d >> 1);
+                   ((int64_t)head * (cap / kTile) + t / kTile) * (16 * rbytes) + tile_word(p);
     for (int v = tid; v < 8 * rbytes; v += kEncThreads) {
       if ((rec[v >> 5] >> (v & 31)) & 1u)
         __hip_atomic_fetch_or(tw + 2 * v, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -242,7 +223,8 @@ aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_d
   if (n_tok <= kSmallBatch) {
     hipLaunchKernelGGL(encode_token_kernel, dim3((unsigned)n_tok, (unsigned)n_heads),
                        dim3(kEncThreads), 0, (hipStream_t)stream, params, x, (int)x_dtype,
-                       x_tok_stride, (int)layout, static_cast<uint8_t*>(codes), alpha, cap, pos);
+                       x_tok_stride, (int)layout, static_cast<uint8_t*>(codes), alpha, cap, pos,
+                       nullptr, (int64_t)0, (int64_t)0);
     return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
   }
   const int64_t first = pos / kTile, last = (pos + n_tok - 1) / kTile;
@@ -250,6 +232,18 @@ aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_d
   hipLaunchKernelGGL(encode_exact_kernel, grid, dim3(kEncThreads), 0, (hipStream_t)stream,
                      params, x, (int)x_dtype, n_tok, x_tok_stride, (int)layout,
                      static_cast<uint8_t*>(codes), alpha, cap, pos);
+  return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
+}
+
+aatc_status launch_encode_last(const void* params, int n_heads, int batch, const void* x,
+                               aatc_dtype x_dtype, aatc_layout layout, void* codes,
+                               uint16_t* alpha, int64_t cap, int record_bytes,
+                               const int32_t* seq_len, void* stream) {
+  hipLaunchKernelGGL(encode_token_kernel, dim3((unsigned)batch, (unsigned)n_heads),
+                     dim3(kEncThreads), 0, (hipStream_t)stream, params, x, (int)x_dtype,
+                     (int64_t)n_heads * kD, (int)layout, static_cast<uint8_t*>(codes), alpha,
+                     cap, (int64_t)0, seq_len, (int64_t)n_heads * cap * record_bytes,
+                     (int64_t)n_heads * cap);
   return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
 }
 

@@ -18,6 +18,12 @@ aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_d
                           void* codes, uint16_t* alpha, int64_t cap, int64_t pos,
                           void* stream);
 
+// Encodes token seq_len[b] - 1 of every sequence b (caches [batch][n_heads][cap] ...).
+aatc_status launch_encode_last(const void* params, int n_heads, int batch, const void* x,
+                               aatc_dtype x_dtype, aatc_layout layout, void* codes,
+                               uint16_t* alpha, int64_t cap, int record_bytes,
+                               const int32_t* seq_len, void* stream);
+
 size_t decode_workspace_bytes(int batch, int n_q_heads, int n_kv_heads, int64_t cap);
 
 aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
@@ -25,6 +31,8 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
                           const void* k_codes, const uint16_t* k_alpha, const void* v_codes,
                           const uint16_t* v_alpha, const int32_t* seq_len, int64_t cap,
                           int k_record_bytes, int v_record_bytes, float softmax_scale,
-                          float* out, void* workspace, void* stream);
+                          float* out, void* workspace, void* stream,
+                          const void* x_k = nullptr, const void* x_v = nullptr,
+                          aatc_dtype x_dtype = AATC_BF16);
 
 }  // namespace aatc

@@ -206,3 +206,65 @@ def test_end_to_end_with_host_calibration():
     out, _ = _decode(case, pk, pv, kc, ka, vc, va)
     ref = _oracle_decode(case)
     assert rel_l2(out[0], ref[0]) <= TOL
+
+
+APPEND_CASES = {
+    # new token first in a 1024-token split, last in a split, mid-tile, alone, no token
+    "cfg2_split_edges": dict(cfg=2, n_tokens=1025, batch=5, lens=[1025, 1024, 700, 1, 0]),
+    "cfg3_gqa7_ragged": dict(cfg=3, n_tokens=600, batch=2, lens=[600, 129]),
+    "cfg4_4bit_wide_records": dict(cfg=4, n_tokens=200, avg_bits=4.0),
+    "generic_gqa16": dict(cfg=2, n_tokens=300, n_q_heads=32, n_kv_heads=2),
+}
+
+
+@pytest.mark.parametrize("name", list(APPEND_CASES))
+def test_append_decode_matches_encode_then_decode(name):
+    """One aatc_append_decode_attention call gives the codes of encoding the new token and
+    the outputs of decoding the updated cache (oracle and separate calls)."""
+    _log(f"[append] {name}")
+    case = Case(**APPEND_CASES[name])
+    w = case.w
+    B, H, HQ, cap = w.batch, w.n_kv_heads, w.n_q_heads, case.cap
+    rk, rv = case.cal_k[0].record_bytes, case.cal_v[0].record_bytes
+    pk, pv, _, _, _, _ = _gpu_caches(case)
+    kc = record_cache(H, cap, rk, batch=B).fill_(0xA5)       # stale bytes everywhere
+    vc = tile_cache(H, cap, rv, batch=B).fill_(0x5A)
+    ka, va = alpha_cache(H, cap, batch=B), alpha_cache(H, cap, batch=B)
+    xk_new = torch.zeros((B, H, 128), dtype=torch.bfloat16 if w.dtype == "bf16" else torch.float32)
+    xv_new = torch.zeros_like(xk_new)
+    for b in range(B):
+        n = case.lens[b]
+        if n == 0:
+            continue
+        xk, xv = case.x_tokens(b, "k"), case.x_tokens(b, "v")
+        if n > 1:
+            P.aatc_encode(pk, H, xk, n - 1, H * 128, P.LAYOUT_RECORDS, kc[b], ka[b], cap, 0)
+            P.aatc_encode(pv, H, xv, n - 1, H * 128, P.LAYOUT_TILES, vc[b], va[b], cap, 0)
+        xk_new[b], xv_new[b] = xk[n - 1].cpu(), xv[n - 1].cpu()
+    q = stored_to_torch(np.stack(case.q)).cuda()
+    lens = torch.tensor(case.lens, dtype=torch.int32, device="cuda")
+    out = torch.full((B, HQ, 128), float("nan"), dtype=torch.float32, device="cuda")
+    ws = torch.zeros(P.aatc_decode_workspace_bytes(B, HQ, H, cap), dtype=torch.uint8,
+                     device="cuda")
+    P.aatc_append_decode_attention(pk, pv, B, HQ, H, q, xk_new.cuda(), xv_new.cuda(), kc, ka,
+                                   vc, va, lens, cap, rk, rv, 1 / np.sqrt(128), out, ws)
+    torch.cuda.synchronize()
+    for b in range(B):
+        n = case.lens[b]
+        for h in range(H):
+            ok_, oa = case.oracle_encode(b, h, "k")
+            ov_, ova = case.oracle_encode(b, h, "v")
+            np.testing.assert_array_equal(kc[b, h, :n].cpu().numpy(), ok_)
+            np.testing.assert_array_equal(ka[b, h, :n].cpu().numpy().view(np.uint16), oa.view(np.uint16))
+            got_v = ora.tiles_to_records(vc[b, h].cpu().numpy(), rv)[:n]
+            np.testing.assert_array_equal(got_v, ov_)
+            np.testing.assert_array_equal(va[b, h, :n].cpu().numpy().view(np.uint16), ova.view(np.uint16))
+    got = out.cpu().numpy()
+    ref = _oracle_decode(case)
+    sep, _ = _decode(case, pk, pv, kc, ka, vc, va)
+    for b in range(B):
+        if case.lens[b] == 0:
+            assert np.all(got[b] == 0)
+            continue
+        assert rel_l2(got[b], ref[b]) <= TOL, (b, case.lens[b], rel_l2(got[b], ref[b]))
+        assert rel_l2(got[b], sep[b]) <= 1e-5, (b, case.lens[b])

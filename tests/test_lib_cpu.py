@@ -19,7 +19,8 @@ HEADER = os.path.join(ROOT, "include", "aatc.h")
 def test_library_exports_every_declared_symbol():
     from paper_2608_14191_amd._lib import exported_symbols_declared_in_header
     names = exported_symbols_declared_in_header(HEADER)
-    assert {"aatc_calibrate", "aatc_encode", "aatc_decode_attention"} <= set(names)
+    assert {"aatc_calibrate", "aatc_encode", "aatc_decode_attention",
+            "aatc_append_decode_attention"} <= set(names)
     lib = P.library()
     for n in names:
         assert hasattr(lib, n), n
@@ -157,3 +158,23 @@ def test_encode_and_decode_validate_before_launch():
     assert L.aatc_decode_attention(*bad) == 5
     bad = list(args); bad[5] = 64
     assert L.aatc_decode_attention(*bad) == 2
+
+
+def test_append_decode_validates_before_launch():
+    """The fused append + decode entry point checks the decode arguments and the new
+    tokens on the host."""
+    L = P.library()
+    p = _fake()
+    ws = P.aatc_decode_workspace_bytes(1, 32, 8, 4096)
+    args = [p, p, 1, 32, 8, 128, p, 1, p, p, 1, p, p, p, p, p, 4096, 44, 44, 0.088, p, p, ws,
+            None]
+    bad = list(args); bad[8] = None                  # no new keys
+    assert L.aatc_append_decode_attention(*bad) == 1
+    bad = list(args); bad[10] = 2                    # f16 tokens are not accepted
+    assert L.aatc_append_decode_attention(*bad) == 1
+    bad = list(args); bad[9] = _fake(4097)           # misaligned bf16 values
+    assert L.aatc_append_decode_attention(*bad) == 1
+    bad = list(args); bad[16] = 100                  # cap not a multiple of 64
+    assert L.aatc_append_decode_attention(*bad) == 1
+    bad = list(args); bad[22] = ws - 1               # workspace too small
+    assert L.aatc_append_decode_attention(*bad) == 5
