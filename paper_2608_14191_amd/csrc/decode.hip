@@ -37,6 +37,7 @@ constexpr int kCoherent = 16;                    // cache policy sc1: device-coh
 constexpr int kMergeU = 8;                       // split partials in flight per merging thread
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(1))) uint32_t* gdword;   // global-memory dword
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v2f __attribute__((ext_vector_type(2)));
 
@@ -194,20 +195,67 @@ constexpr size_t merge_lds_bytes(int G, int NTHR) {
   return (size_t)(6 * NTHR + G * kD + (NTHR / 32) * G * kD) * sizeof(float);
 }
 
+// Inverse transform o = T_V o~ of G vectors with NTHR threads: thread (j4, cb) holds T_V
+// rows 4 j4 .. 4 j4 + 3 at columns CW cb .. CW cb + CW - 1 (CW = 4096 / NTHR).
+template <int NTHR>
+struct TvBlock {
+  static constexpr int NCB = NTHR / 32, CW = kD / NCB;
+  v4f t[4][CW / 4];
+  __device__ void load(const HeadParams* hv) {
+    const int j4 = threadIdx.x & 31, cb = threadIdx.x >> 5;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+      for (int k = 0; k < CW / 4; ++k)
+        t[jj][k] = reinterpret_cast<const v4f*>(hv->T)[(4 * j4 + jj) * (kD / 4) + (CW / 4) * cb + k];
+  }
+  // osum: LDS [G][kD] input; ored: LDS [NCB][G][kD] scratch.  Calls sink(h, j, o_hj) once
+  // per output, after a barrier; the caller synchronizes before osum is reused.
+  template <class Sink>
+  __device__ void apply(const float* osum, float* ored, int G, Sink sink) const {
+    const int tid = threadIdx.x, j4 = tid & 31, cb = tid >> 5;
+    for (int h = 0; h < G; ++h) {
+      const v4f* oh = reinterpret_cast<const v4f*>(osum + h * kD) + (CW / 4) * cb;
+      v4f ov4[CW / 4];
+#pragma unroll
+      for (int k = 0; k < CW / 4; ++k) ov4[k] = oh[k];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        v4f p = t[jj][0] * ov4[0];
+#pragma unroll
+        for (int k = 1; k < CW / 4; ++k) p += t[jj][k] * ov4[k];
+        ored[(cb * G + h) * kD + 4 * j4 + jj] = p.x + p.y + p.z + p.w;
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < G * kD; i += NTHR) {
+      const int h = i / kD, j = i % kD;
+      float acc = 0.f;
+#pragma unroll
+      for (int b = 0; b < NCB; ++b) acc += ored[(b * G + h) * kD + j];
+      sink(h, j, acc);
+    }
+  }
+};
+
 // Called by every workgroup after it stored its partial with device-coherent stores.
 // The last workgroup of the (sequence, KV head) `row` to arrive merges the split
-// partials of its G query heads, applies o = T_V o~ / l and resets the arrival counter.
-// A NaN split maximum (records that do not match the parameters) makes the output NaN.
-template <int NTHR>
+// partials of its G query heads into o = sum / l and resets the arrival counter; with TV
+// the partials are in the transformed domain and it applies T_V as well.  A NaN split
+// maximum (records that do not match the parameters) makes the output NaN.
+template <int NTHR, bool TV>
 __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int64_t row, int G,
                                               int n_splits, const Partial* partials,
                                               unsigned* counters, float* out_rows, float* lds) {
   constexpr int NCB = NTHR / 32;          // column blocks of the T_V product
-  constexpr int CW = kD / NCB;            // columns per block
   __shared__ unsigned last_s;
   const int tid = threadIdx.x;
   __builtin_amdgcn_s_waitcnt(0);          // this thread's partial stores have completed
   __syncthreads();
+  // Every workgroup fetches T_V alongside its arrival count; only the last one uses it.
+  const HeadParams* hv = head_params(params_v, kvh);
+  TvBlock<NTHR> tv;
+  if (TV) tv.load(hv);
   if (tid == 0) {
     const unsigned prev = __hip_atomic_fetch_add(&counters[row], 1u, __ATOMIC_RELAXED,
                                                  __HIP_MEMORY_SCOPE_AGENT);
@@ -215,18 +263,6 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
   }
   __syncthreads();
   if (!last_s) return;
-
-  // (a) T_V rows 4 j4 .. 4 j4 + 3 at columns CW cb .. CW cb + CW - 1 per thread, in
-  //     flight together with the partials.
-  const HeadParams* hv = head_params(params_v, kvh);
-  const int j4 = tid & 31, cb = tid >> 5;
-  v4f tv[4][CW / 4];
-#pragma unroll
-  for (int jj = 0; jj < 4; ++jj)
-#pragma unroll
-    for (int k = 0; k < CW / 4; ++k)
-      tv[jj][k] = reinterpret_cast<const v4f*>(hv->T)[(4 * j4 + jj) * (kD / 4) + (CW / 4) * cb + k];
-
   float* cm = lds;                                         // [NTHR] group maxima
   float* cl = cm + NTHR;                                   // [NTHR] group sums
   v4f* cacc = reinterpret_cast<v4f*>(cl + NTHR);           // [NTHR]
@@ -235,39 +271,39 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
   const __amdgpu_buffer_rsrc_t prs =
       make_rsrc(partials + row * n_splits * G, (uint32_t)(n_splits * G * sizeof(Partial)));
 
-  // (b) Online merge over the splits: slot (head, float4 column) per thread; groups of
-  //     threads take interleaved splits and combine at the end.
+  // (a) Online merge over the splits: slot (head, float4 column) per thread; groups of
+  //     threads take interleaved splits and combine at the end.  T_V is fetched right
+  //     after the first batch of partials (loads complete in order).
   const int slots = G * (kD / 4);
   for (int base = 0; base < slots; base += NTHR) {
     const int width = min(slots - base, NTHR);
     const int ngroups = NTHR / width;
     const int slot = base + tid % width, grp = tid / width;
     const int h = slot >> 5, c4 = slot & 31;
+    const bool active = grp < ngroups;
     float M = -INFINITY, Ls = 0.f;
     v4f acc = {0.f, 0.f, 0.f, 0.f};
     bool bad = false;
-    if (grp < ngroups) {
-      for (int s0 = grp; s0 < n_splits; s0 += kMergeU * ngroups) {
-        v2f hd[kMergeU];
-        v4f ov[kMergeU];
+    for (int s0 = grp; s0 < n_splits || s0 == grp; s0 += kMergeU * ngroups) {
+      v2f hd[kMergeU];
+      v4f ov[kMergeU];
 #pragma unroll
-        for (int u = 0; u < kMergeU; ++u) {        // past the last split the loads read 0
-          const uint32_t off = (uint32_t)(((s0 + u * ngroups) * G + h) * sizeof(Partial));
-          hd[u] = buf_load8_coherent(prs, off);
-          ov[u] = (v4f)__builtin_amdgcn_raw_buffer_load_b128(prs, (int)(off + 16 + 16 * c4), 0,
-                                                            kCoherent);
-        }
+      for (int u = 0; u < kMergeU; ++u) {        // past the last split the loads read 0
+        const uint32_t off = (uint32_t)(((s0 + u * ngroups) * G + h) * sizeof(Partial));
+        hd[u] = buf_load8_coherent(prs, off);
+        ov[u] = (v4f)__builtin_amdgcn_raw_buffer_load_b128(prs, (int)(off + 16 + 16 * c4), 0,
+                                                          kCoherent);
+      }
 #pragma unroll
-        for (int u = 0; u < kMergeU; ++u) {
-          const float ms = (s0 + u * ngroups < n_splits) ? hd[u].x : -INFINITY;
-          bad |= (ms != ms);
-          if (ms > -INFINITY) {
-            const float mn = fmaxf(M, ms);
-            const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
-            acc = acc * sa + ov[u] * sb;
-            Ls = Ls * sa + hd[u].y * sb;
-            M = mn;
-          }
+      for (int u = 0; u < kMergeU; ++u) {
+        const float ms = (active && s0 + u * ngroups < n_splits) ? hd[u].x : -INFINITY;
+        bad |= (ms != ms);
+        if (ms > -INFINITY) {
+          const float mn = fmaxf(M, ms);
+          const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
+          acc = acc * sa + ov[u] * sb;
+          Ls = Ls * sa + hd[u].y * sb;
+          M = mn;
         }
       }
     }
@@ -296,28 +332,11 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
     }
     __syncthreads();
   }
-  // (c) o_j = sum_c T_V[j][c] o~_c: partial sums over this thread's columns, then over
-  //     the column blocks.
-  for (int h = 0; h < G; ++h) {
-    const v4f* oh = reinterpret_cast<const v4f*>(osum + h * kD) + (CW / 4) * cb;
-    v4f ov4[CW / 4];
-#pragma unroll
-    for (int k = 0; k < CW / 4; ++k) ov4[k] = oh[k];
-#pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      v4f p = tv[jj][0] * ov4[0];
-#pragma unroll
-      for (int k = 1; k < CW / 4; ++k) p += tv[jj][k] * ov4[k];
-      ored[(cb * G + h) * kD + 4 * j4 + jj] = p.x + p.y + p.z + p.w;
-    }
-  }
-  __syncthreads();
-  for (int i = tid; i < G * kD; i += NTHR) {
-    const int h = i / kD, j = i % kD;
-    float acc = 0.f;
-#pragma unroll
-    for (int b = 0; b < NCB; ++b) acc += ored[(b * G + h) * kD + j];
-    out_rows[(int64_t)h * kD + j] = acc;
+  // (b) o = T_V o~ (transformed-domain partials), or o~ itself.
+  if constexpr (TV) {
+    tv.apply(osum, ored, G, [&](int h, int j, float o) { out_rows[(int64_t)h * kD + j] = o; });
+  } else {
+    for (int i = tid; i < G * kD; i += NTHR) out_rows[i] = osum[i];
   }
   if (tid == 0) counters[row] = 0u;
 }
@@ -472,7 +491,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
     st_dev(&part[tid].m, !layout_ok ? NAN : (nt > 0) ? mh[tid] : -INFINITY);
     st_dev(&part[tid].l, !layout_ok ? NAN : (nt > 0) ? lh[tid] : 0.f);
   }
-  merge_if_last<kThreads>(params_v, kvh, kv_row, G, n_splits, partials, counters,
+  merge_if_last<kThreads, true>(params_v, kvh, kv_row, G, n_splits, partials, counters,
                           out + ((int64_t)seq * n_q_heads + kvh * G) * kD, dyn);
 }
 
@@ -561,7 +580,6 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   }
   // Queries, element r NTHR + tid, read as the aligned dword that holds the element
   // (either type, no branch; the dword never leaves the element's page).
-  typedef const __attribute__((address_space(1))) uint32_t* gdword;
   const bool q_bf = a.q_dtype == AATC_BF16;
   uint32_t qraw[NR];
   bool qhi[NR];
@@ -582,6 +600,31 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   const int len = (int)min<int64_t>(max(a.seq_len[seq], 0), a.cap);
   const int nt = max(0, min(S, len - t0));
 
+  // Fused append: the workgroup whose split holds token len - 1 encodes it (K with
+  // threads 0..255, V with 256..511; two halves of j per channel), exactly as the encode
+  // kernels do, and patches its copy of the cache.  Its loads go out before the
+  // cache's, so they do not queue behind the cache stream.
+  const int p_loc = len - 1 - t0;
+  const bool is_app = APPEND && len > 0 && p_loc < S;          // p_loc >= 0 follows from nt > 0
+  const int et = tid >> 8, ec = tid & (kD - 1), ejp = (tid >> 7) & 1;
+  uint4 etq[8];
+  uint32_t exraw = 0u;                 // the token element's dword, converted at first use
+  bool exhi = false;
+  float e_inv_s = 0.f;
+  if constexpr (APPEND) {
+    if (is_app && nt > 0) {
+      const HeadParams* eh = et ? hv : hk;
+      const uint4* trow = reinterpret_cast<const uint4*>(eh->Tqt + ec * kD + 64 * ejp);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) etq[k] = trow[k];
+      e_inv_s = eh->inv_s[ec];
+      const int64_t i = ((int64_t)seq * a.n_kv_heads + kvh) * kD + ec;
+      const uintptr_t ad = reinterpret_cast<uintptr_t>(et ? a.x_v : a.x_k) +
+                           (a.x_dtype == AATC_BF16 ? 2 * i : 4 * i);
+      exraw = *reinterpret_cast<gdword>(ad & ~(uintptr_t)3);
+      exhi = (ad & 2) != 0;
+    }
+  }
   // (1) This split's packed cache, into registers (loads past the capacity read 0).  The
   //     layout check below gates the compute, not these loads.
   const int n_load = min(S, (nt + kTile - 1) / kTile * kTile);
@@ -606,26 +649,6 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     rak = buf_load16<0>(make_rsrc(a.k_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
     rav = buf_load16<0>(make_rsrc(a.v_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
   }
-  // Fused append: the workgroup whose split holds token len - 1 encodes it (K with
-  // threads 0..255, V with 256..511; two halves of j per channel), exactly as the encode
-  // kernels do, and patches its copy of the cache.  Its loads go out here.
-  const int p_loc = len - 1 - t0;
-  const bool is_app = APPEND && len > 0 && p_loc < S;          // p_loc >= 0 follows from nt > 0
-  const int et = tid >> 8, ec = tid & (kD - 1), ejp = (tid >> 7) & 1;
-  uint4 etq[8];
-  float ex = 0.f, e_inv_s = 0.f;
-  if constexpr (APPEND) {
-    if (is_app && nt > 0) {
-      const HeadParams* eh = et ? hv : hk;
-      const uint4* trow = reinterpret_cast<const uint4*>(eh->Tqt + ec * kD + 64 * ejp);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) etq[k] = trow[k];
-      e_inv_s = eh->inv_s[ec];
-      if (!ejp)
-        ex = load_elem(et ? a.x_v : a.x_k, a.x_dtype,
-                       ((int64_t)seq * a.n_kv_heads + kvh) * kD + ec);
-    }
-  }
   // Keep the compiler from moving work that waits on the early loads above the cache loads.
   __builtin_amdgcn_sched_barrier(0);
   // No branch on the split's contents: an empty split computes on masked tokens and
@@ -644,6 +667,56 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     qs[r * NTHR + tid] = ((r * NTHR + tid) / kD < G) ? qv : 0.f;
   }
   __syncthreads();                                   // qs, qmx
+
+  // (1b) Fused append: encode the new token of both tensors into LDS records (first,
+  //      so that it overlaps the cache still landing).
+  __shared__ int exs[2][kD];
+  __shared__ long long epart[2][kD];
+  __shared__ uint32_t erec[2][kMaxBudget / 32];
+  __shared__ float ered[8];
+  __shared__ uint16_t ea16[2];
+  if constexpr (APPEND) {
+    if (is_app && nt > 0) {
+      if (tid < 2 * (kMaxBudget / 32)) (&erec[0][0])[tid] = 0u;
+      const int eb = et ? vbc : kb, eoff = et ? voc : koff;
+      const float ex = ejp ? 0.f
+                           : (a.x_dtype == AATC_BF16
+                                  ? __uint_as_float((exhi ? (exraw >> 16) : (exraw & 0xffffu)) << 16)
+                                  : __uint_as_float(exraw));
+      float m = wave_max(fabsf(ex));
+      if (lane == 0) ered[wave] = m;
+      __syncthreads();
+      const int shift = token_shift(fmaxf(ered[4 * et], ered[4 * et + 1]));
+      if (!ejp) exs[et][ec] = (int)rintf(ldexpf(ex, shift));
+      __syncthreads();
+      long long acc = 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int* xr = &exs[et][64 * ejp + 8 * k];
+        const uint32_t tw[4] = {etq[k].x, etq[k].y, etq[k].z, etq[k].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          acc += (long long)xr[2 * i] * (long long)(int16_t)(tw[i] & 0xffffu);
+          acc += (long long)xr[2 * i + 1] * (long long)(int16_t)(tw[i] >> 16);
+        }
+      }
+      if (ejp) epart[et][ec] = acc;
+      __syncthreads();
+      float r = 0.f;
+      if (!ejp) r = fixed_point_result(acc + epart[et][ec], shift) * e_inv_s;
+      const float am = wave_max((!ejp && eb > 0) ? fabsf(r) : 0.f);
+      if (lane == 0) ered[wave] = am;
+      __syncthreads();
+      const __half a16 = token_alpha(fmaxf(ered[4 * et], ered[4 * et + 1]));
+      const float inv_a = inverse_alpha(a16);
+      if (!ejp && eb > 0) {
+        const uint32_t u = quantize_code(r, inv_a, eb);
+        atomicOr(&erec[et][eoff >> 5], u << (eoff & 31));
+        if ((eoff & 31) + eb > 32) atomicOr(&erec[et][(eoff >> 5) + 1], u >> (32 - (eoff & 31)));
+      }
+      if (ec == 0 && !ejp) ea16[et] = __half_as_ushort(a16);
+    }
+  }
 
   // (2) q~ = T_K^T q: RJ-row partial sums per thread, then over the NJQ row blocks.
   float* scr = reinterpret_cast<float*>(smem);       // [NJQ][NH][kD]
@@ -737,51 +810,6 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     for (int s = 0; s < 2 * NP; ++s)
       bq[rt][s] = *reinterpret_cast<const v4i*>(ql + ((L * NH + h) * 2 * NP + s) * 64 + 16 * g);
     fex[rt] = fexp_s[h];
-  }
-
-  // (2b) Fused append: encode the new token of both tensors into LDS records.
-  __shared__ int exs[2][kD];
-  __shared__ long long epart[2][kD];
-  __shared__ uint32_t erec[2][kMaxBudget / 32];
-  __shared__ float ered[8];
-  __shared__ uint16_t ea16[2];
-  if constexpr (APPEND) {
-    if (is_app && nt > 0) {
-      if (tid < 2 * (kMaxBudget / 32)) (&erec[0][0])[tid] = 0u;
-      const int eb = et ? vbc : kb, eoff = et ? voc : koff;
-      float m = wave_max(fabsf(ex));
-      if (lane == 0) ered[wave] = m;
-      __syncthreads();
-      const int shift = token_shift(fmaxf(ered[4 * et], ered[4 * et + 1]));
-      if (!ejp) exs[et][ec] = (int)rintf(ldexpf(ex, shift));
-      __syncthreads();
-      long long acc = 0;
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int* xr = &exs[et][64 * ejp + 8 * k];
-        const uint32_t tw[4] = {etq[k].x, etq[k].y, etq[k].z, etq[k].w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          acc += (long long)xr[2 * i] * (long long)(int16_t)(tw[i] & 0xffffu);
-          acc += (long long)xr[2 * i + 1] * (long long)(int16_t)(tw[i] >> 16);
-        }
-      }
-      if (ejp) epart[et][ec] = acc;
-      __syncthreads();
-      float r = 0.f;
-      if (!ejp) r = fixed_point_result(acc + epart[et][ec], shift) * e_inv_s;
-      const float am = wave_max((!ejp && eb > 0) ? fabsf(r) : 0.f);
-      if (lane == 0) ered[wave] = am;
-      __syncthreads();
-      const __half a16 = token_alpha(fmaxf(ered[4 * et], ered[4 * et + 1]));
-      const float inv_a = inverse_alpha(a16);
-      if (!ejp && eb > 0) {
-        const uint32_t u = quantize_code(r, inv_a, eb);
-        atomicOr(&erec[et][eoff >> 5], u << (eoff & 31));
-        if ((eoff & 31) + eb > 32) atomicOr(&erec[et][(eoff >> 5) + 1], u >> (32 - (eoff & 31)));
-      }
-      if (ec == 0 && !ejp) ea16[et] = __half_as_ushort(a16);
-    }
   }
 
   // (3) Land the cache in LDS (over the query-transform scratch).
@@ -950,6 +978,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   const int NVT = (BV + 15) >> 4;
   const uint32_t m0 = 0x01010101u << (2 * g), m1 = m0 << 1;
   float* ob = reinterpret_cast<float*>(smem + a.off_ob);   // [NH][ob_stride]
+  // The splits of a (sequence, KV head) run on one XCD (block order above); each touches a
+  // slice of T_V here so that the merging workgroup finds it in that XCD's L2.
+  const uint32_t tv_touch = reinterpret_cast<gdword>(reinterpret_cast<uintptr_t>(hv->T))[
+      (split * NTHR + tid) * 16 % (kD * kD)];
   for (int vt = wave; vt < NVT; vt += NW) {
     v4i acc[NT], acc2[NT];                          // even / odd chunks: two MFMA chains
 #pragma unroll
@@ -976,6 +1008,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   }
   __syncthreads();
 
+  asm volatile("" ::"v"(tv_touch));      // keeps the touch load
   // (7) Partial: o~_c = s_c 2^(1-b_c-fv) (sum_{k < b-1} 2^k O'(c,k) - 2^(b-1) O'(c,b-1)),
   //     one (head, channel) per thread.
 #pragma unroll
@@ -1003,7 +1036,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     buf_store16_coherent((v4f){layout_ok ? m : NAN, l, 0.f, 0.f}, prs,
                          (uint32_t)((split * G + tid) * sizeof(Partial)));
   }
-  merge_if_last<NTHR>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters, out_rows,
+  merge_if_last<NTHR, true>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters, out_rows,
                       reinterpret_cast<float*>(smem));
 }
 
@@ -1040,6 +1073,7 @@ static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
     a.off_ob = (int)off;
     off += (size_t)NH * a.ob_stride * 4;
   }
+
   const size_t lds = off;
   if (lds > 160 * 1024 - 4 * 1024) return AATC_E_UNSUPPORTED;
   static size_t set_lds = 0;
