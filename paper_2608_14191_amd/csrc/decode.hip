@@ -534,7 +534,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   constexpr int AL = S / 8;           // 16-byte loads of one alpha array (one per thread)
   constexpr int NR = NH * kD / NTHR;  // (head, channel) items per thread
   constexpr int NPI = (NH * 4 * NP * 8 + NTHR - 1) / NTHR;   // plane items per thread
-  static_assert(NTILE % 4 == 0, "a wave owns whole 64-token chunks");
+  static_assert(NTILE % 4 == 0, "a wave owns whole 64-token chunks (and tile pairs)");
   static_assert(AL <= NTHR && NR >= 1, "thread mapping");
   static_assert(!APPEND || NW == 8, "the fused append maps one tensor to 256 threads");
   extern __shared__ __align__(16) uint8_t smem[];
@@ -867,43 +867,58 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   float zr[NTILE][NT];
   float avt[NTILE];
   float amax = 0.f;
+  // Tiles go in pairs: two independent MFMA chains interleave.
 #pragma unroll
-  for (int tt = 0; tt < NTILE; ++tt) {
-    const int tok0 = wb + 16 * tt;
-    const uint8_t* rec = kbuf + (tok0 + n) * RK;
-    v4i acc[NT];
-#pragma unroll
-    for (int rt = 0; rt < NT; ++rt) acc[rt] = (v4i){0, 0, 0, 0};
+  for (int tp = 0; tp < NTILE; tp += 2) {
+    v4i acc[2][NT];
+    uint32_t wd[2][NP];
     // Lane group g holds record dwords g NP .. g NP + NP - 1; dwords past the record
     // (they belong to the next token) meet zero query weights.
-    uint32_t wd[NP];
 #pragma unroll
-    for (int P = 0; P < NP; ++P) wd[P] = *reinterpret_cast<const uint32_t*>(rec + 4 * (g * NP + P));
+    for (int u = 0; u < 2; ++u) {
+      const uint8_t* rec = kbuf + (wb + 16 * (tp + u) + n) * RK;
+#pragma unroll
+      for (int P = 0; P < NP; ++P)
+        wd[u][P] = *reinterpret_cast<const uint32_t*>(rec + 4 * (g * NP + P));
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) acc[u][rt] = (v4i){0, 0, 0, 0};
+    }
 #pragma unroll
     for (int P = 0; P < NP; ++P) {
-      const uint32_t w = wd[P];
-      const v4i a0 = {(int)(w & 0x01010101u), (int)(w & 0x02020202u),
-                      (int)(w & 0x04040404u), (int)(w & 0x08080808u)};
-      const v4i a1 = {(int)(w & 0x10101010u), (int)(w & 0x20202020u),
-                      (int)(w & 0x40404040u), (int)(w & 0x80808080u)};
+      v4i a0[2], a1[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const uint32_t w = wd[u][P];
+        a0[u] = (v4i){(int)(w & 0x01010101u), (int)(w & 0x02020202u), (int)(w & 0x04040404u),
+                      (int)(w & 0x08080808u)};
+        a1[u] = (v4i){(int)(w & 0x10101010u), (int)(w & 0x20202020u), (int)(w & 0x40404040u),
+                      (int)(w & 0x80808080u)};
+      }
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) acc[u][rt] = mfma_i8(a0[u], bq[rt][2 * P], acc[u][rt]);
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) acc[u][rt] = mfma_i8(a1[u], bq[rt][2 * P + 1], acc[u][rt]);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int tt = tp + u;
+      const int tok = wb + 16 * tt + 4 * g + L;
+      const bool tok_ok = tok < nt;
+      const float ak = half_bits_to_float(akb[tok]);
+      const float av = half_bits_to_float(avb[tok]);
+      avt[tt] = tok_ok ? av : 0.f;
+      amax = fmaxf(amax, fabsf(avt[tt]));
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) {
-        acc[rt] = mfma_i8(a0, bq[rt][2 * P], acc[rt]);
-        acc[rt] = mfma_i8(a1, bq[rt][2 * P + 1], acc[rt]);
+        const float x[4] = {(float)acc[u][rt][0] * lw, (float)acc[u][rt][1] * lw,
+                            (float)acc[u][rt][2] * lw, (float)acc[u][rt][3] * lw};
+        const float f = quad_reduce_scatter(x, L);
+        zr[tt][rt] = (tok_ok && 4 * rt + hc < G) ? ldexpf(f * ak, -fex[rt]) : -INFINITY;
       }
-    }
-    const int tok = tok0 + 4 * g + L;
-    const bool tok_ok = tok < nt;
-    const float ak = half_bits_to_float(akb[tok]);
-    const float av = half_bits_to_float(avb[tok]);
-    avt[tt] = tok_ok ? av : 0.f;
-    amax = fmaxf(amax, fabsf(avt[tt]));
-#pragma unroll
-    for (int rt = 0; rt < NT; ++rt) {
-      const float x[4] = {(float)acc[rt][0] * lw, (float)acc[rt][1] * lw, (float)acc[rt][2] * lw,
-                          (float)acc[rt][3] * lw};
-      const float f = quad_reduce_scatter(x, L);
-      zr[tt][rt] = (tok_ok && 4 * rt + hc < G) ? ldexpf(f * ak, -fex[rt]) : -INFINITY;
     }
   }
 
@@ -982,27 +997,34 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   // slice of T_V here so that the merging workgroup finds it in that XCD's L2.
   const uint32_t tv_touch = reinterpret_cast<gdword>(reinterpret_cast<uintptr_t>(hv->T))[
       (split * NTHR + tid) * 16 % (kD * kD)];
-  for (int vt = wave; vt < NVT; vt += NW) {
-    v4i acc[NT], acc2[NT];                          // even / odd chunks: two MFMA chains
+  // B operands stay in registers when they fit (16 x 4 VGPRs).
+  constexpr bool kPbRegs = NCH * NT <= 16;
+  v4i pbr[kPbRegs ? NCH * NT : 1];
+  if constexpr (kPbRegs) {
 #pragma unroll
-    for (int rt = 0; rt < NT; ++rt) acc[rt] = acc2[rt] = (v4i){0, 0, 0, 0};
+    for (int i = 0; i < NCH * NT; ++i) pbr[i] = pb[i * 64 + lane];
+  }
+  for (int vt = wave; vt < NVT; vt += NW) {
+    v4i acc[4][NT];                                 // chunk % 4: four MFMA chains
+#pragma unroll
+    for (int c4 = 0; c4 < 4; ++c4)
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) acc[c4][rt] = (v4i){0, 0, 0, 0};
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
       const uint2 ww = *reinterpret_cast<const uint2*>(vbuf + ch * kTile * RV + 8 * (16 * vt + n));
       const v4i av4 = {(int)(ww.x & m0), (int)(ww.x & m1), (int)(ww.y & m0), (int)(ww.y & m1)};
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) {
-        if (ch & 1)
-          acc2[rt] = mfma_i8(av4, pb[(ch * NT + rt) * 64 + lane], acc2[rt]);
-        else
-          acc[rt] = mfma_i8(av4, pb[(ch * NT + rt) * 64 + lane], acc[rt]);
+        const v4i bop = kPbRegs ? pbr[kPbRegs ? ch * NT + rt : 0] : pb[(ch * NT + rt) * 64 + lane];
+        acc[ch & 3][rt] = mfma_i8(av4, bop, acc[ch & 3][rt]);
       }
     }
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) {
-      acc[rt] += acc2[rt];
-      const float x[4] = {(float)acc[rt][0] * lw, (float)acc[rt][1] * lw, (float)acc[rt][2] * lw,
-                          (float)acc[rt][3] * lw};
+      acc[0][rt] += acc[1][rt] + acc[2][rt] + acc[3][rt];
+      const float x[4] = {(float)acc[0][rt][0] * lw, (float)acc[0][rt][1] * lw,
+                          (float)acc[0][rt][2] * lw, (float)acc[0][rt][3] * lw};
       ob[(4 * rt + hc) * a.ob_stride + 16 * vt + 4 * g + L] = quad_reduce_scatter(x, L);
     }
   }
