@@ -18,6 +18,9 @@ FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     # packed fp32 instructions stay off: plain fp32 code is scalar or float2 VALU.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # single-lane arrival counts stay plain atomics (the atomic optimizer would rewrite
+    # them into wave scans that wait for the result at once).
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
 ]
 

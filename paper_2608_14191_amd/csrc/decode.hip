@@ -68,7 +68,7 @@ struct DecodeArgs {
   int n_splits, n_blocks;         // splits per (sequence, KV head); rows x splits
   int rk, rv;                     // record bytes
   float scale_log2e;
-  int off_v, off_ak, off_av, off_ql, off_pb, off_ob, ob_stride;   // dynamic LDS layout
+  int off_v, off_ak, off_av, off_ql, off_pb, off_ob, ob_stride, off_es;   // dynamic LDS layout
 };
 
 __device__ inline float load_q(const void* q, int dtype, int64_t idx) {
@@ -239,11 +239,8 @@ struct TvBlock {
 };
 
 // Called by every workgroup after it stored its partial with device-coherent stores.
-// The last workgroup of the (sequence, KV head) `row` to arrive merges the split
-// partials of its G query heads into o = sum / l and resets the arrival counter; with TV
-// the partials are in the transformed domain and it applies T_V as well.  A NaN split
-// maximum (records that do not match the parameters) makes the output NaN.
-template <int NTHR, bool TV>
+// The last of a (sequence, KV head) to arrive merges the split partials.
+template <int NTHR, bool TV, bool ONE_PASS = false>
 __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int64_t row, int G,
                                               int n_splits, const Partial* partials,
                                               unsigned* counters, float* out_rows, float* lds) {
@@ -252,15 +249,15 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
   const int tid = threadIdx.x;
   __builtin_amdgcn_s_waitcnt(0);          // this thread's partial stores have completed
   __syncthreads();
-  // Every workgroup fetches T_V alongside its arrival count; only the last one uses it.
+  // The arrival count goes out first; every workgroup then fetches T_V, which the merge
+  // would need, under the count's round trip.
+  unsigned prev = 0u;
+  if (tid == 0)
+    prev = __hip_atomic_fetch_add(&counters[row], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const HeadParams* hv = head_params(params_v, kvh);
   TvBlock<NTHR> tv;
   if (TV) tv.load(hv);
-  if (tid == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(&counters[row], 1u, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT);
-    last_s = (prev == (unsigned)n_splits - 1u) ? 1u : 0u;
-  }
+  if (tid == 0) last_s = (prev == (unsigned)n_splits - 1u) ? 1u : 0u;
   __syncthreads();
   if (!last_s) return;
   float* cm = lds;                                         // [NTHR] group maxima
@@ -272,10 +269,10 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
       make_rsrc(partials + row * n_splits * G, (uint32_t)(n_splits * G * sizeof(Partial)));
 
   // (a) Online merge over the splits: slot (head, float4 column) per thread; groups of
-  //     threads take interleaved splits and combine at the end.  T_V is fetched right
-  //     after the first batch of partials (loads complete in order).
+  //     threads take interleaved splits and combine at the end.
+  // (ONE_PASS: G kD / 4 <= NTHR, one slot per thread, no loop.)
   const int slots = G * (kD / 4);
-  for (int base = 0; base < slots; base += NTHR) {
+  for (int base = 0; base < (ONE_PASS ? 1 : slots); base += NTHR) {
     const int width = min(slots - base, NTHR);
     const int ngroups = NTHR / width;
     const int slot = base + tid % width, grp = tid / width;
@@ -284,28 +281,37 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
     float M = -INFINITY, Ls = 0.f;
     v4f acc = {0.f, 0.f, 0.f, 0.f};
     bool bad = false;
-    for (int s0 = grp; s0 < n_splits || s0 == grp; s0 += kMergeU * ngroups) {
-      v2f hd[kMergeU];
-      v4f ov[kMergeU];
+    v2f hd[kMergeU];
+    v4f ov[kMergeU];
+    auto issue = [&](int s0) {                     // past the last split the loads read 0
 #pragma unroll
-      for (int u = 0; u < kMergeU; ++u) {        // past the last split the loads read 0
+      for (int u = 0; u < kMergeU; ++u) {
         const uint32_t off = (uint32_t)(((s0 + u * ngroups) * G + h) * sizeof(Partial));
         hd[u] = buf_load8_coherent(prs, off);
         ov[u] = (v4f)__builtin_amdgcn_raw_buffer_load_b128(prs, (int)(off + 16 + 16 * c4), 0,
                                                           kCoherent);
       }
+    };
+    // Branch-free, so that every load of a batch is issued before the first wait (an
+    // empty split has o~ = 0, and loads past the last split read 0).
+    auto consume = [&](int s0) {
 #pragma unroll
       for (int u = 0; u < kMergeU; ++u) {
         const float ms = (active && s0 + u * ngroups < n_splits) ? hd[u].x : -INFINITY;
         bad |= (ms != ms);
-        if (ms > -INFINITY) {
-          const float mn = fmaxf(M, ms);
-          const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
-          acc = acc * sa + ov[u] * sb;
-          Ls = Ls * sa + hd[u].y * sb;
-          M = mn;
-        }
+        const float mn = fmaxf(M, ms);
+        const float sa = (mn == -INFINITY) ? 1.f : exp2f(M - mn);
+        const float sb = (ms == -INFINITY) ? 0.f : exp2f(ms - mn);
+        acc = acc * sa + ov[u] * sb;
+        Ls = Ls * sa + hd[u].y * sb;
+        M = mn;
       }
+    };
+    issue(grp);
+    consume(grp);
+    for (int s0 = grp + kMergeU * ngroups; s0 < n_splits; s0 += kMergeU * ngroups) {
+      issue(s0);
+      consume(s0);
     }
     cm[tid] = bad ? NAN : M;
     cl[tid] = Ls;
@@ -343,6 +349,18 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
 
 // ---------------------------------------------------------------------------------------
 // Generic VALU kernel (any G <= 16, any budget).
+// LDS of the fused append's encode (its own region).
+struct AppendScratch {
+  int xs[8][kD];                       // per wave: the token in fixed point
+  uint32_t erec[2][kMaxBudget / 32];   // key record, value record
+  int ecode[2][kD];                    // signed codes
+  float vnew[kD];                      // transformed value of the token
+  float red[8];
+  float zpart[16];
+  float znew[kMaxNH];                  // log2-domain score of the token per head
+  uint32_t ea16[2];                    // fp16 scales
+};
+
 // ---------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void decode_split_kernel(
     const void* __restrict__ params_k, const void* __restrict__ params_v, int n_q_heads,
@@ -492,7 +510,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
     st_dev(&part[tid].l, !layout_ok ? NAN : (nt > 0) ? lh[tid] : 0.f);
   }
   merge_if_last<kThreads, true>(params_v, kvh, kv_row, G, n_splits, partials, counters,
-                          out + ((int64_t)seq * n_q_heads + kvh * G) * kD, dyn);
+                                out + ((int64_t)seq * n_q_heads + kvh * G) * kD, dyn);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -535,6 +553,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   constexpr int NR = NH * kD / NTHR;  // (head, channel) items per thread
   constexpr int NPI = (NH * 4 * NP * 8 + NTHR - 1) / NTHR;   // plane items per thread
   static_assert(NTILE % 4 == 0, "a wave owns whole 64-token chunks (and tile pairs)");
+  static_assert(kMaxNH * (kD / 4) <= 64 * NW, "the merge takes one (head, 4 columns) slot per thread");
   static_assert(AL <= NTHR && NR >= 1, "thread mapping");
   static_assert(!APPEND || NW == 8, "the fused append maps one tensor to 256 threads");
   extern __shared__ __align__(16) uint8_t smem[];
@@ -598,56 +617,73 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   Partial* parts = a.partials + row * a.n_splits * G;
   float* out_rows = a.out + ((int64_t)seq * a.n_q_heads + kvh * G) * kD;
   const int len = (int)min<int64_t>(max(a.seq_len[seq], 0), a.cap);
-  const int nt = max(0, min(S, len - t0));
-
-  // Fused append: the workgroup whose split holds token len - 1 encodes it (K with
-  // threads 0..255, V with 256..511; two halves of j per channel), exactly as the encode
-  // kernels do, and patches its copy of the cache.  Its loads go out before the
-  // cache's, so they do not queue behind the cache stream.
+  // With a fused append the splits stop short of the new token at len - 1: the split
+  // that holds it encodes it and adds it to its own partial.
+  const int nt = max(0, min(S, (APPEND ? len - 1 : len) - t0));
   const int p_loc = len - 1 - t0;
-  const bool is_app = APPEND && len > 0 && p_loc < S;          // p_loc >= 0 follows from nt > 0
-  const int et = tid >> 8, ec = tid & (kD - 1), ejp = (tid >> 7) & 1;
-  uint4 etq[8];
-  uint32_t exraw = 0u;                 // the token element's dword, converted at first use
-  bool exhi = false;
+  const bool own = APPEND && len > 0 && p_loc >= 0 && p_loc < S;
+  AppendScratch* es = reinterpret_cast<AppendScratch*>(smem + a.off_es);
+
+  // Fused append inputs, for the split that holds the new token (issued ahead of the
+  // cache): wave w takes tensor w / 4 (key, value), lane l channel 32 (w % 4) + l % 32 and
+  // half l / 32 of j.  Elsewhere the descriptors are empty, so these loads read nothing.
+  v4i etq[8];
+  uint32_t exr[2];
   float e_inv_s = 0.f;
+  int e_b = 0, e_off = 0;
+  // (et is uniform over a wave; readfirstlane lets the descriptors live in scalar registers)
+  const int et = __builtin_amdgcn_readfirstlane(wave >> 2);
+  const int ec = 32 * (wave & 3) + (lane & 31), ejp = lane >> 5;
+  const int x_es = a.x_dtype == AATC_BF16 ? 2 : 4;
   if constexpr (APPEND) {
-    if (is_app && nt > 0) {
-      const HeadParams* eh = et ? hv : hk;
-      const uint4* trow = reinterpret_cast<const uint4*>(eh->Tqt + ec * kD + 64 * ejp);
+    const HeadParams* eh = et ? hv : hk;
+    const __amdgpu_buffer_rsrc_t trs = make_rsrc(eh->Tqt, own ? (uint32_t)(kD * kD * 2) : 0u);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) etq[k] = trow[k];
-      e_inv_s = eh->inv_s[ec];
-      const int64_t i = ((int64_t)seq * a.n_kv_heads + kvh) * kD + ec;
-      const uintptr_t ad = reinterpret_cast<uintptr_t>(et ? a.x_v : a.x_k) +
-                           (a.x_dtype == AATC_BF16 ? 2 * i : 4 * i);
-      exraw = *reinterpret_cast<gdword>(ad & ~(uintptr_t)3);
-      exhi = (ad & 2) != 0;
-    }
+    for (int k = 0; k < 8; ++k)
+      etq[k] = buf_load16<0>(trs, (uint32_t)((ec * kD + 64 * ejp) * 2 + 16 * k));
+    const __amdgpu_buffer_rsrc_t xrs =
+        make_rsrc(static_cast<const uint8_t*>(et ? a.x_v : a.x_k) + row * kD * x_es,
+                  own ? (uint32_t)(kD * x_es) : 0u);
+    exr[0] = __builtin_amdgcn_raw_buffer_load_b32(xrs, (lane * x_es) & ~3, 0, 0);
+    exr[1] = __builtin_amdgcn_raw_buffer_load_b32(xrs, ((lane + 64) * x_es) & ~3, 0, 0);
+    e_inv_s = eh->inv_s[ec];
+    e_b = eh->bits[ec];
+    e_off = eh->bit_off[ec];
   }
+
   // (1) This split's packed cache, into registers (loads past the capacity read 0).  The
-  //     layout check below gates the compute, not these loads.
-  const int n_load = min(S, (nt + kTile - 1) / kTile * kTile);
+  //     layout check below gates the compute, not these loads.  A compute unit serves
+  //     its loads in order, so execution barriers put every wave's loads above ahead of
+  //     any cache load, and the key records and token scales ahead of the value tiles:
+  //     the query transform and the key phase then need not wait for the value stream.
+  const int nl = max(0, min(S, len - t0));      // tokens up to the new one (its tile lands too)
+  const int n_load = min(S, (nl + kTile - 1) / kTile * kTile);
   const int nk16 = n_load * RK / 16, nv16 = n_load * RV / 16, na16 = n_load / 8;
   const __amdgpu_buffer_rsrc_t krs = make_rsrc(a.k_codes + row * a.cap * RK, (uint32_t)(a.cap * RK));
   const __amdgpu_buffer_rsrc_t vrs = make_rsrc(a.v_codes + row * a.cap * RV, (uint32_t)(a.cap * RV));
   // Loads a thread does not need get an offset past the descriptor (they return 0).
   constexpr uint32_t kNone = 0x80000000u;
   v4i rk[NLD], rv[NLD], rak, rav;
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
     const int idx = tid + i * NTHR;
     rk[i] = buf_load16<0>(krs, idx < nk16 ? (uint32_t)(t0 * RK + 16 * idx) : kNone);
   }
-#pragma unroll
-  for (int i = 0; i < NLD; ++i) {
-    const int idx = tid + i * NTHR;
-    rv[i] = buf_load16<0>(vrs, idx < nv16 ? (uint32_t)(t0 * RV + 16 * idx) : kNone);
-  }
   {
     const uint32_t aoff = (tid < na16) ? (uint32_t)(2 * t0 + 16 * tid) : kNone;
     rak = buf_load16<0>(make_rsrc(a.k_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
     rav = buf_load16<0>(make_rsrc(a.v_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int i = 0; i < NLD; ++i) {
+    const int idx = tid + i * NTHR;
+    rv[i] = buf_load16<0>(vrs, idx < nv16 ? (uint32_t)(t0 * RV + 16 * idx) : kNone);
   }
   // Keep the compiler from moving work that waits on the early loads above the cache loads.
   __builtin_amdgcn_sched_barrier(0);
@@ -667,56 +703,6 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     qs[r * NTHR + tid] = ((r * NTHR + tid) / kD < G) ? qv : 0.f;
   }
   __syncthreads();                                   // qs, qmx
-
-  // (1b) Fused append: encode the new token of both tensors into LDS records (first,
-  //      so that it overlaps the cache still landing).
-  __shared__ int exs[2][kD];
-  __shared__ long long epart[2][kD];
-  __shared__ uint32_t erec[2][kMaxBudget / 32];
-  __shared__ float ered[8];
-  __shared__ uint16_t ea16[2];
-  if constexpr (APPEND) {
-    if (is_app && nt > 0) {
-      if (tid < 2 * (kMaxBudget / 32)) (&erec[0][0])[tid] = 0u;
-      const int eb = et ? vbc : kb, eoff = et ? voc : koff;
-      const float ex = ejp ? 0.f
-                           : (a.x_dtype == AATC_BF16
-                                  ? __uint_as_float((exhi ? (exraw >> 16) : (exraw & 0xffffu)) << 16)
-                                  : __uint_as_float(exraw));
-      float m = wave_max(fabsf(ex));
-      if (lane == 0) ered[wave] = m;
-      __syncthreads();
-      const int shift = token_shift(fmaxf(ered[4 * et], ered[4 * et + 1]));
-      if (!ejp) exs[et][ec] = (int)rintf(ldexpf(ex, shift));
-      __syncthreads();
-      long long acc = 0;
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int* xr = &exs[et][64 * ejp + 8 * k];
-        const uint32_t tw[4] = {etq[k].x, etq[k].y, etq[k].z, etq[k].w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          acc += (long long)xr[2 * i] * (long long)(int16_t)(tw[i] & 0xffffu);
-          acc += (long long)xr[2 * i + 1] * (long long)(int16_t)(tw[i] >> 16);
-        }
-      }
-      if (ejp) epart[et][ec] = acc;
-      __syncthreads();
-      float r = 0.f;
-      if (!ejp) r = fixed_point_result(acc + epart[et][ec], shift) * e_inv_s;
-      const float am = wave_max((!ejp && eb > 0) ? fabsf(r) : 0.f);
-      if (lane == 0) ered[wave] = am;
-      __syncthreads();
-      const __half a16 = token_alpha(fmaxf(ered[4 * et], ered[4 * et + 1]));
-      const float inv_a = inverse_alpha(a16);
-      if (!ejp && eb > 0) {
-        const uint32_t u = quantize_code(r, inv_a, eb);
-        atomicOr(&erec[et][eoff >> 5], u << (eoff & 31));
-        if ((eoff & 31) + eb > 32) atomicOr(&erec[et][(eoff >> 5) + 1], u >> (32 - (eoff & 31)));
-      }
-      if (ec == 0 && !ejp) ea16[et] = __half_as_ushort(a16);
-    }
-  }
 
   // (2) q~ = T_K^T q: RJ-row partial sums per thread, then over the NJQ row blocks.
   float* scr = reinterpret_cast<float*>(smem);       // [NJQ][NH][kD]
@@ -738,6 +724,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   // Channel weight Q_c = q~_c s_c scale log2(e) (the weight of the code's sign bit up to
   // sign), kept in LDS; the largest |Q_c| of a head sets its fixed-point exponent.
   float* qcl = qs;                                   // [NH][kD], over the consumed queries
+  float qck[NR];                                     // kept for a fused append
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
     const int h = (r * NTHR + tid) / kD;
@@ -746,6 +733,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     for (int j = 0; j < NJQ; ++j) qq += scr[(j * NH + h) * kD + cq];
     const float qc = (h < G && kb > 0) ? qq * ks * a.scale_log2e : 0.f;
     qcl[h * kD + cq] = qc;
+    qck[r] = qc;
     const float m = wave_max(fabsf(qc));
     if (lane == 0) atomicMax(&qmx[h], __float_as_uint(m));
   }
@@ -812,7 +800,92 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     fex[rt] = fexp_s[h];
   }
 
-  // (3) Land the cache in LDS (over the query-transform scratch).
+  // Fused append: encode the new token of both tensors exactly as the encode kernels do
+  // (while the key records are still landing), and form its score per head and its
+  // transformed value.
+  if constexpr (APPEND) {
+    if (own) {                                   // uniform over the workgroup
+      if (tid < 2 * (kMaxBudget / 32)) (&es->erec[0][0])[tid] = 0u;
+      auto elem = [&](uint32_t w, int i) {
+        return x_es == 2 ? __uint_as_float((((i * 2) & 2) ? (w >> 16) : (w & 0xffffu)) << 16)
+                         : __uint_as_float(w);
+      };
+      const float xa = elem(exr[0], lane), xb = elem(exr[1], lane + 64);
+      const int shift = token_shift(wave_max(fmaxf(fabsf(xa), fabsf(xb))));
+      int* xs = es->xs[wave];                    // this wave's copy: no barrier needed
+      xs[lane] = (int)rintf(ldexpf(xa, shift));
+      xs[lane + 64] = (int)rintf(ldexpf(xb, shift));
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // sum_j X_j Tq_jc exactly: |X_j|, |Tq_jc| <= 2^14, so four products fit 32 bits.
+      long long acc = 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int4 x0 = *reinterpret_cast<const int4*>(xs + 64 * ejp + 8 * k);
+        const int4 x1 = *reinterpret_cast<const int4*>(xs + 64 * ejp + 8 * k + 4);
+        const uint32_t tw[4] = {(uint32_t)etq[k][0], (uint32_t)etq[k][1], (uint32_t)etq[k][2],
+                                (uint32_t)etq[k][3]};
+        const int p0 = __mul24(x0.x, (int)(int16_t)(tw[0] & 0xffffu)) +
+                       __mul24(x0.y, (int)(int16_t)(tw[0] >> 16)) +
+                       __mul24(x0.z, (int)(int16_t)(tw[1] & 0xffffu)) +
+                       __mul24(x0.w, (int)(int16_t)(tw[1] >> 16));
+        const int p1 = __mul24(x1.x, (int)(int16_t)(tw[2] & 0xffffu)) +
+                       __mul24(x1.y, (int)(int16_t)(tw[2] >> 16)) +
+                       __mul24(x1.z, (int)(int16_t)(tw[3] & 0xffffu)) +
+                       __mul24(x1.w, (int)(int16_t)(tw[3] >> 16));
+        acc += (long long)p0;
+        acc += (long long)p1;
+      }
+      acc += (long long)(((uint64_t)(uint32_t)__shfl_xor((int)(acc >> 32), 32, 64) << 32) |
+                         (uint32_t)__shfl_xor((int)acc, 32, 64));
+      const float r = fixed_point_result(acc, shift) * e_inv_s;
+      const float am = wave_max(e_b > 0 ? fabsf(r) : 0.f);
+      if (lane == 0) es->red[wave] = am;
+      __syncthreads();
+      const __half a16 = token_alpha(fmaxf(fmaxf(es->red[4 * et], es->red[4 * et + 1]),
+                                           fmaxf(es->red[4 * et + 2], es->red[4 * et + 3])));
+      const float inv_a = inverse_alpha(a16);
+      int code = 0;
+      if (lane < 32 && e_b > 0) {
+        const uint32_t u = quantize_code(r, inv_a, e_b);
+        atomicOr(&es->erec[et][e_off >> 5], u << (e_off & 31));
+        if ((e_off & 31) + e_b > 32) atomicOr(&es->erec[et][(e_off >> 5) + 1], u >> (32 - (e_off & 31)));
+        code = (int)(u << (32 - e_b)) >> (32 - e_b);      // sign-extended b-bit code
+      }
+      if (lane < 32) es->ecode[et][ec] = code;
+      if ((wave & 3) == 0 && lane == 0) es->ea16[et] = __half_as_ushort(a16);
+      __syncthreads();
+      // The token's key record and scales into the caches (its value bits follow once the
+      // value tiles have landed).
+      const int64_t tg = row * a.cap + len - 1;
+      for (int i = tid; i < RK / 4; i += NTHR)
+        reinterpret_cast<uint32_t*>(a.k_codes + tg * RK)[i] = es->erec[0][i];
+      if (tid == 0) {
+        a.k_alpha[tg] = (uint16_t)es->ea16[0];
+        a.v_alpha[tg] = (uint16_t)es->ea16[1];
+      }
+      // Score terms z = alpha^K sum_c Q_c 2^(1 - b_c) code_c (per head) and the value
+      // v~_c = alpha^V s_c 2^(1 - b_c) code_c, channel cq per thread.
+#pragma unroll
+      for (int r2 = 0; r2 < NR; ++r2) {
+        float t = kb ? qck[r2] * ldexpf((float)es->ecode[0][cq], 1 - kb) : 0.f;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) t += __shfl_xor(t, o, 64);
+        if (lane == 0) es->zpart[(r2 * NTHR + tid) >> 6] = t;
+      }
+      if (tid < kD)
+        es->vnew[tid] = vbc ? ldexpf(half_bits_to_float((uint16_t)es->ea16[1]) * vsc *
+                                         (float)es->ecode[1][tid], 1 - vbc)
+                            : 0.f;
+      __syncthreads();
+      if (tid < G)
+        es->znew[tid] = half_bits_to_float((uint16_t)es->ea16[0]) *
+                        (es->zpart[2 * tid] + es->zpart[2 * tid + 1]);
+    }
+  }
+
+  // (3) Land the key records and token scales in LDS (over the query-transform scratch);
+  //     the value tiles land after the softmax.
   uint8_t* kbuf = smem;
   uint8_t* vbuf = smem + a.off_v;
   uint16_t* akb = reinterpret_cast<uint16_t*>(smem + a.off_ak);
@@ -822,45 +895,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     const int idx = tid + i * NTHR;
     if (idx < nk16) reinterpret_cast<v4i*>(kbuf)[idx] = rk[i];
   }
-#pragma unroll
-  for (int i = 0; i < NLD; ++i) {
-    const int idx = tid + i * NTHR;
-    if (idx < nv16) reinterpret_cast<v4i*>(vbuf)[idx] = rv[i];
-  }
   if (tid < na16) {
     reinterpret_cast<v4i*>(akb)[tid] = rak;
     reinterpret_cast<v4i*>(avb)[tid] = rav;
   }
   __syncthreads();
-  if constexpr (APPEND) {
-    // Patch the landed cache with the new token and write it back: its key record and
-    // scales, and the value-tile words that hold its bits (whole words from LDS: the
-    // tile is resident, and no other workgroup touches it).
-    if (is_app && nt > 0) {
-      const int64_t tg = row * a.cap + t0 + p_loc;
-      for (int i = tid; i < RK / 4; i += NTHR) {
-        reinterpret_cast<uint32_t*>(kbuf + p_loc * RK)[i] = erec[0][i];
-        reinterpret_cast<uint32_t*>(a.k_codes + tg * RK)[i] = erec[0][i];
-      }
-      if (tid == 0) {
-        akb[p_loc] = a.k_alpha[tg] = ea16[0];
-        avb[p_loc] = a.v_alpha[tg] = ea16[1];
-      }
-      const int tp = p_loc & (kTile - 1);
-      const uint32_t bit = 1u << tile_bit(tp);
-      uint32_t* lt = reinterpret_cast<uint32_t*>(vbuf + (p_loc / kTile) * kTile * RV) + tile_word(tp);
-      uint32_t* gt = reinterpret_cast<uint32_t*>(a.v_codes + (row * a.cap + t0) * RV +
-                                                 (int64_t)(p_loc / kTile) * kTile * RV) +
-                     tile_word(tp);
-      for (int v = tid; v < 8 * RV; v += NTHR) {
-        const uint32_t w = (lt[2 * v] & ~bit) | (((erec[1][v >> 5] >> (v & 31)) & 1u) ? bit : 0u);
-        lt[2 * v] = w;
-        gt[2 * v] = w;
-      }
-    }
-    __syncthreads();
-  }
-
   // (4) Key scores of this wave's tokens: lane L of a quad ends with token 4 g + L.
   const int wb = wave * TW;
   const float lw = (float)(1 << (8 * L));            // weight of this lane's limb
@@ -985,6 +1024,12 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     lsum += __shfl_xor(lsum, 32, 64);
     if (g == 0 && L == 0) wsum[wave][4 * rt + hc] = lsum;
   }
+  // The value tiles land now (their region held nothing since the query transform).
+#pragma unroll
+  for (int i = 0; i < NLD; ++i) {
+    const int idx = tid + i * NTHR;
+    if (idx < nv16) reinterpret_cast<v4i*>(vbuf)[idx] = rv[i];
+  }
   __syncthreads();
 
   // (6) Value bits x P limbs over all chunks of the split; value-bit tiles are dealt to
@@ -1028,9 +1073,21 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
       ob[(4 * rt + hc) * a.ob_stride + 16 * vt + 4 * g + L] = quad_reduce_scatter(x, L);
     }
   }
+
   __syncthreads();
 
   asm volatile("" ::"v"(tv_touch));      // keeps the touch load
+  if (APPEND && own) {
+    // The appended token's value bits: whole words from the resident tile (no other
+    // workgroup touches it), its bit replaced.
+    const int tp = p_loc & (kTile - 1), tb = p_loc - tp;
+    const uint32_t bit = 1u << tile_bit(tp);
+    const uint32_t* lt = reinterpret_cast<const uint32_t*>(vbuf + tb * RV) + tile_word(tp);
+    uint32_t* gt = reinterpret_cast<uint32_t*>(a.v_codes + (row * a.cap + t0 + tb) * RV) +
+                   tile_word(tp);
+    for (int v = tid; v < 8 * RV; v += NTHR)
+      gt[2 * v] = (lt[2 * v] & ~bit) | (((es->erec[1][v >> 5] >> (v & 31)) & 1u) ? bit : 0u);
+  }
   // (7) Partial: o~_c = s_c 2^(1-b_c-fv) (sum_{k < b-1} 2^k O'(c,k) - 2^(b-1) O'(c,b-1)),
   //     one (head, channel) per thread.
 #pragma unroll
@@ -1044,7 +1101,14 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
         const float t = ldexpf(oh[min(voc + k, 8 * RV - 1)], k);
         acc += (k < vbc) ? ((k == vbc - 1) ? -t : t) : 0.f;
       }
-      const float o = vbc ? ldexpf(vsc * acc, 1 - vbc - fv) : 0.f;
+      float o = vbc ? ldexpf(vsc * acc, 1 - vbc - fv) : 0.f;
+      if (APPEND && own) {                       // the appended token joins this partial
+        float mh = wmax[0][h];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) mh = fmaxf(mh, wmax[w][h]);
+        const float z = es->znew[h], mn = fmaxf(mh, z);
+        o = o * exp2f(mh - mn) + es->vnew[cq] * exp2f(z - mn);
+      }
       buf_store4_coherent(o, prs, (uint32_t)((split * G + h) * sizeof(Partial) + 16 + 4 * cq));
     }
   }
@@ -1055,11 +1119,16 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
       m = fmaxf(m, wmax[w][tid]);
       l += wsum[w][tid];
     }
+    if (APPEND && own) {
+      const float z = es->znew[tid], mn = fmaxf(m, z);
+      l = l * exp2f(m - mn) + exp2f(z - mn);
+      m = mn;
+    }
     buf_store16_coherent((v4f){layout_ok ? m : NAN, l, 0.f, 0.f}, prs,
                          (uint32_t)((split * G + tid) * sizeof(Partial)));
   }
-  merge_if_last<NTHR, true>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters, out_rows,
-                      reinterpret_cast<float*>(smem));
+  merge_if_last<NTHR, true, true>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
+                                  out_rows, reinterpret_cast<float*>(smem));
 }
 
 }  // namespace
@@ -1096,6 +1165,8 @@ static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
     off += (size_t)NH * a.ob_stride * 4;
   }
 
+  a.off_es = (int)off;
+  if (APPEND) off += (sizeof(AppendScratch) + 15) / 16 * 16;
   const size_t lds = off;
   if (lds > 160 * 1024 - 4 * 1024) return AATC_E_UNSUPPORTED;
   static size_t set_lds = 0;
