@@ -63,6 +63,7 @@ struct DecodeArgs {
   float* out;
   unsigned* counters;
   Partial* partials;
+  float* append_r;                // fused append: [rows][2][d] transformed coefficients
   int64_t cap;
   int n_q_heads, n_kv_heads, G, q_dtype;
   int n_splits, n_blocks;         // splits per (sequence, KV head); rows x splits
@@ -113,6 +114,48 @@ __device__ inline float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
   return v;
+}
+
+// Wave-wide maximum and sum without LDS round trips: quad butterflies and row rotations
+// (DPP), then the four row results read as scalars.
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ inline float wave_max_dpp(float v) {
+  v = fmaxf(v, dpp_f<0xB1>(v));            // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_f<0x4E>(v));            // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_f<0x124>(v));           // row_ror:4
+  v = fmaxf(v, dpp_f<0x128>(v));           // row_ror:8
+  const int b = __float_as_int(v);
+  return fmaxf(fmaxf(__int_as_float(__builtin_amdgcn_readlane(b, 0)),
+                     __int_as_float(__builtin_amdgcn_readlane(b, 16))),
+               fmaxf(__int_as_float(__builtin_amdgcn_readlane(b, 32)),
+                     __int_as_float(__builtin_amdgcn_readlane(b, 48))));
+}
+__device__ inline float wave_sum_dpp(float v) {
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x124>(v);
+  v += dpp_f<0x128>(v);
+  const int b = __float_as_int(v);
+  return (__int_as_float(__builtin_amdgcn_readlane(b, 0)) +
+          __int_as_float(__builtin_amdgcn_readlane(b, 16))) +
+         (__int_as_float(__builtin_amdgcn_readlane(b, 32)) +
+          __int_as_float(__builtin_amdgcn_readlane(b, 48)));
+}
+
+template <int CTRL>
+__device__ inline int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+__device__ inline int wave_sum_i32(int v) {         // exact while the sum fits 32 bits
+  v += dpp_i<0xB1>(v);
+  v += dpp_i<0x4E>(v);
+  v += dpp_i<0x124>(v);
+  v += dpp_i<0x128>(v);
+  return (__builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16)) +
+         (__builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48));
 }
 
 __device__ inline float block_reduce(float v, bool is_max, float* scratch) {
@@ -171,10 +214,15 @@ __device__ inline v4i mfma_i8(v4i a, v4i b, v4i c) {
 }
 
 // ---------------------------------------------------------------------------------------
-// Workspace: arrival counters per (sequence, KV head), then the split partials.
+// Workspace: arrival counters per (sequence, KV head), the split partials, and the
+// appended token's transformed coefficients (key then value, per (sequence, KV head)).
 // ---------------------------------------------------------------------------------------
+// Arrival counters sit 256 bytes apart: the device-scope atomics on one cache line
+// serialize, and every split of every (sequence, KV head) arrives at nearly once.
+constexpr int kCtrStride = 64;
+
 struct WsLayout {
-  size_t counters, partials, total;
+  size_t counters, partials, append_r, total;
 };
 
 __host__ __device__ inline size_t round256(size_t x) { return (x + 255) / 256 * 256; }
@@ -184,8 +232,9 @@ inline WsLayout ws_layout(int batch, int n_q_heads, int n_kv_heads, int64_t cap)
   const size_t n_splits = (size_t)((cap + kMinSplit - 1) / kMinSplit);
   WsLayout w;
   w.counters = 0;
-  w.partials = round256(rows * sizeof(unsigned));
-  w.total = w.partials + (size_t)batch * n_q_heads * n_splits * sizeof(Partial);
+  w.partials = round256(rows * kCtrStride * sizeof(unsigned));
+  w.append_r = round256(w.partials + (size_t)batch * n_q_heads * n_splits * sizeof(Partial));
+  w.total = w.append_r + rows * 2 * kD * sizeof(float);   // fused append: r_c per row
   return w;
 }
 
@@ -238,12 +287,24 @@ struct TvBlock {
   }
 };
 
+// Extra work of the merging workgroup (the fused append supplies one, below).
+struct NoHook {
+  __device__ void prefetch() {}
+  __device__ void during_loads() {}
+  __device__ void fold(int, int, float&, float&, v4f&) const {}
+  __device__ void fold1(int, int, float&, float&, float&) const {}
+  __device__ void finish() {}
+};
+
 // Called by every workgroup after it stored its partial with device-coherent stores.
-// The last of a (sequence, KV head) to arrive merges the split partials.
-template <int NTHR, bool TV, bool ONE_PASS = false>
+// The last of a (sequence, KV head) to arrive merges the split partials.  The hook's
+// loads go out ahead of the partials', its during_loads() runs while they are in flight,
+// fold() adds one more (score, value) term per output slot, finish() runs at the end.
+template <int NTHR, bool TV, bool ONE_PASS = false, class Hook = NoHook>
 __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int64_t row, int G,
                                               int n_splits, const Partial* partials,
-                                              unsigned* counters, float* out_rows, float* lds) {
+                                              unsigned* counters, float* out_rows, float* lds,
+                                              Hook& hook) {
   constexpr int NCB = NTHR / 32;          // column blocks of the T_V product
   __shared__ unsigned last_s;
   const int tid = threadIdx.x;
@@ -253,13 +314,16 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
   // would need, under the count's round trip.
   unsigned prev = 0u;
   if (tid == 0)
-    prev = __hip_atomic_fetch_add(&counters[row], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    prev = __hip_atomic_fetch_add(&counters[row * kCtrStride], 1u, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
   const HeadParams* hv = head_params(params_v, kvh);
   TvBlock<NTHR> tv;
   if (TV) tv.load(hv);
   if (tid == 0) last_s = (prev == (unsigned)n_splits - 1u) ? 1u : 0u;
   __syncthreads();
   if (!last_s) return;
+  hook.prefetch();
+  __builtin_amdgcn_sched_barrier(0);
   float* cm = lds;                                         // [NTHR] group maxima
   float* cl = cm + NTHR;                                   // [NTHR] group sums
   v4f* cacc = reinterpret_cast<v4f*>(cl + NTHR);           // [NTHR]
@@ -308,6 +372,7 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
       }
     };
     issue(grp);
+    if (base == 0) hook.during_loads();
     consume(grp);
     for (int s0 = grp + kMergeU * ngroups; s0 < n_splits; s0 += kMergeU * ngroups) {
       issue(s0);
@@ -333,6 +398,7 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
           M = mn;
         }
       }
+      hook.fold(h, c4, M, Ls, acc);
       const float inv_l = bad ? NAN : (Ls > 0.f ? 1.f / Ls : 0.f);
       reinterpret_cast<v4f*>(osum)[h * (kD / 4) + c4] = acc * inv_l;
     }
@@ -344,14 +410,129 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
   } else {
     for (int i = tid; i < G * kD; i += NTHR) out_rows[i] = osum[i];
   }
-  if (tid == 0) counters[row] = 0u;
+  hook.finish();
+  if (tid == 0) counters[row * kCtrStride] = 0u;
+}
+
+// The merge of the MFMA kernel: one output element (head h, channel c) per thread and
+// pass, every split's (m, l) read once per wave (lane s holds split s of a batch) and its
+// weight 2^(m_s - M) broadcast from that lane; no LDS combine.
+// NH: head slots of the kernel (G <= NH); each thread holds NP elements and loads a batch
+// of kMergeB splits for each (at most 64 loads).
+template <int NTHR, int NH, class Hook>
+__device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh, int64_t row,
+                                                   int G, int n_splits, const Partial* partials,
+                                                   unsigned* counters, float* out_rows,
+                                                   float* lds, Hook& hook) {
+  constexpr int NP = (NH * kD + NTHR - 1) / NTHR;
+  constexpr int kMergeB = NP == 1 ? 32 : 64 / NP;
+  static_assert(NTHR % kD == 0 && NP * kMergeB <= 64 && kMergeB >= 8, "thread mapping");
+  __shared__ unsigned last_s;
+  const int tid = threadIdx.x, lane = tid & 63;
+  __builtin_amdgcn_s_waitcnt(0);          // this thread's partial stores have completed
+  __syncthreads();
+  // The arrival count goes out first; every workgroup then fetches T_V, which the merge
+  // would need, under the count's round trip.
+  unsigned prev = 0u;
+  if (tid == 0)
+    prev = __hip_atomic_fetch_add(&counters[row * kCtrStride], 1u, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+  const HeadParams* hv = head_params(params_v, kvh);
+  TvBlock<NTHR> tv;
+  tv.load(hv);
+  if (tid == 0) last_s = (prev == (unsigned)n_splits - 1u) ? 1u : 0u;
+  __syncthreads();
+  if (!last_s) return;
+  hook.prefetch();
+  __builtin_amdgcn_sched_barrier(0);
+  float* osum = lds;                                       // [G][kD]
+  float* ored = osum + G * kD;                             // [NTHR / 32][G][kD]
+  const __amdgpu_buffer_rsrc_t prs =
+      make_rsrc(partials + row * n_splits * G, (uint32_t)(n_splits * G * sizeof(Partial)));
+  float M[NP], Ls[NP], acc[NP];
+  bool bad[NP];
+  v2f hd[NP];
+  float ov[NP][kMergeB];
+  // Loads of a batch: past the last split (or head) they read 0 and count as empty.
+  auto issue = [&](int s0) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const int slot = p * NTHR + tid, h = min(slot / kD, G - 1), c = slot % kD;
+      const uint32_t hoff = (uint32_t)(((s0 + (lane & (kMergeB - 1))) * G + h) * sizeof(Partial));
+      hd[p] = buf_load8_coherent(prs, (slot / kD < G) ? hoff : 0x80000000u);
+#pragma unroll
+      for (int u = 0; u < kMergeB; ++u) {
+        const uint32_t off = (uint32_t)(((s0 + u) * G + h) * sizeof(Partial) + 16 + 4 * c);
+        ov[p][u] = __int_as_float(
+            __builtin_amdgcn_raw_buffer_load_b32(prs, (slot / kD < G) ? (int)off : (int)0x80000000,
+                                                 0, kCoherent));
+      }
+    }
+  };
+  auto consume = [&](int s0) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const bool in = (lane < kMergeB) & (s0 + lane < n_splits);
+      const float ms = in ? hd[p].x : -INFINITY;
+      bad[p] |= __builtin_amdgcn_ballot_w64(ms != ms) != 0;
+      const float mb = wave_max_dpp(ms);                   // (NaN lanes are ignored)
+      const float mn = fmaxf(M[p], mb);
+      const float sa = (mn == -INFINITY) ? 1.f : exp2f(M[p] - mn);
+      const float w = (ms == -INFINITY || ms != ms) ? 0.f : exp2f(ms - mn);
+      Ls[p] = Ls[p] * sa + wave_sum_dpp(w * hd[p].y);
+      float a2 = acc[p] * sa;
+      const int wb = __float_as_int(w);
+#pragma unroll
+      for (int u = 0; u < kMergeB; ++u)
+        a2 = fmaf(__int_as_float(__builtin_amdgcn_readlane(wb, u)), ov[p][u], a2);
+      acc[p] = a2;
+      M[p] = mn;
+    }
+  };
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    M[p] = -INFINITY;
+    Ls[p] = 0.f;
+    acc[p] = 0.f;
+    bad[p] = false;
+  }
+  issue(0);
+  hook.during_loads();
+  consume(0);
+  for (int s0 = kMergeB; s0 < n_splits; s0 += kMergeB) {
+    issue(s0);
+    consume(s0);
+  }
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int slot = p * NTHR + tid, h = slot / kD, c = slot % kD;
+    if (h < G) {
+      hook.fold1(h, c, M[p], Ls[p], acc[p]);
+      osum[slot] = bad[p] ? NAN : (Ls[p] > 0.f ? acc[p] / Ls[p] : 0.f);
+    }
+  }
+  __syncthreads();
+  // o = T_V o~ (the partials are in the transformed domain).
+  tv.apply(osum, ored, G, [&](int h, int j, float o) { out_rows[(int64_t)h * kD + j] = o; });
+  hook.finish();
+  if (tid == 0) counters[row * kCtrStride] = 0u;
 }
 
 // ---------------------------------------------------------------------------------------
 // Generic VALU kernel (any G <= 16, any budget).
-// LDS of the fused append's encode (its own region).
-struct AppendScratch {
-  int xs[8][kD];                       // per wave: the token in fixed point
+// ---------------------------------------------------------------------------------------
+// Fused append.  The splits stop short of the new token (position len - 1) and share its
+// encode (exactly the encode kernels' arithmetic): split s computes the transformed
+// coefficients r_c = h_c / s_c of the dot products d = s + n_splits (w + 8 i) of the
+// 2 x 128 (key channels, then value channels), one per wave, and stores them in the
+// workspace.  The merging workgroup loads the 256 coefficients ahead of the partials and,
+// while those are in flight, takes the token scales, quantizes, and forms the token's score
+// z = alpha^K sum_c Q_c 2^(1 - b_c) code_c per head (Q_c: the key phase's channel weights)
+// and transformed value v~_c = alpha^V s_c 2^(1 - b_c) code_c; it folds them into the
+// merge as one more term and writes the codes into both caches.  Every split has been read
+// when the last one arrives, so nothing else touches the new slot.
+// ---------------------------------------------------------------------------------------
+struct AppendScratch {                 // LDS region of its own
   uint32_t erec[2][kMaxBudget / 32];   // key record, value record
   int ecode[2][kD];                    // signed codes
   float vnew[kD];                      // transformed value of the token
@@ -359,6 +540,137 @@ struct AppendScratch {
   float zpart[16];
   float znew[kMaxNH];                  // log2-domain score of the token per head
   uint32_t ea16[2];                    // fp16 scales
+};
+
+// r = h / s of one transformed coefficient, from this lane's two elements of the token
+// (raw dwords: bf16 halves or fp32) and of the column of Tq (int16 halves): the integer
+// dot product is exact (each lane's two products stay below 2^29, and the wave sums
+// split them into 16-bit halves), then rounded once.
+__device__ inline float append_coefficient(uint32_t x0, uint32_t x1, uint32_t t0, uint32_t t1,
+                                           int x_dtype, float inv_s) {
+  const int lane = threadIdx.x & 63;
+  const bool bf = x_dtype == AATC_BF16;
+  const float xa = bf ? __uint_as_float(((lane & 1) ? (x0 >> 16) : (x0 & 0xffffu)) << 16)
+                      : __uint_as_float(x0);
+  const float xb = bf ? __uint_as_float(((lane & 1) ? (x1 >> 16) : (x1 & 0xffffu)) << 16)
+                      : __uint_as_float(x1);
+  const int shift = token_shift(wave_max_dpp(fmaxf(fabsf(xa), fabsf(xb))));
+  const int ta = (int)(int16_t)((lane & 1) ? (t0 >> 16) : (t0 & 0xffffu));
+  const int tb = (int)(int16_t)((lane & 1) ? (t1 >> 16) : (t1 & 0xffffu));
+  const int p = (int)rintf(ldexpf(xa, shift)) * ta + (int)rintf(ldexpf(xb, shift)) * tb;
+  const long long hi = wave_sum_i32(p >> 16), lo = wave_sum_i32(p & 0xffff);
+  return fixed_point_result(hi * 65536 + lo, shift) * inv_s;
+}
+
+template <int NTHR, int NR>
+struct AppendHook {
+  static_assert(NTHR >= 2 * kD && NR * NTHR / 64 <= 16, "thread mapping");
+  uint8_t* k_codes;
+  uint16_t* k_alpha;
+  uint8_t* v_codes;
+  uint16_t* v_alpha;
+  const float* coeff;                  // this row's 2 x 128 coefficients (workspace)
+  int64_t row, cap;
+  int len, G, rk, rv;
+  bool on;                             // the sequence has a token to append
+  int kb, koff, vbc, voc;              // tables of channel tid % kD
+  float vsc;
+  float qck[NR];                       // Q_c of (head (r NTHR + tid) / kD, channel tid % kD)
+  AppendScratch* sc;
+  float r;                             // coefficient of tensor tid / kD, channel tid % kD
+
+  __device__ void prefetch() {
+    const int tid = threadIdx.x;
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, on ? (uint32_t)(2 * kD * 4) : 0u);
+    r = __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, 4 * min(tid, 2 * kD - 1), 0,
+                                                             kCoherent));
+  }
+
+  __device__ void during_loads() {
+    if (!on) return;                   // uniform over the workgroup
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int et = tid >> 7, cq = tid & (kD - 1);              // et < 2: waves 0..3
+    const int eb = et ? vbc : kb, eoff = et ? voc : koff;
+    if (tid < 2 * (kMaxBudget / 32)) (&sc->erec[0][0])[tid] = 0u;
+    if (tid < 2 * kD) {
+      const float am = wave_max_dpp(eb > 0 ? fabsf(r) : 0.f);
+      if (lane == 0) sc->red[wave] = am;
+    }
+    __syncthreads();
+    if (tid < 2 * kD) {
+      const __half a16 = token_alpha(fmaxf(sc->red[2 * et], sc->red[2 * et + 1]));
+      int code = 0;
+      if (eb > 0) {
+        const uint32_t u = quantize_code(r, inverse_alpha(a16), eb);
+        atomicOr(&sc->erec[et][eoff >> 5], u << (eoff & 31));
+        if ((eoff & 31) + eb > 32) atomicOr(&sc->erec[et][(eoff >> 5) + 1], u >> (32 - (eoff & 31)));
+        code = (int)(u << (32 - eb)) >> (32 - eb);      // sign-extended b-bit code
+      }
+      sc->ecode[et][cq] = code;
+      if (cq == 0) sc->ea16[et] = __half_as_ushort(a16);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r2 = 0; r2 < NR; ++r2) {
+      const float t = kb ? qck[r2] * ldexpf((float)sc->ecode[0][cq], 1 - kb) : 0.f;
+      const float w = wave_sum_dpp(t);
+      if (lane == 0) sc->zpart[(r2 * NTHR + tid) >> 6] = w;
+    }
+    if (tid < kD)
+      sc->vnew[tid] = vbc ? ldexpf(half_bits_to_float((uint16_t)sc->ea16[1]) * vsc *
+                                       (float)sc->ecode[1][tid], 1 - vbc)
+                          : 0.f;
+    __syncthreads();
+    if (tid < G)
+      sc->znew[tid] = half_bits_to_float((uint16_t)sc->ea16[0]) *
+                      (sc->zpart[2 * tid] + sc->zpart[2 * tid + 1]);
+    // (read after the merge's next barrier)
+  }
+
+  __device__ void fold(int h, int c4, float& M, float& Ls, v4f& acc) const {
+    if (!on) return;
+    const float ms = sc->znew[h];
+    const v4f v = reinterpret_cast<const v4f*>(sc->vnew)[c4];
+    const float mn = fmaxf(M, ms);
+    const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
+    acc = acc * sa + v * sb;
+    Ls = Ls * sa + sb;
+    M = mn;
+  }
+
+  __device__ void fold1(int h, int c, float& M, float& Ls, float& acc) const {
+    if (!on) return;
+    const float ms = sc->znew[h];
+    const float mn = fmaxf(M, ms);
+    const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
+    acc = acc * sa + sc->vnew[c] * sb;
+    Ls = Ls * sa + sb;
+    M = mn;
+  }
+
+  // The codes go to the caches last: the key record and both scales, and the token's
+  // bits of its value tile (one atomic per record bit: the tile's other tokens share
+  // those words).
+  __device__ void finish() {
+    if (!on) return;
+    const int tid = threadIdx.x;
+    const int64_t tg = row * cap + (len - 1);
+    for (int i = tid; i < rk / 4; i += NTHR)
+      reinterpret_cast<uint32_t*>(k_codes + tg * rk)[i] = sc->erec[0][i];
+    if (tid == 0) {
+      k_alpha[tg] = (uint16_t)sc->ea16[0];
+      v_alpha[tg] = (uint16_t)sc->ea16[1];
+    }
+    const int p = len - 1, tp = p & (kTile - 1);
+    const uint32_t bit = 1u << tile_bit(tp);
+    uint32_t* gt = reinterpret_cast<uint32_t*>(v_codes + (row * cap + (p - tp)) * rv) + tile_word(tp);
+    for (int v = tid; v < 8 * rv; v += NTHR) {
+      if ((sc->erec[1][v >> 5] >> (v & 31)) & 1u)
+        __hip_atomic_fetch_or(&gt[2 * v], bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      else
+        __hip_atomic_fetch_and(&gt[2 * v], ~bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
 };
 
 // ---------------------------------------------------------------------------------------
@@ -509,8 +821,9 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
     st_dev(&part[tid].m, !layout_ok ? NAN : (nt > 0) ? mh[tid] : -INFINITY);
     st_dev(&part[tid].l, !layout_ok ? NAN : (nt > 0) ? lh[tid] : 0.f);
   }
+  NoHook none;
   merge_if_last<kThreads, true>(params_v, kvh, kv_row, G, n_splits, partials, counters,
-                                out + ((int64_t)seq * n_q_heads + kvh * G) * kD, dyn);
+                                out + ((int64_t)seq * n_q_heads + kvh * G) * kD, dyn, none);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -563,13 +876,19 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 15, g = lane >> 4, hc = n >> 2, L = n & 3;
-  // XCD-aware order: workgroups are dealt to the 8 XCDs round robin, so consecutive
-  // splits of a (sequence, KV head) are given block ids that land on one XCD.
-  const int lb = (int)(blockIdx.x & 7) * (int)(gridDim.x >> 3) + (int)(blockIdx.x >> 3);
-  if (lb >= a.n_blocks) return;
-  const int64_t row = lb / a.n_splits;
-  const int split = lb % a.n_splits;
-  const int seq = (int)(row / a.n_kv_heads), kvh = (int)(row % a.n_kv_heads);
+  // XCD-aware order (grid a multiple of 8): workgroups are dealt to the 8 XCDs round
+  // robin, so consecutive splits of a (sequence, KV head) are given block ids that land
+  // on one XCD.  The grid is exactly rows x splits, so no workgroup exits early (an early
+  // exit would split the argument loads into dependent round trips).
+  const int nb8 = (int)(gridDim.x >> 3);
+  const int lb = (gridDim.x & 7) ? (int)blockIdx.x
+                                 : (int)(blockIdx.x & 7) * nb8 + (int)(blockIdx.x >> 3);
+  const int row32 = lb / a.n_splits;                 // (32-bit: rows x splits < 2^30)
+  const int split = lb - row32 * a.n_splits;
+  const int seq = row32 / a.n_kv_heads, kvh = row32 - seq * a.n_kv_heads;
+  const int64_t row = row32;
+  const int len_raw = a.seq_len[seq];               // first: its round trip gates the cache loads
+  __builtin_amdgcn_sched_barrier(0);
   const int G = a.G, RK = a.rk, RV = a.rv;
   const int RWK = RK >> 2;
   const HeadParams* hk = head_params(a.params_k, kvh);
@@ -616,56 +935,44 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
 
   Partial* parts = a.partials + row * a.n_splits * G;
   float* out_rows = a.out + ((int64_t)seq * a.n_q_heads + kvh * G) * kD;
-  const int len = (int)min<int64_t>(max(a.seq_len[seq], 0), a.cap);
-  // With a fused append the splits stop short of the new token at len - 1: the split
-  // that holds it encodes it and adds it to its own partial.
+  const int len = (int)min<int64_t>(max(len_raw, 0), a.cap);
+  // With a fused append the splits stop short of the new token at len - 1; the merging
+  // workgroup encodes it and adds it to the merge.
   const int nt = max(0, min(S, (APPEND ? len - 1 : len) - t0));
-  const int p_loc = len - 1 - t0;
-  const bool own = APPEND && len > 0 && p_loc >= 0 && p_loc < S;
-  AppendScratch* es = reinterpret_cast<AppendScratch*>(smem + a.off_es);
 
-  // Fused append inputs, for the split that holds the new token (issued ahead of the
-  // cache): wave w takes tensor w / 4 (key, value), lane l channel 32 (w % 4) + l % 32 and
-  // half l / 32 of j.  Elsewhere the descriptors are empty, so these loads read nothing.
-  v4i etq[8];
-  uint32_t exr[2];
-  float e_inv_s = 0.f;
-  int e_b = 0, e_off = 0;
-  // (et is uniform over a wave; readfirstlane lets the descriptors live in scalar registers)
-  const int et = __builtin_amdgcn_readfirstlane(wave >> 2);
-  const int ec = 32 * (wave & 3) + (lane & 31), ejp = lane >> 5;
-  const int x_es = a.x_dtype == AATC_BF16 ? 2 : 4;
+  // Fused append: this wave's first coefficient (dot product ad; see the append notes) -
+  // the token's two elements of this lane and the matching two of column ad % kD of Tq
+  // (issued ahead of the cache; empty descriptors when there is none).
+  const int x_eb = a.x_dtype == AATC_BF16 ? 2 : 4;
+  const int ad = __builtin_amdgcn_readfirstlane(split + a.n_splits * wave);
+  const bool ad_on = APPEND && len > 0 && ad < 2 * kD;
+  uint32_t ax[2] = {0u, 0u}, atq[2] = {0u, 0u};
+  float a_inv_s = 0.f;
   if constexpr (APPEND) {
-    const HeadParams* eh = et ? hv : hk;
-    const __amdgpu_buffer_rsrc_t trs = make_rsrc(eh->Tqt, own ? (uint32_t)(kD * kD * 2) : 0u);
-#pragma unroll
-    for (int k = 0; k < 8; ++k)
-      etq[k] = buf_load16<0>(trs, (uint32_t)((ec * kD + 64 * ejp) * 2 + 16 * k));
+    const HeadParams* eh = ad >= kD ? hv : hk;
+    const int ac = ad & (kD - 1);
     const __amdgpu_buffer_rsrc_t xrs =
-        make_rsrc(static_cast<const uint8_t*>(et ? a.x_v : a.x_k) + row * kD * x_es,
-                  own ? (uint32_t)(kD * x_es) : 0u);
-    exr[0] = __builtin_amdgcn_raw_buffer_load_b32(xrs, (lane * x_es) & ~3, 0, 0);
-    exr[1] = __builtin_amdgcn_raw_buffer_load_b32(xrs, ((lane + 64) * x_es) & ~3, 0, 0);
-    e_inv_s = eh->inv_s[ec];
-    e_b = eh->bits[ec];
-    e_off = eh->bit_off[ec];
+        make_rsrc(static_cast<const uint8_t*>(ad >= kD ? a.x_v : a.x_k) + row * kD * x_eb,
+                  ad_on ? (uint32_t)(kD * x_eb) : 0u);
+    const __amdgpu_buffer_rsrc_t trs = make_rsrc(eh->Tqt + ac * kD, ad_on ? 2u * kD : 0u);
+    ax[0] = __builtin_amdgcn_raw_buffer_load_b32(xrs, (lane * x_eb) & ~3, 0, 0);
+    ax[1] = __builtin_amdgcn_raw_buffer_load_b32(xrs, ((lane + 64) * x_eb) & ~3, 0, 0);
+    atq[0] = __builtin_amdgcn_raw_buffer_load_b32(trs, (2 * lane) & ~3, 0, 0);
+    atq[1] = __builtin_amdgcn_raw_buffer_load_b32(trs, (2 * (lane + 64)) & ~3, 0, 0);
+    a_inv_s = eh->inv_s[ac];
   }
 
   // (1) This split's packed cache, into registers (loads past the capacity read 0).  The
-  //     layout check below gates the compute, not these loads.  A compute unit serves
-  //     its loads in order, so execution barriers put every wave's loads above ahead of
-  //     any cache load, and the key records and token scales ahead of the value tiles:
-  //     the query transform and the key phase then need not wait for the value stream.
-  const int nl = max(0, min(S, len - t0));      // tokens up to the new one (its tile lands too)
-  const int n_load = min(S, (nl + kTile - 1) / kTile * kTile);
+  //     layout check below gates the compute, not these loads.  Each wave issues its key
+  //     records and token scales ahead of its value tiles, with no barrier in between
+  //     (holding loads back until every wave has issued starves the memory pipeline).
+  const int n_load = min(S, (nt + kTile - 1) / kTile * kTile);
   const int nk16 = n_load * RK / 16, nv16 = n_load * RV / 16, na16 = n_load / 8;
   const __amdgpu_buffer_rsrc_t krs = make_rsrc(a.k_codes + row * a.cap * RK, (uint32_t)(a.cap * RK));
   const __amdgpu_buffer_rsrc_t vrs = make_rsrc(a.v_codes + row * a.cap * RV, (uint32_t)(a.cap * RV));
   // Loads a thread does not need get an offset past the descriptor (they return 0).
   constexpr uint32_t kNone = 0x80000000u;
   v4i rk[NLD], rv[NLD], rak, rav;
-  __builtin_amdgcn_sched_barrier(0);
-  __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
@@ -677,9 +984,6 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     rak = buf_load16<0>(make_rsrc(a.k_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
     rav = buf_load16<0>(make_rsrc(a.v_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
   }
-  __builtin_amdgcn_sched_barrier(0);
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
     const int idx = tid + i * NTHR;
@@ -800,87 +1104,25 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     fex[rt] = fexp_s[h];
   }
 
-  // Fused append: encode the new token of both tensors exactly as the encode kernels do
-  // (while the key records are still landing), and form its score per head and its
-  // transformed value.
+  // Fused append: this split's coefficients (while its key records are still landing).
   if constexpr (APPEND) {
-    if (own) {                                   // uniform over the workgroup
-      if (tid < 2 * (kMaxBudget / 32)) (&es->erec[0][0])[tid] = 0u;
-      auto elem = [&](uint32_t w, int i) {
-        return x_es == 2 ? __uint_as_float((((i * 2) & 2) ? (w >> 16) : (w & 0xffffu)) << 16)
-                         : __uint_as_float(w);
-      };
-      const float xa = elem(exr[0], lane), xb = elem(exr[1], lane + 64);
-      const int shift = token_shift(wave_max(fmaxf(fabsf(xa), fabsf(xb))));
-      int* xs = es->xs[wave];                    // this wave's copy: no barrier needed
-      xs[lane] = (int)rintf(ldexpf(xa, shift));
-      xs[lane + 64] = (int)rintf(ldexpf(xb, shift));
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      // sum_j X_j Tq_jc exactly: |X_j|, |Tq_jc| <= 2^14, so four products fit 32 bits.
-      long long acc = 0;
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int4 x0 = *reinterpret_cast<const int4*>(xs + 64 * ejp + 8 * k);
-        const int4 x1 = *reinterpret_cast<const int4*>(xs + 64 * ejp + 8 * k + 4);
-        const uint32_t tw[4] = {(uint32_t)etq[k][0], (uint32_t)etq[k][1], (uint32_t)etq[k][2],
-                                (uint32_t)etq[k][3]};
-        const int p0 = __mul24(x0.x, (int)(int16_t)(tw[0] & 0xffffu)) +
-                       __mul24(x0.y, (int)(int16_t)(tw[0] >> 16)) +
-                       __mul24(x0.z, (int)(int16_t)(tw[1] & 0xffffu)) +
-                       __mul24(x0.w, (int)(int16_t)(tw[1] >> 16));
-        const int p1 = __mul24(x1.x, (int)(int16_t)(tw[2] & 0xffffu)) +
-                       __mul24(x1.y, (int)(int16_t)(tw[2] >> 16)) +
-                       __mul24(x1.z, (int)(int16_t)(tw[3] & 0xffffu)) +
-                       __mul24(x1.w, (int)(int16_t)(tw[3] >> 16));
-        acc += (long long)p0;
-        acc += (long long)p1;
+    if (ad_on) {                                 // uniform over the wave
+      float* rdst = a.append_r + row * 2 * kD;
+      const __amdgpu_buffer_rsrc_t rrs = make_rsrc(rdst, 2 * kD * 4);
+      float rc = append_coefficient(ax[0], ax[1], atq[0], atq[1], a.x_dtype, a_inv_s);
+      if (lane == 0) buf_store4_coherent(rc, rrs, (uint32_t)(4 * ad));
+      // Further coefficients when the row has fewer than 32 splits.
+      for (int d = ad + 8 * a.n_splits; d < 2 * kD; d += 8 * a.n_splits) {
+        const HeadParams* eh = d >= kD ? hv : hk;
+        const int c = d & (kD - 1);
+        const uint8_t* xb = static_cast<const uint8_t*>(d >= kD ? a.x_v : a.x_k) + row * kD * x_eb;
+        const uint32_t x0 = *reinterpret_cast<const uint32_t*>(xb + ((lane * x_eb) & ~3));
+        const uint32_t x1 = *reinterpret_cast<const uint32_t*>(xb + (((lane + 64) * x_eb) & ~3));
+        const uint32_t* tc = reinterpret_cast<const uint32_t*>(eh->Tqt + c * kD);
+        rc = append_coefficient(x0, x1, tc[lane >> 1], tc[(lane + 64) >> 1], a.x_dtype,
+                                eh->inv_s[c]);
+        if (lane == 0) buf_store4_coherent(rc, rrs, (uint32_t)(4 * d));
       }
-      acc += (long long)(((uint64_t)(uint32_t)__shfl_xor((int)(acc >> 32), 32, 64) << 32) |
-                         (uint32_t)__shfl_xor((int)acc, 32, 64));
-      const float r = fixed_point_result(acc, shift) * e_inv_s;
-      const float am = wave_max(e_b > 0 ? fabsf(r) : 0.f);
-      if (lane == 0) es->red[wave] = am;
-      __syncthreads();
-      const __half a16 = token_alpha(fmaxf(fmaxf(es->red[4 * et], es->red[4 * et + 1]),
-                                           fmaxf(es->red[4 * et + 2], es->red[4 * et + 3])));
-      const float inv_a = inverse_alpha(a16);
-      int code = 0;
-      if (lane < 32 && e_b > 0) {
-        const uint32_t u = quantize_code(r, inv_a, e_b);
-        atomicOr(&es->erec[et][e_off >> 5], u << (e_off & 31));
-        if ((e_off & 31) + e_b > 32) atomicOr(&es->erec[et][(e_off >> 5) + 1], u >> (32 - (e_off & 31)));
-        code = (int)(u << (32 - e_b)) >> (32 - e_b);      // sign-extended b-bit code
-      }
-      if (lane < 32) es->ecode[et][ec] = code;
-      if ((wave & 3) == 0 && lane == 0) es->ea16[et] = __half_as_ushort(a16);
-      __syncthreads();
-      // The token's key record and scales into the caches (its value bits follow once the
-      // value tiles have landed).
-      const int64_t tg = row * a.cap + len - 1;
-      for (int i = tid; i < RK / 4; i += NTHR)
-        reinterpret_cast<uint32_t*>(a.k_codes + tg * RK)[i] = es->erec[0][i];
-      if (tid == 0) {
-        a.k_alpha[tg] = (uint16_t)es->ea16[0];
-        a.v_alpha[tg] = (uint16_t)es->ea16[1];
-      }
-      // Score terms z = alpha^K sum_c Q_c 2^(1 - b_c) code_c (per head) and the value
-      // v~_c = alpha^V s_c 2^(1 - b_c) code_c, channel cq per thread.
-#pragma unroll
-      for (int r2 = 0; r2 < NR; ++r2) {
-        float t = kb ? qck[r2] * ldexpf((float)es->ecode[0][cq], 1 - kb) : 0.f;
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) t += __shfl_xor(t, o, 64);
-        if (lane == 0) es->zpart[(r2 * NTHR + tid) >> 6] = t;
-      }
-      if (tid < kD)
-        es->vnew[tid] = vbc ? ldexpf(half_bits_to_float((uint16_t)es->ea16[1]) * vsc *
-                                         (float)es->ecode[1][tid], 1 - vbc)
-                            : 0.f;
-      __syncthreads();
-      if (tid < G)
-        es->znew[tid] = half_bits_to_float((uint16_t)es->ea16[0]) *
-                        (es->zpart[2 * tid] + es->zpart[2 * tid + 1]);
     }
   }
 
@@ -1077,17 +1319,6 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   __syncthreads();
 
   asm volatile("" ::"v"(tv_touch));      // keeps the touch load
-  if (APPEND && own) {
-    // The appended token's value bits: whole words from the resident tile (no other
-    // workgroup touches it), its bit replaced.
-    const int tp = p_loc & (kTile - 1), tb = p_loc - tp;
-    const uint32_t bit = 1u << tile_bit(tp);
-    const uint32_t* lt = reinterpret_cast<const uint32_t*>(vbuf + tb * RV) + tile_word(tp);
-    uint32_t* gt = reinterpret_cast<uint32_t*>(a.v_codes + (row * a.cap + t0 + tb) * RV) +
-                   tile_word(tp);
-    for (int v = tid; v < 8 * RV; v += NTHR)
-      gt[2 * v] = (lt[2 * v] & ~bit) | (((es->erec[1][v >> 5] >> (v & 31)) & 1u) ? bit : 0u);
-  }
   // (7) Partial: o~_c = s_c 2^(1-b_c-fv) (sum_{k < b-1} 2^k O'(c,k) - 2^(b-1) O'(c,b-1)),
   //     one (head, channel) per thread.
 #pragma unroll
@@ -1101,14 +1332,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
         const float t = ldexpf(oh[min(voc + k, 8 * RV - 1)], k);
         acc += (k < vbc) ? ((k == vbc - 1) ? -t : t) : 0.f;
       }
-      float o = vbc ? ldexpf(vsc * acc, 1 - vbc - fv) : 0.f;
-      if (APPEND && own) {                       // the appended token joins this partial
-        float mh = wmax[0][h];
-#pragma unroll
-        for (int w = 1; w < NW; ++w) mh = fmaxf(mh, wmax[w][h]);
-        const float z = es->znew[h], mn = fmaxf(mh, z);
-        o = o * exp2f(mh - mn) + es->vnew[cq] * exp2f(z - mn);
-      }
+      const float o = vbc ? ldexpf(vsc * acc, 1 - vbc - fv) : 0.f;
       buf_store4_coherent(o, prs, (uint32_t)((split * G + h) * sizeof(Partial) + 16 + 4 * cq));
     }
   }
@@ -1119,16 +1343,38 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
       m = fmaxf(m, wmax[w][tid]);
       l += wsum[w][tid];
     }
-    if (APPEND && own) {
-      const float z = es->znew[tid], mn = fmaxf(m, z);
-      l = l * exp2f(m - mn) + exp2f(z - mn);
-      m = mn;
-    }
     buf_store16_coherent((v4f){layout_ok ? m : NAN, l, 0.f, 0.f}, prs,
                          (uint32_t)((split * G + tid) * sizeof(Partial)));
   }
-  merge_if_last<NTHR, true, true>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
-                                  out_rows, reinterpret_cast<float*>(smem));
+  if constexpr (APPEND) {
+    AppendHook<NTHR, NR> hook;
+    hook.coeff = a.append_r + row * 2 * kD;
+    hook.k_codes = a.k_codes;
+    hook.k_alpha = a.k_alpha;
+    hook.v_codes = a.v_codes;
+    hook.v_alpha = a.v_alpha;
+    hook.row = row;
+    hook.cap = a.cap;
+    hook.len = len;
+    hook.G = G;
+    hook.rk = RK;
+    hook.rv = RV;
+    hook.on = len > 0;
+    hook.kb = kb;
+    hook.koff = koff;
+    hook.vbc = vbc;
+    hook.voc = voc;
+    hook.vsc = vsc;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) hook.qck[r] = qck[r];
+    hook.sc = reinterpret_cast<AppendScratch*>(smem + a.off_es);
+    merge_if_last_wide<NTHR, NH>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
+                                 out_rows, reinterpret_cast<float*>(smem), hook);
+  } else {
+    NoHook none;
+    merge_if_last_wide<NTHR, NH>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
+                                 out_rows, reinterpret_cast<float*>(smem), none);
+  }
 }
 
 }  // namespace
@@ -1176,7 +1422,7 @@ static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
       return AATC_E_DEVICE;
     set_lds = lds;
   }
-  const unsigned grid = (unsigned)((a.n_blocks + 7) / 8 * 8);
+  const unsigned grid = (unsigned)a.n_blocks;
   hipLaunchKernelGGL((decode_mfma_kernel<NT, NTILE, NP, NW, APPEND>), dim3(grid), dim3(NTHR), lds,
                      st, a);
   return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
@@ -1240,6 +1486,7 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
     a.out = out;
     a.counters = ctr;
     a.partials = parts;
+    a.append_r = reinterpret_cast<float*>(ws + wl.append_r);
     a.cap = cap;
     a.n_q_heads = n_q_heads;
     a.n_kv_heads = n_kv_heads;
