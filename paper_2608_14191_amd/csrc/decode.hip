@@ -122,29 +122,49 @@ template <int CTRL>
 __device__ inline float dpp_f(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
 }
+// Lane l and lane l ^ 16 (l ^ 32) combined without LDS: the row swaps of gfx950 return
+// both halves of the exchange, so op(r[0], r[1]) is op(v, partner) in every lane.
+__device__ inline float xor16_max(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float xor32_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float xor16_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ inline float xor32_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ inline int xor16_sum(int v) {
+  const auto r = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+  return (int)r[0] + (int)r[1];
+}
+__device__ inline int xor32_sum(int v) {
+  const auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+  return (int)r[0] + (int)r[1];
+}
+
+// Wave-wide maximum and sum without LDS round trips: quad butterflies and row rotations
+// (DPP), then the row swaps; every lane ends with the result.
 __device__ inline float wave_max_dpp(float v) {
   v = fmaxf(v, dpp_f<0xB1>(v));            // quad_perm [1,0,3,2]
   v = fmaxf(v, dpp_f<0x4E>(v));            // quad_perm [2,3,0,1]
   v = fmaxf(v, dpp_f<0x124>(v));           // row_ror:4
   v = fmaxf(v, dpp_f<0x128>(v));           // row_ror:8
-  const int b = __float_as_int(v);
-  return fmaxf(fmaxf(__int_as_float(__builtin_amdgcn_readlane(b, 0)),
-                     __int_as_float(__builtin_amdgcn_readlane(b, 16))),
-               fmaxf(__int_as_float(__builtin_amdgcn_readlane(b, 32)),
-                     __int_as_float(__builtin_amdgcn_readlane(b, 48))));
+  return xor32_max(xor16_max(v));
 }
 __device__ inline float wave_sum_dpp(float v) {
   v += dpp_f<0xB1>(v);
   v += dpp_f<0x4E>(v);
   v += dpp_f<0x124>(v);
   v += dpp_f<0x128>(v);
-  const int b = __float_as_int(v);
-  return (__int_as_float(__builtin_amdgcn_readlane(b, 0)) +
-          __int_as_float(__builtin_amdgcn_readlane(b, 16))) +
-         (__int_as_float(__builtin_amdgcn_readlane(b, 32)) +
-          __int_as_float(__builtin_amdgcn_readlane(b, 48)));
+  return xor32_sum(xor16_sum(v));
 }
-
 template <int CTRL>
 __device__ inline int dpp_i(int v) {
   return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
@@ -154,8 +174,7 @@ __device__ inline int wave_sum_i32(int v) {         // exact while the sum fits 
   v += dpp_i<0x4E>(v);
   v += dpp_i<0x124>(v);
   v += dpp_i<0x128>(v);
-  return (__builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16)) +
-         (__builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48));
+  return xor32_sum(xor16_sum(v));
 }
 
 __device__ inline float block_reduce(float v, bool is_max, float* scratch) {
@@ -431,15 +450,10 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
   const int tid = threadIdx.x, lane = tid & 63;
   __builtin_amdgcn_s_waitcnt(0);          // this thread's partial stores have completed
   __syncthreads();
-  // The arrival count goes out first; every workgroup then fetches T_V, which the merge
-  // would need, under the count's round trip.
   unsigned prev = 0u;
   if (tid == 0)
     prev = __hip_atomic_fetch_add(&counters[row * kCtrStride], 1u, __ATOMIC_RELAXED,
                                   __HIP_MEMORY_SCOPE_AGENT);
-  const HeadParams* hv = head_params(params_v, kvh);
-  TvBlock<NTHR> tv;
-  tv.load(hv);
   if (tid == 0) last_s = (prev == (unsigned)n_splits - 1u) ? 1u : 0u;
   __syncthreads();
   if (!last_s) return;
@@ -497,6 +511,11 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
     bad[p] = false;
   }
   issue(0);
+  // T_V after the first partials (a compute unit serves its loads in order; T_V is needed
+  // last), then the hook's work while they are in flight.
+  const HeadParams* hv = head_params(params_v, kvh);
+  TvBlock<NTHR> tv;
+  tv.load(hv);
   hook.during_loads();
   consume(0);
   for (int s0 = kMergeB; s0 < n_splits; s0 += kMergeB) {
@@ -974,6 +993,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   constexpr uint32_t kNone = 0x80000000u;
   v4i rk[NLD], rv[NLD], rak, rav;
   __builtin_amdgcn_sched_barrier(0);
+#if AATC_FRONT_WAIT
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_sched_barrier(0);
+#endif
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
     const int idx = tid + i * NTHR;
@@ -1038,7 +1061,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     const float qc = (h < G && kb > 0) ? qq * ks * a.scale_log2e : 0.f;
     qcl[h * kD + cq] = qc;
     qck[r] = qc;
-    const float m = wave_max(fabsf(qc));
+    const float m = wave_max_dpp(fabsf(qc));
     if (lane == 0) atomicMax(&qmx[h], __float_as_uint(m));
   }
   __syncthreads();
@@ -1211,11 +1234,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
 #pragma unroll
     for (int tt = 0; tt < NTILE; ++tt) m = fmaxf(m, zr[tt][rt]);
     m = quad_max(m);
-    m = fmaxf(m, __shfl_xor(m, 16, 64));
-    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    m = xor32_max(xor16_max(m));
     if (g == 0 && L == 0) wmax[wave][4 * rt + hc] = m;
   }
-  amax = wave_max(amax);
+  amax = wave_max_dpp(amax);
   if (lane == 0) wav[wave] = amax;
   __syncthreads();
   float mh[NT];
@@ -1262,8 +1284,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
           (v4i){(int)y[0], (int)y[1], (int)y[2], (int)y[3]};
     }
     lsum = quad_sum(lsum);
-    lsum += __shfl_xor(lsum, 16, 64);
-    lsum += __shfl_xor(lsum, 32, 64);
+    lsum = xor32_sum(xor16_sum(lsum));
     if (g == 0 && L == 0) wsum[wave][4 * rt + hc] = lsum;
   }
   // The value tiles land now (their region held nothing since the query transform).
