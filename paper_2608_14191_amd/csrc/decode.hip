@@ -228,6 +228,23 @@ __device__ inline uint32_t pack_limbs(int x) {
   return ((uint32_t)x + 0x80808080u) ^ 0x80808080u;
 }
 
+// s_waitcnt vmcnt(n) for a wave-uniform n known only at run time (0 <= n < 64).
+__device__ inline void wait_vmcnt(int n) {
+#define AATC_VMW(k)                                                                         \
+  case k:                                                                                  \
+    __builtin_amdgcn_s_waitcnt(((k) & 0xF) | (0x7 << 4) | (0xF << 8) | (((k) >> 4) << 14)); \
+    break;
+#define AATC_VMW4(k) AATC_VMW(k) AATC_VMW(k + 1) AATC_VMW(k + 2) AATC_VMW(k + 3)
+  switch (__builtin_amdgcn_readfirstlane(n)) {
+    AATC_VMW4(0) AATC_VMW4(4) AATC_VMW4(8) AATC_VMW4(12) AATC_VMW4(16) AATC_VMW4(20)
+    AATC_VMW4(24) AATC_VMW4(28) AATC_VMW4(32) AATC_VMW4(36) AATC_VMW4(40) AATC_VMW4(44)
+    AATC_VMW4(48) AATC_VMW4(52) AATC_VMW4(56) AATC_VMW4(60)
+    default: __builtin_amdgcn_s_waitcnt(0); break;
+  }
+#undef AATC_VMW4
+#undef AATC_VMW
+}
+
 __device__ inline v4i mfma_i8(v4i a, v4i b, v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
 }
@@ -556,8 +573,7 @@ struct AppendScratch {                 // LDS region of its own
   int ecode[2][kD];                    // signed codes
   float vnew[kD];                      // transformed value of the token
   float red[8];
-  float zpart[16];
-  float znew[kMaxNH];                  // log2-domain score of the token per head
+  float zpart[16];                     // per-wave sums of the token's score terms
   uint32_t ea16[2];                    // fp16 scales
 };
 
@@ -639,16 +655,16 @@ struct AppendHook {
       sc->vnew[tid] = vbc ? ldexpf(half_bits_to_float((uint16_t)sc->ea16[1]) * vsc *
                                        (float)sc->ecode[1][tid], 1 - vbc)
                           : 0.f;
-    __syncthreads();
-    if (tid < G)
-      sc->znew[tid] = half_bits_to_float((uint16_t)sc->ea16[0]) *
-                      (sc->zpart[2 * tid] + sc->zpart[2 * tid + 1]);
-    // (read after the merge's next barrier)
+    __syncthreads();                   // zpart, vnew and the scales visible from here on
+  }
+  // The token's log2-domain score for head h (every reader forms it from the wave sums).
+  __device__ float znew(int h) const {
+    return half_bits_to_float((uint16_t)sc->ea16[0]) * (sc->zpart[2 * h] + sc->zpart[2 * h + 1]);
   }
 
   __device__ void fold(int h, int c4, float& M, float& Ls, v4f& acc) const {
     if (!on) return;
-    const float ms = sc->znew[h];
+    const float ms = znew(h);
     const v4f v = reinterpret_cast<const v4f*>(sc->vnew)[c4];
     const float mn = fmaxf(M, ms);
     const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
@@ -659,7 +675,7 @@ struct AppendHook {
 
   __device__ void fold1(int h, int c, float& M, float& Ls, float& acc) const {
     if (!on) return;
-    const float ms = sc->znew[h];
+    const float ms = znew(h);
     const float mn = fmaxf(M, ms);
     const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
     acc = acc * sa + sc->vnew[c] * sb;
@@ -879,11 +895,18 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   constexpr int NCH = S / 64;         // 64-token chunks per workgroup
   constexpr int CPW = NTILE / 4;      // chunks per wave
   constexpr int NLD = S * 64 / 16 / NTHR;   // 16-byte loads per thread per cache (64-byte records)
-  constexpr int NJQ = NTHR / 32;      // row blocks of the query transform
+  // With eight waves the cache streams straight into LDS, issued by the upper half of the
+  // waves; the lower half builds the query planes meanwhile (a wave whose loads wait for
+  // queue space can do nothing else).  With four, every wave loads into registers.
+  constexpr bool DMA = NW == 8;
+  constexpr int NWC = DMA ? NW / 2 : NW;    // waves that build the query planes
+  constexpr int NTC = 64 * NWC;             // their threads
+  constexpr int NJQ = NTC / 32;       // row blocks of the query transform
   constexpr int RJ = kD / NJQ;        // rows per block
   constexpr int AL = S / 8;           // 16-byte loads of one alpha array (one per thread)
   constexpr int NR = NH * kD / NTHR;  // (head, channel) items per thread
-  constexpr int NPI = (NH * 4 * NP * 8 + NTHR - 1) / NTHR;   // plane items per thread
+  constexpr int NRC = NH * kD / NTC;  // the same per plane-building thread
+  constexpr int NPI = (NH * 4 * NP * 8 + NTC - 1) / NTC;    // plane items per thread
   static_assert(NTILE % 4 == 0, "a wave owns whole 64-token chunks (and tile pairs)");
   static_assert(kMaxNH * (kD / 4) <= 64 * NW, "the merge takes one (head, 4 columns) slot per thread");
   static_assert(AL <= NTHR && NR >= 1, "thread mapping");
@@ -892,6 +915,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   __shared__ unsigned qmx[NH];
   __shared__ int fexp_s[NH];
   __shared__ float wmax[NW][NH], wsum[NW][NH], wav[NW];
+  __shared__ unsigned csync;          // arrivals of the plane-building waves
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 15, g = lane >> 4, hc = n >> 2, L = n & 3;
@@ -914,43 +938,74 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   const HeadParams* hv = head_params(a.params_v, kvh);
   const int t0 = split * S;
 
-  // (0) Loads that need nothing: T_K rows RJ jq .. RJ jq + RJ - 1 at columns 4 c4 .. + 3,
-  //     the channel tables, the queries.
-  const int c4 = tid & 31, jq = tid >> 5, cq = tid & (kD - 1);
-  v4f tr[RJ];
-#pragma unroll
-  for (int jj = 0; jj < RJ; ++jj)
-    tr[jj] = reinterpret_cast<const v4f*>(hk->T)[(RJ * jq + jj) * (kD / 4) + c4];
+  // (0) Loads that need nothing.  Every thread: the channel tables of channel cq.  The
+  //     plane-building threads (tc < NTC): T_K rows RJ jq .. RJ jq + RJ - 1 at columns
+  //     4 c4 .. + 3, the bit descriptors, the queries, and (fused append) their share of
+  //     the new token's transform.  Loads are unconditional (clamped indices or empty
+  //     descriptors), so the wait counters stay exact.
+  const bool cw = !DMA || wave < NWC;                 // builds the query planes (per wave)
+  const int c4 = tid & 31, jq = (tid >> 5) % NJQ, cq = tid & (kD - 1);
   const int kb = hk->bits[cq], koff = hk->bit_off[cq];
   const float ks = hk->s[cq];
   const int vbc = hv->bits[cq], voc = hv->bit_off[cq];
   const float vsc = hv->s[cq];
-  // Plane items (head, record dword D, bit d of each byte): the 4 record bits 32 D +
-  // 8 j + d, j = 0..3, of one head.
-  // (Every load here is unconditional, with clamped indices: the wait counters then stay
-  // exact, and waiting for these does not wait for the cache loads issued after them.)
+  v4f tr[RJ];
   uint2 desc[NPI];
-#pragma unroll
-  for (int r = 0; r < NPI; ++r) {
-    const int dd = (r * NTHR + tid) % (8 * RWK);                 // < 128: in the table
-    desc[r] = reinterpret_cast<const uint2*>(hk->bit_desc)[dd];
-  }
-  // Queries, element r NTHR + tid, read as the aligned dword that holds the element
-  // (either type, no branch; the dword never leaves the element's page).
   const bool q_bf = a.q_dtype == AATC_BF16;
-  uint32_t qraw[NR];
-  bool qhi[NR];
-  {
+  uint32_t qraw[NRC];
+  bool qhi[NRC];
+  // Fused append: dot products d = split + n_splits k, k = wave + NWC i, of the 2 x 128
+  // (key channels, then value channels); the first two of each plane-building wave are
+  // fetched here (the token's two elements of this lane and the matching two of column
+  // d % kD of Tq), further ones (fewer than 32 splits) when they are computed.
+  const int x_eb = a.x_dtype == AATC_BF16 ? 2 : 4;
+  constexpr int KF = 2;                               // coefficients fetched up front
+  int adk[KF];
+  uint32_t ax[KF][2], atq[KF][2];
+  float a_inv_s[KF];
+  if (cw) {
+#pragma unroll
+    for (int jj = 0; jj < RJ; ++jj)
+      tr[jj] = reinterpret_cast<const v4f*>(hk->T)[(RJ * jq + jj) * (kD / 4) + c4];
+    // Plane items (head, record dword D, bit d of each byte): the 4 record bits 32 D +
+    // 8 j + d, j = 0..3, of one head.
+#pragma unroll
+    for (int r = 0; r < NPI; ++r) {
+      const int dd = (r * NTC + tid) % (8 * RWK);                // < 128: in the table
+      desc[r] = reinterpret_cast<const uint2*>(hk->bit_desc)[dd];
+    }
+    // Queries, element r NTC + tid, read as the aligned dword that holds the element
+    // (either type, no branch; the dword never leaves the element's page).
     const int64_t qb = ((int64_t)seq * a.n_q_heads + kvh * G) * kD;
 #pragma unroll
-    for (int r = 0; r < NR; ++r) {
-      const int64_t i = qb + min(r * NTHR + tid, G * kD - 1);
+    for (int r = 0; r < NRC; ++r) {
+      const int64_t i = qb + min(r * NTC + tid, G * kD - 1);
       const uintptr_t ad = reinterpret_cast<uintptr_t>(a.q) + (q_bf ? 2 * i : 4 * i);
       qraw[r] = *reinterpret_cast<gdword>(ad & ~(uintptr_t)3);
       qhi[r] = (ad & 2) != 0;
     }
+    if constexpr (APPEND) {
+#pragma unroll
+      for (int f = 0; f < KF; ++f) {
+        const int d = __builtin_amdgcn_readfirstlane(split + a.n_splits * (wave + NWC * f));
+        adk[f] = d;
+        const bool on = d < 2 * kD;
+        const HeadParams* eh = d >= kD ? hv : hk;
+        const int ac = d & (kD - 1);
+        const __amdgpu_buffer_rsrc_t xrs =
+            make_rsrc(static_cast<const uint8_t*>(d >= kD ? a.x_v : a.x_k) + row * kD * x_eb,
+                      on ? (uint32_t)(kD * x_eb) : 0u);
+        const __amdgpu_buffer_rsrc_t trs = make_rsrc(eh->Tqt + ac * kD, on ? 2u * kD : 0u);
+        ax[f][0] = __builtin_amdgcn_raw_buffer_load_b32(xrs, (lane * x_eb) & ~3, 0, 0);
+        ax[f][1] = __builtin_amdgcn_raw_buffer_load_b32(xrs, ((lane + 64) * x_eb) & ~3, 0, 0);
+        atq[f][0] = __builtin_amdgcn_raw_buffer_load_b32(trs, (2 * lane) & ~3, 0, 0);
+        atq[f][1] = __builtin_amdgcn_raw_buffer_load_b32(trs, (2 * (lane + 64)) & ~3, 0, 0);
+        a_inv_s[f] = eh->inv_s[ac];
+      }
+    }
   }
   if (tid < NH) qmx[tid] = 0u;
+  if (tid == 0) csync = 0u;
 
   Partial* parts = a.partials + row * a.n_splits * G;
   float* out_rows = a.out + ((int64_t)seq * a.n_q_heads + kvh * G) * kD;
@@ -959,160 +1014,218 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   // workgroup encodes it and adds it to the merge.
   const int nt = max(0, min(S, (APPEND ? len - 1 : len) - t0));
 
-  // Fused append: this wave's first coefficient (dot product ad; see the append notes) -
-  // the token's two elements of this lane and the matching two of column ad % kD of Tq
-  // (issued ahead of the cache; empty descriptors when there is none).
-  const int x_eb = a.x_dtype == AATC_BF16 ? 2 : 4;
-  const int ad = __builtin_amdgcn_readfirstlane(split + a.n_splits * wave);
-  const bool ad_on = APPEND && len > 0 && ad < 2 * kD;
-  uint32_t ax[2] = {0u, 0u}, atq[2] = {0u, 0u};
-  float a_inv_s = 0.f;
-  if constexpr (APPEND) {
-    const HeadParams* eh = ad >= kD ? hv : hk;
-    const int ac = ad & (kD - 1);
-    const __amdgpu_buffer_rsrc_t xrs =
-        make_rsrc(static_cast<const uint8_t*>(ad >= kD ? a.x_v : a.x_k) + row * kD * x_eb,
-                  ad_on ? (uint32_t)(kD * x_eb) : 0u);
-    const __amdgpu_buffer_rsrc_t trs = make_rsrc(eh->Tqt + ac * kD, ad_on ? 2u * kD : 0u);
-    ax[0] = __builtin_amdgcn_raw_buffer_load_b32(xrs, (lane * x_eb) & ~3, 0, 0);
-    ax[1] = __builtin_amdgcn_raw_buffer_load_b32(xrs, ((lane + 64) * x_eb) & ~3, 0, 0);
-    atq[0] = __builtin_amdgcn_raw_buffer_load_b32(trs, (2 * lane) & ~3, 0, 0);
-    atq[1] = __builtin_amdgcn_raw_buffer_load_b32(trs, (2 * (lane + 64)) & ~3, 0, 0);
-    a_inv_s = eh->inv_s[ac];
-  }
-
-  // (1) This split's packed cache, into registers (loads past the capacity read 0).  The
-  //     layout check below gates the compute, not these loads.  Each wave issues its key
-  //     records and token scales ahead of its value tiles, with no barrier in between
-  //     (holding loads back until every wave has issued starves the memory pipeline).
+  // (1) This split's packed cache (loads past the capacity read 0).  The layout check
+  //     below gates the compute, not these loads.
   const int n_load = min(S, (nt + kTile - 1) / kTile * kTile);
   const int nk16 = n_load * RK / 16, nv16 = n_load * RV / 16, na16 = n_load / 8;
   const __amdgpu_buffer_rsrc_t krs = make_rsrc(a.k_codes + row * a.cap * RK, (uint32_t)(a.cap * RK));
   const __amdgpu_buffer_rsrc_t vrs = make_rsrc(a.v_codes + row * a.cap * RV, (uint32_t)(a.cap * RV));
+  const __amdgpu_buffer_rsrc_t akrs = make_rsrc(a.k_alpha + row * a.cap, (uint32_t)(a.cap * 2));
+  const __amdgpu_buffer_rsrc_t avrs = make_rsrc(a.v_alpha + row * a.cap, (uint32_t)(a.cap * 2));
+  uint8_t* kbuf = smem;
+  uint8_t* vbuf = smem + a.off_v;
+  uint16_t* akb = reinterpret_cast<uint16_t*>(smem + a.off_ak);
+  uint16_t* avb = reinterpret_cast<uint16_t*>(smem + a.off_av);
   // Loads a thread does not need get an offset past the descriptor (they return 0).
   constexpr uint32_t kNone = 0x80000000u;
-  v4i rk[NLD], rv[NLD], rak, rav;
-  __builtin_amdgcn_sched_barrier(0);
-#if AATC_FRONT_WAIT
-  __builtin_amdgcn_s_waitcnt(0);
-  __builtin_amdgcn_sched_barrier(0);
-#endif
+  v4i rk[DMA ? 1 : NLD], rv[DMA ? 1 : NLD], rak, rav;
+  int nv_mine = 0;                                    // value-tile transfers of this wave
+  if constexpr (DMA) {
+    // Every wave's small loads are queued before the first cache transfer.
+    __syncthreads();
+    if (!cw) {
+      // 1 KiB transfers straight into LDS (lane l's 16 bytes at 16 l): key records, the
+      // token scales, then the value tiles, dealt to the issuing waves round robin.  Only
+      // whole 1 KiB blocks of the regions are written (their sizes are 1 KiB multiples).
+      constexpr int NWD = NW - NWC;
+      const int wd = wave - NWC;
+      const int nki = (n_load * RK + 1023) >> 10, nai = (2 * n_load + 1023) >> 10;
+      const int nvi = (n_load * RV + 1023) >> 10;
+      for (int j = wd; j < nki; j += NWD)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            krs, (__attribute__((address_space(3))) void*)(kbuf + 1024 * j), 16,
+            t0 * RK + 1024 * j + 16 * lane, 0, 0, 0);
+      for (int j = wd; j < nai; j += NWD) {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            akrs, (__attribute__((address_space(3))) void*)((uint8_t*)akb + 1024 * j), 16,
+            2 * t0 + 1024 * j + 16 * lane, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            avrs, (__attribute__((address_space(3))) void*)((uint8_t*)avb + 1024 * j), 16,
+            2 * t0 + 1024 * j + 16 * lane, 0, 0, 0);
+      }
+      for (int j = wd; j < nvi; j += NWD) {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            vrs, (__attribute__((address_space(3))) void*)(vbuf + 1024 * j), 16,
+            t0 * RV + 1024 * j + 16 * lane, 0, 0, 0);
+        ++nv_mine;
+      }
+    }
+  } else {
+    // Each wave issues its key records and token scales ahead of its value tiles.
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-  for (int i = 0; i < NLD; ++i) {
-    const int idx = tid + i * NTHR;
-    rk[i] = buf_load16<0>(krs, idx < nk16 ? (uint32_t)(t0 * RK + 16 * idx) : kNone);
-  }
-  {
-    const uint32_t aoff = (tid < na16) ? (uint32_t)(2 * t0 + 16 * tid) : kNone;
-    rak = buf_load16<0>(make_rsrc(a.k_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
-    rav = buf_load16<0>(make_rsrc(a.v_alpha + row * a.cap, (uint32_t)(a.cap * 2)), aoff);
-  }
+    for (int i = 0; i < NLD; ++i) {
+      const int idx = tid + i * NTHR;
+      rk[i] = buf_load16<0>(krs, idx < nk16 ? (uint32_t)(t0 * RK + 16 * idx) : kNone);
+    }
+    {
+      const uint32_t aoff = (tid < na16) ? (uint32_t)(2 * t0 + 16 * tid) : kNone;
+      rak = buf_load16<0>(akrs, aoff);
+      rav = buf_load16<0>(avrs, aoff);
+    }
 #pragma unroll
-  for (int i = 0; i < NLD; ++i) {
-    const int idx = tid + i * NTHR;
-    rv[i] = buf_load16<0>(vrs, idx < nv16 ? (uint32_t)(t0 * RV + 16 * idx) : kNone);
+    for (int i = 0; i < NLD; ++i) {
+      const int idx = tid + i * NTHR;
+      rv[i] = buf_load16<0>(vrs, idx < nv16 ? (uint32_t)(t0 * RV + 16 * idx) : kNone);
+    }
+    // Keep the compiler from moving work that waits on the early loads above the cache loads.
+    __builtin_amdgcn_sched_barrier(0);
   }
-  // Keep the compiler from moving work that waits on the early loads above the cache loads.
-  __builtin_amdgcn_sched_barrier(0);
   // No branch on the split's contents: an empty split computes on masked tokens and
   // stores (m, l, o~) = (-inf, 0, 0); records that do not match the parameters store a
   // NaN maximum (the value budget is clamped to the record so LDS accesses stay in range).
   const bool layout_ok = (hk->record_bytes == RK) & (hv->record_bytes == RV);
   const __amdgpu_buffer_rsrc_t prs =
       make_rsrc(parts, (uint32_t)(a.n_splits * G * sizeof(Partial)));
-  // Only now wait for the queries (issued before the cache, so the cache stays in flight).
-  float* qs = reinterpret_cast<float*>(smem) + NJQ * NH * kD;     // [NH][kD]
-#pragma unroll
-  for (int r = 0; r < NR; ++r) {
-    const uint32_t w = qraw[r];
-    const float qv = q_bf ? __uint_as_float((qhi[r] ? (w >> 16) : (w & 0xffffu)) << 16)
-                          : __uint_as_float(w);
-    qs[r * NTHR + tid] = ((r * NTHR + tid) / kD < G) ? qv : 0.f;
-  }
-  __syncthreads();                                   // qs, qmx
 
-  // (2) q~ = T_K^T q: RJ-row partial sums per thread, then over the NJQ row blocks.
-  float* scr = reinterpret_cast<float*>(smem);       // [NJQ][NH][kD]
-  {
-    v4f acc[NH];
-#pragma unroll
-    for (int h = 0; h < NH; ++h) acc[h] = (v4f){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int jj = 0; jj < RJ; jj += 4)
-#pragma unroll
-      for (int h = 0; h < NH; ++h) {
-        const v4f qv = *reinterpret_cast<const v4f*>(qs + h * kD + RJ * jq + jj);
-        acc[h] += tr[jj] * qv.x + tr[jj + 1] * qv.y + tr[jj + 2] * qv.z + tr[jj + 3] * qv.w;
-      }
-#pragma unroll
-    for (int h = 0; h < NH; ++h) reinterpret_cast<v4f*>(scr)[(jq * NH + h) * (kD / 4) + c4] = acc[h];
-  }
-  __syncthreads();
-  // Channel weight Q_c = q~_c s_c scale log2(e) (the weight of the code's sign bit up to
-  // sign), kept in LDS; the largest |Q_c| of a head sets its fixed-point exponent.
+  // (2) Query planes, by the plane-building waves; they synchronize among themselves
+  //     (the other waves are busy issuing the cache) through an LDS arrival count, or
+  //     through workgroup barriers when every wave builds.
+  unsigned csync_target = 0u;
+  auto plane_sync = [&]() {
+    if constexpr (DMA) {
+      csync_target += NWC;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      if (lane == 0) __hip_atomic_fetch_add(&csync, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      while (__hip_atomic_load(&csync, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < csync_target)
+        __builtin_amdgcn_s_sleep(1);
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    } else {
+      __syncthreads();
+    }
+  };
+  // Scratch of the planes: over the value operands (written only after the planes) with
+  // eight waves, over the cache region with four (the cache lands after the planes).
+  float* scr = reinterpret_cast<float*>(smem + (DMA ? a.off_pb : 0));   // [NJQ][NH][kD]
+  float* qs = scr + NJQ * NH * kD;                                     // [NH][kD]
   float* qcl = qs;                                   // [NH][kD], over the consumed queries
-  float qck[NR];                                     // kept for a fused append
-#pragma unroll
-  for (int r = 0; r < NR; ++r) {
-    const int h = (r * NTHR + tid) / kD;
-    float qq = 0.f;
-#pragma unroll
-    for (int j = 0; j < NJQ; ++j) qq += scr[(j * NH + h) * kD + cq];
-    const float qc = (h < G && kb > 0) ? qq * ks * a.scale_log2e : 0.f;
-    qcl[h * kD + cq] = qc;
-    qck[r] = qc;
-    const float m = wave_max_dpp(fabsf(qc));
-    if (lane == 0) atomicMax(&qmx[h], __float_as_uint(m));
-  }
-  __syncthreads();
-  if (tid < NH) {
-    int e = 0;
-    frexpf(__uint_as_float(qmx[tid]), &e);
-    fexp_s[tid] = qmx[tid] ? 30 - e : 0;
-  }
-  // Record bit v = 32 D + 8 j + d  ->  K-step 2 (D % NP) + d / 4, lane group D / NP,
-  // byte 4 (d % 4) + j of the 16-byte operand; dwords RWK .. 4 NP - 1 get weight 0.  Weight 2^(k + 1 - b) Q_c / 2^d, negated
-  // for the sign bit and for d = 7 (int8 0x80 = -128); the four limbs of the four bits
-  // j = 0..3 are transposed into one dword per limb plane.
   uint8_t* ql = smem + a.off_ql;                     // [4][NH][2 NP][64]
-  for (int i = tid; i < 4 * NH * 2 * 4 * (4 * NP - RWK); i += NTHR) {
-    const int D = RWK + i / (4 * NH * 2 * 4), rest = i % (4 * NH * 2 * 4);
-    const int plane = rest / 8, st = 2 * (D % NP) + ((rest >> 2) & 1);
-    *reinterpret_cast<uint32_t*>(ql + (plane * 2 * NP + st) * 64 + ((D / NP) << 4) +
-                                 4 * (rest & 3)) = 0u;
-  }
+  float rcf[KF] = {0.f, 0.f};                        // fused append: this wave's coefficients
+  if (cw) {
 #pragma unroll
-  for (int r = 0; r < NPI; ++r) {
-    const int i = r * NTHR + tid;
-    const int h = i / (8 * RWK), dd = i % (8 * RWK), D = dd >> 3, d = dd & 7;
-    if (h < G) {
+    for (int r = 0; r < NRC; ++r) {
+      const uint32_t w = qraw[r];
+      const float qv = q_bf ? __uint_as_float((qhi[r] ? (w >> 16) : (w & 0xffffu)) << 16)
+                            : __uint_as_float(w);
+      qs[r * NTC + tid] = ((r * NTC + tid) / kD < G) ? qv : 0.f;
+    }
+    plane_sync();                                    // qs, qmx
+    // q~ = T_K^T q: RJ-row partial sums per thread, then over the NJQ row blocks.
+    {
+      v4f acc[NH];
+#pragma unroll
+      for (int h = 0; h < NH; ++h) acc[h] = (v4f){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int jj = 0; jj < RJ; jj += 4)
+#pragma unroll
+        for (int h = 0; h < NH; ++h) {
+          const v4f qv = *reinterpret_cast<const v4f*>(qs + h * kD + RJ * jq + jj);
+          acc[h] += tr[jj] * qv.x + tr[jj + 1] * qv.y + tr[jj + 2] * qv.z + tr[jj + 3] * qv.w;
+        }
+#pragma unroll
+      for (int h = 0; h < NH; ++h) reinterpret_cast<v4f*>(scr)[(jq * NH + h) * (kD / 4) + c4] = acc[h];
+    }
+    plane_sync();
+    // Channel weight Q_c = q~_c s_c scale log2(e) (the weight of the code's sign bit up to
+    // sign), kept in LDS; the largest |Q_c| of a head sets its fixed-point exponent.
+#pragma unroll
+    for (int r = 0; r < NRC; ++r) {
+      const int h = (r * NTC + tid) / kD;
+      float qq = 0.f;
+#pragma unroll
+      for (int j = 0; j < NJQ; ++j) qq += scr[(j * NH + h) * kD + cq];
+      const float qc = (h < G && kb > 0) ? qq * ks * a.scale_log2e : 0.f;
+      qcl[h * kD + cq] = qc;
+      const float m = wave_max_dpp(fabsf(qc));
+      if (lane == 0) atomicMax(&qmx[h], __float_as_uint(m));
+    }
+    plane_sync();
+    if (tid < NH) {
       int e = 0;
-      const unsigned qm = qmx[h];
-      frexpf(__uint_as_float(qm), &e);
-      const int fe = qm ? 30 - e : 0;
-      uint32_t x[4];
+      frexpf(__uint_as_float(qmx[tid]), &e);
+      fexp_s[tid] = qmx[tid] ? 30 - e : 0;
+    }
+    // Record bit v = 32 D + 8 j + d  ->  K-step 2 (D % NP) + d / 4, lane group D / NP,
+    // byte 4 (d % 4) + j of the 16-byte operand; dwords RWK .. 4 NP - 1 get weight 0.
+    // Weight 2^(k + 1 - b) Q_c / 2^d, negated for the sign bit and for d = 7 (int8 0x80 =
+    // -128); the four limbs of the four bits j = 0..3 are transposed into one dword per
+    // limb plane.
+    for (int i = tid; i < 4 * NH * 2 * 4 * (4 * NP - RWK); i += NTC) {
+      const int D = RWK + i / (4 * NH * 2 * 4), rest = i % (4 * NH * 2 * 4);
+      const int plane = rest / 8, st = 2 * (D % NP) + ((rest >> 2) & 1);
+      *reinterpret_cast<uint32_t*>(ql + (plane * 2 * NP + st) * 64 + ((D / NP) << 4) +
+                                   4 * (rest & 3)) = 0u;
+    }
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t ent = ((j < 2 ? desc[r].x : desc[r].y) >> (16 * (j & 1))) & 0xffffu;
-        const float qv = qcl[h * kD + (ent & 127)];
-        int fx = (int)rintf(ldexpf(qv, (int)((ent >> 8) & 15) - 8 + fe - d));
-        if ((((ent >> 14) & 1) != 0) != (d == 7)) fx = -fx;
-        x[j] = (ent & 0x8000u) ? pack_limbs(fx) : 0u;
+    for (int r = 0; r < NPI; ++r) {
+      const int i = r * NTC + tid;
+      const int h = i / (8 * RWK), dd = i % (8 * RWK), D = dd >> 3, d = dd & 7;
+      if (h < G) {
+        int e = 0;
+        const unsigned qm = qmx[h];
+        frexpf(__uint_as_float(qm), &e);
+        const int fe = qm ? 30 - e : 0;
+        uint32_t x[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t ent = ((j < 2 ? desc[r].x : desc[r].y) >> (16 * (j & 1))) & 0xffffu;
+          const float qv = qcl[h * kD + (ent & 127)];
+          int fx = (int)rintf(ldexpf(qv, (int)((ent >> 8) & 15) - 8 + fe - d));
+          if ((((ent >> 14) & 1) != 0) != (d == 7)) fx = -fx;
+          x[j] = (ent & 0x8000u) ? pack_limbs(fx) : 0u;
+        }
+        // x[j] = (limb 0..3 of bit j)  ->  y[L] = (limb L of bits 0..3)
+        const uint32_t t0 = __builtin_amdgcn_perm(x[1], x[0], 0x05010400u);
+        const uint32_t t1 = __builtin_amdgcn_perm(x[3], x[2], 0x05010400u);
+        const uint32_t t2 = __builtin_amdgcn_perm(x[1], x[0], 0x07030602u);
+        const uint32_t t3 = __builtin_amdgcn_perm(x[3], x[2], 0x07030602u);
+        const uint32_t y[4] = {__builtin_amdgcn_perm(t1, t0, 0x05040100u),
+                               __builtin_amdgcn_perm(t1, t0, 0x07060302u),
+                               __builtin_amdgcn_perm(t3, t2, 0x05040100u),
+                               __builtin_amdgcn_perm(t3, t2, 0x07060302u)};
+        const int st = 2 * (D % NP) + (d >> 2);
+        const int pos = ((D / NP) << 4) + ((d & 3) << 2);
+#pragma unroll
+        for (int l4 = 0; l4 < 4; ++l4)
+          *reinterpret_cast<uint32_t*>(ql + ((l4 * NH + h) * 2 * NP + st) * 64 + pos) = y[l4];
       }
-      // x[j] = (limb 0..3 of bit j)  ->  y[L] = (limb L of bits 0..3)
-      const uint32_t t0 = __builtin_amdgcn_perm(x[1], x[0], 0x05010400u);
-      const uint32_t t1 = __builtin_amdgcn_perm(x[3], x[2], 0x05010400u);
-      const uint32_t t2 = __builtin_amdgcn_perm(x[1], x[0], 0x07030602u);
-      const uint32_t t3 = __builtin_amdgcn_perm(x[3], x[2], 0x07030602u);
-      const uint32_t y[4] = {__builtin_amdgcn_perm(t1, t0, 0x05040100u),
-                             __builtin_amdgcn_perm(t1, t0, 0x07060302u),
-                             __builtin_amdgcn_perm(t3, t2, 0x05040100u),
-                             __builtin_amdgcn_perm(t3, t2, 0x07060302u)};
-      const int st = 2 * (D % NP) + (d >> 2);
-      const int pos = ((D / NP) << 4) + ((d & 3) << 2);
+    }
+    // Fused append: this wave's coefficients (stored after the value phase, when no
+    // cache transfer is queued ahead of the stores).
+    if constexpr (APPEND) {
 #pragma unroll
-      for (int l4 = 0; l4 < 4; ++l4)
-        *reinterpret_cast<uint32_t*>(ql + ((l4 * NH + h) * 2 * NP + st) * 64 + pos) = y[l4];
+      for (int f = 0; f < KF; ++f)
+        if (adk[f] < 2 * kD)                         // uniform over the wave
+          rcf[f] = append_coefficient(ax[f][0], ax[f][1], atq[f][0], atq[f][1], a.x_dtype,
+                                      a_inv_s[f]);
+    }
+  }
+
+  // (3) The key records and token scales in LDS: the issuing waves wait for their own
+  //     transfers of those (the value tiles may still be landing), or every wave stores
+  //     its registers (over the query-transform scratch).
+  if constexpr (DMA) {
+    if (!cw) wait_vmcnt(nv_mine);
+  } else {
+    __syncthreads();                                 // the planes' scratch is consumed
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int idx = tid + i * NTHR;
+      if (idx < nk16) reinterpret_cast<v4i*>(kbuf)[idx] = rk[i];
+    }
+    if (tid < na16) {
+      reinterpret_cast<v4i*>(akb)[tid] = rak;
+      reinterpret_cast<v4i*>(avb)[tid] = rav;
     }
   }
   __syncthreads();
@@ -1126,45 +1239,14 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
       bq[rt][s] = *reinterpret_cast<const v4i*>(ql + ((L * NH + h) * 2 * NP + s) * 64 + 16 * g);
     fex[rt] = fexp_s[h];
   }
-
-  // Fused append: this split's coefficients (while its key records are still landing).
+  // Q_c per (head, channel) item, for a fused append (eight waves: the planes' scratch
+  // is intact until the softmax writes the value operands).
+  float qck[NR] = {};
   if constexpr (APPEND) {
-    if (ad_on) {                                 // uniform over the wave
-      float* rdst = a.append_r + row * 2 * kD;
-      const __amdgpu_buffer_rsrc_t rrs = make_rsrc(rdst, 2 * kD * 4);
-      float rc = append_coefficient(ax[0], ax[1], atq[0], atq[1], a.x_dtype, a_inv_s);
-      if (lane == 0) buf_store4_coherent(rc, rrs, (uint32_t)(4 * ad));
-      // Further coefficients when the row has fewer than 32 splits.
-      for (int d = ad + 8 * a.n_splits; d < 2 * kD; d += 8 * a.n_splits) {
-        const HeadParams* eh = d >= kD ? hv : hk;
-        const int c = d & (kD - 1);
-        const uint8_t* xb = static_cast<const uint8_t*>(d >= kD ? a.x_v : a.x_k) + row * kD * x_eb;
-        const uint32_t x0 = *reinterpret_cast<const uint32_t*>(xb + ((lane * x_eb) & ~3));
-        const uint32_t x1 = *reinterpret_cast<const uint32_t*>(xb + (((lane + 64) * x_eb) & ~3));
-        const uint32_t* tc = reinterpret_cast<const uint32_t*>(eh->Tqt + c * kD);
-        rc = append_coefficient(x0, x1, tc[lane >> 1], tc[(lane + 64) >> 1], a.x_dtype,
-                                eh->inv_s[c]);
-        if (lane == 0) buf_store4_coherent(rc, rrs, (uint32_t)(4 * d));
-      }
-    }
+#pragma unroll
+    for (int r = 0; r < NR; ++r) qck[r] = qcl[((r * NTHR + tid) / kD) * kD + cq];
   }
 
-  // (3) Land the key records and token scales in LDS (over the query-transform scratch);
-  //     the value tiles land after the softmax.
-  uint8_t* kbuf = smem;
-  uint8_t* vbuf = smem + a.off_v;
-  uint16_t* akb = reinterpret_cast<uint16_t*>(smem + a.off_ak);
-  uint16_t* avb = reinterpret_cast<uint16_t*>(smem + a.off_av);
-#pragma unroll
-  for (int i = 0; i < NLD; ++i) {
-    const int idx = tid + i * NTHR;
-    if (idx < nk16) reinterpret_cast<v4i*>(kbuf)[idx] = rk[i];
-  }
-  if (tid < na16) {
-    reinterpret_cast<v4i*>(akb)[tid] = rak;
-    reinterpret_cast<v4i*>(avb)[tid] = rav;
-  }
-  __syncthreads();
   // (4) Key scores of this wave's tokens: lane L of a quad ends with token 4 g + L.
   const int wb = wave * TW;
   const float lw = (float)(1 << (8 * L));            // weight of this lane's limb
@@ -1287,11 +1369,16 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     lsum = xor32_sum(xor16_sum(lsum));
     if (g == 0 && L == 0) wsum[wave][4 * rt + hc] = lsum;
   }
-  // The value tiles land now (their region held nothing since the query transform).
+  // The value tiles: the issuing waves wait for the rest of their transfers, or every
+  // wave stores its registers (their region held nothing since the query transform).
+  if constexpr (DMA) {
+    if (!cw) wait_vmcnt(0);
+  } else {
 #pragma unroll
-  for (int i = 0; i < NLD; ++i) {
-    const int idx = tid + i * NTHR;
-    if (idx < nv16) reinterpret_cast<v4i*>(vbuf)[idx] = rv[i];
+    for (int i = 0; i < NLD; ++i) {
+      const int idx = tid + i * NTHR;
+      if (idx < nv16) reinterpret_cast<v4i*>(vbuf)[idx] = rv[i];
+    }
   }
   __syncthreads();
 
@@ -1340,6 +1427,27 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   __syncthreads();
 
   asm volatile("" ::"v"(tv_touch));      // keeps the touch load
+  if constexpr (APPEND) {
+    // Fused append: the coefficients into the workspace (device-coherent, before this
+    // workgroup's arrival), and further ones when the row has fewer than 32 splits.
+    if (cw) {
+      const __amdgpu_buffer_rsrc_t rrs = make_rsrc(a.append_r + row * 2 * kD, 2 * kD * 4);
+#pragma unroll
+      for (int f = 0; f < KF; ++f)
+        if (adk[f] < 2 * kD && lane == 0) buf_store4_coherent(rcf[f], rrs, (uint32_t)(4 * adk[f]));
+      for (int d = split + a.n_splits * (wave + NWC * KF); d < 2 * kD; d += a.n_splits * NWC) {
+        const HeadParams* eh = d >= kD ? hv : hk;
+        const int c = d & (kD - 1);
+        const uint8_t* xb = static_cast<const uint8_t*>(d >= kD ? a.x_v : a.x_k) + row * kD * x_eb;
+        const uint32_t x0 = *reinterpret_cast<const uint32_t*>(xb + ((lane * x_eb) & ~3));
+        const uint32_t x1 = *reinterpret_cast<const uint32_t*>(xb + (((lane + 64) * x_eb) & ~3));
+        const uint32_t* tc = reinterpret_cast<const uint32_t*>(eh->Tqt + c * kD);
+        const float rc = append_coefficient(x0, x1, tc[lane >> 1], tc[(lane + 64) >> 1],
+                                            a.x_dtype, eh->inv_s[c]);
+        if (lane == 0) buf_store4_coherent(rc, rrs, (uint32_t)(4 * d));
+      }
+    }
+  }
   // (7) Partial: o~_c = s_c 2^(1-b_c-fv) (sum_{k < b-1} 2^k O'(c,k) - 2^(b-1) O'(c,b-1)),
   //     one (head, channel) per thread.
 #pragma unroll
@@ -1414,16 +1522,26 @@ static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
   // LDS: key records | value tiles | alpha^K | alpha^V   (front, also the query-transform
   // and merge scratch) | query limb planes | value operands | [O' if it does not fit
   // over the key records].
+  // Eight waves: the cache streams into LDS while the query planes are built, so their
+  // scratch shares the value-operand region (written only after the planes) instead of
+  // the cache region.  The transfers write whole 1 KiB blocks of the cache regions.
+  constexpr bool DMA = NW == 8;
+  constexpr int NJQ = (DMA ? NTHR / 2 : NTHR) / 32;
+  const size_t scr_bytes = (size_t)(NJQ + 1) * NH * kD * sizeof(float);
+  if (DMA && (((size_t)S * a.rk) % 1024 || ((size_t)S * a.rv) % 1024 || (2 * S) % 1024))
+    return AATC_E_UNSUPPORTED;
   a.off_v = S * a.rk;
   a.off_ak = a.off_v + S * a.rv;
   a.off_av = a.off_ak + 2 * S;
   size_t front = (size_t)a.off_av + 2 * S;
-  front = std::max(front, (size_t)(NTHR / 32 + 1) * NH * kD * sizeof(float));
+  if (!DMA) front = std::max(front, scr_bytes);
   front = std::max(front, merge_lds_bytes(a.G, NTHR));
   front = round256(front);
   a.off_ql = (int)front;
   a.off_pb = a.off_ql + 4 * NH * 2 * NP * 64;
-  size_t off = (size_t)a.off_pb + (size_t)(S / 64) * NT * 64 * 16;
+  size_t pb_bytes = (size_t)(S / 64) * NT * 64 * 16;
+  if (DMA) pb_bytes = std::max(pb_bytes, scr_bytes);
+  size_t off = (size_t)a.off_pb + pb_bytes;
   a.ob_stride = 8 * a.rv;
   if ((size_t)NH * a.ob_stride * 4 <= (size_t)S * a.rk) {
     a.off_ob = 0;
