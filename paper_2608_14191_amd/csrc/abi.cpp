@@ -64,8 +64,12 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
       const aatc_calibration& c = per_head[h];
       auto* hp = const_cast<HeadParams*>(head_params(host_buf, h));
       std::memcpy(hp->T, c.transform, sizeof(hp->T));
-      for (int j = 0; j < kD; ++j)
-        for (int ch = 0; ch < kD; ++ch) hp->Tt[ch * kD + j] = c.transform[j * kD + ch];
+      for (int w = 0; w < 8; ++w)
+        for (int i = 0; i < 8; ++i)
+          for (int l = 0; l < 64; ++l)
+            for (int e = 0; e < 4; ++e)
+              hp->Tm[((w * 8 + i) * 64 + l) * 4 + e] =
+                  c.transform[(16 * w + l / 4) * kD + 32 * (l % 4) + 4 * i + e];
       for (int i = 0; i < kD * kD; ++i)
         hp->Tq[i] = (int16_t)std::nearbyint(std::ldexp((double)c.transform[i], kTFrac));
       for (int j = 0; j < kD; ++j)

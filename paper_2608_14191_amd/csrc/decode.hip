@@ -323,6 +323,42 @@ struct TvBlock {
   }
 };
 
+// o = T_V o~ with one output row per lane quad: lane l of wave w holds row 16 w' + l / 4
+// (w' = w + NTHR / 64 p over the passes p) at columns 32 (l % 4) .. + 31, read from the
+// merge-ordered copy of T_V in whole 1 KiB blocks; the quad sums its four parts (DPP).
+template <int NTHR>
+struct TvQuad {
+  static constexpr int NPASS = 512 / NTHR;
+  static_assert(NPASS * NTHR == 512, "256 or 512 threads");
+  v4f t[NPASS][8];
+  __device__ void load(const HeadParams* hv) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int p = 0; p < NPASS; ++p)
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        t[p][i] = reinterpret_cast<const v4f*>(hv->Tm)[((wave + (NTHR / 64) * p) * 8 + i) * 64 + lane];
+  }
+  // osum: LDS [G][kD], complete (the caller synchronizes).  Calls sink(h, j, o_hj) once
+  // per output, from the quad's first lane.
+  template <class Sink>
+  __device__ void apply(const float* osum, int G, Sink sink) const {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, q = lane & 3;
+#pragma unroll
+    for (int p = 0; p < NPASS; ++p) {
+      const int j = 16 * (wave + (NTHR / 64) * p) + (lane >> 2);
+      for (int h = 0; h < G; ++h) {
+        const v4f* oh = reinterpret_cast<const v4f*>(osum + h * kD + 32 * q);
+        v4f acc = t[p][0] * oh[0];
+#pragma unroll
+        for (int i = 1; i < 8; ++i) acc += t[p][i] * oh[i];
+        const float o = quad_sum((acc.x + acc.y) + (acc.z + acc.w));
+        if (q == 0) sink(h, j, o);
+      }
+    }
+  }
+};
+
 // Extra work of the merging workgroup (the fused append supplies one, below).
 struct NoHook {
   __device__ void prefetch() {}
@@ -477,7 +513,6 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
   hook.prefetch();
   __builtin_amdgcn_sched_barrier(0);
   float* osum = lds;                                       // [G][kD]
-  float* ored = osum + G * kD;                             // [NTHR / 32][G][kD]
   const __amdgpu_buffer_rsrc_t prs =
       make_rsrc(partials + row * n_splits * G, (uint32_t)(n_splits * G * sizeof(Partial)));
   float M[NP], Ls[NP], acc[NP];
@@ -531,7 +566,7 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
   // T_V after the first partials (a compute unit serves its loads in order; T_V is needed
   // last), then the hook's work while they are in flight.
   const HeadParams* hv = head_params(params_v, kvh);
-  TvBlock<NTHR> tv;
+  TvQuad<NTHR> tv;
   tv.load(hv);
   hook.during_loads();
   consume(0);
@@ -549,7 +584,7 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
   }
   __syncthreads();
   // o = T_V o~ (the partials are in the transformed domain).
-  tv.apply(osum, ored, G, [&](int h, int j, float o) { out_rows[(int64_t)h * kD + j] = o; });
+  tv.apply(osum, G, [&](int h, int j, float o) { out_rows[(int64_t)h * kD + j] = o; });
   hook.finish();
   if (tid == 0) counters[row * kCtrStride] = 0u;
 }
@@ -1354,7 +1389,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
       for (int qd = 0; qd < 4; ++qd) {
         const int tt = 4 * ch + qd;
         const float z = zr[tt][rt];
-        const float p = (z == -INFINITY) ? 0.f : exp2f(z - mh[rt]);
+        // (the hardware exp2: results below 2^-126 flush to 0, below any weight that counts)
+        const float p = (z == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(z - mh[rt]);
         lsum += p;
         const int fx = (int)rintf(p * avt[tt] * ((qd & 1) ? sc_odd : sc_even));
         uint32_t x = pack_limbs(fx);
@@ -1390,7 +1426,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   float* ob = reinterpret_cast<float*>(smem + a.off_ob);   // [NH][ob_stride]
   // The splits of a (sequence, KV head) run on one XCD (block order above); each touches a
   // slice of T_V here so that the merging workgroup finds it in that XCD's L2.
-  const uint32_t tv_touch = reinterpret_cast<gdword>(reinterpret_cast<uintptr_t>(hv->T))[
+  const uint32_t tv_touch = reinterpret_cast<gdword>(reinterpret_cast<uintptr_t>(hv->Tm))[
       (split * NTHR + tid) * 16 % (kD * kD)];
   // B operands stay in registers when they fit (16 x 4 VGPRs).
   constexpr bool kPbRegs = NCH * NT <= 16;

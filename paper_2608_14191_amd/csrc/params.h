@@ -18,7 +18,9 @@ constexpr uint32_t kMagic = 0x43544141u;  // "AATC"
 
 struct alignas(256) HeadParams {
   float T[kD * kD];               // [j][c] transform, storage channels (fp32)
-  float Tt[kD * kD];              // [c][j] the same transform, transposed
+  // The same transform in the decode merge's load order: 16-byte unit (8 w + i) 64 + l
+  // holds T[16 w + l / 4][32 (l % 4) + 4 i .. + 3], w, i < 8, l < 64.
+  float Tm[kD * kD];
   int16_t Tq[kD * kD];            // [j][c] rint(T * 2^14), |Tq| <= 2^14
   int16_t Tqt[kD * kD];           // [c][j] the same, transposed
   float inv_s[kD];                // fp32 1/s_c (0 for dropped or zero-scale channels)
@@ -40,6 +42,7 @@ struct alignas(256) HeadParams {
 
 // The decode kernel reads these fields with 16-, 8- and 4-byte vector loads.
 static_assert(offsetof(HeadParams, T) % 16 == 0, "T alignment");
+static_assert(offsetof(HeadParams, Tm) % 16 == 0, "Tm alignment");
 static_assert(offsetof(HeadParams, Tqt) % 16 == 0, "Tqt alignment");
 static_assert(offsetof(HeadParams, s) % 16 == 0, "s alignment");
 static_assert(offsetof(HeadParams, bit_off) % 8 == 0, "bit_off alignment");
