@@ -204,8 +204,11 @@ aatc_status aatc_decode_attention(const void* dev_params_k, const void* dev_para
  * v_alpha) at position seq_len[b] - 1 of every sequence b (Alg. 1: the new key and value
  * are projected, quantized and appended), followed by aatc_decode_attention with the
  * same arguments; codes, scales and outputs are identical to that sequence of calls.
- * Sequences with seq_len[b] = 0 append nothing.  One launch where the decode kernel
- * takes the append into the workgroup that reads the new token's split.
+ * Sequences with seq_len[b] = 0 append nothing.  With G <= 8 and records of at most
+ * 64 bytes it is one launch: every workgroup of a (sequence, KV head) computes a share
+ * of the new token's exact transform coefficients into the workspace, and the
+ * workgroup that merges the splits quantizes and stores the token and adds its term to
+ * the attention.  Other shapes run the per-token encode before the decode launch.
  *
  * x_k, x_v   device [batch][n_kv_heads][d] new key / value token of each sequence,
  *            x_dtype F32 or BF16.
