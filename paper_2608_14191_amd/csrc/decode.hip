@@ -228,6 +228,20 @@ __device__ inline uint32_t pack_limbs(int x) {
   return ((uint32_t)x + 0x80808080u) ^ 0x80808080u;
 }
 
+// s_waitcnt immediates (gfx9 layout: vmcnt [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+constexpr int kWaitVm0 = (0x7 << 4) | (0xF << 8);            // vmcnt(0) only
+constexpr int kWaitLgkm0 = 0xF | (0x7 << 4) | (0x3 << 14);    // lgkmcnt(0) only
+
+// s_barrier alone, with no wait on outstanding memory operations (unlike __syncthreads(),
+// whose fence waits for every load of the wave, LDS transfers included).  The memory
+// clobber keeps the compiler's memory accesses on their side; the scheduling barriers
+// keep other instructions (and the waits they would bring) there too.
+__device__ inline void plain_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 // s_waitcnt vmcnt(n) for a wave-uniform n known only at run time (0 <= n < 64).
 __device__ inline void wait_vmcnt(int n) {
 #define AATC_VMW(k)                                                                         \
@@ -973,17 +987,26 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   const HeadParams* hv = head_params(a.params_v, kvh);
   const int t0 = split * S;
 
-  // (0) Loads that need nothing.  Every thread: the channel tables of channel cq.  The
-  //     plane-building threads (tc < NTC): T_K rows RJ jq .. RJ jq + RJ - 1 at columns
-  //     4 c4 .. + 3, the bit descriptors, the queries, and (fused append) their share of
-  //     the new token's transform.  Loads are unconditional (clamped indices or empty
+  // (0) Loads that need nothing, by the plane-building threads (tc < NTC): the channel
+  //     tables of channel cq, T_K rows RJ jq .. RJ jq + RJ - 1 at columns 4 c4 .. + 3,
+  //     the bit descriptors, the queries, and (fused append) their share of the new
+  //     token's transform.  Loads are unconditional (clamped indices or empty
   //     descriptors), so the wait counters stay exact.
   const bool cw = !DMA || wave < NWC;                 // builds the query planes (per wave)
   const int c4 = tid & 31, jq = (tid >> 5) % NJQ, cq = tid & (kD - 1);
-  const int kb = hk->bits[cq], koff = hk->bit_off[cq];
-  const float ks = hk->s[cq];
-  const int vbc = hv->bits[cq], voc = hv->bit_off[cq];
-  const float vsc = hv->s[cq];
+  // The channel tables: loaded up front by the plane-building waves, and by the issuing
+  // waves once their key transfers have landed (they use them only after the value phase).
+  int kb = 0, koff = 0, vbc = 0, voc = 0, v_budget = 0;
+  float ks = 0.f, vsc = 0.f;
+  auto load_tables = [&]() {
+    v_budget = hv->budget;
+    kb = hk->bits[cq];
+    koff = hk->bit_off[cq];
+    ks = hk->s[cq];
+    vbc = hv->bits[cq];
+    voc = hv->bit_off[cq];
+    vsc = hv->s[cq];
+  };
   v4f tr[RJ];
   uint2 desc[NPI];
   const bool q_bf = a.q_dtype == AATC_BF16;
@@ -991,14 +1014,15 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   bool qhi[NRC];
   // Fused append: dot products d = split + n_splits k, k = wave + NWC i, of the 2 x 128
   // (key channels, then value channels); the first two of each plane-building wave are
-  // fetched here (the token's two elements of this lane and the matching two of column
-  // d % kD of Tq), further ones (fewer than 32 splits) when they are computed.
+  // fetched up front (the token's two elements of this lane and the matching two of
+  // column d % kD of Tq), further ones (fewer than 32 splits) when they are computed.
   const int x_eb = a.x_dtype == AATC_BF16 ? 2 : 4;
   constexpr int KF = 2;                               // coefficients fetched up front
   int adk[KF];
   uint32_t ax[KF][2], atq[KF][2];
   float a_inv_s[KF];
-  if (cw) {
+  auto front_loads = [&]() {
+    load_tables();
 #pragma unroll
     for (int jj = 0; jj < RJ; ++jj)
       tr[jj] = reinterpret_cast<const v4f*>(hk->T)[(RJ * jq + jj) * (kD / 4) + c4];
@@ -1038,9 +1062,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
         a_inv_s[f] = eh->inv_s[ac];
       }
     }
-  }
-  if (tid < NH) qmx[tid] = 0u;
-  if (tid == 0) csync = 0u;
+  };
 
   Partial* parts = a.partials + row * a.n_splits * G;
   float* out_rows = a.out + ((int64_t)seq * a.n_q_heads + kvh * G) * kD;
@@ -1065,57 +1087,33 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   constexpr uint32_t kNone = 0x80000000u;
   v4i rk[DMA ? 1 : NLD], rv[DMA ? 1 : NLD], rak, rav;
   int nv_mine = 0;                                    // value-tile transfers of this wave
-  if constexpr (DMA) {
-    // Every wave's small loads are queued before the first cache transfer.
-    __syncthreads();
-    if (!cw) {
-      // 1 KiB transfers straight into LDS (lane l's 16 bytes at 16 l): key records, the
-      // token scales, then the value tiles, dealt to the issuing waves round robin.  Only
-      // whole 1 KiB blocks of the regions are written (their sizes are 1 KiB multiples).
-      constexpr int NWD = NW - NWC;
-      const int wd = wave - NWC;
-      const int nki = (n_load * RK + 1023) >> 10, nai = (2 * n_load + 1023) >> 10;
-      const int nvi = (n_load * RV + 1023) >> 10;
-      for (int j = wd; j < nki; j += NWD)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            krs, (__attribute__((address_space(3))) void*)(kbuf + 1024 * j), 16,
-            t0 * RK + 1024 * j + 16 * lane, 0, 0, 0);
-      for (int j = wd; j < nai; j += NWD) {
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            akrs, (__attribute__((address_space(3))) void*)((uint8_t*)akb + 1024 * j), 16,
-            2 * t0 + 1024 * j + 16 * lane, 0, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            avrs, (__attribute__((address_space(3))) void*)((uint8_t*)avb + 1024 * j), 16,
-            2 * t0 + 1024 * j + 16 * lane, 0, 0, 0);
-      }
-      for (int j = wd; j < nvi; j += NWD) {
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            vrs, (__attribute__((address_space(3))) void*)(vbuf + 1024 * j), 16,
-            t0 * RV + 1024 * j + 16 * lane, 0, 0, 0);
-        ++nv_mine;
-      }
+  // 1 KiB transfers straight into LDS (lane l's 16 bytes at 16 l): key records, the token
+  // scales, then the value tiles, dealt to the issuing waves round robin.  Only whole
+  // 1 KiB blocks of the regions are written (their sizes are 1 KiB multiples).
+  auto issue_cache = [&]() {
+    constexpr int NWD = NW - NWC;
+    const int wd = __builtin_amdgcn_readfirstlane(wave - NWC);
+    const int nki = (n_load * RK + 1023) >> 10, nai = (2 * n_load + 1023) >> 10;
+    const int nvi = (n_load * RV + 1023) >> 10;
+    for (int j = wd; j < nki; j += NWD)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          krs, (__attribute__((address_space(3))) void*)(kbuf + 1024 * j), 16,
+          t0 * RK + 1024 * j + 16 * lane, 0, 0, 0);
+    for (int j = wd; j < nai; j += NWD) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          akrs, (__attribute__((address_space(3))) void*)((uint8_t*)akb + 1024 * j), 16,
+          2 * t0 + 1024 * j + 16 * lane, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          avrs, (__attribute__((address_space(3))) void*)((uint8_t*)avb + 1024 * j), 16,
+          2 * t0 + 1024 * j + 16 * lane, 0, 0, 0);
     }
-  } else {
-    // Each wave issues its key records and token scales ahead of its value tiles.
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int idx = tid + i * NTHR;
-      rk[i] = buf_load16<0>(krs, idx < nk16 ? (uint32_t)(t0 * RK + 16 * idx) : kNone);
+    for (int j = wd; j < nvi; j += NWD) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          vrs, (__attribute__((address_space(3))) void*)(vbuf + 1024 * j), 16,
+          t0 * RV + 1024 * j + 16 * lane, 0, 0, 0);
+      ++nv_mine;
     }
-    {
-      const uint32_t aoff = (tid < na16) ? (uint32_t)(2 * t0 + 16 * tid) : kNone;
-      rak = buf_load16<0>(akrs, aoff);
-      rav = buf_load16<0>(avrs, aoff);
-    }
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int idx = tid + i * NTHR;
-      rv[i] = buf_load16<0>(vrs, idx < nv16 ? (uint32_t)(t0 * RV + 16 * idx) : kNone);
-    }
-    // Keep the compiler from moving work that waits on the early loads above the cache loads.
-    __builtin_amdgcn_sched_barrier(0);
-  }
+  };
   // No branch on the split's contents: an empty split computes on masked tokens and
   // stores (m, l, o~) = (-inf, 0, 0); records that do not match the parameters store a
   // NaN maximum (the value budget is clamped to the record so LDS accesses stay in range).
@@ -1146,7 +1144,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   float* qcl = qs;                                   // [NH][kD], over the consumed queries
   uint8_t* ql = smem + a.off_ql;                     // [4][NH][2 NP][64]
   float rcf[KF] = {0.f, 0.f};                        // fused append: this wave's coefficients
-  if (cw) {
+  auto build_planes = [&]() {
 #pragma unroll
     for (int r = 0; r < NRC; ++r) {
       const uint32_t w = qraw[r];
@@ -1244,14 +1242,58 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
           rcf[f] = append_coefficient(ax[f][0], ax[f][1], atq[f][0], atq[f][1], a.x_dtype,
                                       a_inv_s[f]);
     }
-  }
+  };
 
-  // (3) The key records and token scales in LDS: the issuing waves wait for their own
-  //     transfers of those (the value tiles may still be landing), or every wave stores
-  //     its registers (over the query-transform scratch).
+  // (3) Front.  Eight waves: the plane-building and the issuing waves take separate arms
+  //     up to the barrier where the key records and scales have landed; the value tiles
+  //     keep landing through the key phase.  The barriers are plain s_barrier after
+  //     explicit waits: __syncthreads() would make the issuing waves wait for all of their
+  //     transfers.  The explicit vmcnt(0) waits cost nothing (no load of the wave is in
+  //     flight there) but tell the compiler so: with the two arms merged, it would
+  //     otherwise take the other arm's loads as pending and wait on them later with counts
+  //     that also cover the cache transfers.
   if constexpr (DMA) {
-    if (!cw) wait_vmcnt(nv_mine);
+    if (cw) {
+      front_loads();
+      if (tid < NH) qmx[tid] = 0u;
+      if (tid == 0) csync = 0u;
+      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+      plain_barrier();                               // the small loads are queued first
+      build_planes();
+      __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    } else {
+      plain_barrier();
+      __builtin_amdgcn_s_waitcnt(kWaitVm0);
+      issue_cache();
+      wait_vmcnt(nv_mine);                           // key records and scales landed
+      load_tables();
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    plain_barrier();
   } else {
+    front_loads();
+    if (tid < NH) qmx[tid] = 0u;
+    if (tid == 0) csync = 0u;
+    // Each wave issues its key records and token scales ahead of its value tiles.
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int idx = tid + i * NTHR;
+      rk[i] = buf_load16<0>(krs, idx < nk16 ? (uint32_t)(t0 * RK + 16 * idx) : kNone);
+    }
+    {
+      const uint32_t aoff = (tid < na16) ? (uint32_t)(2 * t0 + 16 * tid) : kNone;
+      rak = buf_load16<0>(akrs, aoff);
+      rav = buf_load16<0>(avrs, aoff);
+    }
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int idx = tid + i * NTHR;
+      rv[i] = buf_load16<0>(vrs, idx < nv16 ? (uint32_t)(t0 * RV + 16 * idx) : kNone);
+    }
+    // Keep the compiler from moving work that waits on the early loads above the cache loads.
+    __builtin_amdgcn_sched_barrier(0);
+    build_planes();
     __syncthreads();                                 // the planes' scratch is consumed
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
@@ -1262,8 +1304,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
       reinterpret_cast<v4i*>(akb)[tid] = rak;
       reinterpret_cast<v4i*>(avb)[tid] = rav;
     }
+    __syncthreads();
   }
-  __syncthreads();
   v4i bq[NT][2 * NP];
   int fex[NT];
 #pragma unroll
@@ -1420,7 +1462,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
 
   // (6) Value bits x P limbs over all chunks of the split; value-bit tiles are dealt to
   //     the waves round robin.  O'(v) goes to LDS (over the consumed key records).
-  const int BV = min(hv->budget, 8 * RV);
+  const int BV = min(v_budget, 8 * RV);
   const int NVT = (BV + 15) >> 4;
   const uint32_t m0 = 0x01010101u << (2 * g), m1 = m0 << 1;
   float* ob = reinterpret_cast<float*>(smem + a.off_ob);   // [NH][ob_stride]
