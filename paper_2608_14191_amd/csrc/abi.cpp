@@ -13,6 +13,19 @@ namespace {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// bf16 of a finite fp32 value, round to nearest even, and back (exact).
+uint16_t f32_to_bf16_rne(float x) {
+  uint32_t u;
+  std::memcpy(&u, &x, 4);
+  return (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+float bf16_to_f32(uint16_t h) {
+  const uint32_t u = (uint32_t)h << 16;
+  float x;
+  std::memcpy(&x, &u, 4);
+  return x;
+}
+
 bool calibration_ok(const aatc_calibration& c) {
   if (c.d != kD) return false;
   int sum = 0, active = 0, prev = kMaxBits;
@@ -65,11 +78,15 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
       auto* hp = const_cast<HeadParams*>(head_params(host_buf, h));
       std::memcpy(hp->T, c.transform, sizeof(hp->T));
       for (int w = 0; w < 8; ++w)
-        for (int i = 0; i < 8; ++i)
+        for (int kk = 0; kk < 4; ++kk)
           for (int l = 0; l < 64; ++l)
-            for (int e = 0; e < 4; ++e)
-              hp->Tm[((w * 8 + i) * 64 + l) * 4 + e] =
-                  c.transform[(16 * w + l / 4) * kD + 32 * (l % 4) + 4 * i + e];
+            for (int e = 0; e < 8; ++e) {
+              const float x = c.transform[(16 * w + l % 16) * kD + 32 * kk + 8 * (l / 16) + e];
+              const uint16_t hi = f32_to_bf16_rne(x);
+              const uint16_t lo = f32_to_bf16_rne(x - bf16_to_f32(hi));
+              hp->Tm[(((w * 4 + kk) * 2 + 0) * 64 + l) * 8 + e] = hi;
+              hp->Tm[(((w * 4 + kk) * 2 + 1) * 64 + l) * 8 + e] = lo;
+            }
       for (int i = 0; i < kD * kD; ++i)
         hp->Tq[i] = (int16_t)std::nearbyint(std::ldexp((double)c.transform[i], kTFrac));
       for (int j = 0; j < kD; ++j)

@@ -70,6 +70,10 @@ struct DecodeArgs {
   int rk, rv;                     // record bytes
   float scale_log2e;
   int off_v, off_ak, off_av, off_ql, off_pb, off_ob, ob_stride, off_es;   // dynamic LDS layout
+  // T_V staged in LDS for the merge (eight waves): 8 KiB slice w (the rows wave w applies)
+  // at 8 KiB w over the key records for w < tv_nk, else at off_tv + 8 KiB (w - tv_nk);
+  // tv_nk < 0: the merge reads T_V from global memory.
+  int tv_nk, off_tv;
 };
 
 __device__ inline float load_q(const void* q, int dtype, int64_t idx) {
@@ -242,6 +246,25 @@ __device__ inline void plain_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
+// 16 bytes per lane from a raw buffer straight into LDS at lds_base + 16 lane (lanes whose
+// offset is past the descriptor write zeros), issued where the compiler does not see it:
+// its wait counting would otherwise make the next LDS read of the wave wait for the
+// transfer.  The caller waits (s_waitcnt vmcnt) before the destination is read.  M0 holds
+// the LDS base for the transfer and is restored; one wait state separates the M0 write
+// from the transfer that reads it.
+__device__ inline void lds_copy16_untracked(v4i desc, uint32_t lds_base, uint32_t voffset) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(voffset), "s"(desc)
+      : "memory");
+}
+
 // s_waitcnt vmcnt(n) for a wave-uniform n known only at run time (0 <= n < 64).
 __device__ inline void wait_vmcnt(int n) {
 #define AATC_VMW(k)                                                                         \
@@ -337,38 +360,72 @@ struct TvBlock {
   }
 };
 
-// o = T_V o~ with one output row per lane quad: lane l of wave w holds row 16 w' + l / 4
-// (w' = w + NTHR / 64 p over the passes p) at columns 32 (l % 4) .. + 31, read from the
-// merge-ordered copy of T_V in whole 1 KiB blocks; the quad sums its four parts (DPP).
+// o = T_V o~ on the matrix cores in bf16 pairs: with T = Th + Tl and o~ = oh + ol (each
+// term bf16, the second the first's remainder), T o~ = Th oh + Th ol + Tl oh up to
+// |Tl ol| + rounding, about 2^-16 relative; the three products accumulate in fp32
+// (v_mfma_f32_16x16x32_bf16).  Wave w computes output rows 16 w' .. + 15 (w' = w + NTHR /
+// 64 p over the passes p) for up to 16 vectors: A = its 16-row block of T (the
+// parameter block's operand-ordered copy), B column n = vector n.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// bf16 of x (round to nearest even) and of the remainder x - bf16(x).
+__device__ inline void bf16_pair(float x, __bf16& hi, __bf16& lo) {
+  hi = (__bf16)x;
+  lo = (__bf16)(x - (float)hi);
+}
+
 template <int NTHR>
-struct TvQuad {
+struct TvMfma {
   static constexpr int NPASS = 512 / NTHR;
   static_assert(NPASS * NTHR == 512, "256 or 512 threads");
-  v4f t[NPASS][8];
+  bf16x8 a[NPASS][4][2];                  // [pass][k-step][Th, Tl]
   __device__ void load(const HeadParams* hv) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const bf16x8* tp = reinterpret_cast<const bf16x8*>(hv->Tm);
 #pragma unroll
     for (int p = 0; p < NPASS; ++p)
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        t[p][i] = reinterpret_cast<const v4f*>(hv->Tm)[((wave + (NTHR / 64) * p) * 8 + i) * 64 + lane];
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+          a[p][kk][t] = tp[(((wave + (NTHR / 64) * p) * 4 + kk) * 2 + t) * 64 + lane];
   }
-  // osum: LDS [G][kD], complete (the caller synchronizes).  Calls sink(h, j, o_hj) once
-  // per output, from the quad's first lane.
+  // The same from this wave's 8 KiB block staged in LDS at byte offset slice (eight waves:
+  // one block per wave).  LDS-typed loads: a generic pointer would make these flat loads,
+  // which the compiler cannot count in order with the partials' loads.
+  __device__ void load_lds(uint32_t slice) {
+    const int lane = threadIdx.x & 63;
+    const __attribute__((address_space(3))) bf16x8* sp =
+        (const __attribute__((address_space(3))) bf16x8*)(uintptr_t)slice;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) a[0][kk][t] = sp[(kk * 2 + t) * 64 + lane];
+  }
+  // B operands in LDS: ob[t] (t = 0: oh, 1: ol) holds [k-step][lane] 16-byte units, lane
+  // 16 g + n: vector n at elements 32 kk + 8 g .. + 7 (put() writes one element).
+  __device__ static void put(__bf16* ob_hi, __bf16* ob_lo, int n, int c, float x) {
+    const int i = ((c >> 5) * 64 + 16 * ((c >> 3) & 3) + n) * 8 + (c & 7);
+    bf16_pair(x, ob_hi[i], ob_lo[i]);
+  }
+  // Calls sink(n, j0, o[j0 .. j0 + 3] of vector n) for n < G (the caller synchronizes
+  // after the puts).
   template <class Sink>
-  __device__ void apply(const float* osum, int G, Sink sink) const {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, q = lane & 3;
+  __device__ void apply(const __bf16* ob_hi, const __bf16* ob_lo, int G, Sink sink) const {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, n = lane & 15;
+    const bf16x8* bh = reinterpret_cast<const bf16x8*>(ob_hi);
+    const bf16x8* bl = reinterpret_cast<const bf16x8*>(ob_lo);
 #pragma unroll
     for (int p = 0; p < NPASS; ++p) {
-      const int j = 16 * (wave + (NTHR / 64) * p) + (lane >> 2);
-      for (int h = 0; h < G; ++h) {
-        const v4f* oh = reinterpret_cast<const v4f*>(osum + h * kD + 32 * q);
-        v4f acc = t[p][0] * oh[0];
+      v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = acc0, acc2 = acc0;
 #pragma unroll
-        for (int i = 1; i < 8; ++i) acc += t[p][i] * oh[i];
-        const float o = quad_sum((acc.x + acc.y) + (acc.z + acc.w));
-        if (q == 0) sink(h, j, o);
+      for (int kk = 0; kk < 4; ++kk) {
+        const bf16x8 h8 = bh[kk * 64 + lane], l8 = bl[kk * 64 + lane];
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[p][kk][0], h8, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[p][kk][0], l8, acc1, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[p][kk][1], h8, acc2, 0, 0, 0);
       }
+      if (n < G) sink(n, 16 * (wave + (NTHR / 64) * p) + 4 * (lane >> 4), acc0 + acc1 + acc2);
     }
   }
 };
@@ -509,7 +566,7 @@ template <int NTHR, int NH, class Hook>
 __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh, int64_t row,
                                                    int G, int n_splits, const Partial* partials,
                                                    unsigned* counters, float* out_rows,
-                                                   float* lds, Hook& hook) {
+                                                   float* lds, int tv_slice, Hook& hook) {
   constexpr int NP = (NH * kD + NTHR - 1) / NTHR;
   constexpr int kMergeB = NP == 1 ? 32 : 64 / NP;
   static_assert(NTHR % kD == 0 && NP * kMergeB <= 64 && kMergeB >= 8, "thread mapping");
@@ -526,7 +583,9 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
   if (!last_s) return;
   hook.prefetch();
   __builtin_amdgcn_sched_barrier(0);
-  float* osum = lds;                                       // [G][kD]
+  // The merged vectors as B operands of the T_V product (bf16 pairs, 2 x 4 KiB).
+  __bf16* ob_hi = reinterpret_cast<__bf16*>(lds);
+  __bf16* ob_lo = ob_hi + 4 * 64 * 8;
   const __amdgpu_buffer_rsrc_t prs =
       make_rsrc(partials + row * n_splits * G, (uint32_t)(n_splits * G * sizeof(Partial)));
   float M[NP], Ls[NP], acc[NP];
@@ -579,9 +638,12 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
   issue(0);
   // T_V after the first partials (a compute unit serves its loads in order; T_V is needed
   // last), then the hook's work while they are in flight.
-  const HeadParams* hv = head_params(params_v, kvh);
-  TvQuad<NTHR> tv;
-  tv.load(hv);
+  // T_V: staged in LDS by this wave (its transfers have landed), read now; else loaded from
+  // global memory just before it is applied (when no other load is in flight, so that the
+  // two paths' loads do not meet in the compiler's wait counting).
+  TvMfma<NTHR> tv;
+  const bool tv_staged = NTHR == 512 && __builtin_amdgcn_readfirstlane(tv_slice) >= 0;
+  if (tv_staged) tv.load_lds((uint32_t)__builtin_amdgcn_readfirstlane(tv_slice));
   hook.during_loads();
   consume(0);
   for (int s0 = kMergeB; s0 < n_splits; s0 += kMergeB) {
@@ -593,12 +655,15 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
     const int slot = p * NTHR + tid, h = slot / kD, c = slot % kD;
     if (h < G) {
       hook.fold1(h, c, M[p], Ls[p], acc[p]);
-      osum[slot] = bad[p] ? NAN : (Ls[p] > 0.f ? acc[p] / Ls[p] : 0.f);
+      TvMfma<NTHR>::put(ob_hi, ob_lo, h, c, bad[p] ? NAN : (Ls[p] > 0.f ? acc[p] / Ls[p] : 0.f));
     }
   }
+  if (!tv_staged) tv.load(head_params(params_v, kvh));
   __syncthreads();
   // o = T_V o~ (the partials are in the transformed domain).
-  tv.apply(osum, G, [&](int h, int j, float o) { out_rows[(int64_t)h * kD + j] = o; });
+  tv.apply(ob_hi, ob_lo, G, [&](int h, int j0, v4f o) {
+    *reinterpret_cast<v4f*>(out_rows + (int64_t)h * kD + j0) = o;
+  });
   hook.finish();
   if (tid == 0) counters[row * kCtrStride] = 0u;
 }
@@ -936,7 +1001,11 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
 // flight: q~ = T_K^T q (fp32), then per bit the 32-bit fixed-point limbs.
 // ---------------------------------------------------------------------------------------
 template <int NT, int NTILE, int NP, int NW, bool APPEND>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const DecodeArgs a) {
+// At most two waves per SIMD ever share a compute unit with this kernel (LDS holds one
+// eight-wave workgroup), so it may use up to 256 VGPRs per lane.
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * NW, 64 * NW),
+                          amdgpu_waves_per_eu(2, 2)))
+void decode_mfma_kernel(const DecodeArgs a) {
   constexpr int NTHR = 64 * NW;       // threads per workgroup
   constexpr int NH = 4 * NT;          // head slots: 4 per column tile
   constexpr int TW = 16 * NTILE;      // tokens per wave
@@ -1450,7 +1519,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   // The value tiles: the issuing waves wait for the rest of their transfers, or every
   // wave stores its registers (their region held nothing since the query transform).
   if constexpr (DMA) {
-    if (!cw) wait_vmcnt(0);
+    // (Every wave: no load of the plane-building waves is in flight here, and the explicit
+    // wait keeps the compiler from carrying the issuing waves' loads past this point.)
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
   } else {
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
@@ -1461,31 +1532,75 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
   __syncthreads();
 
   // (6) Value bits x P limbs over all chunks of the split; value-bit tiles are dealt to
-  //     the waves round robin.  O'(v) goes to LDS (over the consumed key records).
+  //     the waves round robin.  O'(v) goes to LDS (over the consumed key records with four
+  //     waves; its own region with eight, where T_V may be staged there).
   const int BV = min(v_budget, 8 * RV);
   const int NVT = (BV + 15) >> 4;
   const uint32_t m0 = 0x01010101u << (2 * g), m1 = m0 << 1;
   float* ob = reinterpret_cast<float*>(smem + a.off_ob);   // [NH][ob_stride]
-  // The splits of a (sequence, KV head) run on one XCD (block order above); each touches a
-  // slice of T_V here so that the merging workgroup finds it in that XCD's L2.
+  // T_V for the merge.  Each workgroup touches a slice so that the merging one finds T_V
+  // in L2 (the splits of a (sequence, KV head) run on one XCD; block order above).  Eight
+  // waves with room in LDS: every workgroup also stages it (the merging one is not known
+  // yet), each wave its own 8 KiB slice, while this phase runs.
+  int tv_slice = -1;                                  // LDS byte offset of this wave's slice
   const uint32_t tv_touch = reinterpret_cast<gdword>(reinterpret_cast<uintptr_t>(hv->Tm))[
       (split * NTHR + tid) * 16 % (kD * kD)];
+  if (DMA && a.tv_nk >= 0) {
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    uint8_t* dst = smem + (wv < a.tv_nk ? 8192 * wv : a.off_tv + 8192 * (wv - a.tv_nk));
+    const uint64_t tb = reinterpret_cast<uint64_t>(hv->Tm);
+    const v4i tdesc = {(int)(uint32_t)tb, (int)((uint32_t)(tb >> 32) & 0xffffu),
+                       (int)(kD * kD * sizeof(float)), kRsrcWord3};
+    const uint32_t lb = (uint32_t)reinterpret_cast<uintptr_t>(
+        (__attribute__((address_space(3))) uint8_t*)dst);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      lds_copy16_untracked(tdesc, lb + 1024 * j, 8192 * wv + 1024 * j + 16 * lane);
+    tv_slice = (int)lb;
+  }
   // B operands stay in registers when they fit (16 x 4 VGPRs).
   constexpr bool kPbRegs = NCH * NT <= 16;
   v4i pbr[kPbRegs ? NCH * NT : 1];
   if constexpr (kPbRegs) {
 #pragma unroll
-    for (int i = 0; i < NCH * NT; ++i) pbr[i] = pb[i * 64 + lane];
+    for (int i = 0; i < NCH * NT; ++i) {
+      pbr[i] = pb[i * 64 + lane];
+      asm volatile("" : "+v"(pbr[i]));             // kept in registers, not re-read per tile
+    }
   }
-  for (int vt = wave; vt < NVT; vt += NW) {
+  // LDS address of this lane's value-bit dword pair in each chunk for tile vt = wave; tile
+  // wave + NW it is 128 NW it bytes further (an immediate offset: no address arithmetic in
+  // the loop).
+  uint32_t vaddr[NCH];
+  {
+    const uint32_t vb = (uint32_t)reinterpret_cast<uintptr_t>(
+        (__attribute__((address_space(3))) uint8_t*)vbuf) + 8 * n + 128 * wave;
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      vaddr[ch] = vb + ch * kTile * RV;
+      asm volatile("" : "+v"(vaddr[ch]));          // computed once, not per tile
+    }
+  }
+  constexpr int kMaxIt = (64 * 8 / 16 + NW - 1) / NW;   // records of at most 64 bytes
+#pragma unroll
+  for (int it = 0; it < kMaxIt; ++it) {
+    const int vt = wave + NW * it;
+    if (vt >= NVT) break;                           // (uniform)
     v4i acc[4][NT];                                 // chunk % 4: four MFMA chains
 #pragma unroll
     for (int c4 = 0; c4 < 4; ++c4)
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) acc[c4][rt] = (v4i){0, 0, 0, 0};
+    // All of the tile's value-bit words first (one LDS round trip), then the products.
+    typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+    v2u wws[NCH];
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch)
+      wws[ch] = *(const __attribute__((address_space(3))) v2u*)(uintptr_t)(
+          vaddr[ch] + 128 * NW * it);
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
-      const uint2 ww = *reinterpret_cast<const uint2*>(vbuf + ch * kTile * RV + 8 * (16 * vt + n));
+      const v2u ww = wws[ch];
       const v4i av4 = {(int)(ww.x & m0), (int)(ww.x & m1), (int)(ww.y & m0), (int)(ww.y & m1)};
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) {
@@ -1553,6 +1668,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     buf_store16_coherent((v4f){layout_ok ? m : NAN, l, 0.f, 0.f}, prs,
                          (uint32_t)((split * G + tid) * sizeof(Partial)));
   }
+  // The merge's 8 KiB scratch: over the consumed value operands with eight waves (the key
+  // record region may hold T_V), over the key records with four.
+  float* merge_scratch = reinterpret_cast<float*>(smem + (DMA ? a.off_pb : 0));
   if constexpr (APPEND) {
     AppendHook<NTHR, NR> hook;
     hook.coeff = a.append_r + row * 2 * kD;
@@ -1576,11 +1694,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void decode_mfma_kernel(const Deco
     for (int r = 0; r < NR; ++r) hook.qck[r] = qck[r];
     hook.sc = reinterpret_cast<AppendScratch*>(smem + a.off_es);
     merge_if_last_wide<NTHR, NH>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
-                                 out_rows, reinterpret_cast<float*>(smem), hook);
+                                 out_rows, merge_scratch, tv_slice, hook);
   } else {
     NoHook none;
     merge_if_last_wide<NTHR, NH>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
-                                 out_rows, reinterpret_cast<float*>(smem), none);
+                                 out_rows, merge_scratch, tv_slice, none);
   }
 }
 
@@ -1621,17 +1739,37 @@ static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
   if (DMA) pb_bytes = std::max(pb_bytes, scr_bytes);
   size_t off = (size_t)a.off_pb + pb_bytes;
   a.ob_stride = 8 * a.rv;
-  if ((size_t)NH * a.ob_stride * 4 <= (size_t)S * a.rk) {
-    a.off_ob = 0;
-  } else {
-    a.off_ob = (int)off;
-    off += (size_t)NH * a.ob_stride * 4;
+  const size_t ob_bytes = (size_t)NH * a.ob_stride * 4;
+  const size_t es_bytes = APPEND ? (sizeof(AppendScratch) + 15) / 16 * 16 : 0;
+  constexpr size_t kLdsMax = 160 * 1024 - 4 * 1024;
+  // Eight waves: O' in its own region and T_V staged for the merge, 8 KiB slices over the
+  // key records (free after the key phase) and the rest after everything else, when that
+  // fits; otherwise O' over the key records and T_V from global memory.
+  a.tv_nk = -1;
+  a.off_tv = 0;
+  if (DMA) {
+    const int nk = (int)std::min<size_t>(8, (size_t)S * a.rk / 8192);
+    const size_t off_tv = round256(off + ob_bytes + es_bytes);
+    if (off_tv + (size_t)(8 - nk) * 8192 <= kLdsMax) {
+      a.tv_nk = nk;
+      a.off_ob = (int)off;
+      a.off_es = (int)(off + ob_bytes);
+      a.off_tv = (int)off_tv;
+      off = off_tv + (size_t)(8 - nk) * 8192;
+    }
   }
-
-  a.off_es = (int)off;
-  if (APPEND) off += (sizeof(AppendScratch) + 15) / 16 * 16;
+  if (a.tv_nk < 0) {
+    if (ob_bytes <= (size_t)S * a.rk) {
+      a.off_ob = 0;
+    } else {
+      a.off_ob = (int)off;
+      off += ob_bytes;
+    }
+    a.off_es = (int)off;
+    off += es_bytes;
+  }
   const size_t lds = off;
-  if (lds > 160 * 1024 - 4 * 1024) return AATC_E_UNSUPPORTED;
+  if (lds > kLdsMax) return AATC_E_UNSUPPORTED;
   static size_t set_lds = 0;
   if (lds > set_lds) {
     if (hipFuncSetAttribute((const void*)decode_mfma_kernel<NT, NTILE, NP, NW, APPEND>,

@@ -18,9 +18,11 @@ constexpr uint32_t kMagic = 0x43544141u;  // "AATC"
 
 struct alignas(256) HeadParams {
   float T[kD * kD];               // [j][c] transform, storage channels (fp32)
-  // The same transform in the decode merge's load order: 16-byte unit (8 w + i) 64 + l
-  // holds T[16 w + l / 4][32 (l % 4) + 4 i .. + 3], w, i < 8, l < 64.
-  float Tm[kD * kD];
+  // The same transform as two bf16 terms, Th = bf16(T) and Tl = bf16(T - Th), laid out as
+  // the decode merge's matrix-core A operands: 16-byte unit ((4 w + kk) 2 + t) 64 + l holds
+  // term t (0: Th, 1: Tl) of T[16 w + l % 16][32 kk + 8 (l / 16) .. + 7], w < 8, kk < 4,
+  // l < 64 (8 KiB per block of 16 rows).
+  uint16_t Tm[2 * kD * kD];
   int16_t Tq[kD * kD];            // [j][c] rint(T * 2^14), |Tq| <= 2^14
   int16_t Tqt[kD * kD];           // [c][j] the same, transposed
   float inv_s[kD];                // fp32 1/s_c (0 for dropped or zero-scale channels)

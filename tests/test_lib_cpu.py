@@ -123,6 +123,43 @@ def test_params_pack_validation():
         P.aatc_params_pack([bad])
 
 
+def test_params_pack_bf16_pair_copy_of_transform():
+    """The parameter block's bf16-pair copy of T (the merge's matrix-core operands):
+    unit ((4 w + kk) 2 + t) 64 + l holds term t of T[16 w + l % 16][32 kk + 8 (l / 16) ..
+    + 7]; the first term is T rounded to bf16 (nearest even), the second the remainder
+    rounded likewise, so the pair is within 2^-16 |T| + 2^-133 of T."""
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((512, 128)).astype(np.float32)
+    cals = [abi_calibration(ora.calibrate(x + 0.1 * h, 2.75)) for h in range(2)]
+    blk = P.aatc_params_pack(cals)
+    hp_bytes = (P.aatc_params_bytes(2) - 256) // 2
+    for h in range(2):
+        base = 256 + h * hp_bytes
+        T = np.frombuffer(blk, dtype=np.float32, count=128 * 128, offset=base).reshape(128, 128)
+        assert np.array_equal(T, np.asarray(cals[h].transform, dtype=np.float32).reshape(128, 128))
+        tm = np.frombuffer(blk, dtype=np.uint16, count=2 * 128 * 128,
+                           offset=base + 128 * 128 * 4).reshape(8, 4, 2, 64, 8)
+        def as_f32(b):
+            return (b.astype(np.uint32) << 16).view(np.float32)
+        hi = np.empty((128, 128), np.float32)
+        lo = np.empty((128, 128), np.float32)
+        for w in range(8):
+            for kk in range(4):
+                for l in range(64):
+                    j, c0 = 16 * w + l % 16, 32 * kk + 8 * (l // 16)
+                    hi[j, c0:c0 + 8] = as_f32(tm[w, kk, 0, l])
+                    lo[j, c0:c0 + 8] = as_f32(tm[w, kk, 1, l])
+        # the first term: nearest bf16 (ties even), by a direct search of the neighbours
+        u = T.view(np.uint32)
+        down = (u & 0xffff0000).view(np.float32)
+        up = ((u & 0xffff0000) + 0x10000).astype(np.uint32).view(np.float32)
+        d_down, d_up = np.abs(T - down), np.abs(up - T)
+        even_down = ((u >> 16) & 1) == 0
+        want = np.where((d_down < d_up) | ((d_down == d_up) & even_down), down, up)
+        assert np.array_equal(hi, want)
+        assert np.all(np.abs(T.astype(np.float64) - hi - lo) <= 2.0 ** -16 * np.abs(T) + 2.0 ** -133)
+
+
 def _fake(addr=4096):
     return ctypes.c_void_p(addr)
 
