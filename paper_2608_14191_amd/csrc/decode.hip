@@ -597,11 +597,16 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       const int slot = p * NTHR + tid, h = min(slot / kD, G - 1), c = slot % kD;
-      const uint32_t hoff = (uint32_t)(((s0 + (lane & (kMergeB - 1))) * G + h) * sizeof(Partial));
+      // 32-bit offsets (the descriptor holds less than 2^31 bytes): split u's part is a
+      // uniform product, the rest 24-bit (no 64-bit multiply-adds on pending registers).
+      const uint32_t step = (uint32_t)G * (uint32_t)sizeof(Partial);
+      const uint32_t hoff = __umul24((uint32_t)(s0 + (lane & (kMergeB - 1))), step) +
+                            __umul24((uint32_t)h, (uint32_t)sizeof(Partial));
       hd[p] = buf_load8_coherent(prs, (slot / kD < G) ? hoff : 0x80000000u);
 #pragma unroll
       for (int u = 0; u < kMergeB; ++u) {
-        const uint32_t off = (uint32_t)(((s0 + u) * G + h) * sizeof(Partial) + 16 + 4 * c);
+        const uint32_t off = (uint32_t)(s0 + u) * step +
+                             __umul24((uint32_t)h, (uint32_t)sizeof(Partial)) + 16 + 4 * c;
         ov[p][u] = __int_as_float(
             __builtin_amdgcn_raw_buffer_load_b32(prs, (slot / kD < G) ? (int)off : (int)0x80000000,
                                                  0, kCoherent));
@@ -638,13 +643,14 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
   issue(0);
   // T_V after the first partials (a compute unit serves its loads in order; T_V is needed
   // last), then the hook's work while they are in flight.
-  // T_V: staged in LDS by this wave (its transfers have landed), read now; else loaded from
-  // global memory just before it is applied (when no other load is in flight, so that the
-  // two paths' loads do not meet in the compiler's wait counting).
+  // T_V: staged in LDS by this wave (its transfers have landed), read after the hook's LDS
+  // work while the partials land; else loaded from global memory just before it is applied
+  // (when no other load is in flight, so that the two paths' loads do not meet in the
+  // compiler's wait counting).
   TvMfma<NTHR> tv;
   const bool tv_staged = NTHR == 512 && __builtin_amdgcn_readfirstlane(tv_slice) >= 0;
-  if (tv_staged) tv.load_lds((uint32_t)__builtin_amdgcn_readfirstlane(tv_slice));
   hook.during_loads();
+  if (tv_staged) tv.load_lds((uint32_t)__builtin_amdgcn_readfirstlane(tv_slice));
   consume(0);
   for (int s0 = kMergeB; s0 < n_splits; s0 += kMergeB) {
     issue(s0);
@@ -684,10 +690,8 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
 // ---------------------------------------------------------------------------------------
 struct AppendScratch {                 // LDS region of its own
   uint32_t erec[2][kMaxBudget / 32];   // key record, value record
-  int ecode[2][kD];                    // signed codes
   float vnew[kD];                      // transformed value of the token
-  float red[8];
-  float zpart[16];                     // per-wave sums of the token's score terms
+  float znew[16];                      // the token's log2-domain score per head
   uint32_t ea16[2];                    // fp16 scales
 };
 
@@ -711,9 +715,9 @@ __device__ inline float append_coefficient(uint32_t x0, uint32_t x1, uint32_t t0
   return fixed_point_result(hi * 65536 + lo, shift) * inv_s;
 }
 
-template <int NTHR, int NR>
+template <int NTHR, int NH>
 struct AppendHook {
-  static_assert(NTHR >= 2 * kD && NR * NTHR / 64 <= 16, "thread mapping");
+  static_assert(NTHR >= 2 * kD && NH <= 16, "thread mapping");
   uint8_t* k_codes;
   uint16_t* k_alpha;
   uint8_t* v_codes;
@@ -722,59 +726,70 @@ struct AppendHook {
   int64_t row, cap;
   int len, G, rk, rv;
   bool on;                             // the sequence has a token to append
-  int kb, koff, vbc, voc;              // tables of channel tid % kD
-  float vsc;
-  float qck[NR];                       // Q_c of (head (r NTHR + tid) / kD, channel tid % kD)
+  // Wave 0 encodes the key token, wave 1 the value token, lane l channels l and l + 64:
+  int e_b[2], e_off[2];                // their widths and first record bits
+  float e_s[2];                        // their scales s_c (value token)
+  float qk[2][NH];                     // Q_c of every head for them (key token)
   AppendScratch* sc;
-  float r;                             // coefficient of tensor tid / kD, channel tid % kD
+  float r2[2];                         // their coefficients r_c = h_c / s_c
 
   __device__ void prefetch() {
-    const int tid = threadIdx.x;
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(coeff, on ? (uint32_t)(2 * kD * 4) : 0u);
-    r = __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, 4 * min(tid, 2 * kD - 1), 0,
-                                                             kCoherent));
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const __amdgpu_buffer_rsrc_t rs =
+        make_rsrc(coeff, (on && wave < 2) ? (uint32_t)(2 * kD * 4) : 0u);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      r2[i] = __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+          rs, 4 * ((wave & 1) * kD + lane + 64 * i), 0, kCoherent));
   }
 
+  // The token's codes, scales, score per head and transformed value, each tensor by one
+  // wave (wave reductions only); one barrier publishes them.
   __device__ void during_loads() {
     if (!on) return;                   // uniform over the workgroup
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int et = tid >> 7, cq = tid & (kD - 1);              // et < 2: waves 0..3
-    const int eb = et ? vbc : kb, eoff = et ? voc : koff;
-    if (tid < 2 * (kMaxBudget / 32)) (&sc->erec[0][0])[tid] = 0u;
-    if (tid < 2 * kD) {
-      const float am = wave_max_dpp(eb > 0 ? fabsf(r) : 0.f);
-      if (lane == 0) sc->red[wave] = am;
-    }
-    __syncthreads();
-    if (tid < 2 * kD) {
-      const __half a16 = token_alpha(fmaxf(sc->red[2 * et], sc->red[2 * et + 1]));
-      int code = 0;
-      if (eb > 0) {
-        const uint32_t u = quantize_code(r, inverse_alpha(a16), eb);
-        atomicOr(&sc->erec[et][eoff >> 5], u << (eoff & 31));
-        if ((eoff & 31) + eb > 32) atomicOr(&sc->erec[et][(eoff >> 5) + 1], u >> (32 - (eoff & 31)));
-        code = (int)(u << (32 - eb)) >> (32 - eb);      // sign-extended b-bit code
-      }
-      sc->ecode[et][cq] = code;
-      if (cq == 0) sc->ea16[et] = __half_as_ushort(a16);
-    }
-    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (wave < 2) {
+      const int et = wave;
+      if (lane < kMaxBudget / 32) sc->erec[et][lane] = 0u;
+      float m = 0.f;
 #pragma unroll
-    for (int r2 = 0; r2 < NR; ++r2) {
-      const float t = kb ? qck[r2] * ldexpf((float)sc->ecode[0][cq], 1 - kb) : 0.f;
-      const float w = wave_sum_dpp(t);
-      if (lane == 0) sc->zpart[(r2 * NTHR + tid) >> 6] = w;
+      for (int i = 0; i < 2; ++i) m = fmaxf(m, e_b[i] > 0 ? fabsf(r2[i]) : 0.f);
+      const __half a16 = token_alpha(wave_max_dpp(m));
+      const float inv = inverse_alpha(a16);
+      int code[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        code[i] = 0;
+        const int eb = e_b[i], eoff = e_off[i];
+        if (eb > 0) {
+          const uint32_t u = quantize_code(r2[i], inv, eb);
+          atomicOr(&sc->erec[et][eoff >> 5], u << (eoff & 31));
+          if ((eoff & 31) + eb > 32) atomicOr(&sc->erec[et][(eoff >> 5) + 1], u >> (32 - (eoff & 31)));
+          code[i] = (int)(u << (32 - eb)) >> (32 - eb);      // sign-extended b-bit code
+        }
+      }
+      const float af = __half2float(a16);
+      if (et == 0) {
+#pragma unroll
+        for (int h = 0; h < NH; ++h) {
+          float t = 0.f;
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            t += e_b[i] ? qk[i][h] * ldexpf((float)code[i], 1 - e_b[i]) : 0.f;
+          const float z = wave_sum_dpp(t);
+          if (lane == 0) sc->znew[h] = af * z;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          sc->vnew[lane + 64 * i] = e_b[i] ? ldexpf(af * e_s[i] * (float)code[i], 1 - e_b[i]) : 0.f;
+      }
+      if (lane == 0) sc->ea16[et] = __half_as_ushort(a16);
     }
-    if (tid < kD)
-      sc->vnew[tid] = vbc ? ldexpf(half_bits_to_float((uint16_t)sc->ea16[1]) * vsc *
-                                       (float)sc->ecode[1][tid], 1 - vbc)
-                          : 0.f;
-    __syncthreads();                   // zpart, vnew and the scales visible from here on
+    __syncthreads();                   // codes, scales, znew and vnew visible from here on
   }
-  // The token's log2-domain score for head h (every reader forms it from the wave sums).
-  __device__ float znew(int h) const {
-    return half_bits_to_float((uint16_t)sc->ea16[0]) * (sc->zpart[2 * h] + sc->zpart[2 * h + 1]);
-  }
+  // The token's log2-domain score for head h.
+  __device__ float znew(int h) const { return sc->znew[h]; }
 
   __device__ void fold(int h, int c4, float& M, float& Ls, v4f& acc) const {
     if (!on) return;
@@ -1067,8 +1082,21 @@ void decode_mfma_kernel(const DecodeArgs a) {
   // waves once their key transfers have landed (they use them only after the value phase).
   int kb = 0, koff = 0, vbc = 0, voc = 0, v_budget = 0;
   float ks = 0.f, vsc = 0.f;
+  // Fused append: waves 0 and 1 encode the key and the value token, lane l channels l and
+  // l + 64 (their widths, first bits and scales).
+  int e_b[2] = {0, 0}, e_off[2] = {0, 0};
+  float e_s[2] = {0.f, 0.f};
   auto load_tables = [&]() {
     v_budget = hv->budget;
+    if (APPEND && wave < 2) {
+      const HeadParams* eh = wave == 0 ? hk : hv;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        e_b[i] = eh->bits[lane + 64 * i];
+        e_off[i] = eh->bit_off[lane + 64 * i];
+        e_s[i] = eh->s[lane + 64 * i];
+      }
+    }
     kb = hk->bits[cq];
     koff = hk->bit_off[cq];
     ks = hk->s[cq];
@@ -1385,12 +1413,17 @@ void decode_mfma_kernel(const DecodeArgs a) {
       bq[rt][s] = *reinterpret_cast<const v4i*>(ql + ((L * NH + h) * 2 * NP + s) * 64 + 16 * g);
     fex[rt] = fexp_s[h];
   }
-  // Q_c per (head, channel) item, for a fused append (eight waves: the planes' scratch
-  // is intact until the softmax writes the value operands).
-  float qck[NR] = {};
+  // Q_c of every head for channels lane and lane + 64, for the fused append's key token
+  // (eight waves: the planes' scratch is intact until the softmax writes the value
+  // operands).
+  float qk[2][NH] = {};
   if constexpr (APPEND) {
+    if (wave == 0) {
 #pragma unroll
-    for (int r = 0; r < NR; ++r) qck[r] = qcl[((r * NTHR + tid) / kD) * kD + cq];
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int h = 0; h < NH; ++h) qk[i][h] = qcl[h * kD + lane + 64 * i];
+    }
   }
 
   // (4) Key scores of this wave's tokens: lane L of a quad ends with token 4 g + L.
@@ -1672,7 +1705,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
   // record region may hold T_V), over the key records with four.
   float* merge_scratch = reinterpret_cast<float*>(smem + (DMA ? a.off_pb : 0));
   if constexpr (APPEND) {
-    AppendHook<NTHR, NR> hook;
+    AppendHook<NTHR, NH> hook;
     hook.coeff = a.append_r + row * 2 * kD;
     hook.k_codes = a.k_codes;
     hook.k_alpha = a.k_alpha;
@@ -1685,13 +1718,14 @@ void decode_mfma_kernel(const DecodeArgs a) {
     hook.rk = RK;
     hook.rv = RV;
     hook.on = len > 0;
-    hook.kb = kb;
-    hook.koff = koff;
-    hook.vbc = vbc;
-    hook.voc = voc;
-    hook.vsc = vsc;
 #pragma unroll
-    for (int r = 0; r < NR; ++r) hook.qck[r] = qck[r];
+    for (int i = 0; i < 2; ++i) {
+      hook.e_b[i] = e_b[i];
+      hook.e_off[i] = e_off[i];
+      hook.e_s[i] = e_s[i];
+#pragma unroll
+      for (int h = 0; h < NH; ++h) hook.qk[i][h] = qk[i][h];
+    }
     hook.sc = reinterpret_cast<AppendScratch*>(smem + a.off_es);
     merge_if_last_wide<NTHR, NH>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
                                  out_rows, merge_scratch, tv_slice, hook);
