@@ -180,6 +180,63 @@ __device__ inline int wave_sum_i32(int v) {         // exact while the sum fits 
   v += dpp_i<0x128>(v);
   return xor32_sum(xor16_sum(v));
 }
+// One step of a reduce-scatter across lanes l and l ^ BIT (BIT = 8, 16 or 32): the lane
+// with that bit clear keeps the sums of the lower half of the C values, the other the
+// upper half.  (The row swaps return the pair ordered by lane: lower lane's value first.)
+template <int C, int BIT>
+__device__ inline void reduce_scatter_step(const float (&in)[C], float (&out)[C / 2]) {
+  const bool up = (threadIdx.x & BIT) != 0;
+#pragma unroll
+  for (int i = 0; i < C / 2; ++i) {
+    const float k = up ? in[C / 2 + i] : in[i];
+    const float s = up ? in[i] : in[C / 2 + i];
+    float p;
+    if constexpr (BIT == 32) {
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+      p = __uint_as_float(up ? r[0] : r[1]);
+    } else if constexpr (BIT == 16) {
+      const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+      p = __uint_as_float(up ? r[0] : r[1]);
+    } else {
+      static_assert(BIT == 8, "bits 3, 4, 5");
+      p = dpp_f<0x128>(s);                     // row_ror:8 within rows of 16: lane l ^ 8
+    }
+    out[i] = k + p;
+  }
+}
+
+// N independent reductions taken step by step together, so that each step's exchanges
+// overlap (a single chain waits on every step).
+template <int N>
+__device__ inline void wave_max_n(float (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dpp_f<0xB1>(v[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dpp_f<0x4E>(v[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dpp_f<0x124>(v[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dpp_f<0x128>(v[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = xor16_max(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = xor32_max(v[i]);
+}
+template <int N>
+__device__ inline void wave_sum_i32_n(int (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += dpp_i<0xB1>(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += dpp_i<0x4E>(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += dpp_i<0x124>(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += dpp_i<0x128>(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = xor16_sum(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = xor32_sum(v[i]);
+}
 
 __device__ inline float block_reduce(float v, bool is_max, float* scratch) {
 #pragma unroll
@@ -715,6 +772,38 @@ __device__ inline float append_coefficient(uint32_t x0, uint32_t x1, uint32_t t0
   return fixed_point_result(hi * 65536 + lo, shift) * inv_s;
 }
 
+// F coefficients at once (the same arithmetic, reductions interleaved).
+template <int F>
+__device__ inline void append_coefficients(const uint32_t (&x)[F][2], const uint32_t (&t)[F][2],
+                                           int x_dtype, const float (&inv_s)[F], float (&out)[F]) {
+  const int lane = threadIdx.x & 63;
+  const bool bf = x_dtype == AATC_BF16;
+  float xa[F], xb[F], m[F];
+#pragma unroll
+  for (int f = 0; f < F; ++f) {
+    xa[f] = bf ? __uint_as_float(((lane & 1) ? (x[f][0] >> 16) : (x[f][0] & 0xffffu)) << 16)
+               : __uint_as_float(x[f][0]);
+    xb[f] = bf ? __uint_as_float(((lane & 1) ? (x[f][1] >> 16) : (x[f][1] & 0xffffu)) << 16)
+               : __uint_as_float(x[f][1]);
+    m[f] = fmaxf(fabsf(xa[f]), fabsf(xb[f]));
+  }
+  wave_max_n(m);
+  int shift[F], hl[2 * F];
+#pragma unroll
+  for (int f = 0; f < F; ++f) {
+    shift[f] = token_shift(m[f]);
+    const int ta = (int)(int16_t)((lane & 1) ? (t[f][0] >> 16) : (t[f][0] & 0xffffu));
+    const int tb = (int)(int16_t)((lane & 1) ? (t[f][1] >> 16) : (t[f][1] & 0xffffu));
+    const int p = (int)rintf(ldexpf(xa[f], shift[f])) * ta + (int)rintf(ldexpf(xb[f], shift[f])) * tb;
+    hl[2 * f] = p >> 16;
+    hl[2 * f + 1] = p & 0xffff;
+  }
+  wave_sum_i32_n(hl);
+#pragma unroll
+  for (int f = 0; f < F; ++f)
+    out[f] = fixed_point_result((long long)hl[2 * f] * 65536 + hl[2 * f + 1], shift[f]) * inv_s[f];
+}
+
 template <int NTHR, int NH>
 struct AppendHook {
   static_assert(NTHR >= 2 * kD && NH <= 16, "thread mapping");
@@ -1077,11 +1166,19 @@ void decode_mfma_kernel(const DecodeArgs a) {
   //     token's transform.  Loads are unconditional (clamped indices or empty
   //     descriptors), so the wait counters stay exact.
   const bool cw = !DMA || wave < NWC;                 // builds the query planes (per wave)
-  const int c4 = tid & 31, jq = (tid >> 5) % NJQ, cq = tid & (kD - 1);
+  // The query transform: lane l of plane-building wave w holds T_K rows RJ jq .. + RJ - 1
+  // (row block jq = l / 8) at columns 4 c4 .. + 3 (c4 = 8 w + l % 8), so the sums over the
+  // row blocks stay inside the wave.
+  static_assert(NJQ == 8 && RJ == 16 && NWC == 4, "query transform mapping");
+  const int jq = lane >> 3, c4 = 8 * (wave % NWC) + (lane & 7), cq = tid & (kD - 1);
+  constexpr int NVL = NH / 2;                   // q~ values a lane ends with
+  // Scale and width of the lane's channels 4 c4 + (NVL jq + i) % 4 (head (NVL jq + i) / 4).
+  float ksq[NVL];
+  int kbq[NVL];
   // The channel tables: loaded up front by the plane-building waves, and by the issuing
   // waves once their key transfers have landed (they use them only after the value phase).
-  int kb = 0, koff = 0, vbc = 0, voc = 0, v_budget = 0;
-  float ks = 0.f, vsc = 0.f;
+  int vbc = 0, voc = 0, v_budget = 0;
+  float vsc = 0.f;
   // Fused append: waves 0 and 1 encode the key and the value token, lane l channels l and
   // l + 64 (their widths, first bits and scales).
   int e_b[2] = {0, 0}, e_off[2] = {0, 0};
@@ -1097,9 +1194,6 @@ void decode_mfma_kernel(const DecodeArgs a) {
         e_s[i] = eh->s[lane + 64 * i];
       }
     }
-    kb = hk->bits[cq];
-    koff = hk->bit_off[cq];
-    ks = hk->s[cq];
     vbc = hv->bits[cq];
     voc = hv->bit_off[cq];
     vsc = hv->s[cq];
@@ -1120,6 +1214,12 @@ void decode_mfma_kernel(const DecodeArgs a) {
   float a_inv_s[KF];
   auto front_loads = [&]() {
     load_tables();
+#pragma unroll
+    for (int i = 0; i < NVL; ++i) {
+      const int c = 4 * c4 + ((NVL * jq + i) & 3);
+      ksq[i] = hk->s[c];
+      kbq[i] = hk->bits[c];
+    }
 #pragma unroll
     for (int jj = 0; jj < RJ; ++jj)
       tr[jj] = reinterpret_cast<const v4f*>(hk->T)[(RJ * jq + jj) * (kD / 4) + c4];
@@ -1238,7 +1338,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
   // eight waves, over the cache region with four (the cache lands after the planes).
   float* scr = reinterpret_cast<float*>(smem + (DMA ? a.off_pb : 0));   // [NJQ][NH][kD]
   float* qs = scr + NJQ * NH * kD;                                     // [NH][kD]
-  float* qcl = qs;                                   // [NH][kD], over the consumed queries
+  float* qcl = scr;                                  // [NH][kD]
   uint8_t* ql = smem + a.off_ql;                     // [4][NH][2 NP][64]
   float rcf[KF] = {0.f, 0.f};                        // fused append: this wave's coefficients
   auto build_planes = [&]() {
@@ -1250,7 +1350,9 @@ void decode_mfma_kernel(const DecodeArgs a) {
       qs[r * NTC + tid] = ((r * NTC + tid) / kD < G) ? qv : 0.f;
     }
     plane_sync();                                    // qs, qmx
-    // q~ = T_K^T q: RJ-row partial sums per thread, then over the NJQ row blocks.
+    // q~ = T_K^T q: RJ-row partial sums per lane, then over the wave's 8 row blocks
+    // (reduce-scatter across lane bits 3..5): lane l ends with value NVL jq + i of the 4 NH
+    // (head, column) sums of its column quad.
     {
       v4f acc[NH];
 #pragma unroll
@@ -1262,24 +1364,36 @@ void decode_mfma_kernel(const DecodeArgs a) {
           const v4f qv = *reinterpret_cast<const v4f*>(qs + h * kD + RJ * jq + jj);
           acc[h] += tr[jj] * qv.x + tr[jj + 1] * qv.y + tr[jj + 2] * qv.z + tr[jj + 3] * qv.w;
         }
+      float v0[4 * NH], v1[2 * NH], v2[NH], v3[NVL];
 #pragma unroll
-      for (int h = 0; h < NH; ++h) reinterpret_cast<v4f*>(scr)[(jq * NH + h) * (kD / 4) + c4] = acc[h];
+      for (int h = 0; h < NH; ++h) {
+        v0[4 * h] = acc[h].x;
+        v0[4 * h + 1] = acc[h].y;
+        v0[4 * h + 2] = acc[h].z;
+        v0[4 * h + 3] = acc[h].w;
+      }
+      reduce_scatter_step<4 * NH, 32>(v0, v1);
+      reduce_scatter_step<2 * NH, 16>(v1, v2);
+      reduce_scatter_step<NH, 8>(v2, v3);
+      // Channel weight Q_c = q~_c s_c scale log2(e) (the weight of the code's sign bit up
+      // to sign), kept in LDS; the largest |Q_c| of a head sets its fixed-point exponent.
+      const int hl = (NVL * jq) >> 2;                // the lane's head
+      float mloc = 0.f;
+#pragma unroll
+      for (int i = 0; i < NVL; ++i) {
+        const int c = 4 * c4 + ((NVL * jq + i) & 3);
+        const float qc = (hl < G && kbq[i] > 0) ? v3[i] * ksq[i] * a.scale_log2e : 0.f;
+        qcl[hl * kD + c] = qc;
+        mloc = fmaxf(mloc, fabsf(qc));
+      }
+      // Over the lanes that hold head hl: lane bits 0..2, and bit 3 when NH = 4.
+      mloc = fmaxf(mloc, dpp_f<0xB1>(mloc));         // quad_perm [1,0,3,2]
+      mloc = fmaxf(mloc, dpp_f<0x4E>(mloc));         // quad_perm [2,3,0,1]
+      mloc = fmaxf(mloc, dpp_f<0x141>(mloc));        // row_half_mirror
+      if constexpr (NH == 4) mloc = fmaxf(mloc, dpp_f<0x128>(mloc));   // row_ror:8
+      if ((lane & (NH == 4 ? 15 : 7)) == 0) atomicMax(&qmx[hl], __float_as_uint(mloc));
     }
-    plane_sync();
-    // Channel weight Q_c = q~_c s_c scale log2(e) (the weight of the code's sign bit up to
-    // sign), kept in LDS; the largest |Q_c| of a head sets its fixed-point exponent.
-#pragma unroll
-    for (int r = 0; r < NRC; ++r) {
-      const int h = (r * NTC + tid) / kD;
-      float qq = 0.f;
-#pragma unroll
-      for (int j = 0; j < NJQ; ++j) qq += scr[(j * NH + h) * kD + cq];
-      const float qc = (h < G && kb > 0) ? qq * ks * a.scale_log2e : 0.f;
-      qcl[h * kD + cq] = qc;
-      const float m = wave_max_dpp(fabsf(qc));
-      if (lane == 0) atomicMax(&qmx[h], __float_as_uint(m));
-    }
-    plane_sync();
+    plane_sync();                                    // qcl, qmx
     if (tid < NH) {
       int e = 0;
       frexpf(__uint_as_float(qmx[tid]), &e);
@@ -1296,49 +1410,71 @@ void decode_mfma_kernel(const DecodeArgs a) {
       *reinterpret_cast<uint32_t*>(ql + (plane * 2 * NP + st) * 64 + ((D / NP) << 4) +
                                    4 * (rest & 3)) = 0u;
     }
+    // Items without branches or divisions, all channel-weight reads issued together:
+    // the fixed-point exponent of every head first, then every item's four weights.
+    const int nbh = 8 * RWK;                         // items per head
+    int fe_h[NH];
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      int e = 0;
+      const unsigned qm = qmx[h];
+      frexpf(__uint_as_float(qm), &e);
+      fe_h[h] = qm ? 30 - e : 0;
+    }
+    int hi_[NPI], dd_[NPI];
+    float qv_[NPI][4];
 #pragma unroll
     for (int r = 0; r < NPI; ++r) {
       const int i = r * NTC + tid;
-      const int h = i / (8 * RWK), dd = i % (8 * RWK), D = dd >> 3, d = dd & 7;
-      if (h < G) {
-        int e = 0;
-        const unsigned qm = qmx[h];
-        frexpf(__uint_as_float(qm), &e);
-        const int fe = qm ? 30 - e : 0;
-        uint32_t x[4];
+      int h = 0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t ent = ((j < 2 ? desc[r].x : desc[r].y) >> (16 * (j & 1))) & 0xffffu;
-          const float qv = qcl[h * kD + (ent & 127)];
-          int fx = (int)rintf(ldexpf(qv, (int)((ent >> 8) & 15) - 8 + fe - d));
-          if ((((ent >> 14) & 1) != 0) != (d == 7)) fx = -fx;
-          x[j] = (ent & 0x8000u) ? pack_limbs(fx) : 0u;
-        }
-        // x[j] = (limb 0..3 of bit j)  ->  y[L] = (limb L of bits 0..3)
-        const uint32_t t0 = __builtin_amdgcn_perm(x[1], x[0], 0x05010400u);
-        const uint32_t t1 = __builtin_amdgcn_perm(x[3], x[2], 0x05010400u);
-        const uint32_t t2 = __builtin_amdgcn_perm(x[1], x[0], 0x07030602u);
-        const uint32_t t3 = __builtin_amdgcn_perm(x[3], x[2], 0x07030602u);
-        const uint32_t y[4] = {__builtin_amdgcn_perm(t1, t0, 0x05040100u),
-                               __builtin_amdgcn_perm(t1, t0, 0x07060302u),
-                               __builtin_amdgcn_perm(t3, t2, 0x05040100u),
-                               __builtin_amdgcn_perm(t3, t2, 0x07060302u)};
-        const int st = 2 * (D % NP) + (d >> 2);
-        const int pos = ((D / NP) << 4) + ((d & 3) << 2);
+      for (int hh = 1; hh < NH; ++hh) h += (i >= hh * nbh) ? 1 : 0;
+      hi_[r] = h;
+      dd_[r] = i - h * nbh;
 #pragma unroll
-        for (int l4 = 0; l4 < 4; ++l4)
-          *reinterpret_cast<uint32_t*>(ql + ((l4 * NH + h) * 2 * NP + st) * 64 + pos) = y[l4];
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t ent = ((j < 2 ? desc[r].x : desc[r].y) >> (16 * (j & 1))) & 0xffffu;
+        qv_[r][j] = qcl[h * kD + (ent & 127)];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < NPI; ++r) {
+      const int i = r * NTC + tid, h = hi_[r], D = dd_[r] >> 3, d = dd_[r] & 7;
+      int fe = fe_h[0];
+#pragma unroll
+      for (int hh = 1; hh < NH; ++hh) fe = (h == hh) ? fe_h[hh] : fe;
+      uint32_t x[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t ent = ((j < 2 ? desc[r].x : desc[r].y) >> (16 * (j & 1))) & 0xffffu;
+        int fx = (int)rintf(ldexpf(qv_[r][j], (int)((ent >> 8) & 15) - 8 + fe - d));
+        if ((((ent >> 14) & 1) != 0) != (d == 7)) fx = -fx;
+        x[j] = (ent & 0x8000u) ? pack_limbs(fx) : 0u;
+      }
+      // x[j] = (limb 0..3 of bit j)  ->  y[L] = (limb L of bits 0..3)
+      const uint32_t t0 = __builtin_amdgcn_perm(x[1], x[0], 0x05010400u);
+      const uint32_t t1 = __builtin_amdgcn_perm(x[3], x[2], 0x05010400u);
+      const uint32_t t2 = __builtin_amdgcn_perm(x[1], x[0], 0x07030602u);
+      const uint32_t t3 = __builtin_amdgcn_perm(x[3], x[2], 0x07030602u);
+      const uint32_t y[4] = {__builtin_amdgcn_perm(t1, t0, 0x05040100u),
+                             __builtin_amdgcn_perm(t1, t0, 0x07060302u),
+                             __builtin_amdgcn_perm(t3, t2, 0x05040100u),
+                             __builtin_amdgcn_perm(t3, t2, 0x07060302u)};
+      const int st = 2 * (D % NP) + (d >> 2);
+      const int pos = ((D / NP) << 4) + ((d & 3) << 2);
+      // Items past the last head's go to the consumed queries instead.
+      const bool ok = i < G * nbh;
+#pragma unroll
+      for (int l4 = 0; l4 < 4; ++l4) {
+        uint8_t* dst = ok ? ql + ((l4 * NH + h) * 2 * NP + st) * 64 + pos
+                          : reinterpret_cast<uint8_t*>(qs) + 16 * (tid & 63) + 4 * l4;
+        *reinterpret_cast<uint32_t*>(dst) = y[l4];
       }
     }
     // Fused append: this wave's coefficients (stored after the value phase, when no
     // cache transfer is queued ahead of the stores).
-    if constexpr (APPEND) {
-#pragma unroll
-      for (int f = 0; f < KF; ++f)
-        if (adk[f] < 2 * kD)                         // uniform over the wave
-          rcf[f] = append_coefficient(ax[f][0], ax[f][1], atq[f][0], atq[f][1], a.x_dtype,
-                                      a_inv_s[f]);
-    }
+    if constexpr (APPEND)
+      append_coefficients<KF>(ax, atq, a.x_dtype, a_inv_s, rcf);  // (past 2 kD: unused)
   };
 
   // (3) Front.  Eight waves: the plane-building and the issuing waves take separate arms
