@@ -70,10 +70,6 @@ struct DecodeArgs {
   int rk, rv;                     // record bytes
   float scale_log2e;
   int off_v, off_ak, off_av, off_ql, off_pb, off_ob, ob_stride, off_es;   // dynamic LDS layout
-  // T_V staged in LDS for the merge (eight waves): 8 KiB slice w (the rows wave w applies)
-  // at 8 KiB w over the key records for w < tv_nk, else at off_tv + 8 KiB (w - tv_nk);
-  // tv_nk < 0: the merge reads T_V from global memory.
-  int tv_nk, off_tv;
 };
 
 __device__ inline float load_q(const void* q, int dtype, int64_t idx) {
@@ -303,25 +299,6 @@ __device__ inline void plain_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// 16 bytes per lane from a raw buffer straight into LDS at lds_base + 16 lane (lanes whose
-// offset is past the descriptor write zeros), issued where the compiler does not see it:
-// its wait counting would otherwise make the next LDS read of the wave wait for the
-// transfer.  The caller waits (s_waitcnt vmcnt) before the destination is read.  M0 holds
-// the LDS base for the transfer and is restored; one wait state separates the M0 write
-// from the transfer that reads it.
-__device__ inline void lds_copy16_untracked(v4i desc, uint32_t lds_base, uint32_t voffset) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(lds_base), "v"(voffset), "s"(desc)
-      : "memory");
-}
-
 // s_waitcnt vmcnt(n) for a wave-uniform n known only at run time (0 <= n < 64).
 __device__ inline void wait_vmcnt(int n) {
 #define AATC_VMW(k)                                                                         \
@@ -446,18 +423,6 @@ struct TvMfma {
 #pragma unroll
         for (int t = 0; t < 2; ++t)
           a[p][kk][t] = tp[(((wave + (NTHR / 64) * p) * 4 + kk) * 2 + t) * 64 + lane];
-  }
-  // The same from this wave's 8 KiB block staged in LDS at byte offset slice (eight waves:
-  // one block per wave).  LDS-typed loads: a generic pointer would make these flat loads,
-  // which the compiler cannot count in order with the partials' loads.
-  __device__ void load_lds(uint32_t slice) {
-    const int lane = threadIdx.x & 63;
-    const __attribute__((address_space(3))) bf16x8* sp =
-        (const __attribute__((address_space(3))) bf16x8*)(uintptr_t)slice;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-      for (int t = 0; t < 2; ++t) a[0][kk][t] = sp[(kk * 2 + t) * 64 + lane];
   }
   // B operands in LDS: ob[t] (t = 0: oh, 1: ol) holds [k-step][lane] 16-byte units, lane
   // 16 g + n: vector n at elements 32 kk + 8 g .. + 7 (put() writes one element).
@@ -623,7 +588,7 @@ template <int NTHR, int NH, class Hook>
 __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh, int64_t row,
                                                    int G, int n_splits, const Partial* partials,
                                                    unsigned* counters, float* out_rows,
-                                                   float* lds, int tv_slice, Hook& hook) {
+                                                   float* lds, Hook& hook) {
   constexpr int NP = (NH * kD + NTHR - 1) / NTHR;
   constexpr int kMergeB = NP == 1 ? 32 : 64 / NP;
   static_assert(NTHR % kD == 0 && NP * kMergeB <= 64 && kMergeB >= 8, "thread mapping");
@@ -700,14 +665,8 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
   issue(0);
   // T_V after the first partials (a compute unit serves its loads in order; T_V is needed
   // last), then the hook's work while they are in flight.
-  // T_V: staged in LDS by this wave (its transfers have landed), read after the hook's LDS
-  // work while the partials land; else loaded from global memory just before it is applied
-  // (when no other load is in flight, so that the two paths' loads do not meet in the
-  // compiler's wait counting).
   TvMfma<NTHR> tv;
-  const bool tv_staged = NTHR == 512 && __builtin_amdgcn_readfirstlane(tv_slice) >= 0;
   hook.during_loads();
-  if (tv_staged) tv.load_lds((uint32_t)__builtin_amdgcn_readfirstlane(tv_slice));
   consume(0);
   for (int s0 = kMergeB; s0 < n_splits; s0 += kMergeB) {
     issue(s0);
@@ -721,7 +680,9 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
       TvMfma<NTHR>::put(ob_hi, ob_lo, h, c, bad[p] ? NAN : (Ls[p] > 0.f ? acc[p] / Ls[p] : 0.f));
     }
   }
-  if (!tv_staged) tv.load(head_params(params_v, kvh));
+  // T_V (its L2 lines touched by every split) after the partials: a compute unit serves its
+  // loads in order, and T_V is needed last.
+  tv.load(head_params(params_v, kvh));
   __syncthreads();
   // o = T_V o~ (the partials are in the transformed domain).
   tv.apply(ob_hi, ob_lo, G, [&](int h, int j0, v4f o) {
@@ -1701,32 +1662,15 @@ void decode_mfma_kernel(const DecodeArgs a) {
   __syncthreads();
 
   // (6) Value bits x P limbs over all chunks of the split; value-bit tiles are dealt to
-  //     the waves round robin.  O'(v) goes to LDS (over the consumed key records with four
-  //     waves; its own region with eight, where T_V may be staged there).
+  //     the waves round robin.  O'(v) goes to LDS (over the consumed key records).
   const int BV = min(v_budget, 8 * RV);
   const int NVT = (BV + 15) >> 4;
   const uint32_t m0 = 0x01010101u << (2 * g), m1 = m0 << 1;
   float* ob = reinterpret_cast<float*>(smem + a.off_ob);   // [NH][ob_stride]
-  // T_V for the merge.  Each workgroup touches a slice so that the merging one finds T_V
-  // in L2 (the splits of a (sequence, KV head) run on one XCD; block order above).  Eight
-  // waves with room in LDS: every workgroup also stages it (the merging one is not known
-  // yet), each wave its own 8 KiB slice, while this phase runs.
-  int tv_slice = -1;                                  // LDS byte offset of this wave's slice
+  // The splits of a (sequence, KV head) run on one XCD (block order above); each touches a
+  // slice of T_V here so that the merging workgroup finds it in that XCD's L2.
   const uint32_t tv_touch = reinterpret_cast<gdword>(reinterpret_cast<uintptr_t>(hv->Tm))[
       (split * NTHR + tid) * 16 % (kD * kD)];
-  if (DMA && a.tv_nk >= 0) {
-    const int wv = __builtin_amdgcn_readfirstlane(wave);
-    uint8_t* dst = smem + (wv < a.tv_nk ? 8192 * wv : a.off_tv + 8192 * (wv - a.tv_nk));
-    const uint64_t tb = reinterpret_cast<uint64_t>(hv->Tm);
-    const v4i tdesc = {(int)(uint32_t)tb, (int)((uint32_t)(tb >> 32) & 0xffffu),
-                       (int)(kD * kD * sizeof(float)), kRsrcWord3};
-    const uint32_t lb = (uint32_t)reinterpret_cast<uintptr_t>(
-        (__attribute__((address_space(3))) uint8_t*)dst);
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      lds_copy16_untracked(tdesc, lb + 1024 * j, 8192 * wv + 1024 * j + 16 * lane);
-    tv_slice = (int)lb;
-  }
   // B operands stay in registers when they fit (16 x 4 VGPRs).
   constexpr bool kPbRegs = NCH * NT <= 16;
   v4i pbr[kPbRegs ? NCH * NT : 1];
@@ -1837,8 +1781,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
     buf_store16_coherent((v4f){layout_ok ? m : NAN, l, 0.f, 0.f}, prs,
                          (uint32_t)((split * G + tid) * sizeof(Partial)));
   }
-  // The merge's 8 KiB scratch: over the consumed value operands with eight waves (the key
-  // record region may hold T_V), over the key records with four.
+  // The merge's 8 KiB scratch: over the consumed value operands with eight waves, over the
+  // key records with four.
   float* merge_scratch = reinterpret_cast<float*>(smem + (DMA ? a.off_pb : 0));
   if constexpr (APPEND) {
     AppendHook<NTHR, NH> hook;
@@ -1864,11 +1808,11 @@ void decode_mfma_kernel(const DecodeArgs a) {
     }
     hook.sc = reinterpret_cast<AppendScratch*>(smem + a.off_es);
     merge_if_last_wide<NTHR, NH>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
-                                 out_rows, merge_scratch, tv_slice, hook);
+                                 out_rows, merge_scratch, hook);
   } else {
     NoHook none;
     merge_if_last_wide<NTHR, NH>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
-                                 out_rows, merge_scratch, tv_slice, none);
+                                 out_rows, merge_scratch, none);
   }
 }
 
@@ -1912,32 +1856,14 @@ static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
   const size_t ob_bytes = (size_t)NH * a.ob_stride * 4;
   const size_t es_bytes = APPEND ? (sizeof(AppendScratch) + 15) / 16 * 16 : 0;
   constexpr size_t kLdsMax = 160 * 1024 - 4 * 1024;
-  // Eight waves: O' in its own region and T_V staged for the merge, 8 KiB slices over the
-  // key records (free after the key phase) and the rest after everything else, when that
-  // fits; otherwise O' over the key records and T_V from global memory.
-  a.tv_nk = -1;
-  a.off_tv = 0;
-  if (DMA) {
-    const int nk = (int)std::min<size_t>(8, (size_t)S * a.rk / 8192);
-    const size_t off_tv = round256(off + ob_bytes + es_bytes);
-    if (off_tv + (size_t)(8 - nk) * 8192 <= kLdsMax) {
-      a.tv_nk = nk;
-      a.off_ob = (int)off;
-      a.off_es = (int)(off + ob_bytes);
-      a.off_tv = (int)off_tv;
-      off = off_tv + (size_t)(8 - nk) * 8192;
-    }
+  if (ob_bytes <= (size_t)S * a.rk) {
+    a.off_ob = 0;
+  } else {
+    a.off_ob = (int)off;
+    off += ob_bytes;
   }
-  if (a.tv_nk < 0) {
-    if (ob_bytes <= (size_t)S * a.rk) {
-      a.off_ob = 0;
-    } else {
-      a.off_ob = (int)off;
-      off += ob_bytes;
-    }
-    a.off_es = (int)off;
-    off += es_bytes;
-  }
+  a.off_es = (int)off;
+  off += es_bytes;
   const size_t lds = off;
   if (lds > kLdsMax) return AATC_E_UNSUPPORTED;
   static size_t set_lds = 0;
