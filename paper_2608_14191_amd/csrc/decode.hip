@@ -219,6 +219,21 @@ __device__ inline void wave_max_n(float (&v)[N]) {
   for (int i = 0; i < N; ++i) v[i] = xor32_max(v[i]);
 }
 template <int N>
+__device__ inline void wave_sum_n(float (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += dpp_f<0xB1>(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += dpp_f<0x4E>(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += dpp_f<0x124>(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] += dpp_f<0x128>(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = xor16_sum(v[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = xor32_sum(v[i]);
+}
+template <int N>
 __device__ inline void wave_sum_i32_n(int (&v)[N]) {
 #pragma unroll
   for (int i = 0; i < N; ++i) v[i] += dpp_i<0xB1>(v[i]);
@@ -820,15 +835,18 @@ struct AppendHook {
       }
       const float af = __half2float(a16);
       if (et == 0) {
+        float z[NH];
 #pragma unroll
         for (int h = 0; h < NH; ++h) {
-          float t = 0.f;
+          z[h] = 0.f;
 #pragma unroll
           for (int i = 0; i < 2; ++i)
-            t += e_b[i] ? qk[i][h] * ldexpf((float)code[i], 1 - e_b[i]) : 0.f;
-          const float z = wave_sum_dpp(t);
-          if (lane == 0) sc->znew[h] = af * z;
+            z[h] += e_b[i] ? qk[i][h] * ldexpf((float)code[i], 1 - e_b[i]) : 0.f;
         }
+        wave_sum_n(z);
+#pragma unroll
+        for (int h = 0; h < NH; ++h)
+          if (lane == 0) sc->znew[h] = af * z[h];
       } else {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
@@ -1529,19 +1547,29 @@ void decode_mfma_kernel(const DecodeArgs a) {
   float zr[NTILE][NT];
   float avt[NTILE];
   float amax = 0.f;
+  // Every tile's record dwords and token scales first (one LDS round trip), then the
+  // products; lane group g holds record dwords g NP .. g NP + NP - 1, and dwords past the
+  // record (they belong to the next token) meet zero query weights.
+  uint32_t wda[NTILE][NP];
+  uint16_t aka[NTILE], ava[NTILE];
+#pragma unroll
+  for (int tt = 0; tt < NTILE; ++tt) {
+    const uint8_t* rec = kbuf + (wb + 16 * tt + n) * RK;
+#pragma unroll
+    for (int P = 0; P < NP; ++P) wda[tt][P] = *reinterpret_cast<const uint32_t*>(rec + 4 * (g * NP + P));
+    aka[tt] = akb[wb + 16 * tt + 4 * g + L];
+    ava[tt] = avb[wb + 16 * tt + 4 * g + L];
+  }
+  __builtin_amdgcn_sched_barrier(0);
   // Tiles go in pairs: two independent MFMA chains interleave.
 #pragma unroll
   for (int tp = 0; tp < NTILE; tp += 2) {
     v4i acc[2][NT];
     uint32_t wd[2][NP];
-    // Lane group g holds record dwords g NP .. g NP + NP - 1; dwords past the record
-    // (they belong to the next token) meet zero query weights.
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const uint8_t* rec = kbuf + (wb + 16 * (tp + u) + n) * RK;
 #pragma unroll
-      for (int P = 0; P < NP; ++P)
-        wd[u][P] = *reinterpret_cast<const uint32_t*>(rec + 4 * (g * NP + P));
+      for (int P = 0; P < NP; ++P) wd[u][P] = wda[tp + u][P];
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) acc[u][rt] = (v4i){0, 0, 0, 0};
     }
@@ -1570,8 +1598,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
       const int tt = tp + u;
       const int tok = wb + 16 * tt + 4 * g + L;
       const bool tok_ok = tok < nt;
-      const float ak = half_bits_to_float(akb[tok]);
-      const float av = half_bits_to_float(avb[tok]);
+      const float ak = half_bits_to_float(aka[tt]);
+      const float av = half_bits_to_float(ava[tt]);
       avt[tt] = tok_ok ? av : 0.f;
       amax = fmaxf(amax, fabsf(avt[tt]));
 #pragma unroll
@@ -1711,6 +1739,9 @@ void decode_mfma_kernel(const DecodeArgs a) {
     for (int ch = 0; ch < NCH; ++ch)
       wws[ch] = *(const __attribute__((address_space(3))) v2u*)(uintptr_t)(
           vaddr[ch] + 128 * NW * it);
+    // (The scheduler would otherwise pair each read with its products: one LDS round
+    // trip per chunk.)
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
       const v2u ww = wws[ch];
