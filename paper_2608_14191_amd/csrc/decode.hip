@@ -96,6 +96,9 @@ __device__ inline v4i buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
 __device__ inline v2f buf_load8_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return (v2f)__builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, kCoherent);
 }
+__device__ inline v4f buf_load16_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return (v4f)__builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kCoherent);
+}
 __device__ inline void buf_store16_coherent(v4f v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
   __builtin_amdgcn_raw_buffer_store_b128((v4i)v, r, (int)off, 0, kCoherent);
 }
@@ -164,6 +167,19 @@ __device__ inline float wave_sum_dpp(float v) {
   v += dpp_f<0x124>(v);
   v += dpp_f<0x128>(v);
   return xor32_sum(xor16_sum(v));
+}
+// Maximum and sum over each row of 16 lanes (every lane of the row ends with it).
+__device__ inline float row16_max(float v) {
+  v = fmaxf(v, dpp_f<0xB1>(v));
+  v = fmaxf(v, dpp_f<0x4E>(v));
+  v = fmaxf(v, dpp_f<0x124>(v));
+  return fmaxf(v, dpp_f<0x128>(v));
+}
+__device__ inline float row16_sum(float v) {
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x124>(v);
+  return v + dpp_f<0x128>(v);
 }
 template <int CTRL>
 __device__ inline int dpp_i(int v) {
@@ -471,6 +487,8 @@ struct TvMfma {
 struct NoHook {
   __device__ void prefetch() {}
   __device__ void during_loads() {}
+  __device__ void encode() {}
+  __device__ void publish() {}
   __device__ void fold(int, int, float&, float&, v4f&) const {}
   __device__ void fold1(int, int, float&, float&, float&) const {}
   __device__ void finish() {}
@@ -478,8 +496,8 @@ struct NoHook {
 
 // Called by every workgroup after it stored its partial with device-coherent stores.
 // The last of a (sequence, KV head) to arrive merges the split partials.  The hook's
-// loads go out ahead of the partials', its during_loads() runs while they are in flight,
-// fold() adds one more (score, value) term per output slot, finish() runs at the end.
+// loads go out ahead of the partials', its during_loads() (encode(), then the barrier of
+// publish()) runs while they are in flight, fold() adds one more (score, value) term per output slot, finish() runs at the end.
 template <int NTHR, bool TV, bool ONE_PASS = false, class Hook = NoHook>
 __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int64_t row, int G,
                                               int n_splits, const Partial* partials,
@@ -594,21 +612,50 @@ __device__ __forceinline__ void merge_if_last(const void* params_v, int kvh, int
   if (tid == 0) counters[row * kCtrStride] = 0u;
 }
 
-// The merge of the MFMA kernel: one output element (head h, channel c) per thread and
-// pass, every split's (m, l) read once per wave (lane s holds split s of a batch) and its
-// weight 2^(m_s - M) broadcast from that lane; no LDS combine.
-// NH: head slots of the kernel (G <= NH); each thread holds NP elements and loads a batch
-// of kMergeB splits for each (at most 64 loads).
-template <int NTHR, int NH, class Hook>
+// The merge of the MFMA kernel.  The partials go in batches of SB splits.  For each head
+// one of waves 2.. (the table waves) keeps the running maximum M and sum L, and per batch
+// writes the rescale 2^(M_old - M) and the splits' weights 2^(m_s - M) to LDS; every
+// thread loads the partial vectors of one (head, channel quad) unit for its group's SU
+// splits of the batch (16-byte loads) and adds them up with those weights after the
+// batch's barrier.  Waves 0 and 1 run the hook's encode while their loads are in flight
+// (the first barrier also publishes it).  The NG group sums of a unit meet in LDS; then
+// each output element (head h, channel c) takes its one more hook term and goes into the
+// B operands of o = T_V o~.
+// LDS: T_V B operands (8 KiB) | weights [2][NH][SB] | rescales [2][NH] | (M, L, bad) [NH]
+// | group sums [NG][NU] (16 B each).  TV_HELD: the caller has loaded tv (every split does,
+// during its value phase, so the merging one starts with T_V in registers); otherwise the
+// merge loads it after the partials.
+template <int NTHR, int NH>
+struct WideMerge {
+  static constexpr int NW = NTHR / 64;
+  static constexpr int NU = NH * (kD / 4);            // (head, channel quad) units
+  static constexpr int NG = NTHR / NU;                // split groups
+  static constexpr int SU = 8;                        // splits per thread and batch
+  static constexpr int SB = SU * NG;                  // splits per batch
+  static constexpr int NTW = NW - 2;                  // table waves
+  static constexpr int NHW = (NH + NTW - 1) / NTW;    // heads per table wave
+  static constexpr int NP = (NH * kD + NTHR - 1) / NTHR;   // output elements per thread
+  static_assert(NG >= 1 && NG * NU == NTHR && SB <= 64 && NTW >= 1, "thread mapping");
+  static constexpr int kWt = 2 * 4 * 64 * 8 / 2;     // float offsets of the regions
+  static constexpr int kSa = kWt + 2 * NH * SB;
+  static constexpr int kFin = kSa + 2 * NH;
+  static constexpr int kRed = (kFin + 4 * NH + 3) / 4 * 4;
+  static constexpr int kFloats = kRed + 4 * NTHR;
+};
+
+template <int NTHR, int NH>
+constexpr size_t wide_merge_lds_bytes() { return WideMerge<NTHR, NH>::kFloats * sizeof(float); }
+
+template <int NTHR, int NH, bool TV_HELD, class Hook>
 __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh, int64_t row,
                                                    int G, int n_splits, const Partial* partials,
                                                    unsigned* counters, float* out_rows,
-                                                   float* lds, Hook& hook) {
-  constexpr int NP = (NH * kD + NTHR - 1) / NTHR;
-  constexpr int kMergeB = NP == 1 ? 32 : 64 / NP;
-  static_assert(NTHR % kD == 0 && NP * kMergeB <= 64 && kMergeB >= 8, "thread mapping");
+                                                   float* lds, TvMfma<NTHR>& tv, Hook& hook) {
+  using WM = WideMerge<NTHR, NH>;
+  constexpr int SU = WM::SU, SB = WM::SB, NU = WM::NU, NTW = WM::NTW, NHW = WM::NHW;
   __shared__ unsigned last_s;
   const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   __builtin_amdgcn_s_waitcnt(0);          // this thread's partial stores have completed
   __syncthreads();
   unsigned prev = 0u;
@@ -620,88 +667,131 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
   if (!last_s) return;
   hook.prefetch();
   __builtin_amdgcn_sched_barrier(0);
-  // The merged vectors as B operands of the T_V product (bf16 pairs, 2 x 4 KiB).
   __bf16* ob_hi = reinterpret_cast<__bf16*>(lds);
   __bf16* ob_lo = ob_hi + 4 * 64 * 8;
+  float* wt = lds + WM::kWt;
+  float* sat = lds + WM::kSa;
+  v4f* fin = reinterpret_cast<v4f*>(lds + WM::kFin);
+  v4f* red = reinterpret_cast<v4f*>(lds + WM::kRed);
   const __amdgpu_buffer_rsrc_t prs =
       make_rsrc(partials + row * n_splits * G, (uint32_t)(n_splits * G * sizeof(Partial)));
-  float M[NP], Ls[NP], acc[NP];
-  bool bad[NP];
-  v2f hd[NP];
-  float ov[NP][kMergeB];
-  // Loads of a batch: past the last split (or head) they read 0 and count as empty.
+  // 32-bit offsets: the descriptor covers less than 2^31 bytes.
+  const uint32_t step = (uint32_t)G * (uint32_t)sizeof(Partial);
+  const int u = tid % NU, q = tid / NU, h = u / (kD / 4), c4 = u % (kD / 4);
+  const bool unit_on = h < G;
+  const bool table = wave >= 2;
+  float tM[NHW], tL[NHW];
+  bool tbad[NHW];
+#pragma unroll
+  for (int i = 0; i < NHW; ++i) {
+    tM[i] = -INFINITY;
+    tL[i] = 0.f;
+    tbad[i] = false;
+  }
+  v2f thd[NHW];
+  v4f ov[SU];
+  v4f acc = {0.f, 0.f, 0.f, 0.f};
+  // A batch's loads (past the last split or head they read 0): the table waves' (m, l)
+  // first, then every thread's vectors.
   auto issue = [&](int s0) {
+    if (table) {
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      const int slot = p * NTHR + tid, h = min(slot / kD, G - 1), c = slot % kD;
-      // 32-bit offsets (the descriptor holds less than 2^31 bytes): split u's part is a
-      // uniform product, the rest 24-bit (no 64-bit multiply-adds on pending registers).
-      const uint32_t step = (uint32_t)G * (uint32_t)sizeof(Partial);
-      const uint32_t hoff = __umul24((uint32_t)(s0 + (lane & (kMergeB - 1))), step) +
-                            __umul24((uint32_t)h, (uint32_t)sizeof(Partial));
-      hd[p] = buf_load8_coherent(prs, (slot / kD < G) ? hoff : 0x80000000u);
-#pragma unroll
-      for (int u = 0; u < kMergeB; ++u) {
-        const uint32_t off = (uint32_t)(s0 + u) * step +
-                             __umul24((uint32_t)h, (uint32_t)sizeof(Partial)) + 16 + 4 * c;
-        ov[p][u] = __int_as_float(
-            __builtin_amdgcn_raw_buffer_load_b32(prs, (slot / kD < G) ? (int)off : (int)0x80000000,
-                                                 0, kCoherent));
+      for (int i = 0; i < NHW; ++i) {
+        const int h2 = wave - 2 + NTW * i;
+        const bool on = (h2 < G) & (lane < SB) & (s0 + lane < n_splits);
+        thd[i] = buf_load8_coherent(
+            prs, on ? (uint32_t)(s0 + lane) * step + (uint32_t)h2 * (uint32_t)sizeof(Partial)
+                    : 0x80000000u);
       }
     }
-  };
-  auto consume = [&](int s0) {
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      const bool in = (lane < kMergeB) & (s0 + lane < n_splits);
-      const float ms = in ? hd[p].x : -INFINITY;
-      bad[p] |= __builtin_amdgcn_ballot_w64(ms != ms) != 0;
-      const float mb = wave_max_dpp(ms);                   // (NaN lanes are ignored)
-      const float mn = fmaxf(M[p], mb);
-      const float sa = (mn == -INFINITY) ? 1.f : exp2f(M[p] - mn);
-      const float w = (ms == -INFINITY || ms != ms) ? 0.f : exp2f(ms - mn);
-      Ls[p] = Ls[p] * sa + wave_sum_dpp(w * hd[p].y);
-      float a2 = acc[p] * sa;
-      const int wb = __float_as_int(w);
-#pragma unroll
-      for (int u = 0; u < kMergeB; ++u)
-        a2 = fmaf(__int_as_float(__builtin_amdgcn_readlane(wb, u)), ov[p][u], a2);
-      acc[p] = a2;
-      M[p] = mn;
+    for (int k = 0; k < SU; ++k) {
+      const int sp = s0 + q * SU + k;
+      const bool on = unit_on & (sp < n_splits);
+      ov[k] = buf_load16_coherent(
+          prs, on ? (uint32_t)sp * step + (uint32_t)h * (uint32_t)sizeof(Partial) + 16u +
+                        16u * (uint32_t)c4
+                  : 0x80000000u);
     }
   };
+  // The table waves' part of a batch (NaN maxima mark records that did not match).
+  auto tables = [&](int s0, int b) {
+    if (!table) return;
 #pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    M[p] = -INFINITY;
-    Ls[p] = 0.f;
-    acc[p] = 0.f;
-    bad[p] = false;
-  }
+    for (int i = 0; i < NHW; ++i) {
+      const int h2 = wave - 2 + NTW * i;
+      if (h2 >= G) continue;                         // (uniform over the wave)
+      const bool in = (lane < SB) & (s0 + lane < n_splits);
+      const float ms = in ? thd[i].x : -INFINITY;
+      tbad[i] |= __builtin_amdgcn_ballot_w64(ms != ms) != 0;
+      const float mn = fmaxf(tM[i], wave_max_dpp(ms));    // (NaN lanes are ignored)
+      // (the hardware exp2: weights below 2^-126 of the largest flush to 0)
+      const float sa = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(tM[i] - mn);
+      const float w = (ms == -INFINITY || ms != ms) ? 0.f : __builtin_amdgcn_exp2f(ms - mn);
+      tL[i] = tL[i] * sa + wave_sum_dpp(w * thd[i].y);
+      tM[i] = mn;
+      if (lane < SB) wt[((b & 1) * NH + h2) * SB + lane] = w;
+      if (lane == 0) sat[(b & 1) * NH + h2] = sa;
+    }
+  };
+  auto accumulate = [&](int b) {
+    if (!unit_on) return;
+    const v4f* wv = reinterpret_cast<const v4f*>(wt + ((b & 1) * NH + h) * SB + q * SU);
+    const float sa = sat[(b & 1) * NH + h];
+    float w[SU];
+#pragma unroll
+    for (int k = 0; k < SU / 4; ++k) {
+      const v4f x = wv[k];
+      w[4 * k] = x[0], w[4 * k + 1] = x[1], w[4 * k + 2] = x[2], w[4 * k + 3] = x[3];
+    }
+    v4f a0 = acc * sa, a1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < SU; k += 2) {
+      a0 += w[k] * ov[k];
+      a1 += w[k + 1] * ov[k + 1];
+    }
+    acc = a0 + a1;
+  };
   issue(0);
-  // T_V after the first partials (a compute unit serves its loads in order; T_V is needed
-  // last), then the hook's work while they are in flight.
-  TvMfma<NTHR> tv;
-  hook.during_loads();
-  consume(0);
-  for (int s0 = kMergeB; s0 < n_splits; s0 += kMergeB) {
+  hook.encode();                          // waves 0 and 1, while the loads are in flight
+  for (int s0 = 0, b = 0;; ++b) {
+    tables(s0, b);
+    __syncthreads();                      // the batch's weights (first: the hook's encode)
+    accumulate(b);
+    s0 += SB;
+    if (s0 >= n_splits) break;
     issue(s0);
-    consume(s0);
   }
+  if (table && lane == 0) {
 #pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    const int slot = p * NTHR + tid, h = slot / kD, c = slot % kD;
-    if (h < G) {
-      hook.fold1(h, c, M[p], Ls[p], acc[p]);
-      TvMfma<NTHR>::put(ob_hi, ob_lo, h, c, bad[p] ? NAN : (Ls[p] > 0.f ? acc[p] / Ls[p] : 0.f));
+    for (int i = 0; i < NHW; ++i) {
+      const int h2 = wave - 2 + NTW * i;
+      if (h2 < G) fin[h2] = (v4f){tM[i], tL[i], tbad[i] ? 1.f : 0.f, 0.f};
+    }
+  }
+  red[q * NU + u] = acc;
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < WM::NP; ++p) {
+    const int slot = p * NTHR + tid, hh = slot / kD, c = slot % kD;
+    if (hh < G) {
+      float a = 0.f;
+#pragma unroll
+      for (int g = 0; g < WM::NG; ++g)
+        a += reinterpret_cast<const float*>(red + g * NU + hh * (kD / 4))[c];
+      const v4f f = fin[hh];
+      float M = f[0], Ls = f[1];
+      hook.fold1(hh, c, M, Ls, a);
+      TvMfma<NTHR>::put(ob_hi, ob_lo, hh, c, f[2] != 0.f ? NAN : (Ls > 0.f ? a / Ls : 0.f));
     }
   }
   // T_V (its L2 lines touched by every split) after the partials: a compute unit serves its
   // loads in order, and T_V is needed last.
-  tv.load(head_params(params_v, kvh));
+  if constexpr (!TV_HELD) tv.load(head_params(params_v, kvh));
   __syncthreads();
   // o = T_V o~ (the partials are in the transformed domain).
-  tv.apply(ob_hi, ob_lo, G, [&](int h, int j0, v4f o) {
-    *reinterpret_cast<v4f*>(out_rows + (int64_t)h * kD + j0) = o;
+  tv.apply(ob_hi, ob_lo, G, [&](int hh, int j0, v4f o) {
+    *reinterpret_cast<v4f*>(out_rows + (int64_t)hh * kD + j0) = o;
   });
   hook.finish();
   if (tid == 0) counters[row * kCtrStride] = 0u;
@@ -809,8 +899,15 @@ struct AppendHook {
   }
 
   // The token's codes, scales, score per head and transformed value, each tensor by one
-  // wave (wave reductions only); one barrier publishes them.
+  // wave (wave reductions only); the barrier of publish() makes them visible.
   __device__ void during_loads() {
+    encode();
+    publish();
+  }
+  __device__ void publish() {
+    if (on) __syncthreads();           // (uniform over the workgroup)
+  }
+  __device__ void encode() {
     if (!on) return;                   // uniform over the workgroup
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (wave < 2) {
@@ -854,7 +951,6 @@ struct AppendHook {
       }
       if (lane == 0) sc->ea16[et] = __half_as_ushort(a16);
     }
-    __syncthreads();                   // codes, scales, znew and vnew visible from here on
   }
   // The token's log2-domain score for head h.
   __device__ float znew(int h) const { return sc->znew[h]; }
@@ -874,7 +970,7 @@ struct AppendHook {
     if (!on) return;
     const float ms = znew(h);
     const float mn = fmaxf(M, ms);
-    const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
+    const float sa = __builtin_amdgcn_exp2f(M - mn), sb = __builtin_amdgcn_exp2f(ms - mn);
     acc = acc * sa + sc->vnew[c] * sb;
     Ls = Ls * sa + sb;
     M = mn;
@@ -1526,7 +1622,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
 #pragma unroll
     for (int s = 0; s < 2 * NP; ++s)
       bq[rt][s] = *reinterpret_cast<const v4i*>(ql + ((L * NH + h) * 2 * NP + s) * 64 + 16 * g);
-    fex[rt] = fexp_s[h];
+    fex[rt] = fexp_s[4 * rt + g];        // (the head of this lane's scores)
   }
   // Q_c of every head for channels lane and lane + 64, for the fused append's key token
   // (eight waves: the planes' scratch is intact until the softmax writes the value
@@ -1541,9 +1637,11 @@ void decode_mfma_kernel(const DecodeArgs a) {
     }
   }
 
-  // (4) Key scores of this wave's tokens: lane L of a quad ends with token 4 g + L.
+  // (4) Key scores of this wave's tokens.  The query planes are the A operand (row 4 h + L:
+  //     head h, limb L) and the record bits the B operand (column: token), so lane 16 h + n
+  //     ends with the four limb sums of head h for token n of the tile and recombines them
+  //     itself.
   const int wb = wave * TW;
-  const float lw = (float)(1 << (8 * L));            // weight of this lane's limb
   float zr[NTILE][NT];
   float avt[NTILE];
   float amax = 0.f;
@@ -1557,8 +1655,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
     const uint8_t* rec = kbuf + (wb + 16 * tt + n) * RK;
 #pragma unroll
     for (int P = 0; P < NP; ++P) wda[tt][P] = *reinterpret_cast<const uint32_t*>(rec + 4 * (g * NP + P));
-    aka[tt] = akb[wb + 16 * tt + 4 * g + L];
-    ava[tt] = avb[wb + 16 * tt + 4 * g + L];
+    aka[tt] = akb[wb + 16 * tt + n];
+    ava[tt] = avb[wb + 16 * tt + n];
   }
   __builtin_amdgcn_sched_barrier(0);
   // Tiles go in pairs: two independent MFMA chains interleave.
@@ -1587,16 +1685,16 @@ void decode_mfma_kernel(const DecodeArgs a) {
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
-        for (int u = 0; u < 2; ++u) acc[u][rt] = mfma_i8(a0[u], bq[rt][2 * P], acc[u][rt]);
+        for (int u = 0; u < 2; ++u) acc[u][rt] = mfma_i8(bq[rt][2 * P], a0[u], acc[u][rt]);
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
-        for (int u = 0; u < 2; ++u) acc[u][rt] = mfma_i8(a1[u], bq[rt][2 * P + 1], acc[u][rt]);
+        for (int u = 0; u < 2; ++u) acc[u][rt] = mfma_i8(bq[rt][2 * P + 1], a1[u], acc[u][rt]);
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int tt = tp + u;
-      const int tok = wb + 16 * tt + 4 * g + L;
+      const int tok = wb + 16 * tt + n;
       const bool tok_ok = tok < nt;
       const float ak = half_bits_to_float(aka[tt]);
       const float av = half_bits_to_float(ava[tt]);
@@ -1604,10 +1702,11 @@ void decode_mfma_kernel(const DecodeArgs a) {
       amax = fmaxf(amax, fabsf(avt[tt]));
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) {
-        const float x[4] = {(float)acc[u][rt][0] * lw, (float)acc[u][rt][1] * lw,
-                            (float)acc[u][rt][2] * lw, (float)acc[u][rt][3] * lw};
-        const float f = quad_reduce_scatter(x, L);
-        zr[tt][rt] = (tok_ok && 4 * rt + hc < G) ? ldexpf(f * ak, -fex[rt]) : -INFINITY;
+        const v4i d = acc[u][rt];                 // limbs 0..3 (weights 256^i)
+        float f = fmaf((float)d[3], 256.f, (float)d[2]);
+        f = fmaf(f, 256.f, (float)d[1]);
+        f = fmaf(f, 256.f, (float)d[0]);
+        zr[tt][rt] = (tok_ok && 4 * rt + g < G) ? ldexpf(f * ak, -fex[rt]) : -INFINITY;
       }
     }
   }
@@ -1619,9 +1718,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
     float m = -INFINITY;
 #pragma unroll
     for (int tt = 0; tt < NTILE; ++tt) m = fmaxf(m, zr[tt][rt]);
-    m = quad_max(m);
-    m = xor32_max(xor16_max(m));
-    if (g == 0 && L == 0) wmax[wave][4 * rt + hc] = m;
+    m = row16_max(m);
+    if (n == 0) wmax[wave][4 * rt + g] = m;
   }
   amax = wave_max_dpp(amax);
   if (lane == 0) wav[wave] = amax;
@@ -1629,9 +1727,9 @@ void decode_mfma_kernel(const DecodeArgs a) {
   float mh[NT];
 #pragma unroll
   for (int rt = 0; rt < NT; ++rt) {
-    mh[rt] = wmax[0][4 * rt + hc];
+    mh[rt] = wmax[0][4 * rt + g];
 #pragma unroll
-    for (int w = 1; w < NW; ++w) mh[rt] = fmaxf(mh[rt], wmax[w][4 * rt + hc]);
+    for (int w = 1; w < NW; ++w) mh[rt] = fmaxf(mh[rt], wmax[w][4 * rt + g]);
   }
   int fv = 0;
   {
@@ -1642,9 +1740,10 @@ void decode_mfma_kernel(const DecodeArgs a) {
     frexpf(am, &e);
     fv = am > 0.f ? 30 - e : 0;           // P <= max alpha^V < 2^e, so P 2^fv < 2^30
   }
-  // Token 16 q + 4 g + L of a chunk sits at bit d = 2 g + q % 2 of its value byte.
-  const float sc_even = ldexpf(1.f, fv - 2 * g);
-  const float sc_odd = (g == 3 ? -1.f : 1.f) * ldexpf(1.f, fv - 2 * g - 1);
+  // Token 16 q + 4 e + L of a chunk sits at bit d = 2 e + q % 2 of its value byte; this
+  // lane's tokens have e = hc.
+  const float sc_even = ldexpf(1.f, fv - 2 * hc);
+  const float sc_odd = (hc == 3 ? -1.f : 1.f) * ldexpf(1.f, fv - 2 * hc - 1);
   const uint32_t sel_a = (L & 2) ? 0x03020706u : 0x05040100u;
   const uint32_t sel_b = (L & 1) ? 0x03070105u : 0x06020400u;
   v4i* pb = reinterpret_cast<v4i*>(smem + a.off_pb);  // [NCH][NT][64] value operands
@@ -1667,12 +1766,13 @@ void decode_mfma_kernel(const DecodeArgs a) {
         x = __builtin_amdgcn_perm(quad_xor2(x), x, sel_a);
         y[qd] = __builtin_amdgcn_perm(quad_xor1(x), x, sel_b);
       }
-      pb[((wave * CPW + ch) * NT + rt) * 64 + lane] =
+      // Limb L of head g for tokens 16 q + 4 hc + (0..3): lane 16 hc + 4 g + L of the
+      // value phase's B operand.
+      pb[((wave * CPW + ch) * NT + rt) * 64 + 16 * hc + 4 * g + L] =
           (v4i){(int)y[0], (int)y[1], (int)y[2], (int)y[3]};
     }
-    lsum = quad_sum(lsum);
-    lsum = xor32_sum(xor16_sum(lsum));
-    if (g == 0 && L == 0) wsum[wave][4 * rt + hc] = lsum;
+    lsum = row16_sum(lsum);
+    if (n == 0) wsum[wave][4 * rt + g] = lsum;
   }
   // The value tiles: the issuing waves wait for the rest of their transfers, or every
   // wave stores its registers (their region held nothing since the query transform).
@@ -1695,10 +1795,18 @@ void decode_mfma_kernel(const DecodeArgs a) {
   const int NVT = (BV + 15) >> 4;
   const uint32_t m0 = 0x01010101u << (2 * g), m1 = m0 << 1;
   float* ob = reinterpret_cast<float*>(smem + a.off_ob);   // [NH][ob_stride]
-  // The splits of a (sequence, KV head) run on one XCD (block order above); each touches a
-  // slice of T_V here so that the merging workgroup finds it in that XCD's L2.
-  const uint32_t tv_touch = reinterpret_cast<gdword>(reinterpret_cast<uintptr_t>(hv->Tm))[
-      (split * NTHR + tid) * 16 % (kD * kD)];
+  // T_V for the merge: with eight waves every split loads its matrix-core operands now (32
+  // VGPRs; they land during the value phase, and the split that merges has them at hand).
+  // Otherwise each split touches a slice of T_V, so that the merging one finds it in its
+  // XCD's L2 (the splits of a (sequence, KV head) run on one XCD: block order above).
+  constexpr bool kTvHeld = TvMfma<NTHR>::NPASS == 1;
+  TvMfma<NTHR> tv;
+  uint32_t tv_touch = 0u;
+  if constexpr (kTvHeld)
+    tv.load(hv);
+  else
+    tv_touch = reinterpret_cast<gdword>(reinterpret_cast<uintptr_t>(hv->Tm))[
+        (split * NTHR + tid) * 16 % (kD * kD)];
   // B operands stay in registers when they fit (16 x 4 VGPRs).
   constexpr bool kPbRegs = NCH * NT <= 16;
   v4i pbr[kPbRegs ? NCH * NT : 1];
@@ -1749,15 +1857,18 @@ void decode_mfma_kernel(const DecodeArgs a) {
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) {
         const v4i bop = kPbRegs ? pbr[kPbRegs ? ch * NT + rt : 0] : pb[(ch * NT + rt) * 64 + lane];
-        acc[ch & 3][rt] = mfma_i8(av4, bop, acc[ch & 3][rt]);
+        acc[ch & 3][rt] = mfma_i8(bop, av4, acc[ch & 3][rt]);
       }
     }
+    // (P limbs are the A operand: lane 16 h + n ends with the four limb sums of head h for
+    // value bit 16 vt + n.)
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) {
-      acc[0][rt] += acc[1][rt] + acc[2][rt] + acc[3][rt];
-      const float x[4] = {(float)acc[0][rt][0] * lw, (float)acc[0][rt][1] * lw,
-                          (float)acc[0][rt][2] * lw, (float)acc[0][rt][3] * lw};
-      ob[(4 * rt + hc) * a.ob_stride + 16 * vt + 4 * g + L] = quad_reduce_scatter(x, L);
+      const v4i d = acc[0][rt] + acc[1][rt] + acc[2][rt] + acc[3][rt];
+      float f = fmaf((float)d[3], 256.f, (float)d[2]);
+      f = fmaf(f, 256.f, (float)d[1]);
+      f = fmaf(f, 256.f, (float)d[0]);
+      ob[(4 * rt + g) * a.ob_stride + 16 * vt + n] = f;
     }
   }
 
@@ -1812,9 +1923,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
     buf_store16_coherent((v4f){layout_ok ? m : NAN, l, 0.f, 0.f}, prs,
                          (uint32_t)((split * G + tid) * sizeof(Partial)));
   }
-  // The merge's 8 KiB scratch: over the consumed value operands with eight waves, over the
-  // key records with four.
-  float* merge_scratch = reinterpret_cast<float*>(smem + (DMA ? a.off_pb : 0));
+  // The merge's scratch: from the start of the front region (its cache and O' are consumed).
+  float* merge_scratch = reinterpret_cast<float*>(smem);
   if constexpr (APPEND) {
     AppendHook<NTHR, NH> hook;
     hook.coeff = a.append_r + row * 2 * kD;
@@ -1838,12 +1948,12 @@ void decode_mfma_kernel(const DecodeArgs a) {
       for (int h = 0; h < NH; ++h) hook.qk[i][h] = qk[i][h];
     }
     hook.sc = reinterpret_cast<AppendScratch*>(smem + a.off_es);
-    merge_if_last_wide<NTHR, NH>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
-                                 out_rows, merge_scratch, hook);
+    merge_if_last_wide<NTHR, NH, kTvHeld>(a.params_v, kvh, row, G, a.n_splits, a.partials,
+                                          a.counters, out_rows, merge_scratch, tv, hook);
   } else {
     NoHook none;
-    merge_if_last_wide<NTHR, NH>(a.params_v, kvh, row, G, a.n_splits, a.partials, a.counters,
-                                 out_rows, merge_scratch, none);
+    merge_if_last_wide<NTHR, NH, kTvHeld>(a.params_v, kvh, row, G, a.n_splits, a.partials,
+                                          a.counters, out_rows, merge_scratch, tv, none);
   }
 }
 
@@ -1876,7 +1986,7 @@ static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
   a.off_av = a.off_ak + 2 * S;
   size_t front = (size_t)a.off_av + 2 * S;
   if (!DMA) front = std::max(front, scr_bytes);
-  front = std::max(front, merge_lds_bytes(a.G, NTHR));
+  front = std::max(front, wide_merge_lds_bytes<NTHR, NH>());
   front = round256(front);
   a.off_ql = (int)front;
   a.off_pb = a.off_ql + 4 * NH * 2 * NP * 64;
