@@ -1811,11 +1811,12 @@ void decode_mfma_kernel(const DecodeArgs a) {
   constexpr bool kPbRegs = NCH * NT <= 16;
   v4i pbr[kPbRegs ? NCH * NT : 1];
   if constexpr (kPbRegs) {
+    // All reads first (one LDS round trip), then the pins that keep them in registers
+    // rather than re-read per tile.
 #pragma unroll
-    for (int i = 0; i < NCH * NT; ++i) {
-      pbr[i] = pb[i * 64 + lane];
-      asm volatile("" : "+v"(pbr[i]));             // kept in registers, not re-read per tile
-    }
+    for (int i = 0; i < NCH * NT; ++i) pbr[i] = pb[i * 64 + lane];
+#pragma unroll
+    for (int i = 0; i < NCH * NT; ++i) asm volatile("" : "+v"(pbr[i]));
   }
   // LDS address of this lane's value-bit dword pair in each chunk for tile vt = wave; tile
   // wave + NW it is 128 NW it bytes further (an immediate offset: no address arithmetic in
@@ -1835,11 +1836,11 @@ void decode_mfma_kernel(const DecodeArgs a) {
   for (int it = 0; it < kMaxIt; ++it) {
     const int vt = wave + NW * it;
     if (vt >= NVT) break;                           // (uniform)
-    v4i acc[4][NT];                                 // chunk % 4: four MFMA chains
+    // One accumulator per column tile: a dependent product takes its predecessor's result
+    // straight from the matrix unit.
+    v4i acc[NT];
 #pragma unroll
-    for (int c4 = 0; c4 < 4; ++c4)
-#pragma unroll
-      for (int rt = 0; rt < NT; ++rt) acc[c4][rt] = (v4i){0, 0, 0, 0};
+    for (int rt = 0; rt < NT; ++rt) acc[rt] = (v4i){0, 0, 0, 0};
     // All of the tile's value-bit words first (one LDS round trip), then the products.
     typedef uint32_t v2u __attribute__((ext_vector_type(2)));
     v2u wws[NCH];
@@ -1857,14 +1858,14 @@ void decode_mfma_kernel(const DecodeArgs a) {
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) {
         const v4i bop = kPbRegs ? pbr[kPbRegs ? ch * NT + rt : 0] : pb[(ch * NT + rt) * 64 + lane];
-        acc[ch & 3][rt] = mfma_i8(bop, av4, acc[ch & 3][rt]);
+        acc[rt] = mfma_i8(bop, av4, acc[rt]);
       }
     }
     // (P limbs are the A operand: lane 16 h + n ends with the four limb sums of head h for
     // value bit 16 vt + n.)
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) {
-      const v4i d = acc[0][rt] + acc[1][rt] + acc[2][rt] + acc[3][rt];
+      const v4i d = acc[rt];
       float f = fmaf((float)d[3], 256.f, (float)d[2]);
       f = fmaf(f, 256.f, (float)d[1]);
       f = fmaf(f, 256.f, (float)d[0]);
