@@ -445,15 +445,18 @@ struct TvMfma {
   static_assert(NPASS * NTHR == 512, "256 or 512 threads");
   bf16x8 a[NPASS][4][2];                  // [pass][k-step][Th, Tl]
   __device__ void load(const HeadParams* hv) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) load_step(hv, kk);
+  }
+  // The operands of k-step kk only (the loads can be spread out).
+  __device__ void load_step(const HeadParams* hv, int kk) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const bf16x8* tp = reinterpret_cast<const bf16x8*>(hv->Tm);
 #pragma unroll
     for (int p = 0; p < NPASS; ++p)
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-          a[p][kk][t] = tp[(((wave + (NTHR / 64) * p) * 4 + kk) * 2 + t) * 64 + lane];
+      for (int t = 0; t < 2; ++t)
+        a[p][kk][t] = tp[(((wave + (NTHR / 64) * p) * 4 + kk) * 2 + t) * 64 + lane];
   }
   // B operands in LDS: ob[t] (t = 0: oh, 1: ol) holds [k-step][lane] 16-byte units, lane
   // 16 g + n: vector n at elements 32 kk + 8 g .. + 7 (put() writes one element).
@@ -1789,53 +1792,65 @@ void decode_mfma_kernel(const DecodeArgs a) {
   }
   __syncthreads();
 
-  // (6) Value bits x P limbs over all chunks of the split; value-bit tiles are dealt to
-  //     the waves round robin.  O'(v) goes to LDS (over the consumed key records).
+  // (6) Value bits x P limbs; value-bit tiles of 16 bits are dealt to the waves round
+  //     robin.  O'(v) goes to LDS (over the consumed key records).  With eight waves the
+  //     chunks go in two halves: waves 0-3 take the first half of every tile, waves 4-7
+  //     the second (each reads only its half's P operands, and O' has one copy per half),
+  //     and the two groups walk the tiles in opposite orders, so that the two waves of a
+  //     SIMD (s and s + 4) have the same number of tiles between them on every SIMD.
   const int BV = min(v_budget, 8 * RV);
   const int NVT = (BV + 15) >> 4;
   const uint32_t m0 = 0x01010101u << (2 * g), m1 = m0 << 1;
-  float* ob = reinterpret_cast<float*>(smem + a.off_ob);   // [NH][ob_stride]
-  // T_V for the merge: with eight waves every split loads its matrix-core operands now (32
-  // VGPRs; they land during the value phase, and the split that merges has them at hand).
-  // Otherwise each split touches a slice of T_V, so that the merging one finds it in its
-  // XCD's L2 (the splits of a (sequence, KV head) run on one XCD: block order above).
+  constexpr bool kHalves = NW == 8 && NCH % 2 == 0;
+  constexpr int NCW = kHalves ? NCH / 2 : NCH;        // chunks of a wave's tile pass
+  constexpr int NWT = kHalves ? NW / 2 : NW;          // waves over the tiles of one half
+  const int hf = kHalves ? (wave >> 2) : 0;           // this wave's chunk half
+  const int wj = kHalves ? (hf ? 3 - (wave & 3) : (wave & 3)) : wave;   // its first tile
+  float* ob = reinterpret_cast<float*>(smem + a.off_ob);   // [halves][NH][ob_stride]
+  // T_V for the merge: with eight waves every split loads its matrix-core operands during
+  // the value loop (32 VGPRs, one k-step per tile, so that the loads never back up the
+  // memory queue), and the split that merges has them at hand.  Otherwise each split
+  // touches a slice of T_V, so that the merging one finds it in its XCD's L2 (the splits of
+  // a (sequence, KV head) run on one XCD: block order above).
   constexpr bool kTvHeld = TvMfma<NTHR>::NPASS == 1;
   TvMfma<NTHR> tv;
   uint32_t tv_touch = 0u;
-  if constexpr (kTvHeld)
-    tv.load(hv);
-  else
+  if constexpr (!kTvHeld)
     tv_touch = reinterpret_cast<gdword>(reinterpret_cast<uintptr_t>(hv->Tm))[
         (split * NTHR + tid) * 16 % (kD * kD)];
-  // B operands stay in registers when they fit (16 x 4 VGPRs).
-  constexpr bool kPbRegs = NCH * NT <= 16;
-  v4i pbr[kPbRegs ? NCH * NT : 1];
+  // A operands (this half's chunks) stay in registers when they fit (16 x 4 VGPRs).
+  constexpr bool kPbRegs = NCW * NT <= 16;
+  const v4i* pbh = pb + hf * NCW * NT * 64;
+  v4i pbr[kPbRegs ? NCW * NT : 1];
   if constexpr (kPbRegs) {
     // All reads first (one LDS round trip), then the pins that keep them in registers
     // rather than re-read per tile.
 #pragma unroll
-    for (int i = 0; i < NCH * NT; ++i) pbr[i] = pb[i * 64 + lane];
+    for (int i = 0; i < NCW * NT; ++i) pbr[i] = pbh[i * 64 + lane];
 #pragma unroll
-    for (int i = 0; i < NCH * NT; ++i) asm volatile("" : "+v"(pbr[i]));
+    for (int i = 0; i < NCW * NT; ++i) asm volatile("" : "+v"(pbr[i]));
   }
-  // LDS address of this lane's value-bit dword pair in each chunk for tile vt = wave; tile
-  // wave + NW it is 128 NW it bytes further (an immediate offset: no address arithmetic in
-  // the loop).
-  uint32_t vaddr[NCH];
+  // LDS address of this lane's value-bit dword pair in each chunk of the half for tile
+  // vt = wj; tile wj + NWT it is 128 NWT it bytes further (an immediate offset: no address
+  // arithmetic in the loop).
+  uint32_t vaddr[NCW];
   {
     const uint32_t vb = (uint32_t)reinterpret_cast<uintptr_t>(
-        (__attribute__((address_space(3))) uint8_t*)vbuf) + 8 * n + 128 * wave;
+        (__attribute__((address_space(3))) uint8_t*)vbuf) + 8 * n + 128 * wj;
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      vaddr[ch] = vb + ch * kTile * RV;
+    for (int ch = 0; ch < NCW; ++ch) {
+      vaddr[ch] = vb + (hf * NCW + ch) * kTile * RV;
       asm volatile("" : "+v"(vaddr[ch]));          // computed once, not per tile
     }
   }
-  constexpr int kMaxIt = (64 * 8 / 16 + NW - 1) / NW;   // records of at most 64 bytes
+  float* obh = ob + hf * NH * a.ob_stride;
+  constexpr int kMaxIt = (64 * 8 / 16 + NWT - 1) / NWT;   // records of at most 64 bytes
 #pragma unroll
   for (int it = 0; it < kMaxIt; ++it) {
-    const int vt = wave + NW * it;
+    const int vt = wj + NWT * it;
     if (vt >= NVT) break;                           // (uniform)
+    if constexpr (kTvHeld)
+      if (it < 4) tv.load_step(hv, it);
     // One accumulator per column tile: a dependent product takes its predecessor's result
     // straight from the matrix unit.
     v4i acc[NT];
@@ -1843,21 +1858,21 @@ void decode_mfma_kernel(const DecodeArgs a) {
     for (int rt = 0; rt < NT; ++rt) acc[rt] = (v4i){0, 0, 0, 0};
     // All of the tile's value-bit words first (one LDS round trip), then the products.
     typedef uint32_t v2u __attribute__((ext_vector_type(2)));
-    v2u wws[NCH];
+    v2u wws[NCW];
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch)
+    for (int ch = 0; ch < NCW; ++ch)
       wws[ch] = *(const __attribute__((address_space(3))) v2u*)(uintptr_t)(
-          vaddr[ch] + 128 * NW * it);
+          vaddr[ch] + 128 * NWT * it);
     // (The scheduler would otherwise pair each read with its products: one LDS round
     // trip per chunk.)
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
+    for (int ch = 0; ch < NCW; ++ch) {
       const v2u ww = wws[ch];
       const v4i av4 = {(int)(ww.x & m0), (int)(ww.x & m1), (int)(ww.y & m0), (int)(ww.y & m1)};
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) {
-        const v4i bop = kPbRegs ? pbr[kPbRegs ? ch * NT + rt : 0] : pb[(ch * NT + rt) * 64 + lane];
+        const v4i bop = kPbRegs ? pbr[kPbRegs ? ch * NT + rt : 0] : pbh[(ch * NT + rt) * 64 + lane];
         acc[rt] = mfma_i8(bop, av4, acc[rt]);
       }
     }
@@ -1869,8 +1884,15 @@ void decode_mfma_kernel(const DecodeArgs a) {
       float f = fmaf((float)d[3], 256.f, (float)d[2]);
       f = fmaf(f, 256.f, (float)d[1]);
       f = fmaf(f, 256.f, (float)d[0]);
-      ob[(4 * rt + g) * a.ob_stride + 16 * vt + n] = f;
+      obh[(4 * rt + g) * a.ob_stride + 16 * vt + n] = f;
     }
+  }
+  if constexpr (kTvHeld) {
+    // (k-steps the loop did not reach: fewer than four tiles for this wave)
+    const int nit = NVT > wj ? (NVT - wj + NWT - 1) / NWT : 0;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+      if (kk >= nit) tv.load_step(hv, kk);
   }
 
   __syncthreads();
@@ -1907,7 +1929,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
       float acc = 0.f;
 #pragma unroll
       for (int k = 0; k < kMaxBits; ++k) {
-        const float t = ldexpf(oh[min(voc + k, 8 * RV - 1)], k);
+        const int v = min(voc + k, 8 * RV - 1);
+        const float t = ldexpf(kHalves ? oh[v] + oh[NH * a.ob_stride + v] : oh[v], k);
         acc += (k < vbc) ? ((k == vbc - 1) ? -t : t) : 0.f;
       }
       const float o = vbc ? ldexpf(vsc * acc, 1 - vbc - fv) : 0.f;
@@ -1995,7 +2018,8 @@ static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
   if (DMA) pb_bytes = std::max(pb_bytes, scr_bytes);
   size_t off = (size_t)a.off_pb + pb_bytes;
   a.ob_stride = 8 * a.rv;
-  const size_t ob_bytes = (size_t)NH * a.ob_stride * 4;
+  // O' per (head, value bit); eight waves keep one copy per chunk half.
+  const size_t ob_bytes = (size_t)(NW == 8 && S % 128 == 0 ? 2 : 1) * NH * a.ob_stride * 4;
   const size_t es_bytes = APPEND ? (sizeof(AppendScratch) + 15) / 16 * 16 : 0;
   constexpr size_t kLdsMax = 160 * 1024 - 4 * 1024;
   if (ob_bytes <= (size_t)S * a.rk) {
