@@ -2,6 +2,8 @@
 // inference part; Sec. 5.2).  Exact VALU kernel: the transform is evaluated as an exact
 // integer dot product on fixed-point operands, so every code is reproducible bit for
 // bit.  Works for any token count; one workgroup per (64-token tile, KV head).
+#include <algorithm>
+
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -110,6 +112,228 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
       const uint32_t old = (mask == 0xffffffffu) ? 0u : out[wi];
       out[wi] = (old & ~mask) | nw;
     }
+  }
+}
+
+// The same canonical encode with the transform on the matrix cores.  The exact integer
+// dot product h_c = sum_j X_j Tq_jc is split into int8 limbs, X = 256 X1 + X0 and
+// Tq = 256 B1 + B0 (X0, B0 in [-128, 127]; X1, B1 in [-64, 64]), and formed from three
+// v_mfma_i32_16x16x64_i8 sums that stay exact in int32: S11 = sum X1 B1 (< 2^19),
+// S10 = sum X1 B0 + X0 B1 (< 2^22), S00 = sum X0 B0 (< 2^21); then
+// h_c = 65536 S11 + (256 S10 + S00) in int64.  Everything after the dot product is the
+// exact kernel's arithmetic, so the codes agree bit for bit.
+// One workgroup of 4 waves per 64-token tile at a time (a grid-stride loop over the tiles
+// of a KV head, so the limb tables of the head's transform are built once per workgroup);
+// wave w takes the tile's tokens 16 w .. 16 w + 15 against all 128 channels.  Lane
+// 16 kg + n reads token n's elements j = 64 kc + 16 kg .. + 15 (kc = 0, 1), the A operand
+// rows; the B operand lane (channel 16 ct + n) reads the same j of row c of Tq^T.  The
+// products leave lane 16 kg + n with channel 16 ct + n of tokens 4 kg + i, i < 4.
+// Needs 16-byte aligned token rows (checked by the launcher).
+constexpr int kTbPitch = 144;                    // bytes per channel row of the limb tables
+
+typedef int ev4i __attribute__((ext_vector_type(4)));
+
+// Low balanced int8 limb of |v| <= 2^14: v = 256 hi + lo with lo in [-128, 127].
+__device__ inline int limb_lo(int v) { return ((v + 128) & 255) - 128; }
+
+template <int CTRL>
+__device__ inline float enc_dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+// Maximum over each row of 16 lanes.
+__device__ inline float enc_row16_max(float v) {
+  v = fmaxf(v, enc_dpp<0xB1>(v));
+  v = fmaxf(v, enc_dpp<0x4E>(v));
+  v = fmaxf(v, enc_dpp<0x124>(v));
+  return fmaxf(v, enc_dpp<0x128>(v));
+}
+// Maximum over lanes l, l ^ 16, l ^ 32 and l ^ 48 (the gfx950 row swaps).
+__device__ inline float enc_cross_row_max(float v) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
+    const void* __restrict__ params, const void* __restrict__ x, int64_t n_tok,
+    int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
+    int64_t cap, int64_t pos) {
+  static_assert(kEncThreads == 256, "four waves of 16 tokens per 64-token tile");
+  __shared__ __align__(16) int8_t tb[2][kD * kTbPitch];   // [limb][channel c][j]
+  __shared__ uint32_t rec[kTile][kRecWords];              // records of the tile's tokens
+  __shared__ __align__(16) int shift_s[kTile];
+
+  const int head = blockIdx.y;
+  const HeadParams* hp = head_params(params, head);
+  const int rbytes = hp->record_bytes;
+  const int rwords = rbytes / 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 15, kg = lane >> 4;
+
+  // Limb tables of the transposed fixed-point transform (two elements per thread step).
+  for (int i = tid; i < kD * kD / 2; i += kEncThreads) {
+    const uint32_t w = reinterpret_cast<const uint32_t*>(hp->Tqt)[i];
+    const int c = (2 * i) >> 7, j = (2 * i) & (kD - 1);
+    const int v0 = (int)(int16_t)(w & 0xffffu), v1 = (int)(int16_t)(w >> 16);
+    const int l0 = limb_lo(v0), l1 = limb_lo(v1);
+    const int h0 = (v0 - l0) >> 8, h1 = (v1 - l1) >> 8;
+    *reinterpret_cast<uint16_t*>(&tb[0][c * kTbPitch + j]) = (uint16_t)((l0 & 255) | ((l1 & 255) << 8));
+    *reinterpret_cast<uint16_t*>(&tb[1][c * kTbPitch + j]) = (uint16_t)((h0 & 255) | ((h1 & 255) << 8));
+  }
+  // This lane's channels 16 ct + n: widths, first record bits, 1/s_c.
+  int bc[8], oc[8];
+  float isc[8];
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct) {
+    const int c = 16 * ct + n;
+    bc[ct] = hp->bits[c];
+    oc[ct] = hp->bit_off[c];
+    isc[ct] = hp->inv_s[c];
+  }
+
+  const int64_t first = pos / kTile, last = (pos + n_tok - 1) / kTile;
+  for (int64_t tile = first + blockIdx.x; tile <= last; tile += gridDim.x) {
+    const int64_t tile_base = tile * kTile;
+    const int64_t t_begin = max(tile_base, pos);
+    const int64_t t_end = min(tile_base + kTile, pos + n_tok);
+    for (int i = tid; i < kTile * kRecWords; i += kEncThreads) (&rec[0][0])[i] = 0u;
+    // (1) Token 16 wave + n: its elements 64 kc + 16 kg + e, its fixed-point shift.
+    const int tl = 16 * wave + n;
+    const int64_t t = tile_base + tl;
+    const bool valid = t >= t_begin && t < t_end;
+    float xv[2][16];
+    if (valid) {
+      const int64_t base = (t - pos) * x_stride + (int64_t)head * kD;
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc) {
+        if constexpr (BF16) {
+          const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(x) + base +
+                                                          64 * kc + 16 * kg);
+          const uint4 u[2] = {p[0], p[1]};
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const uint32_t wv[4] = {u[q].x, u[q].y, u[q].z, u[q].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              xv[kc][8 * q + 2 * e] = __uint_as_float(wv[e] << 16);
+              xv[kc][8 * q + 2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
+            }
+          }
+        } else {
+          const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(x) + base +
+                                                            64 * kc + 16 * kg);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float4 f = p[q];
+            xv[kc][4 * q] = f.x, xv[kc][4 * q + 1] = f.y, xv[kc][4 * q + 2] = f.z,
+            xv[kc][4 * q + 3] = f.w;
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) xv[kc][e] = 0.f;
+    }
+    float m = 0.f;
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) m = fmaxf(m, fabsf(xv[kc][e]));
+    const int shift = token_shift(enc_cross_row_max(m));
+    if (kg == 0) shift_s[tl] = shift;
+    // (2) The limbs of X = rint(x 2^shift) as A operands (byte e: element e).
+    ev4i A0[2], A1[2];
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t lo = 0u, hi = 0u;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int X = (int)rintf(ldexpf(xv[kc][4 * q + e], shift));
+          const int l = limb_lo(X);
+          lo |= (uint32_t)(l & 255) << (8 * e);
+          hi |= (uint32_t)(((X - l) >> 8) & 255) << (8 * e);
+        }
+        A0[kc][q] = (int)lo;
+        A1[kc][q] = (int)hi;
+      }
+    // (3) The three limb sums per (token, channel).
+    ev4i s11[8], s10[8], s00[8];
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) {
+      s11[ct] = s10[ct] = s00[ct] = (ev4i){0, 0, 0, 0};
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc) {
+        const int o = (16 * ct + n) * kTbPitch + 64 * kc + 16 * kg;
+        const ev4i b0 = *reinterpret_cast<const ev4i*>(&tb[0][o]);
+        const ev4i b1 = *reinterpret_cast<const ev4i*>(&tb[1][o]);
+        s11[ct] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1[kc], b1, s11[ct], 0, 0, 0);
+        s10[ct] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1[kc], b0, s10[ct], 0, 0, 0);
+        s10[ct] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[kc], b1, s10[ct], 0, 0, 0);
+        s00[ct] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[kc], b0, s00[ct], 0, 0, 0);
+      }
+    }
+    // (4) Tokens 16 wave + 4 kg + i of this lane (their shifts from this wave's lanes).
+    const ev4i sh4 = *reinterpret_cast<const ev4i*>(&shift_s[16 * wave + 4 * kg]);
+    float r[8][4], am[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int low = s10[ct][i] * 256 + s00[ct][i];
+        const long long h = (long long)s11[ct][i] * 65536 + (long long)low;
+        r[ct][i] = fixed_point_result(h, sh4[i]) * isc[ct];
+        if (bc[ct] > 0) am[i] = fmaxf(am[i], fabsf(r[ct][i]));
+      }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float a = enc_row16_max(am[i]);
+      const __half a16 = token_alpha(a);
+      const float inv_a = inverse_alpha(a16);
+      const int tok = 16 * wave + 4 * kg + i;
+      const int64_t tg = tile_base + tok;
+      if (tg >= t_begin && tg < t_end) {
+#pragma unroll
+        for (int ct = 0; ct < 8; ++ct) {
+          const int b = bc[ct], off = oc[ct];
+          if (b > 0) {
+            const uint32_t u = quantize_code(r[ct][i], inv_a, b);
+            atomicOr(&rec[tok][off >> 5], u << (off & 31));
+            if ((off & 31) + b > 32) atomicOr(&rec[tok][(off >> 5) + 1], u >> (32 - (off & 31)));
+          }
+        }
+        if (n == 0) alpha[(int64_t)head * cap + tg] = __half_as_ushort(a16);
+      }
+    }
+    __syncthreads();
+    const int lo = (int)(t_begin - tile_base), hi = (int)(t_end - tile_base);
+    if (layout == AATC_LAYOUT_RECORDS) {
+      uint32_t* out = reinterpret_cast<uint32_t*>(codes) + ((int64_t)head * cap + tile_base) * rwords;
+      for (int i = lo * rwords + tid; i < hi * rwords; i += kEncThreads)
+        out[i] = rec[i / rwords][i % rwords];
+    } else {
+      uint32_t* out = reinterpret_cast<uint32_t*>(codes) +
+                      ((int64_t)head * (cap / kTile) + tile) * (16 * rbytes);
+      for (int wi = tid; wi < 16 * rbytes; wi += kEncThreads) {
+        const int v = wi >> 1, W = wi & 1;
+        uint32_t mask = 0, nw = 0;
+        for (int p = 0; p < 32; ++p) {
+          const int tt = 16 * (2 * W + (p & 1)) + 4 * ((p >> 1) & 3) + (p >> 3);
+          if (tt >= lo && tt < hi) {
+            mask |= 1u << p;
+            nw |= ((rec[tt][v >> 5] >> (v & 31)) & 1u) << p;
+          }
+        }
+        if (!mask) continue;
+        const uint32_t old = (mask == 0xffffffffu) ? 0u : out[wi];
+        out[wi] = (old & ~mask) | nw;
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -228,7 +452,25 @@ aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_d
     return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
   }
   const int64_t first = pos / kTile, last = (pos + n_tok - 1) / kTile;
-  dim3 grid((unsigned)(last - first + 1), (unsigned)n_heads);
+  const int64_t n_tiles = last - first + 1;
+  const size_t esize = x_dtype == AATC_BF16 ? 2 : 4;
+  const bool aligned = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
+                       ((size_t)x_tok_stride * esize) % 16 == 0;
+  if (aligned) {
+    // A grid-stride loop of at most 64 workgroups per KV head (each builds the head's limb
+    // tables once).
+    dim3 grid((unsigned)std::min<int64_t>(n_tiles, 64), (unsigned)n_heads);
+    if (x_dtype == AATC_BF16)
+      hipLaunchKernelGGL(encode_mfma_kernel<true>, grid, dim3(kEncThreads), 0,
+                         (hipStream_t)stream, params, x, n_tok, x_tok_stride, (int)layout,
+                         static_cast<uint8_t*>(codes), alpha, cap, pos);
+    else
+      hipLaunchKernelGGL(encode_mfma_kernel<false>, grid, dim3(kEncThreads), 0,
+                         (hipStream_t)stream, params, x, n_tok, x_tok_stride, (int)layout,
+                         static_cast<uint8_t*>(codes), alpha, cap, pos);
+    return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
+  }
+  dim3 grid((unsigned)n_tiles, (unsigned)n_heads);
   hipLaunchKernelGGL(encode_exact_kernel, grid, dim3(kEncThreads), 0, (hipStream_t)stream,
                      params, x, (int)x_dtype, n_tok, x_tok_stride, (int)layout,
                      static_cast<uint8_t*>(codes), alpha, cap, pos);
