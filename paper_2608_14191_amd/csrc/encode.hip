@@ -155,6 +155,44 @@ __device__ inline float enc_cross_row_max(float v) {
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
+// One stage of a 32 x 32 bit-matrix transpose over the 32 lanes of each half wave (lane i
+// holds row i): blocks of S bits are exchanged with lane i ^ S.
+template <int S, uint32_t M>
+__device__ inline uint32_t bit_transpose_stage(uint32_t x, int lane) {
+  const uint32_t y = (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1f | (S << 10));
+  return (lane & S) ? ((x & ~M) | ((y >> S) & M)) : ((x & M) | ((y & M) << S));
+}
+
+template <bool BF16>
+__device__ inline void load_token_elems(const void* x, int64_t base, int kg, float (&xv)[2][16]) {
+#pragma unroll
+  for (int kc = 0; kc < 2; ++kc) {
+    if constexpr (BF16) {
+      const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(x) + base +
+                                                      64 * kc + 16 * kg);
+      const uint4 u[2] = {p[0], p[1]};
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const uint32_t wv[4] = {u[q].x, u[q].y, u[q].z, u[q].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          xv[kc][8 * q + 2 * e] = __uint_as_float(wv[e] << 16);
+          xv[kc][8 * q + 2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
+        }
+      }
+    } else {
+      const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(x) + base +
+                                                        64 * kc + 16 * kg);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 f = p[q];
+        xv[kc][4 * q] = f.x, xv[kc][4 * q + 1] = f.y, xv[kc][4 * q + 2] = f.z,
+        xv[kc][4 * q + 3] = f.w;
+      }
+    }
+  }
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int64_t n_tok,
@@ -171,15 +209,27 @@ __global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
   const int rwords = rbytes / 4;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 15, kg = lane >> 4;
 
-  // Limb tables of the transposed fixed-point transform (two elements per thread step).
-  for (int i = tid; i < kD * kD / 2; i += kEncThreads) {
-    const uint32_t w = reinterpret_cast<const uint32_t*>(hp->Tqt)[i];
-    const int c = (2 * i) >> 7, j = (2 * i) & (kD - 1);
-    const int v0 = (int)(int16_t)(w & 0xffffu), v1 = (int)(int16_t)(w >> 16);
-    const int l0 = limb_lo(v0), l1 = limb_lo(v1);
-    const int h0 = (v0 - l0) >> 8, h1 = (v1 - l1) >> 8;
-    *reinterpret_cast<uint16_t*>(&tb[0][c * kTbPitch + j]) = (uint16_t)((l0 & 255) | ((l1 & 255) << 8));
-    *reinterpret_cast<uint16_t*>(&tb[1][c * kTbPitch + j]) = (uint16_t)((h0 & 255) | ((h1 & 255) << 8));
+  // Limb tables of the transposed fixed-point transform: thread tid converts elements
+  // 8 (tid + 256 k) .. + 7 of Tq^T (all 16-byte loads issued first).
+  {
+    uint4 tw[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) tw[k] = reinterpret_cast<const uint4*>(hp->Tqt)[tid + kEncThreads * k];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int e0 = 8 * (tid + kEncThreads * k), c = e0 >> 7, j = e0 & (kD - 1);
+      const uint32_t wv[4] = {tw[k].x, tw[k].y, tw[k].z, tw[k].w};
+      uint32_t lo[2] = {0u, 0u}, hi[2] = {0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int v = (int)(int16_t)((e & 1) ? (wv[e >> 1] >> 16) : (wv[e >> 1] & 0xffffu));
+        const int l = limb_lo(v);
+        lo[e >> 2] |= (uint32_t)(l & 255) << (8 * (e & 3));
+        hi[e >> 2] |= (uint32_t)(((v - l) >> 8) & 255) << (8 * (e & 3));
+      }
+      *reinterpret_cast<uint2*>(&tb[0][c * kTbPitch + j]) = make_uint2(lo[0], lo[1]);
+      *reinterpret_cast<uint2*>(&tb[1][c * kTbPitch + j]) = make_uint2(hi[0], hi[1]);
+    }
   }
   // This lane's channels 16 ct + n: widths, first record bits, 1/s_c.
   int bc[8], oc[8];
@@ -191,52 +241,32 @@ __global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
     oc[ct] = hp->bit_off[c];
     isc[ct] = hp->inv_s[c];
   }
+  // Value tiles: lane p of a wave stands for tile bit position p (word p / 32, bit p % 32),
+  // i.e. token 16 (2 (p / 32) + p % 2) + 4 ((p / 2) % 4) + (p % 32) / 8.
+  const int ptok = 16 * (2 * (lane >> 5) + (lane & 1)) + 4 * ((lane >> 1) & 3) + ((lane & 31) >> 3);
 
   const int64_t first = pos / kTile, last = (pos + n_tok - 1) / kTile;
-  for (int64_t tile = first + blockIdx.x; tile <= last; tile += gridDim.x) {
-    const int64_t tile_base = tile * kTile;
-    const int64_t t_begin = max(tile_base, pos);
-    const int64_t t_end = min(tile_base + kTile, pos + n_tok);
-    for (int i = tid; i < kTile * kRecWords; i += kEncThreads) (&rec[0][0])[i] = 0u;
-    // (1) Token 16 wave + n: its elements 64 kc + 16 kg + e, its fixed-point shift.
-    const int tl = 16 * wave + n;
-    const int64_t t = tile_base + tl;
-    const bool valid = t >= t_begin && t < t_end;
-    float xv[2][16];
-    if (valid) {
-      const int64_t base = (t - pos) * x_stride + (int64_t)head * kD;
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc) {
-        if constexpr (BF16) {
-          const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(x) + base +
-                                                          64 * kc + 16 * kg);
-          const uint4 u[2] = {p[0], p[1]};
-#pragma unroll
-          for (int q = 0; q < 2; ++q) {
-            const uint32_t wv[4] = {u[q].x, u[q].y, u[q].z, u[q].w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              xv[kc][8 * q + 2 * e] = __uint_as_float(wv[e] << 16);
-              xv[kc][8 * q + 2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
-            }
-          }
-        } else {
-          const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(x) + base +
-                                                            64 * kc + 16 * kg);
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float4 f = p[q];
-            xv[kc][4 * q] = f.x, xv[kc][4 * q + 1] = f.y, xv[kc][4 * q + 2] = f.z,
-            xv[kc][4 * q + 3] = f.w;
-          }
-        }
-      }
+  // Token 16 wave + n of the tile: the element loads run one tile ahead.
+  const int tl = 16 * wave + n;
+  float xv[2][16];
+  auto fetch = [&](int64_t tile) {
+    const int64_t t = tile * kTile + tl;
+    if (tile <= last && t >= pos && t < pos + n_tok) {
+      load_token_elems<BF16>(x, (t - pos) * x_stride + (int64_t)head * kD, kg, xv);
     } else {
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
         for (int e = 0; e < 16; ++e) xv[kc][e] = 0.f;
     }
+  };
+  fetch(first + blockIdx.x);
+  for (int64_t tile = first + blockIdx.x; tile <= last; tile += gridDim.x) {
+    const int64_t tile_base = tile * kTile;
+    const int64_t t_begin = max(tile_base, pos);
+    const int64_t t_end = min(tile_base + kTile, pos + n_tok);
+    for (int i = tid; i < kTile * kRecWords; i += kEncThreads) (&rec[0][0])[i] = 0u;
+    // (1) The token's fixed-point shift (max over its 128 elements: 4 lanes).
     float m = 0.f;
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc)
@@ -261,34 +291,46 @@ __global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
         A0[kc][q] = (int)lo;
         A1[kc][q] = (int)hi;
       }
-    // (3) The three limb sums per (token, channel).
-    ev4i s11[8], s10[8], s00[8];
-#pragma unroll
-    for (int ct = 0; ct < 8; ++ct) {
-      s11[ct] = s10[ct] = s00[ct] = (ev4i){0, 0, 0, 0};
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc) {
-        const int o = (16 * ct + n) * kTbPitch + 64 * kc + 16 * kg;
-        const ev4i b0 = *reinterpret_cast<const ev4i*>(&tb[0][o]);
-        const ev4i b1 = *reinterpret_cast<const ev4i*>(&tb[1][o]);
-        s11[ct] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1[kc], b1, s11[ct], 0, 0, 0);
-        s10[ct] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1[kc], b0, s10[ct], 0, 0, 0);
-        s10[ct] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[kc], b1, s10[ct], 0, 0, 0);
-        s00[ct] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[kc], b0, s00[ct], 0, 0, 0);
-      }
-    }
-    // (4) Tokens 16 wave + 4 kg + i of this lane (their shifts from this wave's lanes).
+    fetch(tile + gridDim.x);                      // the next tile's elements, in flight
+    if (tile == first + blockIdx.x) __syncthreads();   // (the limb tables)
+    // (3) Four channel tiles at a time: the three limb sums, then r_c.  Tokens
+    //     16 wave + 4 kg + i of this lane take their shifts from this wave's lanes.
     const ev4i sh4 = *reinterpret_cast<const ev4i*>(&shift_s[16 * wave + 4 * kg]);
     float r[8][4], am[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ct = 0; ct < 8; ++ct)
+    for (int c4 = 0; c4 < 8; c4 += 4) {
+      ev4i s11[4], s10[4], s00[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int low = s10[ct][i] * 256 + s00[ct][i];
-        const long long h = (long long)s11[ct][i] * 65536 + (long long)low;
-        r[ct][i] = fixed_point_result(h, sh4[i]) * isc[ct];
-        if (bc[ct] > 0) am[i] = fmaxf(am[i], fabsf(r[ct][i]));
+      for (int u = 0; u < 4; ++u) {
+        const int ct = c4 + u;
+        s11[u] = s10[u] = s00[u] = (ev4i){0, 0, 0, 0};
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+          const int o = (16 * ct + n) * kTbPitch + 64 * kc + 16 * kg;
+          const ev4i b0 = *reinterpret_cast<const ev4i*>(&tb[0][o]);
+          const ev4i b1 = *reinterpret_cast<const ev4i*>(&tb[1][o]);
+          s11[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1[kc], b1, s11[u], 0, 0, 0);
+          s10[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1[kc], b0, s10[u], 0, 0, 0);
+          s10[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[kc], b1, s10[u], 0, 0, 0);
+          s00[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[kc], b0, s00[u], 0, 0, 0);
+        }
       }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int ct = c4 + u;
+          // 65536 S11 + (256 S10 + S00), exact in fp64 (< 2^37), then the one rounding
+          // of the canonical result.
+          const int low = s10[u][i] * 256 + s00[u][i];
+          const double h = fma((double)s11[u][i], 65536.0, (double)low);
+          r[ct][i] = (float)ldexp(h, -(sh4[i] + kTFrac)) * isc[ct];
+          if (bc[ct] > 0) am[i] = fmaxf(am[i], fabsf(r[ct][i]));
+        }
+      // (one half's accumulators at a time)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // (4) Token scales, codes, records.
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float a = enc_row16_max(am[i]);
@@ -316,21 +358,23 @@ __global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
       for (int i = lo * rwords + tid; i < hi * rwords; i += kEncThreads)
         out[i] = rec[i / rwords][i % rwords];
     } else {
+      // Record word w of the tile's tokens -> tile words 64 w .. 64 w + 63.  Lane p holds
+      // the word of the token at position p; a 32 x 32 bit transpose within each half of
+      // the wave (five butterfly stages on lane-xor swizzles) leaves lane 32 W + b with bit
+      // 32 w + b over the positions of half W: tile word 2 (32 w + b) + W.
       uint32_t* out = reinterpret_cast<uint32_t*>(codes) +
                       ((int64_t)head * (cap / kTile) + tile) * (16 * rbytes);
-      for (int wi = tid; wi < 16 * rbytes; wi += kEncThreads) {
-        const int v = wi >> 1, W = wi & 1;
-        uint32_t mask = 0, nw = 0;
-        for (int p = 0; p < 32; ++p) {
-          const int tt = 16 * (2 * W + (p & 1)) + 4 * ((p >> 1) & 3) + (p >> 3);
-          if (tt >= lo && tt < hi) {
-            mask |= 1u << p;
-            nw |= ((rec[tt][v >> 5] >> (v & 31)) & 1u) << p;
-          }
-        }
-        if (!mask) continue;
-        const uint32_t old = (mask == 0xffffffffu) ? 0u : out[wi];
-        out[wi] = (old & ~mask) | nw;
+      const uint64_t vmask = __builtin_amdgcn_ballot_w64(ptok >= lo && ptok < hi);
+      const uint32_t keep = ~(uint32_t)((lane >> 5) ? (vmask >> 32) : vmask);
+      for (int w = wave; w < rwords; w += kEncThreads / 64) {
+        uint32_t x = rec[ptok][w];
+        x = bit_transpose_stage<16, 0x0000ffffu>(x, lane);
+        x = bit_transpose_stage<8, 0x00ff00ffu>(x, lane);
+        x = bit_transpose_stage<4, 0x0f0f0f0fu>(x, lane);
+        x = bit_transpose_stage<2, 0x33333333u>(x, lane);
+        x = bit_transpose_stage<1, 0x55555555u>(x, lane);
+        uint32_t* o = out + 64 * w + 2 * (lane & 31) + (lane >> 5);
+        *o = keep ? ((*o & keep) | (x & ~keep)) : x;
       }
     }
     __syncthreads();
@@ -457,9 +501,9 @@ aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_d
   const bool aligned = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
                        ((size_t)x_tok_stride * esize) % 16 == 0;
   if (aligned) {
-    // A grid-stride loop of at most 64 workgroups per KV head (each builds the head's limb
+    // A grid-stride loop of at most 128 workgroups per KV head (each builds the head's limb
     // tables once).
-    dim3 grid((unsigned)std::min<int64_t>(n_tiles, 64), (unsigned)n_heads);
+    dim3 grid((unsigned)std::min<int64_t>(n_tiles, 128), (unsigned)n_heads);
     if (x_dtype == AATC_BF16)
       hipLaunchKernelGGL(encode_mfma_kernel<true>, grid, dim3(kEncThreads), 0,
                          (hipStream_t)stream, params, x, n_tok, x_tok_stride, (int)layout,
