@@ -125,9 +125,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
 // One workgroup of 4 waves per 64-token tile at a time (a grid-stride loop over the tiles
 // of a KV head, so the limb tables of the head's transform are built once per workgroup);
 // wave w takes the tile's tokens 16 w .. 16 w + 15 against all 128 channels.  Lane
-// 16 kg + n reads token n's elements j = 64 kc + 16 kg .. + 15 (kc = 0, 1), the A operand
-// rows; the B operand lane (channel 16 ct + n) reads the same j of row c of Tq^T.  The
-// products leave lane 16 kg + n with channel 16 ct + n of tokens 4 kg + i, i < 4.
+// 16 kg + n reads token n's elements j = 64 kc + 16 kg .. + 15 (kc = 0, 1): the B operand
+// columns; the A operand lane (channel 16 ct + n) reads the same j of row c of Tq^T.  The
+// products leave lane 16 kg + n with channels 16 ct + 4 kg + i, i < 4, of its own token, so
+// a lane's four consecutive codes go into the record as one bit field.
 // Needs 16-byte aligned token rows (checked by the launcher).
 constexpr int kTbPitch = 144;                    // bytes per channel row of the limb tables
 
@@ -194,14 +195,17 @@ __device__ inline void load_token_elems(const void* x, int64_t base, int kg, flo
 }
 
 template <bool BF16>
-__global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
+__global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
+                          amdgpu_waves_per_eu(2, 2))) void encode_mfma_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int64_t n_tok,
     int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
     int64_t cap, int64_t pos) {
   static_assert(kEncThreads == 256, "four waves of 16 tokens per 64-token tile");
   __shared__ __align__(16) int8_t tb[2][kD * kTbPitch];   // [limb][channel c][j]
   __shared__ uint32_t rec[kTile][kRecWords];              // records of the tile's tokens
-  __shared__ __align__(16) int shift_s[kTile];
+  __shared__ __align__(16) float tab_is[kD];              // 1 / s_c
+  __shared__ __align__(16) uint32_t tab_b[kD / 4];        // widths, four channels a word
+  __shared__ __align__(16) uint16_t tab_o[kD];            // first record bits
 
   const int head = blockIdx.y;
   const HeadParams* hp = head_params(params, head);
@@ -231,16 +235,12 @@ __global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
       *reinterpret_cast<uint2*>(&tb[1][c * kTbPitch + j]) = make_uint2(hi[0], hi[1]);
     }
   }
-  // This lane's channels 16 ct + n: widths, first record bits, 1/s_c.
-  int bc[8], oc[8];
-  float isc[8];
-#pragma unroll
-  for (int ct = 0; ct < 8; ++ct) {
-    const int c = 16 * ct + n;
-    bc[ct] = hp->bits[c];
-    oc[ct] = hp->bit_off[c];
-    isc[ct] = hp->inv_s[c];
+  // Channel tables (read per tile by the lanes that hold channels 16 ct + 4 kg + i).
+  if (tid < kD) {
+    tab_is[tid] = hp->inv_s[tid];
+    tab_o[tid] = hp->bit_off[tid];
   }
+  if (tid < kD / 4) tab_b[tid] = reinterpret_cast<const uint32_t*>(hp->bits)[tid];
   // Value tiles: lane p of a wave stands for tile bit position p (word p / 32, bit p % 32),
   // i.e. token 16 (2 (p / 32) + p % 2) + 4 ((p / 2) % 4) + (p % 32) / 8.
   const int ptok = 16 * (2 * (lane >> 5) + (lane & 1)) + 4 * ((lane >> 1) & 3) + ((lane & 31) >> 3);
@@ -265,6 +265,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
     const int64_t tile_base = tile * kTile;
     const int64_t t_begin = max(tile_base, pos);
     const int64_t t_end = min(tile_base + kTile, pos + n_tok);
+    const bool valid = tile_base + tl >= t_begin && tile_base + tl < t_end;
     for (int i = tid; i < kTile * kRecWords; i += kEncThreads) (&rec[0][0])[i] = 0u;
     // (1) The token's fixed-point shift (max over its 128 elements: 4 lanes).
     float m = 0.f;
@@ -273,7 +274,6 @@ __global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
 #pragma unroll
       for (int e = 0; e < 16; ++e) m = fmaxf(m, fabsf(xv[kc][e]));
     const int shift = token_shift(enc_cross_row_max(m));
-    if (kg == 0) shift_s[tl] = shift;
     // (2) The limbs of X = rint(x 2^shift) as A operands (byte e: element e).
     ev4i A0[2], A1[2];
 #pragma unroll
@@ -292,11 +292,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
         A1[kc][q] = (int)hi;
       }
     fetch(tile + gridDim.x);                      // the next tile's elements, in flight
-    if (tile == first + blockIdx.x) __syncthreads();   // (the limb tables)
-    // (3) Four channel tiles at a time: the three limb sums, then r_c.  Tokens
-    //     16 wave + 4 kg + i of this lane take their shifts from this wave's lanes.
-    const ev4i sh4 = *reinterpret_cast<const ev4i*>(&shift_s[16 * wave + 4 * kg]);
-    float r[8][4], am[4] = {0.f, 0.f, 0.f, 0.f};
+    if (tile == first + blockIdx.x) __syncthreads();   // (the limb and channel tables)
+    // (3) Four channel tiles at a time: the three limb sums, then r_c for channels
+    //     16 ct + 4 kg + i of this lane's token.
+    float r[8][4], am = 0.f;
 #pragma unroll
     for (int c4 = 0; c4 < 8; c4 += 4) {
       ev4i s11[4], s10[4], s00[4];
@@ -309,47 +308,56 @@ __global__ __launch_bounds__(kEncThreads) void encode_mfma_kernel(
           const int o = (16 * ct + n) * kTbPitch + 64 * kc + 16 * kg;
           const ev4i b0 = *reinterpret_cast<const ev4i*>(&tb[0][o]);
           const ev4i b1 = *reinterpret_cast<const ev4i*>(&tb[1][o]);
-          s11[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1[kc], b1, s11[u], 0, 0, 0);
-          s10[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A1[kc], b0, s10[u], 0, 0, 0);
-          s10[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[kc], b1, s10[u], 0, 0, 0);
-          s00[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A0[kc], b0, s00[u], 0, 0, 0);
+          s11[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A1[kc], s11[u], 0, 0, 0);
+          s10[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A1[kc], s10[u], 0, 0, 0);
+          s10[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A0[kc], s10[u], 0, 0, 0);
+          s00[u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A0[kc], s00[u], 0, 0, 0);
         }
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 4; ++u) {
+        const int ct = c4 + u, c0 = 16 * ct + 4 * kg;
+        const float4 is4 = *reinterpret_cast<const float4*>(&tab_is[c0]);
+        const float isv[4] = {is4.x, is4.y, is4.z, is4.w};
+        const uint32_t bw = tab_b[c0 >> 2];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int ct = c4 + u;
           // 65536 S11 + (256 S10 + S00), exact in fp64 (< 2^37), then the one rounding
           // of the canonical result.
           const int low = s10[u][i] * 256 + s00[u][i];
           const double h = fma((double)s11[u][i], 65536.0, (double)low);
-          r[ct][i] = (float)ldexp(h, -(sh4[i] + kTFrac)) * isc[ct];
-          if (bc[ct] > 0) am[i] = fmaxf(am[i], fabsf(r[ct][i]));
+          r[ct][i] = (float)ldexp(h, -(shift + kTFrac)) * isv[i];
+          if ((bw >> (8 * i)) & 255u) am = fmaxf(am, fabsf(r[ct][i]));
         }
+      }
       // (one half's accumulators at a time)
       __builtin_amdgcn_sched_barrier(0);
     }
-    // (4) Token scales, codes, records.
+    // (4) The token's scale (its 128 channels: 4 lanes), its codes and record: channels
+    //     16 ct + 4 kg .. + 3 are consecutive in the record, one bit field of <= 32 bits.
+    const __half a16 = token_alpha(enc_cross_row_max(am));
+    const float inv_a = inverse_alpha(a16);
+    if (valid) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float a = enc_row16_max(am[i]);
-      const __half a16 = token_alpha(a);
-      const float inv_a = inverse_alpha(a16);
-      const int tok = 16 * wave + 4 * kg + i;
-      const int64_t tg = tile_base + tok;
-      if (tg >= t_begin && tg < t_end) {
+      for (int ct = 0; ct < 8; ++ct) {
+        const int c0 = 16 * ct + 4 * kg;
+        const uint32_t bw = tab_b[c0 >> 2];
+        uint32_t field = 0u;
+        int width = 0;
 #pragma unroll
-        for (int ct = 0; ct < 8; ++ct) {
-          const int b = bc[ct], off = oc[ct];
-          if (b > 0) {
-            const uint32_t u = quantize_code(r[ct][i], inv_a, b);
-            atomicOr(&rec[tok][off >> 5], u << (off & 31));
-            if ((off & 31) + b > 32) atomicOr(&rec[tok][(off >> 5) + 1], u >> (32 - (off & 31)));
-          }
+        for (int i = 0; i < 4; ++i) {
+          const int b = (int)((bw >> (8 * i)) & 255u);
+          const uint32_t u = b ? quantize_code(r[ct][i], inv_a, b) : 0u;
+          field |= u << width;
+          width += b;
         }
-        if (n == 0) alpha[(int64_t)head * cap + tg] = __half_as_ushort(a16);
+        const int off = tab_o[c0];
+        if (width > 0) {
+          atomicOr(&rec[tl][off >> 5], field << (off & 31));
+          if ((off & 31) + width > 32) atomicOr(&rec[tl][(off >> 5) + 1], field >> (32 - (off & 31)));
+        }
       }
+      if (kg == 0) alpha[(int64_t)head * cap + tile_base + tl] = __half_as_ushort(a16);
     }
     __syncthreads();
     const int lo = (int)(t_begin - tile_base), hi = (int)(t_end - tile_base);
