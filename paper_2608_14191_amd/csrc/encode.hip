@@ -196,7 +196,7 @@ __device__ inline void load_token_elems(const void* x, int64_t base, int kg, flo
 
 template <bool BF16>
 __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
-                          amdgpu_waves_per_eu(2, 2))) void encode_mfma_kernel(
+                          amdgpu_waves_per_eu(3, 3))) void encode_mfma_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int64_t n_tok,
     int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
     int64_t cap, int64_t pos) {
