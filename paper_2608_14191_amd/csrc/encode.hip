@@ -509,9 +509,9 @@ aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_d
   const bool aligned = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
                        ((size_t)x_tok_stride * esize) % 16 == 0;
   if (aligned) {
-    // A grid-stride loop of at most 128 workgroups per KV head (each builds the head's limb
+    // A grid-stride loop of at most 96 workgroups per KV head (each builds the head's limb
     // tables once).
-    dim3 grid((unsigned)std::min<int64_t>(n_tiles, 128), (unsigned)n_heads);
+    dim3 grid((unsigned)std::min<int64_t>(n_tiles, 96), (unsigned)n_heads);
     if (x_dtype == AATC_BF16)
       hipLaunchKernelGGL(encode_mfma_kernel<true>, grid, dim3(kEncThreads), 0,
                          (hipStream_t)stream, params, x, n_tok, x_tok_stride, (int)layout,
