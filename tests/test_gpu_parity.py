@@ -174,6 +174,33 @@ def test_encode_incremental_appends_match_bulk():
         np.testing.assert_array_equal(va[h, :300].cpu().numpy().view(np.uint16), av.view(np.uint16))
 
 
+def test_encode_unaligned_rows_match_oracle():
+    """Token rows that are not 16-byte aligned take the VALU encode path: same codes."""
+    case = Case(cfg=2, n_tokens=200)
+    H, cap, n = case.w.n_kv_heads, case.cap, 200
+    pk, pv = device_params(case.cal_k), device_params(case.cal_v)
+    caches = {}
+    for kind, pp, cal, layout in (("k", pk, case.cal_k, P.LAYOUT_RECORDS),
+                                  ("v", pv, case.cal_v, P.LAYOUT_TILES)):
+        x = case.x_tokens(0, kind).reshape(n, H * 128)
+        xp = torch.zeros((n, H * 128 + 1), dtype=x.dtype, device=x.device)
+        xp[:, :H * 128] = x
+        rb = cal[0].record_bytes
+        codes = record_cache(H, cap, rb) if kind == "k" else tile_cache(H, cap, rb)
+        al = alpha_cache(H, cap)
+        P.aatc_encode(pp, H, xp, n, H * 128 + 1, layout, codes, al, cap, 0)
+        caches[kind] = (codes, al)
+    torch.cuda.synchronize()
+    for h in range(H):
+        rk, ak = case.oracle_encode(0, h, "k")
+        rv, av = case.oracle_encode(0, h, "v")
+        np.testing.assert_array_equal(caches["k"][0][h, :n].cpu().numpy(), rk)
+        np.testing.assert_array_equal(caches["k"][1][h, :n].cpu().numpy().view(np.uint16), ak.view(np.uint16))
+        got = ora.tiles_to_records(caches["v"][0][h].cpu().numpy(), rv.shape[1])
+        np.testing.assert_array_equal(got[:n], rv)
+        np.testing.assert_array_equal(caches["v"][1][h, :n].cpu().numpy().view(np.uint16), av.view(np.uint16))
+
+
 def test_decode_edge_lengths():
     """Empty, single-token, tile-edge and ragged lengths in one batch."""
     lens = [0, 1, 63, 64, 65, 511, 512, 513]
