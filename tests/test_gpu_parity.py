@@ -295,3 +295,63 @@ def test_append_decode_matches_encode_then_decode(name):
             continue
         assert rel_l2(got[b], ref[b]) <= TOL, (b, case.lens[b], rel_l2(got[b], ref[b]))
         assert rel_l2(got[b], sep[b]) <= 1e-5, (b, case.lens[b])
+
+
+FULL_SIZE = {
+    # the benchmark's workload and launch (append the last token, decode all 32768)
+    "cfg2_llama_32k": dict(cfg=2, sample=[(0, 0), (0, 5)]),
+    "cfg3_qwen_16k_b8": dict(cfg=3, sample=[(3, 1), (7, 3)]),
+}
+
+
+@pytest.mark.parametrize("name", list(FULL_SIZE))
+def test_full_size_sampled(name):
+    """Full-size workloads through aatc_append_decode_attention: the packed caches of
+    sampled (sequence, KV head) pairs are bit-exact, including the appended token, and
+    the outputs of their query heads are within TOL of the oracle."""
+    spec = FULL_SIZE[name]
+    full = workload(spec["cfg"])
+    _log(f"[full] {name}: batch {full.batch}, {full.n_tokens} tokens, "
+         f"{full.n_q_heads}/{full.n_kv_heads} heads")
+    case = Case(cfg=spec["cfg"], n_tokens=full.n_tokens, batch=full.batch)
+    w = case.w
+    B, H, HQ, cap = w.batch, w.n_kv_heads, w.n_q_heads, case.cap
+    rk, rv = case.cal_k[0].record_bytes, case.cal_v[0].record_bytes
+    pk, pv = device_params(case.cal_k), device_params(case.cal_v)
+    kc, vc = record_cache(H, cap, rk, batch=B), tile_cache(H, cap, rv, batch=B)
+    ka, va = alpha_cache(H, cap, batch=B), alpha_cache(H, cap, batch=B)
+    xk_new = torch.zeros((B, H, 128), dtype=torch.bfloat16 if w.dtype == "bf16" else torch.float32)
+    xv_new = torch.zeros_like(xk_new)
+    for b in range(B):
+        n = case.lens[b]
+        xk, xv = case.x_tokens(b, "k"), case.x_tokens(b, "v")
+        P.aatc_encode(pk, H, xk, n - 1, H * 128, P.LAYOUT_RECORDS, kc[b], ka[b], cap, 0)
+        P.aatc_encode(pv, H, xv, n - 1, H * 128, P.LAYOUT_TILES, vc[b], va[b], cap, 0)
+        xk_new[b], xv_new[b] = xk[n - 1].cpu(), xv[n - 1].cpu()
+        del xk, xv
+    q = stored_to_torch(np.stack(case.q)).cuda()
+    lens = torch.tensor(case.lens, dtype=torch.int32, device="cuda")
+    out = torch.full((B, HQ, 128), float("nan"), dtype=torch.float32, device="cuda")
+    ws = torch.zeros(P.aatc_decode_workspace_bytes(B, HQ, H, cap), dtype=torch.uint8,
+                     device="cuda")
+    P.aatc_append_decode_attention(pk, pv, B, HQ, H, q, xk_new.cuda(), xv_new.cuda(), kc, ka,
+                                   vc, va, lens, cap, rk, rv, 1 / np.sqrt(128), out, ws)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    assert np.all(np.isfinite(got))
+    g = HQ // H
+    for b, h in spec["sample"]:
+        n = case.lens[b]
+        ok_, oa = case.oracle_encode(b, h, "k")
+        ov_, ova = case.oracle_encode(b, h, "v")
+        np.testing.assert_array_equal(kc[b, h, :n].cpu().numpy(), ok_)
+        np.testing.assert_array_equal(ka[b, h, :n].cpu().numpy().view(np.uint16), oa.view(np.uint16))
+        np.testing.assert_array_equal(ora.tiles_to_records(vc[b, h].cpu().numpy(), rv)[:n], ov_)
+        np.testing.assert_array_equal(va[b, h, :n].cpu().numpy().view(np.uint16), ova.view(np.uint16))
+        kh = ora.decode_tokens(ok_, oa, case.cal_k[h])
+        vh = ora.decode_tokens(ov_, ova, case.cal_v[h])
+        q32 = w.as_f32(case.q[b])[h * g:(h + 1) * g]
+        ref = ora.softmax_attention(q32, kh, vh, 1 / np.sqrt(128))
+        err = rel_l2(got[b, h * g:(h + 1) * g], ref)
+        _log(f"  seq {b} kv head {h}: rel_l2 {err:.3e}")
+        assert err <= TOL
