@@ -134,6 +134,18 @@ constexpr int kTbPitch = 144;                    // bytes per channel row of the
 
 typedef int ev4i __attribute__((ext_vector_type(4)));
 
+// The canonical quantizer without branches: the same code as quantize_code for b >= 1,
+// and 0 for b = 0 (whose r is 0: 1/s is stored as 0 for dropped channels).
+__device__ inline uint32_t quantize_code_nb(float r, float inv_a, int b) {
+  const int bb = max(b, 1);
+  const float xq = ldexpf(r * inv_a, bb - 1);
+  const float f = floorf(xq);
+  int code = (int)f + ((xq - f) >= 0.5f ? 1 : 0);
+  const int half = 1 << (bb - 1);
+  code = min(max(code, -half), half - 1);
+  return __builtin_amdgcn_ubfe((uint32_t)code, 0u, (uint32_t)b);
+}
+
 // Low balanced int8 limb of |v| <= 2^14: v = 256 hi + lo with lo in [-128, 127].
 __device__ inline int limb_lo(int v) { return ((v + 128) & 255) - 128; }
 
@@ -327,7 +339,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
           const int low = s10[u][i] * 256 + s00[u][i];
           const double h = fma((double)s11[u][i], 65536.0, (double)low);
           r[ct][i] = (float)ldexp(h, -(shift + kTFrac)) * isv[i];
-          if ((bw >> (8 * i)) & 255u) am = fmaxf(am, fabsf(r[ct][i]));
+          am = fmaxf(am, fabsf(r[ct][i]));          // (r = 0 on dropped channels)
         }
       }
       // (one half's accumulators at a time)
@@ -347,7 +359,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int b = (int)((bw >> (8 * i)) & 255u);
-          const uint32_t u = b ? quantize_code(r[ct][i], inv_a, b) : 0u;
+          const uint32_t u = quantize_code_nb(r[ct][i], inv_a, b);
           field |= u << width;
           width += b;
         }
