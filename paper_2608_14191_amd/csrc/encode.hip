@@ -295,16 +295,21 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
     for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        uint32_t lo = 0u, hi = 0u;
+        // The low limb's byte is X mod 256 and the high limb is floor((X + 128) / 256);
+        // byte e of each dword gathered with two byte permutes.
+        uint32_t X[4], H[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int X = (int)rintf(ldexpf(xv[kc][4 * q + e], shift));
-          const int l = limb_lo(X);
-          lo |= (uint32_t)(l & 255) << (8 * e);
-          hi |= (uint32_t)(((X - l) >> 8) & 255) << (8 * e);
+          X[e] = (uint32_t)(int)rintf(ldexpf(xv[kc][4 * q + e], shift));
+          H[e] = (uint32_t)(((int)X[e] + 128) >> 8);
         }
-        A0[kc][q] = (int)lo;
-        A1[kc][q] = (int)hi;
+        // v_perm_b32(a, b, sel): byte k of the result is byte sel_k of the pair {a: 4..7, b: 0..3}
+        const uint32_t lo01 = __builtin_amdgcn_perm(X[1], X[0], 0x0c0c0400u);
+        const uint32_t lo23 = __builtin_amdgcn_perm(X[3], X[2], 0x04000c0cu);
+        const uint32_t hi01 = __builtin_amdgcn_perm(H[1], H[0], 0x0c0c0400u);
+        const uint32_t hi23 = __builtin_amdgcn_perm(H[3], H[2], 0x04000c0cu);
+        A0[kc][q] = (int)(lo01 | lo23);
+        A1[kc][q] = (int)(hi01 | hi23);
       }
     fetch(tile + gridDim.x);                      // the next tile's elements, in flight
     if (tile == first + blockIdx.x) __syncthreads();   // (the limb and channel tables)
