@@ -290,26 +290,6 @@ __device__ inline uint32_t quad_xor2(uint32_t v) {
 __device__ inline float quad_xor1(float v) { return __uint_as_float(quad_xor1(__float_as_uint(v))); }
 __device__ inline float quad_xor2(float v) { return __uint_as_float(quad_xor2(__float_as_uint(v))); }
 
-// Reduce-scatter over the quad: lane L of the quad returns sum over the quad's lanes of
-// their x[L].
-__device__ inline float quad_reduce_scatter(const float x[4], int L) {
-  const bool o1 = L & 1, o2 = L & 2;
-  const float k0 = o1 ? x[1] : x[0], s0 = o1 ? x[0] : x[1];
-  const float k1 = o1 ? x[3] : x[2], s1 = o1 ? x[2] : x[3];
-  const float y0 = k0 + quad_xor1(s0), y1 = k1 + quad_xor1(s1);
-  const float keep = o2 ? y1 : y0, send = o2 ? y0 : y1;
-  return keep + quad_xor2(send);
-}
-
-__device__ inline float quad_max(float v) {
-  v = fmaxf(v, quad_xor1(v));
-  return fmaxf(v, quad_xor2(v));
-}
-__device__ inline float quad_sum(float v) {
-  v += quad_xor1(v);
-  return v + quad_xor2(v);
-}
-
 // Four balanced int8 limbs of a 32-bit value |x| < 2^30, packed in one dword (limb L in
 // byte L, two's complement): x = sum_L limb_L 256^L.
 __device__ inline uint32_t pack_limbs(int x) {
