@@ -150,6 +150,9 @@ aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_t n_kv_head
  *              TILES needs cap % 64 == 0; tokens of a partly written tile that lie
  *              outside [pos, pos + n_tok) keep their bits.
  * n_tok == 0 is a no-op.  Errors: AATC_E_INVALID.
+ * Speed: more than 16 tokens with 16-byte aligned token rows (x and x_tok_stride times
+ * the element size) run on the matrix cores; other layouts take a slower kernel that
+ * writes the same codes.
  */
 aatc_status aatc_encode(const void* dev_params, int32_t n_kv_heads, int32_t d,
                         const void* x, aatc_dtype x_dtype, int64_t n_tok,
