@@ -301,10 +301,16 @@ FULL_SIZE = {
     # the benchmark's workload and launch (append the last token, decode all 32768)
     "cfg2_llama_32k": dict(cfg=2, sample=[(0, 0), (0, 5)]),
     "cfg3_qwen_16k_b8": dict(cfg=3, sample=[(3, 1), (7, 3)]),
+    # the largest decode workload: 4 x 131072 tokens, 2.0 bits, zero-bit key channels,
+    # 128 splits per (sequence, KV head) into one merge
+    "cfg5_long_131k_b4": dict(cfg=5, sample=[(0, 0), (3, 6)]),
 }
+# generating 4 x 8 x 131072 stored tokens per tensor takes about a minute on the host
+_FULL_SLOW = {"cfg5_long_131k_b4"}
 
 
-@pytest.mark.parametrize("name", list(FULL_SIZE))
+@pytest.mark.parametrize("name", [pytest.param(n, marks=pytest.mark.timeout(360))
+                                  if n in _FULL_SLOW else n for n in FULL_SIZE])
 def test_full_size_sampled(name):
     """Full-size workloads through aatc_append_decode_attention: the packed caches of
     sampled (sequence, KV head) pairs are bit-exact, including the appended token, and
@@ -314,6 +320,7 @@ def test_full_size_sampled(name):
     _log(f"[full] {name}: batch {full.batch}, {full.n_tokens} tokens, "
          f"{full.n_q_heads}/{full.n_kv_heads} heads")
     case = Case(cfg=spec["cfg"], n_tokens=full.n_tokens, batch=full.batch)
+    _log(f"  generated, bits k {case.cal_k[0].record_bytes * 8} v {case.cal_v[0].record_bytes * 8}")
     w = case.w
     B, H, HQ, cap = w.batch, w.n_kv_heads, w.n_q_heads, case.cap
     rk, rv = case.cal_k[0].record_bytes, case.cal_v[0].record_bytes
