@@ -362,3 +362,34 @@ def test_full_size_sampled(name):
         err = rel_l2(got[b, h * g:(h + 1) * g], ref)
         _log(f"  seq {b} kv head {h}: rel_l2 {err:.3e}")
         assert err <= TOL
+
+
+@pytest.mark.parametrize("avg_bits", [2.75, 4.0])
+def test_full_size_prefill_encode_sampled(avg_bits):
+    """The prefill workload at full size (65536 new tokens x 8 KV heads, one aatc_encode
+    per tensor, as the benchmark launches it): sampled heads' key records, value tiles
+    and scales are bit-exact against the oracle at both budgets."""
+    full = workload(4)
+    _log(f"[full] prefill encode: {full.n_tokens} tokens, {full.n_kv_heads} heads, "
+         f"{avg_bits} bits")
+    case = Case(cfg=4, n_tokens=full.n_tokens, avg_bits=avg_bits)
+    w = case.w
+    H, cap, n = w.n_kv_heads, case.cap, case.lens[0]
+    rk, rv = case.cal_k[0].record_bytes, case.cal_v[0].record_bytes
+    pk, pv = device_params(case.cal_k), device_params(case.cal_v)
+    kc, vc = record_cache(H, cap, rk), tile_cache(H, cap, rv)
+    ka, va = alpha_cache(H, cap), alpha_cache(H, cap)
+    xk, xv = case.x_tokens(0, "k"), case.x_tokens(0, "v")
+    P.aatc_encode(pk, H, xk, n, H * 128, P.LAYOUT_RECORDS, kc, ka, cap, 0)
+    P.aatc_encode(pv, H, xv, n, H * 128, P.LAYOUT_TILES, vc, va, cap, 0)
+    torch.cuda.synchronize()
+    for h in (1, 6):
+        ok_, oa = case.oracle_encode(0, h, "k")
+        ov_, ova = case.oracle_encode(0, h, "v")
+        got = kc[h, :n].cpu().numpy()
+        bad = np.argwhere(np.any(got != ok_, axis=1))
+        assert bad.size == 0, f"head {h}: key records differ at tokens {bad[:5].ravel()}"
+        np.testing.assert_array_equal(ka[h, :n].cpu().numpy().view(np.uint16), oa.view(np.uint16))
+        np.testing.assert_array_equal(vc[h].cpu().numpy(), oracle_tiles(ov_, cap))
+        np.testing.assert_array_equal(va[h, :n].cpu().numpy().view(np.uint16), ova.view(np.uint16))
+        _log(f"  head {h}: records {rk} / {rv} B bit-exact")
