@@ -153,6 +153,50 @@ def allocate_bits(w_var: np.ndarray, budget: int, b_max: int) -> np.ndarray:
     return b
 
 
+def allocate_global(sigma2, weight, avg_bits: float, b_max: int, n_protect: int = 3,
+                    protect_extra: int = 0, normalize_weight: bool = False,
+                    pct: float = 95.0) -> np.ndarray:
+    """One tensor's (keys' or values') widths over all layers at once.
+
+    The water-filling problem of Sec. 5.2 sums the distortion over layers under a single
+    budget; App. E adds two rules for it: each layer's variances (and, for the keys, its
+    weights) are divided by that layer's own 95th percentile, which removes the activation
+    scale that differs between layers, and the first three layers are protected with a
+    fixed budget of the average width (values) or the average plus one bit (keys).
+    Readings (the paper gives no formula):
+      - the total budget is round(avg_bits m L) bits for L layers of m channels; the
+        protected layers take round((avg_bits + protect_extra) m) each and the other
+        layers share what is left, by the greedy of ``allocate_bits`` over all their
+        channels (first (layer, channel) on ties);
+      - inside a protected layer the same greedy runs on its own channels;
+      - the percentile interpolates linearly; a layer whose percentile is 0 is not scaled.
+    ``sigma2`` and ``weight`` are [L][m] (``weight`` None means 1).  Returns bits [L][m].
+    """
+    s2 = np.asarray(sigma2, dtype=np.float64)
+    if s2.ndim != 2:
+        raise ValueError("sigma2 must be [layers][channels]")
+    n_layers, m = s2.shape
+    w = np.ones_like(s2) if weight is None else np.asarray(weight, dtype=np.float64)
+    if w.shape != s2.shape or not (np.all(s2 >= 0) and np.all(w >= 0)):
+        raise ValueError("weights and variances must be non-negative and of one shape")
+
+    def per_layer_scaled(a):
+        p = np.percentile(a, pct, axis=1, keepdims=True)
+        return a / np.where(p > 0, p, 1.0)
+
+    w_var = (per_layer_scaled(w) if normalize_weight else w) * per_layer_scaled(s2)
+    n_prot = min(n_protect, n_layers)
+    total = int(np.floor(avg_bits * m * n_layers + 0.5))
+    prot = int(np.floor((avg_bits + protect_extra) * m + 0.5))
+    bits = np.zeros((n_layers, m), dtype=np.int64)
+    for layer in range(n_prot):
+        bits[layer] = allocate_bits(w_var[layer], prot, b_max)
+    if n_layers > n_prot:
+        rest = total - n_prot * prot
+        bits[n_prot:] = allocate_bits(w_var[n_prot:].ravel(), rest, b_max).reshape(-1, m)
+    return bits
+
+
 def allocation_objective(w_var: np.ndarray, bits: np.ndarray) -> float:
     """sum_c W_c 2^(-2 b_c) (eq. waterfilling-keys)."""
     return float(np.sum(np.ldexp(np.asarray(w_var, dtype=np.float64), -2 * np.asarray(bits))))

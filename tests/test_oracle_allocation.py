@@ -128,3 +128,75 @@ def test_channel_scale_is_99th_percentile_of_magnitude():
     # sorted |h_c|: 300 zeros, then 1..100 (x 2^-c); position 0.99 * 399 = 395.01
     for c in range(d):
         assert float(cal.s16[c]) == float(np.float16(96.01 * 2.0 ** -c))
+
+
+# ---- one budget over all layers (Sec. 5.2; App. E's normalization and protected layers)
+
+def test_global_pool_is_optimal_brute_force():
+    """Layers whose two channels have equal variance are normalized to (1, 1) whatever
+    their scale, so the pool's objective is sum w_c 4^-b_c; the greedy over all layers
+    reaches the minimum of every allocation of the budget (enumerated)."""
+    import itertools
+    s2 = np.array([[0.3, 0.3], [7.0, 7.0], [1e-3, 1e-3]])
+    w = np.array([[5.0, 0.25], [1.0, 3.0], [0.5, 9.0]])
+    b_max = 3
+    for avg in (0.5, 1.0, 1.5, 2.0):
+        got = aatc.allocate_global(s2, w, avg, b_max, n_protect=0)
+        total = int(np.floor(avg * 6 + 0.5))
+        assert got.sum() == total
+        best = min(float(np.sum(w.ravel() * 4.0 ** -np.array(b)))
+                   for b in itertools.product(range(b_max + 1), repeat=6) if sum(b) == total)
+        assert np.sum(w * 4.0 ** -got) == pytest.approx(best, rel=1e-15)
+
+
+def test_global_single_layer_is_the_per_head_allocation():
+    """With one unprotected layer the per-layer scale is a common factor, which the
+    greedy's decisions do not see: the widths are those of allocate_bits on w sigma2."""
+    rng = np.random.default_rng(11)
+    s2, w = rng.gamma(0.7, size=(1, 64)), rng.gamma(1.5, size=(1, 64))
+    for norm in (False, True):
+        got = aatc.allocate_global(s2, w, 2.75, 8, n_protect=0, normalize_weight=norm)
+        np.testing.assert_array_equal(got[0], aatc.allocate_bits(w[0] * s2[0], 176, 8))
+
+
+def test_global_layer_scale_is_removed():
+    """Scaling one layer's variances (and, when normalized, its weights) by a power of
+    two leaves every width unchanged; identical layers at different scales get
+    identical widths."""
+    rng = np.random.default_rng(5)
+    s2, w = rng.gamma(0.5, size=(6, 32)), rng.gamma(1.0, size=(6, 32))
+    base = aatc.allocate_global(s2, w, 2.0, 8, n_protect=2, protect_extra=1,
+                               normalize_weight=True)
+    k = np.ldexp(1.0, np.array([-12, 3, 0, 7, -2, 20]))[:, None]
+    j = np.ldexp(1.0, np.array([4, -6, 1, 0, 9, -3]))[:, None]
+    np.testing.assert_array_equal(
+        aatc.allocate_global(s2 * k, w * j, 2.0, 8, n_protect=2, protect_extra=1,
+                            normalize_weight=True), base)
+    same = np.repeat(s2[:1], 4, axis=0) * np.ldexp(1.0, np.array([-10, 0, 5, -3]))[:, None]
+    got = aatc.allocate_global(same, None, 2.5, 8, n_protect=0)
+    assert np.all(got == got[0])
+
+
+def test_global_budgets_and_protected_layers():
+    rng = np.random.default_rng(8)
+    s2, w = rng.gamma(0.5, size=(7, 40)), rng.gamma(1.0, size=(7, 40))
+    avg, m, L = 2.75, 40, 7
+    got = aatc.allocate_global(s2, w, avg, 8, n_protect=3, protect_extra=1, normalize_weight=True)
+    assert got.min() >= 0 and got.max() <= 8
+    assert got.sum() == int(np.floor(avg * m * L + 0.5))
+    for layer in range(3):
+        assert got[layer].sum() == int(np.floor((avg + 1) * m + 0.5))
+        # a protected layer is allocated on its own channels
+        np.testing.assert_array_equal(got[layer], aatc.allocate_bits(w[layer] * s2[layer],
+                                                                    int(got[layer].sum()), 8))
+    # all layers protected: the total plays no part
+    allp = aatc.allocate_global(s2[:2], None, 2.0, 8, n_protect=3, protect_extra=1)
+    assert list(allp.sum(axis=1)) == [120, 120]
+
+
+def test_global_rejects_unmeetable_budgets():
+    s2 = np.ones((4, 8))
+    with pytest.raises(ValueError):     # protected layers take more than the total
+        aatc.allocate_global(s2, None, 0.5, 8, n_protect=3, protect_extra=1)
+    with pytest.raises(ValueError):     # the pool exceeds b_max per channel
+        aatc.allocate_global(s2, None, 8.5, 8, n_protect=0)
