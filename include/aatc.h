@@ -114,6 +114,37 @@ aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int32_t d,
                            aatc_calibration* out);
 
 /*
+ * aatc_allocate_global -- integer widths of one tensor (keys or values) over all layers
+ * under a single budget (host only).
+ *
+ * Sec. 5.2 states the water-filling problem summed over layers with one budget per
+ * tensor; App. E divides each layer's variances (and the key weights) by that layer's
+ * own 95th percentile, and protects the first layers with a fixed budget (the average
+ * width for values, one bit more for keys).  Readings: the total is round(avg_bits m L)
+ * bits; each protected layer takes round((avg_bits + protect_extra) m) and allocates it
+ * over its own channels; the other layers share the rest; every allocation is the greedy
+ * of aatc_calibrate (largest W_c 4^-b_c first, lowest (layer, channel) on ties) on
+ * W = w' sigma2', the percentile interpolating linearly and a zero percentile leaving
+ * the layer unscaled.
+ *
+ * sigma2   host, [n_layers][m] channel variances (eigenvalues, any channel order), >= 0.
+ * weight   host, [n_layers][m] channel weights >= 0, or NULL for all ones.
+ * m        channels per layer (all KV heads of the layer together).
+ * b_max    1..8; n_protect >= 0 (3 in the paper; more than n_layers protects all).
+ * protect_extra     bits above the average for protected layers (1 keys, 0 values).
+ * normalize_weight  nonzero: the weights are scaled per layer as well (keys).
+ * bits     host, caller-allocated [n_layers][m], fully written on success.
+ * Errors: AATC_E_INVALID for NULL pointers, sizes or ranges, negative or non-finite
+ * inputs, and budgets that no allocation in [0, b_max] meets.  The decode kernels take
+ * one record width per call, so the heads of one layer must end with equal totals to
+ * share a call.
+ */
+aatc_status aatc_allocate_global(const double* sigma2, const double* weight,
+                                 int32_t n_layers, int32_t m, double avg_bits,
+                                 int32_t b_max, int32_t n_protect, int32_t protect_extra,
+                                 int32_t normalize_weight, uint8_t* bits);
+
+/*
  * aatc_params_bytes / aatc_params_pack -- build the device parameter block of one
  * tensor (K or V) for n_kv_heads heads from their calibrations (host only).
  *

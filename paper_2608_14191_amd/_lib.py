@@ -133,6 +133,27 @@ def aatc_calibrate(x_calib, avg_bits: float, b_max: int = 8, percentile: float =
     return out
 
 
+_L.aatc_allocate_global.restype = ctypes.c_int
+_L.aatc_allocate_global.argtypes = [_vp, _vp, _i32, _i32, _f64, _i32, _i32, _i32, _i32, _vp]
+
+
+def aatc_allocate_global(sigma2, weight, avg_bits: float, b_max: int = 8, n_protect: int = 3,
+                         protect_extra: int = 0, normalize_weight: bool = False) -> np.ndarray:
+    """Widths [L][m] of one tensor over all layers under one budget (host only)."""
+    s2 = np.ascontiguousarray(sigma2, dtype=np.float64)
+    if s2.ndim != 2:
+        raise ValueError("sigma2 must be [layers][channels]")
+    w = None if weight is None else np.ascontiguousarray(weight, dtype=np.float64)
+    if w is not None and w.shape != s2.shape:
+        raise ValueError("weight and sigma2 differ in shape")
+    bits = np.zeros(s2.shape, dtype=np.uint8)
+    st = _L.aatc_allocate_global(_np_ptr(s2), None if w is None else _np_ptr(w), s2.shape[0],
+                                 s2.shape[1], float(avg_bits), b_max, n_protect, protect_extra,
+                                 int(bool(normalize_weight)), _np_ptr(bits))
+    _check("aatc_allocate_global", st)
+    return bits
+
+
 def aatc_params_bytes(n_kv_heads: int) -> int:
     return int(_L.aatc_params_bytes(int(n_kv_heads)))
 

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstring>
 #include <numeric>
+#include <queue>
 #include <vector>
 
 #include "aatc.h"
@@ -278,6 +279,85 @@ extern "C" aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int
       std::sort(col.begin(), col.end());
       out->scale_f16[c] = f64_to_f16_bits(percentile_linear(col, percentile));
     }
+    return AATC_OK;
+  } catch (...) {
+    return AATC_E_INVALID;
+  }
+}
+
+namespace aatc {
+namespace {
+
+// Greedy marginal allocation of `budget` bits over w_var[0..n): each bit goes to the
+// channel of largest W_c 4^(-b_c) among those below b_max, the lowest index on ties.  A
+// heap holds one entry per open channel with its current gain; ldexp keeps the gains
+// exact, so the decisions are those of a scan for the first maximum.
+void greedy_bits(const double* w_var, int64_t n, int64_t budget, int b_max, uint8_t* bits) {
+  struct Entry { double gain; int64_t idx; };
+  auto less = [](const Entry& a, const Entry& b) {
+    return a.gain < b.gain || (a.gain == b.gain && a.idx > b.idx);
+  };
+  std::priority_queue<Entry, std::vector<Entry>, decltype(less)> heap(less);
+  for (int64_t c = 0; c < n; ++c) {
+    bits[c] = 0;
+    heap.push({w_var[c], c});
+  }
+  for (int64_t step = 0; step < budget; ++step) {
+    const Entry e = heap.top();
+    heap.pop();
+    const int b = ++bits[e.idx];
+    if (b < b_max) heap.push({std::ldexp(w_var[e.idx], -2 * b), e.idx});
+  }
+}
+
+}  // namespace
+}  // namespace aatc
+
+extern "C" aatc_status aatc_allocate_global(const double* sigma2, const double* weight,
+                                            int32_t n_layers, int32_t m, double avg_bits,
+                                            int32_t b_max, int32_t n_protect,
+                                            int32_t protect_extra, int32_t normalize_weight,
+                                            uint8_t* bits) {
+  try {
+    if (!sigma2 || !bits || n_layers < 1 || m < 1 || b_max < 1 || b_max > AATC_MAX_BITS ||
+        n_protect < 0 || protect_extra < 0 || !std::isfinite(avg_bits) || avg_bits < 0.0)
+      return AATC_E_INVALID;
+    const int64_t n = (int64_t)n_layers * m;
+    for (int64_t i = 0; i < n; ++i) {
+      if (!(std::isfinite(sigma2[i]) && sigma2[i] >= 0.0)) return AATC_E_INVALID;
+      if (weight && !(std::isfinite(weight[i]) && weight[i] >= 0.0)) return AATC_E_INVALID;
+    }
+    const int n_prot = std::min(n_protect, n_layers);
+    const int64_t total = (int64_t)std::floor(avg_bits * m * n_layers + 0.5);
+    const int64_t prot = (int64_t)std::floor((avg_bits + protect_extra) * m + 0.5);
+    const int64_t rest = total - n_prot * prot;
+    const int64_t cap = (int64_t)m * b_max;
+    if (n_prot > 0 && prot > cap) return AATC_E_INVALID;
+    if (n_layers > n_prot && (rest < 0 || rest > (n_layers - n_prot) * cap))
+      return AATC_E_INVALID;
+    // Per-layer scale: the layer's 95th percentile (linear interpolation), 1 if it is 0.
+    auto layer_scale = [&](const double* a) {
+      std::vector<double> v(a, a + m);
+      std::sort(v.begin(), v.end());
+      const double p = percentile_linear(v, 0.95);
+      return p > 0.0 ? p : 1.0;
+    };
+    std::vector<double> w_var(n);
+    for (int l = 0; l < n_layers; ++l) {
+      const double* s2 = sigma2 + (int64_t)l * m;
+      const double* w = weight ? weight + (int64_t)l * m : nullptr;
+      const double ps = layer_scale(s2);
+      const double pw = (w && normalize_weight) ? layer_scale(w) : 1.0;
+      for (int c = 0; c < m; ++c) {
+        const double wc = w ? (normalize_weight ? w[c] / pw : w[c]) : 1.0;
+        w_var[(int64_t)l * m + c] = wc * (s2[c] / ps);
+      }
+    }
+    for (int l = 0; l < n_prot; ++l)
+      greedy_bits(w_var.data() + (int64_t)l * m, m, prot, b_max, bits + (int64_t)l * m);
+    if (n_layers > n_prot)
+      greedy_bits(w_var.data() + (int64_t)n_prot * m, n - (int64_t)n_prot * m, rest, b_max,
+                  bits + (int64_t)n_prot * m);
     return AATC_OK;
   } catch (...) {
     return AATC_E_INVALID;

@@ -215,3 +215,40 @@ def test_append_decode_validates_before_launch():
     assert L.aatc_append_decode_attention(*bad) == 1
     bad = list(args); bad[22] = ws - 1               # workspace too small
     assert L.aatc_append_decode_attention(*bad) == 5
+
+
+def _global_cases():
+    rng = np.random.default_rng(2024)
+    ints = rng.integers(0, 4, size=(5, 16)).astype(np.float64)      # many exact ties
+    zero = rng.gamma(0.5, size=(4, 24))
+    zero[1] = 0.0                                                   # percentile 0
+    return [
+        (rng.gamma(0.5, size=(5, 8)), rng.gamma(1.0, size=(5, 8)), 2.0, 8, 3, 1, True),
+        (rng.gamma(0.3, size=(8, 512)), rng.gamma(1.0, size=(8, 512)), 2.75, 8, 3, 1, True),
+        (rng.gamma(0.3, size=(8, 512)), None, 2.75, 8, 3, 0, False),
+        (ints, ints[::-1].copy(), 1.5, 4, 0, 0, True),
+        (zero, None, 3.0, 6, 1, 0, False),
+        (rng.gamma(0.5, size=(2, 64)), None, 2.0, 8, 3, 1, False),  # all protected
+        (rng.gamma(0.5, size=(1, 128)), rng.gamma(1.0, size=(1, 128)), 2.0, 8, 0, 0, True),
+    ]
+
+
+@pytest.mark.parametrize("case", range(7))
+def test_allocate_global_matches_oracle(case):
+    """aatc_allocate_global against the oracle, width for width."""
+    s2, w, avg, b_max, n_prot, extra, norm = _global_cases()[case]
+    want = ora.allocate_global(s2, w, avg, b_max, n_protect=n_prot, protect_extra=extra,
+                               normalize_weight=norm)
+    got = P.aatc_allocate_global(s2, w, avg, b_max, n_prot, extra, norm)
+    np.testing.assert_array_equal(got.astype(np.int64), want)
+
+
+def test_allocate_global_errors():
+    s2 = np.ones((4, 8))
+    for args in [(s2, None, 0.5, 8, 3, 1, False),      # protected layers exceed the total
+                 (s2, None, 8.5, 8, 0, 0, False),      # the pool exceeds b_max
+                 (s2, None, 2.0, 9, 3, 0, False),      # b_max above 8
+                 (-s2, None, 2.0, 8, 3, 0, False),     # negative variance
+                 (s2, np.full((4, 8), np.nan), 2.0, 8, 3, 0, False)]:
+        with pytest.raises(P.AatcError):
+            P.aatc_allocate_global(*args)
