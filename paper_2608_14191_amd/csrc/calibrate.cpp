@@ -320,8 +320,9 @@ extern "C" aatc_status aatc_allocate_global(const double* sigma2, const double* 
                                             uint8_t* bits) {
   try {
     if (!sigma2 || !bits || n_layers < 1 || m < 1 || b_max < 1 || b_max > AATC_MAX_BITS ||
-        n_protect < 0 || protect_extra < 0 || !std::isfinite(avg_bits) || avg_bits < 0.0)
-      return AATC_E_INVALID;
+        n_protect < 0 || protect_extra < 0 || protect_extra > AATC_MAX_BITS ||
+        !std::isfinite(avg_bits) || avg_bits < 0.0 || avg_bits > AATC_MAX_BITS)
+      return AATC_E_INVALID;                       // (also keeps the budgets in int64)
     const int64_t n = (int64_t)n_layers * m;
     for (int64_t i = 0; i < n; ++i) {
       if (!(std::isfinite(sigma2[i]) && sigma2[i] >= 0.0)) return AATC_E_INVALID;

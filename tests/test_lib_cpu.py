@@ -248,6 +248,7 @@ def test_allocate_global_errors():
     for args in [(s2, None, 0.5, 8, 3, 1, False),      # protected layers exceed the total
                  (s2, None, 8.5, 8, 0, 0, False),      # the pool exceeds b_max
                  (s2, None, 2.0, 9, 3, 0, False),      # b_max above 8
+                 (s2, None, 1e300, 8, 0, 0, False),    # an average beyond any width
                  (-s2, None, 2.0, 8, 3, 0, False),     # negative variance
                  (s2, np.full((4, 8), np.nan), 2.0, 8, 3, 0, False)]:
         with pytest.raises(P.AatcError):
