@@ -71,7 +71,9 @@ typedef struct {
   int32_t record_bytes;         /* R = 4 * ceil(B / 32) */
   int32_t d_active;             /* channels with >= 1 bit */
   float transform[AATC_HEAD_DIM * AATC_HEAD_DIM]; /* row-major [j][c] = T_jc: column c
-                                   is the unit eigenvector of storage channel c */
+                                   is the unit eigenvector of storage channel c, stored
+                                   on the 2^-22 grid (every entry a multiple of 2^-22,
+                                   |T_jc| <= 1, so exactly an fp32 number) */
   uint8_t bits[AATC_HEAD_DIM];  /* width of storage channel c, non-increasing */
   uint16_t scale_f16[AATC_HEAD_DIM]; /* s_c as fp16 bits (0 for dropped channels) */
   int32_t perm[AATC_HEAD_DIM];  /* eigen index (by decreasing eigenvalue) of channel c */
@@ -94,6 +96,7 @@ typedef struct {
  *   with sum_c b_c = round(avg_bits * d) and 0 <= b_c <= b_max, by exact greedy
  *   marginal allocation (ties to the lower eigen index); s_c = fp16 of the
  *   `percentile` quantile (linear interpolation) of |h_c| over the calibration tokens.
+ *   The transform is stored with each entry rounded to the nearest multiple of 2^-22.
  *
  * x_calib  host [n_calib][d] fp32 calibration samples of this head (n_calib >= 2).
  * q_calib  host [n_q][d] fp32 calibration queries of the q_group query heads that
@@ -148,14 +151,13 @@ aatc_status aatc_allocate_global(const double* sigma2, const double* weight,
  * aatc_params_bytes / aatc_params_pack -- build the device parameter block of one
  * tensor (K or V) for n_kv_heads heads from their calibrations (host only).
  *
- * The block holds, per head, the fp32 transform, its fixed-point copy used by the
- * encoder (rint(T * 2^14)), widths, bit offsets, fp16 scales and their fp32
- * reciprocals, and bit-to-channel tables for the decoder.  All heads of a tensor
- * must have the same budget (so the same record size).  The caller copies the
- * `bytes` written to `host_buf` into device memory (16-byte aligned) and passes that
- * device pointer to aatc_encode / aatc_decode_attention.
+ * The block holds, per head, the transform (fp32 and as the integers T * 2^22), widths,
+ * bit offsets, fp16 scales and their fp32 reciprocals, and bit-to-channel tables for the
+ * decoder.  All heads of a tensor must have the same budget (so the same record size).
+ * The caller copies the `bytes` written to `host_buf` into device memory (16-byte
+ * aligned) and passes that device pointer to aatc_encode / aatc_decode_attention.
  * Errors: AATC_E_INVALID (NULL, n_kv_heads < 1, bytes too small, budgets differ,
- * malformed calibration).
+ * malformed calibration, a transform entry off the 2^-22 grid or above 1 in magnitude).
  */
 size_t aatc_params_bytes(int32_t n_kv_heads);
 aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_t n_kv_heads,
@@ -165,12 +167,11 @@ aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_t n_kv_head
  * aatc_encode -- append n_tok tokens of one sequence to a compressed cache.
  *
  * Algorithm 1 (inference part: project and append quantized codes) with Sec. 5.2:
- * per token and head, h = T^T x (eq. transformed-cache) in exact fixed-point
- * arithmetic (x scaled per token so max |x_j| lies in [2^13, 2^14) and rounded to
- * integers; T rounded to multiples of 2^-14; one final fp32 rounding); r_c = h_c *
- * (1/s_c); alpha = fp16(max over stored channels of |r_c|); code_c = clamp(floor(
- * r_c * (1/alpha) * 2^(b_c - 1) + 1/2), -2^(b_c-1), 2^(b_c-1) - 1) stored as its
- * b_c-bit two's complement pattern, packed in `layout`.
+ * per token and head, h = T^T x (eq. transformed-cache) with h_c the exact value of
+ * sum_j x_j T_jc rounded once to fp32 (nearest, ties to even); r_c = fl32(h_c * (1/s_c));
+ * alpha = fp16(max over stored channels of |r_c|); code_c = clamp(floor(r_c * (1/alpha) *
+ * 2^(b_c - 1) + 1/2), -2^(b_c-1), 2^(b_c-1) - 1) (the product rounded to fp32, the floor
+ * exact) stored as its b_c-bit two's complement pattern, packed in `layout`.
  *
  * dev_params   device block from aatc_params_pack (this tensor, n_kv_heads heads).
  * x            device [n_tok] tokens, token t at x + t * x_tok_stride elements, each

@@ -23,8 +23,8 @@ Calibration (Alg. 1, offline part; Sec. 5.1 and 5.2), per KV head and tensor (K 
   5. Per-channel scale s_c = 99th percentile of |h_c| over the calibration tokens
      (Sec. 5.2, "The right scaling").
 Encoding (Alg. 1, online part; Sec. 5.2), per token and head:
-  6. h = T^T x (eq. transformed-cache), computed by the canonical fixed-point
-     arithmetic below.
+  6. h = T^T x (eq. transformed-cache): the exact product of the token with the stored
+     transform, rounded once to fp32.
   7. alpha = max_c |h_c / s_c| over the stored channels; the signed uniform quantizer
      with step Delta_c = 2 alpha s_c / 2^b_c (Sec. 5.2).
   8. Bit packing of the codes (layout defined below; the paper is silent on it).
@@ -40,10 +40,12 @@ Readings where the paper is silent or ambiguous (each listed in the design doc)
 * Var-only weights are w = 1 on the orthonormal PCA coefficients (W_c = eigenvalue),
   the reconstruction-error criterion the paper equates with per-layer KVTC.
 * alpha is taken over the stored channels only (zero-bit channels are not cached).
-* Canonical arithmetic, so that codes are reproducible bit for bit: the transform is
-  evaluated exactly in integers on a per-token fixed-point x (13 fractional bits below
-  the token's leading bit) and a fixed-point T (14 fractional bits); the quantizer is
-  the fp32 sequence of ``quantize``.  alpha and s_c are stored as fp16.
+* Stored transform: the fp64 eigenvectors rounded to multiples of 2^-22 (every entry
+  is then exactly an fp32 number).  The transform of a token is the exact real product
+  sum_j x_j T_jc of the token as given (bf16 or fp32 values) with that stored matrix,
+  rounded once to fp32 (nearest, ties to even): a result with a plain definition that
+  does not depend on any order of summation.  The quantizer is the fp32 sequence of
+  ``quantize``.  alpha and s_c are stored as fp16.
 * Storage order of channels: stable sort by bit width, widest first (eigen order
   breaks ties), so dropped channels form a suffix.
 
@@ -54,13 +56,13 @@ the packing layout.  The tests pin them to worked examples of this spec.
 from __future__ import annotations
 
 import dataclasses
+from fractions import Fraction
 from typing import Optional
 
 import numpy as np
 
-# Canonical fixed-point transform parameters (see module docstring).
-X_LEAD_BIT = 13      # the largest |x_j| of a token maps into [2^13, 2^14)
-T_FRAC_BITS = 14     # T entries are multiples of 2^-14
+# The stored transform's entries are multiples of 2^-T_FRAC_BITS (see module docstring).
+T_FRAC_BITS = 22
 TILE_TOKENS = 64     # tokens per tile of the value-cache layout
 FP16_MAX = 65504.0
 
@@ -202,6 +204,14 @@ def allocation_objective(w_var: np.ndarray, bits: np.ndarray) -> float:
     return float(np.sum(np.ldexp(np.asarray(w_var, dtype=np.float64), -2 * np.asarray(bits))))
 
 
+def stored_transform(t64: np.ndarray) -> np.ndarray:
+    """The transform as stored: each entry rounded to the nearest multiple of 2^-22 (ties
+    to even).  For |t| <= 1 that is at most 23 significant bits, so the result is exact
+    in fp32; it is returned as float32."""
+    t = np.asarray(t64, dtype=np.float64)
+    return np.ldexp(np.rint(np.ldexp(t, T_FRAC_BITS)), -T_FRAC_BITS).astype(np.float32)
+
+
 def to_f16(x) -> np.ndarray:
     """Round to fp16 (nearest, ties to even), saturating at the largest finite value."""
     x = np.asarray(x, dtype=np.float64)
@@ -219,7 +229,7 @@ class Calibration:
     bits: np.ndarray          # [d] int64, storage order, non-increasing
     perm: np.ndarray          # [d] eigen index of each storage channel
     T64: np.ndarray           # [d, d] fp64, column c = eigenvector of storage channel c
-    T32: np.ndarray           # [d, d] fp32 rounding of T64 (the transform the path uses)
+    T32: np.ndarray           # [d, d] the stored transform: T64 on the 2^-22 grid (fp32)
     s16: np.ndarray           # [d] fp16 per-channel scales (0 for dropped channels)
     sigma2: np.ndarray        # [d] eigenvalues, eigen order
     weight: np.ndarray        # [d] channel weights, eigen order
@@ -251,7 +261,7 @@ def calibrate(x_calib: np.ndarray, avg_bits: float, b_max: int = 8,
     perm = np.argsort(-bits_eig, kind="stable")
     bits = bits_eig[perm]
     t64 = p[:, perm]
-    t32 = t64.astype(np.float32)
+    t32 = stored_transform(t64)
     # Per-channel scale: 99th percentile of |h_c| over the calibration tokens.
     h = x @ t64
     s = np.zeros(d)
@@ -269,22 +279,85 @@ def calibrate(x_calib: np.ndarray, avg_bits: float, b_max: int = 8,
 # --------------------------------------------------------------------------------------
 # Encoding
 # --------------------------------------------------------------------------------------
-def fixed_point_transform(x32: np.ndarray, t32: np.ndarray) -> np.ndarray:
-    """h = T^T x per token (eq. transformed-cache) in canonical fixed-point arithmetic.
+def round_to_f32(q: Fraction) -> np.float32:
+    """The fp32 number nearest to the rational q (ties to even), with fp32 subnormals and
+    overflow to infinity: the rounding IEEE 754 defines, written out on exact integers."""
+    q = Fraction(q)
+    if q == 0:
+        return np.float32(0.0)
+    neg = q < 0
+    a = -q if neg else q
+    e = a.numerator.bit_length() - a.denominator.bit_length()   # 2^(e-1) < a < 2^(e+1)
+    if a < Fraction(2) ** e:
+        e -= 1                                                  # now 2^e <= a < 2^(e+1)
+    quantum = Fraction(2) ** (max(e, -126) - 23)                # 24 significant bits,
+    m = round(a / quantum)                                      # fewer below 2^-126
+    v = m * quantum
+    if v >= Fraction(2) ** 128:
+        return np.float32(-np.inf if neg else np.inf)
+    return np.float32(-float(v) if neg else float(v))           # exact: v is an fp32 value
 
-    x is scaled per token by 2^S so its largest magnitude lies in [2^13, 2^14) and
-    rounded to integers (ties to even); T is rounded to multiples of 2^-14.  The
-    integer dot products are exact; the result is rounded once to fp32 (ties to even).
+
+def exact_dot_f32(x, t) -> np.float32:
+    """fl32(sum_j x_j t_j) with the sum taken in exact rational arithmetic."""
+    acc = Fraction(0)
+    for xj, tj in zip(np.asarray(x, dtype=np.float64), np.asarray(t, dtype=np.float64)):
+        acc += Fraction(float(xj)) * Fraction(float(tj))
+    return round_to_f32(acc)
+
+
+def transform(x32: np.ndarray, t32: np.ndarray) -> np.ndarray:
+    """h = T^T x per token (eq. transformed-cache; Alg. 1 "project"): h_c is the exact
+    value of sum_j x_j T_jc rounded once to fp32 (nearest, ties to even).  An exact zero
+    is +0.
+
+    x: [n, d] fp32 values (bf16 tokens widened exactly); t: [d, m] the stored transform,
+    multiples of 2^-22 with |t| <= 1.  The sum is formed exactly in integers: with
+    Tq = t 2^22 and, per token, x_j = 2^-S (X_j + 2^-31 Y_j) with integers X_j, Y_j (S puts
+    max |X| in [2^30, 2^31); |Y| <= 2^30), the sum is 2^-(S+22+31) (2^31 H + L) with
+    H = X Tq and L = Y Tq exact in int64 (below 2^60 for d <= 128).
+      - Where L = 0 (every element a multiple of 2^-S, as for bf16 tokens whose elements
+        are all above 2^-23 of the largest) the result is the int64 H converted to fp32,
+        which rounds once, to nearest with ties to even (pinned by the tests), times the
+        power of two, exact for normal results.
+      - Elsewhere the integer 2^31 H + L is rounded by ``round_to_f32``.
+      - Tokens whose elements are not all multiples of 2^-(S+31), and results in the fp32
+        subnormal range, are redone from the definition in exact rational arithmetic.
     """
-    x = np.asarray(x32, dtype=np.float32).astype(np.float64)
-    m = np.max(np.abs(x), axis=1) if x.shape[1] else np.zeros(x.shape[0])
-    e = np.frexp(m)[1].astype(np.int64) - 1          # floor(log2 m) for m > 0
-    shift = np.where(m > 0, X_LEAD_BIT - e, 0)
-    xi = np.rint(np.ldexp(x, shift[:, None])).astype(np.int64)
-    ti = np.rint(np.ldexp(np.asarray(t32, dtype=np.float32).astype(np.float64),
-                          T_FRAC_BITS)).astype(np.int64)
-    hi = xi @ ti
-    return np.ldexp(hi.astype(np.float64), -(shift + T_FRAC_BITS)[:, None]).astype(np.float32)
+    x = np.asarray(x32, dtype=np.float32)
+    t = np.asarray(t32, dtype=np.float32)
+    n, d = x.shape
+    if d > 128:
+        raise ValueError("at most 128 elements per token")
+    tq_f = np.ldexp(t.astype(np.float64), T_FRAC_BITS)
+    if not (np.all(tq_f == np.rint(tq_f)) and np.all(np.abs(tq_f) <= 2.0 ** T_FRAC_BITS)):
+        raise ValueError("the transform must be on the 2^-22 grid with |t| <= 1")
+    tq = tq_f.astype(np.int64)
+    xd = x.astype(np.float64)
+    m = np.max(np.abs(xd), axis=1) if d else np.zeros(n)
+    e = np.frexp(m)[1] - 1                                   # 2^e <= m < 2^(e+1)
+    S = np.where(m > 0, 30 - e, 0)
+    v = np.ldexp(xd, S[:, None])                             # exact (power-of-two scale)
+    X = np.rint(v)
+    Yf = np.ldexp(v - X, 31)                                 # v - X is exact
+    Y = np.rint(Yf)
+    split_ok = np.all(Y == Yf, axis=1)
+    H = X.astype(np.int64) @ tq
+    h = np.ldexp(H.astype(np.float32), -(S + T_FRAC_BITS)[:, None])
+    rows = np.flatnonzero(split_ok & np.any(Y != 0, axis=1))
+    if rows.size:
+        L = Y[rows].astype(np.int64) @ tq
+        for r, i in enumerate(rows):
+            for c in range(t.shape[1]):
+                V = int(H[i, c]) * 2 ** 31 + int(L[r, c])
+                h[i, c] = round_to_f32(Fraction(V, 2 ** int(S[i] + T_FRAC_BITS + 31))
+                                       if S[i] + T_FRAC_BITS + 31 >= 0 else
+                                       Fraction(V * 2 ** int(-(S[i] + T_FRAC_BITS + 31))))
+    redo = ~split_ok[:, None] | ((np.abs(h) < np.float32(2.0 ** -126)) & (h != 0))
+    for i, c in np.argwhere(redo):
+        h[i, c] = exact_dot_f32(x[i], t[:, c])
+    h[h == 0] = 0.0
+    return h
 
 
 def inverse_f32(v: np.ndarray) -> np.ndarray:
@@ -425,15 +498,16 @@ def tiles_to_records(tiles: np.ndarray, rbytes: int) -> np.ndarray:
 
 def encode(x32: np.ndarray, cal: Calibration):
     """Encode tokens [n, d] of one head: (records [n, R] uint8, alpha16 [n], codes [n, d])."""
-    h = fixed_point_transform(x32, cal.T32)
+    h = transform(x32, cal.T32)
     code, alpha16 = quantize(h, cal.bits, cal.s16)
     return pack_records(code, cal.bits), alpha16, code
 
 
 def decode_tokens(rec: np.ndarray, alpha16: np.ndarray, cal: Calibration) -> np.ndarray:
-    """Reconstructed tokens [n, d] in the original coordinates: x^ = T h^ (fp64)."""
+    """Reconstructed tokens [n, d] in the original coordinates: x^ = T h^ (fp64), with the
+    stored transform that encoded them."""
     h = dequantize(unpack_records(rec, cal.bits), alpha16, cal.bits, cal.s16)
-    return h @ cal.T64.T
+    return h @ np.asarray(cal.T32, dtype=np.float64).T
 
 
 # --------------------------------------------------------------------------------------

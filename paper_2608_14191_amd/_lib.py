@@ -222,7 +222,7 @@ def aatc_append_decode_attention(dev_params_k, dev_params_v, batch: int, n_q_hea
     """Appends token seq_len[b] - 1 (x_k[b], x_v[b]: [n_kv_heads][128]) to the caches and
     runs the decode step over the updated caches, in one launch."""
     if _dtype_code(x_k) != _dtype_code(x_v):
-        raise AatcError("x_k and x_v must have the same dtype")
+        raise AatcError("aatc_append_decode_attention (x_k and x_v dtypes differ)", E_INVALID)
     st = _L.aatc_append_decode_attention(
         _dptr(dev_params_k), _dptr(dev_params_v), int(batch), int(n_q_heads), int(n_kv_heads),
         HEAD_DIM, _dptr(q), _dtype_code(q), _dptr(x_k), _dptr(x_v), _dtype_code(x_k),

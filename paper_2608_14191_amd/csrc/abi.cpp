@@ -35,8 +35,15 @@ bool calibration_ok(const aatc_calibration& c) {
     sum += c.bits[i];
     if (c.bits[i]) ++active;
   }
-  return sum == c.budget_bits && active == c.d_active && sum > 0 &&
-         c.record_bytes == 4 * ((sum + 31) / 32);
+  if (!(sum == c.budget_bits && active == c.d_active && sum > 0 &&
+        c.record_bytes == 4 * ((sum + 31) / 32)))
+    return false;
+  // The stored transform: every entry a multiple of 2^-22 with magnitude at most 1.
+  for (int i = 0; i < kD * kD; ++i) {
+    const double q = std::ldexp((double)c.transform[i], kTFrac);
+    if (!(std::fabs(q) <= (double)(1 << kTFrac)) || q != std::nearbyint(q)) return false;
+  }
+  return true;
 }
 
 }  // namespace
@@ -87,10 +94,11 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
               hp->Tm[(((w * 4 + kk) * 2 + 0) * 64 + l) * 8 + e] = hi;
               hp->Tm[(((w * 4 + kk) * 2 + 1) * 64 + l) * 8 + e] = lo;
             }
-      for (int i = 0; i < kD * kD; ++i)
-        hp->Tq[i] = (int16_t)std::nearbyint(std::ldexp((double)c.transform[i], kTFrac));
       for (int j = 0; j < kD; ++j)
-        for (int ch = 0; ch < kD; ++ch) hp->Tqt[ch * kD + j] = hp->Tq[j * kD + ch];
+        for (int ch = 0; ch < kD; ++ch)
+          hp->Tqt[ch * kD + j] =
+              (int32_t)std::ldexp((double)c.transform[j * kD + ch], kTFrac);   // exact
+      float inv_s_max = 0.f;
       int off = 0;
       for (int ch = 0; ch < kD; ++ch) {
         const int b = c.bits[ch];
@@ -102,6 +110,7 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
         // fp32 1/s correctly rounded: the fp64 quotient of an 11-bit divisor rounds
         // to fp32 without a double-rounding error.
         hp->inv_s[ch] = (b && s > 0.0) ? (float)(1.0 / s) : 0.0f;
+        inv_s_max = std::fmax(inv_s_max, hp->inv_s[ch]);
         for (int k = 0; k < b; ++k) {
           const int v = off + k;
           hp->virt_chan[v] = (uint8_t)ch;
@@ -114,6 +123,7 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
       hp->d_active = c.d_active;
       hp->budget = c.budget_bits;
       hp->record_bytes = c.record_bytes;
+      hp->inv_s_max = inv_s_max;
     }
     return AATC_OK;
   } catch (...) {

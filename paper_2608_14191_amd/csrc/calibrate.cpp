@@ -262,7 +262,11 @@ extern "C" aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int
       out->sigma2[c] = lam[c];
       out->weight[c] = w[c];
       out->bits_eig[c] = (uint8_t)b_eig[c];
-      for (int j = 0; j < d; ++j) out->transform[(size_t)j * d + c] = (float)p[(size_t)j * d + e];
+      // The stored transform: each entry rounded to the nearest multiple of 2^-22 (ties
+      // to even), exactly representable in fp32.
+      for (int j = 0; j < d; ++j)
+        out->transform[(size_t)j * d + c] =
+            (float)std::ldexp(std::nearbyint(std::ldexp(p[(size_t)j * d + e], aatc::kTFrac)), -aatc::kTFrac);
     }
     out->d_active = d_active;
 

@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 
 #include "encode_core.h"
 #include "launch.h"
@@ -63,7 +64,7 @@ struct DecodeArgs {
   float* out;
   unsigned* counters;
   Partial* partials;
-  float* append_r;                // fused append: [rows][2][d] transformed coefficients
+  float* append_r;                // fused append: [rows][kAppStride] coefficients, bounds
   int64_t cap;
   int n_q_heads, n_kv_heads, G, q_dtype;
   int n_splits, n_blocks;         // splits per (sequence, KV head); rows x splits
@@ -339,6 +340,10 @@ __device__ inline v4i mfma_i8(v4i a, v4i b, v4i c) {
 // serialize, and every split of every (sequence, KV head) arrives at nearly once.
 constexpr int kCtrStride = 64;
 
+// Fused append, per (sequence, KV head): r_c of the key then the value token (2 x 128),
+// then each token's fixed-point error bound eh (0 when exact), padded to 16 bytes.
+constexpr int kAppStride = 2 * kD + 4;
+
 struct WsLayout {
   size_t counters, partials, append_r, total;
 };
@@ -352,7 +357,7 @@ inline WsLayout ws_layout(int batch, int n_q_heads, int n_kv_heads, int64_t cap)
   w.counters = 0;
   w.partials = round256(rows * kCtrStride * sizeof(unsigned));
   w.append_r = round256(w.partials + (size_t)batch * n_q_heads * n_splits * sizeof(Partial));
-  w.total = w.append_r + rows * 2 * kD * sizeof(float);   // fused append: r_c per row
+  w.total = w.append_r + rows * kAppStride * sizeof(float);   // fused append, per row
   return w;
 }
 
@@ -801,30 +806,17 @@ struct AppendScratch {                 // LDS region of its own
   uint32_t ea16[2];                    // fp16 scales
 };
 
-// r = h / s of one transformed coefficient, from this lane's two elements of the token
-// (raw dwords: bf16 halves or fp32) and of the column of Tq (int16 halves): the integer
-// dot product is exact (each lane's two products stay below 2^29, and the wave sums
-// split them into 16-bit halves), then rounded once.
-__device__ inline float append_coefficient(uint32_t x0, uint32_t x1, uint32_t t0, uint32_t t1,
-                                           int x_dtype, float inv_s) {
-  const int lane = threadIdx.x & 63;
-  const bool bf = x_dtype == AATC_BF16;
-  const float xa = bf ? __uint_as_float(((lane & 1) ? (x0 >> 16) : (x0 & 0xffffu)) << 16)
-                      : __uint_as_float(x0);
-  const float xb = bf ? __uint_as_float(((lane & 1) ? (x1 >> 16) : (x1 & 0xffffu)) << 16)
-                      : __uint_as_float(x1);
-  const int shift = token_shift(wave_max_dpp(fmaxf(fabsf(xa), fabsf(xb))));
-  const int ta = (int)(int16_t)((lane & 1) ? (t0 >> 16) : (t0 & 0xffffu));
-  const int tb = (int)(int16_t)((lane & 1) ? (t1 >> 16) : (t1 & 0xffffu));
-  const int p = (int)rintf(ldexpf(xa, shift)) * ta + (int)rintf(ldexpf(xb, shift)) * tb;
-  const long long hi = wave_sum_i32(p >> 16), lo = wave_sum_i32(p & 0xffff);
-  return fixed_point_result(hi * 65536 + lo, shift) * inv_s;
-}
-
-// F coefficients at once (the same arithmetic, reductions interleaved).
+// r = h~ / s of F transformed coefficients of the appended token (the encode kernels'
+// arithmetic, reductions interleaved), from this lane's two elements of the token (raw
+// dwords: bf16 halves or fp32) and of the coefficient's column of the integer transform:
+// X_j = rint(x_j 2^S) with max |X| in [2^21, 2^22), H = sum_j X_j Tq_jc exact (each lane's
+// two products below 2^45, the wave sums taken as 24-bit halves in int32), h~ =
+// fl32(H 2^-(S+22)).  eh = E 2^-S (1 + 2^-16), E = sum_j |x_j 2^S - X_j|, bounds |h - h~|
+// for the exact h (eh = 0: h~ is exact).
 template <int F>
-__device__ inline void append_coefficients(const uint32_t (&x)[F][2], const uint32_t (&t)[F][2],
-                                           int x_dtype, const float (&inv_s)[F], float (&out)[F]) {
+__device__ inline void append_coefficients(const uint32_t (&x)[F][2], const int (&t)[F][2],
+                                           int x_dtype, const float (&inv_s)[F], float (&out)[F],
+                                           float (&eh)[F]) {
   const int lane = threadIdx.x & 63;
   const bool bf = x_dtype == AATC_BF16;
   float xa[F], xb[F], m[F];
@@ -838,19 +830,25 @@ __device__ inline void append_coefficients(const uint32_t (&x)[F][2], const uint
   }
   wave_max_n(m);
   int shift[F], hl[2 * F];
+  float E[F];
 #pragma unroll
   for (int f = 0; f < F; ++f) {
     shift[f] = token_shift(m[f]);
-    const int ta = (int)(int16_t)((lane & 1) ? (t[f][0] >> 16) : (t[f][0] & 0xffffu));
-    const int tb = (int)(int16_t)((lane & 1) ? (t[f][1] >> 16) : (t[f][1] & 0xffffu));
-    const int p = (int)rintf(ldexpf(xa[f], shift[f])) * ta + (int)rintf(ldexpf(xb[f], shift[f])) * tb;
-    hl[2 * f] = p >> 16;
-    hl[2 * f + 1] = p & 0xffff;
+    const float va = ldexpf(xa[f], shift[f]), vb = ldexpf(xb[f], shift[f]);
+    const float ra = rintf(va), rb = rintf(vb);
+    E[f] = fabsf(va - ra) + fabsf(vb - rb);
+    const long long p = (long long)(int)ra * t[f][0] + (long long)(int)rb * t[f][1];
+    hl[2 * f] = (int)(p >> 24);
+    hl[2 * f + 1] = (int)(p & 0xffffff);
   }
   wave_sum_i32_n(hl);
+  wave_sum_n(E);
 #pragma unroll
-  for (int f = 0; f < F; ++f)
-    out[f] = fixed_point_result((long long)hl[2 * f] * 65536 + hl[2 * f + 1], shift[f]) * inv_s[f];
+  for (int f = 0; f < F; ++f) {
+    const double H = fma((double)hl[2 * f], 16777216.0, (double)hl[2 * f + 1]);
+    out[f] = integer_result(H, shift[f]) * inv_s[f];
+    eh[f] = ldexpf(E[f] * (1.f + 0x1p-16f), -shift[f]);
+  }
 }
 
 template <int NTHR, int NH>
@@ -860,7 +858,10 @@ struct AppendHook {
   uint16_t* k_alpha;
   uint8_t* v_codes;
   uint16_t* v_alpha;
-  const float* coeff;                  // this row's 2 x 128 coefficients (workspace)
+  const float* coeff;                  // this row's coefficients and bounds (workspace)
+  const HeadParams* ehp[2];            // key and value parameters of this KV head
+  const void* xrow[2];                 // the new key and value token of this row
+  int x_dtype;
   int64_t row, cap;
   int len, G, rk, rv;
   bool on;                             // the sequence has a token to append
@@ -870,15 +871,18 @@ struct AppendHook {
   float qk[2][NH];                     // Q_c of every head for them (key token)
   AppendScratch* sc;
   float r2[2];                         // their coefficients r_c = h_c / s_c
+  float eh;                            // the wave's token: fixed-point error bound
 
   __device__ void prefetch() {
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const __amdgpu_buffer_rsrc_t rs =
-        make_rsrc(coeff, (on && wave < 2) ? (uint32_t)(2 * kD * 4) : 0u);
+        make_rsrc(coeff, (on && wave < 2) ? (uint32_t)(kAppStride * 4) : 0u);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
       r2[i] = __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(
           rs, 4 * ((wave & 1) * kD + lane + 64 * i), 0, kCoherent));
+    eh = __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, 4 * (2 * kD + (wave & 1)), 0,
+                                                             kCoherent));
   }
 
   // The token's codes, scales, score per head and transformed value, each tensor by one
@@ -896,6 +900,17 @@ struct AppendHook {
     if (wave < 2) {
       const int et = wave;
       if (lane < kMaxBudget / 32) sc->erec[et][lane] = 0u;
+      // A token that is not exact in fixed point keeps its coefficients if the certificate
+      // holds; otherwise (rarely) the exact routine recomputes them.
+      const float ehw = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(eh)));
+      const HeadParams* ep = et ? ehp[1] : ehp[0];
+      if (ehw > 0.f && !wave_certify(ep, r2, ehw)) {
+        const void* xr = et ? xrow[1] : xrow[0];
+        float xl[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) xl[i] = load_elem(xr, x_dtype, lane + 64 * i);
+        exact_r_wave(ep, xl, xr, x_dtype, r2);
+      }
       float m = 0.f;
 #pragma unroll
       for (int i = 0; i < 2; ++i) m = fmaxf(m, e_b[i] > 0 ? fabsf(r2[i]) : 0.f);
@@ -1194,7 +1209,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ unsigned qmx[NH];
   __shared__ int fexp_s[NH];
-  __shared__ float wmax[NW][NH], wsum[NW][NH], wav[NW];
+  __shared__ float wmax[NW][NH], wsum[NW][NH], wpa[NW][NH];
+  __shared__ int fv_s[NH];
   __shared__ unsigned csync;          // arrivals of the plane-building waves
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1268,7 +1284,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
   const int x_eb = a.x_dtype == AATC_BF16 ? 2 : 4;
   constexpr int KF = 2;                               // coefficients fetched up front
   int adk[KF];
-  uint32_t ax[KF][2], atq[KF][2];
+  uint32_t ax[KF][2];
+  int atq[KF][2];
   float a_inv_s[KF];
   auto front_loads = [&]() {
     load_tables();
@@ -1309,11 +1326,11 @@ void decode_mfma_kernel(const DecodeArgs a) {
         const __amdgpu_buffer_rsrc_t xrs =
             make_rsrc(static_cast<const uint8_t*>(d >= kD ? a.x_v : a.x_k) + row * kD * x_eb,
                       on ? (uint32_t)(kD * x_eb) : 0u);
-        const __amdgpu_buffer_rsrc_t trs = make_rsrc(eh->Tqt + ac * kD, on ? 2u * kD : 0u);
+        const __amdgpu_buffer_rsrc_t trs = make_rsrc(eh->Tqt + ac * kD, on ? 4u * kD : 0u);
         ax[f][0] = __builtin_amdgcn_raw_buffer_load_b32(xrs, (lane * x_eb) & ~3, 0, 0);
         ax[f][1] = __builtin_amdgcn_raw_buffer_load_b32(xrs, ((lane + 64) * x_eb) & ~3, 0, 0);
-        atq[f][0] = __builtin_amdgcn_raw_buffer_load_b32(trs, (2 * lane) & ~3, 0, 0);
-        atq[f][1] = __builtin_amdgcn_raw_buffer_load_b32(trs, (2 * (lane + 64)) & ~3, 0, 0);
+        atq[f][0] = (int)__builtin_amdgcn_raw_buffer_load_b32(trs, 4 * lane, 0, 0);
+        atq[f][1] = (int)__builtin_amdgcn_raw_buffer_load_b32(trs, 4 * (lane + 64), 0, 0);
         a_inv_s[f] = eh->inv_s[ac];
       }
     }
@@ -1399,6 +1416,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
   float* qcl = scr;                                  // [NH][kD]
   uint8_t* ql = smem + a.off_ql;                     // [4][NH][2 NP][64]
   float rcf[KF] = {0.f, 0.f};                        // fused append: this wave's coefficients
+  float reh[KF] = {0.f, 0.f};                        // and the token's error bounds
   auto build_planes = [&]() {
 #pragma unroll
     for (int r = 0; r < NRC; ++r) {
@@ -1532,7 +1550,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
     // Fused append: this wave's coefficients (stored after the value phase, when no
     // cache transfer is queued ahead of the stores).
     if constexpr (APPEND)
-      append_coefficients<KF>(ax, atq, a.x_dtype, a_inv_s, rcf);  // (past 2 kD: unused)
+      append_coefficients<KF>(ax, atq, a.x_dtype, a_inv_s, rcf, reh);  // (past 2 kD: unused)
   };
 
   // (3) Front.  Eight waves: the plane-building and the issuing waves take separate arms
@@ -1627,7 +1645,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
   const int wb = wave * TW;
   float zr[NTILE][NT];
   float avt[NTILE];
-  float amax = 0.f;
+  float lav[NTILE];                      // log2 alpha^V (-inf for 0 and past the tokens)
   // Every tile's record dwords and token scales first (one LDS round trip), then the
   // products; lane group g holds record dwords g NP .. g NP + NP - 1, and dwords past the
   // record (they belong to the next token) meet zero query weights.
@@ -1682,7 +1700,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
       const float ak = half_bits_to_float(aka[tt]);
       const float av = half_bits_to_float(ava[tt]);
       avt[tt] = tok_ok ? av : 0.f;
-      amax = fmaxf(amax, fabsf(avt[tt]));
+      lav[tt] = avt[tt] > 0.f ? __builtin_amdgcn_logf(avt[tt]) : -INFINITY;
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) {
         const v4i d = acc[u][rt];                 // limbs 0..3 (weights 256^i)
@@ -1695,38 +1713,50 @@ void decode_mfma_kernel(const DecodeArgs a) {
   }
 
   // (5) Softmax: one maximum per head over the workgroup, and one fixed-point exponent
-  //     for P from the largest alpha^V.
+  //     per head for P alpha^V from its largest value, max_i 2^(z_i - m) alpha^V_i =
+  //     2^(max_i (z_i + log2 alpha^V_i) - m) (both maxima in one reduction).
 #pragma unroll
   for (int rt = 0; rt < NT; ++rt) {
-    float m = -INFINITY;
+    float m = -INFINITY, m2 = -INFINITY;
 #pragma unroll
-    for (int tt = 0; tt < NTILE; ++tt) m = fmaxf(m, zr[tt][rt]);
+    for (int tt = 0; tt < NTILE; ++tt) {
+      m = fmaxf(m, zr[tt][rt]);
+      m2 = fmaxf(m2, zr[tt][rt] + lav[tt]);
+    }
     m = row16_max(m);
-    if (n == 0) wmax[wave][4 * rt + g] = m;
+    m2 = row16_max(m2);
+    if (n == 0) {
+      wmax[wave][4 * rt + g] = m;
+      wpa[wave][4 * rt + g] = m2;
+    }
   }
-  amax = wave_max_dpp(amax);
-  if (lane == 0) wav[wave] = amax;
   __syncthreads();
   float mh[NT];
+  int fvh[NT];
 #pragma unroll
   for (int rt = 0; rt < NT; ++rt) {
     mh[rt] = wmax[0][4 * rt + g];
+    float m2 = wpa[0][4 * rt + g];
 #pragma unroll
-    for (int w = 1; w < NW; ++w) mh[rt] = fmaxf(mh[rt], wmax[w][4 * rt + g]);
-  }
-  int fv = 0;
-  {
-    float am = wav[0];
-#pragma unroll
-    for (int w = 1; w < NW; ++w) am = fmaxf(am, wav[w]);
+    for (int w = 1; w < NW; ++w) {
+      mh[rt] = fmaxf(mh[rt], wmax[w][4 * rt + g]);
+      m2 = fmaxf(m2, wpa[w][4 * rt + g]);
+    }
+    // P alpha^V <= 2^(m2 - m) < 2^e; one bit of margin for the hardware exp2 and log2,
+    // so P alpha^V 2^fv < 2^30.
     int e = 0;
-    frexpf(am, &e);
-    fv = am > 0.f ? 30 - e : 0;           // P <= max alpha^V < 2^e, so P 2^fv < 2^30
+    frexpf(__builtin_amdgcn_exp2f(m2 - mh[rt]), &e);
+    fvh[rt] = m2 > -INFINITY ? 29 - e : 0;
+    if (n == 0 && wave == 0) fv_s[4 * rt + g] = fvh[rt];
   }
   // Token 16 q + 4 e + L of a chunk sits at bit d = 2 e + q % 2 of its value byte; this
   // lane's tokens have e = hc.
-  const float sc_even = ldexpf(1.f, fv - 2 * hc);
-  const float sc_odd = (hc == 3 ? -1.f : 1.f) * ldexpf(1.f, fv - 2 * hc - 1);
+  float sc_even[NT], sc_odd[NT];
+#pragma unroll
+  for (int rt = 0; rt < NT; ++rt) {
+    sc_even[rt] = ldexpf(1.f, fvh[rt] - 2 * hc);
+    sc_odd[rt] = (hc == 3 ? -1.f : 1.f) * ldexpf(1.f, fvh[rt] - 2 * hc - 1);
+  }
   const uint32_t sel_a = (L & 2) ? 0x03020706u : 0x05040100u;
   const uint32_t sel_b = (L & 1) ? 0x03070105u : 0x06020400u;
   v4i* pb = reinterpret_cast<v4i*>(smem + a.off_pb);  // [NCH][NT][64] value operands
@@ -1743,7 +1773,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
         // (the hardware exp2: results below 2^-126 flush to 0, below any weight that counts)
         const float p = (z == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(z - mh[rt]);
         lsum += p;
-        const int fx = (int)rintf(p * avt[tt] * ((qd & 1) ? sc_odd : sc_even));
+        const int fx = (int)rintf(p * avt[tt] * ((qd & 1) ? sc_odd[rt] : sc_even[rt]));
         uint32_t x = pack_limbs(fx);
         // quad byte transpose: (token L, limbs 0..3) -> (limb L, tokens 0..3)
         x = __builtin_amdgcn_perm(quad_xor2(x), x, sel_a);
@@ -1882,20 +1912,27 @@ void decode_mfma_kernel(const DecodeArgs a) {
     // Fused append: the coefficients into the workspace (device-coherent, before this
     // workgroup's arrival), and further ones when the row has fewer than 32 splits.
     if (cw) {
-      const __amdgpu_buffer_rsrc_t rrs = make_rsrc(a.append_r + row * 2 * kD, 2 * kD * 4);
+      // Coefficient d at d; the wave with the token's first channel (d = 0 keys, 128
+      // values) also stores the token's error bound at 2 kD + d / kD.
+      const __amdgpu_buffer_rsrc_t rrs = make_rsrc(a.append_r + row * kAppStride, kAppStride * 4);
 #pragma unroll
-      for (int f = 0; f < KF; ++f)
+      for (int f = 0; f < KF; ++f) {
         if (adk[f] < 2 * kD && lane == 0) buf_store4_coherent(rcf[f], rrs, (uint32_t)(4 * adk[f]));
+        if (adk[f] < 2 * kD && (adk[f] & (kD - 1)) == 0 && lane == 0)
+          buf_store4_coherent(reh[f], rrs, (uint32_t)(4 * (2 * kD + adk[f] / kD)));
+      }
       for (int d = split + a.n_splits * (wave + NWC * KF); d < 2 * kD; d += a.n_splits * NWC) {
         const HeadParams* eh = d >= kD ? hv : hk;
         const int c = d & (kD - 1);
         const uint8_t* xb = static_cast<const uint8_t*>(d >= kD ? a.x_v : a.x_k) + row * kD * x_eb;
-        const uint32_t x0 = *reinterpret_cast<const uint32_t*>(xb + ((lane * x_eb) & ~3));
-        const uint32_t x1 = *reinterpret_cast<const uint32_t*>(xb + (((lane + 64) * x_eb) & ~3));
-        const uint32_t* tc = reinterpret_cast<const uint32_t*>(eh->Tqt + c * kD);
-        const float rc = append_coefficient(x0, x1, tc[lane >> 1], tc[(lane + 64) >> 1],
-                                            a.x_dtype, eh->inv_s[c]);
-        if (lane == 0) buf_store4_coherent(rc, rrs, (uint32_t)(4 * d));
+        const uint32_t xw[1][2] = {{*reinterpret_cast<const uint32_t*>(xb + ((lane * x_eb) & ~3)),
+                                    *reinterpret_cast<const uint32_t*>(xb + (((lane + 64) * x_eb) & ~3))}};
+        const int tw[1][2] = {{eh->Tqt[c * kD + lane], eh->Tqt[c * kD + lane + 64]}};
+        const float isv[1] = {eh->inv_s[c]};
+        float rc[1], ec[1];
+        append_coefficients<1>(xw, tw, a.x_dtype, isv, rc, ec);
+        if (lane == 0) buf_store4_coherent(rc[0], rrs, (uint32_t)(4 * d));
+        if (c == 0 && lane == 0) buf_store4_coherent(ec[0], rrs, (uint32_t)(4 * (2 * kD + d / kD)));
       }
     }
   }
@@ -1913,7 +1950,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
         const float t = ldexpf(kHalves ? oh[v] + oh[NH * a.ob_stride + v] : oh[v], k);
         acc += (k < vbc) ? ((k == vbc - 1) ? -t : t) : 0.f;
       }
-      const float o = vbc ? ldexpf(vsc * acc, 1 - vbc - fv) : 0.f;
+      const float o = vbc ? ldexpf(vsc * acc, 1 - vbc - fv_s[h]) : 0.f;
       buf_store4_coherent(o, prs, (uint32_t)((split * G + h) * sizeof(Partial) + 16 + 4 * cq));
     }
   }
@@ -1931,7 +1968,12 @@ void decode_mfma_kernel(const DecodeArgs a) {
   float* merge_scratch = reinterpret_cast<float*>(smem);
   if constexpr (APPEND) {
     AppendHook<NTHR, NH> hook;
-    hook.coeff = a.append_r + row * 2 * kD;
+    hook.coeff = a.append_r + row * kAppStride;
+    hook.ehp[0] = hk;
+    hook.ehp[1] = hv;
+    hook.xrow[0] = static_cast<const uint8_t*>(a.x_k) + row * kD * x_eb;
+    hook.xrow[1] = static_cast<const uint8_t*>(a.x_v) + row * kD * x_eb;
+    hook.x_dtype = a.x_dtype;
     hook.k_codes = a.k_codes;
     hook.k_alpha = a.k_alpha;
     hook.v_codes = a.v_codes;
@@ -1966,6 +2008,32 @@ void decode_mfma_kernel(const DecodeArgs a) {
 size_t decode_workspace_bytes(int batch, int n_q_heads, int n_kv_heads, int64_t cap) {
   return ws_layout(batch, n_q_heads, n_kv_heads, cap).total;
 }
+
+// The dynamic LDS limit of one kernel, raised on each device the first time a launch there
+// needs more.  Safe for concurrent callers: a race can only repeat the (idempotent)
+// attribute call, and the recorded limit only grows.
+class LdsLimit {
+ public:
+  bool ensure(const void* kernel, size_t lds) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return false;
+    if (dev < 0 || dev >= kDevices)      // beyond the table: set it every time
+      return hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)lds) == hipSuccess;
+    size_t cur = set_[dev].load(std::memory_order_acquire);
+    if (lds <= cur) return true;
+    if (hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+        hipSuccess)
+      return false;
+    while (cur < lds && !set_[dev].compare_exchange_weak(cur, lds, std::memory_order_acq_rel)) {
+    }
+    return true;
+  }
+
+ private:
+  static constexpr int kDevices = 64;
+  std::atomic<size_t> set_[kDevices] = {};
+};
 
 template <int NT, int NTILE, int NP, int NW, bool APPEND>
 static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
@@ -2012,13 +2080,9 @@ static aatc_status launch_mfma(DecodeArgs a, int batch, hipStream_t st) {
   off += es_bytes;
   const size_t lds = off;
   if (lds > kLdsMax) return AATC_E_UNSUPPORTED;
-  static size_t set_lds = 0;
-  if (lds > set_lds) {
-    if (hipFuncSetAttribute((const void*)decode_mfma_kernel<NT, NTILE, NP, NW, APPEND>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-      return AATC_E_DEVICE;
-    set_lds = lds;
-  }
+  static LdsLimit limit;
+  if (!limit.ensure((const void*)decode_mfma_kernel<NT, NTILE, NP, NW, APPEND>, lds))
+    return AATC_E_DEVICE;
   const unsigned grid = (unsigned)a.n_blocks;
   hipLaunchKernelGGL((decode_mfma_kernel<NT, NTILE, NP, NW, APPEND>), dim3(grid), dim3(NTHR), lds,
                      st, a);
@@ -2107,13 +2171,8 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
   const int n_splits = (int)((cap + kSplit - 1) / kSplit);
   size_t lds = std::max((size_t)G * (kSplit + kMaxBudget) * sizeof(float), merge_lds_bytes(G, kThreads));
   if (lds > 160 * 1024 - 24 * 1024) return AATC_E_UNSUPPORTED;
-  static size_t set_lds0 = 0;
-  if (lds > set_lds0) {
-    if (hipFuncSetAttribute((const void*)decode_split_kernel,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-      return AATC_E_DEVICE;
-    set_lds0 = lds;
-  }
+  static LdsLimit limit;
+  if (!limit.ensure((const void*)decode_split_kernel, lds)) return AATC_E_DEVICE;
   dim3 grid((unsigned)n_splits, (unsigned)n_kv_heads, (unsigned)batch);
   hipLaunchKernelGGL(decode_split_kernel, grid, dim3(kThreads), lds, st, params_k, params_v,
                      n_q_heads, n_kv_heads, q, (int)q_dtype,

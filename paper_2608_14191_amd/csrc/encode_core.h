@@ -1,12 +1,13 @@
 // Per-token encode arithmetic shared by the encode kernels and the decode kernel's fused
-// append (Sec. 5.2 quantizer, fixed-point transform of the canonical encode).  Device
-// code only.
+// append (Sec. 5.2 quantizer; the transform of Alg. 1 "project", h = T^T x, rounded once
+// to fp32 from its exact value).  Device code only.
 #pragma once
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
 #include "aatc.h"
+#include "exact_dot.h"
 #include "params.h"
 
 namespace aatc {
@@ -19,16 +20,20 @@ __device__ inline float load_elem(const void* x, int dtype, int64_t idx) {
   return static_cast<const float*>(x)[idx];
 }
 
-// Fixed-point shift of a token: max |x_j| 2^shift lies in [2^13, 2^14) (0 for a zero token).
+// Fixed-point shift of a token for the integer transform: max |x_j| 2^shift lies in
+// [2^21, 2^22), so X_j = rint(x_j 2^shift) splits into three balanced int8 limbs (0 for a
+// zero token).  X_j equals x_j 2^shift exactly unless |x_j| is below about 2^-14 max |x|
+// (bf16) or carries more bits (fp32).
 __device__ inline int token_shift(float max_abs) {
   int e = 0;
   frexpf(max_abs, &e);                             // max_abs = f 2^e, f in [0.5, 1)
   return (max_abs > 0.f) ? (kXLead - (e - 1)) : 0;
 }
 
-// h_c from the exact integer sum of X_j Tq_jc: one rounding to fp32.
-__device__ inline float fixed_point_result(long long acc, int shift) {
-  return (float)ldexp((double)acc, -(shift + kTFrac));
+// h = fl32(H 2^-(shift + 22)) for the exact integer H = sum_j X_j Tq_j (|H| < 2^51, exact
+// in fp64): when every X_j is exact this is the canonical h.
+__device__ inline float integer_result(double H, int shift) {
+  return (float)ldexp(H, -(shift + kTFrac));
 }
 
 // Token scale alpha = fp16(max |r_c| over stored channels) and fp32 1/alpha, correctly
@@ -57,5 +62,129 @@ __device__ inline uint32_t quantize_code(float r, float inv_a, int b) {
 // record bit v of token p at bit tile_bit(p).
 __device__ inline int tile_word(int p) { return (p >> 4) >> 1; }
 __device__ inline int tile_bit(int p) { return 8 * (p & 3) + 2 * ((p >> 2) & 3) + ((p >> 4) & 1); }
+
+__device__ inline float wave_max64(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// The exact fallback for one channel: h_c from the token in memory and column c of the
+// integer transform.
+__device__ inline float exact_h_channel(const void* xrow, int dtype, const int32_t* tcol) {
+  return exact_dot_q22([&](int j) { return load_elem(xrow, dtype, j); },
+                       [&](int j) { return tcol[j]; }, kD);
+}
+
+// r_c = fl32(h_c (1/s_c)) with h_c = fl32(sum_j x_j T_jc) exact, for channels c = lane and
+// lane + 64 of one token, computed by one wave.  xl holds this lane's elements lane and
+// lane + 64 (as fp32); xrow / dtype address the token in memory for the exact fallback.
+// The fp64 sums of x_j Tq_jc (every product exact: at most 24 + 23 bits) are within
+// 128 2^-53 (1 + tiny) sum_j |x_j Tq_jc| of the exact sum; where that interval, scaled by
+// 2^-22, rounds to one fp32 number it is h_c, elsewhere the exact accumulator of
+// exact_dot.h decides.
+__device__ inline void exact_r_wave(const HeadParams* hp, const float (&xl)[2],
+                                    const void* xrow, int dtype, float (&r)[2]) {
+  const int lane = threadIdx.x & 63;
+  double s[2] = {0.0, 0.0}, a[2] = {0.0, 0.0};
+  const int4* tc[2] = {reinterpret_cast<const int4*>(hp->Tqt + lane * kD),
+                       reinterpret_cast<const int4*>(hp->Tqt + (lane + 64) * kD)};
+#pragma unroll 1
+  for (int jb = 0; jb < kD; jb += 16) {
+    int4 tv[2][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) tv[i][q] = tc[i][jb / 4 + q];
+    const float xw = (jb < 64) ? xl[0] : xl[1];
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj) {
+      const double xd =
+          (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(xw), (jb + jj) & 63));
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int4 t4 = tv[i][jj >> 2];
+        const int ti = (jj & 3) == 0 ? t4.x : (jj & 3) == 1 ? t4.y : (jj & 3) == 2 ? t4.z : t4.w;
+        const double t = (double)ti;
+        s[i] = fma(xd, t, s[i]);
+        a[i] = fma(fabs(xd), fabs(t), a[i]);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int c = lane + 64 * i;
+    const double sv = ldexp(s[i], -kTFrac), av = ldexp(a[i], -kTFrac);
+    const double b = av * (kD * 0x1p-52);
+    const double bb = b * (1.0 + 0x1p-48) + fabs(sv) * 0x1p-51 + 0x1p-1060;
+    const float lo = (float)(sv - bb), hi = (float)(sv + bb);
+    float h = lo;
+    if (lo != hi) h = exact_h_channel(xrow, dtype, hp->Tqt + c * kD);
+    r[i] = h * hp->inv_s[c];
+  }
+}
+
+// Certificate of a token encoded from the fixed-point transform (one wave, lane l:
+// channels l and l + 64): r holds fl32(fl32(h~) / s) with |h - h~| <= eh for the exact h.
+// True if the fp16 scale and every code are certainly those of the exact transform: the
+// fp16 rounding of the largest |r| cannot change within the bound, and no code's
+// quantizer input lies within the bound (in its units, plus the fp32 roundings of both
+// evaluations) of a rounding boundary.
+__device__ inline bool wave_certify(const HeadParams* hp, const float (&r)[2], float eh) {
+  const int lane = threadIdx.x & 63;
+  int b[2];
+  float m = 0.f;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    b[i] = hp->bits[lane + 64 * i];
+    m = fmaxf(m, b[i] > 0 ? fabsf(r[i]) : 0.f);
+  }
+  const float amax = wave_max64(m);
+  const __half a16 = token_alpha(amax);
+  const float inv = inverse_alpha(a16);
+  const float ma = eh * hp->inv_s_max * (1.f + 0x1p-20f) + 0x1p-21f * amax + 0x1p-140f;
+  bool ok = __half_as_ushort(token_alpha(fmaxf(amax - ma, 0.f))) ==
+            __half_as_ushort(token_alpha(amax + ma));
+  const float ea = eh * inv;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    if (b[i] > 0) {
+      const float xq = ldexpf(r[i] * inv, b[i] - 1);
+      const float f = floorf(xq);
+      const float code = f + ((xq - f) >= 0.5f ? 1.f : 0.f);
+      const float dev = fabsf(xq - code);
+      const float k = ldexpf(hp->inv_s[lane + 64 * i], b[i] - 1) * (1.f + 0x1p-20f);
+      const float mg = fmaf(k, ea, fmaf(0x1p-21f, fabsf(xq), 0x1p-22f));
+      ok = ok && (dev + mg < 0.5f);
+    }
+  }
+  return __builtin_amdgcn_ballot_w64(!ok) == 0ull;
+}
+
+// One token's codes from r (lane l: channels l and l + 64, one wave), OR-ed into its
+// record row `rec` (zero on entry; LDS); returns the fp16 token scale.
+__device__ inline __half wave_quantize_into(const HeadParams* hp, const float (&r)[2],
+                                            uint32_t* rec) {
+  const int lane = threadIdx.x & 63;
+  int b[2], off[2];
+  float m = 0.f;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    b[i] = hp->bits[lane + 64 * i];
+    off[i] = hp->bit_off[lane + 64 * i];
+    m = fmaxf(m, b[i] > 0 ? fabsf(r[i]) : 0.f);
+  }
+  const __half a16 = token_alpha(wave_max64(m));
+  const float inv = inverse_alpha(a16);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    if (b[i] > 0) {
+      const uint32_t u = quantize_code(r[i], inv, b[i]);
+      atomicOr(&rec[off[i] >> 5], u << (off[i] & 31));
+      if ((off[i] & 31) + b[i] > 32) atomicOr(&rec[(off[i] >> 5) + 1], u >> (32 - (off[i] & 31)));
+    }
+  }
+  return a16;
+}
 
 }  // namespace aatc

@@ -12,19 +12,18 @@ constexpr int kD = 128;                   // head dimension
 constexpr int kMaxBits = 8;               // widest channel code
 constexpr int kMaxBudget = kD * kMaxBits; // most bits per token record
 constexpr int kTile = 64;                 // tokens per value-cache tile
-constexpr int kTFrac = 14;                // fixed-point fraction bits of T
-constexpr int kXLead = 13;                // per-token x scaled into [2^13, 2^14)
+constexpr int kTFrac = 22;                // the stored transform: multiples of 2^-22
+constexpr int kXLead = 21;                // encoder: per-token x scaled into [2^21, 2^22)
 constexpr uint32_t kMagic = 0x43544141u;  // "AATC"
 
 struct alignas(256) HeadParams {
-  float T[kD * kD];               // [j][c] transform, storage channels (fp32)
+  float T[kD * kD];               // [j][c] stored transform (multiples of 2^-22, exact fp32)
   // The same transform as two bf16 terms, Th = bf16(T) and Tl = bf16(T - Th), laid out as
   // the decode merge's matrix-core A operands: 16-byte unit ((4 w + kk) 2 + t) 64 + l holds
   // term t (0: Th, 1: Tl) of T[16 w + l % 16][32 kk + 8 (l / 16) .. + 7], w < 8, kk < 4,
   // l < 64 (8 KiB per block of 16 rows).
   uint16_t Tm[2 * kD * kD];
-  int16_t Tq[kD * kD];            // [j][c] rint(T * 2^14), |Tq| <= 2^14
-  int16_t Tqt[kD * kD];           // [c][j] the same, transposed
+  int32_t Tqt[kD * kD];           // [c][j] T * 2^22 (integers, |Tq| <= 2^22), transposed
   float inv_s[kD];                // fp32 1/s_c (0 for dropped or zero-scale channels)
   float s[kD];                    // s_c as fp32 (exact value of the fp16 scale)
   uint16_t s16[kD];               // s_c fp16 bits
@@ -39,7 +38,7 @@ struct alignas(256) HeadParams {
   int32_t d_active;
   int32_t budget;
   int32_t record_bytes;
-  int32_t pad_;
+  float inv_s_max;                // largest 1/s_c over the stored channels
 };
 
 // The decode kernel reads these fields with 16-, 8- and 4-byte vector loads.

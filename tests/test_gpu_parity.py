@@ -1,7 +1,9 @@
 """GPU parity: the HIP path through the C ABI against the CPU oracle.
 
 Bar: bit-exact packed codes and fp16 token scales; decode attention within 2e-3
-relative L2 of the oracle's exact fp64 attention over the decoded cache.
+relative L2 of the oracle's exact fp64 attention over the decoded cache, for every query
+head separately, and within 2e-3 of that head's largest output magnitude element by
+element.
 """
 import numpy as np
 import pytest
@@ -20,6 +22,19 @@ TOL = 2e-3
 
 def _log(msg):
     print(msg, flush=True)
+
+
+def _assert_heads_close(got, ref, what=""):
+    """Per query head: relative L2 <= TOL and max |error| <= TOL * max |ref|."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    worst = 0.0
+    for j in range(ref.shape[0]):
+        err = rel_l2(got[j], ref[j])
+        worst = max(worst, err)
+        assert err <= TOL, f"{what} query head {j}: rel L2 {err:.3e}"
+        assert np.abs(got[j] - ref[j]).max() <= TOL * np.abs(ref[j]).max(), f"{what} head {j}"
+    return worst
 
 
 class Case:
@@ -143,9 +158,11 @@ def test_encode_bit_exact_and_decode_parity(name):
     out, _ = _decode(case, pk, pv, kc, ka, vc, va)
     ref = _oracle_decode(case)
     for b in range(case.w.batch):
-        err = rel_l2(out[b], ref[b])
-        _log(f"  seq {b} len {case.lens[b]} rel_l2 {err:.3e}")
-        assert err <= TOL
+        if case.lens[b] == 0:
+            assert np.all(out[b] == 0)
+            continue
+        err = _assert_heads_close(out[b], ref[b], f"seq {b}")
+        _log(f"  seq {b} len {case.lens[b]} worst head rel_l2 {err:.3e}")
 
 
 def test_encode_incremental_appends_match_bulk():
@@ -210,7 +227,7 @@ def test_decode_edge_lengths():
     ref = _oracle_decode(case)
     assert np.all(out[0] == 0)
     for b in range(1, len(lens)):
-        assert rel_l2(out[b], ref[b]) <= TOL, (b, lens[b])
+        _assert_heads_close(out[b], ref[b], f"seq {b} len {lens[b]}")
 
 
 def test_decode_repeatable_and_workspace_reusable():
@@ -232,7 +249,7 @@ def test_end_to_end_with_host_calibration():
     pk_, pv_, kc, ka, vc, va = _gpu_caches(case, pk, pv)
     out, _ = _decode(case, pk, pv, kc, ka, vc, va)
     ref = _oracle_decode(case)
-    assert rel_l2(out[0], ref[0]) <= TOL
+    _assert_heads_close(out[0], ref[0])
 
 
 APPEND_CASES = {
@@ -293,24 +310,28 @@ def test_append_decode_matches_encode_then_decode(name):
         if case.lens[b] == 0:
             assert np.all(got[b] == 0)
             continue
-        assert rel_l2(got[b], ref[b]) <= TOL, (b, case.lens[b], rel_l2(got[b], ref[b]))
+        _assert_heads_close(got[b], ref[b], f"seq {b} len {case.lens[b]}")
         assert rel_l2(got[b], sep[b]) <= 1e-5, (b, case.lens[b])
 
 
 FULL_SIZE = {
-    # the benchmark's workload and launch (append the last token, decode all 32768)
-    "cfg2_llama_32k": dict(cfg=2, sample=[(0, 0), (0, 5)]),
-    "cfg3_qwen_16k_b8": dict(cfg=3, sample=[(3, 1), (7, 3)]),
+    # the benchmark's workload and launch (append the last token, decode all 32768):
+    # every KV head
+    "cfg2_llama_32k": dict(cfg=2, sample=[(0, h) for h in range(8)]),
+    # every KV head of two of the eight sequences
+    "cfg3_qwen_16k_b8": dict(cfg=3, sample=[(b, h) for b in (3, 7) for h in range(4)]),
     # the largest decode workload: 4 x 131072 tokens, 2.0 bits, zero-bit key channels,
-    # 128 splits per (sequence, KV head) into one merge
-    "cfg5_long_131k_b4": dict(cfg=5, sample=[(0, 0), (3, 6)]),
+    # 128 splits per (sequence, KV head) into one merge; every KV head of two sequences
+    "cfg5_long_131k_b4": dict(cfg=5, sample=[(b, h) for b in (0, 3) for h in range(8)]),
 }
 # generating 4 x 8 x 131072 stored tokens per tensor takes about a minute on the host
 _FULL_SLOW = {"cfg5_long_131k_b4"}
 
 
-@pytest.mark.parametrize("name", [pytest.param(n, marks=pytest.mark.timeout(360))
-                                  if n in _FULL_SLOW else n for n in FULL_SIZE])
+@pytest.mark.parametrize("name", [pytest.param(n, marks=pytest.mark.timeout(600))
+                                  if n in _FULL_SLOW else
+                                  pytest.param(n, marks=pytest.mark.timeout(300))
+                                  for n in FULL_SIZE])
 def test_full_size_sampled(name):
     """Full-size workloads through aatc_append_decode_attention: the packed caches of
     sampled (sequence, KV head) pairs are bit-exact, including the appended token, and
@@ -359,16 +380,16 @@ def test_full_size_sampled(name):
         vh = ora.decode_tokens(ov_, ova, case.cal_v[h])
         q32 = w.as_f32(case.q[b])[h * g:(h + 1) * g]
         ref = ora.softmax_attention(q32, kh, vh, 1 / np.sqrt(128))
-        err = rel_l2(got[b, h * g:(h + 1) * g], ref)
-        _log(f"  seq {b} kv head {h}: rel_l2 {err:.3e}")
-        assert err <= TOL
+        err = _assert_heads_close(got[b, h * g:(h + 1) * g], ref, f"seq {b} kv head {h}")
+        _log(f"  seq {b} kv head {h}: worst query head rel_l2 {err:.3e}")
 
 
+@pytest.mark.timeout(300)
 @pytest.mark.parametrize("avg_bits", [2.75, 4.0])
 def test_full_size_prefill_encode_sampled(avg_bits):
     """The prefill workload at full size (65536 new tokens x 8 KV heads, one aatc_encode
-    per tensor, as the benchmark launches it): sampled heads' key records, value tiles
-    and scales are bit-exact against the oracle at both budgets."""
+    per tensor, as the benchmark launches it): every head's key records, value tiles and
+    scales are bit-exact against the oracle at both budgets."""
     full = workload(4)
     _log(f"[full] prefill encode: {full.n_tokens} tokens, {full.n_kv_heads} heads, "
          f"{avg_bits} bits")
@@ -383,7 +404,7 @@ def test_full_size_prefill_encode_sampled(avg_bits):
     P.aatc_encode(pk, H, xk, n, H * 128, P.LAYOUT_RECORDS, kc, ka, cap, 0)
     P.aatc_encode(pv, H, xv, n, H * 128, P.LAYOUT_TILES, vc, va, cap, 0)
     torch.cuda.synchronize()
-    for h in (1, 6):
+    for h in range(H):
         ok_, oa = case.oracle_encode(0, h, "k")
         ov_, ova = case.oracle_encode(0, h, "v")
         got = kc[h, :n].cpu().numpy()

@@ -1,4 +1,6 @@
 """Pins of the oracle's transform step (Sec. 3.1, Sec. 5.1, App. D)."""
+from fractions import Fraction
+
 import numpy as np
 import pytest
 
@@ -89,37 +91,114 @@ def test_key_and_value_weights_special_cases():
     np.testing.assert_allclose(aatc.value_weights(p, np.eye(d)), np.ones(d), atol=1e-12)
 
 
-def test_fixed_point_transform_identity_on_grid():
-    """T = I and inputs with <= 14 significant bits below the token maximum: exact."""
-    rng = np.random.default_rng(5)
-    d = 16
-    ints = rng.integers(-8191, 8192, size=(40, d))
-    ints[:, 0] = 8191
-    x = np.ldexp(ints.astype(np.float64), rng.integers(-20, 5, size=(40, 1))).astype(np.float32)
-    h = aatc.fixed_point_transform(x, np.eye(d, dtype=np.float32))
-    np.testing.assert_array_equal(h, x)
+def _rational_transform(x, t):
+    """Every element by exact rational arithmetic: the definition with no fast path."""
+    out = np.zeros((x.shape[0], t.shape[1]), dtype=np.float32)
+    for i in range(x.shape[0]):
+        for c in range(t.shape[1]):
+            acc = Fraction(0)
+            for j in range(x.shape[1]):
+                acc += Fraction(float(x[i, j])) * Fraction(float(t[j, c]))
+            out[i, c] = aatc.round_to_f32(acc)
+    return out
 
 
-def test_fixed_point_transform_error_bound():
-    """|h - T^T x| stays within the fixed-point resolution bound for real data."""
-    rng = np.random.default_rng(6)
-    x = (rng.standard_normal((500, 128)) * rng.lognormal(0, 2, size=(500, 1))).astype(np.float32)
-    t = haar_orthogonal(rng, 128).astype(np.float32)
-    h = aatc.fixed_point_transform(x, t).astype(np.float64)
-    exact = x.astype(np.float64) @ t.astype(np.float64)
-    xa = np.abs(x.astype(np.float64))
-    m = xa.max(axis=1)
-    e = np.frexp(m)[1] - 1
-    x_res = np.ldexp(0.5, -(aatc.X_LEAD_BIT - e))               # half an x step
-    bound = (xa.sum(axis=1) * 2.0 ** -(aatc.T_FRAC_BITS + 1)
-             + x_res * np.abs(t).sum(axis=0).max() * (1 + 2.0 ** -14))[:, None]
-    bound = bound + np.abs(exact) * 2.0 ** -24
-    assert np.all(np.abs(h - exact) <= bound)
-    assert np.all(np.abs(h - exact) <= 1e-3 * np.linalg.norm(x, axis=1, keepdims=True))
+def test_stored_transform_grid():
+    """Entries are the nearest multiples of 2^-22, exactly representable in fp32."""
+    rng = np.random.default_rng(7)
+    t64 = haar_orthogonal(rng, 128)
+    t = aatc.stored_transform(t64)
+    assert t.dtype == np.float32
+    q = np.ldexp(t.astype(np.float64), 22)
+    np.testing.assert_array_equal(q, np.rint(q))
+    assert np.abs(t.astype(np.float64) - t64).max() <= 2.0 ** -23
+    np.testing.assert_array_equal(aatc.stored_transform(np.eye(16)), np.eye(16))
 
 
-def test_fixed_point_transform_zero_token():
-    x = np.zeros((3, 8), dtype=np.float32)
-    x[1, 2] = 1.5
-    h = aatc.fixed_point_transform(x, np.eye(8, dtype=np.float32))
-    np.testing.assert_array_equal(h, x)
+def test_round_to_f32_matches_ieee_cast():
+    """round_to_f32 on rationals that are fp64 numbers equals the hardware fp64 -> fp32
+    conversion (round to nearest, ties to even), including ties, subnormals and overflow."""
+    rng = np.random.default_rng(8)
+    vals = [1 + 2.0 ** -24, 1 + 3 * 2.0 ** -24, -(1 + 2.0 ** -24), 2.0 ** -149,
+            2.0 ** -150, 3 * 2.0 ** -151, 2.0 ** -126 * (1 - 2.0 ** -25), 3.4028235677973366e38,
+            2.0 ** 128 * (1 - 2.0 ** -25), 2.0 ** 128 * (1 - 2.0 ** -26), 0.1, -7.25e-40]
+    vals += list(rng.standard_normal(2000) * np.exp2(rng.integers(-160, 130, 2000)))
+    for v in vals:
+        with np.errstate(over="ignore"):
+            want = np.float64(v).astype(np.float32)
+        got = aatc.round_to_f32(Fraction(v))
+        assert got == want or (np.isinf(got) and np.isinf(want) and got == want), v
+
+
+def test_int64_to_f32_cast_rounds_to_nearest_even():
+    """The oracle's transform relies on numpy's int64 -> float32 conversion rounding once,
+    to nearest with ties to even: checked against exact rational rounding on ties and on
+    integers with many trailing zeros."""
+    ties = [2 ** 24 + 1, 2 ** 24 + 3, -(2 ** 24 + 1), 2 ** 59 + 2 ** 35, 2 ** 59 + 2 ** 35 + 1,
+            -(2 ** 40 + 2 ** 16), -(2 ** 40 + 2 ** 16 + 1), 2 ** 60 - 1]
+    rng = np.random.default_rng(13)
+    v = rng.integers(-2 ** 62, 2 ** 62, size=4000)
+    v = (v >> rng.integers(0, 40, size=v.size)) << rng.integers(0, 20, size=v.size)
+    vals = np.concatenate([np.array(ties, dtype=np.int64), v])
+    got = vals.astype(np.float32)
+    for a, g in zip(vals, got):
+        assert aatc.round_to_f32(Fraction(int(a))) == g, int(a)
+
+
+def test_transform_matches_rational_definition():
+    """Random bf16-valued and fp32 tokens against exact rational sums, element by element."""
+    from kvsynth.gen import bf16_bits_to_f32, f32_to_bf16_bits
+    rng = np.random.default_rng(9)
+    t = aatc.stored_transform(haar_orthogonal(rng, 128))[:, :12]
+    xb = bf16_bits_to_f32(f32_to_bf16_bits(
+        (rng.standard_normal((6, 128)) * rng.lognormal(0, 3, (6, 1))).astype(np.float32)))
+    xf = (rng.standard_normal((6, 128)) * np.exp2(rng.integers(-30, 30, (6, 128)))).astype(np.float32)
+    for x in (xb, xf):
+        np.testing.assert_array_equal(aatc.transform(x, t), _rational_transform(x, t))
+
+
+def test_transform_near_ties():
+    """Sums within 2^-62 of an fp32 halfway point: summing in fp64 and then rounding to
+    fp32 rounds twice and lands on the tie; the exact sum does not."""
+    t = np.zeros((4, 1), dtype=np.float32)
+    t[:, 0] = [1.0, 2.0 ** -22, 2.0 ** -22, 2.0 ** -22]
+    cases = [
+        # (x, exact result)
+        ([1.0, 0.25, 2.0 ** -40, 0.0], 1 + 2.0 ** -23),      # just above the tie: up
+        ([1.0, 0.25, -2.0 ** -40, 0.0], 1.0),                # just below the tie: down
+        ([1.0, 0.25, 0.0, 0.0], 1.0),                        # the tie itself: to even
+        ([1.0, 0.75, 0.0, 0.0], 1 + 2.0 ** -22),             # odd neighbour below: up
+        ([-1.0, -0.25, -2.0 ** -40, 0.0], -(1 + 2.0 ** -23)),
+        ([2.0 ** -100, 2.0 ** -100, 2.0 ** -60, -2.0 ** -60], 2.0 ** -100 + 2.0 ** -122),
+    ]
+    x = np.array([c[0] for c in cases], dtype=np.float32)
+    want = np.array([[c[1]] for c in cases], dtype=np.float32)
+    np.testing.assert_array_equal(aatc.transform(x, t), want)
+    np.testing.assert_array_equal(_rational_transform(x, t), want)
+    naive = (x.astype(np.float64) @ t.astype(np.float64)).astype(np.float32)
+    assert naive[0, 0] != want[0, 0] and naive[4, 0] != want[4, 0]
+
+
+def test_transform_identity_sign_and_scaling():
+    """T = I gives h = x; h(-x) = -h(x); power-of-two scaling of x scales h exactly."""
+    rng = np.random.default_rng(10)
+    x = (rng.standard_normal((50, 128)) * np.exp2(rng.integers(-20, 20, (50, 1)))).astype(np.float32)
+    np.testing.assert_array_equal(aatc.transform(x, np.eye(128, dtype=np.float32)), x)
+    t = aatc.stored_transform(haar_orthogonal(rng, 128))
+    h = aatc.transform(x, t)
+    np.testing.assert_array_equal(aatc.transform(-x, t), -h)
+    np.testing.assert_array_equal(aatc.transform(np.ldexp(x, 7), t), np.ldexp(h, 7))
+    # and the zero token
+    np.testing.assert_array_equal(aatc.transform(np.zeros((2, 128), np.float32), t), 0)
+
+
+def test_transform_subnormal_results():
+    """Sums below 2^-126 round to the fp32 subnormal grid (quantum 2^-149)."""
+    t = np.zeros((2, 1), dtype=np.float32)
+    t[:, 0] = [2.0 ** -22, 2.0 ** -22]
+    x = np.array([[2.0 ** -120, 2.0 ** -126],            # 2^-142 + 2^-148: exact
+                  [2.0 ** -126, 2.0 ** -127]], dtype=np.float32)   # 2^-148 + 2^-149: exact
+    want = np.array([[2.0 ** -142 + 2.0 ** -148], [3 * 2.0 ** -149]], dtype=np.float32)
+    np.testing.assert_array_equal(aatc.transform(x, t), want)
+    x2 = np.array([[2.0 ** -127, 2.0 ** -149 * 3]], dtype=np.float32)  # 2^-149 + 1.5 2^-171
+    np.testing.assert_array_equal(aatc.transform(x2, t), np.float32(2.0 ** -149))
