@@ -127,29 +127,12 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
 // consecutive codes go into the record as one bit field.
 // Needs 16-byte aligned token rows (checked by the launcher).
 // ---------------------------------------------------------------------------------------
-constexpr int kTbPitch = 144;                    // bytes per channel row of the limb tables
+// Limb tables in matrix-core operand order: the 16 bytes lane l of a wave feeds for
+// channel tile ct and k half kc sit at ((2 ct + kc) 64 + l) 16, so every operand read is one
+// contiguous 1 KiB per wave (no bank conflicts).
+constexpr int kTbBytes = 8 * 2 * 64 * 16;       // one limb of the 128 x 128 transform
 
 typedef int ev4i __attribute__((ext_vector_type(4)));
-
-// The canonical quantizer without branches: the same code as quantize_code for b >= 1,
-// and 0 for b = 0 (whose r is 0: 1/s is stored as 0 for dropped channels).  The rounding
-// floor(xq) + (frac(xq) >= 0.5) is one v_cvt_rpi_i32_f32, which rounds the exact
-// xq + 1/2 down (checked against the two-step form on the hardware: boundary values
-// k + 1/2 and k within 64 ulps for |k| <= 130, and 2^24 values in all).  `dev` receives
-// |xq - code| before the clamp (at most 1/2): the input's distance to the nearest rounding
-// boundary is 1/2 - dev.
-__device__ inline uint32_t quantize_code_nb(float r, float inv_a, int b, float& xq_out,
-                                            float& dev) {
-  const int bb = max(b, 1);
-  const float xq = ldexpf(r * inv_a, bb - 1);
-  int code;
-  asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(code) : "v"(xq));
-  xq_out = xq;
-  dev = fabsf(xq - (float)code);
-  const int half = 1 << (bb - 1);
-  code = min(max(code, -half), half - 1);
-  return __builtin_amdgcn_ubfe((uint32_t)code, 0u, (uint32_t)b);
-}
 
 template <int CTRL>
 __device__ inline float enc_dpp(float v) {
@@ -234,11 +217,16 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
     int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
     int64_t cap, int64_t pos) {
   static_assert(kEncThreads == 256, "four waves of 16 tokens per 64-token tile");
-  __shared__ __align__(16) int8_t tb[3][kD * kTbPitch];   // [limb][channel c][j]
+  __shared__ __align__(16) int8_t tb[3][kTbBytes];       // [limb][ct][kc][lane][16]
   __shared__ uint32_t rec[kTile][kRecWords];              // records of the tile's tokens
+  // Channel tables, read per tile by the lanes that hold channels 16 ct + 4 kg + i.
   __shared__ __align__(16) float tab_is[kD];              // 1 / s_c
   __shared__ __align__(16) float tab_k[kD];               // 2^(b_c - 1) / s_c (1 + 2^-20)
-  __shared__ __align__(16) uint32_t tab_b[kD / 4];        // widths, four channels a word
+  __shared__ __align__(16) float tab_p2[kD];              // 2^(b_c - 1) (1 for b_c = 0)
+  __shared__ __align__(16) float tab_hi[kD];              // 2^(b_c - 1) - 1: largest code
+  __shared__ __align__(16) uint32_t tab_msk[kD];          // 2^b_c - 1
+  __shared__ __align__(16) uint32_t tab_sh[kD];           // bit of c in its group's field
+  __shared__ __align__(16) uint32_t tab_w[kD / 4];        // width of each group of four
   __shared__ __align__(16) uint16_t tab_o[kD];            // first record bits
   __shared__ unsigned long long fixmask;                  // tokens to encode exactly
 
@@ -248,28 +236,41 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 15, kg = lane >> 4;
   const int dtype = BF16 ? AATC_BF16 : AATC_F32;
 
-  // Limb tables of the transposed integer transform: thread tid converts elements
-  // 8 (tid + 256 k) .. + 7 of Tq^T.
-  for (int k = 0; k < 8; ++k) {
-    const int e0 = 8 * (tid + kEncThreads * k), c = e0 >> 7, j = e0 & (kD - 1);
-    const int4 w0 = reinterpret_cast<const int4*>(hp->Tqt)[2 * (tid + kEncThreads * k)];
-    const int4 w1 = reinterpret_cast<const int4*>(hp->Tqt)[2 * (tid + kEncThreads * k) + 1];
-    const int va[4] = {w0.x, w0.y, w0.z, w0.w}, vb[4] = {w1.x, w1.y, w1.z, w1.w};
-    uint32_t la[3], lb[3];
-    limb_bytes4(va, la);
-    limb_bytes4(vb, lb);
+  // Limb tables of the transposed integer transform: operand slot u = (2 ct + kc) 64 + l
+  // (l = 16 kg + n) holds Tq^T[16 ct + n][64 kc + 16 kg .. + 15]; thread tid fills slots
+  // tid + 256 k.
+  for (int k = 0; k < 4; ++k) {
+    const int u = tid + kEncThreads * k, l = u & 63, ct = u >> 7, kc = (u >> 6) & 1;
+    const int4* src = reinterpret_cast<const int4*>(hp->Tqt + (16 * ct + (l & 15)) * kD +
+                                                    64 * kc + 16 * (l >> 4));
+    uint32_t w[3][4];
 #pragma unroll
-    for (int l = 0; l < 3; ++l)
-      *reinterpret_cast<uint2*>(&tb[l][c * kTbPitch + j]) = make_uint2(la[l], lb[l]);
+    for (int q = 0; q < 4; ++q) {
+      const int4 t4 = src[q];
+      const int v[4] = {t4.x, t4.y, t4.z, t4.w};
+      uint32_t lb[3];
+      limb_bytes4(v, lb);
+#pragma unroll
+      for (int li = 0; li < 3; ++li) w[li][q] = lb[li];
+    }
+#pragma unroll
+    for (int li = 0; li < 3; ++li)
+      *reinterpret_cast<uint4*>(&tb[li][16 * u]) = make_uint4(w[li][0], w[li][1], w[li][2], w[li][3]);
   }
-  // Channel tables (read per tile by the lanes that hold channels 16 ct + 4 kg + i).
   if (tid < kD) {
     const int b = hp->bits[tid];
     tab_is[tid] = hp->inv_s[tid];
     tab_k[tid] = ldexpf(hp->inv_s[tid], max(b, 1) - 1) * (1.f + 0x1p-20f);
+    tab_p2[tid] = ldexpf(1.f, max(b, 1) - 1);
+    tab_hi[tid] = ldexpf(1.f, max(b, 1) - 1) - 1.f;
+    tab_msk[tid] = (1u << b) - 1u;
+    int sh = 0;
+    for (int c = tid & ~3; c < tid; ++c) sh += hp->bits[c];
+    tab_sh[tid] = (uint32_t)sh;
     tab_o[tid] = hp->bit_off[tid];
   }
-  if (tid < kD / 4) tab_b[tid] = reinterpret_cast<const uint32_t*>(hp->bits)[tid];
+  if (tid < kD / 4)
+    tab_w[tid] = hp->bits[4 * tid] + hp->bits[4 * tid + 1] + hp->bits[4 * tid + 2] + hp->bits[4 * tid + 3];
   for (int i = tid; i < kTile * kRecWords; i += kEncThreads) (&rec[0][0])[i] = 0u;
   if (tid == 0) fixmask = 0ull;
   const float inv_s_max = hp->inv_s_max;
@@ -342,7 +343,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
       for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int o = (16 * (c4 + u) + n) * kTbPitch + 64 * kc + 16 * kg;
+          const int o = 16 * ((2 * (c4 + u) + kc) * 64 + lane);
           const ev4i b0 = *reinterpret_cast<const ev4i*>(&tb[0][o]);
           const ev4i b1 = *reinterpret_cast<const ev4i*>(&tb[1][o]);
           const ev4i b2 = *reinterpret_cast<const ev4i*>(&tb[2][o]);
@@ -397,25 +398,38 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
 #pragma unroll
       for (int ct = 0; ct < 8; ++ct) {
         const int c0 = 16 * ct + 4 * kg;
-        const uint32_t bw = tab_b[c0 >> 2];
+        const float4 p4 = *reinterpret_cast<const float4*>(&tab_p2[c0]);
+        const float4 h4 = *reinterpret_cast<const float4*>(&tab_hi[c0]);
+        const uint4 m4 = *reinterpret_cast<const uint4*>(&tab_msk[c0]);
+        const uint4 s4 = *reinterpret_cast<const uint4*>(&tab_sh[c0]);
+        const float p2[4] = {p4.x, p4.y, p4.z, p4.w}, hv[4] = {h4.x, h4.y, h4.z, h4.w};
+        const uint32_t mk[4] = {m4.x, m4.y, m4.z, m4.w}, sh[4] = {s4.x, s4.y, s4.z, s4.w};
         float4 k4;
         if constexpr (CERT) k4 = *reinterpret_cast<const float4*>(&tab_k[c0]);
         uint32_t f = 0u;
-        int width = 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int b = (int)((bw >> (8 * i)) & 255u);
-          float xq, dev;
-          const uint32_t u = quantize_code_nb(r[ct][i], inv_a, b, xq, dev);
+          // The canonical quantizer: xq = fl32(r / alpha) 2^(b-1) (the power of two is
+          // exact), code = floor(xq + 1/2) clamped to [-2^(b-1), 2^(b-1) - 1], b-bit two's
+          // complement.  Clamping xq first (the bounds are integers) and then rounding half
+          // up with v_cvt_rpi_i32_f32 gives the same code (checked on the hardware against
+          // floor(xq) + (frac >= 1/2): boundary values within 64 ulps of k and k + 1/2 for
+          // |k| <= 130, 2^24 values in all).  Dropped channels have r = 0 and mask 0.
+          const float xq = (r[ct][i] * inv_a) * p2[i];
+          const float xc = __builtin_amdgcn_fmed3f(xq, -p2[i], hv[i]);
+          int code;
+          asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(code) : "v"(xc));
           if constexpr (CERT) {
-            const float kc = i == 0 ? k4.x : i == 1 ? k4.y : i == 2 ? k4.z : k4.w;
-            // distance to the nearest boundary 1/2 - dev against the bound in x units,
-            // plus both evaluations' fp32 roundings and that of xq + 1/2
-            const float mg = fmaf(kc, ea, fmaf(0x1p-21f, fabsf(xq), 0x1p-22f));
+            int cu;
+            asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(cu) : "v"(xq));
+            const float dev = fabsf(xq - (float)cu);   // 1/2 - distance to a boundary
+            const float kf = i == 0 ? k4.x : i == 1 ? k4.y : i == 2 ? k4.z : k4.w;
+            // the bound in x units, plus both evaluations' fp32 roundings and that of
+            // xq + 1/2
+            const float mg = fmaf(kf, ea, fmaf(0x1p-21f, fabsf(xq), 0x1p-22f));
             uncertain |= (dev + mg >= 0.5f);
           }
-          f |= u << width;
-          width += b;
+          f |= ((uint32_t)code & mk[i]) << sh[i];
         }
         field[ct] = f;
       }
@@ -430,8 +444,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
 #pragma unroll
       for (int ct = 0; ct < 8; ++ct) {
         const int c0 = 16 * ct + 4 * kg;
-        const uint32_t bw = tab_b[c0 >> 2];
-        const int width = (int)((bw & 255u) + ((bw >> 8) & 255u) + ((bw >> 16) & 255u) + (bw >> 24));
+        const int width = (int)tab_w[c0 >> 2];
         const int off = tab_o[c0];
         if (width > 0) {
           atomicOr(&rec[tl][off >> 5], field[ct] << (off & 31));
