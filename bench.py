@@ -82,6 +82,41 @@ def setup_decode(cfg_id=2):
                 rk=rk, rv=rv, last_tok=last_tok, cal_k=cal_k, cal_v=cal_v)
 
 
+def setup_decode_random_codes(cfg_id, seed=0):
+    """Another decode workload for throughput only: the configuration's own calibrations
+    (so its record sizes and widths), with caches of uniformly random code bits and token
+    scales in [0.5, 2).  The decode kernel reads every byte whatever its value, so the
+    timing is that of real codes; parity of these shapes is covered by the GPU tests."""
+    import torch
+    import paper_2608_14191_amd as P
+    from kvsynth import workload
+
+    w = workload(cfg_id)
+    H, L, B = w.n_kv_heads, w.n_tokens, w.batch
+    avg = w.cfg["avg_bits"][0]
+    qw = w.cfg["query_weighted_k"]
+    cal_k = [P.aatc_calibrate(w.calib(h, "k"), avg, q_calib=w.calib_queries(h) if qw else None,
+                              q_group=w.group) for h in range(H)]
+    cal_v = [P.aatc_calibrate(w.calib(h, "v"), avg) for h in range(H)]
+    pk = torch.from_numpy(P.aatc_params_pack(cal_k)).cuda()
+    pv = torch.from_numpy(P.aatc_params_pack(cal_v)).cuda()
+    rk, rv = cal_k[0].record_bytes, cal_v[0].record_bytes
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    kc = torch.randint(0, 256, (B, H, L, rk), dtype=torch.uint8, device="cuda", generator=g)
+    vc = torch.randint(0, 256, (B, H, L // 64, 64 * rv), dtype=torch.uint8, device="cuda",
+                       generator=g)
+
+    def scales():
+        a = 0.5 + 1.5 * torch.rand((B, H, L), device="cuda", generator=g)
+        return a.to(torch.float16).view(torch.int16)
+    ka, va = scales(), scales()
+    x_last = [bf16_tensor(np.stack([w.cache(0, h, kind, n=1, start=L - 1)[0]
+                                    for h in range(H)]))[None] for kind in ("k", "v")]
+    q = bf16_tensor(np.stack([w.queries(b) for b in range(B)]))
+    return dict(w=w, P=P, pk=pk, pv=pv, kc=kc, vc=vc, ka=ka, va=va, q=q, cap=L, L=L,
+                rk=rk, rv=rv, last_tok=x_last, cal_k=cal_k, cal_v=cal_v)
+
+
 def decode_bytes(s) -> int:
     w = s["w"]
     return w.batch * w.n_kv_heads * s["L"] * (s["rk"] + s["rv"] + 4)
@@ -189,14 +224,12 @@ def run_encode_bench(avg_bits, reps=3):
                 bytes=int(L * H * (2 * 128 * 2 + rk + rv + 4)))
 
 
-def cpu_baseline(s, target_seconds=15.0):
-    """The oracle's decode attention over a bounded token sample of the same workload."""
+def cpu_baseline(s, target_seconds=15.0, single_thread_seconds=8.0):
+    """The oracle's decode attention over a bounded token sample of the same workload, on
+    all host threads and again on one."""
     from oracle import aatc as ora
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
+    from threadpoolctl import threadpool_info, threadpool_limits
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     w = s["w"]
     H = w.n_kv_heads
 
@@ -214,18 +247,26 @@ def cpu_baseline(s, target_seconds=15.0):
     ka = [s["ka"][0, h, :n].cpu().numpy().view(np.float16) for h in range(H)]
     va = [s["va"][0, h, :n].cpu().numpy().view(np.float16) for h in range(H)]
     q32 = w.as_f32(w.queries(0))
-    reps, t_total = 0, 0.0
-    while t_total < target_seconds and reps < 200:
-        t0 = time.perf_counter()
-        ora.decode_attention(q32, ck, cv, krec, ka, vrec, va, n)
-        t_total += time.perf_counter() - t0
-        reps += 1
-    per = t_total / reps
+
+    def timed(seconds):
+        reps, t_total = 0, 0.0
+        while t_total < seconds and reps < 200:
+            t0 = time.perf_counter()
+            ora.decode_attention(q32, ck, cv, krec, ka, vrec, va, n)
+            t_total += time.perf_counter() - t0
+            reps += 1
+        return reps, t_total / reps
+
     nbytes = H * n * (s["rk"] + s["rv"] + 4)
+    reps, per = timed(target_seconds)
+    with threadpool_limits(limits=1):
+        reps1, per1 = timed(single_thread_seconds)
     return {"value": nbytes / per / 1e9, "unit": "GB/s", "cores": int(threads), "kind": "oracle",
             "sample": f"oracle decode attention of 32 query heads over the first {n} of the "
                       f"32768 cached tokens (8 KV heads), {reps} runs, {per:.2f} s each; "
-                      f"GB/s over the same packed-cache bytes as the GPU metric"}
+                      f"GB/s over the same packed-cache bytes as the GPU metric",
+            "single_thread": {"value": nbytes / per1 / 1e9, "unit": "GB/s", "cores": 1,
+                              "sample": f"the same sample, {reps1} runs, {per1:.2f} s each"}}
 
 
 COUNTERS_SUMMARY = os.path.join(ROOT, "profiles", "decode_mfma_llama31_8b_b1_32k_counters.md")
@@ -294,6 +335,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-encode", action="store_true")
+    ap.add_argument("--no-other-decode", action="store_true",
+                    help="skip the Qwen-shape and long-context decode entries")
     ap.add_argument("--counters", action="store_true",
                     help="eager decodes plus a calibration copy, for rocprofv3 --pmc runs")
     args = ap.parse_args()
@@ -320,7 +363,26 @@ def main():
         for avg in (2.75, 4.0):
             r = run_encode_bench(avg)
             enc.append(r)
-            _log(f"[encode] {avg} bits: {r['seconds'] * 1e3:.2f} ms, {r['tokens_per_s']:.3e} tok/s")
+            _log(f"[encode] {avg} bits: {r['seconds'] * 1e3:.2f} ms, {r['tokens_per_s']:.3e} tok/s, "
+                 f"{r['bytes'] / r['seconds'] / 1e9:.0f} GB/s")
+    other = []
+    if not args.no_other_decode:
+        names = {3: "qwen25_7b_decode_b8_16k: batch 8, 28 q / 4 kv heads, 16384 tokens, 2.75 bits",
+                 5: "llama31_8b_decode_b4_128k: batch 4, 32 q / 8 kv heads, 131072 tokens, "
+                    "2.0 bits, query-weighted keys"}
+        for cfg in (3, 5):
+            so = setup_decode_random_codes(cfg)
+            nb = decode_bytes(so)
+            el, km, nc, _ = run_decode_bench(so, 40, 5)
+            other.append({"workload": names[cfg], "bytes_per_step": nb,
+                          "us_per_step": round(el / 40 * 1e6, 2),
+                          "kernel_us": round(km * 1e3, 2),
+                          "kernel_GBps": round(nb / (km * 1e-3) / 1e9, 1),
+                          "frac": round(nb / (km * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "cache_copies": nc, "data": "random code bits, real calibrations"})
+            _log(f"[decode cfg {cfg}] kernel {km * 1e3:.1f} us, {nb / (km * 1e-3) / 1e9:.0f} GB/s")
+            del so
+            torch.cuda.empty_cache()
     line = {
         "metric": "decode-attention HBM GB/s (% of peak) on packed KV; encode tokens/sec",
         "value": round(value, 2),
@@ -344,7 +406,11 @@ def main():
                      "traffic": counted_traffic()},
         "encode": [{"workload": f"llama31_8b_prefill_64k at {r['avg_bits']} bits",
                     "tokens_per_s": round(r["tokens_per_s"], 1),
-                    "ms": round(r["seconds"] * 1e3, 3)} for r in enc],
+                    "ms": round(r["seconds"] * 1e3, 3),
+                    "hbm_bytes": r["bytes"],
+                    "roofline_frac": round(r["bytes"] / r["seconds"] / 1e9 / HBM_PEAK_GBS, 4)}
+                   for r in enc],
+        "decode_other": other,
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(s)
