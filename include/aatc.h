@@ -261,6 +261,29 @@ aatc_status aatc_append_decode_attention(const void* dev_params_k, const void* d
                                          float softmax_scale, float* out, void* workspace,
                                          size_t ws_bytes, void* stream);
 
+/*
+ * aatc_append_decode_attention_noalloc -- aatc_append_decode_attention without a caller
+ * workspace, for callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).
+ *
+ * The same step and results as aatc_append_decode_attention with the same arguments; the
+ * workspace is the library's own static device array (32 MiB, one per GPU the library
+ * runs on, held until the process ends; no allocation at any call).  Its limit: at most
+ * 256 (sequence, KV head) rows (batch * n_kv_heads), and aatc_decode_workspace_bytes of
+ * the call plus a fixed 64 KiB counter region within 32 MiB (about batch * n_q_heads *
+ * cap / 512 * 528 bytes of partials: e.g. batch 4, 32 query heads, 131072 tokens).  Larger
+ * requests return AATC_E_WORKSPACE before anything is launched.  Calls that overlap on one
+ * GPU share the array and race: order them on one stream.
+ * Errors: as aatc_append_decode_attention; AATC_E_DEVICE if the array's address cannot be
+ * obtained.
+ */
+aatc_status aatc_append_decode_attention_noalloc(
+    const void* dev_params_k, const void* dev_params_v, int32_t batch, int32_t n_q_heads,
+    int32_t n_kv_heads, int32_t d, const void* q, aatc_dtype q_dtype, const void* x_k,
+    const void* x_v, aatc_dtype x_dtype, void* k_codes, uint16_t* k_alpha, void* v_codes,
+    uint16_t* v_alpha, const int32_t* seq_len, int64_t cap, int32_t k_record_bytes,
+    int32_t v_record_bytes, float softmax_scale, float* out, void* stream);
+
 /* Human-readable name of a status code (static string). */
 const char* aatc_status_string(aatc_status s);
 

@@ -91,6 +91,12 @@ _L.aatc_append_decode_attention.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32, _v
                                             ctypes.c_int, _vp, _vp, ctypes.c_int, _vp, _vp, _vp,
                                             _vp, _vp, _i64, _i32, _i32, _f32, _vp, _vp, _sz, _vp]
 
+_L.aatc_append_decode_attention_noalloc.restype = ctypes.c_int
+_L.aatc_append_decode_attention_noalloc.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32, _vp,
+                                                    ctypes.c_int, _vp, _vp, ctypes.c_int, _vp,
+                                                    _vp, _vp, _vp, _vp, _i64, _i32, _i32, _f32,
+                                                    _vp, _vp]
+
 
 def library() -> ctypes.CDLL:
     return _L
@@ -230,3 +236,21 @@ def aatc_append_decode_attention(dev_params_k, dev_params_v, batch: int, n_q_hea
         int(cap), int(k_record_bytes), int(v_record_bytes), float(softmax_scale), _dptr(out),
         _dptr(workspace), int(workspace.numel() * workspace.element_size()), _stream(stream))
     _check("aatc_append_decode_attention", st)
+
+
+def aatc_append_decode_attention_noalloc(dev_params_k, dev_params_v, batch: int, n_q_heads: int,
+                                         n_kv_heads: int, q, x_k, x_v, k_codes, k_alpha,
+                                         v_codes, v_alpha, seq_len, cap: int,
+                                         k_record_bytes: int, v_record_bytes: int,
+                                         softmax_scale: float, out, stream=None):
+    """aatc_append_decode_attention with the library's static workspace (no allocation)."""
+    if _dtype_code(x_k) != _dtype_code(x_v):
+        raise AatcError("aatc_append_decode_attention_noalloc (x_k and x_v dtypes differ)",
+                        E_INVALID)
+    st = _L.aatc_append_decode_attention_noalloc(
+        _dptr(dev_params_k), _dptr(dev_params_v), int(batch), int(n_q_heads), int(n_kv_heads),
+        HEAD_DIM, _dptr(q), _dtype_code(q), _dptr(x_k), _dptr(x_v), _dtype_code(x_k),
+        _dptr(k_codes), _dptr(k_alpha), _dptr(v_codes), _dptr(v_alpha), _dptr(seq_len),
+        int(cap), int(k_record_bytes), int(v_record_bytes), float(softmax_scale), _dptr(out),
+        _stream(stream))
+    _check("aatc_append_decode_attention_noalloc", st)

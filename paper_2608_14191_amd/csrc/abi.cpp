@@ -169,10 +169,10 @@ aatc_status check_decode(const void* dev_params_k, const void* dev_params_v, int
                          const void* v_codes, const uint16_t* v_alpha, const int32_t* seq_len,
                          int64_t cap, int32_t k_record_bytes, int32_t v_record_bytes,
                          float softmax_scale, const float* out, const void* workspace,
-                         size_t ws_bytes) {
+                         size_t ws_bytes, bool static_ws = false) {
   if (d != kD) return AATC_E_UNSUPPORTED;
   if (!dev_params_k || !dev_params_v || !q || !k_codes || !k_alpha || !v_codes || !v_alpha ||
-      !seq_len || !out || !workspace)
+      !seq_len || !out || (!workspace && !static_ws))
     return AATC_E_INVALID;
   if (batch < 1 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0)
     return AATC_E_INVALID;
@@ -188,8 +188,21 @@ aatc_status check_decode(const void* dev_params_k, const void* dev_params_v, int
       !aligned(seq_len, 4) || !aligned(out, 16) || !aligned(workspace, 256) ||
       !aligned(q, q_dtype == AATC_F32 ? 4 : 2))
     return AATC_E_INVALID;
-  if (ws_bytes < decode_workspace_bytes(batch, n_q_heads, n_kv_heads, cap))
+  if (static_ws) {
+    if ((int64_t)batch * n_kv_heads > kScratchRows ||
+        decode_workspace_bytes(batch, n_q_heads, n_kv_heads, cap, kScratchRows) > kScratchBytes)
+      return AATC_E_WORKSPACE;
+  } else if (ws_bytes < decode_workspace_bytes(batch, n_q_heads, n_kv_heads, cap)) {
     return AATC_E_WORKSPACE;
+  }
+  return AATC_OK;
+}
+
+aatc_status check_new_tokens(const void* x_k, const void* x_v, aatc_dtype x_dtype) {
+  if (!x_k || !x_v) return AATC_E_INVALID;
+  if (x_dtype != AATC_F32 && x_dtype != AATC_BF16) return AATC_E_INVALID;
+  const size_t xa = x_dtype == AATC_F32 ? 4 : 2;
+  if (!aligned(x_k, xa) || !aligned(x_v, xa)) return AATC_E_INVALID;
   return AATC_OK;
 }
 
@@ -228,14 +241,38 @@ extern "C" aatc_status aatc_append_decode_attention(
                                        seq_len, cap, k_record_bytes, v_record_bytes,
                                        softmax_scale, out, workspace, ws_bytes);
     if (e != AATC_OK) return e;
-    if (!x_k || !x_v) return AATC_E_INVALID;
-    if (x_dtype != AATC_F32 && x_dtype != AATC_BF16) return AATC_E_INVALID;
-    const size_t xa = x_dtype == AATC_F32 ? 4 : 2;
-    if (!aligned(x_k, xa) || !aligned(x_v, xa)) return AATC_E_INVALID;
+    const aatc_status ex = check_new_tokens(x_k, x_v, x_dtype);
+    if (ex != AATC_OK) return ex;
     return launch_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads, q, q_dtype,
                          k_codes, k_alpha, v_codes, v_alpha, seq_len, cap, k_record_bytes,
                          v_record_bytes, softmax_scale, out, workspace, stream, x_k, x_v,
                          x_dtype);
+  } catch (...) {
+    return AATC_E_INVALID;
+  }
+}
+
+extern "C" aatc_status aatc_append_decode_attention_noalloc(
+    const void* dev_params_k, const void* dev_params_v, int32_t batch, int32_t n_q_heads,
+    int32_t n_kv_heads, int32_t d, const void* q, aatc_dtype q_dtype, const void* x_k,
+    const void* x_v, aatc_dtype x_dtype, void* k_codes, uint16_t* k_alpha, void* v_codes,
+    uint16_t* v_alpha, const int32_t* seq_len, int64_t cap, int32_t k_record_bytes,
+    int32_t v_record_bytes, float softmax_scale, float* out, void* stream) {
+  try {
+    const aatc_status e = check_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads,
+                                       d, q, q_dtype, k_codes, k_alpha, v_codes, v_alpha,
+                                       seq_len, cap, k_record_bytes, v_record_bytes,
+                                       softmax_scale, out, nullptr, 0, true);
+    if (e != AATC_OK) return e;
+    const aatc_status ex = check_new_tokens(x_k, x_v, x_dtype);
+    if (ex != AATC_OK) return ex;
+    void* ws = nullptr;
+    const aatc_status es = noalloc_scratch(&ws, stream);
+    if (es != AATC_OK) return es;
+    return launch_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads, q, q_dtype,
+                         k_codes, k_alpha, v_codes, v_alpha, seq_len, cap, k_record_bytes,
+                         v_record_bytes, softmax_scale, out, ws, stream, x_k, x_v, x_dtype,
+                         kScratchRows);
   } catch (...) {
     return AATC_E_INVALID;
   }

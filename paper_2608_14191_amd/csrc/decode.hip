@@ -350,12 +350,17 @@ struct WsLayout {
 
 __host__ __device__ inline size_t round256(size_t x) { return (x + 255) / 256 * 256; }
 
-inline WsLayout ws_layout(int batch, int n_q_heads, int n_kv_heads, int64_t cap) {
+// counter_rows > rows reserves the counters of that many rows, so that the counters keep
+// one place whatever the shape of the call (the static workspace of the no-allocation entry
+// point: counters left at zero by one call are where the next call looks for them).
+inline WsLayout ws_layout(int batch, int n_q_heads, int n_kv_heads, int64_t cap,
+                          int counter_rows = 0) {
   const size_t rows = (size_t)batch * n_kv_heads;
+  const size_t crows = std::max(rows, (size_t)std::max(counter_rows, 0));
   const size_t n_splits = (size_t)((cap + kMinSplit - 1) / kMinSplit);
   WsLayout w;
   w.counters = 0;
-  w.partials = round256(rows * kCtrStride * sizeof(unsigned));
+  w.partials = round256(crows * kCtrStride * sizeof(unsigned));
   w.append_r = round256(w.partials + (size_t)batch * n_q_heads * n_splits * sizeof(Partial));
   w.total = w.append_r + rows * kAppStride * sizeof(float);   // fused append, per row
   return w;
@@ -2005,8 +2010,9 @@ void decode_mfma_kernel(const DecodeArgs a) {
 
 }  // namespace
 
-size_t decode_workspace_bytes(int batch, int n_q_heads, int n_kv_heads, int64_t cap) {
-  return ws_layout(batch, n_q_heads, n_kv_heads, cap).total;
+size_t decode_workspace_bytes(int batch, int n_q_heads, int n_kv_heads, int64_t cap,
+                              int counter_rows) {
+  return ws_layout(batch, n_q_heads, n_kv_heads, cap, counter_rows).total;
 }
 
 // The dynamic LDS limit of one kernel, raised on each device the first time a launch there
@@ -2120,9 +2126,10 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
                           const void* k_codes, const uint16_t* k_alpha, const void* v_codes,
                           const uint16_t* v_alpha, const int32_t* seq_len, int64_t cap,
                           int rk, int rv, float softmax_scale, float* out, void* workspace,
-                          void* stream, const void* x_k, const void* x_v, aatc_dtype x_dtype) {
+                          void* stream, const void* x_k, const void* x_v, aatc_dtype x_dtype,
+                          int counter_rows) {
   const int G = n_q_heads / n_kv_heads;
-  const WsLayout wl = ws_layout(batch, n_q_heads, n_kv_heads, cap);
+  const WsLayout wl = ws_layout(batch, n_q_heads, n_kv_heads, cap, counter_rows);
   char* ws = static_cast<char*>(workspace);
   auto* ctr = reinterpret_cast<unsigned*>(ws + wl.counters);
   auto* parts = reinterpret_cast<Partial*>(ws + wl.partials);

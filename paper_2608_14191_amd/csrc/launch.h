@@ -24,7 +24,9 @@ aatc_status launch_encode_last(const void* params, int n_heads, int batch, const
                                uint16_t* alpha, int64_t cap, int record_bytes,
                                const int32_t* seq_len, void* stream);
 
-size_t decode_workspace_bytes(int batch, int n_q_heads, int n_kv_heads, int64_t cap);
+// counter_rows: see ws_layout (0: the call's own rows).
+size_t decode_workspace_bytes(int batch, int n_q_heads, int n_kv_heads, int64_t cap,
+                              int counter_rows = 0);
 
 aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
                           int n_q_heads, int n_kv_heads, const void* q, aatc_dtype q_dtype,
@@ -33,6 +35,13 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
                           int k_record_bytes, int v_record_bytes, float softmax_scale,
                           float* out, void* workspace, void* stream,
                           const void* x_k = nullptr, const void* x_v = nullptr,
-                          aatc_dtype x_dtype = AATC_BF16);
+                          aatc_dtype x_dtype = AATC_BF16, int counter_rows = 0);
+
+// The static workspace of aatc_append_decode_attention_noalloc (noalloc.hip).
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+constexpr int kScratchRows = 256;      // (sequence, KV head) rows with a fixed counter slot
+// This device's static workspace: its address (hipGetSymbolAddress, once per device, with
+// the counters region cleared by a kernel on `stream` at that first call).
+aatc_status noalloc_scratch(void** ptr, void* stream);
 
 }  // namespace aatc

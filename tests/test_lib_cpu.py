@@ -243,6 +243,19 @@ def test_append_decode_binding_rejects_mixed_token_dtypes():
     assert e.value.status == 1
 
 
+def test_noalloc_entry_point_rejects_oversized_requests():
+    """The static workspace takes at most 256 (sequence, KV head) rows and 32 MiB; larger
+    requests return AATC_E_WORKSPACE before any launch (host checks only)."""
+    L = P.library()
+    p = _fake()
+    args = [p, p, 40, 32, 8, 128, p, 1, p, p, 1, p, p, p, p, p, 4096, 44, 44, 0.088, p, None]
+    assert L.aatc_append_decode_attention_noalloc(*args) == 5        # 320 rows
+    args = [p, p, 32, 32, 8, 128, p, 1, p, p, 1, p, p, p, p, p, 1 << 20, 44, 44, 0.088, p, None]
+    assert L.aatc_append_decode_attention_noalloc(*args) == 5        # partials beyond 32 MiB
+    bad = [p, p, 1, 32, 8, 128, p, 1, None, p, 1, p, p, p, p, p, 4096, 44, 44, 0.088, p, None]
+    assert L.aatc_append_decode_attention_noalloc(*bad) == 1         # no new keys
+
+
 def _global_cases():
     rng = np.random.default_rng(2024)
     ints = rng.integers(0, 4, size=(5, 16)).astype(np.float64)      # many exact ties
