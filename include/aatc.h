@@ -262,6 +262,49 @@ aatc_status aatc_append_decode_attention(const void* dev_params_k, const void* d
                                          size_t ws_bytes, void* stream);
 
 /*
+ * aatc_decode_attention_segmented -- decode attention over a compressed cache plus a
+ * segment of tokens kept at input precision.
+ *
+ * The paper's inference path (Sec. 6, experimental setup; App. E, "AATC") keeps the first
+ * s tokens and the most recent w tokens of each sequence at full precision and quantizes
+ * the rest (aatc_segment_counts gives the split).  The result is exact softmax attention
+ * of each query head over the union of the seq_len[b] tokens of the compressed caches (as
+ * in aatc_decode_attention) and the seg_len[b] segment tokens, whose order does not matter:
+ *   o = sum_i softmax_i(scale q . k_i) v_i,  k_i, v_i dequantized or as stored.
+ * The segment is one more softmax partial: a small kernel computes it (in the original
+ * domain, then T_V^T into the transformed domain of the merge) before the decode launch.
+ *
+ * seg_k, seg_v  device [batch][n_kv_heads][seg_cap][d] segment keys and values, seg_dtype
+ *               F32 or BF16 (2- or 4-byte aligned).
+ * seg_len       device [batch] int32 tokens in the segment (clamped to [0, seg_cap]).
+ * seg_cap       1..256.
+ * Other arguments, the workspace and errors as in aatc_decode_attention.
+ */
+aatc_status aatc_decode_attention_segmented(
+    const void* dev_params_k, const void* dev_params_v, int32_t batch, int32_t n_q_heads,
+    int32_t n_kv_heads, int32_t d, const void* q, aatc_dtype q_dtype, const void* k_codes,
+    const uint16_t* k_alpha, const void* v_codes, const uint16_t* v_alpha,
+    const int32_t* seq_len, int64_t cap, int32_t k_record_bytes, int32_t v_record_bytes,
+    float softmax_scale, const void* seg_k, const void* seg_v, aatc_dtype seg_dtype,
+    const int32_t* seg_len, int32_t seg_cap, float* out, void* workspace, size_t ws_bytes,
+    void* stream);
+
+/*
+ * aatc_segment_counts -- the split of a sequence of n_tokens tokens under the paper's
+ * full-precision policy (Sec. 6 experimental setup; App. E, "AATC": s = 4, w = 128,
+ * step 16): the first `sink` tokens and a recent window stay at input precision; each
+ * time the window holds `window` tokens, its oldest `step` tokens are quantized into the
+ * compressed cache.  With m = max(n_tokens - sink, 0) tokens after the sink,
+ * n_compressed = 0 if m < window, else step * (floor((m - window) / step) + 1): tokens
+ * sink .. sink + n_compressed - 1 are compressed, the other n_segment tokens (the sink
+ * and the window, which then holds window - step .. window - 1 tokens) are not.
+ * Host only.  Errors: AATC_E_INVALID (NULL outputs, n_tokens < 0, sink < 0, window < 1,
+ * step outside [1, window]).
+ */
+aatc_status aatc_segment_counts(int64_t n_tokens, int32_t sink, int32_t window, int32_t step,
+                                int64_t* n_compressed, int32_t* n_segment);
+
+/*
  * aatc_append_decode_attention_noalloc -- aatc_append_decode_attention without a caller
  * workspace, for callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid allocation).

@@ -542,3 +542,44 @@ def decode_attention(q32: np.ndarray, cal_k, cal_v, k_rec, k_alpha, v_rec, v_alp
         vh = decode_tokens(v_rec[h][:seq_len], v_alpha[h][:seq_len], cal_v[h])
         out[h * g:(h + 1) * g] = softmax_attention(q32[h * g:(h + 1) * g], kh, vh, scale)
     return out
+
+
+# --------------------------------------------------------------------------------------
+# Full-precision sink and recent window (Sec. 6 experimental setup; App. E, "AATC")
+# --------------------------------------------------------------------------------------
+def segment_split(n_tokens: int, sink: int = 4, window: int = 128, step: int = 16):
+    """Which of a sequence's first ``n_tokens`` tokens are compressed and which stay at
+    input precision, by playing the paper's policy token by token: the first ``sink``
+    tokens are kept; later tokens enter the recent window, and whenever the window holds
+    ``window`` tokens its oldest ``step`` are quantized (appended to the compressed cache).
+    Returns (compressed token indices in cache order, segment token indices)."""
+    kept = list(range(min(sink, n_tokens)))
+    compressed, win = [], []
+    for t in range(len(kept), n_tokens):
+        win.append(t)
+        if len(win) == window:
+            compressed.extend(win[:step])
+            win = win[step:]
+    return np.array(compressed, dtype=np.int64), np.array(kept + win, dtype=np.int64)
+
+
+def attention_with_segment(q32, cal_k, cal_v, k_rec, k_alpha, v_rec, v_alpha, n_comp: int,
+                           seg_k, seg_v, scale: Optional[float] = None) -> np.ndarray:
+    """Exact softmax attention of each query head over the union of its KV head's
+    ``n_comp`` compressed tokens (decoded: records, fp16 scales, calibration) and its
+    segment tokens kept at input precision (``seg_k[h]``, ``seg_v[h]``: [n, d] fp32 values).
+    Query head j reads KV head j // (H_q / H_kv).  Returns [H_q, d] fp64."""
+    hq, d = q32.shape
+    hkv = len(cal_k)
+    g = hq // hkv
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    out = np.zeros((hq, d))
+    for h in range(hkv):
+        kh = decode_tokens(k_rec[h][:n_comp], k_alpha[h][:n_comp], cal_k[h])
+        vh = decode_tokens(v_rec[h][:n_comp], v_alpha[h][:n_comp], cal_v[h])
+        kk = np.concatenate([kh, np.asarray(seg_k[h], dtype=np.float64)], axis=0)
+        vv = np.concatenate([vh, np.asarray(seg_v[h], dtype=np.float64)], axis=0)
+        if kk.shape[0] == 0:
+            continue
+        out[h * g:(h + 1) * g] = softmax_attention(q32[h * g:(h + 1) * g], kk, vv, scale)
+    return out

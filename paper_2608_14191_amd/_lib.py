@@ -96,6 +96,14 @@ _L.aatc_append_decode_attention_noalloc.argtypes = [_vp, _vp, _i32, _i32, _i32, 
                                                     ctypes.c_int, _vp, _vp, ctypes.c_int, _vp,
                                                     _vp, _vp, _vp, _vp, _i64, _i32, _i32, _f32,
                                                     _vp, _vp]
+_L.aatc_decode_attention_segmented.restype = ctypes.c_int
+_L.aatc_decode_attention_segmented.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32, _vp,
+                                               ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _i64,
+                                               _i32, _i32, _f32, _vp, _vp, ctypes.c_int, _vp,
+                                               _i32, _vp, _vp, _sz, _vp]
+_L.aatc_segment_counts.restype = ctypes.c_int
+_L.aatc_segment_counts.argtypes = [_i64, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_int64),
+                                   ctypes.POINTER(ctypes.c_int32)]
 
 
 def library() -> ctypes.CDLL:
@@ -254,3 +262,33 @@ def aatc_append_decode_attention_noalloc(dev_params_k, dev_params_v, batch: int,
         int(cap), int(k_record_bytes), int(v_record_bytes), float(softmax_scale), _dptr(out),
         _stream(stream))
     _check("aatc_append_decode_attention_noalloc", st)
+
+
+def aatc_decode_attention_segmented(dev_params_k, dev_params_v, batch: int, n_q_heads: int,
+                                    n_kv_heads: int, q, k_codes, k_alpha, v_codes, v_alpha,
+                                    seq_len, cap: int, k_record_bytes: int, v_record_bytes: int,
+                                    softmax_scale: float, seg_k, seg_v, seg_len, seg_cap: int,
+                                    out, workspace, stream=None):
+    """Decode attention over the compressed caches plus the full-precision segment
+    (seg_k / seg_v: [batch][n_kv_heads][seg_cap][128])."""
+    if _dtype_code(seg_k) != _dtype_code(seg_v):
+        raise AatcError("aatc_decode_attention_segmented (seg_k and seg_v dtypes differ)",
+                        E_INVALID)
+    st = _L.aatc_decode_attention_segmented(
+        _dptr(dev_params_k), _dptr(dev_params_v), int(batch), int(n_q_heads), int(n_kv_heads),
+        HEAD_DIM, _dptr(q), _dtype_code(q), _dptr(k_codes), _dptr(k_alpha), _dptr(v_codes),
+        _dptr(v_alpha), _dptr(seq_len), int(cap), int(k_record_bytes), int(v_record_bytes),
+        float(softmax_scale), _dptr(seg_k), _dptr(seg_v), _dtype_code(seg_k), _dptr(seg_len),
+        int(seg_cap), _dptr(out), _dptr(workspace),
+        int(workspace.numel() * workspace.element_size()), _stream(stream))
+    _check("aatc_decode_attention_segmented", st)
+
+
+def aatc_segment_counts(n_tokens: int, sink: int = 4, window: int = 128, step: int = 16):
+    """(n_compressed, n_segment) of a sequence under the full-precision sink/window policy."""
+    c = ctypes.c_int64()
+    g = ctypes.c_int32()
+    _check("aatc_segment_counts",
+           _L.aatc_segment_counts(int(n_tokens), int(sink), int(window), int(step),
+                                  ctypes.byref(c), ctypes.byref(g)))
+    return int(c.value), int(g.value)

@@ -252,6 +252,47 @@ extern "C" aatc_status aatc_append_decode_attention(
   }
 }
 
+extern "C" aatc_status aatc_decode_attention_segmented(
+    const void* dev_params_k, const void* dev_params_v, int32_t batch, int32_t n_q_heads,
+    int32_t n_kv_heads, int32_t d, const void* q, aatc_dtype q_dtype, const void* k_codes,
+    const uint16_t* k_alpha, const void* v_codes, const uint16_t* v_alpha,
+    const int32_t* seq_len, int64_t cap, int32_t k_record_bytes, int32_t v_record_bytes,
+    float softmax_scale, const void* seg_k, const void* seg_v, aatc_dtype seg_dtype,
+    const int32_t* seg_len, int32_t seg_cap, float* out, void* workspace, size_t ws_bytes,
+    void* stream) {
+  try {
+    const aatc_status e = check_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads,
+                                       d, q, q_dtype, k_codes, k_alpha, v_codes, v_alpha,
+                                       seq_len, cap, k_record_bytes, v_record_bytes,
+                                       softmax_scale, out, workspace, ws_bytes);
+    if (e != AATC_OK) return e;
+    if (!seg_k || !seg_v || !seg_len) return AATC_E_INVALID;
+    if (seg_dtype != AATC_F32 && seg_dtype != AATC_BF16) return AATC_E_INVALID;
+    if (seg_cap < 1 || seg_cap > 256) return AATC_E_INVALID;
+    const size_t sa = seg_dtype == AATC_F32 ? 4 : 2;
+    if (!aligned(seg_k, sa) || !aligned(seg_v, sa) || !aligned(seg_len, 4)) return AATC_E_INVALID;
+    return launch_decode(dev_params_k, dev_params_v, batch, n_q_heads, n_kv_heads, q, q_dtype,
+                         k_codes, k_alpha, v_codes, v_alpha, seq_len, cap, k_record_bytes,
+                         v_record_bytes, softmax_scale, out, workspace, stream, nullptr, nullptr,
+                         AATC_BF16, 0, seg_k, seg_v, seg_dtype, seg_len, seg_cap);
+  } catch (...) {
+    return AATC_E_INVALID;
+  }
+}
+
+extern "C" aatc_status aatc_segment_counts(int64_t n_tokens, int32_t sink, int32_t window,
+                                           int32_t step, int64_t* n_compressed,
+                                           int32_t* n_segment) {
+  if (!n_compressed || !n_segment) return AATC_E_INVALID;
+  if (n_tokens < 0 || sink < 0 || window < 1 || step < 1 || step > window)
+    return AATC_E_INVALID;
+  const int64_t m = n_tokens > sink ? n_tokens - sink : 0;    // tokens after the sink
+  const int64_t c = m < window ? 0 : (int64_t)step * ((m - window) / step + 1);
+  *n_compressed = c;
+  *n_segment = (int32_t)(n_tokens - c);
+  return AATC_OK;
+}
+
 extern "C" aatc_status aatc_append_decode_attention_noalloc(
     const void* dev_params_k, const void* dev_params_v, int32_t batch, int32_t n_q_heads,
     int32_t n_kv_heads, int32_t d, const void* q, aatc_dtype q_dtype, const void* x_k,

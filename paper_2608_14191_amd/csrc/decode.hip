@@ -65,6 +65,7 @@ struct DecodeArgs {
   unsigned* counters;
   Partial* partials;
   float* append_r;                // fused append: [rows][kAppStride] coefficients, bounds
+  const Partial* seg;             // full-precision segment partials [rows][G], or null
   int64_t cap;
   int n_q_heads, n_kv_heads, G, q_dtype;
   int n_splits, n_blocks;         // splits per (sequence, KV head); rows x splits
@@ -345,7 +346,7 @@ constexpr int kCtrStride = 64;
 constexpr int kAppStride = 2 * kD + 4;
 
 struct WsLayout {
-  size_t counters, partials, append_r, total;
+  size_t counters, partials, append_r, seg, total;
 };
 
 __host__ __device__ inline size_t round256(size_t x) { return (x + 255) / 256 * 256; }
@@ -362,7 +363,9 @@ inline WsLayout ws_layout(int batch, int n_q_heads, int n_kv_heads, int64_t cap,
   w.counters = 0;
   w.partials = round256(crows * kCtrStride * sizeof(unsigned));
   w.append_r = round256(w.partials + (size_t)batch * n_q_heads * n_splits * sizeof(Partial));
-  w.total = w.append_r + rows * kAppStride * sizeof(float);   // fused append, per row
+  // the full-precision segment's partial per (sequence, query head)
+  w.seg = round256(w.append_r + rows * kAppStride * sizeof(float));
+  w.total = w.seg + (size_t)batch * n_q_heads * sizeof(Partial);
   return w;
 }
 
@@ -791,6 +794,151 @@ __device__ __forceinline__ void merge_if_last_wide(const void* params_v, int kvh
 }
 
 // ---------------------------------------------------------------------------------------
+// Full-precision segment (the first tokens and the recent window kept at input precision,
+// Sec. 6 and App. E): exact softmax attention of each query head over the segment's tokens
+// in the original domain, one workgroup per (sequence, KV head), written as one more split
+// partial in the transformed domain (o~ = T_V^T sum_t p_t v_t, with the log2-domain maximum
+// and sum of its weights), which the merge of the compressed-cache splits folds in.
+// ---------------------------------------------------------------------------------------
+constexpr int kSegThreads = 256;
+constexpr int kSegMax = 256;           // tokens of one segment
+
+__global__ __launch_bounds__(kSegThreads) void segment_partial_kernel(
+    const void* __restrict__ params_v, int n_q_heads, int n_kv_heads,
+    const void* __restrict__ q, int q_dtype, const void* __restrict__ seg_k,
+    const void* __restrict__ seg_v, int seg_dtype, const int32_t* __restrict__ seg_len,
+    int seg_cap, float scale_log2e, Partial* __restrict__ seg_out) {
+  __shared__ float qs[kMaxGroup][kD];
+  __shared__ float z[kMaxGroup][kSegMax];
+  __shared__ float orw[kMaxGroup][kD];
+  __shared__ float red[kSegThreads / 64][kMaxGroup];
+  __shared__ float mh[kMaxGroup], lh[kMaxGroup];
+  const int row = blockIdx.x, kvh = row % n_kv_heads, seq = row / n_kv_heads;
+  const int G = n_q_heads / n_kv_heads;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = min(max(seg_len[seq], 0), seg_cap);
+  const int64_t tok0 = (int64_t)row * seg_cap;        // [batch][n_kv_heads][seg_cap][d]
+  for (int i = tid; i < G * kD; i += kSegThreads)
+    qs[i / kD][i % kD] =
+        load_q(q, q_dtype, ((int64_t)seq * n_q_heads + kvh * G) * kD + i) * scale_log2e;
+  __syncthreads();
+  // Logits: thread t takes token t for every head.
+  for (int t = tid; t < n; t += kSegThreads) {
+    float acc[kMaxGroup];
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h) acc[h] = 0.f;
+    for (int j = 0; j < kD; ++j) {
+      const float kv = load_elem(seg_k, seg_dtype, (tok0 + t) * kD + j);
+#pragma unroll
+      for (int h = 0; h < kMaxGroup; ++h)
+        if (h < G) acc[h] = fmaf(qs[h][j], kv, acc[h]);
+    }
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h)
+      if (h < G) z[h][t] = acc[h];
+  }
+  __syncthreads();
+  // Maximum and sum per head (the log2-domain weights 2^(z - m)).
+  for (int h = 0; h < G; ++h) {
+    float m = -INFINITY;
+    for (int t = tid; t < n; t += kSegThreads) m = fmaxf(m, z[h][t]);
+    m = wave_max_dpp(m);
+    if (lane == 0) red[wave][h] = m;
+  }
+  __syncthreads();
+  if (tid < G) {
+    float m = red[0][tid];
+    for (int w = 1; w < kSegThreads / 64; ++w) m = fmaxf(m, red[w][tid]);
+    mh[tid] = m;
+  }
+  __syncthreads();
+  for (int h = 0; h < G; ++h) {
+    float l = 0.f;
+    for (int t = tid; t < n; t += kSegThreads) {
+      const float p = exp2f(z[h][t] - mh[h]);
+      z[h][t] = p;
+      l += p;
+    }
+    l = wave_sum_dpp(l);
+    if (lane == 0) red[wave][h] = l;
+  }
+  __syncthreads();
+  if (tid < G) {
+    float l = 0.f;
+    for (int w = 0; w < kSegThreads / 64; ++w) l += red[w][tid];
+    lh[tid] = l;
+  }
+  // Value sums in the original domain: thread (half, j) over its half of the heads.
+  {
+    const int j = tid % kD, h0 = (tid / kD) * (kMaxGroup / 2);
+    float acc[kMaxGroup / 2];
+#pragma unroll
+    for (int i = 0; i < kMaxGroup / 2; ++i) acc[i] = 0.f;
+    for (int t = 0; t < n; ++t) {
+      const float vv = load_elem(seg_v, seg_dtype, (tok0 + t) * kD + j);
+#pragma unroll
+      for (int i = 0; i < kMaxGroup / 2; ++i)
+        if (h0 + i < G) acc[i] = fmaf(z[h0 + i][t], vv, acc[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < kMaxGroup / 2; ++i)
+      if (h0 + i < G) orw[h0 + i][j] = acc[i];
+  }
+  __syncthreads();
+  // Into the transformed domain of the merge: o~_c = sum_j T_V[j][c] o_j.
+  const HeadParams* hv = head_params(params_v, kvh);
+  Partial* out = seg_out + (int64_t)row * G;
+  {
+    const int c = tid % kD, h0 = (tid / kD) * (kMaxGroup / 2);
+    float acc[kMaxGroup / 2];
+#pragma unroll
+    for (int i = 0; i < kMaxGroup / 2; ++i) acc[i] = 0.f;
+    for (int j = 0; j < kD; ++j) {
+      const float t = hv->T[j * kD + c];
+#pragma unroll
+      for (int i = 0; i < kMaxGroup / 2; ++i)
+        if (h0 + i < G) acc[i] = fmaf(t, orw[h0 + i][j], acc[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < kMaxGroup / 2; ++i)
+      if (h0 + i < G) out[h0 + i].o[c] = acc[i];
+  }
+  if (tid < G) {
+    out[tid].m = n > 0 ? mh[tid] : -INFINITY;
+    out[tid].l = n > 0 ? lh[tid] : 0.f;
+  }
+}
+
+// The merging workgroup folds the segment's partial of its (sequence, KV head) into every
+// output element (written by segment_partial_kernel, which ran before this launch).
+struct SegHook {
+  const Partial* seg;                  // this row's G partials
+  __device__ void prefetch() {}
+  __device__ void during_loads() {}
+  __device__ void encode() {}
+  __device__ void publish() {}
+  __device__ void fold1(int h, int c, float& M, float& Ls, float& acc) const {
+    const float ms = seg[h].m;
+    if (ms == -INFINITY) return;
+    const float mn = fmaxf(M, ms);
+    const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
+    acc = acc * sa + seg[h].o[c] * sb;
+    Ls = Ls * sa + seg[h].l * sb;
+    M = mn;
+  }
+  __device__ void fold(int h, int c4, float& M, float& Ls, v4f& acc) const {
+    const float ms = seg[h].m;
+    if (ms == -INFINITY) return;
+    const float mn = fmaxf(M, ms);
+    const float sa = exp2f(M - mn), sb = exp2f(ms - mn);
+    acc = acc * sa + reinterpret_cast<const v4f*>(seg[h].o)[c4] * sb;
+    Ls = Ls * sa + seg[h].l * sb;
+    M = mn;
+  }
+  __device__ void finish() {}
+};
+
+// ---------------------------------------------------------------------------------------
 // Generic VALU kernel (any G <= 16, any budget).
 // ---------------------------------------------------------------------------------------
 // Fused append.  The splits stop short of the new token (position len - 1) and share its
@@ -1012,7 +1160,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
     const uint8_t* __restrict__ v_codes, const uint16_t* __restrict__ v_alpha,
     const int32_t* __restrict__ seq_len, int64_t cap, float scale, float* __restrict__ out,
     unsigned* __restrict__ counters, Partial* __restrict__ partials, int n_splits, int rk,
-    int rv) {
+    int rv, const Partial* __restrict__ seg) {
   extern __shared__ float dyn[];
   __shared__ float qs[kMaxGroup][kD];
   __shared__ float qp[kMaxGroup][kD];
@@ -1152,9 +1300,16 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
     st_dev(&part[tid].m, !layout_ok ? NAN : (nt > 0) ? mh[tid] : -INFINITY);
     st_dev(&part[tid].l, !layout_ok ? NAN : (nt > 0) ? lh[tid] : 0.f);
   }
-  NoHook none;
-  merge_if_last<kThreads, true>(params_v, kvh, kv_row, G, n_splits, partials, counters,
-                                out + ((int64_t)seq * n_q_heads + kvh * G) * kD, dyn, none);
+  float* out_rows = out + ((int64_t)seq * n_q_heads + kvh * G) * kD;
+  if (seg) {
+    SegHook sh{seg + kv_row * G};
+    merge_if_last<kThreads, true>(params_v, kvh, kv_row, G, n_splits, partials, counters,
+                                  out_rows, dyn, sh);
+  } else {
+    NoHook none;
+    merge_if_last<kThreads, true>(params_v, kvh, kv_row, G, n_splits, partials, counters,
+                                  out_rows, dyn, none);
+  }
 }
 
 // ---------------------------------------------------------------------------------------
@@ -2001,6 +2156,10 @@ void decode_mfma_kernel(const DecodeArgs a) {
     hook.sc = reinterpret_cast<AppendScratch*>(smem + a.off_es);
     merge_if_last_wide<NTHR, NH, kTvHeld>(a.params_v, kvh, row, G, a.n_splits, a.partials,
                                           a.counters, out_rows, merge_scratch, tv, hook);
+  } else if (a.seg) {
+    SegHook sh{a.seg + row * G};
+    merge_if_last_wide<NTHR, NH, kTvHeld>(a.params_v, kvh, row, G, a.n_splits, a.partials,
+                                          a.counters, out_rows, merge_scratch, tv, sh);
   } else {
     NoHook none;
     merge_if_last_wide<NTHR, NH, kTvHeld>(a.params_v, kvh, row, G, a.n_splits, a.partials,
@@ -2127,7 +2286,8 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
                           const uint16_t* v_alpha, const int32_t* seq_len, int64_t cap,
                           int rk, int rv, float softmax_scale, float* out, void* workspace,
                           void* stream, const void* x_k, const void* x_v, aatc_dtype x_dtype,
-                          int counter_rows) {
+                          int counter_rows, const void* seg_k, const void* seg_v,
+                          aatc_dtype seg_dtype, const int32_t* seg_len, int seg_cap) {
   const int G = n_q_heads / n_kv_heads;
   const WsLayout wl = ws_layout(batch, n_q_heads, n_kv_heads, cap, counter_rows);
   char* ws = static_cast<char*>(workspace);
@@ -2138,6 +2298,19 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
   if (cap * std::max(rk, rv) >= ((int64_t)1 << 31)) return AATC_E_UNSUPPORTED;
   if ((cap / kMinSplit + 1) * G * (int64_t)sizeof(Partial) >= ((int64_t)1 << 31))
     return AATC_E_UNSUPPORTED;
+  // The full-precision segment's partials first (stream order makes them visible to the
+  // merging workgroups of the launch below).
+  const Partial* seg = nullptr;
+  if (seg_k) {
+    if (seg_cap > kSegMax || x_k) return AATC_E_UNSUPPORTED;
+    Partial* sp = reinterpret_cast<Partial*>(ws + wl.seg);
+    hipLaunchKernelGGL(segment_partial_kernel, dim3((unsigned)(batch * n_kv_heads)),
+                       dim3(kSegThreads), 0, st, params_v, n_q_heads, n_kv_heads, q,
+                       (int)q_dtype, seg_k, seg_v, (int)seg_dtype, seg_len, seg_cap,
+                       softmax_scale * kLog2e, sp);
+    if (hipGetLastError() != hipSuccess) return AATC_E_DEVICE;
+    seg = sp;
+  }
   if (G <= kMaxNH && rk <= 64 && rv <= 64) {
     DecodeArgs a{};
     a.params_k = params_k;
@@ -2155,6 +2328,7 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
     a.counters = ctr;
     a.partials = parts;
     a.append_r = reinterpret_cast<float*>(ws + wl.append_r);
+    a.seg = seg;
     a.cap = cap;
     a.n_q_heads = n_q_heads;
     a.n_kv_heads = n_kv_heads;
@@ -2185,7 +2359,7 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
                      n_q_heads, n_kv_heads, q, (int)q_dtype,
                      static_cast<const uint8_t*>(k_codes), k_alpha,
                      static_cast<const uint8_t*>(v_codes), v_alpha, seq_len, cap,
-                     softmax_scale, out, ctr, parts, n_splits, rk, rv);
+                     softmax_scale, out, ctr, parts, n_splits, rk, rv, seg);
   return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
 }
 

@@ -35,7 +35,10 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
                           int k_record_bytes, int v_record_bytes, float softmax_scale,
                           float* out, void* workspace, void* stream,
                           const void* x_k = nullptr, const void* x_v = nullptr,
-                          aatc_dtype x_dtype = AATC_BF16, int counter_rows = 0);
+                          aatc_dtype x_dtype = AATC_BF16, int counter_rows = 0,
+                          const void* seg_k = nullptr, const void* seg_v = nullptr,
+                          aatc_dtype seg_dtype = AATC_BF16, const int32_t* seg_len = nullptr,
+                          int seg_cap = 0);
 
 // The static workspace of aatc_append_decode_attention_noalloc (noalloc.hip).
 constexpr size_t kScratchBytes = (size_t)32 << 20;
