@@ -117,6 +117,26 @@ aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int32_t d,
                            aatc_calibration* out);
 
 /*
+ * aatc_calibrate_bits -- aatc_calibrate with the widths given instead of allocated.
+ *
+ * For widths that come from one budget over several heads or layers (aatc_allocate_global,
+ * Sec. 5.2 and Alg. 1 "allocate bits globally"): the same covariance, transform, weights,
+ * storage order and scales as aatc_calibrate, with b_c = bits_eig[c] for the channel of
+ * the c-th largest eigenvalue.
+ *
+ * bits_eig      host [d] widths in eigen order (decreasing eigenvalue), each 0..8, sum >= 1.
+ * record_bytes  0 for the smallest record 4 * ceil(B / 32), else the record size to use
+ *               (a multiple of 4, at least that, at most 128): the heads of one tensor
+ *               whose budgets differ share the record size of the widest this way.
+ * Other arguments and errors as in aatc_calibrate (avg_bits and b_max are not taken).
+ */
+aatc_status aatc_calibrate_bits(const float* x_calib, int64_t n_calib, int32_t d,
+                                const float* q_calib, int64_t n_q, int32_t q_group,
+                                const float* w_o, int32_t d_out, const uint8_t* bits_eig,
+                                int32_t record_bytes, double percentile,
+                                aatc_calibration* out);
+
+/*
  * aatc_allocate_global -- integer widths of one tensor (keys or values) over all layers
  * under a single budget (host only).
  *
@@ -138,9 +158,10 @@ aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int32_t d,
  * normalize_weight  nonzero: the weights are scaled per layer as well (keys).
  * bits     host, caller-allocated [n_layers][m], fully written on success.
  * Errors: AATC_E_INVALID for NULL pointers, sizes or ranges, negative or non-finite
- * inputs, and budgets that no allocation in [0, b_max] meets.  The decode kernels take
- * one record width per call, so the heads of one layer must end with equal totals to
- * share a call.
+ * inputs, and budgets that no allocation in [0, b_max] meets.  A layer's heads may end with
+ * different totals: aatc_calibrate_bits gives each its widths, padded to one record size
+ * for the tensor (the largest 4 * ceil(B_h / 32) of the layer), which one parameter block
+ * and one decode call take.
  */
 aatc_status aatc_allocate_global(const double* sigma2, const double* weight,
                                  int32_t n_layers, int32_t m, double avg_bits,
@@ -153,10 +174,11 @@ aatc_status aatc_allocate_global(const double* sigma2, const double* weight,
  *
  * The block holds, per head, the transform (fp32 and as the integers T * 2^22), widths,
  * bit offsets, fp16 scales and their fp32 reciprocals, and bit-to-channel tables for the
- * decoder.  All heads of a tensor must have the same budget (so the same record size).
+ * decoder.  All heads of a tensor must have the same record size; their budgets may
+ * differ (each head's bits beyond its budget are zero padding).
  * The caller copies the `bytes` written to `host_buf` into device memory (16-byte
  * aligned) and passes that device pointer to aatc_encode / aatc_decode_attention.
- * Errors: AATC_E_INVALID (NULL, n_kv_heads < 1, bytes too small, budgets differ,
+ * Errors: AATC_E_INVALID (NULL, n_kv_heads < 1, bytes too small, record sizes differ,
  * malformed calibration, a transform entry off the 2^-22 grid or above 1 in magnitude).
  */
 size_t aatc_params_bytes(int32_t n_kv_heads);

@@ -238,17 +238,24 @@ class Calibration:
 
 def calibrate(x_calib: np.ndarray, avg_bits: float, b_max: int = 8,
               percentile: float = 0.99, q_calib: Optional[np.ndarray] = None,
-              group: int = 1, w_o: Optional[np.ndarray] = None) -> Calibration:
+              group: int = 1, w_o: Optional[np.ndarray] = None,
+              bits_eig: Optional[np.ndarray] = None,
+              record_bytes: Optional[int] = None) -> Calibration:
     """Alg. 1 (calibration) for one KV head and one tensor.
 
     ``q_calib`` (keys) or ``w_o`` (values) select the attention-aware weights; with
     neither, w = 1 (var-only).  The budget is B = round(avg_bits * d) bits per token.
+    With ``bits_eig`` the widths (eigen order) are given instead of allocated, as when one
+    budget is allocated over several heads and layers (``allocate_global``); then
+    ``avg_bits`` is not used.  ``record_bytes`` pads the records to a larger size (the heads
+    of one tensor share the record size of the widest).
     """
     x = np.asarray(x_calib, dtype=np.float64)
     n, d = x.shape
     if n < 2:
         raise ValueError("need at least 2 calibration samples")
-    budget = int(np.floor(avg_bits * d + 0.5))
+    budget = (int(np.sum(bits_eig)) if bits_eig is not None
+              else int(np.floor(avg_bits * d + 0.5)))
     p, lam = pca_basis(covariance(x))
     if q_calib is not None:
         w = key_weights(p, q_calib, group)
@@ -257,7 +264,9 @@ def calibrate(x_calib: np.ndarray, avg_bits: float, b_max: int = 8,
     else:
         w = np.ones(d)
     w_var = w * lam
-    bits_eig = allocate_bits(w_var, budget, b_max)
+    if bits_eig is None:
+        bits_eig = allocate_bits(w_var, budget, b_max)
+    bits_eig = np.asarray(bits_eig, dtype=np.int64)
     perm = np.argsort(-bits_eig, kind="stable")
     bits = bits_eig[perm]
     t64 = p[:, perm]
@@ -270,7 +279,11 @@ def calibrate(x_calib: np.ndarray, avg_bits: float, b_max: int = 8,
             s[c] = np.percentile(np.abs(h[:, c]), 100.0 * percentile)
     s16 = to_f16(s)
     s16[bits == 0] = 0
-    return Calibration(d=d, budget=budget, record_bytes=4 * ((budget + 31) // 32),
+    min_rb = 4 * ((budget + 31) // 32)
+    if record_bytes is not None and (record_bytes < min_rb or record_bytes % 4):
+        raise ValueError("record_bytes below the budget or not whole dwords")
+    return Calibration(d=d, budget=budget,
+                       record_bytes=min_rb if record_bytes is None else int(record_bytes),
                        d_active=int(np.count_nonzero(bits)), bits=bits, perm=perm,
                        T64=t64, T32=t32, s16=s16, sigma2=lam, weight=w,
                        bits_eig=bits_eig)
@@ -413,19 +426,19 @@ def dequantize(code: np.ndarray, alpha16: np.ndarray, bits: np.ndarray,
 # --------------------------------------------------------------------------------------
 # Packing (the paper does not specify one; this is the layout the path defines)
 # --------------------------------------------------------------------------------------
-def pack_records(code: np.ndarray, bits: np.ndarray) -> np.ndarray:
+def pack_records(code: np.ndarray, bits: np.ndarray, rbytes: Optional[int] = None) -> np.ndarray:
     """Token-major records: the codes of one token as one LSB-first bit string.
 
     Channel c (storage order) occupies bits [o_c, o_c + b_c) with o_c = sum of the
     earlier widths and holds the b_c-bit two's complement pattern of its code, least
     significant bit first; bit i of the record is bit i % 8 of byte i // 8.  The record
-    is zero-padded to R = 4 * ceil(B / 32) bytes.
+    is zero-padded to R = 4 * ceil(B / 32) bytes, or to ``rbytes`` if given.
     """
     code = np.asarray(code, dtype=np.int64)
     bits = np.asarray(bits, dtype=np.int64)
     n = code.shape[0]
     budget = int(bits.sum())
-    rbytes = 4 * ((budget + 31) // 32)
+    rbytes = 4 * ((budget + 31) // 32) if rbytes is None else int(rbytes)
     flat = np.zeros((n, 8 * rbytes), dtype=np.uint8)
     off = 0
     for c, b in enumerate(bits):
@@ -500,7 +513,7 @@ def encode(x32: np.ndarray, cal: Calibration):
     """Encode tokens [n, d] of one head: (records [n, R] uint8, alpha16 [n], codes [n, d])."""
     h = transform(x32, cal.T32)
     code, alpha16 = quantize(h, cal.bits, cal.s16)
-    return pack_records(code, cal.bits), alpha16, code
+    return pack_records(code, cal.bits, cal.record_bytes), alpha16, code
 
 
 def decode_tokens(rec: np.ndarray, alpha16: np.ndarray, cal: Calibration) -> np.ndarray:

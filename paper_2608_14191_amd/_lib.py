@@ -73,6 +73,9 @@ _L.aatc_status_string.argtypes = [ctypes.c_int]
 _L.aatc_calibrate.restype = ctypes.c_int
 _L.aatc_calibrate.argtypes = [_vp, _i64, _i32, _vp, _i64, _i32, _vp, _i32, _f64, _i32, _f64,
                               ctypes.POINTER(Calibration)]
+_L.aatc_calibrate_bits.restype = ctypes.c_int
+_L.aatc_calibrate_bits.argtypes = [_vp, _i64, _i32, _vp, _i64, _i32, _vp, _i32, _vp, _i32, _f64,
+                                   ctypes.POINTER(Calibration)]
 _L.aatc_params_bytes.restype = _sz
 _L.aatc_params_bytes.argtypes = [_i32]
 _L.aatc_params_pack.restype = ctypes.c_int
@@ -292,3 +295,19 @@ def aatc_segment_counts(n_tokens: int, sink: int = 4, window: int = 128, step: i
            _L.aatc_segment_counts(int(n_tokens), int(sink), int(window), int(step),
                                   ctypes.byref(c), ctypes.byref(g)))
     return int(c.value), int(g.value)
+
+
+def aatc_calibrate_bits(x_calib, bits_eig, record_bytes: int = 0, percentile: float = 0.99,
+                        q_calib=None, q_group: int = 1, w_o=None) -> Calibration:
+    """aatc_calibrate with the widths (eigen order) given, e.g. from aatc_allocate_global."""
+    x = np.ascontiguousarray(x_calib, dtype=np.float32)
+    b = np.ascontiguousarray(bits_eig, dtype=np.uint8)
+    q = None if q_calib is None else np.ascontiguousarray(q_calib, dtype=np.float32)
+    wo = None if w_o is None else np.ascontiguousarray(w_o, dtype=np.float32)
+    out = Calibration()
+    st = _L.aatc_calibrate_bits(_np_ptr(x), x.shape[0], x.shape[1], _np_ptr(q),
+                                0 if q is None else q.shape[0], int(q_group), _np_ptr(wo),
+                                0 if wo is None else wo.shape[1], _np_ptr(b), int(record_bytes),
+                                float(percentile), ctypes.byref(out))
+    _check("aatc_calibrate_bits", st)
+    return out

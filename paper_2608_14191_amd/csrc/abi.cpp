@@ -35,8 +35,11 @@ bool calibration_ok(const aatc_calibration& c) {
     sum += c.bits[i];
     if (c.bits[i]) ++active;
   }
+  // Records hold at least the budget, in whole dwords (more when the heads of one tensor
+  // share the record size of the widest).
   if (!(sum == c.budget_bits && active == c.d_active && sum > 0 &&
-        c.record_bytes == 4 * ((sum + 31) / 32)))
+        c.record_bytes >= 4 * ((sum + 31) / 32) && c.record_bytes % 4 == 0 &&
+        c.record_bytes <= kMaxBudget / 8))
     return false;
   // The stored transform: every entry a multiple of 2^-22 with magnitude at most 1.
   for (int i = 0; i < kD * kD; ++i) {
@@ -72,7 +75,7 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
     if (bytes < params_bytes(n_kv_heads)) return AATC_E_INVALID;
     for (int h = 0; h < n_kv_heads; ++h) {
       if (!calibration_ok(per_head[h])) return AATC_E_INVALID;
-      if (per_head[h].budget_bits != per_head[0].budget_bits) return AATC_E_INVALID;
+      if (per_head[h].record_bytes != per_head[0].record_bytes) return AATC_E_INVALID;
     }
     std::memset(host_buf, 0, params_bytes(n_kv_heads));
     auto* hdr = static_cast<TensorHeader*>(host_buf);

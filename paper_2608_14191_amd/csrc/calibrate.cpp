@@ -136,22 +136,40 @@ double percentile_linear(const std::vector<double>& sorted, double q) {
 
 using namespace aatc;
 
-extern "C" aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int32_t d,
-                                      const float* q_calib, int64_t n_q, int32_t q_group,
-                                      const float* w_o, int32_t d_out, double avg_bits,
-                                      int32_t b_max, double percentile,
-                                      aatc_calibration* out) {
+namespace {
+
+// The calibration of aatc_calibrate; with `bits_given` (eigen order) the widths are taken
+// as they are instead of allocated, and a nonzero `record_bytes_given` pads the records.
+aatc_status calibrate_impl(const float* x_calib, int64_t n_calib, int32_t d,
+                           const float* q_calib, int64_t n_q, int32_t q_group,
+                           const float* w_o, int32_t d_out, double avg_bits, int32_t b_max,
+                           const uint8_t* bits_given, int32_t record_bytes_given,
+                           double percentile, aatc_calibration* out) {
   try {
     if (!x_calib || !out) return AATC_E_INVALID;
     if (d != AATC_HEAD_DIM) return AATC_E_UNSUPPORTED;
     if (n_calib < 2 || b_max < 1 || b_max > AATC_MAX_BITS) return AATC_E_INVALID;
     if (!(percentile > 0.0 && percentile <= 1.0)) return AATC_E_INVALID;
-    if (!(avg_bits > 0.0) || !std::isfinite(avg_bits)) return AATC_E_INVALID;
     if (q_calib && w_o) return AATC_E_INVALID;
     if (q_calib && (q_group < 1 || n_q < q_group || n_q % q_group != 0)) return AATC_E_INVALID;
     if (w_o && d_out < 1) return AATC_E_INVALID;
-    const int64_t budget = (int64_t)std::floor(avg_bits * d + 0.5);
-    if (budget < 1 || budget > (int64_t)d * b_max) return AATC_E_INVALID;
+    int64_t budget = 0;
+    if (bits_given) {
+      for (int c = 0; c < d; ++c) {
+        if (bits_given[c] > b_max) return AATC_E_INVALID;
+        budget += bits_given[c];
+      }
+      if (budget < 1) return AATC_E_INVALID;
+    } else {
+      if (!(avg_bits > 0.0) || !std::isfinite(avg_bits)) return AATC_E_INVALID;
+      budget = (int64_t)std::floor(avg_bits * d + 0.5);
+      if (budget < 1 || budget > (int64_t)d * b_max) return AATC_E_INVALID;
+    }
+    const int32_t min_rb = (int32_t)(4 * ((budget + 31) / 32));
+    if (record_bytes_given != 0 &&
+        (record_bytes_given < min_rb || record_bytes_given % 4 != 0 ||
+         record_bytes_given > AATC_HEAD_DIM * AATC_MAX_BITS / 8))
+      return AATC_E_INVALID;
 
     const size_t n = (size_t)n_calib;
     for (size_t i = 0; i < n * d; ++i)
@@ -228,11 +246,13 @@ extern "C" aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int
       }
     }
 
-    // 4. Integer reverse water-filling: greedy marginal allocation.
+    // 4. Integer reverse water-filling: greedy marginal allocation (or the given widths).
     std::vector<double> wv(d);
     for (int c = 0; c < d; ++c) wv[c] = w[c] * lam[c];
     std::vector<int> b_eig(d, 0);
-    for (int64_t step = 0; step < budget; ++step) {
+    if (bits_given)
+      for (int c = 0; c < d; ++c) b_eig[c] = bits_given[c];
+    for (int64_t step = 0; !bits_given && step < budget; ++step) {
       int best = -1;
       double gbest = 0.0;
       for (int c = 0; c < d; ++c) {
@@ -252,7 +272,7 @@ extern "C" aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int
     std::memset(out, 0, sizeof(*out));
     out->d = d;
     out->budget_bits = (int32_t)budget;
-    out->record_bytes = (int32_t)(4 * ((budget + 31) / 32));
+    out->record_bytes = record_bytes_given ? record_bytes_given : min_rb;
     int d_active = 0;
     for (int c = 0; c < d; ++c) {
       int e = perm[c];
@@ -287,6 +307,27 @@ extern "C" aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int
   } catch (...) {
     return AATC_E_INVALID;
   }
+}
+
+}  // namespace
+
+extern "C" aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int32_t d,
+                                      const float* q_calib, int64_t n_q, int32_t q_group,
+                                      const float* w_o, int32_t d_out, double avg_bits,
+                                      int32_t b_max, double percentile,
+                                      aatc_calibration* out) {
+  return calibrate_impl(x_calib, n_calib, d, q_calib, n_q, q_group, w_o, d_out, avg_bits,
+                        b_max, nullptr, 0, percentile, out);
+}
+
+extern "C" aatc_status aatc_calibrate_bits(const float* x_calib, int64_t n_calib, int32_t d,
+                                           const float* q_calib, int64_t n_q, int32_t q_group,
+                                           const float* w_o, int32_t d_out,
+                                           const uint8_t* bits_eig, int32_t record_bytes,
+                                           double percentile, aatc_calibration* out) {
+  if (!bits_eig) return AATC_E_INVALID;
+  return calibrate_impl(x_calib, n_calib, d, q_calib, n_q, q_group, w_o, d_out, 0.0,
+                        AATC_MAX_BITS, bits_eig, record_bytes, percentile, out);
 }
 
 namespace aatc {

@@ -256,6 +256,35 @@ def test_noalloc_entry_point_rejects_oversized_requests():
     assert L.aatc_append_decode_attention_noalloc(*bad) == 1         # no new keys
 
 
+def test_calibrate_bits_matches_oracle_and_pads_records():
+    """aatc_calibrate_bits (widths given, eigen order) against the oracle's calibration
+    with the same widths; a padded record size is kept; params_pack takes heads with
+    different budgets that share one record size, and rejects record sizes that differ."""
+    w = workload(2, n_tokens=64)
+    rng = np.random.default_rng(31)
+    cals = []
+    for head, budget in ((0, 300), (1, 352), (2, 290)):
+        x = w.calib(head, "k")
+        bits = ora.allocate_bits(np.arange(128, 0, -1) ** 1.5 * rng.uniform(0.5, 1.5, 128),
+                                 budget, 8)
+        c = P.aatc_calibrate_bits(x, bits, record_bytes=44)
+        o = ora.calibrate(x, 0.0, bits_eig=bits, record_bytes=44)
+        np.testing.assert_array_equal(np.ctypeslib.as_array(c.bits_eig), bits)
+        np.testing.assert_array_equal(c.bits_np, o.bits)
+        np.testing.assert_array_equal(np.ctypeslib.as_array(c.perm), o.perm)
+        np.testing.assert_array_equal(c.s16.view(np.uint16), o.s16.view(np.uint16))
+        assert (c.budget_bits, c.record_bytes, c.d_active) == (o.budget, 44, o.d_active) == \
+            (budget, 44, int(np.count_nonzero(bits)))
+        cals.append(c)
+    P.aatc_params_pack(cals)                                  # budgets 300, 352, 290
+    with pytest.raises(P.AatcError):
+        P.aatc_calibrate_bits(w.calib(0, "k"), bits, record_bytes=32)   # 290 bits > 32 B
+    small = P.aatc_calibrate_bits(w.calib(0, "k"), ora.allocate_bits(np.ones(128), 100, 8))
+    assert small.record_bytes == 16
+    with pytest.raises(P.AatcError):
+        P.aatc_params_pack([cals[0], small])                  # record sizes differ
+
+
 def _global_cases():
     rng = np.random.default_rng(2024)
     ints = rng.integers(0, 4, size=(5, 16)).astype(np.float64)      # many exact ties

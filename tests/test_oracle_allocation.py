@@ -200,3 +200,24 @@ def test_global_rejects_unmeetable_budgets():
         aatc.allocate_global(s2, None, 0.5, 8, n_protect=3, protect_extra=1)
     with pytest.raises(ValueError):     # the pool exceeds b_max per channel
         aatc.allocate_global(s2, None, 8.5, 8, n_protect=0)
+
+
+def test_calibrate_with_given_bits_is_the_allocation():
+    """The oracle's calibration with its own greedy widths passed in is the calibration
+    itself; records padded to a larger size only add zero bytes."""
+    rng = np.random.default_rng(41)
+    x = rng.standard_normal((512, 128)) @ rng.standard_normal((128, 128))
+    a = aatc.calibrate(x, 2.75)
+    b = aatc.calibrate(x, 0.0, bits_eig=a.bits_eig)
+    np.testing.assert_array_equal(a.bits, b.bits)
+    np.testing.assert_array_equal(a.perm, b.perm)
+    np.testing.assert_array_equal(a.s16, b.s16)
+    assert (a.budget, a.record_bytes) == (b.budget, b.record_bytes) == (352, 44)
+    c = aatc.calibrate(x, 0.0, bits_eig=a.bits_eig, record_bytes=64)
+    xs = x[:20].astype(np.float32)
+    ra, aa, _ = aatc.encode(xs, a)
+    rc, ac, _ = aatc.encode(xs, c)
+    assert rc.shape == (20, 64)
+    np.testing.assert_array_equal(rc[:, :44], ra)
+    assert not rc[:, 44:].any()
+    np.testing.assert_array_equal(aa, ac)
