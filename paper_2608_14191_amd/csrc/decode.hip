@@ -1409,8 +1409,9 @@ void decode_mfma_kernel(const DecodeArgs a) {
   // Scale and width of the lane's channels 4 c4 + (NVL jq + i) % 4 (head (NVL jq + i) / 4).
   float ksq[NVL];
   int kbq[NVL];
-  // The channel tables: loaded up front by the plane-building waves, and by the issuing
-  // waves once their key transfers have landed (they use them only after the value phase).
+  // The channel tables (used only after the value phase): with eight waves every wave loads
+  // them after the join.  In the front they would queue behind the cache stream, and the
+  // wait before the join would then cover them.
   int vbc = 0, voc = 0, v_budget = 0;
   float vsc = 0.f;
   // Fused append: waves 0 and 1 encode the key and the value token, lane l channels l and
@@ -1448,7 +1449,6 @@ void decode_mfma_kernel(const DecodeArgs a) {
   int atq[KF][2];
   float a_inv_s[KF];
   auto front_loads = [&]() {
-    load_tables();
 #pragma unroll
     for (int i = 0; i < NVL; ++i) {
       const int c = 4 * c4 + ((NVL * jq + i) & 3);
@@ -1735,12 +1735,13 @@ void decode_mfma_kernel(const DecodeArgs a) {
       __builtin_amdgcn_s_waitcnt(kWaitVm0);
       issue_cache();
       wait_vmcnt(nv_mine);                           // key records and scales landed
-      load_tables();
     }
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     plain_barrier();
+    load_tables();
   } else {
     front_loads();
+    load_tables();
     if (tid < NH) qmx[tid] = 0u;
     if (tid == 0) csync = 0u;
     // Each wave issues its key records and token scales ahead of its value tiles.

@@ -25,6 +25,9 @@ namespace {
 
 constexpr int kEncThreads = 256;                 // four waves
 constexpr int kRecWords = kMaxBudget / 32;       // words of the largest record
+// LDS record rows are one word longer than the largest record, so that one word of many
+// rows (the tile transpose, the per-token bit fields) falls into different banks.
+constexpr int kRecStride = kRecWords + 1;
 constexpr int kSmallBatch = 16;                  // appends up to this many tokens: per-token kernel
 
 // This lane's two elements (lane, lane + 64) of a token.
@@ -34,10 +37,10 @@ __device__ inline void load_token_pair(const void* xrow, int dtype, float (&xl)[
   xl[1] = load_elem(xrow, dtype, lane + 64);
 }
 
-// Writes the records [lo, hi) of a 64-token tile from LDS rows (`rec`, rows of kRecWords
+// Writes the records [lo, hi) of a 64-token tile from LDS rows (`rec`, rows of kRecStride
 // words) into the cache in `layout`, and clears every LDS word it reads.  Tile bits of
 // tokens outside [lo, hi) keep their value in memory.
-__device__ inline void write_tile(uint32_t (*rec)[kRecWords], int lo, int hi, int rwords,
+__device__ inline void write_tile(uint32_t (*rec)[kRecStride], int lo, int hi, int rwords,
                                   int layout, uint8_t* codes, int64_t head, int64_t cap,
                                   int64_t tile, int nthreads) {
   const int tid = threadIdx.x;
@@ -77,7 +80,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
     int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
     int64_t cap, int64_t pos) {
-  __shared__ uint32_t rec[kTile][kRecWords];
+  __shared__ uint32_t rec[kTile][kRecStride];
   const int head = blockIdx.y;
   const HeadParams* hp = head_params(params, head);
   const int rwords = hp->record_bytes / 4;
@@ -86,7 +89,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
   const int64_t t_begin = max(tile_base, pos);
   const int64_t t_end = min(tile_base + kTile, pos + n_tok);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  for (int i = tid; i < kTile * kRecWords; i += kEncThreads) (&rec[0][0])[i] = 0u;
+  for (int i = tid; i < kTile * kRecStride; i += kEncThreads) (&rec[0][0])[i] = 0u;
   __syncthreads();
   for (int64_t t = t_begin + wave; t < t_end; t += kEncThreads / 64) {
     const void* xrow = static_cast<const char*>(x) +
@@ -218,7 +221,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
     int64_t cap, int64_t pos) {
   static_assert(kEncThreads == 256, "four waves of 16 tokens per 64-token tile");
   __shared__ __align__(16) int8_t tb[3][kTbBytes];       // [limb][ct][kc][lane][16]
-  __shared__ uint32_t rec[kTile][kRecWords];              // records of the tile's tokens
+  __shared__ uint32_t rec[kTile][kRecStride];              // records of the tile's tokens
   // Channel tables, read per tile by the lanes that hold channels 16 ct + 4 kg + i.
   __shared__ __align__(16) float tab_is[kD];              // 1 / s_c
   __shared__ __align__(16) float tab_k[kD];               // 2^(b_c - 1) / s_c (1 + 2^-20)
@@ -271,7 +274,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
   }
   if (tid < kD / 4)
     tab_w[tid] = hp->bits[4 * tid] + hp->bits[4 * tid + 1] + hp->bits[4 * tid + 2] + hp->bits[4 * tid + 3];
-  for (int i = tid; i < kTile * kRecWords; i += kEncThreads) (&rec[0][0])[i] = 0u;
+  for (int i = tid; i < kTile * kRecStride; i += kEncThreads) (&rec[0][0])[i] = 0u;
   if (tid == 0) fixmask = 0ull;
   const float inv_s_max = hp->inv_s_max;
   // Value tiles: lane p of a wave stands for tile bit position p (word p / 32, bit p % 32),
