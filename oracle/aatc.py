@@ -26,7 +26,10 @@ Encoding (Alg. 1, online part; Sec. 5.2), per token and head:
   6. h = T^T x (eq. transformed-cache): the exact product of the token with the stored
      transform, rounded once to fp32.
   7. alpha = max_c |h_c / s_c| over the stored channels; the signed uniform quantizer
-     with step Delta_c = 2 alpha s_c / 2^b_c (Sec. 5.2).
+     with step Delta_c = 2 alpha s_c / 2^b_c (Sec. 5.2), in one of two readings:
+     "midtread", the printed qtz/dqtz pair (levels k Delta), or "midrise", the
+     symmetric quantizer of Sec. 4's remark and App. B's noise model (levels
+     (k + 1/2) Delta, error at most half a step over the whole range).
   8. Bit packing of the codes (layout defined below; the paper is silent on it).
 Decode attention (Alg. 1, online part; Def. 1):
   9. Reconstruct K = H^ T^T and V = H^ T^T, then o = softmax(q K^T / sqrt(d)) V in fp64.
@@ -48,6 +51,13 @@ Readings where the paper is silent or ambiguous (each listed in the design doc)
   ``quantize``.  alpha and s_c are stored as fp16.
 * Storage order of channels: stable sort by bit width, widest first (eigen order
   breaks ties), so dropped channels form a suffix.
+* Quantizer: the printed formula (midtread) puts a level at 0, lets the top cell absorb
+  values up to a full step above the largest level, and at b = 1 has the levels
+  {-alpha s, 0}.  That contradicts the passages that call the quantizer symmetric with
+  errors of at most half a step (Sec. 4, the remark after Assumption 1; App. B, the
+  noise model).  The midrise reading satisfies them: code = clamp(floor(h / Delta),
+  -2^(b-1), 2^(b-1) - 1), h^ = (code + 1/2) Delta.  Both are offered; midtread is the
+  default.  Widths go up to b_max = 16 (App. E allows 0 to 16 bits per channel).
 
 Parity unpinned (spec choices with no value in the paper to check against): the
 percentile interpolation (linear between order statistics), the storage order and
@@ -65,6 +75,8 @@ import numpy as np
 T_FRAC_BITS = 22
 TILE_TOKENS = 64     # tokens per tile of the value-cache layout
 FP16_MAX = 65504.0
+MAX_BITS = 16        # widest channel code (App. E: 0 to 16 bits per channel)
+QUANTIZERS = ("midtread", "midrise")
 
 
 # --------------------------------------------------------------------------------------
@@ -234,13 +246,15 @@ class Calibration:
     sigma2: np.ndarray        # [d] eigenvalues, eigen order
     weight: np.ndarray        # [d] channel weights, eigen order
     bits_eig: np.ndarray      # [d] bits, eigen order
+    quantizer: str = "midtread"   # "midtread" (the printed formula) or "midrise"
 
 
 def calibrate(x_calib: np.ndarray, avg_bits: float, b_max: int = 8,
               percentile: float = 0.99, q_calib: Optional[np.ndarray] = None,
               group: int = 1, w_o: Optional[np.ndarray] = None,
               bits_eig: Optional[np.ndarray] = None,
-              record_bytes: Optional[int] = None) -> Calibration:
+              record_bytes: Optional[int] = None,
+              quantizer: str = "midtread") -> Calibration:
     """Alg. 1 (calibration) for one KV head and one tensor.
 
     ``q_calib`` (keys) or ``w_o`` (values) select the attention-aware weights; with
@@ -248,8 +262,13 @@ def calibrate(x_calib: np.ndarray, avg_bits: float, b_max: int = 8,
     With ``bits_eig`` the widths (eigen order) are given instead of allocated, as when one
     budget is allocated over several heads and layers (``allocate_global``); then
     ``avg_bits`` is not used.  ``record_bytes`` pads the records to a larger size (the heads
-    of one tensor share the record size of the widest).
+    of one tensor share the record size of the widest).  ``quantizer`` names the reading of
+    the quantizer that encode and decode use (it changes neither the widths nor the scales).
     """
+    if quantizer not in QUANTIZERS:
+        raise ValueError(f"quantizer must be one of {QUANTIZERS}")
+    if not 1 <= b_max <= MAX_BITS:
+        raise ValueError(f"b_max must be in 1..{MAX_BITS}")
     x = np.asarray(x_calib, dtype=np.float64)
     n, d = x.shape
     if n < 2:
@@ -286,7 +305,7 @@ def calibrate(x_calib: np.ndarray, avg_bits: float, b_max: int = 8,
                        record_bytes=min_rb if record_bytes is None else int(record_bytes),
                        d_active=int(np.count_nonzero(bits)), bits=bits, perm=perm,
                        T64=t64, T32=t32, s16=s16, sigma2=lam, weight=w,
-                       bits_eig=bits_eig)
+                       bits_eig=bits_eig, quantizer=quantizer)
 
 
 # --------------------------------------------------------------------------------------
@@ -380,14 +399,16 @@ def inverse_f32(v: np.ndarray) -> np.ndarray:
     return np.where(v != 0, np.float32(1) / safe, np.float32(0)).astype(np.float32)
 
 
-def quantize(h32: np.ndarray, bits: np.ndarray, s16: np.ndarray):
+def quantize(h32: np.ndarray, bits: np.ndarray, s16: np.ndarray, kind: str = "midtread"):
     """Signed uniform quantizer with per-token scale alpha (Sec. 5.2).
 
     For each token: alpha = max_c |h_c / s_c| over channels with b_c >= 1; with
     Delta_c = 2 alpha s_c / 2^b_c the code is clamp(floor(h_c / Delta_c + 1/2),
-    -2^(b-1), 2^(b-1) - 1).
+    -2^(b-1), 2^(b-1) - 1) (midtread, the printed formula) or clamp(floor(h_c / Delta_c),
+    -2^(b-1), 2^(b-1) - 1) (midrise, whose level is (code + 1/2) Delta_c).
     The canonical fp32 evaluation is r = h * (1/s), alpha16 = fp16(max |r|),
-    y = r * (1/alpha16), x = y * 2^(b-1), code = floor(x + 1/2) taken exactly.
+    y = r * (1/alpha16), x = y * 2^(b-1) (exact), code = floor(x + 1/2) taken exactly
+    (midtread) or floor(x) (midrise).
     Returns (code [n, d] int64 with 0 for dropped channels, alpha16 [n] fp16).
     """
     h = np.asarray(h32, dtype=np.float32)
@@ -404,7 +425,12 @@ def quantize(h32: np.ndarray, bits: np.ndarray, s16: np.ndarray):
     y = (r * inv_a[:, None]).astype(np.float32)
     x = np.ldexp(y, np.maximum(bits - 1, 0)[None, :]).astype(np.float32)
     f = np.floor(x)
-    code = f + ((x - f) >= np.float32(0.5))
+    if kind == "midrise":
+        code = f
+    elif kind == "midtread":
+        code = f + ((x - f) >= np.float32(0.5))
+    else:
+        raise ValueError(f"unknown quantizer {kind!r}")
     half = np.left_shift(1, np.maximum(bits - 1, 0))
     lo = np.where(keep, -half, 0)
     hi = np.where(keep, half - 1, 0)
@@ -413,14 +439,20 @@ def quantize(h32: np.ndarray, bits: np.ndarray, s16: np.ndarray):
 
 
 def dequantize(code: np.ndarray, alpha16: np.ndarray, bits: np.ndarray,
-               s16: np.ndarray) -> np.ndarray:
-    """h^_c = Delta_c * code_c = alpha s_c 2^(1-b_c) code_c; 0 for b_c = 0."""
+               s16: np.ndarray, kind: str = "midtread") -> np.ndarray:
+    """h^_c = Delta_c * code_c = alpha s_c 2^(1-b_c) code_c (midtread) or
+    Delta_c * (code_c + 1/2) (midrise); 0 for b_c = 0."""
     bits = np.asarray(bits, dtype=np.int64)
     keep = bits > 0
     s = np.asarray(s16, dtype=np.float16).astype(np.float64)
     a = np.asarray(alpha16, dtype=np.float16).astype(np.float64)
     step = np.where(keep, s * np.ldexp(1.0, 1 - bits), 0.0)
-    return a[:, None] * step[None, :] * np.asarray(code, dtype=np.float64)
+    level = np.asarray(code, dtype=np.float64)
+    if kind == "midrise":
+        level = level + 0.5
+    elif kind != "midtread":
+        raise ValueError(f"unknown quantizer {kind!r}")
+    return a[:, None] * step[None, :] * level
 
 
 # --------------------------------------------------------------------------------------
@@ -512,14 +544,14 @@ def tiles_to_records(tiles: np.ndarray, rbytes: int) -> np.ndarray:
 def encode(x32: np.ndarray, cal: Calibration):
     """Encode tokens [n, d] of one head: (records [n, R] uint8, alpha16 [n], codes [n, d])."""
     h = transform(x32, cal.T32)
-    code, alpha16 = quantize(h, cal.bits, cal.s16)
+    code, alpha16 = quantize(h, cal.bits, cal.s16, cal.quantizer)
     return pack_records(code, cal.bits, cal.record_bytes), alpha16, code
 
 
 def decode_tokens(rec: np.ndarray, alpha16: np.ndarray, cal: Calibration) -> np.ndarray:
     """Reconstructed tokens [n, d] in the original coordinates: x^ = T h^ (fp64), with the
     stored transform that encoded them."""
-    h = dequantize(unpack_records(rec, cal.bits), alpha16, cal.bits, cal.s16)
+    h = dequantize(unpack_records(rec, cal.bits), alpha16, cal.bits, cal.s16, cal.quantizer)
     return h @ np.asarray(cal.T32, dtype=np.float64).T
 
 

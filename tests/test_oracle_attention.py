@@ -107,3 +107,31 @@ def test_gqa_heads_read_their_kv_head():
         np.testing.assert_allclose(out[4 * h:4 * h + 4],
                                    aatc.softmax_attention(q[4 * h:4 * h + 4], kh, vh,
                                                           1 / np.sqrt(128)), rtol=1e-12)
+
+
+def test_midrise_grid_special_case():
+    """T = I and b = 12 (beyond the printed 8-bit setting; App. E allows 16) with the
+    midrise reading: each token's channel 0 is 1 (so alpha = 1, Delta = 2 / 2^b) and the
+    others sit on the midrise levels (code + 1/2) Delta.  Those decode exactly; channel 0
+    lands on the top level 1 - Delta / 2 (midrise has no level at alpha).  The attention
+    equals plain softmax attention over exactly that cache."""
+    rng = np.random.default_rng(3)
+    d, n, b = 8, 40, 12
+    half = 1 << (b - 1)
+    codes = rng.integers(-half, half, size=(n, d))
+    x = ((codes + 0.5) / half).astype(np.float32)
+    x[:, 0] = 1.0
+    cal = _identity_calibration(d, [b] * d, [1.0] * d)
+    cal.quantizer = "midrise"
+    rec, a16, code = aatc.encode(x, cal)
+    assert np.all(a16.astype(np.float64) == 1.0)
+    np.testing.assert_array_equal(code[:, 1:], codes[:, 1:])
+    assert np.all(code[:, 0] == half - 1)
+    expect = x.astype(np.float64)
+    expect[:, 0] = 1.0 - 0.5 / half
+    xh = aatc.decode_tokens(rec, a16, cal)
+    np.testing.assert_array_equal(xh, expect)
+    q = rng.standard_normal((2, d)).astype(np.float32)
+    out = aatc.decode_attention(q, [cal], [cal], [rec], [a16], [rec], [a16], n)
+    np.testing.assert_allclose(out, aatc.softmax_attention(q, expect, expect, 1 / np.sqrt(d)),
+                               rtol=1e-13)

@@ -191,3 +191,153 @@ def test_compression_arithmetic_matches_paper():
         g["llama_aatc_bytes"], rel=5e-3)
     per_token = g["llama_layers"] * g["llama_kv_heads"] * g["head_dim"] * 2 * 2
     assert g["llama_fp16_bytes"] / per_token == pytest.approx(8192, rel=0.02)
+
+
+# ---------------------------------------------------------------------------------------
+# The midrise reading (symmetric levels (code + 1/2) Delta; Sec. 4 remark, App. B noise
+# model) and widths up to 16 bits (App. E).
+# ---------------------------------------------------------------------------------------
+def test_midrise_worked_example_two_bits():
+    g = _golden("quantizer_midrise_example.json")["two_bit"]
+    h = np.array([g["h"]], dtype=np.float32)
+    bits = np.array(g["bits"])
+    c, a16 = aatc.quantize(h, bits, _f16(g["s"]), "midrise")
+    assert float(a16[0]) == g["alpha"]
+    assert c[0].tolist() == g["codes"]
+    c_mt, _ = aatc.quantize(h, bits, _f16(g["s"]), "midtread")
+    assert c_mt[0].tolist() == g["codes_midtread"]
+    rec = aatc.pack_records(c, bits)
+    assert rec[0].tobytes().hex() == g["record_bytes_hex"]
+    hh = aatc.dequantize(c, a16, bits, _f16(g["s"]), "midrise")
+    np.testing.assert_allclose(hh[0], g["h_hat"], atol=0)
+
+
+def test_midrise_worked_example_one_bit():
+    g = _golden("quantizer_midrise_example.json")["one_bit"]
+    h = np.array([g["h"]], dtype=np.float32)
+    bits = np.array(g["bits"])
+    c, a16 = aatc.quantize(h, bits, _f16(g["s"]), "midrise")
+    assert c[0].tolist() == g["codes"]
+    rec = aatc.pack_records(c, bits)
+    assert (np.unpackbits(rec[0], bitorder="little")[:2]).tolist() == g["stored"]
+    hh = aatc.dequantize(c, a16, bits, _f16(g["s"]), "midrise")
+    np.testing.assert_allclose(hh[0], g["h_hat"], atol=0)
+
+
+def _random_case16(seed, n=4000, d=24):
+    rng = np.random.default_rng(seed)
+    bits = np.sort(rng.integers(0, 17, size=d))[::-1]
+    s16 = _f16(rng.lognormal(0, 1, size=d))
+    s16[bits == 0] = 0
+    h = (rng.standard_normal((n, d)) * s16.astype(np.float64) *
+         rng.uniform(0.3, 1.2, size=(n, 1))).astype(np.float32)
+    return h, bits, s16
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_midrise_error_within_half_step_everywhere(seed):
+    """Midrise: |h - h^| <= Delta/2 for every element with |h / s| <= alpha16 (the top
+    cell included: no overload, Sec. 4 remark); elements above alpha16 (the fp16 rounding
+    of alpha) exceed it by at most that rounding.  Widths 0..16."""
+    h, bits, s16 = _random_case16(seed)
+    c, a16 = aatc.quantize(h, bits, s16, "midrise")
+    hh = aatc.dequantize(c, a16, bits, s16, "midrise")
+    keep = bits > 0
+    s = s16.astype(np.float64)
+    a = a16.astype(np.float64)
+    delta = 2 * a[:, None] * s[None, :] * 2.0 ** (-bits[None, :].astype(float))
+    err = np.abs(h.astype(np.float64) - hh)
+    ratio = np.abs(h.astype(np.float64)) / np.where(s > 0, s, 1.0)[None, :]
+    inside = keep[None, :] & (ratio <= a[:, None])
+    # (the fp32 evaluation of r / alpha adds ~2^-23 relative to the position in the cell)
+    tol = delta * 0.5 + a[:, None] * s[None, :] * 2.0 ** -20
+    assert np.all(err[inside] <= tol[inside])
+    over = keep[None, :] & ~inside
+    slack = (ratio - a[:, None]) * s[None, :]
+    assert np.all(err[over] <= (tol + slack)[over])
+    assert np.all(hh[:, ~keep] == 0)
+    half = np.where(keep, 1 << np.maximum(bits - 1, 0), 0)[None, :]
+    assert np.all((c >= -half) & (c < np.maximum(half, 1)))
+
+
+def test_midrise_levels_are_odd_and_b1_is_unbiased():
+    """Midrise levels are symmetric: h -> -h maps the level to minus itself (floor(-x) =
+    -floor(x) - 1 off the integers); at b = 1 the levels are +-alpha s / 2, so the mean
+    error over symmetric inputs vanishes (the printed formula's {-alpha s, 0} does not)."""
+    rng = np.random.default_rng(21)
+    n = 200000
+    for b in (1, 2, 3, 5, 8, 12, 16):
+        v = rng.uniform(-1, 1, n)
+        h = np.stack([np.ones(n), v, -v], axis=1).astype(np.float32)
+        bits = np.array([b, b, b])
+        s16 = _f16([1.0, 1.0, 1.0])
+        c, a16 = aatc.quantize(h, bits, s16, "midrise")
+        hh = aatc.dequantize(c, a16, bits, s16, "midrise")
+        x = h[:, 1].astype(np.float64) * 2.0 ** (b - 1)
+        off = x != np.floor(x)
+        np.testing.assert_array_equal(hh[off, 1], -hh[off, 2])
+    b = 1
+    v = rng.uniform(-1, 1, n)
+    h = np.stack([np.ones(n), v], axis=1).astype(np.float32)
+    for kind, biased in (("midrise", False), ("midtread", True)):
+        c, a16 = aatc.quantize(h, np.array([b, b]), _f16([1.0, 1.0]), kind)
+        hh = aatc.dequantize(c, a16, np.array([b, b]), _f16([1.0, 1.0]), kind)
+        mean_err = float(np.mean(hh[:, 1] - h[:, 1]))
+        if biased:
+            assert mean_err < -0.2               # levels {-1, 0}: mean error -1/2
+        else:
+            assert abs(mean_err) < 5e-3
+
+
+def test_midrise_noise_variance_is_delta_squared_over_12():
+    """Uniform inputs on [-alpha, alpha]: every midrise cell has width Delta and the level
+    at its centre, so MSE = Delta^2 / 12 exactly in the limit (App. B eq. noise-model),
+    for b = 1..16; it falls 4x per bit (Sec. 3.1)."""
+    rng = np.random.default_rng(10)
+    n = 400000
+    prev = None
+    for b in range(1, 17):
+        h = np.stack([np.ones(n), rng.uniform(-1, 1, n)], axis=1).astype(np.float32)
+        bits = np.array([b, b])
+        c, a16 = aatc.quantize(h, bits, _f16([1.0, 1.0]), "midrise")
+        hh = aatc.dequantize(c, a16, bits, _f16([1.0, 1.0]), "midrise")
+        mse = np.mean((h[:, 1].astype(np.float64) - hh[:, 1]) ** 2)
+        delta = 2.0 ** (1 - b)
+        assert mse == pytest.approx(delta ** 2 / 12, rel=0.01)
+        if prev is not None:
+            assert mse / prev == pytest.approx(0.25, rel=0.03)
+        prev = mse
+
+
+def test_sixteen_bit_records_roundtrip():
+    """Widths up to 16 (App. E): fields straddle words; the LSB-first bit string round
+    trips and the two's complement pattern of each code is what is stored."""
+    rng = np.random.default_rng(14)
+    bits = np.sort(rng.integers(0, 17, size=128))[::-1]
+    half = np.where(bits > 0, 1 << np.maximum(bits - 1, 0), 0)
+    c = rng.integers(-32768, 32768, size=(50, 128))
+    c = np.clip(c, -half[None, :], np.maximum(half - 1, 0)[None, :])
+    rec = aatc.pack_records(c, bits)
+    np.testing.assert_array_equal(aatc.unpack_records(rec, bits), c)
+    # the first channel's field, read back by hand from the bit string
+    b0 = int(bits[0])
+    flat = np.unpackbits(rec, axis=1, bitorder="little")
+    field = (flat[:, :b0].astype(np.int64) << np.arange(b0)).sum(axis=1)
+    np.testing.assert_array_equal(field, c[:, 0] & ((1 << b0) - 1))
+
+
+def test_allocation_with_sixteen_bit_cap():
+    """b_max = 16: the budget is spent exactly, no width exceeds 16, a dominant channel
+    takes more than 8 bits when its weighted variance calls for it, and the greedy result
+    attains the minimum of sum_c W_c 4^-b_c over every allocation (brute force)."""
+    import itertools
+    from oracle.aatc import allocate_bits, allocation_objective
+    w = np.array([4.0 ** 12, 1.0, 0.5, 0.25])
+    b = allocate_bits(w, 20, 16)
+    assert int(b.sum()) == 20 and b.max() <= 16 and b[0] > 8
+    best = min(allocation_objective(w, np.array(c))
+               for c in itertools.product(range(17), repeat=4) if sum(c) == 20)
+    assert allocation_objective(w, b) == pytest.approx(best, rel=1e-12)
+    # worked by hand: channel 0 wins every bit until 4^(12 - b0) reaches the others'
+    # gains, then the ties go to the lowest index: (15, 2, 2, 1)
+    assert b.tolist() == [15, 2, 2, 1]
