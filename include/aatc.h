@@ -8,7 +8,7 @@
  *
  * Conventions shared by every entry point:
  *   - Head dimension d is 128 (v1); other values return AATC_E_UNSUPPORTED.
- *   - Channel widths are 0..8 bits (b_max <= 8).
+ *   - Channel widths are 0..16 bits (b_max <= 16; App. E allows 0 to 16 bits).
  *   - "Device" pointers are HIP device memory owned by the caller; "host" pointers are
  *     ordinary host memory.  Device buffers are 16-byte aligned unless stated
  *     otherwise.  The library allocates no device memory, never frees
@@ -45,7 +45,7 @@ extern "C" {
 #endif
 
 #define AATC_HEAD_DIM 128
-#define AATC_MAX_BITS 8
+#define AATC_MAX_BITS 16
 #define AATC_TILE_TOKENS 64
 
 typedef enum {
@@ -62,6 +62,17 @@ typedef enum { AATC_F32 = 0, AATC_BF16 = 1, AATC_F16 = 2 } aatc_dtype;
 typedef enum { AATC_LAYOUT_RECORDS = 0, AATC_LAYOUT_TILES = 1 } aatc_layout;
 
 /*
+ * The two readings of the Sec. 5.2 quantizer (Delta = 2 alpha s_c / 2^b_c; codes stored
+ * as b-bit two's complement either way):
+ *   AATC_QUANT_MIDTREAD  the printed formula: code = clamp(floor(h / Delta + 1/2),
+ *                        -2^(b-1), 2^(b-1) - 1), level code * Delta;
+ *   AATC_QUANT_MIDRISE   the symmetric quantizer of Sec. 4's remark and App. B's noise
+ *                        model: code = clamp(floor(h / Delta), -2^(b-1), 2^(b-1) - 1),
+ *                        level (code + 1/2) Delta (error at most Delta / 2 everywhere).
+ */
+typedef enum { AATC_QUANT_MIDTREAD = 0, AATC_QUANT_MIDRISE = 1 } aatc_quantizer;
+
+/*
  * Calibration artifact of one (KV head, tensor), channels in storage order (widest
  * first; eigen order breaks ties, so zero-bit channels form a suffix).
  */
@@ -70,6 +81,9 @@ typedef struct {
   int32_t budget_bits;          /* B = sum of bits */
   int32_t record_bytes;         /* R = 4 * ceil(B / 32) */
   int32_t d_active;             /* channels with >= 1 bit */
+  int32_t quantizer;            /* aatc_quantizer: AATC_QUANT_MIDTREAD from the calibrate
+                                   entry points; set it before aatc_params_pack for the
+                                   midrise reading (widths and scales do not depend on it) */
   float transform[AATC_HEAD_DIM * AATC_HEAD_DIM]; /* row-major [j][c] = T_jc: column c
                                    is the unit eigenvector of storage channel c, stored
                                    on the 2^-22 grid (every entry a multiple of 2^-22,
@@ -104,7 +118,7 @@ typedef struct {
  * w_o      host [d][d_out] fp32 rows of W_O that read this head's values, or NULL.
  *          At most one of q_calib / w_o may be non-NULL.
  * avg_bits average bits per channel, 0 < avg_bits * d <= d * b_max.
- * b_max    1..8.
+ * b_max    1..16.
  * percentile in (0, 1], 0.99 in the paper.
  * out      host, caller-allocated, fully written on success.
  * Errors: AATC_E_INVALID for NULL/size/range problems, AATC_E_UNSUPPORTED for
@@ -124,9 +138,9 @@ aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int32_t d,
  * storage order and scales as aatc_calibrate, with b_c = bits_eig[c] for the channel of
  * the c-th largest eigenvalue.
  *
- * bits_eig      host [d] widths in eigen order (decreasing eigenvalue), each 0..8, sum >= 1.
+ * bits_eig      host [d] widths in eigen order (decreasing eigenvalue), each 0..16, sum >= 1.
  * record_bytes  0 for the smallest record 4 * ceil(B / 32), else the record size to use
- *               (a multiple of 4, at least that, at most 128): the heads of one tensor
+ *               (a multiple of 4, at least that, at most 256): the heads of one tensor
  *               whose budgets differ share the record size of the widest this way.
  * Other arguments and errors as in aatc_calibrate (avg_bits and b_max are not taken).
  */

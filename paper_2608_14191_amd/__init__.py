@@ -4,7 +4,8 @@ The compute path lives in libaatc.so (host C++ calibration + HIP kernels for gfx
 behind the C ABI of include/aatc.h; ``_lib`` binds it with the same function names.
 """
 from ._lib import (  # noqa: F401
-    BF16, F32, HEAD_DIM, LAYOUT_RECORDS, LAYOUT_TILES, MAX_BITS, TILE_TOKENS,
+    BF16, F32, HEAD_DIM, LAYOUT_RECORDS, LAYOUT_TILES, MAX_BITS, QUANT_MIDRISE,
+    QUANT_MIDTREAD, TILE_TOKENS,
     AatcError, Calibration,
     aatc_allocate_global, aatc_append_decode_attention, aatc_append_decode_attention_noalloc,
     aatc_calibrate, aatc_calibrate_bits, aatc_decode_attention, aatc_decode_attention_segmented,

@@ -16,10 +16,11 @@ import numpy as np
 from .build import LIB
 
 HEAD_DIM = 128
-MAX_BITS = 8
+MAX_BITS = 16
 TILE_TOKENS = 64
 
 OK, E_INVALID, E_UNSUPPORTED, E_NUMERIC, E_DEVICE, E_WORKSPACE = range(6)
+QUANT_MIDTREAD, QUANT_MIDRISE = 0, 1
 F32, BF16, F16 = 0, 1, 2
 LAYOUT_RECORDS, LAYOUT_TILES = 0, 1
 
@@ -38,6 +39,7 @@ class Calibration(ctypes.Structure):
         ("budget_bits", ctypes.c_int32),
         ("record_bytes", ctypes.c_int32),
         ("d_active", ctypes.c_int32),
+        ("quantizer", ctypes.c_int32),
         ("transform", ctypes.c_float * (HEAD_DIM * HEAD_DIM)),
         ("bits", ctypes.c_uint8 * HEAD_DIM),
         ("scale_f16", ctypes.c_uint16 * HEAD_DIM),

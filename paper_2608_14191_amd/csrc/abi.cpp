@@ -1,5 +1,6 @@
 // C ABI entry points: argument validation, parameter-block packing and dispatch to
 // the HIP launchers.  No exception crosses the boundary.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 
@@ -28,6 +29,7 @@ float bf16_to_f32(uint16_t h) {
 
 bool calibration_ok(const aatc_calibration& c) {
   if (c.d != kD) return false;
+  if (c.quantizer != AATC_QUANT_MIDTREAD && c.quantizer != AATC_QUANT_MIDRISE) return false;
   int sum = 0, active = 0, prev = kMaxBits;
   for (int i = 0; i < kD; ++i) {
     if (c.bits[i] > kMaxBits || c.bits[i] > prev) return false;   // non-increasing
@@ -76,6 +78,7 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
     for (int h = 0; h < n_kv_heads; ++h) {
       if (!calibration_ok(per_head[h])) return AATC_E_INVALID;
       if (per_head[h].record_bytes != per_head[0].record_bytes) return AATC_E_INVALID;
+      if (per_head[h].quantizer != per_head[0].quantizer) return AATC_E_INVALID;
     }
     std::memset(host_buf, 0, params_bytes(n_kv_heads));
     auto* hdr = static_cast<TensorHeader*>(host_buf);
@@ -102,7 +105,7 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
           hp->Tqt[ch * kD + j] =
               (int32_t)std::ldexp((double)c.transform[j * kD + ch], kTFrac);   // exact
       float inv_s_max = 0.f;
-      int off = 0;
+      int off = 0, max_bits = 0;
       for (int ch = 0; ch < kD; ++ch) {
         const int b = c.bits[ch];
         hp->bits[ch] = (uint8_t)b;
@@ -113,13 +116,15 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
         // fp32 1/s correctly rounded: the fp64 quotient of an 11-bit divisor rounds
         // to fp32 without a double-rounding error.
         hp->inv_s[ch] = (b && s > 0.0) ? (float)(1.0 / s) : 0.0f;
+        hp->half_step[ch] = (b && c.quantizer == AATC_QUANT_MIDRISE) ? std::ldexp(1.0f, -b) : 0.0f;
+        max_bits = std::max(max_bits, b);
         inv_s_max = std::fmax(inv_s_max, hp->inv_s[ch]);
         for (int k = 0; k < b; ++k) {
           const int v = off + k;
           hp->virt_chan[v] = (uint8_t)ch;
           hp->virt_bit[v] = (uint8_t)k;
           hp->bit_desc[((v >> 5) * 8 + (v & 7)) * 4 + ((v >> 3) & 3)] =
-              (uint16_t)(0x8000 | (k == b - 1 ? 0x4000 : 0) | ((8 + k + 1 - b) << 8) | ch);
+              (uint16_t)(0x8000 | (k == b - 1 ? 0x4000 : 0) | ((kDescBias + k + 1 - b) << 8) | ch);
         }
         off += b;
       }
@@ -127,6 +132,8 @@ extern "C" aatc_status aatc_params_pack(const aatc_calibration* per_head, int32_
       hp->budget = c.budget_bits;
       hp->record_bytes = c.record_bytes;
       hp->inv_s_max = inv_s_max;
+      hp->quantizer = c.quantizer;
+      hp->max_bits = max_bits;
     }
     return AATC_OK;
   } catch (...) {

@@ -1069,16 +1069,17 @@ struct AppendHook {
       for (int i = 0; i < 2; ++i) m = fmaxf(m, e_b[i] > 0 ? fabsf(r2[i]) : 0.f);
       const __half a16 = token_alpha(wave_max_dpp(m));
       const float inv = inverse_alpha(a16);
-      int code[2];
+      const bool midrise = ep->quantizer == AATC_QUANT_MIDRISE;
+      float code[2];                   // the level in steps: code, or code + 1/2 (midrise)
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        code[i] = 0;
+        code[i] = 0.f;
         const int eb = e_b[i], eoff = e_off[i];
         if (eb > 0) {
-          const uint32_t u = quantize_code(r2[i], inv, eb);
+          const uint32_t u = quantize_code(r2[i], inv, eb, midrise);
           atomicOr(&sc->erec[et][eoff >> 5], u << (eoff & 31));
           if ((eoff & 31) + eb > 32) atomicOr(&sc->erec[et][(eoff >> 5) + 1], u >> (32 - (eoff & 31)));
-          code[i] = (int)(u << (32 - eb)) >> (32 - eb);      // sign-extended b-bit code
+          code[i] = (float)((int)(u << (32 - eb)) >> (32 - eb)) + (midrise ? 0.5f : 0.f);
         }
       }
       const float af = __half2float(a16);
@@ -1089,7 +1090,7 @@ struct AppendHook {
           z[h] = 0.f;
 #pragma unroll
           for (int i = 0; i < 2; ++i)
-            z[h] += e_b[i] ? qk[i][h] * ldexpf((float)code[i], 1 - e_b[i]) : 0.f;
+            z[h] += e_b[i] ? qk[i][h] * ldexpf(code[i], 1 - e_b[i]) : 0.f;
         }
         wave_sum_n(z);
 #pragma unroll
@@ -1098,7 +1099,7 @@ struct AppendHook {
       } else {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
-          sc->vnew[lane + 64 * i] = e_b[i] ? ldexpf(af * e_s[i] * (float)code[i], 1 - e_b[i]) : 0.f;
+          sc->vnew[lane + 64 * i] = e_b[i] ? ldexpf(af * e_s[i] * code[i], 1 - e_b[i]) : 0.f;
       }
       if (lane == 0) sc->ea16[et] = __half_as_ushort(a16);
     }
@@ -1166,6 +1167,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
   __shared__ float qp[kMaxGroup][kD];
   __shared__ float red[kThreads / 64];
   __shared__ float mh[kMaxGroup], lh[kMaxGroup];
+  __shared__ float chq[kMaxGroup];      // midrise: the half-step term of the scores
+  __shared__ float wh[kMaxGroup];       // sum over the split of P alpha^V
 
   const int split = blockIdx.x, kvh = blockIdx.y, seq = blockIdx.z;
   const int G = n_q_heads / n_kv_heads;
@@ -1174,8 +1177,9 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
   const HeadParams* hv = head_params(params_v, kvh);
   const bool layout_ok = hk->record_bytes == rk && hv->record_bytes == rv;
   const int bk = hk->budget, bv = hv->budget;
+  const int VS = 8 * max(rk, rv);                   // record bits of the wider tensor
   float* sc = dyn;                                  // [G][kSplit] logits, then weights
-  float* vq = dyn + G * kSplit;                     // [G][kMaxBudget] per-bit weights / sums
+  float* vq = dyn + G * kSplit;                     // [G][VS] per-bit weights / sums
 
   const int len = (int)min<int64_t>(max(seq_len[seq], 0), cap);   // out-of-range lengths clamp
   const int t0 = split * kSplit;
@@ -1199,7 +1203,14 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
     const int h = i / bk, v = i % bk;
     const int c = hk->virt_chan[v], k = hk->virt_bit[v];
     const float w = ldexpf(qp[h][c], k);
-    vq[h * kMaxBudget + v] = (k == hk->bits[c] - 1) ? -w : w;
+    vq[h * VS + v] = (k == hk->bits[c] - 1) ? -w : w;
+  }
+  // Midrise levels (code + 1/2) add (1/2) sum_c q'_c to every score (before alpha^K).
+  if (tid < G) {
+    float a = 0.f;
+    if (hk->quantizer == AATC_QUANT_MIDRISE)
+      for (int c = 0; c < kD; ++c) a += qp[tid][c];
+    chq[tid] = 0.5f * a;
   }
   __syncthreads();
 
@@ -1219,13 +1230,13 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
           bits &= bits - 1;
 #pragma unroll
           for (int h = 0; h < kMaxGroup; ++h)
-            if (h < G) acc[h] += vq[h * kMaxBudget + v];
+            if (h < G) acc[h] += vq[h * VS + v];
         }
       }
       const float ak = half_bits_to_float(k_alpha[kv_row * cap + t]);
 #pragma unroll
       for (int h = 0; h < kMaxGroup; ++h)
-        if (h < G) sc[h * kSplit + tl] = ak * acc[h];
+        if (h < G) sc[h * kSplit + tl] = ak * (acc[h] + chq[h]);
     } else {
       for (int h = 0; h < G; ++h) sc[h * kSplit + tl] = -INFINITY;
     }
@@ -1245,9 +1256,13 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
       l += p;
     }
     l = block_reduce(l, false, red);
+    float ws = 0.f;
+    for (int tl = tid; tl < nt; tl += kThreads) ws += sc[h * kSplit + tl];
+    ws = block_reduce(ws, false, red);
     if (tid == 0) {
       mh[h] = m;
       lh[h] = l;
+      wh[h] = ws;
     }
   }
   __syncthreads();
@@ -1276,7 +1291,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
     }
 #pragma unroll
     for (int h = 0; h < kMaxGroup; ++h)
-      if (h < G) vq[h * kMaxBudget + v] = acc[h];
+      if (h < G) vq[h * VS + v] = acc[h];
   }
   __syncthreads();
 
@@ -1289,10 +1304,11 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(
     if (b && nt > 0) {
       float acc = 0.f;
       for (int k = 0; k < b; ++k) {
-        const float t = ldexpf(vq[h * kMaxBudget + hv->bit_off[c] + k], k);
+        const float t = ldexpf(vq[h * VS + hv->bit_off[c] + k], k);
         acc += (k == b - 1) ? -t : t;
       }
-      o = hv->s[c] * ldexpf(acc, 1 - b);
+      // (midrise: the half step of every level, s_c 2^(-b_c) sum_t P_t alpha^V_t)
+      o = fmaf(hv->s[c] * hv->half_step[c], wh[h], hv->s[c] * ldexpf(acc, 1 - b));
     }
     st_dev(&part[h].o[c], o);
   }
@@ -1371,6 +1387,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
   __shared__ int fexp_s[NH];
   __shared__ float wmax[NW][NH], wsum[NW][NH], wpa[NW][NH];
   __shared__ int fv_s[NH];
+  __shared__ float chs[NH];           // midrise: the half-step term of each head's scores
+  __shared__ float wpav[NW][NH];      // sum of P alpha^V per wave and head
   __shared__ unsigned csync;          // arrivals of the plane-building waves
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1409,11 +1427,12 @@ void decode_mfma_kernel(const DecodeArgs a) {
   // Scale and width of the lane's channels 4 c4 + (NVL jq + i) % 4 (head (NVL jq + i) / 4).
   float ksq[NVL];
   int kbq[NVL];
+  float khs[2];                       // key half steps of channels lane and lane + 64
   // The channel tables (used only after the value phase): with eight waves every wave loads
   // them after the join.  In the front they would queue behind the cache stream, and the
   // wait before the join would then cover them.
-  int vbc = 0, voc = 0, v_budget = 0;
-  float vsc = 0.f;
+  int vbc = 0, voc = 0, v_budget = 0, v_maxb = 0;
+  float vsc = 0.f, vhs = 0.f;
   // Fused append: waves 0 and 1 encode the key and the value token, lane l channels l and
   // l + 64 (their widths, first bits and scales).
   int e_b[2] = {0, 0}, e_off[2] = {0, 0};
@@ -1432,6 +1451,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
     vbc = hv->bits[cq];
     voc = hv->bit_off[cq];
     vsc = hv->s[cq];
+    vhs = hv->half_step[cq];
+    v_maxb = hv->max_bits;
   };
   v4f tr[RJ];
   uint2 desc[NPI];
@@ -1458,6 +1479,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
 #pragma unroll
     for (int jj = 0; jj < RJ; ++jj)
       tr[jj] = reinterpret_cast<const v4f*>(hk->T)[(RJ * jq + jj) * (kD / 4) + c4];
+    khs[0] = hk->half_step[lane];
+    khs[1] = hk->half_step[lane + 64];
     // Plane items (head, record dword D, bit d of each byte): the 4 record bits 32 D +
     // 8 j + d, j = 0..3, of one head.
 #pragma unroll
@@ -1630,6 +1653,12 @@ void decode_mfma_kernel(const DecodeArgs a) {
       if ((lane & (NH == 4 ? 15 : 7)) == 0) atomicMax(&qmx[hl], __float_as_uint(mloc));
     }
     plane_sync();                                    // qcl, qmx
+    // Midrise: every score has the term alpha^K C_h with C_h = sum_c Q_c 2^(-b_c) over the
+    // stored channels (the half step of each level); 0 for the midtread reading.
+    for (int h = wave % NWC; h < NH; h += NWC) {
+      const float cp = wave_sum_dpp(qcl[h * kD + lane] * khs[0] + qcl[h * kD + lane + 64] * khs[1]);
+      if (lane == 0) chs[h] = cp;
+    }
     if (tid < NH) {
       int e = 0;
       frexpf(__uint_as_float(qmx[tid]), &e);
@@ -1683,7 +1712,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const uint32_t ent = ((j < 2 ? desc[r].x : desc[r].y) >> (16 * (j & 1))) & 0xffffu;
-        int fx = (int)rintf(ldexpf(qv_[r][j], (int)((ent >> 8) & 15) - 8 + fe - d));
+        int fx = (int)rintf(ldexpf(qv_[r][j], (int)((ent >> 8) & 15) - kDescBias + fe - d));
         if ((((ent >> 14) & 1) != 0) != (d == 7)) fx = -fx;
         x[j] = (ent & 0x8000u) ? pack_limbs(fx) : 0u;
       }
@@ -1777,14 +1806,15 @@ void decode_mfma_kernel(const DecodeArgs a) {
     __syncthreads();
   }
   v4i bq[NT][2 * NP];
-  int fex[NT];
+  float sfx[NT], chk[NT];
 #pragma unroll
   for (int rt = 0; rt < NT; ++rt) {
     const int h = 4 * rt + hc;
 #pragma unroll
     for (int s = 0; s < 2 * NP; ++s)
       bq[rt][s] = *reinterpret_cast<const v4i*>(ql + ((L * NH + h) * 2 * NP + s) * 64 + 16 * g);
-    fex[rt] = fexp_s[4 * rt + g];        // (the head of this lane's scores)
+    sfx[rt] = ldexpf(1.f, -fexp_s[4 * rt + g]);   // (the head of this lane's scores)
+    chk[rt] = chs[4 * rt + g];
   }
   // Q_c of every head for channels lane and lane + 64, for the fused append's key token
   // (eight waves: the planes' scratch is intact until the softmax writes the value
@@ -1868,7 +1898,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
         float f = fmaf((float)d[3], 256.f, (float)d[2]);
         f = fmaf(f, 256.f, (float)d[1]);
         f = fmaf(f, 256.f, (float)d[0]);
-        zr[tt][rt] = (tok_ok && 4 * rt + g < G) ? ldexpf(f * ak, -fex[rt]) : -INFINITY;
+        zr[tt][rt] = (tok_ok && 4 * rt + g < G) ? fmaf(f, sfx[rt], chk[rt]) * ak : -INFINITY;
       }
     }
   }
@@ -1923,7 +1953,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
   v4i* pb = reinterpret_cast<v4i*>(smem + a.off_pb);  // [NCH][NT][64] value operands
 #pragma unroll
   for (int rt = 0; rt < NT; ++rt) {
-    float lsum = 0.f;
+    float lsum = 0.f, pasum = 0.f;
 #pragma unroll
     for (int ch = 0; ch < CPW; ++ch) {
       uint32_t y[4];
@@ -1934,6 +1964,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
         // (the hardware exp2: results below 2^-126 flush to 0, below any weight that counts)
         const float p = (z == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(z - mh[rt]);
         lsum += p;
+        pasum = fmaf(p, avt[tt], pasum);
         const int fx = (int)rintf(p * avt[tt] * ((qd & 1) ? sc_odd[rt] : sc_even[rt]));
         uint32_t x = pack_limbs(fx);
         // quad byte transpose: (token L, limbs 0..3) -> (limb L, tokens 0..3)
@@ -1946,7 +1977,11 @@ void decode_mfma_kernel(const DecodeArgs a) {
           (v4i){(int)y[0], (int)y[1], (int)y[2], (int)y[3]};
     }
     lsum = row16_sum(lsum);
-    if (n == 0) wsum[wave][4 * rt + g] = lsum;
+    pasum = row16_sum(pasum);
+    if (n == 0) {
+      wsum[wave][4 * rt + g] = lsum;
+      wpav[wave][4 * rt + g] = pasum;
+    }
   }
   // The value tiles: the issuing waves wait for the rest of their transfers, or every
   // wave stores its registers (their region held nothing since the query transform).
@@ -2098,20 +2133,24 @@ void decode_mfma_kernel(const DecodeArgs a) {
     }
   }
   // (7) Partial: o~_c = s_c 2^(1-b_c-fv) (sum_{k < b-1} 2^k O'(c,k) - 2^(b-1) O'(c,b-1)),
-  //     one (head, channel) per thread.
+  //     one (head, channel) per thread; midrise adds s_c 2^(-b_c) sum_i P_i alpha^V_i
+  //     (the half step of every level).
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
     const int h = (r * NTHR + tid) / kD;
     if (h < G) {
       const float* oh = ob + h * a.ob_stride;
       float acc = 0.f;
-#pragma unroll
-      for (int k = 0; k < kMaxBits; ++k) {
+#pragma unroll 8
+      for (int k = 0; k < v_maxb; ++k) {
         const int v = min(voc + k, 8 * RV - 1);
         const float t = ldexpf(kHalves ? oh[v] + oh[NH * a.ob_stride + v] : oh[v], k);
         acc += (k < vbc) ? ((k == vbc - 1) ? -t : t) : 0.f;
       }
-      const float o = vbc ? ldexpf(vsc * acc, 1 - vbc - fv_s[h]) : 0.f;
+      float pa = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) pa += wpav[w][h];
+      const float o = vbc ? fmaf(vsc * vhs, pa, ldexpf(vsc * acc, 1 - vbc - fv_s[h])) : 0.f;
       buf_store4_coherent(o, prs, (uint32_t)((split * G + h) * sizeof(Partial) + 16 + 4 * cq));
     }
   }
@@ -2351,7 +2390,8 @@ aatc_status launch_decode(const void* params_k, const void* params_v, int batch,
     if (e != AATC_OK) return e;
   }
   const int n_splits = (int)((cap + kSplit - 1) / kSplit);
-  size_t lds = std::max((size_t)G * (kSplit + kMaxBudget) * sizeof(float), merge_lds_bytes(G, kThreads));
+  size_t lds = std::max((size_t)G * (kSplit + 8 * std::max(rk, rv)) * sizeof(float),
+                        merge_lds_bytes(G, kThreads));
   if (lds > 160 * 1024 - 24 * 1024) return AATC_E_UNSUPPORTED;
   static LdsLimit limit;
   if (!limit.ensure((const void*)decode_split_kernel, lds)) return AATC_E_DEVICE;

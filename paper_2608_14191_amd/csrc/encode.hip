@@ -73,24 +73,19 @@ __device__ inline void write_tile(uint32_t (*rec)[kRecStride], int lo, int hi, i
   }
 }
 
-// Any layout, any token count: one workgroup per (64-token tile, KV head); wave w encodes
-// the tile's tokens w, w + 4, ... with the exact one-wave routine, into LDS records that
-// the workgroup then writes out.
-__global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
-    const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
-    int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
-    int64_t cap, int64_t pos) {
-  __shared__ uint32_t rec[kTile][kRecStride];
-  const int head = blockIdx.y;
-  const HeadParams* hp = head_params(params, head);
+// One 64-token tile by a workgroup of kEncThreads threads: wave w encodes the tile's
+// tokens w, w + 4, ... with the exact one-wave routine into the LDS rows `rec` (zero on
+// entry, zero again on return), which are then written out.
+__device__ void exact_tile(const HeadParams* hp, const void* __restrict__ x, int dtype,
+                           int64_t n_tok, int64_t x_stride, int layout,
+                           uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
+                           int64_t cap, int64_t pos, int64_t tile, int head,
+                           uint32_t (*rec)[kRecStride]) {
   const int rwords = hp->record_bytes / 4;
-  const int64_t tile = pos / kTile + blockIdx.x;
   const int64_t tile_base = tile * kTile;
   const int64_t t_begin = max(tile_base, pos);
   const int64_t t_end = min(tile_base + kTile, pos + n_tok);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  for (int i = tid; i < kTile * kRecStride; i += kEncThreads) (&rec[0][0])[i] = 0u;
-  __syncthreads();
   for (int64_t t = t_begin + wave; t < t_end; t += kEncThreads / 64) {
     const void* xrow = static_cast<const char*>(x) +
                        ((t - pos) * x_stride + (int64_t)head * kD) * (dtype == AATC_BF16 ? 2 : 4);
@@ -103,6 +98,20 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
   __syncthreads();
   write_tile(rec, (int)(t_begin - tile_base), (int)(t_end - tile_base), rwords, layout, codes,
              head, cap, tile, kEncThreads);
+  __syncthreads();                               // (the cleared rows before their next use)
+}
+
+// Any layout, any token count: one workgroup per (64-token tile, KV head).
+__global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
+    const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
+    int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
+    int64_t cap, int64_t pos) {
+  __shared__ uint32_t rec[kTile][kRecStride];
+  const int head = blockIdx.y;
+  for (int i = threadIdx.x; i < kTile * kRecStride; i += kEncThreads) (&rec[0][0])[i] = 0u;
+  __syncthreads();
+  exact_tile(head_params(params, head), x, dtype, n_tok, x_stride, layout, codes, alpha, cap,
+             pos, pos / kTile + blockIdx.x, head, rec);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -238,6 +247,17 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
   const int rwords = hp->record_bytes / 4;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 15, kg = lane >> 4;
   const int dtype = BF16 ? AATC_BF16 : AATC_F32;
+  // Channels wider than 8 bits: four consecutive codes may not fit one 32-bit field, so
+  // such tensors take the exact one-wave routine per token (uniform over the grid).
+  if (hp->max_bits > 8) {
+    for (int i = tid; i < kTile * kRecStride; i += kEncThreads) (&rec[0][0])[i] = 0u;
+    __syncthreads();
+    for (int64_t tile = pos / kTile + blockIdx.x; tile <= (pos + n_tok - 1) / kTile;
+         tile += gridDim.x)
+      exact_tile(hp, x, dtype, n_tok, x_stride, layout, codes, alpha, cap, pos, tile, head, rec);
+    return;
+  }
+  const bool midrise = hp->quantizer == AATC_QUANT_MIDRISE;
 
   // Limb tables of the transposed integer transform: operand slot u = (2 ct + kc) 64 + l
   // (l = 16 kg + n) holds Tq^T[16 ct + n][64 kc + 16 kg .. + 15]; thread tid fills slots
@@ -386,8 +406,9 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
     const float Et = enc_cross_row_sum(E);
     uint32_t field[8];
     bool uncertain = false;
-    auto codes_of = [&](auto certify) {
+    auto codes_of = [&](auto certify, auto mid_rise) {
       constexpr bool CERT = decltype(certify)::value;
+      constexpr bool MR = decltype(mid_rise)::value;
       float ea = 0.f;
       if constexpr (CERT) {
         // The fixed-point error bound in r units (before 1/s): E 2^-S (1 + 2^-16) covers
@@ -413,34 +434,39 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           // The canonical quantizer: xq = fl32(r / alpha) 2^(b-1) (the power of two is
-          // exact), code = floor(xq + 1/2) clamped to [-2^(b-1), 2^(b-1) - 1], b-bit two's
-          // complement.  Clamping xq first (the bounds are integers) and then rounding half
-          // up with v_cvt_rpi_i32_f32 gives the same code (checked on the hardware against
-          // floor(xq) + (frac >= 1/2): boundary values within 64 ulps of k and k + 1/2 for
-          // |k| <= 130, 2^24 values in all).  Dropped channels have r = 0 and mask 0.
+          // exact), code = floor(xq + 1/2) (midtread) or floor(xq) (midrise) clamped to
+          // [-2^(b-1), 2^(b-1) - 1], b-bit two's complement.  Clamping xq first (the bounds
+          // are integers) and then rounding gives the same code; for midtread the rounding
+          // half up is one v_cvt_rpi_i32_f32 (checked on the hardware against floor(xq) +
+          // (frac >= 1/2): boundary values within 64 ulps of k and k + 1/2 for |k| <= 130,
+          // 2^24 values in all).  Dropped channels have r = 0 and mask 0.
           const float xq = (r[ct][i] * inv_a) * p2[i];
           const float xc = __builtin_amdgcn_fmed3f(xq, -p2[i], hv[i]);
           int code;
-          asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(code) : "v"(xc));
+          if constexpr (MR)
+            code = (int)floorf(xc);
+          else
+            asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(code) : "v"(xc));
           if constexpr (CERT) {
-            int cu;
-            asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(cu) : "v"(xq));
-            const float dev = fabsf(xq - (float)cu);   // 1/2 - distance to a boundary
             const float kf = i == 0 ? k4.x : i == 1 ? k4.y : i == 2 ? k4.z : k4.w;
             // the bound in x units, plus both evaluations' fp32 roundings and that of
             // xq + 1/2
             const float mg = fmaf(kf, ea, fmaf(0x1p-21f, fabsf(xq), 0x1p-22f));
-            uncertain |= (dev + mg >= 0.5f);
+            uncertain |= boundary_distance(xq, MR) <= mg;
           }
           f |= ((uint32_t)code & mk[i]) << sh[i];
         }
         field[ct] = f;
       }
     };
-    if (__builtin_amdgcn_ballot_w64(Et > 0.f) != 0ull)
-      codes_of(std::true_type{});
-    else
-      codes_of(std::false_type{});
+    const bool cert = __builtin_amdgcn_ballot_w64(Et > 0.f) != 0ull;
+    if (midrise) {
+      if (cert) codes_of(std::true_type{}, std::true_type{});
+      else codes_of(std::false_type{}, std::true_type{});
+    } else {
+      if (cert) codes_of(std::true_type{}, std::false_type{});
+      else codes_of(std::false_type{}, std::false_type{});
+    }
     // A token is redone exactly if any of its four lanes could not certify it.
     const bool redo = enc_cross_row_max(uncertain ? 1.f : 0.f) > 0.f;
     if (valid && !redo) {

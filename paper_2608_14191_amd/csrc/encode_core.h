@@ -47,15 +47,24 @@ __device__ inline float inverse_alpha(__half a16) {
 }
 
 // Quantize one transformed coefficient (canonical fp32 sequence); returns the b-bit two's
-// complement pattern of the code.
-__device__ inline uint32_t quantize_code(float r, float inv_a, int b) {
+// complement pattern of the code.  Midtread: floor(x + 1/2) taken exactly; midrise:
+// floor(x) (its level is (code + 1/2) Delta).
+__device__ inline uint32_t quantize_code(float r, float inv_a, int b, bool midrise) {
   float y = r * inv_a;
   float xq = ldexpf(y, b - 1);
   float f = floorf(xq);
-  int code = (int)f + ((xq - f) >= 0.5f ? 1 : 0);
+  int code = (int)f + ((!midrise && (xq - f) >= 0.5f) ? 1 : 0);
   const int half = 1 << (b - 1);
   code = min(max(code, -half), half - 1);
   return (uint32_t)code & ((1u << b) - 1u);
+}
+
+// Distance of a quantizer input x to the nearest decision boundary of its reading:
+// half-integers for midtread (round half up), integers for midrise (floor).
+__device__ inline float boundary_distance(float x, bool midrise) {
+  const float f = floorf(x);
+  const float frac = x - f;                         // exact, in [0, 1)
+  return midrise ? fminf(frac, 1.f - frac) : fabsf(frac - 0.5f);
 }
 
 // Position of a token of a 64-token value tile: word 2 v + tile_word(p) of the tile holds
@@ -146,16 +155,14 @@ __device__ inline bool wave_certify(const HeadParams* hp, const float (&r)[2], f
   bool ok = __half_as_ushort(token_alpha(fmaxf(amax - ma, 0.f))) ==
             __half_as_ushort(token_alpha(amax + ma));
   const float ea = eh * inv;
+  const bool midrise = hp->quantizer == AATC_QUANT_MIDRISE;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     if (b[i] > 0) {
       const float xq = ldexpf(r[i] * inv, b[i] - 1);
-      const float f = floorf(xq);
-      const float code = f + ((xq - f) >= 0.5f ? 1.f : 0.f);
-      const float dev = fabsf(xq - code);
       const float k = ldexpf(hp->inv_s[lane + 64 * i], b[i] - 1) * (1.f + 0x1p-20f);
       const float mg = fmaf(k, ea, fmaf(0x1p-21f, fabsf(xq), 0x1p-22f));
-      ok = ok && (dev + mg < 0.5f);
+      ok = ok && (boundary_distance(xq, midrise) > mg);
     }
   }
   return __builtin_amdgcn_ballot_w64(!ok) == 0ull;
@@ -176,10 +183,11 @@ __device__ inline __half wave_quantize_into(const HeadParams* hp, const float (&
   }
   const __half a16 = token_alpha(wave_max64(m));
   const float inv = inverse_alpha(a16);
+  const bool midrise = hp->quantizer == AATC_QUANT_MIDRISE;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     if (b[i] > 0) {
-      const uint32_t u = quantize_code(r[i], inv, b[i]);
+      const uint32_t u = quantize_code(r[i], inv, b[i], midrise);
       atomicOr(&rec[off[i] >> 5], u << (off[i] & 31));
       if ((off[i] & 31) + b[i] > 32) atomicOr(&rec[(off[i] >> 5) + 1], u >> (32 - (off[i] & 31)));
     }

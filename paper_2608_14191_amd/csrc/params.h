@@ -9,7 +9,7 @@
 namespace aatc {
 
 constexpr int kD = 128;                   // head dimension
-constexpr int kMaxBits = 8;               // widest channel code
+constexpr int kMaxBits = 16;              // widest channel code
 constexpr int kMaxBudget = kD * kMaxBits; // most bits per token record
 constexpr int kTile = 64;                 // tokens per value-cache tile
 constexpr int kTFrac = 22;                // the stored transform: multiples of 2^-22
@@ -32,14 +32,22 @@ struct alignas(256) HeadParams {
   uint8_t virt_chan[kMaxBudget];  // record bit v -> storage channel
   uint8_t virt_bit[kMaxBudget];   // record bit v -> bit index inside that channel's code
   // Record bit v = 32 D + 8 j + d described at [(8 D + d) * 4 + j]: storage channel c
-  // (bits 0-6), 8 + k + 1 - b_c for bit k of a b_c-bit code (bits 8-11), sign bit of
-  // the code (bit 14), bit in use (bit 15).
+  // (bits 0-6), kDescBias + k + 1 - b_c for bit k of a b_c-bit code (bits 8-11), sign
+  // bit of the code (bit 14), bit in use (bit 15).
   uint16_t bit_desc[kMaxBudget];
   int32_t d_active;
   int32_t budget;
   int32_t record_bytes;
   float inv_s_max;                // largest 1/s_c over the stored channels
+  int32_t quantizer;              // aatc_quantizer (0 midtread, 1 midrise)
+  int32_t max_bits;               // widest channel
+  int32_t pad_[2];
+  // Midrise: 2^(-b_c) for stored channels (0 for dropped ones and for midtread), the
+  // extra half step of every level in units of alpha s_c.
+  float half_step[kD];
 };
+// bit_desc exponent field offset: k + 1 - b_c lies in [1 - kMaxBits, 0].
+constexpr int kDescBias = kMaxBits - 1;
 
 // The decode kernel reads these fields with 16-, 8- and 4-byte vector loads.
 static_assert(offsetof(HeadParams, T) % 16 == 0, "T alignment");
@@ -49,6 +57,7 @@ static_assert(offsetof(HeadParams, s) % 16 == 0, "s alignment");
 static_assert(offsetof(HeadParams, bit_off) % 8 == 0, "bit_off alignment");
 static_assert(offsetof(HeadParams, bits) % 4 == 0, "bits alignment");
 static_assert(offsetof(HeadParams, bit_desc) % 8 == 0, "bit_desc alignment");
+static_assert(offsetof(HeadParams, half_step) % 16 == 0, "half_step alignment");
 
 struct alignas(256) TensorHeader {
   uint32_t magic;

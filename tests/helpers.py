@@ -15,6 +15,7 @@ def abi_calibration(cal: "ora.Calibration"):
     c.budget_bits = cal.budget
     c.record_bytes = cal.record_bytes
     c.d_active = cal.d_active
+    c.quantizer = P.QUANT_MIDRISE if cal.quantizer == "midrise" else P.QUANT_MIDTREAD
     np.ctypeslib.as_array(c.transform)[:] = cal.T32.reshape(-1)
     np.ctypeslib.as_array(c.bits)[:] = cal.bits
     np.ctypeslib.as_array(c.scale_f16)[:] = cal.s16.view(np.uint16)

@@ -266,7 +266,12 @@ def test_append_decode_matches_encode_then_decode(name):
     """One aatc_append_decode_attention call gives the codes of encoding the new token and
     the outputs of decoding the updated cache (oracle and separate calls)."""
     _log(f"[append] {name}")
-    case = Case(**APPEND_CASES[name])
+    append_check(Case(**APPEND_CASES[name]))
+
+
+def append_check(case):
+    """The fused append + decode of each sequence's last token against the oracle's codes
+    and attention and against separate encode + decode calls."""
     w = case.w
     B, H, HQ, cap = w.batch, w.n_kv_heads, w.n_q_heads, case.cap
     rk, rv = case.cal_k[0].record_bytes, case.cal_v[0].record_bytes

@@ -203,7 +203,7 @@ def test_encode_and_decode_validate_before_launch():
     assert L.aatc_decode_attention(*bad) == 1
     bad = list(args); bad[14] = 42                   # record size not a multiple of 4
     assert L.aatc_decode_attention(*bad) == 1
-    bad = list(args); bad[15] = 132                  # record larger than 1024 bits
+    bad = list(args); bad[15] = 260                  # record larger than 2048 bits (16 x 128)
     assert L.aatc_decode_attention(*bad) == 1
     bad = list(args); bad[19] = ws - 1               # workspace too small
     assert L.aatc_decode_attention(*bad) == 5
@@ -315,9 +315,44 @@ def test_allocate_global_errors():
     s2 = np.ones((4, 8))
     for args in [(s2, None, 0.5, 8, 3, 1, False),      # protected layers exceed the total
                  (s2, None, 8.5, 8, 0, 0, False),      # the pool exceeds b_max
-                 (s2, None, 2.0, 9, 3, 0, False),      # b_max above 8
+                 (s2, None, 2.0, 17, 3, 0, False),     # b_max above 16
                  (s2, None, 1e300, 8, 0, 0, False),    # an average beyond any width
                  (-s2, None, 2.0, 8, 3, 0, False),     # negative variance
                  (s2, np.full((4, 8), np.nan), 2.0, 8, 3, 0, False)]:
         with pytest.raises(P.AatcError):
             P.aatc_allocate_global(*args)
+
+
+@pytest.mark.parametrize("cfg,head,kind", [(3, 0, "k"), (3, 2, "k"), (2, 1, "k"), (4, 0, "v")])
+def test_host_calibration_sixteen_bit_cap_matches_oracle(cfg, head, kind):
+    """b_max = 16 (App. E): the host allocation gives the oracle's widths, above 8 where
+    the weighted variance calls for it (the Qwen-shape keys take 9 and 10 bits)."""
+    w = workload(cfg, n_tokens=64)
+    x = w.calib(head, kind)
+    avg = 8.0 if cfg == 4 else w.cfg["avg_bits"][0]
+    c = P.aatc_calibrate(x, avg, b_max=16)
+    o = ora.calibrate(x, avg, b_max=16)
+    np.testing.assert_array_equal(c.bits_np, o.bits)
+    np.testing.assert_array_equal(c.s16.view(np.uint16), o.s16.view(np.uint16))
+    assert c.quantizer == P.QUANT_MIDTREAD
+    if cfg == 3:
+        assert c.bits_np.max() > 8
+    with pytest.raises(P.AatcError):
+        P.aatc_calibrate(x, avg, b_max=17)
+
+
+def test_params_pack_quantizer_reading():
+    """The quantizer reading travels in the calibration: one reading per tensor, and only
+    the two defined values are accepted."""
+    w = workload(2, n_tokens=64)
+    cals = [abi_calibration(ora.calibrate(w.calib(h, "k"), 2.75)) for h in range(2)]
+    P.aatc_params_pack(cals)
+    for c in cals:
+        c.quantizer = P.QUANT_MIDRISE
+    P.aatc_params_pack(cals)
+    cals[1].quantizer = P.QUANT_MIDTREAD
+    with pytest.raises(P.AatcError):
+        P.aatc_params_pack(cals)
+    cals[1].quantizer = 7
+    with pytest.raises(P.AatcError):
+        P.aatc_params_pack(cals)
