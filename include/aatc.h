@@ -131,6 +131,31 @@ aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int32_t d,
                            aatc_calibration* out);
 
 /*
+ * aatc_calibrate_whitened -- aatc_calibrate from the layer's input activations and its
+ * projection, in the paper's form (Sec. 5.1 Step 1, eq. AB-factorization; App. D).
+ *
+ * Sigma_X = X^T X / T (fp64, uncentered); its Cholesky factor L (Sigma_X = L L^T); the
+ * whitened weight W~ = L^T W; the right singular vectors P of W~ (the eigenvectors of
+ * W~^T W~, by decreasing singular value, signed like aatc_calibrate's) form the basis, with
+ * channel variances S_c^2 of K = X W in that basis.  The cache stores K P: it differs from
+ * the paper's H = X A (A = L^-T U sqrt(S)) by a per-channel scale only, which changes no
+ * code.  Weights, allocation, storage order and scales then follow aatc_calibrate, on the
+ * samples K = X W (fp64).  With the same samples this is the calibration aatc_calibrate
+ * returns for K (the two forms span the same channels, App. D).
+ *
+ * x_in     host [n_calib][d_model] fp32 input activations of the layer (n_calib >= 2;
+ *          Sigma_X must be positive definite, so n_calib >= d_model in practice).
+ * w_proj   host [d_model][d] fp32 key or value projection of this KV head.
+ * q_calib, n_q, q_group, w_o, d_out, avg_bits, b_max, percentile, out: as in aatc_calibrate.
+ * Errors: as aatc_calibrate; AATC_E_NUMERIC also when Sigma_X is not positive definite.
+ */
+aatc_status aatc_calibrate_whitened(const float* x_in, int64_t n_calib, int32_t d_model,
+                                    const float* w_proj, int32_t d,
+                                    const float* q_calib, int64_t n_q, int32_t q_group,
+                                    const float* w_o, int32_t d_out, double avg_bits,
+                                    int32_t b_max, double percentile, aatc_calibration* out);
+
+/*
  * aatc_calibrate_bits -- aatc_calibrate with the widths given instead of allocated.
  *
  * For widths that come from one budget over several heads or layers (aatc_allocate_global,

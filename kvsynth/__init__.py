@@ -10,5 +10,7 @@ from .gen import (  # noqa: F401
     bf16_bits_to_f32,
     f32_to_bf16_bits,
     haar_orthogonal,
+    layer_inputs,
+    projection,
     workload,
 )

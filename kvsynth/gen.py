@@ -199,3 +199,25 @@ def workload(config_id: int, n_tokens: Optional[int] = None,
     return Workload(config_id=config_id, cfg=cfg,
                     n_tokens=cfg["n_tokens"] if n_tokens is None else n_tokens,
                     batch=cfg["batch"] if batch is None else batch)
+
+
+# ---------------------------------------------------------------------------------------
+# Layer inputs and a projection, for the calibration form that starts from the layer's
+# input activations X and its key or value projection W (K = X W).
+# ---------------------------------------------------------------------------------------
+S_LAYER_X, S_LAYER_W = 8, 9
+
+
+def layer_inputs(seed: int, n: int, d_model: int, p: float = 1.0) -> np.ndarray:
+    """[n, d_model] float32 calibration activations with a decaying spectrum: rows are
+    U diag(sqrt(lam)) z with lam_i = i**-p and a Haar-random U."""
+    u = haar_orthogonal(np.random.default_rng([seed, 0, S_LAYER_X, 0]), d_model)
+    lam = np.arange(1, d_model + 1, dtype=np.float64) ** -p
+    z = np.random.default_rng([seed, 0, S_LAYER_X, 1]).standard_normal((n, d_model))
+    return ((z * np.sqrt(lam)[None, :]) @ u.T).astype(np.float32)
+
+
+def projection(seed: int, d_model: int, d: int) -> np.ndarray:
+    """[d_model, d] float32 projection with Gaussian entries of variance 1 / d_model."""
+    g = np.random.default_rng([seed, 0, S_LAYER_W, 0]).standard_normal((d_model, d))
+    return (g / np.sqrt(d_model)).astype(np.float32)

@@ -308,6 +308,96 @@ def calibrate(x_calib: np.ndarray, avg_bits: float, b_max: int = 8,
                        bits_eig=bits_eig, quantizer=quantizer)
 
 
+def whitened_svd(x_in: np.ndarray, w_proj: np.ndarray):
+    """Sec. 5.1, Step 1 (whitening-based decorrelation), literally:
+
+    Sigma_X = X^T X / T; Sigma_X = L L^T (Cholesky); W~ = L^T W; W~ = U S P^T (reduced
+    SVD); A = L^-T U sqrt(S), B = sqrt(S) P^T, so that W = A B (eq. AB-factorization) and
+    the cache holds H = X A (eq. transformed-cache).  Singular values decreasing; each
+    column of P signed so its largest-magnitude entry is positive (U and A follow).
+    Returns (A [d_model, d], B [d, d], S [d], P [d, d])."""
+    x = np.asarray(x_in, dtype=np.float64)
+    w = np.asarray(w_proj, dtype=np.float64)
+    sig_x = covariance(x)
+    chol = np.linalg.cholesky(sig_x)
+    u, s, pt = np.linalg.svd(chol.T @ w, full_matrices=False)
+    p = pt.T
+    for c in range(p.shape[1]):
+        j = int(np.argmax(np.abs(p[:, c])))
+        if p[j, c] < 0:
+            p[:, c] = -p[:, c]
+            u[:, c] = -u[:, c]
+    a_mat = np.linalg.solve(chol.T, u) * np.sqrt(s)[None, :]
+    b_mat = np.sqrt(s)[:, None] * p.T
+    return a_mat, b_mat, s, p
+
+
+def calibrate_whitened(x_in: np.ndarray, w_proj: np.ndarray, avg_bits: float,
+                       b_max: int = 8, percentile: float = 0.99,
+                       q_calib: Optional[np.ndarray] = None, group: int = 1,
+                       w_o: Optional[np.ndarray] = None,
+                       quantizer: str = "midtread") -> Calibration:
+    """Alg. 1 (calibration) from the layer's input activations X [T, d_model] and its key
+    or value projection W [d_model, d], in the paper's form (Sec. 5.1 Step 1, Sec. 5.2):
+
+    1. the whitened SVD (``whitened_svd``): A, B, S, P;
+    2. channel variances of H = X A: var(h_c) = S_c (A^T Sigma_X A = S);
+    3. weights from B: keys w_c = (1/T) sum over the group's queries of (B_c q)^2
+       (eq. waterfilling-keys), values w_c = ||(B W_O)_c||^2 (Sec. 5.2); without either,
+       w_c = ||B_c||^2 = S_c (var-only as the reconstruction error of K or V, the reading
+       the PCA form uses);
+    4. the integer allocation of w_c S_c (as in ``allocate_bits``);
+    5. the cache stores K = X W in the basis P: h_c = (K P)_c = sqrt(S_c) (X A)_c, which
+       differs from H only by a per-channel scale that changes no code (App. B); so the
+       stored transform is P in storage order and s_c the 99th percentile of |(K P)_c|.
+    """
+    x = np.asarray(x_in, dtype=np.float64)
+    a_mat, b_mat, s, p = whitened_svd(x, w_proj)
+    d = b_mat.shape[0]
+    if q_calib is not None:
+        t = q_calib.shape[0] // group
+        w = ((np.asarray(q_calib, dtype=np.float64) @ b_mat.T) ** 2).sum(axis=0) / t
+    elif w_o is not None:
+        w = ((b_mat @ np.asarray(w_o, dtype=np.float64)) ** 2).sum(axis=1)
+    else:
+        # var-only (reading: the key/value reconstruction error, as for the PCA form):
+        # an error in h_c reaches K through row c of B, ||B_c||^2 = S_c
+        w = s.copy()
+    budget = int(np.floor(avg_bits * d + 0.5))
+    bits_eig = allocate_bits(w * s, budget, b_max)
+    k = x @ np.asarray(w_proj, dtype=np.float64)
+    return _storage_calibration(k, p, s * s, w * s / (s * s), bits_eig, budget, percentile,
+                                None, quantizer)
+
+
+def _storage_calibration(k, p, lam, weight, bits_eig, budget, percentile, record_bytes,
+                         quantizer) -> Calibration:
+    """Storage order, stored transform and scales of a calibration whose basis P (eigen
+    order), channel variances lam and widths (eigen order) are known; k holds the
+    calibration samples in the original coordinates."""
+    d = p.shape[0]
+    bits_eig = np.asarray(bits_eig, dtype=np.int64)
+    perm = np.argsort(-bits_eig, kind="stable")
+    bits = bits_eig[perm]
+    t64 = p[:, perm]
+    t32 = stored_transform(t64)
+    h = np.asarray(k, dtype=np.float64) @ t64
+    s = np.zeros(d)
+    for c in range(d):
+        if bits[c] > 0:
+            s[c] = np.percentile(np.abs(h[:, c]), 100.0 * percentile)
+    s16 = to_f16(s)
+    s16[bits == 0] = 0
+    min_rb = 4 * ((budget + 31) // 32)
+    if record_bytes is not None and (record_bytes < min_rb or record_bytes % 4):
+        raise ValueError("record_bytes below the budget or not whole dwords")
+    return Calibration(d=d, budget=budget,
+                       record_bytes=min_rb if record_bytes is None else int(record_bytes),
+                       d_active=int(np.count_nonzero(bits)), bits=bits, perm=perm,
+                       T64=t64, T32=t32, s16=s16, sigma2=lam, weight=weight,
+                       bits_eig=bits_eig, quantizer=quantizer)
+
+
 # --------------------------------------------------------------------------------------
 # Encoding
 # --------------------------------------------------------------------------------------

@@ -8,7 +8,7 @@ from ._lib import (  # noqa: F401
     QUANT_MIDTREAD, TILE_TOKENS,
     AatcError, Calibration,
     aatc_allocate_global, aatc_append_decode_attention, aatc_append_decode_attention_noalloc,
-    aatc_calibrate, aatc_calibrate_bits, aatc_decode_attention, aatc_decode_attention_segmented,
+    aatc_calibrate, aatc_calibrate_bits, aatc_calibrate_whitened, aatc_decode_attention, aatc_decode_attention_segmented,
     aatc_decode_workspace_bytes, aatc_encode, aatc_segment_counts,
     aatc_params_bytes, aatc_params_pack, aatc_status_string, library,
 )

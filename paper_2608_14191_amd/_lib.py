@@ -75,6 +75,9 @@ _L.aatc_status_string.argtypes = [ctypes.c_int]
 _L.aatc_calibrate.restype = ctypes.c_int
 _L.aatc_calibrate.argtypes = [_vp, _i64, _i32, _vp, _i64, _i32, _vp, _i32, _f64, _i32, _f64,
                               ctypes.POINTER(Calibration)]
+_L.aatc_calibrate_whitened.restype = ctypes.c_int
+_L.aatc_calibrate_whitened.argtypes = [_vp, _i64, _i32, _vp, _i32, _vp, _i64, _i32, _vp, _i32,
+                                       _f64, _i32, _f64, ctypes.POINTER(Calibration)]
 _L.aatc_calibrate_bits.restype = ctypes.c_int
 _L.aatc_calibrate_bits.argtypes = [_vp, _i64, _i32, _vp, _i64, _i32, _vp, _i32, _vp, _i32, _f64,
                                    ctypes.POINTER(Calibration)]
@@ -149,6 +152,26 @@ def aatc_calibrate(x_calib, avg_bits: float, b_max: int = 8, percentile: float =
                            _np_ptr(wo), 0 if wo is None else wo.shape[1],
                            float(avg_bits), int(b_max), float(percentile), ctypes.byref(out))
     _check("aatc_calibrate", st)
+    return out
+
+
+def aatc_calibrate_whitened(x_in, w_proj, avg_bits: float, b_max: int = 8,
+                            percentile: float = 0.99, q_calib=None, q_group: int = 1,
+                            w_o=None) -> Calibration:
+    """Host calibration from layer inputs [T, d_model] and a projection [d_model, d]."""
+    x = np.ascontiguousarray(x_in, dtype=np.float32)
+    w = np.ascontiguousarray(w_proj, dtype=np.float32)
+    if x.ndim != 2 or w.ndim != 2 or w.shape[0] != x.shape[1]:
+        raise ValueError("x_in must be [T, d_model] and w_proj [d_model, d]")
+    q = None if q_calib is None else np.ascontiguousarray(q_calib, dtype=np.float32)
+    wo = None if w_o is None else np.ascontiguousarray(w_o, dtype=np.float32)
+    out = Calibration()
+    st = _L.aatc_calibrate_whitened(_np_ptr(x), x.shape[0], x.shape[1], _np_ptr(w), w.shape[1],
+                                    _np_ptr(q), 0 if q is None else q.shape[0], int(q_group),
+                                    _np_ptr(wo), 0 if wo is None else wo.shape[1],
+                                    float(avg_bits), int(b_max), float(percentile),
+                                    ctypes.byref(out))
+    _check("aatc_calibrate_whitened", st)
     return out
 
 

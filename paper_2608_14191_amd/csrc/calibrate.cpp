@@ -140,13 +140,16 @@ namespace {
 
 // The calibration of aatc_calibrate; with `bits_given` (eigen order) the widths are taken
 // as they are instead of allocated, and a nonzero `record_bytes_given` pads the records.
+// With `gram` the d x d matrix whose eigenvectors form the basis is given (instead of the
+// covariance of the samples) and the samples are `x64` (fp64) instead of `x_calib`.
 aatc_status calibrate_impl(const float* x_calib, int64_t n_calib, int32_t d,
                            const float* q_calib, int64_t n_q, int32_t q_group,
                            const float* w_o, int32_t d_out, double avg_bits, int32_t b_max,
                            const uint8_t* bits_given, int32_t record_bytes_given,
-                           double percentile, aatc_calibration* out) {
+                           double percentile, aatc_calibration* out,
+                           const double* gram = nullptr, const double* x64 = nullptr) {
   try {
-    if (!x_calib || !out) return AATC_E_INVALID;
+    if ((!x_calib && !x64) || !out) return AATC_E_INVALID;
     if (d != AATC_HEAD_DIM) return AATC_E_UNSUPPORTED;
     if (n_calib < 2 || b_max < 1 || b_max > AATC_MAX_BITS) return AATC_E_INVALID;
     if (!(percentile > 0.0 && percentile <= 1.0)) return AATC_E_INVALID;
@@ -172,15 +175,20 @@ aatc_status calibrate_impl(const float* x_calib, int64_t n_calib, int32_t d,
       return AATC_E_INVALID;
 
     const size_t n = (size_t)n_calib;
+    auto sample = [&](size_t i, int j) -> double {
+      return x64 ? x64[i * d + j] : (double)x_calib[i * d + j];
+    };
     for (size_t i = 0; i < n * d; ++i)
-      if (!std::isfinite(x_calib[i])) return AATC_E_NUMERIC;
+      if (!std::isfinite(sample(i / d, (int)(i % d)))) return AATC_E_NUMERIC;
 
-    // 1. Sigma = X^T X / n (fp64, uncentered).
+    // 1. Sigma = X^T X / n (fp64, uncentered), or the given matrix.
     std::vector<double> sigma((size_t)d * d, 0.0);
-    {
+    if (gram) {
+      std::copy(gram, gram + (size_t)d * d, sigma.begin());
+    } else {
       std::vector<double> row(d);
       for (size_t i = 0; i < n; ++i) {
-        for (int j = 0; j < d; ++j) row[j] = x_calib[i * d + j];
+        for (int j = 0; j < d; ++j) row[j] = sample(i, j);
         for (int j = 0; j < d; ++j) {
           double xj = row[j];
           double* s = &sigma[(size_t)j * d];
@@ -297,7 +305,7 @@ aatc_status calibrate_impl(const float* x_calib, int64_t n_calib, int32_t d,
       int e = perm[c];
       for (size_t i = 0; i < n; ++i) {
         double acc = 0.0;
-        for (int j = 0; j < d; ++j) acc += (double)x_calib[i * d + j] * p[(size_t)j * d + e];
+        for (int j = 0; j < d; ++j) acc += sample(i, j) * p[(size_t)j * d + e];
         col[i] = std::fabs(acc);
       }
       std::sort(col.begin(), col.end());
@@ -318,6 +326,87 @@ extern "C" aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int
                                       aatc_calibration* out) {
   return calibrate_impl(x_calib, n_calib, d, q_calib, n_q, q_group, w_o, d_out, avg_bits,
                         b_max, nullptr, 0, percentile, out);
+}
+
+namespace {
+
+// Cholesky factor L (lower, row-major) of a symmetric positive definite n x n matrix;
+// false if it is not numerically positive definite.
+bool cholesky(const std::vector<double>& a, int n, std::vector<double>& l) {
+  l.assign((size_t)n * n, 0.0);
+  for (int j = 0; j < n; ++j) {
+    double s = a[(size_t)j * n + j];
+    for (int k = 0; k < j; ++k) s -= l[(size_t)j * n + k] * l[(size_t)j * n + k];
+    if (!(s > 0.0) || !std::isfinite(s)) return false;
+    const double d = std::sqrt(s);
+    l[(size_t)j * n + j] = d;
+    for (int i = j + 1; i < n; ++i) {
+      double t = a[(size_t)i * n + j];
+      for (int k = 0; k < j; ++k) t -= l[(size_t)i * n + k] * l[(size_t)j * n + k];
+      l[(size_t)i * n + j] = t / d;
+    }
+  }
+  return true;
+}
+
+}  // namespace
+
+extern "C" aatc_status aatc_calibrate_whitened(const float* x_in, int64_t n_calib,
+                                               int32_t d_model, const float* w_proj, int32_t d,
+                                               const float* q_calib, int64_t n_q,
+                                               int32_t q_group, const float* w_o,
+                                               int32_t d_out, double avg_bits, int32_t b_max,
+                                               double percentile, aatc_calibration* out) {
+  try {
+    if (!x_in || !w_proj || !out || d_model < 1) return AATC_E_INVALID;
+    if (d != AATC_HEAD_DIM) return AATC_E_UNSUPPORTED;
+    if (n_calib < 2) return AATC_E_INVALID;
+    const size_t n = (size_t)n_calib, dm = (size_t)d_model;
+    for (size_t i = 0; i < n * dm; ++i)
+      if (!std::isfinite(x_in[i])) return AATC_E_NUMERIC;
+    for (size_t i = 0; i < dm * d; ++i)
+      if (!std::isfinite(w_proj[i])) return AATC_E_NUMERIC;
+    // Sigma_X = X^T X / T (fp64, uncentered) and its Cholesky factor L.
+    std::vector<double> sx(dm * dm, 0.0), row(dm);
+    for (size_t i = 0; i < n; ++i) {
+      for (size_t j = 0; j < dm; ++j) row[j] = x_in[i * dm + j];
+      for (size_t j = 0; j < dm; ++j)
+        for (size_t k = j; k < dm; ++k) sx[j * dm + k] += row[j] * row[k];
+    }
+    for (size_t j = 0; j < dm; ++j)
+      for (size_t k = j; k < dm; ++k) {
+        sx[j * dm + k] /= (double)n;
+        sx[k * dm + j] = sx[j * dm + k];
+      }
+    std::vector<double> l;
+    if (!cholesky(sx, d_model, l)) return AATC_E_NUMERIC;
+    // The whitened weight W~ = L^T W and its Gram matrix W~^T W~: the right singular
+    // vectors of W~ (the basis P) are its eigenvectors, the squared singular values its
+    // eigenvalues.
+    std::vector<double> wt(dm * d, 0.0);
+    for (size_t j = 0; j < dm; ++j)
+      for (size_t k = j; k < dm; ++k) {           // (L^T)_{jk} = L_{kj}, nonzero for k >= j
+        const double lkj = l[k * dm + j];
+        for (int c = 0; c < d; ++c) wt[j * d + c] += lkj * (double)w_proj[k * d + c];
+      }
+    std::vector<double> gram((size_t)d * d, 0.0);
+    for (size_t j = 0; j < dm; ++j)
+      for (int a = 0; a < d; ++a) {
+        const double v = wt[j * d + a];
+        for (int b = 0; b < d; ++b) gram[(size_t)a * d + b] += v * wt[j * d + b];
+      }
+    // The calibration samples of the cache, K = X W (fp64), for the channel scales.
+    std::vector<double> k(n * d, 0.0);
+    for (size_t i = 0; i < n; ++i)
+      for (size_t j = 0; j < dm; ++j) {
+        const double xv = x_in[i * dm + j];
+        for (int c = 0; c < d; ++c) k[i * d + c] += xv * (double)w_proj[j * d + c];
+      }
+    return calibrate_impl(nullptr, n_calib, d, q_calib, n_q, q_group, w_o, d_out, avg_bits,
+                          b_max, nullptr, 0, percentile, out, gram.data(), k.data());
+  } catch (...) {
+    return AATC_E_INVALID;
+  }
 }
 
 extern "C" aatc_status aatc_calibrate_bits(const float* x_calib, int64_t n_calib, int32_t d,

@@ -356,3 +356,38 @@ def test_params_pack_quantizer_reading():
     cals[1].quantizer = 7
     with pytest.raises(P.AatcError):
         P.aatc_params_pack(cals)
+
+
+@pytest.mark.parametrize("weights", ["var_only", "queries"])
+def test_host_whitened_calibration_matches_oracle(weights):
+    """aatc_calibrate_whitened (Cholesky, whitened Gram matrix, Jacobi) against the oracle's
+    literal whitened SVD: widths, storage order and fp16 scales identical; transform within
+    one grid step; and equal to aatc_calibrate on K = X W."""
+    from kvsynth import layer_inputs, projection
+    x = layer_inputs(11, 1024, 160)
+    w = projection(11, 160, 128)
+    kw = {}
+    if weights == "queries":
+        q = np.random.default_rng(3).standard_normal((2 * 300, 128)).astype(np.float32)
+        kw = dict(q_calib=q, q_group=2)
+    c = P.aatc_calibrate_whitened(x, w, 2.75, **kw)
+    o = ora.calibrate_whitened(x, w, 2.75, q_calib=kw.get("q_calib"), group=kw.get("q_group", 1))
+    np.testing.assert_array_equal(c.bits_np, o.bits)
+    np.testing.assert_array_equal(np.ctypeslib.as_array(c.perm), o.perm)
+    np.testing.assert_array_equal(c.s16.view(np.uint16), o.s16.view(np.uint16))
+    assert np.abs(c.T.astype(np.float64) - o.T32).max() <= 2.0 ** -22
+    k = (x.astype(np.float64) @ w.astype(np.float64)).astype(np.float32)
+    c2 = P.aatc_calibrate(k, 2.75, **kw)
+    np.testing.assert_array_equal(c.bits_np, c2.bits_np)
+
+
+def test_host_whitened_calibration_errors():
+    from kvsynth import projection
+    w = projection(1, 32, 128)
+    x = np.zeros((64, 32), dtype=np.float32)                  # Sigma_X = 0: not definite
+    with pytest.raises(P.AatcError):
+        P.aatc_calibrate_whitened(x, w, 2.75)
+    with pytest.raises(ValueError):
+        P.aatc_calibrate_whitened(np.ones((64, 16), np.float32), w, 2.75)
+    with pytest.raises(P.AatcError):
+        P.aatc_calibrate_whitened(np.ones((64, 32), np.float32), projection(1, 32, 64), 2.75)

@@ -202,3 +202,67 @@ def test_transform_subnormal_results():
     np.testing.assert_array_equal(aatc.transform(x, t), want)
     x2 = np.array([[2.0 ** -127, 2.0 ** -149 * 3]], dtype=np.float32)  # 2^-149 + 1.5 2^-171
     np.testing.assert_array_equal(aatc.transform(x2, t), np.float32(2.0 ** -149))
+
+
+# ---------------------------------------------------------------------------------------
+# The paper's form of Step 1 (Sec. 5.1): whitened SVD from layer inputs and a projection
+# ---------------------------------------------------------------------------------------
+def test_whitened_svd_factorization_identities():
+    """eq. AB-factorization: W = A B; A^T Sigma_X A = S (so H = X A has uncorrelated
+    channels of variance S_c, in decreasing order); B = sqrt(S) P^T with orthonormal P."""
+    from kvsynth import layer_inputs, projection
+    x = layer_inputs(3, 1024, 64).astype(np.float64)
+    w = projection(3, 64, 16).astype(np.float64)
+    a_mat, b_mat, s, p = aatc.whitened_svd(x, w)
+    np.testing.assert_allclose(a_mat @ b_mat, w, atol=1e-12 * np.abs(w).max())
+    sig_x = x.T @ x / x.shape[0]
+    np.testing.assert_allclose(a_mat.T @ sig_x @ a_mat, np.diag(s), atol=1e-10 * s[0])
+    h = x @ a_mat
+    np.testing.assert_allclose(h.T @ h / h.shape[0], np.diag(s), atol=1e-10 * s[0])
+    assert np.all(np.diff(s) <= 0)
+    np.testing.assert_allclose(p.T @ p, np.eye(16), atol=1e-12)
+    np.testing.assert_allclose(b_mat @ b_mat.T, np.diag(s), atol=1e-12 * s[0])
+
+
+def test_whitened_calibration_closed_form_on_whitened_inputs():
+    """Sigma_X = I (inputs already white) and W = diag(2, 1, 1/2, 1/4): L = I, W~ = W, the
+    singular values are (2, 1, 1/2, 1/4), P = I, and K's channel variances S^2 = (4, 1, 1/4,
+    1/16) are the worked reverse water-filling example: 4 bits go (3, 1, 0, 0)."""
+    n, d = 4096, 4
+    q, _ = np.linalg.qr(np.random.default_rng(5).standard_normal((n, d)))
+    x = q * np.sqrt(n)                                  # X^T X / n = I exactly (to rounding)
+    w = np.diag([2.0, 1.0, 0.5, 0.25])
+    a_mat, b_mat, s, p = aatc.whitened_svd(x, w)
+    np.testing.assert_allclose(s, [2.0, 1.0, 0.5, 0.25], rtol=1e-12)
+    np.testing.assert_allclose(np.abs(p), np.eye(4), atol=1e-12)
+    cal = aatc.calibrate_whitened(x, w, avg_bits=1.0)
+    np.testing.assert_allclose(cal.sigma2, [4.0, 1.0, 0.25, 0.0625], rtol=1e-12)
+    # the variances come out of an SVD, so the exact ties of the worked example are broken
+    # by the last bit; any of its three optima (objective 0.625) is the answer
+    assert cal.bits_eig.tolist() in ([3, 1, 0, 0], [2, 2, 0, 0], [2, 1, 1, 0])
+    assert aatc.allocation_objective([4.0, 1.0, 0.25, 0.0625], cal.bits_eig) == \
+        pytest.approx(0.625, rel=1e-12)
+
+
+@pytest.mark.parametrize("weights", ["var_only", "queries", "w_o"])
+def test_whitened_calibration_equals_pca_of_the_keys(weights):
+    """App. D: the whitened SVD of W and the PCA of K = X W give the same channels and the
+    same products w_c sigma_c^2, so the same widths, stored transform and scales."""
+    from kvsynth import layer_inputs, projection
+    x = layer_inputs(7, 2048, 192)
+    w = projection(7, 192, 128)
+    k = x.astype(np.float64) @ w.astype(np.float64)
+    rng = np.random.default_rng(8)
+    kw = {}
+    if weights == "queries":
+        kw = dict(q_calib=rng.standard_normal((4 * 200, 128)), group=4)
+    elif weights == "w_o":
+        kw = dict(w_o=rng.standard_normal((128, 96)))
+    c1 = aatc.calibrate_whitened(x, w, 2.75, **kw)
+    c2 = aatc.calibrate(k, 2.75, **kw)
+    np.testing.assert_array_equal(c1.bits, c2.bits)
+    np.testing.assert_array_equal(c1.perm, c2.perm)
+    np.testing.assert_allclose(c1.weight * c1.sigma2, c2.weight * c2.sigma2,
+                               rtol=1e-8, atol=1e-12 * (c2.weight * c2.sigma2).max())
+    np.testing.assert_allclose(c1.T64, c2.T64, atol=1e-10)
+    np.testing.assert_array_equal(c1.s16, c2.s16)
