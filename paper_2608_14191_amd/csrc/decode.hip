@@ -1062,7 +1062,7 @@ struct AppendHook {
         float xl[2];
 #pragma unroll
         for (int i = 0; i < 2; ++i) xl[i] = load_elem(xr, x_dtype, lane + 64 * i);
-        exact_r_wave(ep, xl, xr, x_dtype, r2);
+        exact_r_wave<true>(ep, xl, xr, x_dtype, r2);
       }
       float m = 0.f;
 #pragma unroll

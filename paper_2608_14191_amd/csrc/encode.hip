@@ -29,6 +29,8 @@ constexpr int kRecWords = kMaxBudget / 32;       // words of the largest record
 // rows (the tile transpose, the per-token bit fields) falls into different banks.
 constexpr int kRecStride = kRecWords + 1;
 constexpr int kSmallBatch = 16;                  // appends up to this many tokens: per-token kernel
+constexpr uint16_t kRedo = 0xFFFFu;              // scale mark of a token left to the exact routine
+                                                 // (an fp16 NaN: no token scale has it)
 
 // This lane's two elements (lane, lane + 64) of a token.
 __device__ inline void load_token_pair(const void* xrow, int dtype, float (&xl)[2]) {
@@ -91,7 +93,7 @@ __device__ void exact_tile(const HeadParams* hp, const void* __restrict__ x, int
                        ((t - pos) * x_stride + (int64_t)head * kD) * (dtype == AATC_BF16 ? 2 : 4);
     float xl[2], r[2];
     load_token_pair(xrow, dtype, xl);
-    exact_r_wave(hp, xl, xrow, dtype, r);
+    exact_r_wave<true>(hp, xl, xrow, dtype, r);
     const __half a16 = wave_quantize_into(hp, r, rec[t - tile_base]);
     if (lane == 0) alpha[(int64_t)head * cap + t] = __half_as_ushort(a16);
   }
@@ -240,7 +242,6 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
   __shared__ __align__(16) uint32_t tab_sh[kD];           // bit of c in its group's field
   __shared__ __align__(16) uint32_t tab_w[kD / 4];        // width of each group of four
   __shared__ __align__(16) uint16_t tab_o[kD];            // first record bits
-  __shared__ unsigned long long fixmask;                  // tokens to encode exactly
 
   const int head = blockIdx.y;
   const HeadParams* hp = head_params(params, head);
@@ -295,8 +296,6 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
   if (tid < kD / 4)
     tab_w[tid] = hp->bits[4 * tid] + hp->bits[4 * tid + 1] + hp->bits[4 * tid + 2] + hp->bits[4 * tid + 3];
   for (int i = tid; i < kTile * kRecStride; i += kEncThreads) (&rec[0][0])[i] = 0u;
-  if (tid == 0) fixmask = 0ull;
-  const float inv_s_max = hp->inv_s_max;
   // Value tiles: lane p of a wave stands for tile bit position p (word p / 32, bit p % 32),
   // i.e. token 16 (2 (p / 32) + p % 2) + 4 ((p / 2) % 4) + (p % 32) / 8.
   const int ptok = 16 * (2 * (lane >> 5) + (lane & 1)) + 4 * ((lane >> 1) & 3) + ((lane & 31) >> 3);
@@ -352,9 +351,16 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
       }
     fetch(tile + gridDim.x);                      // the next tile's elements, in flight
     if (tile == first + blockIdx.x) __syncthreads();   // (the limb and channel tables)
+    // The token's fixed-point error bound: |h_c - h~_c| <= eh for every channel (|T| <= 1).
+    // Waves with an inexact token certify their codes (below).
+    const float Et = enc_cross_row_sum(E);
+    const bool cert = __builtin_amdgcn_ballot_w64(Et > 0.f) != 0ull;
+    const float eh = ldexpf(Et * (1.f + 0x1p-16f), -shift);
     // (3) Four channel tiles at a time: the five limb-product sums, H exactly, then
     //     r_c = fl32(fl32(H 2^-(S+22)) / s_c) for channels 16 ct + 4 kg + i of this token.
-    float r[8][4], am = 0.f;
+    //     With a certificate, also the range of the exact max |r_c|: each r_c is within
+    //     eh / s_c (plus fp32 roundings) of its computed value.
+    float r[8][4], am = 0.f, alo = 0.f, ahi = 0.f;
 #pragma unroll
     for (int c4 = 0; c4 < 8; c4 += 4) {
       ev4i s[5][4];
@@ -393,6 +399,11 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
           const double H = fma(fma((double)hi, 256.0, (double)s[2][u][i]), 65536.0, (double)lo);
           r[ct][i] = integer_result(H, shift) * isv[i];
           am = fmaxf(am, fabsf(r[ct][i]));          // (r = 0 on dropped channels)
+          if (cert) {
+            const float er = eh * isv[i] * (1.f + 0x1p-20f);
+            alo = fmaxf(alo, fabsf(r[ct][i]) - er);
+            ahi = fmaxf(ahi, fabsf(r[ct][i]) + er);
+          }
         }
       }
       // (one half's accumulators at a time)
@@ -403,7 +414,6 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
     const float amax = enc_cross_row_max(am);
     const __half a16 = token_alpha(amax);
     const float inv_a = inverse_alpha(a16);
-    const float Et = enc_cross_row_sum(E);
     uint32_t field[8];
     bool uncertain = false;
     auto codes_of = [&](auto certify, auto mid_rise) {
@@ -411,12 +421,14 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
       constexpr bool MR = decltype(mid_rise)::value;
       float ea = 0.f;
       if constexpr (CERT) {
-        // The fixed-point error bound in r units (before 1/s): E 2^-S (1 + 2^-16) covers
-        // the fp32 sum of E; ldexpf may underflow to 0 only below the absolute slack.
-        const float eh = ldexpf(Et * (1.f + 0x1p-16f), -shift);
-        const float ma = eh * inv_s_max * (1.f + 0x1p-20f) + 0x1p-21f * amax + 0x1p-140f;
-        const __half alo = token_alpha(fmaxf(amax - ma, 0.f)), ahi = token_alpha(amax + ma);
-        uncertain = __half_as_ushort(alo) != __half_as_ushort(ahi);
+        // The fp16 scale is certain when both ends of the range of the exact max |r_c|
+        // (over the token's four lanes), widened by the fp32 roundings, round alike.
+        // eh = E 2^-S (1 + 2^-16) covers the fp32 sum of E; ldexpf may underflow to 0
+        // only below the absolute slack.
+        const float lo = enc_cross_row_max(alo) - 0x1p-21f * amax;
+        const float hi = enc_cross_row_max(ahi) + 0x1p-21f * amax + 0x1p-140f;
+        uncertain = __half_as_ushort(token_alpha(fmaxf(lo, 0.f))) !=
+                    __half_as_ushort(token_alpha(hi));
         ea = eh * inv_a;
       }
 #pragma unroll
@@ -459,7 +471,6 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
         field[ct] = f;
       }
     };
-    const bool cert = __builtin_amdgcn_ballot_w64(Et > 0.f) != 0ull;
     if (midrise) {
       if (cert) codes_of(std::true_type{}, std::true_type{});
       else codes_of(std::false_type{}, std::true_type{});
@@ -482,28 +493,12 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
       }
       if (kg == 0) alpha[(int64_t)head * cap + tile_base + tl] = __half_as_ushort(a16);
     }
-    if (valid && redo && kg == 0) atomicOr(&fixmask, 1ull << tl);
+    // (5) A token that failed the certificate keeps a zero record row here and the mark
+    //     kRedo as its scale; encode_fixup_kernel, launched next on the stream, encodes it
+    //     with the exact one-wave routine (a few in ten thousand tokens; done here, each
+    //     would stall the whole workgroup for several dependent memory round trips).
+    if (valid && redo && kg == 0) alpha[(int64_t)head * cap + tile_base + tl] = kRedo;
     __syncthreads();
-    // (5) Tokens that failed the certificate: the exact one-wave routine, wave w taking the
-    //     w-th, (w + 4)-th, ... of them (their record rows are still zero).
-    const unsigned long long fm = fixmask;
-    if (fm) {
-      unsigned long long rest = fm;
-      for (int k = 0; rest; ++k) {
-        const int t = __builtin_ctzll(rest);
-        rest &= rest - 1;
-        if ((k & 3) != wave) continue;
-        const void* xrow = static_cast<const char*>(x) +
-                           ((tile_base + t - pos) * x_stride + (int64_t)head * kD) * (BF16 ? 2 : 4);
-        float xl[2], r2[2];
-        load_token_pair(xrow, dtype, xl);
-        exact_r_wave(hp, xl, xrow, dtype, r2);
-        const __half e16 = wave_quantize_into(hp, r2, rec[t]);
-        if (lane == 0) alpha[(int64_t)head * cap + tile_base + t] = __half_as_ushort(e16);
-      }
-      __syncthreads();
-      if (tid == 0) fixmask = 0ull;
-    }
     const int lo = (int)(t_begin - tile_base), hi = (int)(t_end - tile_base);
     if (layout == AATC_LAYOUT_RECORDS) {
       uint32_t* out = reinterpret_cast<uint32_t*>(codes) + ((int64_t)head * cap + tile_base) * rwords;
@@ -536,9 +531,39 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
   }
 }
 
-// One wave per (token, KV head), for appends of a few tokens: the exact one-wave routine.
-// Tile bits are set and cleared with device atomics, so tokens that share a tile word may
-// be encoded by different workgroups.
+// One token of one KV head by one wave (the exact one-wave routine): codes into the LDS
+// row `rec` (zero on entry), then into the cache.  Tile bits are set and cleared with
+// device atomics, so tokens that share a tile word may be encoded by other workgroups.
+__device__ __forceinline__ void encode_token_wave(const HeadParams* hp, const void* xrow,
+                                                  int dtype, int layout, uint8_t* codes,
+                                                  uint16_t* alpha, int64_t cap, int64_t t,
+                                                  int head, uint32_t* rec) {
+  const int lane = threadIdx.x & 63;
+  const int rbytes = hp->record_bytes;
+  float xl[2], r[2];
+  load_token_pair(xrow, dtype, xl);
+  exact_r_wave(hp, xl, xrow, dtype, r);
+  const __half a16 = wave_quantize_into(hp, r, rec);
+  if (lane == 0) alpha[(int64_t)head * cap + t] = __half_as_ushort(a16);
+  __syncthreads();                                  // (the record, one wave)
+  if (layout == AATC_LAYOUT_RECORDS) {
+    uint32_t* out = reinterpret_cast<uint32_t*>(codes + ((int64_t)head * cap + t) * rbytes);
+    for (int i = lane; i < rbytes / 4; i += 64) out[i] = rec[i];
+  } else {
+    const int p = (int)(t % kTile);
+    const uint32_t bit = 1u << tile_bit(p);
+    uint32_t* tw = reinterpret_cast<uint32_t*>(codes) +
+                   ((int64_t)head * (cap / kTile) + t / kTile) * (16 * rbytes) + tile_word(p);
+    for (int v = lane; v < 8 * rbytes; v += 64) {
+      if ((rec[v >> 5] >> (v & 31)) & 1u)
+        __hip_atomic_fetch_or(tw + 2 * v, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      else
+        __hip_atomic_fetch_and(tw + 2 * v, ~bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+// One wave per (token, KV head), for appends of a few tokens.
 // With `seq_len` set, block x is a sequence instead: it encodes token seq_len[b] - 1 of
 // sequence b (nothing for an empty sequence) into caches `codes_bstride` bytes and
 // `alpha_bstride` scales apart.
@@ -556,33 +581,37 @@ __global__ __launch_bounds__(64) void encode_token_kernel(
     alpha += blockIdx.x * alpha_bstride;
   }
   const int head = blockIdx.y;
-  const HeadParams* hp = head_params(params, head);
-  const int lane = threadIdx.x;
-  const int rbytes = hp->record_bytes;
-  if (lane < kRecWords) rec[lane] = 0u;
+  if (threadIdx.x < kRecWords) rec[threadIdx.x] = 0u;
+  __syncthreads();
   const void* xrow = static_cast<const char*>(x) +
                      ((int64_t)blockIdx.x * x_stride + (int64_t)head * kD) * (dtype == AATC_BF16 ? 2 : 4);
-  float xl[2], r[2];
-  load_token_pair(xrow, dtype, xl);
-  exact_r_wave(hp, xl, xrow, dtype, r);
-  __syncthreads();                                  // (the cleared record)
-  const __half a16 = wave_quantize_into(hp, r, rec);
-  if (lane == 0) alpha[(int64_t)head * cap + t] = __half_as_ushort(a16);
-  __syncthreads();
+  encode_token_wave(head_params(params, head), xrow, dtype, layout, codes, alpha, cap, t, head,
+                    rec);
+}
 
-  if (layout == AATC_LAYOUT_RECORDS) {
-    uint32_t* out = reinterpret_cast<uint32_t*>(codes + ((int64_t)head * cap + t) * rbytes);
-    for (int i = lane; i < rbytes / 4; i += 64) out[i] = rec[i];
-  } else {
-    const int p = (int)(t % kTile);
-    const uint32_t bit = 1u << tile_bit(p);
-    uint32_t* tw = reinterpret_cast<uint32_t*>(codes) +
-                   ((int64_t)head * (cap / kTile) + t / kTile) * (16 * rbytes) + tile_word(p);
-    for (int v = lane; v < 8 * rbytes; v += 64) {
-      if ((rec[v >> 5] >> (v & 31)) & 1u)
-        __hip_atomic_fetch_or(tw + 2 * v, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      else
-        __hip_atomic_fetch_and(tw + 2 * v, ~bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// The tokens the matrix-core kernel left with the mark kRedo (failed certificates): one
+// wave per workgroup scans 64 tokens at a time of each KV head and encodes the marked ones
+// exactly.
+__global__ __launch_bounds__(64) void encode_fixup_kernel(
+    const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
+    int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
+    int64_t cap, int64_t pos) {
+  __shared__ uint32_t rec[kRecWords];
+  const int head = blockIdx.y, lane = threadIdx.x;
+  const HeadParams* hp = head_params(params, head);
+  for (int64_t b = (int64_t)blockIdx.x * 64; b < n_tok; b += (int64_t)gridDim.x * 64) {
+    const int64_t t = pos + b + lane;
+    const bool mark = b + lane < n_tok && alpha[(int64_t)head * cap + t] == kRedo;
+    uint64_t m = __builtin_amdgcn_ballot_w64(mark);
+    while (m) {
+      const int64_t tk = pos + b + __builtin_ctzll(m);
+      m &= m - 1;
+      if (lane < kRecWords) rec[lane] = 0u;
+      __syncthreads();
+      const void* xrow = static_cast<const char*>(x) +
+                         ((tk - pos) * x_stride + (int64_t)head * kD) * (dtype == AATC_BF16 ? 2 : 4);
+      encode_token_wave(hp, xrow, dtype, layout, codes, alpha, cap, tk, head, rec);
+      __syncthreads();                              // (rec is cleared for the next token)
     }
   }
 }
@@ -617,6 +646,12 @@ aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_d
       hipLaunchKernelGGL(encode_mfma_kernel<false>, grid, dim3(kEncThreads), 0,
                          (hipStream_t)stream, params, x, n_tok, x_tok_stride, (int)layout,
                          static_cast<uint8_t*>(codes), alpha, cap, pos);
+    if (hipGetLastError() != hipSuccess) return AATC_E_DEVICE;
+    // The tokens whose certificate failed, exactly (stream order: after the kernel above).
+    const dim3 fgrid((unsigned)std::min<int64_t>((n_tok + 63) / 64, 512), (unsigned)n_heads);
+    hipLaunchKernelGGL(encode_fixup_kernel, fgrid, dim3(64), 0, (hipStream_t)stream, params, x,
+                       (int)x_dtype, n_tok, x_tok_stride, (int)layout,
+                       static_cast<uint8_t*>(codes), alpha, cap, pos);
     return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
   }
   dim3 grid((unsigned)n_tiles, (unsigned)n_heads);

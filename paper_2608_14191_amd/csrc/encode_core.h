@@ -78,9 +78,24 @@ __device__ inline float wave_max64(float v) {
   return v;
 }
 
-// The exact fallback for one channel: h_c from the token in memory and column c of the
-// integer transform.
-__device__ inline float exact_h_channel(const void* xrow, int dtype, const int32_t* tcol) {
+// The exact fallback for one channel: h_c from the token (element j held by lane j % 64
+// of the wave, in xl[j / 64]) and column c of the integer transform, read 16 entries per
+// round trip.
+__device__ inline float exact_h_channel(const float (&xl)[2], const int32_t* tcol) {
+  // (j is uniform; the register is chosen by j, not per lane: the caller may run this with
+  // some lanes inactive, and readlane reads the chosen register of any lane)
+  return exact_dot_q22_batched(
+      [&](int j) {
+        const int a = __builtin_amdgcn_readlane(__float_as_int(xl[0]), j & 63);
+        const int b = __builtin_amdgcn_readlane(__float_as_int(xl[1]), j & 63);
+        return __int_as_float(j < 64 ? a : b);
+      },
+      reinterpret_cast<const int4*>(tcol), kD);
+}
+
+// The same with the token's elements and the column read one entry at a time from memory:
+// fewer registers (for kernels that call it with much else live), one round trip per entry.
+__device__ inline float exact_h_channel_lean(const void* xrow, int dtype, const int32_t* tcol) {
   return exact_dot_q22([&](int j) { return load_elem(xrow, dtype, j); },
                        [&](int j) { return tcol[j]; }, kD);
 }
@@ -92,6 +107,8 @@ __device__ inline float exact_h_channel(const void* xrow, int dtype, const int32
 // 128 2^-53 (1 + tiny) sum_j |x_j Tq_jc| of the exact sum; where that interval, scaled by
 // 2^-22, rounds to one fp32 number it is h_c, elsewhere the exact accumulator of
 // exact_dot.h decides.
+// LEAN selects the exact routine's register-light form.
+template <bool LEAN = false>
 __device__ inline void exact_r_wave(const HeadParams* hp, const float (&xl)[2],
                                     const void* xrow, int dtype, float (&r)[2]) {
   const int lane = threadIdx.x & 63;
@@ -128,7 +145,10 @@ __device__ inline void exact_r_wave(const HeadParams* hp, const float (&xl)[2],
     const double bb = b * (1.0 + 0x1p-48) + fabs(sv) * 0x1p-51 + 0x1p-1060;
     const float lo = (float)(sv - bb), hi = (float)(sv + bb);
     float h = lo;
-    if (lo != hi) h = exact_h_channel(xrow, dtype, hp->Tqt + c * kD);
+    // (a dropped channel's r is 0 whatever h is)
+    if (lo != hi && hp->bits[c] > 0)
+      h = LEAN ? exact_h_channel_lean(xrow, dtype, hp->Tqt + c * kD)
+               : exact_h_channel(xl, hp->Tqt + c * kD);
     r[i] = h * hp->inv_s[c];
   }
 }
@@ -151,9 +171,20 @@ __device__ inline bool wave_certify(const HeadParams* hp, const float (&r)[2], f
   const float amax = wave_max64(m);
   const __half a16 = token_alpha(amax);
   const float inv = inverse_alpha(a16);
-  const float ma = eh * hp->inv_s_max * (1.f + 0x1p-20f) + 0x1p-21f * amax + 0x1p-140f;
-  bool ok = __half_as_ushort(token_alpha(fmaxf(amax - ma, 0.f))) ==
-            __half_as_ushort(token_alpha(amax + ma));
+  // The range of the exact max |r_c|: each r_c within eh / s_c of its computed value (plus
+  // the fp32 roundings, the 2^-21 amax slack).
+  float lo = 0.f, hi = 0.f;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float er = eh * hp->inv_s[lane + 64 * i] * (1.f + 0x1p-20f);
+    const float ar = b[i] > 0 ? fabsf(r[i]) : 0.f;
+    lo = fmaxf(lo, ar - er);
+    hi = fmaxf(hi, ar + er);
+  }
+  lo = wave_max64(lo) - 0x1p-21f * amax;
+  hi = wave_max64(hi) + 0x1p-21f * amax + 0x1p-140f;
+  bool ok = __half_as_ushort(token_alpha(fmaxf(lo, 0.f))) ==
+            __half_as_ushort(token_alpha(hi));
   const float ea = eh * inv;
   const bool midrise = hp->quantizer == AATC_QUANT_MIDRISE;
 #pragma unroll

@@ -32,34 +32,28 @@ AATC_HD inline uint32_t acc_word(const uint32_t (&u)[kAccWords], int i) {
   return r;
 }
 
-// fl32(sum_{j < n} x_j Tq_j 2^-22) exactly rounded.  x_j = xf(j) (any finite fp32 value),
-// Tq_j = tq(j) (integers, |Tq_j| <= 2^22), n <= 128.
-template <typename XF, typename TQ>
-AATC_HD inline float exact_dot_q22(XF xf, TQ tq, int n) {
-  int64_t w[kAccWords];
+// Adds x Tq 2^-22 (x any finite fp32 value, |Tq| <= 2^22) to the accumulator, exactly.
+AATC_HD inline void acc_add(int64_t (&w)[kAccWords], float xv, int32_t t) {
+  uint32_t bits;
+  __builtin_memcpy(&bits, &xv, 4);
+  const uint32_t ef = (bits >> 23) & 255u;
+  const uint64_t m = ef ? ((bits & 0x7fffffu) | 0x800000u) : (bits & 0x7fffffu);
+  const int e = ef ? (int)ef - 150 : -149;            // x = +-m 2^e
+  const uint64_t p = m * (uint64_t)(t < 0 ? -(int64_t)t : (int64_t)t);   // < 2^46
+  const bool neg = ((bits >> 31) != 0u) != (t < 0);
+  const int k = e - 22 + kAccLsb;                     // bit position of p's lsb, 0 .. 253
 #pragma unroll
-  for (int i = 0; i < kAccWords; ++i) w[i] = 0;
-#pragma unroll 1
-  for (int j = 0; j < n; ++j) {
-    const float xv = xf(j);
-    uint32_t bits;
-    __builtin_memcpy(&bits, &xv, 4);
-    const uint32_t ef = (bits >> 23) & 255u;
-    const uint64_t m = ef ? ((bits & 0x7fffffu) | 0x800000u) : (bits & 0x7fffffu);
-    const int e = ef ? (int)ef - 150 : -149;          // x = +-m 2^e
-    const int32_t t = tq(j);
-    const uint64_t p = m * (uint64_t)(t < 0 ? -(int64_t)t : (int64_t)t);   // < 2^46
-    const bool neg = ((bits >> 31) != 0u) != (t < 0);
-    const int k = e - 22 + kAccLsb;                   // bit position of p's lsb, 0 .. 253
-#pragma unroll
-    for (int i = 0; i < kAccWords; ++i) {
-      const int sh = k - 32 * i;
-      uint64_t s = 0;
-      if (sh >= 0 && sh < 32) s = (p << sh) & 0xffffffffull;
-      else if (sh < 0 && sh > -64) s = (p >> (-sh)) & 0xffffffffull;
-      w[i] += neg ? -(int64_t)s : (int64_t)s;         // |w_i| < 2^39
-    }
+  for (int i = 0; i < kAccWords; ++i) {
+    const int sh = k - 32 * i;
+    uint64_t s = 0;
+    if (sh >= 0 && sh < 32) s = (p << sh) & 0xffffffffull;
+    else if (sh < 0 && sh > -64) s = (p >> (-sh)) & 0xffffffffull;
+    w[i] += neg ? -(int64_t)s : (int64_t)s;           // |w_i| < 2^39
   }
+}
+
+// The accumulator's value rounded once to fp32 (nearest, ties to even, with subnormals).
+AATC_HD inline float acc_round(int64_t (&w)[kAccWords]) {
   // Carries: words 0..8 into [0, 2^32), the sign in the top word.
 #pragma unroll
   for (int i = 0; i < kAccWords - 1; ++i) {
@@ -101,5 +95,42 @@ AATC_HD inline float exact_dot_q22(XF xf, TQ tq, int n) {
   const float r = ldexpf((float)mant, L - kAccLsb);   // inf beyond the fp32 range
   return neg ? -r : r;
 }
+
+// fl32(sum_{j < n} x_j Tq_j 2^-22) exactly rounded.  x_j = xf(j) (any finite fp32 value),
+// Tq_j = tq(j) (integers, |Tq_j| <= 2^22), n <= 128.
+template <typename XF, typename TQ>
+AATC_HD inline float exact_dot_q22(XF xf, TQ tq, int n) {
+  int64_t w[kAccWords];
+#pragma unroll
+  for (int i = 0; i < kAccWords; ++i) w[i] = 0;
+#pragma unroll 1
+  for (int j = 0; j < n; ++j) acc_add(w, xf(j), tq(j));
+  return acc_round(w);
+}
+
+#if defined(__HIPCC__)
+// The same sum with Tq read from 16-byte-aligned memory, 16 entries per round trip (the
+// four loads of a group are issued together), n a multiple of 16.
+template <typename XF>
+__device__ inline float exact_dot_q22_batched(XF xf, const int4* tq, int n) {
+  int64_t w[kAccWords];
+#pragma unroll
+  for (int i = 0; i < kAccWords; ++i) w[i] = 0;
+#pragma unroll 1
+  for (int j0 = 0; j0 < n; j0 += 16) {
+    int4 v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = tq[j0 / 4 + q];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      acc_add(w, xf(j0 + 4 * q), v[q].x);
+      acc_add(w, xf(j0 + 4 * q + 1), v[q].y);
+      acc_add(w, xf(j0 + 4 * q + 2), v[q].z);
+      acc_add(w, xf(j0 + 4 * q + 3), v[q].w);
+    }
+  }
+  return acc_round(w);
+}
+#endif
 
 }  // namespace aatc
