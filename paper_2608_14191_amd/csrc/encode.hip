@@ -119,39 +119,52 @@ __global__ __launch_bounds__(kEncThreads) void encode_exact_kernel(
 // ---------------------------------------------------------------------------------------
 // The bulk encode on the matrix cores.
 //
-// Per token, X_j = rint(x_j 2^S) with S such that max |X| lies in [2^21, 2^22), and the
-// integer transform Tq = T 2^22 (|Tq| <= 2^22).  Both split into balanced int8 limbs,
-// X = 2^16 X2 + 2^8 X1 + X0 and Tq = 2^16 T2 + 2^8 T1 + T0 (|X2|, |T2| <= 64, the others
-// in [-128, 127]), and the nine limb products go to v_mfma_i32_16x16x64_i8 in five int32
-// sums by weight, S_k = sum over a + b = k of sum_j X_a T_b (each below 2^23, exact).
-// H = sum_k 2^(8k) S_k = sum_j X_j Tq_jc is below 2^51 and is formed exactly in fp64.
+// Per token, S is chosen with max |x_j| 2^S in [2^21, 2^22) and X_j is x_j 2^S rounded to
+// an integer; the integer transform is Tq = T 2^22 (|Tq| <= 2^22).  Both split into int8
+// limbs, X = 2^16 X2 + 2^8 X1 + X0 and Tq = 2^16 T2 + 2^8 T1 + T0 (X0, X1, T0, T1 in
+// [-128, 127], |X2|, |T2| <= 64), and the nine limb products go to
+// v_mfma_i32_16x16x64_i8 in five int32 sums by weight, S_k = sum over a + b = k of
+// sum_j X_a T_b (each below 2^23, exact).  H = sum_k 2^(8k) S_k = sum_j X_j Tq_jc is below
+// 2^51 and is formed exactly in fp64.
 //   - If every X_j equals x_j 2^S (the token is exact in fixed point), H 2^-(S+22) is the
-//     exact h and one rounding gives the canonical result.
-//   - Otherwise |h - H 2^-(S+22)| <= E 2^-S with E = sum_j |x_j 2^S - X_j|.  The token's
-//     scale and codes are certified against that bound: alpha if the fp16 rounding of the
-//     largest |r| cannot change within it, each code if its fp32 quantizer input lies
-//     farther than the bound (plus the fp32 roundings of both evaluations) from a rounding
-//     boundary.  A token that fails is encoded again by the exact one-wave routine.
-// One workgroup of four waves takes 64-token tiles of one KV head in a grid-stride loop
-// (the limb tables of the head's transform are built once per workgroup); wave w takes
-// tokens 16 w .. 16 w + 15 against all 128 channels.  Lane 16 kg + n reads token n's
-// elements j = 64 kc + 16 kg .. + 15 (kc = 0, 1): the B operand columns; the A operand lane
+//     exact h.  With k = S + 22 in [0, 100] every intermediate below is a normal fp32
+//     number (or zero), so the power of two leaves the roundings: u_c = fl32(fl32(H) / s_c)
+//     is r_c 2^k, alpha is the fp16 rounding of max |u| 2^-k and the quantizer input is
+//     fl32(u_c (2^-k / alpha)), bit for bit the canonical sequence.
+//   - Otherwise |H - H_exact| <= E 2^22 with E = sum_j |x_j 2^S - X_j|.  The token's scale
+//     and codes are certified against that bound: alpha if the fp16 rounding of the largest
+//     |r| cannot change within it, each code if its fp32 quantizer input lies farther than
+//     the bound (plus the fp32 roundings of both evaluations) from a rounding boundary.
+// Tokens that fail, and tokens whose k is out of range, get the scale mark kRedo;
+// encode_fixup_kernel, launched next on the stream, encodes them exactly.
+//
+// A workgroup of twelve waves shares the limb tables of one KV head's transform (48 KiB of
+// LDS, built once).  After that each wave works alone, with no workgroup barrier, on
+// 32-token units (half a 64-token tile): two groups of 16 tokens against all 128 channels,
+// codes OR-ed into the wave's own LDS record rows, then the unit's records, or its half of
+// the tile's bit-transposed words, written out.  Lane 16 kg + n holds token n's elements
+// j = 64 kc + 16 kg .. + 15 (kc = 0, 1): the B operand columns; the A operand lane
 // (channel 16 ct + n) reads the same j of row c of the limb tables.  The products leave
-// lane 16 kg + n with channels 16 ct + 4 kg + i, i < 4, of its own token, so a lane's four
-// consecutive codes go into the record as one bit field.
+// lane 16 kg + n with channels 16 ct + 4 kg + i, i < 4, of its own token: four consecutive
+// codes, one bit field of the record.
 // Needs 16-byte aligned token rows (checked by the launcher).
 // ---------------------------------------------------------------------------------------
 // Limb tables in matrix-core operand order: the 16 bytes lane l of a wave feeds for
 // channel tile ct and k half kc sit at ((2 ct + kc) 64 + l) 16, so every operand read is one
 // contiguous 1 KiB per wave (no bank conflicts).
-constexpr int kTbBytes = 8 * 2 * 64 * 16;       // one limb of the 128 x 128 transform
+constexpr int kTbBytes = 8 * 2 * 64 * 16;        // one limb of the 128 x 128 transform
+constexpr int kMW = 12;                           // waves per matrix-core workgroup
+constexpr int kMThreads = 64 * kMW;
+constexpr int kUnit = 32;                         // tokens per wave work unit
+constexpr int kNarrowWords = kD * 8 / 32;         // largest record of codes up to 8 bits
+constexpr int kStage = kNarrowWords + 1;          // LDS record row stride (one word of padding)
+// X + kXBias (2^15 + 2^7) carries the limbs as bytes: X0 = byte 0 - 128, X1 = byte 1 - 128,
+// X2 = byte 2 (signed).
+constexpr int kXBias = 32896;
 
 typedef int ev4i __attribute__((ext_vector_type(4)));
+typedef unsigned short eu2 __attribute__((ext_vector_type(2)));
 
-template <int CTRL>
-__device__ inline float enc_dpp(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
-}
 // Maximum / sum over lanes l, l ^ 16, l ^ 32 and l ^ 48 (the gfx950 row swaps): the four
 // lanes of one token.
 __device__ inline float enc_cross_row_max(float v) {
@@ -166,6 +179,25 @@ __device__ inline float enc_cross_row_sum(float v) {
   r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
+__device__ inline uint32_t enc_cross_row_umax(uint32_t v) {
+  auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = max((uint32_t)r[0], (uint32_t)r[1]);
+  r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return max((uint32_t)r[0], (uint32_t)r[1]);
+}
+__device__ inline uint32_t enc_cross_row_umin(uint32_t v) {
+  auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = min((uint32_t)r[0], (uint32_t)r[1]);
+  r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return min((uint32_t)r[0], (uint32_t)r[1]);
+}
+
+// Orders one wave's LDS accesses across its lanes (a wave's LDS instructions execute in
+// issue order; this keeps the compiler from moving accesses across the point).
+__device__ inline void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
 
 // One stage of a 32 x 32 bit-matrix transpose over the 32 lanes of each half wave (lane i
 // holds row i): blocks of S bits are exchanged with lane i ^ S.
@@ -175,39 +207,118 @@ __device__ inline uint32_t bit_transpose_stage(uint32_t x, int lane) {
   return (lane & S) ? ((x & ~M) | ((y >> S) & M)) : ((x & M) | ((y & M) << S));
 }
 
-template <bool BF16>
-__device__ inline void load_token_elems(const void* x, int64_t base, int kg, float (&xv)[2][16]) {
+// This lane's 32 elements of a token: the 16 at j = 64 kc + 16 kg .. + 15 for kc = 0, 1.
+template <bool BF16> struct Chunk;
+template <> struct Chunk<true> {
+  uint4 w[2][2];                                   // [kc][half]: bf16 pairs, low half first
+  __device__ void load(const void* x, int64_t base, int kg) {
 #pragma unroll
-  for (int kc = 0; kc < 2; ++kc) {
-    if constexpr (BF16) {
+    for (int kc = 0; kc < 2; ++kc) {
       const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(x) + base +
                                                       64 * kc + 16 * kg);
-      const uint4 u[2] = {p[0], p[1]};
+      w[kc][0] = p[0];
+      w[kc][1] = p[1];
+    }
+  }
+  __device__ void clear() {
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const uint32_t wv[4] = {u[q].x, u[q].y, u[q].z, u[q].w};
+    for (int kc = 0; kc < 2; ++kc) w[kc][0] = w[kc][1] = make_uint4(0u, 0u, 0u, 0u);
+  }
+  __device__ uint32_t word(int kc, int i) const {  // elements 2 i, 2 i + 1
+    const uint4& u = w[kc][i >> 2];
+    const int q = i & 3;
+    return q == 0 ? u.x : q == 1 ? u.y : q == 2 ? u.z : u.w;
+  }
+  __device__ float elem(int kc, int e) const {
+    const uint32_t v = word(kc, e >> 1);
+    return __uint_as_float((e & 1) ? (v & 0xffff0000u) : (v << 16));
+  }
+};
+template <> struct Chunk<false> {
+  float4 w[2][4];
+  __device__ void load(const void* x, int64_t base, int kg) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          xv[kc][8 * q + 2 * e] = __uint_as_float(wv[e] << 16);
-          xv[kc][8 * q + 2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
-        }
-      }
-    } else {
+    for (int kc = 0; kc < 2; ++kc) {
       const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(x) + base +
                                                         64 * kc + 16 * kg);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 f = p[q];
-        xv[kc][4 * q] = f.x, xv[kc][4 * q + 1] = f.y, xv[kc][4 * q + 2] = f.z,
-        xv[kc][4 * q + 3] = f.w;
-      }
+      for (int q = 0; q < 4; ++q) w[kc][q] = p[q];
     }
+  }
+  __device__ void clear() {
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w[kc][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  __device__ float elem(int kc, int e) const {
+    const float4& f = w[kc][e >> 2];
+    const int q = e & 3;
+    return q == 0 ? f.x : q == 1 ? f.y : q == 2 ? f.z : f.w;
+  }
+};
+
+// The token's largest |x_j| (over its four lanes), and whether its fixed-point form may be
+// inexact.  bf16: X_j = x_j 2^S exactly whenever x_j's exponent is at least the largest
+// one's minus 14 (8 significant bits, 22 bits of fixed point), so only tokens with a
+// smaller (or zero, or subnormal) element are flagged.  fp32: always flagged.
+template <bool BF16>
+__device__ inline float chunk_stats(const Chunk<BF16>& c, bool& maybe_inexact) {
+  if constexpr (BF16) {
+    eu2 mx = {0, 0}, mn = {0xffff, 0xffff};
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const eu2 v = __builtin_bit_cast(eu2, c.word(kc, i) & 0x7fff7fffu);
+        mx = __builtin_elementwise_max(mx, v);
+        mn = __builtin_elementwise_min(mn, v);
+      }
+    const uint32_t hi = enc_cross_row_umax(max((uint32_t)mx.x, (uint32_t)mx.y));
+    const uint32_t lo = enc_cross_row_umin(min((uint32_t)mn.x, (uint32_t)mn.y));
+    maybe_inexact = hi != 0u && (lo >> 7) + 14u < (hi >> 7);
+    return __uint_as_float(hi << 16);
+  } else {
+    float m = 0.f;
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) m = fmaxf(m, fabsf(c.elem(kc, e)));
+    maybe_inexact = true;
+    return enc_cross_row_max(m);
   }
 }
 
-// The int8 limb bytes of four integers |v| < 2^22 (or |v| <= 2^22 for the transform):
-// limb 0 = byte 0 of v, limb 1 = byte 1 of v + 128, limb 2 = byte 2 of v + 32896 (the
-// balanced digits: v = 65536 l2 + 256 l1 + l0 with l0, l1 in [-128, 127]).
+// The int8 limbs of X (B operands, byte e of word q: element 4 q + e) from y = X + kXBias
+// (X = y - kXBias is x 2^S rounded toward zero), and with E: this lane's part of
+// E = sum_j |x_j 2^S - X_j| (each term exact).
+template <bool BF16, bool WITH_E>
+__device__ inline void chunk_limbs(const Chunk<BF16>& c, float p2s, ev4i (&A)[3][2], float& E) {
+#pragma unroll
+  for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t y[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float xf = c.elem(kc, 4 * q + e);
+        const int yi = (int)fmaf(xf, p2s, (float)kXBias);
+        y[e] = (uint32_t)yi;
+        if constexpr (WITH_E) E += fabsf(fmaf(xf, p2s, (float)(kXBias - yi)));
+      }
+      // v_perm_b32(a, b, sel): byte k of the result is byte sel_k of {a: 4..7, b: 0..3}
+      const uint32_t p01 = __builtin_amdgcn_perm(y[1], y[0], 0x05010400u);
+      const uint32_t p23 = __builtin_amdgcn_perm(y[3], y[2], 0x05010400u);
+      A[0][kc][q] = (int)(__builtin_amdgcn_perm(p23, p01, 0x05040100u) ^ 0x80808080u);
+      A[1][kc][q] = (int)(__builtin_amdgcn_perm(p23, p01, 0x07060302u) ^ 0x80808080u);
+      A[2][kc][q] = (int)(__builtin_amdgcn_perm(y[1], y[0], 0x0c0c0602u) |
+                          __builtin_amdgcn_perm(y[3], y[2], 0x06020c0cu));
+    }
+}
+
+// The int8 limb bytes of four integers |v| <= 2^22 (the transform): limb 0 = byte 0 of v,
+// limb 1 = byte 1 of v + 128, limb 2 = byte 2 of v + 32896 (the balanced digits:
+// v = 65536 l2 + 256 l1 + l0 with l0, l1 in [-128, 127]).
 __device__ inline void limb_bytes4(const int (&v)[4], uint32_t (&out)[3]) {
   uint32_t y1[4], y2[4];
 #pragma unroll
@@ -215,7 +326,6 @@ __device__ inline void limb_bytes4(const int (&v)[4], uint32_t (&out)[3]) {
     y1[e] = (uint32_t)(v[e] + 128);
     y2[e] = (uint32_t)(v[e] + 32896);
   }
-  // v_perm_b32(a, b, sel): byte k of the result is byte sel_k of the pair {a: 4..7, b: 0..3}
   out[0] = __builtin_amdgcn_perm((uint32_t)v[1], (uint32_t)v[0], 0x0c0c0400u) |
            __builtin_amdgcn_perm((uint32_t)v[3], (uint32_t)v[2], 0x04000c0cu);
   out[1] = __builtin_amdgcn_perm(y1[1], y1[0], 0x0c0c0501u) |
@@ -225,46 +335,45 @@ __device__ inline void limb_bytes4(const int (&v)[4], uint32_t (&out)[3]) {
 }
 
 template <bool BF16>
-__global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
-                          amdgpu_waves_per_eu(2, 2))) void encode_mfma_kernel(
+__global__ __launch_bounds__(kMThreads) void encode_mfma_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int64_t n_tok,
     int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
     int64_t cap, int64_t pos) {
-  static_assert(kEncThreads == 256, "four waves of 16 tokens per 64-token tile");
-  __shared__ __align__(16) int8_t tb[3][kTbBytes];       // [limb][ct][kc][lane][16]
-  __shared__ uint32_t rec[kTile][kRecStride];              // records of the tile's tokens
-  // Channel tables, read per tile by the lanes that hold channels 16 ct + 4 kg + i.
-  __shared__ __align__(16) float tab_is[kD];              // 1 / s_c
-  __shared__ __align__(16) float tab_k[kD];               // 2^(b_c - 1) / s_c (1 + 2^-20)
-  __shared__ __align__(16) float tab_p2[kD];              // 2^(b_c - 1) (1 for b_c = 0)
-  __shared__ __align__(16) float tab_hi[kD];              // 2^(b_c - 1) - 1: largest code
-  __shared__ __align__(16) uint32_t tab_msk[kD];          // 2^b_c - 1
-  __shared__ __align__(16) uint32_t tab_sh[kD];           // bit of c in its group's field
-  __shared__ __align__(16) uint32_t tab_w[kD / 4];        // width of each group of four
-  __shared__ __align__(16) uint16_t tab_o[kD];            // first record bits
+  __shared__ __align__(16) int8_t tb[3][kTbBytes];         // [limb][ct][kc][lane][16]
+  __shared__ uint32_t stage[kMW][kUnit][kStage];           // each wave's record rows
+  // Channel tables, read by the lanes that hold channels 16 ct + 4 kg + i.
+  __shared__ __align__(16) float tab_is[kD];               // 1 / s_c
+  __shared__ __align__(16) float tab_p2[kD];               // 2^(b_c - 1) (1 for b_c = 0)
+  __shared__ __align__(16) float tab_hi[kD];               // 2^(b_c - 1) - 1: largest code
+  __shared__ __align__(16) float tab_k[kD];                // 2^(b_c - 1) / s_c (1 + 2^-20)
+  __shared__ __align__(16) uint32_t tab_sh[kD];            // bit of c in its group's field
+  __shared__ uint32_t tab_bias[kD / 4];                    // sum of 2^(b - 1) << sh
+  __shared__ uint32_t tab_msb[kD / 4];                     // sum of 1 << (sh + b - 1)
+  __shared__ uint32_t tab_w[kD / 4];                       // width of each group of four
+  __shared__ uint16_t tab_o[kD];                           // first record bits
 
   const int head = blockIdx.y;
   const HeadParams* hp = head_params(params, head);
-  const int rwords = hp->record_bytes / 4;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 15, kg = lane >> 4;
-  const int dtype = BF16 ? AATC_BF16 : AATC_F32;
-  // Channels wider than 8 bits: four consecutive codes may not fit one 32-bit field, so
-  // such tensors take the exact one-wave routine per token (uniform over the grid).
+  const int64_t first = pos / kTile, last = (pos + n_tok - 1) / kTile;
+  const int64_t n_units = 2 * (last - first + 1);
   if (hp->max_bits > 8) {
-    for (int i = tid; i < kTile * kRecStride; i += kEncThreads) (&rec[0][0])[i] = 0u;
-    __syncthreads();
-    for (int64_t tile = pos / kTile + blockIdx.x; tile <= (pos + n_tok - 1) / kTile;
-         tile += gridDim.x)
-      exact_tile(hp, x, dtype, n_tok, x_stride, layout, codes, alpha, cap, pos, tile, head, rec);
+    // Codes wider than 8 bits need not fit a four-channel field: every token goes to the
+    // exact routine of encode_fixup_kernel (uniform over the grid).
+    for (int64_t i = (int64_t)blockIdx.x * kMThreads + tid; i < n_tok;
+         i += (int64_t)gridDim.x * kMThreads)
+      alpha[(int64_t)head * cap + pos + i] = kRedo;
     return;
   }
   const bool midrise = hp->quantizer == AATC_QUANT_MIDRISE;
+  const int rwords = hp->record_bytes / 4;
+  // i / rwords = (i rmagic) >> 16 for i < 1024 and rwords <= 32
+  const uint32_t rmagic = rwords ? (65536u + rwords - 1) / rwords : 0u;
 
   // Limb tables of the transposed integer transform: operand slot u = (2 ct + kc) 64 + l
-  // (l = 16 kg + n) holds Tq^T[16 ct + n][64 kc + 16 kg .. + 15]; thread tid fills slots
-  // tid + 256 k.
-  for (int k = 0; k < 4; ++k) {
-    const int u = tid + kEncThreads * k, l = u & 63, ct = u >> 7, kc = (u >> 6) & 1;
+  // (l = 16 kg + n) holds Tq^T[16 ct + n][64 kc + 16 kg .. + 15].
+  for (int u = tid; u < 1024; u += kMThreads) {
+    const int l = u & 63, ct = u >> 7, kc = (u >> 6) & 1;
     const int4* src = reinterpret_cast<const int4*>(hp->Tqt + (16 * ct + (l & 15)) * kD +
                                                     64 * kc + 16 * (l >> 4));
     uint32_t w[3][4];
@@ -287,265 +396,269 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kEncThreads, kEncThreads),
     tab_k[tid] = ldexpf(hp->inv_s[tid], max(b, 1) - 1) * (1.f + 0x1p-20f);
     tab_p2[tid] = ldexpf(1.f, max(b, 1) - 1);
     tab_hi[tid] = ldexpf(1.f, max(b, 1) - 1) - 1.f;
-    tab_msk[tid] = (1u << b) - 1u;
     int sh = 0;
     for (int c = tid & ~3; c < tid; ++c) sh += hp->bits[c];
     tab_sh[tid] = (uint32_t)sh;
     tab_o[tid] = hp->bit_off[tid];
   }
-  if (tid < kD / 4)
-    tab_w[tid] = hp->bits[4 * tid] + hp->bits[4 * tid + 1] + hp->bits[4 * tid + 2] + hp->bits[4 * tid + 3];
-  for (int i = tid; i < kTile * kRecStride; i += kEncThreads) (&rec[0][0])[i] = 0u;
-  // Value tiles: lane p of a wave stands for tile bit position p (word p / 32, bit p % 32),
-  // i.e. token 16 (2 (p / 32) + p % 2) + 4 ((p / 2) % 4) + (p % 32) / 8.
-  const int ptok = 16 * (2 * (lane >> 5) + (lane & 1)) + 4 * ((lane >> 1) & 3) + ((lane & 31) >> 3);
+  if (tid < kD / 4) {
+    uint32_t w = 0u, bias = 0u, msb = 0u;
+    for (int i = 0; i < 4; ++i) {
+      const int b = hp->bits[4 * tid + i];
+      if (b > 0) {
+        bias += (1u << (b - 1)) << w;
+        msb |= 1u << (w + b - 1);
+      }
+      w += b;
+    }
+    tab_w[tid] = w;
+    tab_bias[tid] = bias;
+    tab_msb[tid] = msb;
+  }
+  for (int i = tid; i < kMW * kUnit * kStage; i += kMThreads) (&stage[0][0][0])[i] = 0u;
+  __syncthreads();                                 // (the last workgroup barrier)
 
-  const int64_t first = pos / kTile, last = (pos + n_tok - 1) / kTile;
-  // Token 16 wave + n of the tile: the element loads run one tile ahead.
-  const int tl = 16 * wave + n;
-  float xv[2][16];
-  auto fetch = [&](int64_t tile) {
-    const int64_t t = tile * kTile + tl;
-    if (tile <= last && t >= pos && t < pos + n_tok) {
-      load_token_elems<BF16>(x, (t - pos) * x_stride + (int64_t)head * kD, kg, xv);
-    } else {
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) xv[kc][e] = 0.f;
-    }
+  const int64_t ustep = (int64_t)gridDim.x * kMW;
+  int64_t u = (int64_t)blockIdx.x * kMW + wave;
+  if (u >= n_units) return;
+  uint32_t (*rows)[kStage] = stage[wave];
+  // Group g of unit v: tokens 16 g + n of the unit; the loads run one group ahead.
+  Chunk<BF16> nxt;
+  auto fetch = [&](int64_t v, int g) {
+    const int64_t t = (first + (v >> 1)) * kTile + 32 * (v & 1) + 16 * g + n;
+    if (v < n_units && t >= pos && t < pos + n_tok)
+      nxt.load(x, (t - pos) * x_stride + (int64_t)head * kD, kg);
+    else
+      nxt.clear();
   };
-  fetch(first + blockIdx.x);
-  for (int64_t tile = first + blockIdx.x; tile <= last; tile += gridDim.x) {
-    const int64_t tile_base = tile * kTile;
-    const int64_t t_begin = max(tile_base, pos);
-    const int64_t t_end = min(tile_base + kTile, pos + n_tok);
-    const bool valid = tile_base + tl >= t_begin && tile_base + tl < t_end;
-    // (1) The token's fixed-point shift (max over its 128 elements: 4 lanes).
-    float m = 0.f;
+  fetch(u, 0);
+  for (; u < n_units; u += ustep) {
+    const int64_t tile = first + (u >> 1);
+    const int W = (int)(u & 1);
+    const int64_t ubase = tile * kTile + 32 * W;
+    const int lo = (int)max<int64_t>(pos - ubase, 0);
+    const int hi = (int)min<int64_t>(pos + n_tok - ubase, kUnit);
+#pragma unroll 1
+    for (int g = 0; g < 2; ++g) {
+      const Chunk<BF16> cur = nxt;
+      if (g == 0) fetch(u, 1);
+      else fetch(u + ustep, 0);
+      const int tu = 16 * g + n;
+      const bool valid = tu >= lo && tu < hi;
+      // (1) The token's fixed-point shift and exactness flag.
+      bool maybe = false;
+      const int S = token_shift(chunk_stats<BF16>(cur, maybe));
+      const int k = S + kTFrac;
+      const bool k_ok = k >= 0 && k <= 100;
+      const float p2s = ldexpf(1.f, min(max(S, -kTFrac), 100 - kTFrac));
+      const bool cert = __builtin_amdgcn_ballot_w64(maybe) != 0ull;
+      // (2) The limbs of X as B operands, and E in waves with a flagged token.
+      ev4i A[3][2];
+      float E = 0.f;
+      if (cert) chunk_limbs<BF16, true>(cur, p2s, A, E);
+      else chunk_limbs<BF16, false>(cur, p2s, A, E);
+      // (3) Two channel tiles at a time: the five limb-product sums, H exactly, then
+      //     u_c = fl32(fl32(H) / s_c) for channels 16 ct + 4 kg + i of this token.
+      float uv[8][4], am = 0.f;
+      // (an opaque zero in the operand addresses: the tables are the same for every group,
+      // and loads hoisted out of the loop would hold 192 registers)
+      int tb0;
+      asm volatile("s_mov_b32 %0, 0" : "=s"(tb0));
 #pragma unroll
-    for (int kc = 0; kc < 2; ++kc)
+      for (int cp = 0; cp < 4; ++cp) {
+        ev4i s[5][2];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) m = fmaxf(m, fabsf(xv[kc][e]));
-    const int shift = token_shift(enc_cross_row_max(m));
-    // (2) The limbs of X = rint(x 2^shift) as B operands (byte e: element e), and this
-    //     lane's part of E = sum_j |x_j 2^shift - X_j| (exact: each term is).
-    ev4i A[3][2];
-    float E = 0.f;
+        for (int uu = 0; uu < 2; ++uu)
 #pragma unroll
-    for (int kc = 0; kc < 2; ++kc)
+          for (int kk = 0; kk < 5; ++kk) s[kk][uu] = (ev4i){0, 0, 0, 0};
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        int X[4];
+        for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float v = ldexpf(xv[kc][4 * q + e], shift);
-          const float vr = rintf(v);
-          X[e] = (int)vr;
-          E += fabsf(v - vr);
-        }
-        uint32_t lb[3];
-        limb_bytes4(X, lb);
+          for (int uu = 0; uu < 2; ++uu) {
+            const int o = 16 * ((2 * (2 * cp + uu) + kc) * 64 + lane) + tb0;
+            const ev4i b0 = *reinterpret_cast<const ev4i*>(&tb[0][o]);
+            const ev4i b1 = *reinterpret_cast<const ev4i*>(&tb[1][o]);
+            const ev4i b2 = *reinterpret_cast<const ev4i*>(&tb[2][o]);
+            s[4][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b2, A[2][kc], s[4][uu], 0, 0, 0);
+            s[3][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b2, A[1][kc], s[3][uu], 0, 0, 0);
+            s[2][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b2, A[0][kc], s[2][uu], 0, 0, 0);
+            s[1][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A[0][kc], s[1][uu], 0, 0, 0);
+            s[0][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A[0][kc], s[0][uu], 0, 0, 0);
+            s[3][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A[2][kc], s[3][uu], 0, 0, 0);
+            s[2][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A[1][kc], s[2][uu], 0, 0, 0);
+            s[1][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A[1][kc], s[1][uu], 0, 0, 0);
+            s[2][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A[2][kc], s[2][uu], 0, 0, 0);
+          }
 #pragma unroll
-        for (int l = 0; l < 3; ++l) A[l][kc][q] = (int)lb[l];
-      }
-    fetch(tile + gridDim.x);                      // the next tile's elements, in flight
-    if (tile == first + blockIdx.x) __syncthreads();   // (the limb and channel tables)
-    // The token's fixed-point error bound: |h_c - h~_c| <= eh for every channel (|T| <= 1).
-    // Waves with an inexact token certify their codes (below).
-    const float Et = enc_cross_row_sum(E);
-    const bool cert = __builtin_amdgcn_ballot_w64(Et > 0.f) != 0ull;
-    const float eh = ldexpf(Et * (1.f + 0x1p-16f), -shift);
-    // (3) Four channel tiles at a time: the five limb-product sums, H exactly, then
-    //     r_c = fl32(fl32(H 2^-(S+22)) / s_c) for channels 16 ct + 4 kg + i of this token.
-    //     With a certificate, also the range of the exact max |r_c|: each r_c is within
-    //     eh / s_c (plus fp32 roundings) of its computed value.
-    float r[8][4], am = 0.f, alo = 0.f, ahi = 0.f;
+        for (int uu = 0; uu < 2; ++uu) {
+          const int ct = 2 * cp + uu, c0 = 16 * ct + 4 * kg;
+          const float4 is4 = *reinterpret_cast<const float4*>(&tab_is[c0]);
+          const float isv[4] = {is4.x, is4.y, is4.z, is4.w};
 #pragma unroll
-    for (int c4 = 0; c4 < 8; c4 += 4) {
-      ev4i s[5][4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int k = 0; k < 5; ++k) s[k][u] = (ev4i){0, 0, 0, 0};
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int o = 16 * ((2 * (c4 + u) + kc) * 64 + lane);
-          const ev4i b0 = *reinterpret_cast<const ev4i*>(&tb[0][o]);
-          const ev4i b1 = *reinterpret_cast<const ev4i*>(&tb[1][o]);
-          const ev4i b2 = *reinterpret_cast<const ev4i*>(&tb[2][o]);
-          s[4][u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b2, A[2][kc], s[4][u], 0, 0, 0);
-          s[3][u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b2, A[1][kc], s[3][u], 0, 0, 0);
-          s[2][u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b2, A[0][kc], s[2][u], 0, 0, 0);
-          s[1][u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A[0][kc], s[1][u], 0, 0, 0);
-          s[0][u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A[0][kc], s[0][u], 0, 0, 0);
-          s[3][u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A[2][kc], s[3][u], 0, 0, 0);
-          s[2][u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A[1][kc], s[2][u], 0, 0, 0);
-          s[1][u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A[1][kc], s[1][u], 0, 0, 0);
-          s[2][u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A[2][kc], s[2][u], 0, 0, 0);
-        }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int ct = c4 + u, c0 = 16 * ct + 4 * kg;
-        const float4 is4 = *reinterpret_cast<const float4*>(&tab_is[c0]);
-        const float isv[4] = {is4.x, is4.y, is4.z, is4.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          // H = 2^16 (2^8 (2^8 S4 + S3) + S2) + (2^8 S1 + S0): exact in fp64 (< 2^51).
-          const int hi = s[4][u][i] * 256 + s[3][u][i];
-          const int lo = s[1][u][i] * 256 + s[0][u][i];
-          const double H = fma(fma((double)hi, 256.0, (double)s[2][u][i]), 65536.0, (double)lo);
-          r[ct][i] = integer_result(H, shift) * isv[i];
-          am = fmaxf(am, fabsf(r[ct][i]));          // (r = 0 on dropped channels)
-          if (cert) {
-            const float er = eh * isv[i] * (1.f + 0x1p-20f);
-            alo = fmaxf(alo, fabsf(r[ct][i]) - er);
-            ahi = fmaxf(ahi, fabsf(r[ct][i]) + er);
+          for (int i = 0; i < 4; ++i) {
+            // H = 2^24 (2^8 S4 + S3) + 2^16 S2 + (2^8 S1 + S0): exact in fp64 (< 2^51)
+            const int hi8 = s[4][uu][i] * 256 + s[3][uu][i];
+            const int lo8 = s[1][uu][i] * 256 + s[0][uu][i];
+            const double H = fma(fma((double)hi8, 256.0, (double)s[2][uu][i]), 65536.0, (double)lo8);
+            uv[ct][i] = (float)H * isv[i];
+            am = fmaxf(am, fabsf(uv[ct][i]));        // (u = 0 on dropped channels)
           }
         }
       }
-      // (one half's accumulators at a time)
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // (4) The token's scale (its 128 channels: 4 lanes), its codes and record: channels
-    //     16 ct + 4 kg .. + 3 are consecutive in the record, one bit field of <= 32 bits.
-    const float amax = enc_cross_row_max(am);
-    const __half a16 = token_alpha(amax);
-    const float inv_a = inverse_alpha(a16);
-    uint32_t field[8];
-    bool uncertain = false;
-    auto codes_of = [&](auto certify, auto mid_rise) {
-      constexpr bool CERT = decltype(certify)::value;
-      constexpr bool MR = decltype(mid_rise)::value;
+      // (4) The token's scale (its 128 channels: 4 lanes), then its codes: channels
+      //     16 ct + 4 kg .. + 3 are consecutive in the record, one bit field of <= 32 bits.
+      const float amax_r = ldexpf(enc_cross_row_max(am), -k);
+      const __half a16 = token_alpha(amax_r);
+      const float inv_ak = ldexpf(inverse_alpha(a16), -k);
+      bool bad = !k_ok;
       float ea = 0.f;
-      if constexpr (CERT) {
-        // The fp16 scale is certain when both ends of the range of the exact max |r_c|
-        // (over the token's four lanes), widened by the fp32 roundings, round alike.
-        // eh = E 2^-S (1 + 2^-16) covers the fp32 sum of E; ldexpf may underflow to 0
-        // only below the absolute slack.
-        const float lo = enc_cross_row_max(alo) - 0x1p-21f * amax;
-        const float hi = enc_cross_row_max(ahi) + 0x1p-21f * amax + 0x1p-140f;
-        uncertain = __half_as_ushort(token_alpha(fmaxf(lo, 0.f))) !=
-                    __half_as_ushort(token_alpha(hi));
-        ea = eh * inv_a;
-      }
+      if (cert) {
+        // |H - H_exact| <= eH (with the (1 + 2^-20) of the fp32 products below); the range of
+        // the exact max |r| widened by the fp32 roundings must round to one fp16 scale.
+        const float Et = enc_cross_row_sum(E);
+        const float eH = (Et + 0x1p-143f) * (1.f + 0x1p-16f) * 0x1p22f * (1.f + 0x1p-20f);
+        float alo = 0.f, ahi = 0.f;
 #pragma unroll
-      for (int ct = 0; ct < 8; ++ct) {
-        const int c0 = 16 * ct + 4 * kg;
-        const float4 p4 = *reinterpret_cast<const float4*>(&tab_p2[c0]);
-        const float4 h4 = *reinterpret_cast<const float4*>(&tab_hi[c0]);
-        const uint4 m4 = *reinterpret_cast<const uint4*>(&tab_msk[c0]);
-        const uint4 s4 = *reinterpret_cast<const uint4*>(&tab_sh[c0]);
-        const float p2[4] = {p4.x, p4.y, p4.z, p4.w}, hv[4] = {h4.x, h4.y, h4.z, h4.w};
-        const uint32_t mk[4] = {m4.x, m4.y, m4.z, m4.w}, sh[4] = {s4.x, s4.y, s4.z, s4.w};
-        float4 k4;
-        if constexpr (CERT) k4 = *reinterpret_cast<const float4*>(&tab_k[c0]);
-        uint32_t f = 0u;
+        for (int ct = 0; ct < 8; ++ct) {
+          const float4 is4 = *reinterpret_cast<const float4*>(&tab_is[16 * ct + 4 * kg]);
+          const float isv[4] = {is4.x, is4.y, is4.z, is4.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          // The canonical quantizer: xq = fl32(r / alpha) 2^(b-1) (the power of two is
-          // exact), code = floor(xq + 1/2) (midtread) or floor(xq) (midrise) clamped to
-          // [-2^(b-1), 2^(b-1) - 1], b-bit two's complement.  Clamping xq first (the bounds
-          // are integers) and then rounding gives the same code; for midtread the rounding
-          // half up is one v_cvt_rpi_i32_f32 (checked on the hardware against floor(xq) +
-          // (frac >= 1/2): boundary values within 64 ulps of k and k + 1/2 for |k| <= 130,
-          // 2^24 values in all).  Dropped channels have r = 0 and mask 0.
-          const float xq = (r[ct][i] * inv_a) * p2[i];
-          const float xc = __builtin_amdgcn_fmed3f(xq, -p2[i], hv[i]);
-          int code;
-          if constexpr (MR)
-            code = (int)floorf(xc);
-          else
-            asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(code) : "v"(xc));
-          if constexpr (CERT) {
-            const float kf = i == 0 ? k4.x : i == 1 ? k4.y : i == 2 ? k4.z : k4.w;
-            // the bound in x units, plus both evaluations' fp32 roundings and that of
-            // xq + 1/2
-            const float mg = fmaf(kf, ea, fmaf(0x1p-21f, fabsf(xq), 0x1p-22f));
-            uncertain |= boundary_distance(xq, MR) <= mg;
+          for (int i = 0; i < 4; ++i) {
+            ahi = fmaxf(ahi, fmaf(eH, isv[i], fabsf(uv[ct][i])));
+            alo = fmaxf(alo, fmaf(-eH, isv[i], fabsf(uv[ct][i])));
           }
-          f |= ((uint32_t)code & mk[i]) << sh[i];
         }
-        field[ct] = f;
+        const float lo_r = ldexpf(enc_cross_row_max(alo), -k) - 0x1p-21f * amax_r;
+        const float hi_r = ldexpf(enc_cross_row_max(ahi), -k) + 0x1p-21f * amax_r + 0x1p-140f;
+        const bool a_unc = __half_as_ushort(token_alpha(fmaxf(lo_r, 0.f))) !=
+                           __half_as_ushort(token_alpha(hi_r));
+        // Only tokens with E > 0 need the certificate.
+        ea = Et > 0.f ? eH * inv_ak : -1.f;
+        bad |= Et > 0.f && a_unc;
       }
-    };
-    if (midrise) {
-      if (cert) codes_of(std::true_type{}, std::true_type{});
-      else codes_of(std::false_type{}, std::true_type{});
-    } else {
-      if (cert) codes_of(std::true_type{}, std::false_type{});
-      else codes_of(std::false_type{}, std::false_type{});
-    }
-    // A token is redone exactly if any of its four lanes could not certify it.
-    const bool redo = enc_cross_row_max(uncertain ? 1.f : 0.f) > 0.f;
-    if (valid && !redo) {
+      uint32_t field[8];
+      auto codes_of = [&](auto certify, auto mid_rise) {
+        constexpr bool CERT = decltype(certify)::value;
+        constexpr bool MR = decltype(mid_rise)::value;
 #pragma unroll
-      for (int ct = 0; ct < 8; ++ct) {
-        const int c0 = 16 * ct + 4 * kg;
-        const int width = (int)tab_w[c0 >> 2];
-        const int off = tab_o[c0];
-        if (width > 0) {
-          atomicOr(&rec[tl][off >> 5], field[ct] << (off & 31));
-          if ((off & 31) + width > 32) atomicOr(&rec[tl][(off >> 5) + 1], field[ct] >> (32 - (off & 31)));
+        for (int ct = 0; ct < 8; ++ct) {
+          const int c0 = 16 * ct + 4 * kg;
+          const float4 p4 = *reinterpret_cast<const float4*>(&tab_p2[c0]);
+          const float4 h4 = *reinterpret_cast<const float4*>(&tab_hi[c0]);
+          const uint4 s4 = *reinterpret_cast<const uint4*>(&tab_sh[c0]);
+          const float p2[4] = {p4.x, p4.y, p4.z, p4.w}, hv[4] = {h4.x, h4.y, h4.z, h4.w};
+          const uint32_t sh[4] = {s4.x, s4.y, s4.z, s4.w};
+          float4 k4;
+          if constexpr (CERT) k4 = *reinterpret_cast<const float4*>(&tab_k[c0]);
+          // Offset binary (code + 2^(b-1)) summed into the field, the sign bits flipped at
+          // the end: b-bit two's complement codes.
+          uint32_t f = tab_bias[c0 >> 2];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            // The canonical quantizer: xq = fl32(r / alpha) 2^(b-1) (the power of two is
+            // exact), code = floor(xq + 1/2) (midtread) or floor(xq) (midrise) clamped to
+            // [-2^(b-1), 2^(b-1) - 1].  Clamping xq first (the bounds are integers) and then
+            // rounding gives the same code; for midtread the rounding half up is one
+            // v_cvt_rpi_i32_f32 (checked on the hardware against floor(xq) + (frac >= 1/2):
+            // boundary values within 64 ulps of k and k + 1/2 for |k| <= 130, 2^24 values in
+            // all).  Dropped channels have u = 0 and contribute code 0.
+            const float xq = (uv[ct][i] * inv_ak) * p2[i];
+            const float xc = __builtin_amdgcn_fmed3f(xq, -p2[i], hv[i]);
+            int code;
+            if constexpr (MR)
+              asm("v_cvt_flr_i32_f32 %0, %1" : "=v"(code) : "v"(xc));
+            else
+              asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(code) : "v"(xc));
+            f += (uint32_t)code << sh[i];
+            if constexpr (CERT) {
+              const float kf = i == 0 ? k4.x : i == 1 ? k4.y : i == 2 ? k4.z : k4.w;
+              // the bound in x units, plus both evaluations' fp32 roundings and that of
+              // xq + 1/2; the distance to the nearest boundary from the fraction
+              const float mg = fmaf(kf, ea, fmaf(0x1p-21f, fabsf(xq), 0x1p-22f));
+              const float d = fabsf(__builtin_amdgcn_fractf(xq) - 0.5f);
+              bad |= MR ? (d >= 0.5f - mg) : (d <= mg);
+            }
+          }
+          field[ct] = f ^ tab_msb[c0 >> 2];
+        }
+      };
+      if (midrise) {
+        if (cert) codes_of(std::true_type{}, std::true_type{});
+        else codes_of(std::false_type{}, std::true_type{});
+      } else {
+        if (cert) codes_of(std::true_type{}, std::false_type{});
+        else codes_of(std::false_type{}, std::false_type{});
+      }
+      // A token is redone exactly if any of its four lanes could not certify it.
+      const bool redo = enc_cross_row_max(bad ? 1.f : 0.f) > 0.f;
+      if (valid && !redo) {
+#pragma unroll
+        for (int ct = 0; ct < 8; ++ct) {
+          const int c0 = 16 * ct + 4 * kg;
+          const int width = (int)tab_w[c0 >> 2];
+          const int off = tab_o[c0];
+          if (width > 0) {
+            atomicOr(&rows[tu][off >> 5], field[ct] << (off & 31));
+            if ((off & 31) + width > 32) atomicOr(&rows[tu][(off >> 5) + 1], field[ct] >> (32 - (off & 31)));
+          }
         }
       }
-      if (kg == 0) alpha[(int64_t)head * cap + tile_base + tl] = __half_as_ushort(a16);
+      if (valid && kg == 0)
+        alpha[(int64_t)head * cap + ubase + tu] = redo ? kRedo : __half_as_ushort(a16);
     }
-    // (5) A token that failed the certificate keeps a zero record row here and the mark
-    //     kRedo as its scale; encode_fixup_kernel, launched next on the stream, encodes it
-    //     with the exact one-wave routine (a few in ten thousand tokens; done here, each
-    //     would stall the whole workgroup for several dependent memory round trips).
-    if (valid && redo && kg == 0) alpha[(int64_t)head * cap + tile_base + tl] = kRedo;
-    __syncthreads();
-    const int lo = (int)(t_begin - tile_base), hi = (int)(t_end - tile_base);
+    // (5) The unit out of the wave's rows, each word cleared once read.
+    wave_lds_sync();
     if (layout == AATC_LAYOUT_RECORDS) {
-      uint32_t* out = reinterpret_cast<uint32_t*>(codes) + ((int64_t)head * cap + tile_base) * rwords;
-      for (int i = lo * rwords + tid; i < hi * rwords; i += kEncThreads) {
-        out[i] = rec[i / rwords][i % rwords];
-        rec[i / rwords][i % rwords] = 0u;          // (each word read and cleared by one thread)
+      uint32_t* out = reinterpret_cast<uint32_t*>(codes) + ((int64_t)head * cap + ubase) * rwords;
+      for (int i = lo * rwords + lane; i < hi * rwords; i += 64) {
+        const int q = (int)(((uint32_t)i * rmagic) >> 16), r = i - q * rwords;
+        out[i] = rows[q][r];
+        rows[q][r] = 0u;
       }
     } else {
-      // Record word w of the tile's tokens -> tile words 64 w .. 64 w + 63.  Lane p holds
-      // the word of the token at position p; a 32 x 32 bit transpose within each half of
-      // the wave (five butterfly stages on lane-xor swizzles) leaves lane 32 W + b with bit
-      // 32 w + b over the positions of half W: tile word 2 (32 w + b) + W.
+      // Record word w of the unit's tokens -> tile words 64 w + 2 b + W.  Lane q (and
+      // q + 32, one word further) holds the word of the token at half-tile position q,
+      // i.e. token 16 (q % 2) + 4 ((q / 2) % 4) + q / 8 of the unit; a 32 x 32 bit transpose
+      // within each half of the wave leaves lane q with bit q over the 32 positions.
       uint32_t* out = reinterpret_cast<uint32_t*>(codes) +
                       ((int64_t)head * (cap / kTile) + tile) * (16 * rwords * 4);
-      const uint64_t vmask = __builtin_amdgcn_ballot_w64(ptok >= lo && ptok < hi);
-      const uint32_t keep = ~(uint32_t)((lane >> 5) ? (vmask >> 32) : vmask);
-      for (int w = wave; w < rwords; w += kEncThreads / 64) {
-        uint32_t xw = rec[ptok][w];
-        rec[ptok][w] = 0u;                          // (each word read and cleared by one lane)
+      const int q = lane & 31, hs = lane >> 5;
+      const int ptok = 16 * (q & 1) + 4 * ((q >> 1) & 3) + (q >> 3);
+      const uint32_t keep = ~(uint32_t)__builtin_amdgcn_ballot_w64(ptok >= lo && ptok < hi);
+      for (int w = 0; w < rwords; w += 2) {
+        const int ww = w + hs;
+        uint32_t xw = 0u;
+        if (ww < rwords) {
+          xw = rows[ptok][ww];
+          rows[ptok][ww] = 0u;
+        }
         xw = bit_transpose_stage<16, 0x0000ffffu>(xw, lane);
         xw = bit_transpose_stage<8, 0x00ff00ffu>(xw, lane);
         xw = bit_transpose_stage<4, 0x0f0f0f0fu>(xw, lane);
         xw = bit_transpose_stage<2, 0x33333333u>(xw, lane);
         xw = bit_transpose_stage<1, 0x55555555u>(xw, lane);
-        uint32_t* o = out + 64 * w + 2 * (lane & 31) + (lane >> 5);
-        *o = keep ? ((*o & keep) | (xw & ~keep)) : xw;
+        if (ww < rwords) {
+          uint32_t* o = out + 64 * ww + 2 * q + W;
+          *o = keep ? ((*o & keep) | (xw & ~keep)) : xw;
+        }
       }
     }
-    __syncthreads();                                // (the cleared rows before the next tile's bits)
+    wave_lds_sync();                                // (the cleared rows before the next unit)
   }
 }
 
-// One token of one KV head by one wave (the exact one-wave routine): codes into the LDS
-// row `rec` (zero on entry), then into the cache.  Tile bits are set and cleared with
-// device atomics, so tokens that share a tile word may be encoded by other workgroups.
-__device__ __forceinline__ void encode_token_wave(const HeadParams* hp, const void* xrow,
-                                                  int dtype, int layout, uint8_t* codes,
-                                                  uint16_t* alpha, int64_t cap, int64_t t,
-                                                  int head, uint32_t* rec) {
+// Codes and scale of one token from r (lane l: channels l and l + 64, one wave) into the
+// LDS row `rec` (zero on entry, zero again on return), then into the cache.  Tile bits are
+// set and cleared with device atomics, so tokens that share a tile word may be encoded by
+// other waves at the same time.
+__device__ inline void store_token_wave(const HeadParams* hp, const float (&r)[2], int layout,
+                                        uint8_t* codes, uint16_t* alpha, int64_t cap,
+                                        int64_t t, int head, uint32_t* rec) {
   const int lane = threadIdx.x & 63;
   const int rbytes = hp->record_bytes;
-  float xl[2], r[2];
-  load_token_pair(xrow, dtype, xl);
-  exact_r_wave(hp, xl, xrow, dtype, r);
   const __half a16 = wave_quantize_into(hp, r, rec);
   if (lane == 0) alpha[(int64_t)head * cap + t] = __half_as_ushort(a16);
-  __syncthreads();                                  // (the record, one wave)
+  wave_lds_sync();
   if (layout == AATC_LAYOUT_RECORDS) {
     uint32_t* out = reinterpret_cast<uint32_t*>(codes + ((int64_t)head * cap + t) * rbytes);
     for (int i = lane; i < rbytes / 4; i += 64) out[i] = rec[i];
@@ -561,6 +674,9 @@ __device__ __forceinline__ void encode_token_wave(const HeadParams* hp, const vo
         __hip_atomic_fetch_and(tw + 2 * v, ~bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
+  wave_lds_sync();
+  for (int i = lane; i < kRecWords; i += 64) rec[i] = 0u;
+  wave_lds_sync();
 }
 
 // One wave per (token, KV head), for appends of a few tokens.
@@ -581,38 +697,68 @@ __global__ __launch_bounds__(64) void encode_token_kernel(
     alpha += blockIdx.x * alpha_bstride;
   }
   const int head = blockIdx.y;
-  if (threadIdx.x < kRecWords) rec[threadIdx.x] = 0u;
-  __syncthreads();
+  for (int i = threadIdx.x; i < kRecWords; i += 64) rec[i] = 0u;
+  wave_lds_sync();
   const void* xrow = static_cast<const char*>(x) +
                      ((int64_t)blockIdx.x * x_stride + (int64_t)head * kD) * (dtype == AATC_BF16 ? 2 : 4);
-  encode_token_wave(head_params(params, head), xrow, dtype, layout, codes, alpha, cap, t, head,
-                    rec);
+  const HeadParams* hp = head_params(params, head);
+  float xl[2], r[2];
+  load_token_pair(xrow, dtype, xl);
+  exact_r_wave(hp, xl, xrow, dtype, r);
+  store_token_wave(hp, r, layout, codes, alpha, cap, t, head, rec);
 }
 
-// The tokens the matrix-core kernel left with the mark kRedo (failed certificates): one
-// wave per workgroup scans 64 tokens at a time of each KV head and encodes the marked ones
-// exactly.
-__global__ __launch_bounds__(64) void encode_fixup_kernel(
+// The tokens the matrix-core kernel left with the mark kRedo.  A workgroup scans the marks
+// of kFixTokens tokens of one KV head; if any is set it copies the head's integer
+// transform into LDS (row j: Tq[j][c], rows padded by one word, so the copy and the reads
+// are free of bank conflicts) and its four waves encode the marked tokens exactly, one
+// token per wave at a time.
+constexpr int kFixTokens = 4096;
+__global__ __launch_bounds__(256) void encode_fixup_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
     int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
     int64_t cap, int64_t pos) {
-  __shared__ uint32_t rec[kRecWords];
-  const int head = blockIdx.y, lane = threadIdx.x;
+  __shared__ int32_t tq[kD][kD + 1];
+  __shared__ uint16_t list[kFixTokens];
+  __shared__ int n_list;
+  __shared__ uint32_t rec[4][kRecStride];
+  const int head = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const HeadParams* hp = head_params(params, head);
-  for (int64_t b = (int64_t)blockIdx.x * 64; b < n_tok; b += (int64_t)gridDim.x * 64) {
-    const int64_t t = pos + b + lane;
-    const bool mark = b + lane < n_tok && alpha[(int64_t)head * cap + t] == kRedo;
-    uint64_t m = __builtin_amdgcn_ballot_w64(mark);
-    while (m) {
-      const int64_t tk = pos + b + __builtin_ctzll(m);
-      m &= m - 1;
-      if (lane < kRecWords) rec[lane] = 0u;
-      __syncthreads();
-      const void* xrow = static_cast<const char*>(x) +
-                         ((tk - pos) * x_stride + (int64_t)head * kD) * (dtype == AATC_BF16 ? 2 : 4);
-      encode_token_wave(hp, xrow, dtype, layout, codes, alpha, cap, tk, head, rec);
-      __syncthreads();                              // (rec is cleared for the next token)
-    }
+  const int64_t base = (int64_t)blockIdx.x * kFixTokens;
+  if (tid == 0) n_list = 0;
+  __syncthreads();
+  for (int i = tid; i < kFixTokens && base + i < n_tok; i += 256)
+    if (alpha[(int64_t)head * cap + pos + base + i] == kRedo) list[atomicAdd(&n_list, 1)] = (uint16_t)i;
+  __syncthreads();
+  const int cnt = n_list;
+  if (cnt == 0) return;
+  for (int e = tid; e < kD * kD; e += 256) tq[e & (kD - 1)][e >> 7] = hp->Tqt[e];
+  for (int i = tid; i < 4 * kRecStride; i += 256) (&rec[0][0])[i] = 0u;
+  __syncthreads();
+  const size_t esize = dtype == AATC_BF16 ? 2 : 4;
+  for (int k = wave; k < cnt; k += 4) {
+    const int64_t t = pos + base + list[k];
+    const void* xrow = static_cast<const char*>(x) +
+                       ((t - pos) * x_stride + (int64_t)head * kD) * esize;
+    float xl[2], r[2];
+    load_token_pair(xrow, dtype, xl);
+    // The fp64 sums of exact_r_wave, with the transform from LDS.
+    double s[2] = {0.0, 0.0}, a[2] = {0.0, 0.0};
+    auto acc = [&](float xw, int j0) {
+#pragma unroll 8
+      for (int jj = 0; jj < 64; ++jj) {
+        const double xd = (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(xw), jj));
+        const double t0 = (double)tq[j0 + jj][lane], t1 = (double)tq[j0 + jj][lane + 64];
+        s[0] = fma(xd, t0, s[0]);
+        a[0] = fma(fabs(xd), fabs(t0), a[0]);
+        s[1] = fma(xd, t1, s[1]);
+        a[1] = fma(fabs(xd), fabs(t1), a[1]);
+      }
+    };
+    acc(xl[0], 0);
+    acc(xl[1], 64);
+    exact_r_finish(hp, s, a, xl, xrow, dtype, r);
+    store_token_wave(hp, r, layout, codes, alpha, cap, t, head, rec[wave]);
   }
 }
 
@@ -635,21 +781,22 @@ aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_d
   const bool aligned = (reinterpret_cast<uintptr_t>(x) % 16 == 0) &&
                        ((size_t)x_tok_stride * esize) % 16 == 0;
   if (aligned) {
-    // A grid-stride loop of at most 64 workgroups per KV head (each builds the head's limb
-    // tables once; two per compute unit over the 8 heads of the reference shapes).
-    dim3 grid((unsigned)std::min<int64_t>(n_tiles, 64), (unsigned)n_heads);
+    // About one workgroup of twelve waves per compute unit over all KV heads.
+    const int64_t per_head = std::min<int64_t>(std::max(1, 256 / n_heads),
+                                               (2 * n_tiles + kMW - 1) / kMW);
+    dim3 grid((unsigned)per_head, (unsigned)n_heads);
     if (x_dtype == AATC_BF16)
-      hipLaunchKernelGGL(encode_mfma_kernel<true>, grid, dim3(kEncThreads), 0,
+      hipLaunchKernelGGL(encode_mfma_kernel<true>, grid, dim3(kMThreads), 0,
                          (hipStream_t)stream, params, x, n_tok, x_tok_stride, (int)layout,
                          static_cast<uint8_t*>(codes), alpha, cap, pos);
     else
-      hipLaunchKernelGGL(encode_mfma_kernel<false>, grid, dim3(kEncThreads), 0,
+      hipLaunchKernelGGL(encode_mfma_kernel<false>, grid, dim3(kMThreads), 0,
                          (hipStream_t)stream, params, x, n_tok, x_tok_stride, (int)layout,
                          static_cast<uint8_t*>(codes), alpha, cap, pos);
     if (hipGetLastError() != hipSuccess) return AATC_E_DEVICE;
     // The tokens whose certificate failed, exactly (stream order: after the kernel above).
-    const dim3 fgrid((unsigned)std::min<int64_t>((n_tok + 63) / 64, 512), (unsigned)n_heads);
-    hipLaunchKernelGGL(encode_fixup_kernel, fgrid, dim3(64), 0, (hipStream_t)stream, params, x,
+    const dim3 fgrid((unsigned)((n_tok + kFixTokens - 1) / kFixTokens), (unsigned)n_heads);
+    hipLaunchKernelGGL(encode_fixup_kernel, fgrid, dim3(256), 0, (hipStream_t)stream, params, x,
                        (int)x_dtype, n_tok, x_tok_stride, (int)layout,
                        static_cast<uint8_t*>(codes), alpha, cap, pos);
     return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;

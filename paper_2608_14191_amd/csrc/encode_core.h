@@ -100,13 +100,35 @@ __device__ inline float exact_h_channel_lean(const void* xrow, int dtype, const 
                        [&](int j) { return tcol[j]; }, kD);
 }
 
-// r_c = fl32(h_c (1/s_c)) with h_c = fl32(sum_j x_j T_jc) exact, for channels c = lane and
-// lane + 64 of one token, computed by one wave.  xl holds this lane's elements lane and
-// lane + 64 (as fp32); xrow / dtype address the token in memory for the exact fallback.
-// The fp64 sums of x_j Tq_jc (every product exact: at most 24 + 23 bits) are within
-// 128 2^-53 (1 + tiny) sum_j |x_j Tq_jc| of the exact sum; where that interval, scaled by
-// 2^-22, rounds to one fp32 number it is h_c, elsewhere the exact accumulator of
-// exact_dot.h decides.
+// r_c = fl32(h_c (1/s_c)) for channels c = lane and lane + 64 of one token, from the fp64
+// sums s_i = sum_j x_j Tq_jc and a_i = sum_j |x_j Tq_jc| (every product exact: at most
+// 24 + 23 bits; each sum within 128 2^-53 (1 + tiny) a_i of its exact value).  Where that
+// interval, scaled by 2^-22, rounds to one fp32 number it is h_c, elsewhere the exact
+// accumulator of exact_dot.h decides (xl / xrow / dtype: the token, as below).
+template <bool LEAN = false>
+__device__ inline void exact_r_finish(const HeadParams* hp, const double (&s)[2],
+                                      const double (&a)[2], const float (&xl)[2],
+                                      const void* xrow, int dtype, float (&r)[2]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int c = lane + 64 * i;
+    const double sv = ldexp(s[i], -kTFrac), av = ldexp(a[i], -kTFrac);
+    const double b = av * (kD * 0x1p-52);
+    const double bb = b * (1.0 + 0x1p-48) + fabs(sv) * 0x1p-51 + 0x1p-1060;
+    const float lo = (float)(sv - bb), hi = (float)(sv + bb);
+    float h = lo;
+    // (a dropped channel's r is 0 whatever h is)
+    if (lo != hi && hp->bits[c] > 0)
+      h = LEAN ? exact_h_channel_lean(xrow, dtype, hp->Tqt + c * kD)
+               : exact_h_channel(xl, hp->Tqt + c * kD);
+    r[i] = h * hp->inv_s[c];
+  }
+}
+
+// The same for one wave holding the token: xl holds this lane's elements lane and
+// lane + 64 (as fp32), xrow / dtype address the token in memory for the exact fallback;
+// the transform is read from the parameter block, 16 entries per round trip.
 // LEAN selects the exact routine's register-light form.
 template <bool LEAN = false>
 __device__ inline void exact_r_wave(const HeadParams* hp, const float (&xl)[2],
@@ -137,20 +159,7 @@ __device__ inline void exact_r_wave(const HeadParams* hp, const float (&xl)[2],
       }
     }
   }
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int c = lane + 64 * i;
-    const double sv = ldexp(s[i], -kTFrac), av = ldexp(a[i], -kTFrac);
-    const double b = av * (kD * 0x1p-52);
-    const double bb = b * (1.0 + 0x1p-48) + fabs(sv) * 0x1p-51 + 0x1p-1060;
-    const float lo = (float)(sv - bb), hi = (float)(sv + bb);
-    float h = lo;
-    // (a dropped channel's r is 0 whatever h is)
-    if (lo != hi && hp->bits[c] > 0)
-      h = LEAN ? exact_h_channel_lean(xrow, dtype, hp->Tqt + c * kD)
-               : exact_h_channel(xl, hp->Tqt + c * kD);
-    r[i] = h * hp->inv_s[c];
-  }
+  exact_r_finish<LEAN>(hp, s, a, xl, xrow, dtype, r);
 }
 
 // Certificate of a token encoded from the fixed-point transform (one wave, lane l:
