@@ -289,23 +289,33 @@ __device__ inline float chunk_stats(const Chunk<BF16>& c, bool& maybe_inexact) {
   }
 }
 
-// The int8 limbs of X (B operands, byte e of word q: element 4 q + e) from y = X + kXBias
-// (X = y - kXBias is x 2^S rounded toward zero), and with E: this lane's part of
-// E = sum_j |x_j 2^S - X_j| (each term exact).
-template <bool BF16, bool WITH_E>
-__device__ inline void chunk_limbs(const Chunk<BF16>& c, float p2s, ev4i (&A)[3][2], float& E) {
+// The scale of one token for chunk_y: 2^S.
+struct XScale {
+  float f;
+  __device__ explicit XScale(int S) : f(ldexpf(1.f, S)) {}
+};
+
+// y = X + kXBias for elements 4 q .. 4 q + 3 of k half kc, X = x 2^S rounded to an integer
+// (x 2^S + kXBias rounded to fp32, then toward zero: any rounding would do, since E below is
+// taken against these very integers).  Elements with x 2^S an integer give exactly that
+// integer.  -22 <= S <= 78.
+template <bool BF16>
+__device__ inline void chunk_y(const Chunk<BF16>& c, int kc, int q, const XScale& sc,
+                               uint32_t (&y)[4]) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) y[e] = (uint32_t)(int)fmaf(c.elem(kc, 4 * q + e), sc.f, (float)kXBias);
+}
+
+// The int8 limbs of X as B operands (byte e of word q: element 4 q + e): X0 = byte 0 of y
+// - 128, X1 = byte 1 of y - 128, X2 = byte 2 of y (signed), for y = X + kXBias.
+template <bool BF16>
+__device__ inline void chunk_limbs(const Chunk<BF16>& c, const XScale& sc, ev4i (&A)[3][2]) {
 #pragma unroll
   for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       uint32_t y[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float xf = c.elem(kc, 4 * q + e);
-        const int yi = (int)fmaf(xf, p2s, (float)kXBias);
-        y[e] = (uint32_t)yi;
-        if constexpr (WITH_E) E += fabsf(fmaf(xf, p2s, (float)(kXBias - yi)));
-      }
+      chunk_y<BF16>(c, kc, q, sc, y);
       // v_perm_b32(a, b, sel): byte k of the result is byte sel_k of {a: 4..7, b: 0..3}
       const uint32_t p01 = __builtin_amdgcn_perm(y[1], y[0], 0x05010400u);
       const uint32_t p23 = __builtin_amdgcn_perm(y[3], y[2], 0x05010400u);
@@ -314,6 +324,31 @@ __device__ inline void chunk_limbs(const Chunk<BF16>& c, float p2s, ev4i (&A)[3]
       A[2][kc][q] = (int)(__builtin_amdgcn_perm(y[1], y[0], 0x0c0c0602u) |
                           __builtin_amdgcn_perm(y[3], y[2], 0x06020c0cu));
     }
+}
+
+// This lane's part of E = sum_j |x_j 2^S - X_j| for the X_j of chunk_limbs (each term
+// exact: x_j 2^S - X_j has at most 8 (bf16) or 24 (fp32) significant bits; a product
+// below the fp32 range rounds by under 2^-150, which the caller's slack covers).
+template <bool BF16>
+__device__ inline float chunk_err(const Chunk<BF16>& c, const XScale& sc) {
+  float E = 0.f;
+#pragma unroll
+  for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t y[4];
+      chunk_y<BF16>(c, kc, q, sc, y);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        E += fabsf(fmaf(c.elem(kc, 4 * q + e), sc.f, (float)(kXBias - (int)y[e])));
+    }
+  return E;
+}
+
+// A value the compiler cannot see through (keeps work that depends on it inside its branch).
+__device__ inline float opaque(float v) {
+  asm volatile("" : "+v"(v));
+  return v;
 }
 
 // The int8 limb bytes of four integers |v| <= 2^22 (the transform): limb 0 = byte 0 of v,
@@ -349,7 +384,6 @@ __global__ __launch_bounds__(kMThreads) void encode_mfma_kernel(
   __shared__ __align__(16) uint32_t tab_sh[kD];            // bit of c in its group's field
   __shared__ uint32_t tab_bias[kD / 4];                    // sum of 2^(b - 1) << sh
   __shared__ uint32_t tab_msb[kD / 4];                     // sum of 1 << (sh + b - 1)
-  __shared__ uint32_t tab_w[kD / 4];                       // width of each group of four
   __shared__ uint16_t tab_o[kD];                           // first record bits
 
   const int head = blockIdx.y;
@@ -411,7 +445,6 @@ __global__ __launch_bounds__(kMThreads) void encode_mfma_kernel(
       }
       w += b;
     }
-    tab_w[tid] = w;
     tab_bias[tid] = bias;
     tab_msb[tid] = msb;
   }
@@ -422,10 +455,21 @@ __global__ __launch_bounds__(kMThreads) void encode_mfma_kernel(
   int64_t u = (int64_t)blockIdx.x * kMW + wave;
   if (u >= n_units) return;
   uint32_t (*rows)[kStage] = stage[wave];
-  // Group g of unit v: tokens 16 g + n of the unit; the loads run one group ahead.
+  // Where this lane's eight fields go in a record row: byte offset of the first word (bits
+  // 0-7) and bit within it (bits 8-12); a field spills into the next word at most (the
+  // row's padding word takes a zero OR at the end).
+  uint32_t place[8];
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct) {
+    const int off = tab_o[16 * ct + 4 * kg];
+    place[ct] = (uint32_t)(4 * (off >> 5)) | ((uint32_t)(off & 31) << 8);
+  }
+  // Token t = 64 first + 32 v + 16 g + n of unit v (32 v + 16 g + n past the first tile);
+  // the loads run one group ahead.
+  const int64_t t0 = first * kTile + n;
   Chunk<BF16> nxt;
   auto fetch = [&](int64_t v, int g) {
-    const int64_t t = (first + (v >> 1)) * kTile + 32 * (v & 1) + 16 * g + n;
+    const int64_t t = t0 + 32 * v + 16 * g;
     if (v < n_units && t >= pos && t < pos + n_tok)
       nxt.load(x, (t - pos) * x_stride + (int64_t)head * kD, kg);
     else
@@ -450,60 +494,68 @@ __global__ __launch_bounds__(kMThreads) void encode_mfma_kernel(
       const int S = token_shift(chunk_stats<BF16>(cur, maybe));
       const int k = S + kTFrac;
       const bool k_ok = k >= 0 && k <= 100;
-      const float p2s = ldexpf(1.f, min(max(S, -kTFrac), 100 - kTFrac));
+      const XScale sc(min(max(S, -kTFrac), 100 - kTFrac));
       const bool cert = __builtin_amdgcn_ballot_w64(maybe) != 0ull;
-      // (2) The limbs of X as B operands, and E in waves with a flagged token.
+      // (2) The limbs of X as B operands, and in waves with a flagged token the fixed-point
+      //     error sum E of each token (over its four lanes).
       ev4i A[3][2];
-      float E = 0.f;
-      if (cert) chunk_limbs<BF16, true>(cur, p2s, A, E);
-      else chunk_limbs<BF16, false>(cur, p2s, A, E);
-      // (3) Two channel tiles at a time: the five limb-product sums, H exactly, then
-      //     u_c = fl32(fl32(H) / s_c) for channels 16 ct + 4 kg + i of this token.
+      chunk_limbs<BF16>(cur, sc, A);
+      float Et = 0.f;
+      if (cert) Et = opaque(enc_cross_row_sum(chunk_err<BF16>(cur, sc)));
+      // (3) Channel tile by channel tile: the five limb-product sums (18 products), H exactly,
+      //     then u_c = fl32(fl32(H) / s_c) for channels 16 ct + 4 kg + i of this token.  The
+      //     operands of the next k half are read while the products of this one run, and
+      //     the sums of tile ct - 1 are turned into u while those of tile ct accumulate.
       float uv[8][4], am = 0.f;
       // (an opaque zero in the operand addresses: the tables are the same for every group,
       // and loads hoisted out of the loop would hold 192 registers)
       int tb0;
       asm volatile("s_mov_b32 %0, 0" : "=s"(tb0));
+      auto load_b = [&](int q, ev4i (&bq)[3]) {
+        const int o = 16 * ((2 * (q >> 1) + (q & 1)) * 64 + lane) + tb0;
 #pragma unroll
-      for (int cp = 0; cp < 4; ++cp) {
-        ev4i s[5][2];
+        for (int l = 0; l < 3; ++l) bq[l] = *reinterpret_cast<const ev4i*>(&tb[l][o]);
+      };
+      auto products = [&](const ev4i (&bq)[3], int kc, ev4i (&sa)[5]) {
+        sa[4] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bq[2], A[2][kc], sa[4], 0, 0, 0);
+        sa[3] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bq[2], A[1][kc], sa[3], 0, 0, 0);
+        sa[2] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bq[2], A[0][kc], sa[2], 0, 0, 0);
+        sa[1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bq[1], A[0][kc], sa[1], 0, 0, 0);
+        sa[0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bq[0], A[0][kc], sa[0], 0, 0, 0);
+        sa[3] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bq[1], A[2][kc], sa[3], 0, 0, 0);
+        sa[2] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bq[1], A[1][kc], sa[2], 0, 0, 0);
+        sa[1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bq[0], A[1][kc], sa[1], 0, 0, 0);
+        sa[2] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bq[0], A[2][kc], sa[2], 0, 0, 0);
+      };
+      auto to_u = [&](const ev4i (&sa)[5], int ct) {
+        const float4 is4 = *reinterpret_cast<const float4*>(&tab_is[16 * ct + 4 * kg]);
+        const float isv[4] = {is4.x, is4.y, is4.z, is4.w};
 #pragma unroll
-        for (int uu = 0; uu < 2; ++uu)
-#pragma unroll
-          for (int kk = 0; kk < 5; ++kk) s[kk][uu] = (ev4i){0, 0, 0, 0};
-#pragma unroll
-        for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-          for (int uu = 0; uu < 2; ++uu) {
-            const int o = 16 * ((2 * (2 * cp + uu) + kc) * 64 + lane) + tb0;
-            const ev4i b0 = *reinterpret_cast<const ev4i*>(&tb[0][o]);
-            const ev4i b1 = *reinterpret_cast<const ev4i*>(&tb[1][o]);
-            const ev4i b2 = *reinterpret_cast<const ev4i*>(&tb[2][o]);
-            s[4][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b2, A[2][kc], s[4][uu], 0, 0, 0);
-            s[3][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b2, A[1][kc], s[3][uu], 0, 0, 0);
-            s[2][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b2, A[0][kc], s[2][uu], 0, 0, 0);
-            s[1][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A[0][kc], s[1][uu], 0, 0, 0);
-            s[0][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A[0][kc], s[0][uu], 0, 0, 0);
-            s[3][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A[2][kc], s[3][uu], 0, 0, 0);
-            s[2][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b1, A[1][kc], s[2][uu], 0, 0, 0);
-            s[1][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A[1][kc], s[1][uu], 0, 0, 0);
-            s[2][uu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b0, A[2][kc], s[2][uu], 0, 0, 0);
-          }
-#pragma unroll
-        for (int uu = 0; uu < 2; ++uu) {
-          const int ct = 2 * cp + uu, c0 = 16 * ct + 4 * kg;
-          const float4 is4 = *reinterpret_cast<const float4*>(&tab_is[c0]);
-          const float isv[4] = {is4.x, is4.y, is4.z, is4.w};
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            // H = 2^24 (2^8 S4 + S3) + 2^16 S2 + (2^8 S1 + S0): exact in fp64 (< 2^51)
-            const int hi8 = s[4][uu][i] * 256 + s[3][uu][i];
-            const int lo8 = s[1][uu][i] * 256 + s[0][uu][i];
-            const double H = fma(fma((double)hi8, 256.0, (double)s[2][uu][i]), 65536.0, (double)lo8);
-            uv[ct][i] = (float)H * isv[i];
-            am = fmaxf(am, fabsf(uv[ct][i]));        // (u = 0 on dropped channels)
-          }
+        for (int i = 0; i < 4; ++i) {
+          // H = 2^24 (2^8 S4 + S3) + 2^16 S2 + (2^8 S1 + S0): exact in fp64 (< 2^51)
+          const int hi8 = sa[4][i] * 256 + sa[3][i];
+          const int lo8 = sa[1][i] * 256 + sa[0][i];
+          const double H = fma(fma((double)hi8, 256.0, (double)sa[2][i]), 65536.0, (double)lo8);
+          uv[ct][i] = (float)H * isv[i];
+          am = fmaxf(am, fabsf(uv[ct][i]));          // (u = 0 on dropped channels)
         }
+      };
+      {
+        ev4i bq[2][3], sa[2][5];
+        load_b(0, bq[0]);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int ct = q >> 1, kc = q & 1;
+          if (q + 1 < 16) load_b(q + 1, bq[(q + 1) & 1]);
+          __builtin_amdgcn_sched_barrier(0);            // (the reads stay ahead of the products)
+          if (kc == 0) {
+#pragma unroll
+            for (int kk = 0; kk < 5; ++kk) sa[ct & 1][kk] = (ev4i){0, 0, 0, 0};
+          }
+          products(bq[q & 1], kc, sa[ct & 1]);
+          if (kc == 1 && ct > 0) to_u(sa[(ct - 1) & 1], ct - 1);
+        }
+        to_u(sa[1], 7);
       }
       // (4) The token's scale (its 128 channels: 4 lanes), then its codes: channels
       //     16 ct + 4 kg .. + 3 are consecutive in the record, one bit field of <= 32 bits.
@@ -515,8 +567,8 @@ __global__ __launch_bounds__(kMThreads) void encode_mfma_kernel(
       if (cert) {
         // |H - H_exact| <= eH (with the (1 + 2^-20) of the fp32 products below); the range of
         // the exact max |r| widened by the fp32 roundings must round to one fp16 scale.
-        const float Et = enc_cross_row_sum(E);
-        const float eH = (Et + 0x1p-143f) * (1.f + 0x1p-16f) * 0x1p22f * (1.f + 0x1p-20f);
+        // Only tokens with E > 0 need the certificate.
+        const float eH = opaque((Et + 0x1p-143f) * (1.f + 0x1p-16f) * 0x1p22f * (1.f + 0x1p-20f));
         float alo = 0.f, ahi = 0.f;
 #pragma unroll
         for (int ct = 0; ct < 8; ++ct) {
@@ -532,7 +584,6 @@ __global__ __launch_bounds__(kMThreads) void encode_mfma_kernel(
         const float hi_r = ldexpf(enc_cross_row_max(ahi), -k) + 0x1p-21f * amax_r + 0x1p-140f;
         const bool a_unc = __half_as_ushort(token_alpha(fmaxf(lo_r, 0.f))) !=
                            __half_as_ushort(token_alpha(hi_r));
-        // Only tokens with E > 0 need the certificate.
         ea = Et > 0.f ? eH * inv_ak : -1.f;
         bad |= Et > 0.f && a_unc;
       }
@@ -592,15 +643,13 @@ __global__ __launch_bounds__(kMThreads) void encode_mfma_kernel(
       // A token is redone exactly if any of its four lanes could not certify it.
       const bool redo = enc_cross_row_max(bad ? 1.f : 0.f) > 0.f;
       if (valid && !redo) {
+        char* row = reinterpret_cast<char*>(rows[tu]);
 #pragma unroll
         for (int ct = 0; ct < 8; ++ct) {
-          const int c0 = 16 * ct + 4 * kg;
-          const int width = (int)tab_w[c0 >> 2];
-          const int off = tab_o[c0];
-          if (width > 0) {
-            atomicOr(&rows[tu][off >> 5], field[ct] << (off & 31));
-            if ((off & 31) + width > 32) atomicOr(&rows[tu][(off >> 5) + 1], field[ct] >> (32 - (off & 31)));
-          }
+          uint32_t* w0 = reinterpret_cast<uint32_t*>(row + (place[ct] & 0xffu));
+          const uint64_t v = (uint64_t)field[ct] << ((place[ct] >> 8) & 31u);
+          atomicOr(w0, (uint32_t)v);
+          atomicOr(w0 + 1, (uint32_t)(v >> 32));
         }
       }
       if (valid && kg == 0)
@@ -713,7 +762,7 @@ __global__ __launch_bounds__(64) void encode_token_kernel(
 // transform into LDS (row j: Tq[j][c], rows padded by one word, so the copy and the reads
 // are free of bank conflicts) and its four waves encode the marked tokens exactly, one
 // token per wave at a time.
-constexpr int kFixTokens = 4096;
+constexpr int kFixTokens = 512;
 __global__ __launch_bounds__(256) void encode_fixup_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
     int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
@@ -727,12 +776,38 @@ __global__ __launch_bounds__(256) void encode_fixup_kernel(
   const int64_t base = (int64_t)blockIdx.x * kFixTokens;
   if (tid == 0) n_list = 0;
   __syncthreads();
-  for (int i = tid; i < kFixTokens && base + i < n_tok; i += 256)
-    if (alpha[(int64_t)head * cap + pos + base + i] == kRedo) list[atomicAdd(&n_list, 1)] = (uint16_t)i;
+  {
+    // (all sixteen marks of a thread read before any is tested: one round trip)
+    const uint16_t* am = alpha + (int64_t)head * cap + pos + base;
+    uint16_t mv[kFixTokens / 256];
+#pragma unroll
+    for (int m = 0; m < kFixTokens / 256; ++m) {
+      const int i = tid + 256 * m;
+      mv[m] = base + i < n_tok ? am[i] : (uint16_t)0;
+    }
+#pragma unroll
+    for (int m = 0; m < kFixTokens / 256; ++m)
+      if (mv[m] == kRedo) list[atomicAdd(&n_list, 1)] = (uint16_t)(tid + 256 * m);
+  }
   __syncthreads();
   const int cnt = n_list;
   if (cnt == 0) return;
-  for (int e = tid; e < kD * kD; e += 256) tq[e & (kD - 1)][e >> 7] = hp->Tqt[e];
+  {
+    // 16-byte reads, sixteen per thread in flight: entry 4 e4 + i of Tqt is (c, j) =
+    // (e4 / 32, 4 (e4 % 32) + i).
+    const int4* src = reinterpret_cast<const int4*>(hp->Tqt);
+    int4 v[16];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) v[m] = src[tid + 256 * m];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      const int e4 = tid + 256 * m, c = e4 >> 5, j = 4 * (e4 & 31);
+      tq[j][c] = v[m].x;
+      tq[j + 1][c] = v[m].y;
+      tq[j + 2][c] = v[m].z;
+      tq[j + 3][c] = v[m].w;
+    }
+  }
   for (int i = tid; i < 4 * kRecStride; i += 256) (&rec[0][0])[i] = 0u;
   __syncthreads();
   const size_t esize = dtype == AATC_BF16 ? 2 : 4;
@@ -757,7 +832,7 @@ __global__ __launch_bounds__(256) void encode_fixup_kernel(
     };
     acc(xl[0], 0);
     acc(xl[1], 64);
-    exact_r_finish(hp, s, a, xl, xrow, dtype, r);
+    exact_r_finish(hp, s, a, token_lsb(xl), xl, xrow, dtype, r);
     store_token_wave(hp, r, layout, codes, alpha, cap, t, head, rec[wave]);
   }
 }

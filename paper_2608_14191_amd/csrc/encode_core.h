@@ -100,28 +100,55 @@ __device__ inline float exact_h_channel_lean(const void* xrow, int dtype, const 
                        [&](int j) { return tcol[j]; }, kD);
 }
 
+// The exponent of the lowest set bit over a token's nonzero elements (element j held by lane
+// j % 64 of the wave, in xl[j / 64]): every x_j is a multiple of 2^g.  4096 for a zero token.
+__device__ inline int token_lsb(const float (&xl)[2]) {
+  int g = 4096;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const uint32_t b = __float_as_uint(xl[i]) & 0x7fffffffu;
+    if (b != 0u) {
+      const int ef = (int)(b >> 23), m = (int)(b & 0x7fffffu);
+      g = min(g, ef ? ef - 150 + __builtin_ctz((uint32_t)m | 0x800000u) : -149 + __builtin_ctz((uint32_t)m));
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) g = min(g, __shfl_xor(g, o, 64));
+  return g;
+}
+
 // r_c = fl32(h_c (1/s_c)) for channels c = lane and lane + 64 of one token, from the fp64
 // sums s_i = sum_j x_j Tq_jc and a_i = sum_j |x_j Tq_jc| (every product exact: at most
-// 24 + 23 bits; each sum within 128 2^-53 (1 + tiny) a_i of its exact value).  Where that
-// interval, scaled by 2^-22, rounds to one fp32 number it is h_c, elsewhere the exact
-// accumulator of exact_dot.h decides (xl / xrow / dtype: the token, as below).
+// 24 + 23 bits).  Every product, hence every partial sum, is a multiple of 2^g (g from
+// token_lsb); while a_i stays below 2^(53 + g) each of them is an fp64 number, s_i is exact
+// and one rounding gives h_c (ties included).  Otherwise s_i is within 128 2^-53 (1 + tiny)
+// a_i of its exact value: where that interval, scaled by 2^-22, rounds to one fp32 number
+// it is h_c, elsewhere the exact accumulator of exact_dot.h decides (xl / xrow / dtype: the
+// token, as below).
 template <bool LEAN = false>
 __device__ inline void exact_r_finish(const HeadParams* hp, const double (&s)[2],
-                                      const double (&a)[2], const float (&xl)[2],
+                                      const double (&a)[2], int g, const float (&xl)[2],
                                       const void* xrow, int dtype, float (&r)[2]) {
   const int lane = threadIdx.x & 63;
+  // (a_i itself is within 128 2^-53 of the exact sum of |products|)
+  const double lim = ldexp(1.0 - 0x1p-40, 53 + min(g, 900));
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int c = lane + 64 * i;
     const double sv = ldexp(s[i], -kTFrac), av = ldexp(a[i], -kTFrac);
-    const double b = av * (kD * 0x1p-52);
-    const double bb = b * (1.0 + 0x1p-48) + fabs(sv) * 0x1p-51 + 0x1p-1060;
-    const float lo = (float)(sv - bb), hi = (float)(sv + bb);
-    float h = lo;
-    // (a dropped channel's r is 0 whatever h is)
-    if (lo != hi && hp->bits[c] > 0)
-      h = LEAN ? exact_h_channel_lean(xrow, dtype, hp->Tqt + c * kD)
-               : exact_h_channel(xl, hp->Tqt + c * kD);
+    float h;
+    if (a[i] < lim) {
+      h = (float)sv;
+    } else {
+      const double b = av * (kD * 0x1p-52);
+      const double bb = b * (1.0 + 0x1p-48) + fabs(sv) * 0x1p-51 + 0x1p-1060;
+      const float lo = (float)(sv - bb), hi = (float)(sv + bb);
+      h = lo;
+      // (a dropped channel's r is 0 whatever h is)
+      if (lo != hi && hp->bits[c] > 0)
+        h = LEAN ? exact_h_channel_lean(xrow, dtype, hp->Tqt + c * kD)
+                 : exact_h_channel(xl, hp->Tqt + c * kD);
+    }
     r[i] = h * hp->inv_s[c];
   }
 }
@@ -159,7 +186,7 @@ __device__ inline void exact_r_wave(const HeadParams* hp, const float (&xl)[2],
       }
     }
   }
-  exact_r_finish<LEAN>(hp, s, a, xl, xrow, dtype, r);
+  exact_r_finish<LEAN>(hp, s, a, token_lsb(xl), xl, xrow, dtype, r);
 }
 
 // Certificate of a token encoded from the fixed-point transform (one wave, lane l:
