@@ -271,7 +271,8 @@ def cpu_baseline(s, target_seconds=15.0, single_thread_seconds=8.0):
 
 COUNTERS_SUMMARY = os.path.join(ROOT, "profiles", "decode_mfma_llama31_8b_b1_32k_counters.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_14191_amd", "csrc", f)
-                  for f in ("decode.hip", "params.h", "launch.h", "encode_core.h", "abi.cpp")]
+                  for f in ("decode.hip", "params.h", "launch.h", "encode_core.h", "abi.cpp",
+                            "workspace.h", "exact_dot.h")]
 
 
 def kernel_source_hash() -> str:

@@ -24,13 +24,13 @@
 #include "encode_core.h"
 #include "launch.h"
 #include "params.h"
+#include "workspace.h"
 
 namespace aatc {
 namespace {
 
 constexpr int kThreads = 256;                    // generic kernel: four waves
 constexpr int kSplit = 512;                      // tokens per workgroup, generic kernel
-constexpr int kMinSplit = 256;                   // smallest split of either kernel
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kMaxNH = 8;                        // head slots of the MFMA kernel
 constexpr int kRsrcWord3 = 0x00020000;           // raw buffer descriptor word 3 (gfx950)
@@ -41,13 +41,6 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef const __attribute__((address_space(1))) uint32_t* gdword;   // global-memory dword
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v2f __attribute__((ext_vector_type(2)));
-
-struct alignas(16) Partial {   // per (sequence, KV head, split, head-in-group)
-  float m;                     // split max of the log2-domain logits
-  float l;                     // sum of 2^(z - m)
-  float pad_[2];
-  float o[kD];                 // sum of 2^(z - m) h^V (transformed domain, storage channels)
-};
 
 struct DecodeArgs {
   const void* params_k;
@@ -331,42 +324,6 @@ __device__ inline void wait_vmcnt(int n) {
 
 __device__ inline v4i mfma_i8(v4i a, v4i b, v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
-}
-
-// ---------------------------------------------------------------------------------------
-// Workspace: arrival counters per (sequence, KV head), the split partials, and the
-// appended token's transformed coefficients (key then value, per (sequence, KV head)).
-// ---------------------------------------------------------------------------------------
-// Arrival counters sit 256 bytes apart: the device-scope atomics on one cache line
-// serialize, and every split of every (sequence, KV head) arrives at nearly once.
-constexpr int kCtrStride = 64;
-
-// Fused append, per (sequence, KV head): r_c of the key then the value token (2 x 128),
-// then each token's fixed-point error bound eh (0 when exact), padded to 16 bytes.
-constexpr int kAppStride = 2 * kD + 4;
-
-struct WsLayout {
-  size_t counters, partials, append_r, seg, total;
-};
-
-__host__ __device__ inline size_t round256(size_t x) { return (x + 255) / 256 * 256; }
-
-// counter_rows > rows reserves the counters of that many rows, so that the counters keep
-// one place whatever the shape of the call (the static workspace of the no-allocation entry
-// point: counters left at zero by one call are where the next call looks for them).
-inline WsLayout ws_layout(int batch, int n_q_heads, int n_kv_heads, int64_t cap,
-                          int counter_rows = 0) {
-  const size_t rows = (size_t)batch * n_kv_heads;
-  const size_t crows = std::max(rows, (size_t)std::max(counter_rows, 0));
-  const size_t n_splits = (size_t)((cap + kMinSplit - 1) / kMinSplit);
-  WsLayout w;
-  w.counters = 0;
-  w.partials = round256(crows * kCtrStride * sizeof(unsigned));
-  w.append_r = round256(w.partials + (size_t)batch * n_q_heads * n_splits * sizeof(Partial));
-  // the full-precision segment's partial per (sequence, query head)
-  w.seg = round256(w.append_r + rows * kAppStride * sizeof(float));
-  w.total = w.seg + (size_t)batch * n_q_heads * sizeof(Partial);
-  return w;
 }
 
 // Bytes of LDS the merge of an NTHR-thread workgroup needs (at the start of the dynamic

@@ -97,3 +97,28 @@ def test_centered_variance_identity_monte_carlo():
     emp = ((al - abar[:, None]) ** 2).mean(axis=0)
     pred = (1 - 2 * a) * sd ** 2 + np.sum(a ** 2 * sd ** 2)
     np.testing.assert_allclose(emp, pred, rtol=0.01)
+
+
+def test_output_error_terms_sum_to_the_output_change():
+    """o^ - o = E_K + E_V + E_x exactly (the decomposition of the output error, Sec. 4),
+    with the attention weights perturbed through the keys and the values perturbed directly;
+    each term is also checked against its own definition evaluated elementwise."""
+    q, k, v, w_o = _tiny_problem(11)
+    rng = np.random.default_rng(12)
+    dk = 0.05 * rng.standard_normal(k.shape)
+    dv = 0.05 * rng.standard_normal(v.shape)
+    a = theory.softmax(k @ q)
+    a_hat = theory.softmax((k + dk) @ q)
+    da = a_hat - a
+    o = (a @ v) @ w_o
+    o_hat = (a_hat @ (v + dv)) @ w_o
+    e_k, e_v, e_x = theory.output_error_terms(a, da, v, dv, w_o)
+    np.testing.assert_allclose(e_k + e_v + e_x, o_hat - o, rtol=1e-12, atol=1e-14)
+    t = len(a)
+    np.testing.assert_allclose(e_k, sum(da[i] * (v[i] @ w_o) for i in range(t)), rtol=1e-12)
+    np.testing.assert_allclose(e_v, sum(a[i] * (dv[i] @ w_o) for i in range(t)), rtol=1e-12)
+    np.testing.assert_allclose(e_x, sum(da[i] * (dv[i] @ w_o) for i in range(t)), rtol=1e-12)
+    # E_x is second order: halving both perturbations quarters it
+    a_h = theory.softmax((k + dk / 2) @ q)
+    _, _, e_x2 = theory.output_error_terms(a, a_h - a, v, dv / 2, w_o)
+    assert np.linalg.norm(e_x2) < 0.3 * np.linalg.norm(e_x)
