@@ -190,7 +190,7 @@ def run_decode_bench(s, steps, warmup):
     return elapsed, kern_ms, n_copies, out
 
 
-def run_encode_bench(avg_bits, reps=3):
+def run_encode_bench(avg_bits, reps=5):
     """Prefill encode of 65536 tokens x 8 KV heads (K records + V tiles)."""
     import torch
     import paper_2608_14191_amd as P
@@ -222,6 +222,24 @@ def run_encode_bench(avg_bits, reps=3):
     dt = (time.perf_counter() - t0) / reps
     return dict(avg_bits=avg_bits, tokens=L, seconds=dt, tokens_per_s=L / dt,
                 bytes=int(L * H * (2 * 128 * 2 + rk + rv + 4)))
+
+
+# Dense int8 matrix-core peak of the MI355X (ops/s), for the encode's transform products.
+MFMA_I8_PEAK_OPS = 5.0e15
+
+
+def encode_entry(r):
+    """Bench entry of one prefill encode measurement: throughput, its HBM fraction, and the
+    matrix-core rate: the transform is 65536 x 8 heads x 128 x 128 multiply-adds per tensor
+    (K and V), executed as nine int8 limb products each."""
+    macs = 2 * r["tokens"] * 8 * 128 * 128
+    return {"workload": f"llama31_8b_prefill_64k at {r['avg_bits']} bits",
+            "tokens_per_s": round(r["tokens_per_s"], 1),
+            "ms": round(r["seconds"] * 1e3, 3),
+            "hbm_bytes": r["bytes"],
+            "roofline_frac": round(r["bytes"] / r["seconds"] / 1e9 / HBM_PEAK_GBS, 4),
+            "mfma_int8_ops_per_prefill": 2 * 9 * macs,
+            "mfma_frac": round(2 * 9 * macs / r["seconds"] / MFMA_I8_PEAK_OPS, 4)}
 
 
 def cpu_baseline(s, target_seconds=15.0, single_thread_seconds=8.0):
@@ -340,6 +358,8 @@ def main():
                     help="skip the Qwen-shape and long-context decode entries")
     ap.add_argument("--counters", action="store_true",
                     help="eager decodes plus a calibration copy, for rocprofv3 --pmc runs")
+    ap.add_argument("--encode-only", action="store_true",
+                    help="only the prefill encode entries (for rocprofv3 runs of the encode)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -348,6 +368,10 @@ def main():
         sys.exit(2)
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.encode_only:
+        enc = [run_encode_bench(avg) for avg in (2.75, 4.0)]
+        print(json.dumps({"encode": [encode_entry(r) for r in enc]}), flush=True)
+        return
     s = setup_decode(2)
     if args.counters:
         counters_run(s)
@@ -405,12 +429,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": counted_traffic()},
-        "encode": [{"workload": f"llama31_8b_prefill_64k at {r['avg_bits']} bits",
-                    "tokens_per_s": round(r["tokens_per_s"], 1),
-                    "ms": round(r["seconds"] * 1e3, 3),
-                    "hbm_bytes": r["bytes"],
-                    "roofline_frac": round(r["bytes"] / r["seconds"] / 1e9 / HBM_PEAK_GBS, 4)}
-                   for r in enc],
+        "encode": [encode_entry(r) for r in enc],
         "decode_other": other,
     }
     if not args.no_cpu_baseline:
