@@ -388,7 +388,10 @@ __global__ __launch_bounds__(kMThreads) void encode_mfma_kernel(
 
   const int head = blockIdx.y;
   const HeadParams* hp = head_params(params, head);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 15, kg = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, kg = lane >> 4;
+  // (the wave index as a scalar: the unit and tile indices and addresses derived from it
+  // stay in scalar registers)
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int64_t first = pos / kTile, last = (pos + n_tok - 1) / kTile;
   const int64_t n_units = 2 * (last - first + 1);
   if (hp->max_bits > 8) {
