@@ -2098,12 +2098,16 @@ void decode_mfma_kernel(const DecodeArgs a) {
     if (h < G) {
       const float* oh = ob + h * a.ob_stride;
       float acc = 0.f;
-#pragma unroll 8
-      for (int k = 0; k < v_maxb; ++k) {
+      auto bit_term = [&](int k) {
         const int v = min(voc + k, 8 * RV - 1);
         const float t = ldexpf(kHalves ? oh[v] + oh[NH * a.ob_stride + v] : oh[v], k);
         acc += (k < vbc) ? ((k == vbc - 1) ? -t : t) : 0.f;
-      }
+      };
+      // (the first eight bits unrolled with their reads issued together; wider codes take
+      // the loop after)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) bit_term(k);
+      for (int k = 8; k < v_maxb; ++k) bit_term(k);
       float pa = 0.f;
 #pragma unroll
       for (int w = 0; w < NW; ++w) pa += wpav[w][h];
