@@ -977,6 +977,7 @@ struct AppendHook {
   bool on;                             // the sequence has a token to append
   // Wave 0 encodes the key token, wave 1 the value token, lane l channels l and l + 64:
   int e_b[2], e_off[2];                // their widths and first record bits
+  bool e_mr;                           // the wave's tensor uses the midrise reading
   float e_s[2];                        // their scales s_c (value token)
   float qk[2][NH];                     // Q_c of every head for them (key token)
   AppendScratch* sc;
@@ -1026,7 +1027,7 @@ struct AppendHook {
       for (int i = 0; i < 2; ++i) m = fmaxf(m, e_b[i] > 0 ? fabsf(r2[i]) : 0.f);
       const __half a16 = token_alpha(wave_max_dpp(m));
       const float inv = inverse_alpha(a16);
-      const bool midrise = ep->quantizer == AATC_QUANT_MIDRISE;
+      const bool midrise = e_mr;
       float code[2];                   // the level in steps: code, or code + 1/2 (midrise)
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -1394,6 +1395,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
   // l + 64 (their widths, first bits and scales).
   int e_b[2] = {0, 0}, e_off[2] = {0, 0};
   float e_s[2] = {0.f, 0.f};
+  bool e_mr = false;
   auto load_tables = [&]() {
     v_budget = hv->budget;
     if (APPEND && wave < 2) {
@@ -1404,6 +1406,8 @@ void decode_mfma_kernel(const DecodeArgs a) {
         e_off[i] = eh->bit_off[lane + 64 * i];
         e_s[i] = eh->s[lane + 64 * i];
       }
+      // (read here, not in the merge: a load there waits a full round trip)
+      e_mr = eh->quantizer == AATC_QUANT_MIDRISE;
     }
     vbc = hv->bits[cq];
     voc = hv->bit_off[cq];
@@ -2146,6 +2150,7 @@ void decode_mfma_kernel(const DecodeArgs a) {
     hook.rk = RK;
     hook.rv = RV;
     hook.on = len > 0;
+    hook.e_mr = e_mr;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       hook.e_b[i] = e_b[i];
