@@ -14,4 +14,4 @@ it, and it shares no code with the GPU library.
 Parity status: every function is pinned by the tests under ``tests/test_oracle_*``
 except the items listed as "parity unpinned" in ``oracle/aatc.py``'s header.
 """
-from . import aatc, theory  # noqa: F401
+from . import aatc, groups, theory  # noqa: F401

@@ -437,7 +437,8 @@ def transform(x32: np.ndarray, t32: np.ndarray) -> np.ndarray:
     multiples of 2^-22 with |t| <= 1.  The sum is formed exactly in integers: with
     Tq = t 2^22 and, per token, x_j = 2^-S (X_j + 2^-31 Y_j) with integers X_j, Y_j (S puts
     max |X| in [2^30, 2^31); |Y| <= 2^30), the sum is 2^-(S+22+31) (2^31 H + L) with
-    H = X Tq and L = Y Tq exact in int64 (below 2^60 for d <= 128).
+    H = X Tq and L = Y Tq exact in int64 (|X| <= 2^31 and |Tq| <= 2^22, so every product
+    is at most 2^53 and a sum of d <= 512 of them stays below 2^62).
       - Where L = 0 (every element a multiple of 2^-S, as for bf16 tokens whose elements
         are all above 2^-23 of the largest) the result is the int64 H converted to fp32,
         which rounds once, to nearest with ties to even (pinned by the tests), times the
@@ -449,8 +450,8 @@ def transform(x32: np.ndarray, t32: np.ndarray) -> np.ndarray:
     x = np.asarray(x32, dtype=np.float32)
     t = np.asarray(t32, dtype=np.float32)
     n, d = x.shape
-    if d > 128:
-        raise ValueError("at most 128 elements per token")
+    if d > 512:
+        raise ValueError("at most 512 elements per token")
     tq_f = np.ldexp(t.astype(np.float64), T_FRAC_BITS)
     if not (np.all(tq_f == np.rint(tq_f)) and np.all(np.abs(tq_f) <= 2.0 ** T_FRAC_BITS)):
         raise ValueError("the transform must be on the 2^-22 grid with |t| <= 1")
