@@ -388,6 +388,94 @@ aatc_status aatc_append_decode_attention_noalloc(
     uint16_t* v_alpha, const int32_t* seq_len, int64_t cap, int32_t k_record_bytes,
     int32_t v_record_bytes, float softmax_scale, float* out, void* stream);
 
+/*
+ * Head-group transforms (Sec. 5.1, the remark on head groups: heads are merged into G
+ * groups, each with its own transform block; Sec. 5.2: the token scale is taken per head
+ * group; Sec. 6: G = 2 groups for Llama-3.1-8B's 8 KV heads, G = 1 for Qwen-2.5-7B's 4).
+ *
+ * A group is gkv consecutive KV heads (1 <= gkv <= 4): group g holds KV heads
+ * g gkv .. g gkv + gkv - 1, and its token is the concatenation of their vectors,
+ * d = 128 gkv elements with KV head kk of the group at elements [128 kk, 128 kk + 128).
+ * Everything per KV head above becomes per group: one transform (d x d), one allocation of
+ * round(avg_bits d) bits, per-channel scales, one token scale alpha per (token, group) and
+ * one record per (token, group).  Both tensors use the RECORDS layout:
+ *   codes [n_groups][cap][R] bytes (per sequence), alpha [n_groups][cap] fp16.
+ * Query head j reads KV head k = j / (n_q_heads / n_kv_heads): block k % gkv of group
+ * k / gkv, i.e. q~ = T[block]^T q has d transformed coordinates and o = T_V[block] o~.
+ */
+#define AATC_GROUP_MAX_DIM 512
+
+/* Calibration artifact of one (head group, tensor): aatc_calibration with d up to 512;
+ * transform is [j][c] with row stride d (the first d * d entries are used). */
+typedef struct {
+  int32_t d;                    /* 128 gkv */
+  int32_t budget_bits;
+  int32_t record_bytes;
+  int32_t d_active;
+  int32_t quantizer;
+  float transform[AATC_GROUP_MAX_DIM * AATC_GROUP_MAX_DIM];
+  uint8_t bits[AATC_GROUP_MAX_DIM];
+  uint16_t scale_f16[AATC_GROUP_MAX_DIM];
+  int32_t perm[AATC_GROUP_MAX_DIM];
+  double sigma2[AATC_GROUP_MAX_DIM];
+  double weight[AATC_GROUP_MAX_DIM];
+  uint8_t bits_eig[AATC_GROUP_MAX_DIM];
+} aatc_group_calibration;
+
+/*
+ * aatc_calibrate_group -- aatc_calibrate for one head group: x_calib is [n_calib][d] (the
+ * group's concatenated tokens, d = 128 gkv), q_calib [n_q][d] the group's calibration
+ * queries, each placed in its KV head's block and zero elsewhere (q_group = the group's
+ * query heads: the weights average over tokens and sum over those heads), w_o [d][d_out]
+ * the rows of W_O that read the group's values.  Same steps, arguments and errors as
+ * aatc_calibrate; d must be 128, 256, 384 or 512.
+ */
+aatc_status aatc_calibrate_group(const float* x_calib, int64_t n_calib, int32_t d,
+                                 const float* q_calib, int64_t n_q, int32_t q_group,
+                                 const float* w_o, int32_t d_out, double avg_bits,
+                                 int32_t b_max, double percentile, aatc_group_calibration* out);
+
+/* Bytes of the device parameter block of n_groups groups (about 2 MiB per group), and
+ * its host-side packing (every group must have the same d, record size and quantizer;
+ * the caller copies host_buf to the device).  Errors: AATC_E_INVALID. */
+size_t aatc_group_params_bytes(int32_t n_groups);
+aatc_status aatc_group_params_pack(const aatc_group_calibration* per_group, int32_t n_groups,
+                                   void* host_buf, size_t bytes);
+
+/*
+ * aatc_group_encode -- aatc_encode for head groups: tokens [n_tok] at x + t * x_tok_stride
+ * elements, each [n_groups * d] contiguous (= [n_kv_heads][128]), F32 or BF16; group g's
+ * codes go to codes + (g * cap + pos + t) * R, its scale to alpha[g * cap + pos + t].
+ * h is the exact product with the stored transform rounded once to fp32, as in
+ * aatc_encode.  gkv = d / 128.  Errors: AATC_E_INVALID.
+ */
+aatc_status aatc_group_encode(const void* dev_params, int32_t n_groups, int32_t gkv,
+                              const void* x, aatc_dtype x_dtype, int64_t n_tok,
+                              int64_t x_tok_stride, void* codes, uint16_t* alpha, int64_t cap,
+                              int64_t pos, void* stream);
+
+/*
+ * aatc_group_decode_attention -- aatc_decode_attention over group-compressed caches:
+ * k_codes / v_codes [batch][n_groups][cap][R] (RECORDS), k_alpha / v_alpha
+ * [batch][n_groups][cap] fp16, q [batch][n_q_heads][128], out [batch][n_q_heads][128]
+ * fp32.  Query heads per group (n_q_heads / n_groups) at most 32; records at most 512
+ * bytes.  Three launches on `stream` (query weights, 256-token splits, merge with the
+ * inverse transform); workspace of aatc_group_decode_workspace_bytes bytes, written before
+ * it is read (no zero fill needed).  Errors: AATC_E_INVALID, AATC_E_UNSUPPORTED,
+ * AATC_E_WORKSPACE, AATC_E_DEVICE.
+ */
+size_t aatc_group_decode_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                         int32_t gkv, int64_t cap);
+aatc_status aatc_group_decode_attention(const void* dev_params_k, const void* dev_params_v,
+                                        int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                        int32_t gkv, const void* q, aatc_dtype q_dtype,
+                                        const void* k_codes, const uint16_t* k_alpha,
+                                        const void* v_codes, const uint16_t* v_alpha,
+                                        const int32_t* seq_len, int64_t cap,
+                                        int32_t k_record_bytes, int32_t v_record_bytes,
+                                        float softmax_scale, float* out, void* workspace,
+                                        size_t ws_bytes, void* stream);
+
 /* Human-readable name of a status code (static string). */
 const char* aatc_status_string(aatc_status s);
 

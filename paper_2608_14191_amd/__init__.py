@@ -11,4 +11,7 @@ from ._lib import (  # noqa: F401
     aatc_calibrate, aatc_calibrate_bits, aatc_calibrate_whitened, aatc_decode_attention, aatc_decode_attention_segmented,
     aatc_decode_workspace_bytes, aatc_encode, aatc_segment_counts,
     aatc_params_bytes, aatc_params_pack, aatc_status_string, library,
+    GroupCalibration, aatc_calibrate_group, aatc_group_decode_attention,
+    aatc_group_decode_workspace_bytes, aatc_group_encode, aatc_group_params_bytes,
+    aatc_group_params_pack,
 )

@@ -336,3 +336,118 @@ def aatc_calibrate_bits(x_calib, bits_eig, record_bytes: int = 0, percentile: fl
                                 float(percentile), ctypes.byref(out))
     _check("aatc_calibrate_bits", st)
     return out
+
+
+# --------------------------------------------------------------------------------------
+# Head groups
+# --------------------------------------------------------------------------------------
+GROUP_MAX_DIM = 512
+
+
+class GroupCalibration(ctypes.Structure):
+    """Mirror of aatc_group_calibration (include/aatc.h); transform rows have stride d."""
+
+    _fields_ = [
+        ("d", ctypes.c_int32),
+        ("budget_bits", ctypes.c_int32),
+        ("record_bytes", ctypes.c_int32),
+        ("d_active", ctypes.c_int32),
+        ("quantizer", ctypes.c_int32),
+        ("transform", ctypes.c_float * (GROUP_MAX_DIM * GROUP_MAX_DIM)),
+        ("bits", ctypes.c_uint8 * GROUP_MAX_DIM),
+        ("scale_f16", ctypes.c_uint16 * GROUP_MAX_DIM),
+        ("perm", ctypes.c_int32 * GROUP_MAX_DIM),
+        ("sigma2", ctypes.c_double * GROUP_MAX_DIM),
+        ("weight", ctypes.c_double * GROUP_MAX_DIM),
+        ("bits_eig", ctypes.c_uint8 * GROUP_MAX_DIM),
+    ]
+
+    @property
+    def T(self) -> np.ndarray:
+        d = self.d
+        return np.ctypeslib.as_array(self.transform)[:d * d].reshape(d, d).copy()
+
+    @property
+    def bits_np(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self.bits)[:self.d].astype(np.int64)
+
+    @property
+    def s16(self) -> np.ndarray:
+        return np.ctypeslib.as_array(self.scale_f16)[:self.d].copy().view(np.float16)
+
+
+_L.aatc_calibrate_group.restype = ctypes.c_int
+_L.aatc_calibrate_group.argtypes = [_vp, _i64, _i32, _vp, _i64, _i32, _vp, _i32, _f64, _i32,
+                                    _f64, ctypes.POINTER(GroupCalibration)]
+_L.aatc_group_params_bytes.restype = _sz
+_L.aatc_group_params_bytes.argtypes = [_i32]
+_L.aatc_group_params_pack.restype = ctypes.c_int
+_L.aatc_group_params_pack.argtypes = [ctypes.POINTER(GroupCalibration), _i32, _vp, _sz]
+_L.aatc_group_encode.restype = ctypes.c_int
+_L.aatc_group_encode.argtypes = [_vp, _i32, _i32, _vp, ctypes.c_int, _i64, _i64, _vp, _vp,
+                                 _i64, _i64, _vp]
+_L.aatc_group_decode_workspace_bytes.restype = _sz
+_L.aatc_group_decode_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32, _i64]
+_L.aatc_group_decode_attention.restype = ctypes.c_int
+_L.aatc_group_decode_attention.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32, _vp, ctypes.c_int,
+                                           _vp, _vp, _vp, _vp, _vp, _i64, _i32, _i32, _f32,
+                                           _vp, _vp, _sz, _vp]
+
+
+def aatc_calibrate_group(x_calib, avg_bits: float, b_max: int = 8, percentile: float = 0.99,
+                         q_calib=None, q_group: int = 1, w_o=None) -> GroupCalibration:
+    """Host calibration of one (head group, tensor) from its concatenated tokens [n, d]."""
+    x = np.ascontiguousarray(x_calib, dtype=np.float32)
+    q = None if q_calib is None else np.ascontiguousarray(q_calib, dtype=np.float32)
+    wo = None if w_o is None else np.ascontiguousarray(w_o, dtype=np.float32)
+    out = GroupCalibration()
+    st = _L.aatc_calibrate_group(_np_ptr(x), x.shape[0], x.shape[1] if x.ndim == 2 else 0,
+                                 _np_ptr(q), 0 if q is None else q.shape[0], int(q_group),
+                                 _np_ptr(wo), 0 if wo is None else wo.shape[1],
+                                 float(avg_bits), int(b_max), float(percentile),
+                                 ctypes.byref(out))
+    _check("aatc_calibrate_group", st)
+    return out
+
+
+def aatc_group_params_bytes(n_groups: int) -> int:
+    return int(_L.aatc_group_params_bytes(int(n_groups)))
+
+
+def aatc_group_params_pack(calibrations) -> np.ndarray:
+    """Host parameter block (uint8 numpy array) for a list of per-group GroupCalibration."""
+    n = len(calibrations)
+    arr = (GroupCalibration * n)(*calibrations)
+    buf = np.zeros(aatc_group_params_bytes(n), dtype=np.uint8)
+    _check("aatc_group_params_pack", _L.aatc_group_params_pack(arr, n, _np_ptr(buf), buf.nbytes))
+    return buf
+
+
+def aatc_group_encode(dev_params, n_groups: int, gkv: int, x, n_tok: int, x_tok_stride: int,
+                      codes, alpha, cap: int, pos: int, stream=None):
+    """Append n_tok tokens of x ([n_tok, n_groups * gkv, 128] view) to a sequence's
+    group-compressed cache (codes [n_groups][cap][R], alpha [n_groups][cap])."""
+    st = _L.aatc_group_encode(_dptr(dev_params), int(n_groups), int(gkv), _dptr(x),
+                              _dtype_code(x), int(n_tok), int(x_tok_stride), _dptr(codes),
+                              _dptr(alpha), int(cap), int(pos), _stream(stream))
+    _check("aatc_group_encode", st)
+
+
+def aatc_group_decode_workspace_bytes(batch: int, n_q_heads: int, n_kv_heads: int, gkv: int,
+                                      cap: int) -> int:
+    return int(_L.aatc_group_decode_workspace_bytes(int(batch), int(n_q_heads),
+                                                    int(n_kv_heads), int(gkv), int(cap)))
+
+
+def aatc_group_decode_attention(dev_params_k, dev_params_v, batch: int, n_q_heads: int,
+                                n_kv_heads: int, gkv: int, q, k_codes, k_alpha, v_codes,
+                                v_alpha, seq_len, cap: int, k_record_bytes: int,
+                                v_record_bytes: int, softmax_scale: float, out, workspace,
+                                stream=None):
+    st = _L.aatc_group_decode_attention(
+        _dptr(dev_params_k), _dptr(dev_params_v), int(batch), int(n_q_heads), int(n_kv_heads),
+        int(gkv), _dptr(q), _dtype_code(q), _dptr(k_codes), _dptr(k_alpha), _dptr(v_codes),
+        _dptr(v_alpha), _dptr(seq_len), int(cap), int(k_record_bytes), int(v_record_bytes),
+        float(softmax_scale), _dptr(out), _dptr(workspace),
+        int(workspace.numel() * workspace.element_size()), _stream(stream))
+    _check("aatc_group_decode_attention", st)

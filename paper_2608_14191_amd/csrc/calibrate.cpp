@@ -142,15 +142,21 @@ namespace {
 // as they are instead of allocated, and a nonzero `record_bytes_given` pads the records.
 // With `gram` the d x d matrix whose eigenvectors form the basis is given (instead of the
 // covariance of the samples) and the samples are `x64` (fp64) instead of `x_calib`.
+// Out is aatc_calibration (one KV head, d = 128) or aatc_group_calibration (a head group,
+// d = 128 gkv up to 512); the transform is stored densely with row stride d.
+template <class Out>
 aatc_status calibrate_impl(const float* x_calib, int64_t n_calib, int32_t d,
                            const float* q_calib, int64_t n_q, int32_t q_group,
                            const float* w_o, int32_t d_out, double avg_bits, int32_t b_max,
                            const uint8_t* bits_given, int32_t record_bytes_given,
-                           double percentile, aatc_calibration* out,
+                           double percentile, Out* out,
                            const double* gram = nullptr, const double* x64 = nullptr) {
+  constexpr int kMaxDim = (int)(sizeof(out->bits) / sizeof(out->bits[0]));
   try {
     if ((!x_calib && !x64) || !out) return AATC_E_INVALID;
-    if (d != AATC_HEAD_DIM) return AATC_E_UNSUPPORTED;
+    if (kMaxDim == AATC_HEAD_DIM ? d != AATC_HEAD_DIM
+                                 : (d < AATC_HEAD_DIM || d > kMaxDim || d % AATC_HEAD_DIM))
+      return AATC_E_UNSUPPORTED;
     if (n_calib < 2 || b_max < 1 || b_max > AATC_MAX_BITS) return AATC_E_INVALID;
     if (!(percentile > 0.0 && percentile <= 1.0)) return AATC_E_INVALID;
     if (q_calib && w_o) return AATC_E_INVALID;
@@ -171,7 +177,7 @@ aatc_status calibrate_impl(const float* x_calib, int64_t n_calib, int32_t d,
     const int32_t min_rb = (int32_t)(4 * ((budget + 31) / 32));
     if (record_bytes_given != 0 &&
         (record_bytes_given < min_rb || record_bytes_given % 4 != 0 ||
-         record_bytes_given > AATC_HEAD_DIM * AATC_MAX_BITS / 8))
+         record_bytes_given > d * AATC_MAX_BITS / 8))
       return AATC_E_INVALID;
 
     const size_t n = (size_t)n_calib;
@@ -318,6 +324,15 @@ aatc_status calibrate_impl(const float* x_calib, int64_t n_calib, int32_t d,
 }
 
 }  // namespace
+
+extern "C" aatc_status aatc_calibrate_group(const float* x_calib, int64_t n_calib, int32_t d,
+                                            const float* q_calib, int64_t n_q, int32_t q_group,
+                                            const float* w_o, int32_t d_out, double avg_bits,
+                                            int32_t b_max, double percentile,
+                                            aatc_group_calibration* out) {
+  return calibrate_impl(x_calib, n_calib, d, q_calib, n_q, q_group, w_o, d_out, avg_bits,
+                        b_max, nullptr, 0, percentile, out);
+}
 
 extern "C" aatc_status aatc_calibrate(const float* x_calib, int64_t n_calib, int32_t d,
                                       const float* q_calib, int64_t n_q, int32_t q_group,

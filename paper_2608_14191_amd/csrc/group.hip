@@ -1,0 +1,588 @@
+// AATC under head-group transforms (Sec. 5.1, the remark on head groups; Sec. 5.2, one
+// token scale per head group; Sec. 6: G = 2 groups for Llama's 8 KV heads, 1 for Qwen's 4).
+//
+// A group is gkv consecutive KV heads; its token is the concatenation of their vectors
+// (d = 128 gkv elements, KV head kk of the group at [128 kk, 128 kk + 128)).  Encode and
+// decode follow Alg. 1 on those d-element vectors with the group's transform:
+//   - group_encode_kernel: h = T^T x exactly rounded (the exact one-wave routine of the
+//     per-head path, over d elements), one alpha per (token, group), codes packed into
+//     one token-major record per (token, group);
+//   - group_query_kernel: per query head, the channel weights W_c = q~_c s_c 2^(1-b_c)
+//     scale log2(e) of q~ = T[block]^T q (App. B's effective query; the query of KV head k
+//     lives in block k % gkv of its group);
+//   - group_split_kernel: per (sequence, group, 256-token split) the scores of every query
+//     head of the group, an online softmax over 64-token chunks and the transformed-domain
+//     value sums, on the VALU with the records staged in LDS;
+//   - group_merge_kernel: per (sequence, query head) the merge of the split partials and
+//     the inverse transform o = T[block] o~.
+#include <algorithm>
+#include <atomic>
+
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include "encode_core.h"
+#include "group.h"
+#include "group_launch.h"
+
+namespace aatc {
+namespace {
+
+constexpr int kGThreads = 256;
+constexpr int kGChunk = 64;                       // tokens staged per chunk (one per lane)
+
+__device__ inline void group_wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+__device__ inline float g_wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ inline float g_wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// The signed code of a channel at record bit `off`, width b (1..16), from the record's
+// dwords in LDS (the row has one padding dword after the record).
+__device__ inline int record_code(const uint32_t* row, int off, int b) {
+  const uint32_t w0 = row[off >> 5], w1 = row[(off >> 5) + 1];
+  const uint32_t v = (uint32_t)(((uint64_t)w1 << 32 | w0) >> (off & 31));
+  return (int)(v << (32 - b)) >> (32 - b);
+}
+
+// ---------------------------------------------------------------------------------------
+// Encode: one wave per (token, group); lane l holds elements and channels l + 64 i.
+// h_c = fl32(sum_j x_j T_jc) exactly: fp64 sums of the exact products x_j Tq_jc, exact
+// while the sum of their magnitudes stays below 2^(53 + g) (every product is a multiple of
+// 2^g, g the lowest set bit of the token's elements); otherwise an interval test, and the
+// exact accumulator where the interval straddles an fp32 rounding boundary.
+// ---------------------------------------------------------------------------------------
+template <int NC>
+__global__ __launch_bounds__(kGThreads) void group_encode_kernel(
+    const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
+    int64_t x_stride, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha, int64_t cap,
+    int64_t pos) {
+  constexpr int D = 64 * NC;
+  constexpr int kRow = D * kMaxBits / 32 + 1;
+  __shared__ uint32_t rec[kGThreads / 64][kRow];
+  const int g = blockIdx.y, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t t = (int64_t)blockIdx.x * (kGThreads / 64) + wave;
+  if (t >= n_tok) return;                           // (whole wave; no barrier follows)
+  const GroupParams* gp = group_params(params, g);
+  const int rw = gp->record_bytes >> 2;
+  uint32_t* row = rec[wave];
+  for (int i = lane; i < rw + 1; i += 64) row[i] = 0u;
+  const size_t esize = dtype == AATC_BF16 ? 2 : 4;
+  const void* xrow = static_cast<const char*>(x) + (t * x_stride + (int64_t)g * D) * esize;
+  float xl[NC];
+#pragma unroll
+  for (int i = 0; i < NC; ++i) xl[i] = load_elem(xrow, dtype, lane + 64 * i);
+  // Lowest set bit over the token's nonzero elements (4096 for a zero token).
+  int glsb = 4096;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const uint32_t bv = __float_as_uint(xl[i]) & 0x7fffffffu;
+    if (bv != 0u) {
+      const int ef = (int)(bv >> 23), m = (int)(bv & 0x7fffffu);
+      glsb = min(glsb, ef ? ef - 150 + __builtin_ctz((uint32_t)m | 0x800000u)
+                          : -149 + __builtin_ctz((uint32_t)m));
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) glsb = min(glsb, __shfl_xor(glsb, o, 64));
+  double s[NC], a[NC];
+#pragma unroll
+  for (int k = 0; k < NC; ++k) s[k] = a[k] = 0.0;
+  const int4* tcol[NC];
+#pragma unroll
+  for (int k = 0; k < NC; ++k)
+    tcol[k] = reinterpret_cast<const int4*>(gp->Tqt + (size_t)(lane + 64 * k) * D);
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+#pragma unroll 1
+    for (int jb = 0; jb < 64; jb += 8) {
+      int4 tv[NC][2];
+#pragma unroll
+      for (int k = 0; k < NC; ++k) {
+        tv[k][0] = tcol[k][(64 * i + jb) / 4];
+        tv[k][1] = tcol[k][(64 * i + jb) / 4 + 1];
+      }
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        const double xd =
+            (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(xl[i]), jb + jj));
+#pragma unroll
+        for (int k = 0; k < NC; ++k) {
+          const int4 q = tv[k][jj >> 2];
+          const int ti = (jj & 3) == 0 ? q.x : (jj & 3) == 1 ? q.y : (jj & 3) == 2 ? q.z : q.w;
+          const double tq = (double)ti;
+          s[k] = fma(xd, tq, s[k]);
+          a[k] = fma(fabs(xd), fabs(tq), a[k]);
+        }
+      }
+    }
+  }
+  const double lim = ldexp(1.0 - 0x1p-40, 53 + min(glsb, 900));
+  float r[NC];
+  float m = 0.f;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int c = lane + 64 * k;
+    const double sv = ldexp(s[k], -kTFrac), av = ldexp(a[k], -kTFrac);
+    float h;
+    if (a[k] < lim) {
+      h = (float)sv;
+    } else {
+      const double bnd = av * (D * 0x1p-52);
+      const double bb = bnd * (1.0 + 0x1p-48) + fabs(sv) * 0x1p-51 + 0x1p-1060;
+      const float lo = (float)(sv - bb), hi = (float)(sv + bb);
+      h = lo;
+      if (lo != hi && gp->bits[c] > 0) {
+        // (the exact accumulator holds any sum of up to 512 such products: each is below
+        // 2^46 units of its lsb, so 512 of them stay below 2^137, inside its 320 bits)
+        const int32_t* tc = gp->Tqt + (size_t)c * D;
+        h = exact_dot_q22([&](int j) { return load_elem(xrow, dtype, j); },
+                          [&](int j) { return tc[j]; }, D);
+      }
+    }
+    r[k] = h * gp->inv_s[c];
+    m = fmaxf(m, gp->bits[c] > 0 ? fabsf(r[k]) : 0.f);
+  }
+  const __half a16 = token_alpha(g_wave_max(m));
+  const float inv = inverse_alpha(a16);
+  const bool midrise = gp->quantizer == AATC_QUANT_MIDRISE;
+  group_wave_sync();                                 // the cleared row before the ORs
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int c = lane + 64 * k;
+    const int b = gp->bits[c], off = gp->bit_off[c];
+    if (b > 0) {
+      const uint32_t u = quantize_code(r[k], inv, b, midrise);
+      atomicOr(&row[off >> 5], u << (off & 31));
+      if ((off & 31) + b > 32) atomicOr(&row[(off >> 5) + 1], u >> (32 - (off & 31)));
+    }
+  }
+  group_wave_sync();                                 // every OR before the read-out
+  uint32_t* out = reinterpret_cast<uint32_t*>(codes + ((int64_t)g * cap + pos + t) * gp->record_bytes);
+  for (int i = lane; i < rw; i += 64) out[i] = row[i];
+  if (lane == 0) alpha[(int64_t)g * cap + pos + t] = __half_as_ushort(a16);
+}
+
+// ---------------------------------------------------------------------------------------
+// Decode.
+// ---------------------------------------------------------------------------------------
+struct GroupDecodeArgs {
+  const void* params_k;
+  const void* params_v;
+  const void* q;
+  int q_dtype;
+  const uint8_t* k_codes;
+  const uint16_t* k_alpha;
+  const uint8_t* v_codes;
+  const uint16_t* v_alpha;
+  const int32_t* seq_len;
+  int64_t cap;
+  int n_q_heads, n_kv_heads, gkv, n_groups, heads;   // heads: query heads per group
+  int n_splits;
+  int rwk, rwv;                  // record dwords of the key and value caches
+  float scale_log2e;
+  float* w;                      // workspace regions
+  float* cst;
+  float* part;
+  float* out;
+};
+
+// One workgroup per (sequence, query head): W_c for the head's group channels.
+template <int NC>
+__global__ __launch_bounds__(kGThreads) void group_query_kernel(GroupDecodeArgs a) {
+  constexpr int D = 64 * NC;
+  __shared__ float qs[128];
+  __shared__ float red[kGThreads / 64];
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int gq = a.n_q_heads / a.n_kv_heads;
+  const int k = h / gq, g = k / a.gkv, kk = k % a.gkv, hl = h - g * a.heads;
+  const GroupParams* gp = group_params(a.params_k, g);
+  if (tid < 128) qs[tid] = load_elem(a.q, a.q_dtype, ((int64_t)b * a.n_q_heads + h) * 128 + tid);
+  __syncthreads();
+  const bool midrise = gp->quantizer == AATC_QUANT_MIDRISE;
+  const size_t rowi = ((size_t)b * a.n_groups + g) * a.heads + hl;
+  float csum = 0.f;
+  for (int c = tid; c < D; c += kGThreads) {
+    float acc = 0.f;
+    const float* tcol = gp->T + (size_t)(kk * 128) * D + c;
+#pragma unroll 8
+    for (int j = 0; j < 128; ++j) acc = fmaf(qs[j], tcol[(size_t)j * D], acc);
+    const int bc = gp->bits[c];
+    const float wv = bc > 0 ? ldexpf(acc * gp->s[c] * a.scale_log2e, 1 - bc) : 0.f;
+    a.w[rowi * D + c] = wv;
+    csum += midrise ? 0.5f * wv : 0.f;
+  }
+  csum = g_wave_sum(csum);
+  if ((tid & 63) == 0) red[tid >> 6] = csum;
+  __syncthreads();
+  if (tid == 0) a.cst[rowi] = red[0] + red[1] + red[2] + red[3];
+}
+
+// One workgroup per (sequence, group, split of kGSplit tokens).  NQ: query heads of a group
+// rounded up to a multiple of 4 (the unused ones have zero weights and are not stored).
+template <int NC, int NQ>
+__global__ __launch_bounds__(kGThreads) void group_split_kernel(GroupDecodeArgs a) {
+  constexpr int D = 64 * NC;
+  constexpr int HW = NQ / 4;                        // heads scored by each wave
+  constexpr int CPT = (D + kGThreads - 1) / kGThreads;   // value channels per thread
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ float ak[kGChunk], av[kGChunk];
+  __shared__ float m_run[NQ], l_run[NQ], fac[NQ], cst[NQ];
+  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int len = (int)min((int64_t)max(a.seq_len[b], 0), a.cap);
+  const int s0 = split * kGSplit;
+  if (s0 >= len) return;                            // (whole workgroup, before any barrier)
+  const int s1 = min(len, s0 + kGSplit);
+  const GroupParams* pk = group_params(a.params_k, g);
+  const GroupParams* pv = group_params(a.params_v, g);
+  // (partial rows are [(sequence, group)][split][head])
+  float* pbase = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits + split) * a.heads) * (D + 4);
+  const int rwk = a.rwk, rwv = a.rwv;
+  if (pk->record_bytes != 4 * rwk || pv->record_bytes != 4 * rwv || pk->d != D || pv->d != D) {
+    // caches of another record size than the parameter blocks: NaN outputs
+    if (tid < a.heads) pbase[(size_t)tid * (D + 4)] = NAN;
+    return;
+  }
+  const int rsk = rwk + 1, rsv = rwv + 1;           // LDS row strides (one padding dword)
+  float* wl = reinterpret_cast<float*>(smem);                    // [D][NQ]
+  uint32_t* kc = reinterpret_cast<uint32_t*>(wl + D * NQ);       // [kGChunk][rsk]
+  uint32_t* vc = kc + kGChunk * rsk;                             // [kGChunk][rsv]
+  float* pl = reinterpret_cast<float*>(vc + kGChunk * rsv);      // [kGChunk][NQ]
+  const size_t row0 = ((size_t)b * a.n_groups + g) * a.heads;
+  for (int i = tid; i < D * NQ; i += kGThreads) {
+    const int c = i / NQ, h = i % NQ;
+    wl[i] = h < a.heads ? a.w[(row0 + h) * D + c] : 0.f;
+  }
+  if (tid < NQ) {
+    m_run[tid] = -INFINITY;
+    l_run[tid] = 0.f;
+    cst[tid] = tid < a.heads ? a.cst[row0 + tid] : 0.f;
+  }
+  const int dak = pk->d_active;
+  const bool mr_v = pv->quantizer == AATC_QUANT_MIDRISE;
+  // This thread's value channels.
+  int vb[CPT], vo[CPT];
+  float acc[NQ][CPT];
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = tid + kGThreads * i;
+    vb[i] = c < D ? pv->bits[c] : 0;
+    vo[i] = c < D ? pv->bit_off[c] : 0;
+#pragma unroll
+    for (int h = 0; h < NQ; ++h) acc[h][i] = 0.f;
+  }
+  const size_t tok0 = ((size_t)b * a.n_groups + g) * (size_t)a.cap;
+  const uint32_t* kw = reinterpret_cast<const uint32_t*>(a.k_codes + tok0 * pk->record_bytes);
+  const uint32_t* vw = reinterpret_cast<const uint32_t*>(a.v_codes + tok0 * pv->record_bytes);
+  for (int c0 = s0; c0 < s1; c0 += kGChunk) {
+    const int nc = min(kGChunk, s1 - c0);
+    __syncthreads();                                // the previous chunk's LDS is consumed
+    for (int i = tid; i < nc * rwk; i += kGThreads) {
+      const int t = i / rwk, w = i - t * rwk;
+      kc[t * rsk + w] = kw[(size_t)(c0 + t) * rwk + w];
+    }
+    for (int i = tid; i < nc * rwv; i += kGThreads) {
+      const int t = i / rwv, w = i - t * rwv;
+      vc[t * rsv + w] = vw[(size_t)(c0 + t) * rwv + w];
+    }
+    if (tid < kGChunk) {
+      kc[tid * rsk + rwk] = 0u;
+      vc[tid * rsv + rwv] = 0u;
+      float fk = 0.f, fv = 0.f;
+      if (tid < nc) {
+        fk = __half2float(__ushort_as_half(a.k_alpha[tok0 + c0 + tid]));
+        fv = __half2float(__ushort_as_half(a.v_alpha[tok0 + c0 + tid]));
+      }
+      ak[tid] = fk;
+      av[tid] = fv;
+    }
+    __syncthreads();
+    // Scores: lane = token of the chunk, wave w = heads w HW .. w HW + HW - 1.
+    {
+      const bool ok = lane < nc;
+      const uint32_t* krow = kc + (ok ? lane : 0) * rsk;
+      float z[HW];
+#pragma unroll
+      for (int m = 0; m < HW; ++m) z[m] = 0.f;
+#pragma unroll 2
+      for (int c = 0; c < dak; ++c) {
+        const int bc = pk->bits[c], off = pk->bit_off[c];
+        const float cf = (float)record_code(krow, off, bc);
+        const float* wr = wl + c * NQ + wave * HW;
+#pragma unroll
+        for (int m = 0; m < HW; ++m) z[m] = fmaf(wr[m], cf, z[m]);
+      }
+#pragma unroll
+      for (int m = 0; m < HW; ++m) {
+        const int h = wave * HW + m;
+        const float zf = ok ? ak[lane] * (z[m] + cst[h]) : -INFINITY;
+        const float mold = m_run[h];
+        const float mnew = fmaxf(mold, g_wave_max(zf));
+        const bool any = mnew > -INFINITY;
+        const float p = (ok && any) ? __builtin_amdgcn_exp2f(zf - mnew) : 0.f;
+        const float f = (any && mold > -INFINITY) ? __builtin_amdgcn_exp2f(mold - mnew) : (any ? 0.f : 1.f);
+        const float ps = g_wave_sum(p);
+        pl[lane * NQ + h] = p * av[lane];
+        if (lane == 0) {
+          m_run[h] = mnew;
+          l_run[h] = l_run[h] * f + ps;
+          fac[h] = f;
+        }
+      }
+    }
+    __syncthreads();
+    // Values: thread = value channels tid + 256 i; every token of the chunk.
+#pragma unroll
+    for (int h = 0; h < NQ; ++h) {
+      const float f = fac[h];
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) acc[h][i] *= f;
+    }
+#pragma unroll 1
+    for (int t = 0; t < nc; ++t) {
+      const uint32_t* vrow = vc + t * rsv;
+      float cf[CPT];
+#pragma unroll
+      for (int i = 0; i < CPT; ++i)
+        cf[i] = vb[i] > 0 ? (float)record_code(vrow, vo[i], vb[i]) + (mr_v ? 0.5f : 0.f) : 0.f;
+      const float* pr = pl + t * NQ;
+#pragma unroll
+      for (int h = 0; h < NQ; ++h) {
+        const float p = pr[h];
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) acc[h][i] = fmaf(p, cf[i], acc[h][i]);
+      }
+    }
+  }
+  __syncthreads();
+  // Partial: (m, l) per head, o~_c = s_c 2^(1-b_c) sum_i P_i alpha_i level_ic.
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = tid + kGThreads * i;
+    if (c < D) {
+      const float sc = vb[i] > 0 ? ldexpf(pv->s[c], 1 - vb[i]) : 0.f;
+#pragma unroll
+      for (int h = 0; h < NQ; ++h)
+        if (h < a.heads) pbase[(size_t)h * (D + 4) + 4 + c] = acc[h][i] * sc;
+    }
+  }
+  if (tid < a.heads) {
+    pbase[(size_t)tid * (D + 4)] = m_run[tid];
+    pbase[(size_t)tid * (D + 4) + 1] = l_run[tid];
+  }
+}
+
+// One workgroup per (sequence, query head): merge the splits, then o = T_V[block] o~.
+template <int NC>
+__global__ __launch_bounds__(kGThreads) void group_merge_kernel(GroupDecodeArgs a) {
+  constexpr int D = 64 * NC;
+  __shared__ float ot[D];
+  __shared__ float red[kGThreads / 64];
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
+  const int wave = tid >> 6;
+  const int gq = a.n_q_heads / a.n_kv_heads;
+  const int k = h / gq, g = k / a.gkv, kk = k % a.gkv, hl = h - g * a.heads;
+  float* out = a.out + ((int64_t)b * a.n_q_heads + h) * 128;
+  const int len = (int)min((int64_t)max(a.seq_len[b], 0), a.cap);
+  if (len == 0) {
+    if (tid < 128) out[tid] = 0.f;
+    return;
+  }
+  const int ns = (len + kGSplit - 1) / kGSplit;
+  const float* pb = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits) * a.heads + hl) * (D + 4);
+  const size_t sstride = (size_t)a.heads * (D + 4);
+  float mx = -INFINITY;
+  for (int s = tid; s < ns; s += kGThreads) {
+    const float ms = pb[s * sstride];
+    mx = ms != ms ? ms : fmaxf(mx, ms);             // (a NaN mark is kept)
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float y = __shfl_xor(mx, o, 64);
+    mx = (mx != mx || y != y) ? NAN : fmaxf(mx, y);
+  }
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  float M = red[0];
+  for (int w = 1; w < kGThreads / 64; ++w) M = (M != M || red[w] != red[w]) ? NAN : fmaxf(M, red[w]);
+  if (M != M) {
+    if (tid < 128) out[tid] = NAN;
+    return;
+  }
+  float L = 0.f;
+  float acc[(D + kGThreads - 1) / kGThreads];
+#pragma unroll
+  for (int i = 0; i < (D + kGThreads - 1) / kGThreads; ++i) acc[i] = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const float* p = pb + s * sstride;
+    const float w = __builtin_amdgcn_exp2f(p[0] - M);
+    L = fmaf(w, p[1], L);
+#pragma unroll
+    for (int i = 0; i < (D + kGThreads - 1) / kGThreads; ++i) {
+      const int c = tid + kGThreads * i;
+      if (c < D) acc[i] = fmaf(w, p[4 + c], acc[i]);
+    }
+  }
+  const float inv_l = L > 0.f ? 1.f / L : 0.f;
+#pragma unroll
+  for (int i = 0; i < (D + kGThreads - 1) / kGThreads; ++i) {
+    const int c = tid + kGThreads * i;
+    if (c < D) ot[c] = acc[i] * inv_l;
+  }
+  __syncthreads();
+  const GroupParams* pv = group_params(a.params_v, g);
+  for (int j = wave; j < 128; j += kGThreads / 64) {
+    const float* trow = pv->T + (size_t)(kk * 128 + j) * D;
+    float v = 0.f;
+#pragma unroll
+    for (int m = 0; m < NC; ++m) v = fmaf(trow[lane + 64 * m], ot[lane + 64 * m], v);
+    v = g_wave_sum(v);
+    if (lane == 0) out[j] = v;
+  }
+}
+
+// The dynamic LDS limit of one kernel on the current device, raised once per device when a
+// launch first needs more (an idempotent attribute call; the recorded limit only grows).
+struct GroupLds {
+  std::atomic<size_t> set[64] = {};
+  bool ensure(const void* kernel, size_t lds) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return false;
+    if (dev < 0 || dev >= 64)
+      return hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)lds) == hipSuccess;
+    size_t cur = set[dev].load(std::memory_order_acquire);
+    if (lds <= cur) return true;
+    if (hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+        hipSuccess)
+      return false;
+    while (cur < lds && !set[dev].compare_exchange_weak(cur, lds, std::memory_order_acq_rel)) {
+    }
+    return true;
+  }
+};
+
+template <int NC, int NQ>
+aatc_status launch_split(const GroupDecodeArgs& a, int batch, int rwk, int rwv,
+                         hipStream_t st) {
+  constexpr int D = 64 * NC;
+  const size_t lds = sizeof(float) * (size_t)D * NQ +
+                     sizeof(uint32_t) * (size_t)kGChunk * (rwk + 1 + rwv + 1) +
+                     sizeof(float) * (size_t)kGChunk * NQ;
+  if (lds > 150 * 1024) return AATC_E_UNSUPPORTED;
+  static GroupLds limit;
+  if (!limit.ensure((const void*)group_split_kernel<NC, NQ>, lds)) return AATC_E_DEVICE;
+  hipLaunchKernelGGL((group_split_kernel<NC, NQ>),
+                     dim3((unsigned)a.n_splits, (unsigned)a.n_groups, (unsigned)batch),
+                     dim3(kGThreads), lds, st, a);
+  return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
+}
+
+template <int NC>
+aatc_status launch_decode_nc(GroupDecodeArgs a, int batch, int rwk, int rwv, hipStream_t st) {
+  hipLaunchKernelGGL((group_query_kernel<NC>), dim3((unsigned)a.n_q_heads, (unsigned)batch),
+                     dim3(kGThreads), 0, st, a);
+  if (hipGetLastError() != hipSuccess) return AATC_E_DEVICE;
+  aatc_status s;
+  if (a.heads <= 4) s = launch_split<NC, 4>(a, batch, rwk, rwv, st);
+  else if (a.heads <= 8) s = launch_split<NC, 8>(a, batch, rwk, rwv, st);
+  else if (a.heads <= 16) s = launch_split<NC, 16>(a, batch, rwk, rwv, st);
+  else s = launch_split<NC, 32>(a, batch, rwk, rwv, st);
+  if (s != AATC_OK) return s;
+  hipLaunchKernelGGL((group_merge_kernel<NC>), dim3((unsigned)a.n_q_heads, (unsigned)batch),
+                     dim3(kGThreads), 0, st, a);
+  return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
+}
+
+}  // namespace
+
+aatc_status launch_group_encode(const void* params, int n_groups, int gkv, const void* x,
+                                aatc_dtype x_dtype, int64_t n_tok, int64_t x_tok_stride,
+                                void* codes, uint16_t* alpha, int64_t cap, int64_t pos,
+                                void* stream) {
+  if (n_tok == 0) return AATC_OK;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t blocks = (n_tok + kGThreads / 64 - 1) / (kGThreads / 64);
+  if (blocks > 0x7fffffff) return AATC_E_UNSUPPORTED;
+  const dim3 grid((unsigned)blocks, (unsigned)n_groups);
+  auto* c8 = static_cast<uint8_t*>(codes);
+#define AATC_GENC(NC)                                                                     \
+  hipLaunchKernelGGL(group_encode_kernel<NC>, grid, dim3(kGThreads), 0, st, params, x,   \
+                     (int)x_dtype, n_tok, x_tok_stride, c8, alpha, cap, pos)
+  switch (gkv) {
+    case 1: AATC_GENC(2); break;
+    case 2: AATC_GENC(4); break;
+    case 3: AATC_GENC(6); break;
+    case 4: AATC_GENC(8); break;
+    default: return AATC_E_UNSUPPORTED;
+  }
+#undef AATC_GENC
+  return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
+}
+
+size_t group_decode_workspace_bytes(int batch, int n_q_heads, int n_kv_heads, int gkv,
+                                    int64_t cap) {
+  const int n_groups = n_kv_heads / gkv;
+  const int heads = n_q_heads / n_groups;
+  return group_ws_layout(batch, n_groups, heads, 128 * gkv, cap).total;
+}
+
+aatc_status launch_group_decode(const void* params_k, const void* params_v, int batch,
+                                int n_q_heads, int n_kv_heads, int gkv, const void* q,
+                                aatc_dtype q_dtype, const void* k_codes,
+                                const uint16_t* k_alpha, const void* v_codes,
+                                const uint16_t* v_alpha, const int32_t* seq_len, int64_t cap,
+                                int k_record_bytes, int v_record_bytes, float softmax_scale,
+                                float* out, void* workspace, void* stream) {
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  GroupDecodeArgs a{};
+  a.params_k = params_k;
+  a.params_v = params_v;
+  a.q = q;
+  a.q_dtype = (int)q_dtype;
+  a.k_codes = static_cast<const uint8_t*>(k_codes);
+  a.k_alpha = k_alpha;
+  a.v_codes = static_cast<const uint8_t*>(v_codes);
+  a.v_alpha = v_alpha;
+  a.seq_len = seq_len;
+  a.cap = cap;
+  a.n_q_heads = n_q_heads;
+  a.n_kv_heads = n_kv_heads;
+  a.gkv = gkv;
+  a.n_groups = n_kv_heads / gkv;
+  a.heads = n_q_heads / a.n_groups;
+  a.scale_log2e = softmax_scale * 1.4426950408889634f;
+  const GroupWs l = group_ws_layout(batch, a.n_groups, a.heads, 128 * gkv, cap);
+  a.n_splits = l.n_splits;
+  if ((int64_t)l.n_splits > 0xffff || batch > 0xffff) return AATC_E_UNSUPPORTED;
+  char* ws = static_cast<char*>(workspace);
+  a.w = reinterpret_cast<float*>(ws + l.w);
+  a.cst = reinterpret_cast<float*>(ws + l.c);
+  a.part = reinterpret_cast<float*>(ws + l.partials);
+  a.out = out;
+  const int rwk = k_record_bytes / 4, rwv = v_record_bytes / 4;
+  a.rwk = rwk;
+  a.rwv = rwv;
+  switch (gkv) {
+    case 1: return launch_decode_nc<2>(a, batch, rwk, rwv, st);
+    case 2: return launch_decode_nc<4>(a, batch, rwk, rwv, st);
+    case 3: return launch_decode_nc<6>(a, batch, rwk, rwv, st);
+    case 4: return launch_decode_nc<8>(a, batch, rwk, rwv, st);
+  }
+  return AATC_E_UNSUPPORTED;
+}
+
+}  // namespace aatc

@@ -35,6 +35,35 @@ def device_params(cals, device="cuda"):
     return torch.from_numpy(host).to(device)
 
 
+def abi_group_calibration(cal: "ora.Calibration"):
+    """ctypes aatc_group_calibration holding an oracle calibration of a head group."""
+    import paper_2608_14191_amd as P
+    d = cal.d
+    c = P.GroupCalibration()
+    c.d = d
+    c.budget_bits = cal.budget
+    c.record_bytes = cal.record_bytes
+    c.d_active = cal.d_active
+    c.quantizer = P.QUANT_MIDRISE if cal.quantizer == "midrise" else P.QUANT_MIDTREAD
+    np.ctypeslib.as_array(c.transform)[:d * d] = cal.T32.reshape(-1)
+    np.ctypeslib.as_array(c.bits)[:d] = cal.bits
+    np.ctypeslib.as_array(c.scale_f16)[:d] = cal.s16.view(np.uint16)
+    np.ctypeslib.as_array(c.perm)[:d] = cal.perm
+    np.ctypeslib.as_array(c.sigma2)[:d] = cal.sigma2
+    np.ctypeslib.as_array(c.weight)[:d] = cal.weight
+    np.ctypeslib.as_array(c.bits_eig)[:d] = cal.bits_eig
+    return c
+
+
+def group_device_params(cals, device="cuda"):
+    """Device parameter block (torch uint8) of per-group calibrations (oracle or ABI)."""
+    import torch
+    import paper_2608_14191_amd as P
+    abi = [c if isinstance(c, P.GroupCalibration) else abi_group_calibration(c) for c in cals]
+    host = P.aatc_group_params_pack(abi)
+    return torch.from_numpy(host).to(device)
+
+
 def stored_to_torch(arr):
     """float32 array or bf16 bit array -> torch tensor of the same values (CPU)."""
     import torch

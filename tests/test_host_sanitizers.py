@@ -1,5 +1,5 @@
 """The host side of the library (argument validation, parameter packing, calibration and bit
-allocation: abi.cpp and calibrate.cpp) built with the host compiler's AddressSanitizer and
+allocation: abi.cpp, group_abi.cpp and calibrate.cpp) built with the host compiler's AddressSanitizer and
 UndefinedBehaviorSanitizer, with the HIP launchers replaced by host stubs
 (tests/host_stub/launch_stub.cpp), and driven by the CPU tests of the C ABI."""
 import os
@@ -29,6 +29,7 @@ def test_abi_and_calibration_under_asan_and_ubsan(tmp_path):
            "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
            "-I", os.path.join(ROOT, "include"), "-I", CSRC,
            os.path.join(CSRC, "calibrate.cpp"), os.path.join(CSRC, "abi.cpp"),
+           os.path.join(CSRC, "group_abi.cpp"),
            os.path.join(ROOT, "tests", "host_stub", "launch_stub.cpp"), "-o", str(lib)]
     build = subprocess.run(cmd, capture_output=True, text=True)
     assert build.returncode == 0, build.stderr
@@ -36,7 +37,8 @@ def test_abi_and_calibration_under_asan_and_ubsan(tmp_path):
                ASAN_OPTIONS="detect_leaks=0:abort_on_error=1",
                UBSAN_OPTIONS="print_stacktrace=1:halt_on_error=1")
     run = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                          os.path.join(ROOT, "tests", "test_lib_cpu.py")],
+                          os.path.join(ROOT, "tests", "test_lib_cpu.py"),
+                          os.path.join(ROOT, "tests", "test_lib_groups_cpu.py")],
                          capture_output=True, text=True, env=env, cwd=ROOT, timeout=600)
     tail = (run.stdout + run.stderr)[-3000:]
     assert run.returncode == 0, tail
