@@ -224,6 +224,113 @@ def run_encode_bench(avg_bits, reps=5):
                 bytes=int(L * H * (2 * 128 * 2 + rk + rv + 4)))
 
 
+GROUP_WORKLOAD = ("llama31_8b_decode_b1_32k_groups: batch 1, 32 q / 8 kv heads in 2 head "
+                  "groups of 4 (512 channels each), 32768 tokens, 2.75 bits; step = decode "
+                  "attention (query weights, splits, merge)")
+
+
+def setup_group_decode(gkv=4):
+    """The Llama decode shape under head-group transforms: host calibrations of each group's
+    concatenated calibration draws, the 32768 tokens of every group encoded on the GPU (the
+    group prefill, timed)."""
+    import concurrent.futures as cf
+    import torch
+    import paper_2608_14191_amd as P
+    from kvsynth import workload
+
+    w = workload(2)
+    H, L = w.n_kv_heads, w.n_tokens
+    ng = H // gkv
+    avg = w.cfg["avg_bits"][0]
+    t0 = time.time()
+    xs = [(kind, np.concatenate([w.calib(h, kind) for h in range(g * gkv, (g + 1) * gkv)],
+                                axis=1)) for kind in ("k", "v") for g in range(ng)]
+    with cf.ThreadPoolExecutor(max_workers=len(xs)) as ex:       # (ctypes drops the GIL)
+        cals = list(ex.map(lambda kx: P.aatc_calibrate_group(kx[1], avg), xs))
+    cal_k, cal_v = cals[:ng], cals[ng:]
+    _log(f"[groups] calibrated {len(cals)} group tensors in {time.time() - t0:.1f}s")
+    pk = torch.from_numpy(P.aatc_group_params_pack(cal_k)).cuda()
+    pv = torch.from_numpy(P.aatc_group_params_pack(cal_v)).cuda()
+    rk, rv = cal_k[0].record_bytes, cal_v[0].record_bytes
+    kc = torch.zeros((1, ng, L, rk), dtype=torch.uint8, device="cuda")
+    vc = torch.zeros((1, ng, L, rv), dtype=torch.uint8, device="cuda")
+    ka = torch.zeros((1, ng, L), dtype=torch.int16, device="cuda")
+    va = torch.zeros((1, ng, L), dtype=torch.int16, device="cuda")
+    xk = bf16_tensor(np.stack([w.cache(0, h, "k") for h in range(H)], axis=1))
+    xv = bf16_tensor(np.stack([w.cache(0, h, "v") for h in range(H)], axis=1))
+
+    def prefill():
+        P.aatc_group_encode(pk, ng, gkv, xk, L, H * 128, kc[0], ka[0], L, 0)
+        P.aatc_group_encode(pv, ng, gkv, xv, L, H * 128, vc[0], va[0], L, 0)
+
+    prefill()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    prefill()
+    e1.record()
+    torch.cuda.synchronize()
+    enc_ms = e0.elapsed_time(e1)
+    del xk, xv
+    q = bf16_tensor(w.queries(0)[None])
+    return dict(w=w, P=P, pk=pk, pv=pv, kc=kc, vc=vc, ka=ka, va=va, q=q, L=L, rk=rk, rv=rv,
+                gkv=gkv, ng=ng, enc_ms=enc_ms)
+
+
+def run_group_decode_bench(s, steps=40):
+    """Group decode steps captured in HIP graphs over rotating cache copies; HIP events
+    around the replays give the time of one step's three kernels."""
+    import torch
+    P, w = s["P"], s["w"]
+    H, HQ, L = w.n_kv_heads, w.n_q_heads, s["L"]
+    per_copy = sum(t.numel() for t in (s["kc"], s["vc"])) + 2 * (s["ka"].numel() + s["va"].numel())
+    n_copies = max(2, math.ceil(512e6 / per_copy))
+    copies = [(s["kc"], s["ka"], s["vc"], s["va"])]
+    for _ in range(n_copies - 1):
+        copies.append(tuple(t.clone() for t in copies[0]))
+    lens = torch.full((1,), L, dtype=torch.int32, device="cuda")
+    out = torch.zeros((1, HQ, 128), dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.aatc_group_decode_workspace_bytes(1, HQ, H, s["gkv"], L),
+                     dtype=torch.uint8, device="cuda")
+
+    def step(i):
+        kc, ka, vc, va = copies[i % n_copies]
+        P.aatc_group_decode_attention(s["pk"], s["pv"], 1, HQ, H, s["gkv"], s["q"], kc, ka, vc,
+                                      va, lens, L, s["rk"], s["rv"], 128 ** -0.5, out, ws)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(3):
+            step(i)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(n_copies):
+            step(i)
+    g.replay()
+    torch.cuda.synchronize()
+    reps = max(1, steps // n_copies)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    step_ms = e0.elapsed_time(e1) / (reps * n_copies)
+    nb = s["ng"] * L * (s["rk"] + s["rv"] + 4)
+    tok_s = L / (s["enc_ms"] * 1e-3)
+    return {"workload": GROUP_WORKLOAD, "bytes_per_step": nb,
+            "kernel_us_per_step": round(step_ms * 1e3, 2),
+            "GBps": round(nb / (step_ms * 1e-3) / 1e9, 1),
+            "frac": round(nb / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "cache_copies": n_copies,
+            "prefill_encode": {"tokens": L, "ms": round(s["enc_ms"], 3),
+                               "tokens_per_s": round(tok_s, 1)},
+            "data": "synthetic tokens, host calibrations"}
+
+
 # Dense int8 matrix-core peak of the MI355X (ops/s), for the encode's transform products.
 MFMA_I8_PEAK_OPS = 5.0e15
 
@@ -360,6 +467,10 @@ def main():
                     help="eager decodes plus a calibration copy, for rocprofv3 --pmc runs")
     ap.add_argument("--encode-only", action="store_true",
                     help="only the prefill encode entries (for rocprofv3 runs of the encode)")
+    ap.add_argument("--no-groups", action="store_true",
+                    help="skip the head-group decode entry")
+    ap.add_argument("--groups-only", action="store_true",
+                    help="only the head-group entry (for rocprofv3 runs of the group kernels)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -371,6 +482,9 @@ def main():
     if args.encode_only:
         enc = [run_encode_bench(avg) for avg in (2.75, 4.0)]
         print(json.dumps({"encode": [encode_entry(r) for r in enc]}), flush=True)
+        return
+    if args.groups_only:
+        print(json.dumps({"groups": [run_group_decode_bench(setup_group_decode())]}), flush=True)
         return
     s = setup_decode(2)
     if args.counters:
@@ -408,6 +522,13 @@ def main():
             _log(f"[decode cfg {cfg}] kernel {km * 1e3:.1f} us, {nb / (km * 1e-3) / 1e9:.0f} GB/s")
             del so
             torch.cuda.empty_cache()
+    groups = []
+    if not args.no_groups:
+        sg = setup_group_decode()
+        groups.append(run_group_decode_bench(sg))
+        _log(f"[groups] {groups[-1]['kernel_us_per_step']} us/step, {groups[-1]['GBps']} GB/s")
+        del sg
+        torch.cuda.empty_cache()
     line = {
         "metric": "decode-attention HBM GB/s (% of peak) on packed KV; encode tokens/sec",
         "value": round(value, 2),
@@ -431,6 +552,7 @@ def main():
                      "traffic": counted_traffic()},
         "encode": [encode_entry(r) for r in enc],
         "decode_other": other,
+        "groups": groups,
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(s)

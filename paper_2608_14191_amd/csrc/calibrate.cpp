@@ -87,28 +87,41 @@ bool jacobi_eigen(std::vector<double>& a, int n, std::vector<double>& v,
         double theta = (aqq - app) / (2.0 * apq);
         double t = (theta >= 0 ? 1.0 : -1.0) / (std::fabs(theta) + std::sqrt(theta * theta + 1.0));
         double c = 1.0 / std::sqrt(t * t + 1.0), s = t * c;
-        for (int k = 0; k < n; ++k) {        // A <- A J
-          double akp = a[(size_t)k * n + p], akq = a[(size_t)k * n + q];
-          a[(size_t)k * n + p] = c * akp - s * akq;
-          a[(size_t)k * n + q] = s * akp + c * akq;
+        // A <- J^T A J on the symmetric matrix: rows p and q (contiguous) for k != p, q,
+        // mirrored into columns p and q; then the 2 x 2 block.
+        double* ap = &a[(size_t)p * n];
+        double* aq = &a[(size_t)q * n];
+        for (int k = 0; k < n; ++k) {
+          if (k == p || k == q) continue;
+          const double apk = ap[k], aqk = aq[k];
+          const double np_ = c * apk - s * aqk, nq = s * apk + c * aqk;
+          ap[k] = np_;
+          aq[k] = nq;
+          a[(size_t)k * n + p] = np_;
+          a[(size_t)k * n + q] = nq;
         }
-        for (int k = 0; k < n; ++k) {        // A <- J^T A
-          double apk = a[(size_t)p * n + k], aqk = a[(size_t)q * n + k];
-          a[(size_t)p * n + k] = c * apk - s * aqk;
-          a[(size_t)q * n + k] = s * apk + c * aqk;
-        }
-        a[(size_t)p * n + q] = 0.0;
-        a[(size_t)q * n + p] = 0.0;
-        for (int k = 0; k < n; ++k) {        // V <- V J
-          double vkp = v[(size_t)k * n + p], vkq = v[(size_t)k * n + q];
-          v[(size_t)k * n + p] = c * vkp - s * vkq;
-          v[(size_t)k * n + q] = s * vkp + c * vkq;
+        const double npp = c * c * app - 2.0 * s * c * apq + s * s * aqq;
+        const double nqq = s * s * app + 2.0 * s * c * apq + c * c * aqq;
+        ap[p] = npp;
+        aq[q] = nqq;
+        ap[q] = 0.0;
+        aq[p] = 0.0;
+        // V <- V J, with V held transposed (row i = eigenvector column i): rows p and q.
+        double* vp = &v[(size_t)p * n];
+        double* vq = &v[(size_t)q * n];
+        for (int k = 0; k < n; ++k) {
+          const double vkp = vp[k], vkq = vq[k];
+          vp[k] = c * vkp - s * vkq;
+          vq[k] = s * vkp + c * vkq;
         }
       }
     }
   }
   w.resize(n);
   for (int i = 0; i < n; ++i) w[i] = a[(size_t)i * n + i];
+  // back to V columns = eigenvectors
+  for (int i = 0; i < n; ++i)
+    for (int k = i + 1; k < n; ++k) std::swap(v[(size_t)i * n + k], v[(size_t)k * n + i]);
   return converged;
 }
 

@@ -57,10 +57,10 @@ __device__ inline int record_code(const uint32_t* row, int off, int b) {
 
 // ---------------------------------------------------------------------------------------
 // Encode: one wave per (token, group); lane l holds elements and channels l + 64 i.
-// h_c = fl32(sum_j x_j T_jc) exactly: fp64 sums of the exact products x_j Tq_jc, exact
-// while the sum of their magnitudes stays below 2^(53 + g) (every product is a multiple of
-// 2^g, g the lowest set bit of the token's elements); otherwise an interval test, and the
-// exact accumulator where the interval straddles an fp32 rounding boundary.
+// h_c = fl32(sum_j x_j T_jc) exactly: fp64 sums of the exact products x_j T_jc, exact while
+// |x|_1 stays below 2^(31 + g) (every product is a multiple of 2^(g - 22), g the lowest set
+// bit of the token's elements, and |T| <= 1); otherwise an interval test, and the exact
+// accumulator where the interval straddles an fp32 rounding boundary.
 // ---------------------------------------------------------------------------------------
 template <int NC>
 __global__ __launch_bounds__(kGThreads) void group_encode_kernel(
@@ -96,51 +96,45 @@ __global__ __launch_bounds__(kGThreads) void group_encode_kernel(
   }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) glsb = min(glsb, __shfl_xor(glsb, o, 64));
-  double s[NC], a[NC];
+  // |x|_1 bounds sum_j |x_j T_jc| for every channel (|T| <= 1).
+  float l1 = 0.f;
 #pragma unroll
-  for (int k = 0; k < NC; ++k) s[k] = a[k] = 0.0;
-  const int4* tcol[NC];
+  for (int i = 0; i < NC; ++i) l1 += fabsf(xl[i]);
+  l1 = g_wave_sum(l1);
+  double s[NC];
 #pragma unroll
-  for (int k = 0; k < NC; ++k)
-    tcol[k] = reinterpret_cast<const int4*>(gp->Tqt + (size_t)(lane + 64 * k) * D);
+  for (int k = 0; k < NC; ++k) s[k] = 0.0;
+  // Row j of T (fp32, exact multiples of 2^-22): lane l reads channels l + 64 k, one
+  // coalesced row per element; products x_j T_jc are exact in fp64.
+  const float* trow = gp->T + lane;
 #pragma unroll
   for (int i = 0; i < NC; ++i) {
-#pragma unroll 1
-    for (int jb = 0; jb < 64; jb += 8) {
-      int4 tv[NC][2];
+#pragma unroll 4
+    for (int jj = 0; jj < 64; ++jj) {
+      const double xd =
+          (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(xl[i]), jj));
+      const float* tr = trow + (size_t)(64 * i + jj) * D;
 #pragma unroll
-      for (int k = 0; k < NC; ++k) {
-        tv[k][0] = tcol[k][(64 * i + jb) / 4];
-        tv[k][1] = tcol[k][(64 * i + jb) / 4 + 1];
-      }
-#pragma unroll
-      for (int jj = 0; jj < 8; ++jj) {
-        const double xd =
-            (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(xl[i]), jb + jj));
-#pragma unroll
-        for (int k = 0; k < NC; ++k) {
-          const int4 q = tv[k][jj >> 2];
-          const int ti = (jj & 3) == 0 ? q.x : (jj & 3) == 1 ? q.y : (jj & 3) == 2 ? q.z : q.w;
-          const double tq = (double)ti;
-          s[k] = fma(xd, tq, s[k]);
-          a[k] = fma(fabs(xd), fabs(tq), a[k]);
-        }
-      }
+      for (int k = 0; k < NC; ++k) s[k] = fma(xd, (double)tr[64 * k], s[k]);
     }
   }
-  const double lim = ldexp(1.0 - 0x1p-40, 53 + min(glsb, 900));
+  // Every product, hence every partial sum, is a multiple of 2^(g - 22) (g the lowest set
+  // bit of the token's elements); below 2^(53 + g - 22) in magnitude they are all fp64
+  // numbers and s is exact.  The float sum l1 is within 2^-14 relative of |x|_1.
+  const double l1d = (double)l1 * (1.0 + 0x1p-14);
+  const bool exact = l1d < ldexp(1.0, 31 + min(glsb, 900));
   float r[NC];
   float m = 0.f;
 #pragma unroll
   for (int k = 0; k < NC; ++k) {
     const int c = lane + 64 * k;
-    const double sv = ldexp(s[k], -kTFrac), av = ldexp(a[k], -kTFrac);
+    const double sv = s[k];
     float h;
-    if (a[k] < lim) {
+    if (exact) {
       h = (float)sv;
     } else {
-      const double bnd = av * (D * 0x1p-52);
-      const double bb = bnd * (1.0 + 0x1p-48) + fabs(sv) * 0x1p-51 + 0x1p-1060;
+      // fp64 sum of D exact products: |error| <= D 2^-53 sum |p| <= D 2^-53 |x|_1
+      const double bb = l1d * (D * 0x1p-52) + fabs(sv) * 0x1p-51 + 0x1p-1060;
       const float lo = (float)(sv - bb), hi = (float)(sv + bb);
       h = lo;
       if (lo != hi && gp->bits[c] > 0) {
@@ -198,33 +192,47 @@ struct GroupDecodeArgs {
   float* out;
 };
 
-// One workgroup per (sequence, query head): W_c for the head's group channels.
+// One workgroup per (sequence, query head): W_c for the head's group channels.  Wave w
+// sums the query against rows 32 w .. 32 w + 31 of the head's block of T (lane l: channels
+// l + 64 m, coalesced rows), and the four partial sums meet in LDS.
 template <int NC>
 __global__ __launch_bounds__(kGThreads) void group_query_kernel(GroupDecodeArgs a) {
   constexpr int D = 64 * NC;
   __shared__ float qs[128];
+  __shared__ float part[kGThreads / 64][D];
   __shared__ float red[kGThreads / 64];
-  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
+  const int wave = tid >> 6;
   const int gq = a.n_q_heads / a.n_kv_heads;
   const int k = h / gq, g = k / a.gkv, kk = k % a.gkv, hl = h - g * a.heads;
   const GroupParams* gp = group_params(a.params_k, g);
   if (tid < 128) qs[tid] = load_elem(a.q, a.q_dtype, ((int64_t)b * a.n_q_heads + h) * 128 + tid);
   __syncthreads();
+  float acc[NC];
+#pragma unroll
+  for (int m = 0; m < NC; ++m) acc[m] = 0.f;
+  const float* trow = gp->T + (size_t)(kk * 128 + 32 * wave) * D + lane;
+#pragma unroll 8
+  for (int j = 0; j < 32; ++j) {
+    const float qj = qs[32 * wave + j];
+#pragma unroll
+    for (int m = 0; m < NC; ++m) acc[m] = fmaf(qj, trow[(size_t)j * D + 64 * m], acc[m]);
+  }
+#pragma unroll
+  for (int m = 0; m < NC; ++m) part[wave][lane + 64 * m] = acc[m];
+  __syncthreads();
   const bool midrise = gp->quantizer == AATC_QUANT_MIDRISE;
   const size_t rowi = ((size_t)b * a.n_groups + g) * a.heads + hl;
   float csum = 0.f;
   for (int c = tid; c < D; c += kGThreads) {
-    float acc = 0.f;
-    const float* tcol = gp->T + (size_t)(kk * 128) * D + c;
-#pragma unroll 8
-    for (int j = 0; j < 128; ++j) acc = fmaf(qs[j], tcol[(size_t)j * D], acc);
+    const float qt = (part[0][c] + part[1][c]) + (part[2][c] + part[3][c]);
     const int bc = gp->bits[c];
-    const float wv = bc > 0 ? ldexpf(acc * gp->s[c] * a.scale_log2e, 1 - bc) : 0.f;
+    const float wv = bc > 0 ? ldexpf(qt * gp->s[c] * a.scale_log2e, 1 - bc) : 0.f;
     a.w[rowi * D + c] = wv;
     csum += midrise ? 0.5f * wv : 0.f;
   }
   csum = g_wave_sum(csum);
-  if ((tid & 63) == 0) red[tid >> 6] = csum;
+  if (lane == 0) red[wave] = csum;
   __syncthreads();
   if (tid == 0) a.cst[rowi] = red[0] + red[1] + red[2] + red[3];
 }
@@ -261,7 +269,10 @@ __global__ __launch_bounds__(kGThreads) void group_split_kernel(GroupDecodeArgs 
   uint32_t* kc = reinterpret_cast<uint32_t*>(wl + D * NQ);       // [kGChunk][rsk]
   uint32_t* vc = kc + kGChunk * rsk;                             // [kGChunk][rsv]
   float* pl = reinterpret_cast<float*>(vc + kGChunk * rsv);      // [kGChunk][NQ]
+  uint32_t* kdesc = reinterpret_cast<uint32_t*>(pl + kGChunk * NQ);   // [D]: off | b << 16
   const size_t row0 = ((size_t)b * a.n_groups + g) * a.heads;
+  for (int c = tid; c < D; c += kGThreads)
+    kdesc[c] = (uint32_t)pk->bit_off[c] | ((uint32_t)pk->bits[c] << 16);
   for (int i = tid; i < D * NQ; i += kGThreads) {
     const int c = i / NQ, h = i % NQ;
     wl[i] = h < a.heads ? a.w[(row0 + h) * D + c] : 0.f;
@@ -317,10 +328,10 @@ __global__ __launch_bounds__(kGThreads) void group_split_kernel(GroupDecodeArgs 
       float z[HW];
 #pragma unroll
       for (int m = 0; m < HW; ++m) z[m] = 0.f;
-#pragma unroll 2
+#pragma unroll 4
       for (int c = 0; c < dak; ++c) {
-        const int bc = pk->bits[c], off = pk->bit_off[c];
-        const float cf = (float)record_code(krow, off, bc);
+        const uint32_t dsc = kdesc[c];
+        const float cf = (float)record_code(krow, (int)(dsc & 0xffffu), (int)(dsc >> 16));
         const float* wr = wl + c * NQ + wave * HW;
 #pragma unroll
         for (int m = 0; m < HW; ++m) z[m] = fmaf(wr[m], cf, z[m]);
@@ -385,11 +396,16 @@ __global__ __launch_bounds__(kGThreads) void group_split_kernel(GroupDecodeArgs 
   }
 }
 
-// One workgroup per (sequence, query head): merge the splits, then o = T_V[block] o~.
+// One workgroup per (sequence, query head): merge the splits, then o = T_V[block] o~.  The
+// splits' weights 2^(m_s - M) go to LDS first, so that the weighted sums issue their loads
+// independently.
+constexpr int kGMergeSplits = 1024;              // splits merged per pass of the weights
 template <int NC>
 __global__ __launch_bounds__(kGThreads) void group_merge_kernel(GroupDecodeArgs a) {
   constexpr int D = 64 * NC;
+  constexpr int CPT = (D + kGThreads - 1) / kGThreads;
   __shared__ float ot[D];
+  __shared__ float wsp[kGMergeSplits];
   __shared__ float red[kGThreads / 64];
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
   const int wave = tid >> 6;
@@ -423,22 +439,45 @@ __global__ __launch_bounds__(kGThreads) void group_merge_kernel(GroupDecodeArgs 
     return;
   }
   float L = 0.f;
-  float acc[(D + kGThreads - 1) / kGThreads];
+  float acc[CPT];
 #pragma unroll
-  for (int i = 0; i < (D + kGThreads - 1) / kGThreads; ++i) acc[i] = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const float* p = pb + s * sstride;
-    const float w = __builtin_amdgcn_exp2f(p[0] - M);
-    L = fmaf(w, p[1], L);
+  for (int i = 0; i < CPT; ++i) acc[i] = 0.f;
+  for (int s0 = 0; s0 < ns; s0 += kGMergeSplits) {
+    const int n = min(kGMergeSplits, ns - s0);
+    __syncthreads();                                // (the previous pass's weights are read)
+    float lsum = 0.f;
+    for (int s = tid; s < n; s += kGThreads) {
+      const float* p = pb + (size_t)(s0 + s) * sstride;
+      const float w = __builtin_amdgcn_exp2f(p[0] - M);
+      wsp[s] = w;
+      lsum = fmaf(w, p[1], lsum);
+    }
+    lsum = g_wave_sum(lsum);
+    __syncthreads();
+    if (lane == 0) red[wave] = lsum;
+    __syncthreads();
+    L += (red[0] + red[1]) + (red[2] + red[3]);
 #pragma unroll
-    for (int i = 0; i < (D + kGThreads - 1) / kGThreads; ++i) {
+    for (int i = 0; i < CPT; ++i) {
       const int c = tid + kGThreads * i;
-      if (c < D) acc[i] = fmaf(w, p[4 + c], acc[i]);
+      if (c < D) {
+        const float* p = pb + 4 + c + (size_t)s0 * sstride;
+        float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+        int s = 0;
+        for (; s + 4 <= n; s += 4) {
+          a0 = fmaf(wsp[s], p[(size_t)s * sstride], a0);
+          a1 = fmaf(wsp[s + 1], p[(size_t)(s + 1) * sstride], a1);
+          a2 = fmaf(wsp[s + 2], p[(size_t)(s + 2) * sstride], a2);
+          a3 = fmaf(wsp[s + 3], p[(size_t)(s + 3) * sstride], a3);
+        }
+        for (; s < n; ++s) a0 = fmaf(wsp[s], p[(size_t)s * sstride], a0);
+        acc[i] += (a0 + a1) + (a2 + a3);
+      }
     }
   }
   const float inv_l = L > 0.f ? 1.f / L : 0.f;
 #pragma unroll
-  for (int i = 0; i < (D + kGThreads - 1) / kGThreads; ++i) {
+  for (int i = 0; i < CPT; ++i) {
     const int c = tid + kGThreads * i;
     if (c < D) ot[c] = acc[i] * inv_l;
   }
@@ -481,7 +520,7 @@ aatc_status launch_split(const GroupDecodeArgs& a, int batch, int rwk, int rwv,
   constexpr int D = 64 * NC;
   const size_t lds = sizeof(float) * (size_t)D * NQ +
                      sizeof(uint32_t) * (size_t)kGChunk * (rwk + 1 + rwv + 1) +
-                     sizeof(float) * (size_t)kGChunk * NQ;
+                     sizeof(float) * (size_t)kGChunk * NQ + sizeof(uint32_t) * D;
   if (lds > 150 * 1024) return AATC_E_UNSUPPORTED;
   static GroupLds limit;
   if (!limit.ensure((const void*)group_split_kernel<NC, NQ>, lds)) return AATC_E_DEVICE;
