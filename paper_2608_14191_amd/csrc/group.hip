@@ -396,17 +396,194 @@ __global__ __launch_bounds__(kGThreads) void group_split_kernel(GroupDecodeArgs 
   }
 }
 
+// The same split with the records of all 256 tokens in LDS (key records first, then the
+// value records in the same rows) and eight waves: lane = token, waves 0-3 score the first
+// half of the group's query heads for tokens 0..255 and waves 4-7 the second half (each code
+// feeds NQ / 2 independent products), and thread = value channel.  Used when its LDS fits.
+constexpr int kGWideThreads = 512;
+template <int NC, int NQ>
+__global__ __launch_bounds__(kGWideThreads) void group_split_wide_kernel(GroupDecodeArgs a) {
+  constexpr int D = 64 * NC;
+  constexpr int NT = kGWideThreads;
+  constexpr int HH = NQ / 2;                        // heads scored by each half
+  constexpr int CPT = (D + NT - 1) / NT;
+  static_assert(kGSplit == 256, "four waves of tokens");
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ float ak[kGSplit], av[kGSplit];
+  __shared__ float wred[4][NQ];
+  __shared__ float mh[NQ], lh[NQ], cst[NQ];
+  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tok = tid & (kGSplit - 1), half = wave >> 2;
+  const int len = (int)min((int64_t)max(a.seq_len[b], 0), a.cap);
+  const int s0 = split * kGSplit;
+  if (s0 >= len) return;                            // (whole workgroup, before any barrier)
+  const int nt = min(len, s0 + kGSplit) - s0;
+  const GroupParams* pk = group_params(a.params_k, g);
+  const GroupParams* pv = group_params(a.params_v, g);
+  float* pbase = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits + split) * a.heads) * (D + 4);
+  const int rwk = a.rwk, rwv = a.rwv;
+  if (pk->record_bytes != 4 * rwk || pv->record_bytes != 4 * rwv || pk->d != D || pv->d != D) {
+    if (tid < a.heads) pbase[(size_t)tid * (D + 4)] = NAN;
+    return;
+  }
+  const int rs = max(rwk, rwv) + 1;                 // LDS row stride (one padding dword)
+  float* wl = reinterpret_cast<float*>(smem);                      // [D][NQ]
+  uint32_t* rb = reinterpret_cast<uint32_t*>(wl + D * NQ);         // [kGSplit][rs]
+  float* pl = reinterpret_cast<float*>(rb + kGSplit * rs);         // [kGSplit][NQ]
+  uint32_t* kdesc = reinterpret_cast<uint32_t*>(pl + kGSplit * NQ);   // [D]: off | b << 16
+  const size_t row0 = ((size_t)b * a.n_groups + g) * a.heads;
+  for (int i = tid; i < D * NQ; i += NT) {
+    const int c = i / NQ, h = i % NQ;
+    wl[i] = h < a.heads ? a.w[(row0 + h) * D + c] : 0.f;
+  }
+  for (int c = tid; c < D; c += NT)
+    kdesc[c] = (uint32_t)pk->bit_off[c] | ((uint32_t)pk->bits[c] << 16);
+  if (tid < NQ) cst[tid] = tid < a.heads ? a.cst[row0 + tid] : 0.f;
+  const size_t tok0 = ((size_t)b * a.n_groups + g) * (size_t)a.cap + s0;
+  const uint32_t* kw = reinterpret_cast<const uint32_t*>(a.k_codes + tok0 * pk->record_bytes);
+  const uint32_t* vw = reinterpret_cast<const uint32_t*>(a.v_codes + tok0 * pv->record_bytes);
+  for (int i = tid; i < nt * rwk; i += NT) {
+    const int t = i / rwk, w = i - t * rwk;
+    rb[t * rs + w] = kw[i];
+  }
+  if (tid < kGSplit) {
+    rb[tid * rs + rwk] = 0u;
+    float fk = 0.f, fv = 0.f;
+    if (tid < nt) {
+      fk = __half2float(__ushort_as_half(a.k_alpha[tok0 + tid]));
+      fv = __half2float(__ushort_as_half(a.v_alpha[tok0 + tid]));
+    }
+    ak[tid] = fk;
+    av[tid] = fv;
+  }
+  __syncthreads();
+  // Scores of token `tok` for heads half HH .. half HH + HH - 1.
+  const bool ok = tok < nt;
+  float z[HH];
+  {
+    const uint32_t* krow = rb + (ok ? tok : 0) * rs;
+#pragma unroll
+    for (int h = 0; h < HH; ++h) z[h] = 0.f;
+    const int dak = pk->d_active;
+    const float* wh = wl + half * HH;
+#pragma unroll 2
+    for (int c = 0; c < dak; ++c) {
+      const uint32_t dsc = kdesc[c];
+      const float cf = (float)record_code(krow, (int)(dsc & 0xffffu), (int)(dsc >> 16));
+      const float* wc = wh + c * NQ;
+      if constexpr (HH % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < HH / 4; ++q) {
+          const float4 w4 = reinterpret_cast<const float4*>(wc)[q];
+          z[4 * q] = fmaf(w4.x, cf, z[4 * q]);
+          z[4 * q + 1] = fmaf(w4.y, cf, z[4 * q + 1]);
+          z[4 * q + 2] = fmaf(w4.z, cf, z[4 * q + 2]);
+          z[4 * q + 3] = fmaf(w4.w, cf, z[4 * q + 3]);
+        }
+      } else {
+#pragma unroll
+        for (int h = 0; h < HH; ++h) z[h] = fmaf(wc[h], cf, z[h]);
+      }
+    }
+    const float akt = ak[tok];
+#pragma unroll
+    for (int i = 0; i < HH; ++i) {
+      z[i] = ok ? akt * (z[i] + cst[half * HH + i]) : -INFINITY;
+      const float m = g_wave_max(z[i]);
+      if (lane == 0) wred[wave & 3][half * HH + i] = m;
+    }
+  }
+  __syncthreads();                                  // (every key record read, maxima in)
+  if (tid < NQ) mh[tid] = fmaxf(fmaxf(wred[0][tid], wred[1][tid]), fmaxf(wred[2][tid], wred[3][tid]));
+  for (int i = tid; i < nt * rwv; i += NT) {
+    const int t = i / rwv, w = i - t * rwv;
+    rb[t * rs + w] = vw[i];
+  }
+  if (tid < kGSplit) rb[tid * rs + rwv] = 0u;
+  __syncthreads();
+  {
+    const float avt = av[tok];
+#pragma unroll
+    for (int i = 0; i < HH; ++i) {
+      const int h = half * HH + i;
+      const float p = ok ? __builtin_amdgcn_exp2f(z[i] - mh[h]) : 0.f;
+      pl[tok * NQ + h] = p * avt;
+      const float ps = g_wave_sum(p);
+      if (lane == 0) wred[wave & 3][h] = ps;
+    }
+  }
+  __syncthreads();
+  if (tid < NQ) lh[tid] = (wred[0][tid] + wred[1][tid]) + (wred[2][tid] + wred[3][tid]);
+  // Values: thread = channels tid + 512 i, every token, every head.
+  const bool mr_v = pv->quantizer == AATC_QUANT_MIDRISE;
+  int vb[CPT], vo[CPT];
+  float acc[NQ][CPT];
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = tid + NT * i;
+    vb[i] = c < D ? pv->bits[c] : 0;
+    vo[i] = c < D ? pv->bit_off[c] : 0;
+#pragma unroll
+    for (int h = 0; h < NQ; ++h) acc[h][i] = 0.f;
+  }
+  bool any = false;
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) any = any || vb[i] > 0;
+  if (any) {
+#pragma unroll 2
+    for (int t = 0; t < nt; ++t) {
+      const uint32_t* vrow = rb + t * rs;
+      float cf[CPT];
+#pragma unroll
+      for (int i = 0; i < CPT; ++i)
+        cf[i] = vb[i] > 0 ? (float)record_code(vrow, vo[i], vb[i]) + (mr_v ? 0.5f : 0.f) : 0.f;
+      const float4* pr = reinterpret_cast<const float4*>(pl + t * NQ);
+#pragma unroll
+      for (int q = 0; q < NQ / 4; ++q) {
+        const float4 p4 = pr[q];
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) {
+          acc[4 * q][i] = fmaf(p4.x, cf[i], acc[4 * q][i]);
+          acc[4 * q + 1][i] = fmaf(p4.y, cf[i], acc[4 * q + 1][i]);
+          acc[4 * q + 2][i] = fmaf(p4.z, cf[i], acc[4 * q + 2][i]);
+          acc[4 * q + 3][i] = fmaf(p4.w, cf[i], acc[4 * q + 3][i]);
+        }
+      }
+    }
+  }
+  __syncthreads();                                  // (mh, lh written)
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = tid + NT * i;
+    if (c < D) {
+      const float sc = vb[i] > 0 ? ldexpf(pv->s[c], 1 - vb[i]) : 0.f;
+#pragma unroll
+      for (int h = 0; h < NQ; ++h)
+        if (h < a.heads) pbase[(size_t)h * (D + 4) + 4 + c] = acc[h][i] * sc;
+    }
+  }
+  if (tid < a.heads) {
+    pbase[(size_t)tid * (D + 4)] = mh[tid];
+    pbase[(size_t)tid * (D + 4) + 1] = lh[tid];
+  }
+}
+
 // One workgroup per (sequence, query head): merge the splits, then o = T_V[block] o~.  The
-// splits' weights 2^(m_s - M) go to LDS first, so that the weighted sums issue their loads
-// independently.
+// splits' weights 2^(m_s - M) go to LDS first; thread (sub, c) then sums channel c over one
+// NSUB-th of the splits with independent loads, and the NSUB sums meet in LDS.
+constexpr int kGMergeThreads = 1024;
 constexpr int kGMergeSplits = 1024;              // splits merged per pass of the weights
 template <int NC>
-__global__ __launch_bounds__(kGThreads) void group_merge_kernel(GroupDecodeArgs a) {
+__global__ __launch_bounds__(kGMergeThreads) void group_merge_kernel(GroupDecodeArgs a) {
   constexpr int D = 64 * NC;
-  constexpr int CPT = (D + kGThreads - 1) / kGThreads;
-  __shared__ float ot[D];
+  constexpr int NT = kGMergeThreads;
+  constexpr int NSUB = NT / D;                     // split ranges per channel (2 .. 8)
+  constexpr int NW = NT / 64;
+  __shared__ float ot[NSUB][D];
   __shared__ float wsp[kGMergeSplits];
-  __shared__ float red[kGThreads / 64];
+  __shared__ float red[NW];
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
   const int wave = tid >> 6;
   const int gq = a.n_q_heads / a.n_kv_heads;
@@ -421,7 +598,7 @@ __global__ __launch_bounds__(kGThreads) void group_merge_kernel(GroupDecodeArgs 
   const float* pb = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits) * a.heads + hl) * (D + 4);
   const size_t sstride = (size_t)a.heads * (D + 4);
   float mx = -INFINITY;
-  for (int s = tid; s < ns; s += kGThreads) {
+  for (int s = tid; s < ns; s += NT) {
     const float ms = pb[s * sstride];
     mx = ms != ms ? ms : fmaxf(mx, ms);             // (a NaN mark is kept)
   }
@@ -433,20 +610,18 @@ __global__ __launch_bounds__(kGThreads) void group_merge_kernel(GroupDecodeArgs 
   if (lane == 0) red[wave] = mx;
   __syncthreads();
   float M = red[0];
-  for (int w = 1; w < kGThreads / 64; ++w) M = (M != M || red[w] != red[w]) ? NAN : fmaxf(M, red[w]);
+  for (int w = 1; w < NW; ++w) M = (M != M || red[w] != red[w]) ? NAN : fmaxf(M, red[w]);
   if (M != M) {
     if (tid < 128) out[tid] = NAN;
     return;
   }
-  float L = 0.f;
-  float acc[CPT];
-#pragma unroll
-  for (int i = 0; i < CPT; ++i) acc[i] = 0.f;
+  const int c = tid % D, sub = tid / D;            // (sub >= NSUB: no channel)
+  float L = 0.f, acc = 0.f;
   for (int s0 = 0; s0 < ns; s0 += kGMergeSplits) {
     const int n = min(kGMergeSplits, ns - s0);
     __syncthreads();                                // (the previous pass's weights are read)
     float lsum = 0.f;
-    for (int s = tid; s < n; s += kGThreads) {
+    for (int s = tid; s < n; s += NT) {
       const float* p = pb + (size_t)(s0 + s) * sstride;
       const float w = __builtin_amdgcn_exp2f(p[0] - M);
       wsp[s] = w;
@@ -456,38 +631,38 @@ __global__ __launch_bounds__(kGThreads) void group_merge_kernel(GroupDecodeArgs 
     __syncthreads();
     if (lane == 0) red[wave] = lsum;
     __syncthreads();
-    L += (red[0] + red[1]) + (red[2] + red[3]);
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + kGThreads * i;
-      if (c < D) {
-        const float* p = pb + 4 + c + (size_t)s0 * sstride;
-        float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-        int s = 0;
-        for (; s + 4 <= n; s += 4) {
-          a0 = fmaf(wsp[s], p[(size_t)s * sstride], a0);
-          a1 = fmaf(wsp[s + 1], p[(size_t)(s + 1) * sstride], a1);
-          a2 = fmaf(wsp[s + 2], p[(size_t)(s + 2) * sstride], a2);
-          a3 = fmaf(wsp[s + 3], p[(size_t)(s + 3) * sstride], a3);
-        }
-        for (; s < n; ++s) a0 = fmaf(wsp[s], p[(size_t)s * sstride], a0);
-        acc[i] += (a0 + a1) + (a2 + a3);
+    for (int w = 0; w < NW; ++w) L += red[w];
+    if (sub < NSUB) {
+      const int lo = n * sub / NSUB, hi = n * (sub + 1) / NSUB;
+      const float* p = pb + 4 + c + (size_t)s0 * sstride;
+      float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+      int s = lo;
+      for (; s + 4 <= hi; s += 4) {
+        a0 = fmaf(wsp[s], p[(size_t)s * sstride], a0);
+        a1 = fmaf(wsp[s + 1], p[(size_t)(s + 1) * sstride], a1);
+        a2 = fmaf(wsp[s + 2], p[(size_t)(s + 2) * sstride], a2);
+        a3 = fmaf(wsp[s + 3], p[(size_t)(s + 3) * sstride], a3);
       }
+      for (; s < hi; ++s) a0 = fmaf(wsp[s], p[(size_t)s * sstride], a0);
+      acc += (a0 + a1) + (a2 + a3);
     }
   }
+  if (sub < NSUB) ot[sub][c] = acc;
+  __syncthreads();
   const float inv_l = L > 0.f ? 1.f / L : 0.f;
+  if (tid < D) {
+    float v = 0.f;
 #pragma unroll
-  for (int i = 0; i < CPT; ++i) {
-    const int c = tid + kGThreads * i;
-    if (c < D) ot[c] = acc[i] * inv_l;
+    for (int u = 0; u < NSUB; ++u) v += ot[u][tid];
+    ot[0][tid] = v * inv_l;
   }
   __syncthreads();
   const GroupParams* pv = group_params(a.params_v, g);
-  for (int j = wave; j < 128; j += kGThreads / 64) {
+  for (int j = wave; j < 128; j += NW) {
     const float* trow = pv->T + (size_t)(kk * 128 + j) * D;
     float v = 0.f;
 #pragma unroll
-    for (int m = 0; m < NC; ++m) v = fmaf(trow[lane + 64 * m], ot[lane + 64 * m], v);
+    for (int m = 0; m < NC; ++m) v = fmaf(trow[lane + 64 * m], ot[0][lane + 64 * m], v);
     v = g_wave_sum(v);
     if (lane == 0) out[j] = v;
   }
@@ -518,6 +693,18 @@ template <int NC, int NQ>
 aatc_status launch_split(const GroupDecodeArgs& a, int batch, int rwk, int rwv,
                          hipStream_t st) {
   constexpr int D = 64 * NC;
+  const size_t lds_wide = sizeof(float) * (size_t)D * NQ +
+                          sizeof(uint32_t) * (size_t)kGSplit * (std::max(rwk, rwv) + 1) +
+                          sizeof(float) * (size_t)kGSplit * NQ + sizeof(uint32_t) * D;
+  const dim3 grid((unsigned)a.n_splits, (unsigned)a.n_groups, (unsigned)batch);
+  if (lds_wide <= 144 * 1024) {
+    static GroupLds limit_wide;
+    if (!limit_wide.ensure((const void*)group_split_wide_kernel<NC, NQ>, lds_wide))
+      return AATC_E_DEVICE;
+    hipLaunchKernelGGL((group_split_wide_kernel<NC, NQ>), grid, dim3(kGWideThreads), lds_wide,
+                       st, a);
+    return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
+  }
   const size_t lds = sizeof(float) * (size_t)D * NQ +
                      sizeof(uint32_t) * (size_t)kGChunk * (rwk + 1 + rwv + 1) +
                      sizeof(float) * (size_t)kGChunk * NQ + sizeof(uint32_t) * D;
@@ -542,7 +729,7 @@ aatc_status launch_decode_nc(GroupDecodeArgs a, int batch, int rwk, int rwv, hip
   else s = launch_split<NC, 32>(a, batch, rwk, rwv, st);
   if (s != AATC_OK) return s;
   hipLaunchKernelGGL((group_merge_kernel<NC>), dim3((unsigned)a.n_q_heads, (unsigned)batch),
-                     dim3(kGThreads), 0, st, a);
+                     dim3(kGMergeThreads), 0, st, a);
   return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
 }
 

@@ -151,6 +151,9 @@ CASES = {
                               quantizer="midrise", b_max=16),
     # groups of three (384 channels), fp32 tokens and queries, query-weighting off
     "gkv3_fp32": dict(cfg=1, gkv=3, lens=[96], n_kv_heads=6, n_q_heads=12),
+    # 8 bits over 512 channels: 512-byte records, the split kernel that stages 64-token
+    # chunks (the whole split's records do not fit in LDS)
+    "llama_g2_8bit_records_512b": dict(cfg=2, gkv=4, lens=[300, 129], avg_bits=8.0),
 }
 
 
