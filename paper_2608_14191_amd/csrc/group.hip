@@ -62,110 +62,131 @@ __device__ inline int record_code(const uint32_t* row, int off, int b) {
 // bit of the token's elements, and |T| <= 1); otherwise an interval test, and the exact
 // accumulator where the interval straddles an fp32 rounding boundary.
 // ---------------------------------------------------------------------------------------
+constexpr int kGTokensPerWave = 2;              // tokens sharing each row of T in a wave
 template <int NC>
 __global__ __launch_bounds__(kGThreads) void group_encode_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
     int64_t x_stride, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha, int64_t cap,
     int64_t pos) {
   constexpr int D = 64 * NC;
+  constexpr int TPW = kGTokensPerWave;
   constexpr int kRow = D * kMaxBits / 32 + 1;
   __shared__ uint32_t rec[kGThreads / 64][kRow];
   const int g = blockIdx.y, lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int64_t t = (int64_t)blockIdx.x * (kGThreads / 64) + wave;
-  if (t >= n_tok) return;                           // (whole wave; no barrier follows)
+  const int64_t t0 = ((int64_t)blockIdx.x * (kGThreads / 64) + wave) * TPW;
+  if (t0 >= n_tok) return;                          // (whole wave; no barrier follows)
+  const int nv = (int)min((int64_t)TPW, n_tok - t0);   // this wave's tokens
   const GroupParams* gp = group_params(params, g);
   const int rw = gp->record_bytes >> 2;
   uint32_t* row = rec[wave];
-  for (int i = lane; i < rw + 1; i += 64) row[i] = 0u;
   const size_t esize = dtype == AATC_BF16 ? 2 : 4;
-  const void* xrow = static_cast<const char*>(x) + (t * x_stride + (int64_t)g * D) * esize;
-  float xl[NC];
+  const void* xrow[TPW];
+  float xl[TPW][NC];
 #pragma unroll
-  for (int i = 0; i < NC; ++i) xl[i] = load_elem(xrow, dtype, lane + 64 * i);
-  // Lowest set bit over the token's nonzero elements (4096 for a zero token).
-  int glsb = 4096;
+  for (int u = 0; u < TPW; ++u) {
+    xrow[u] = static_cast<const char*>(x) + ((t0 + min(u, nv - 1)) * x_stride + (int64_t)g * D) * esize;
 #pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const uint32_t bv = __float_as_uint(xl[i]) & 0x7fffffffu;
-    if (bv != 0u) {
-      const int ef = (int)(bv >> 23), m = (int)(bv & 0x7fffffu);
-      glsb = min(glsb, ef ? ef - 150 + __builtin_ctz((uint32_t)m | 0x800000u)
-                          : -149 + __builtin_ctz((uint32_t)m));
-    }
+    for (int i = 0; i < NC; ++i) xl[u][i] = u < nv ? load_elem(xrow[u], dtype, lane + 64 * i) : 0.f;
   }
+  double s[TPW][NC];
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) glsb = min(glsb, __shfl_xor(glsb, o, 64));
-  // |x|_1 bounds sum_j |x_j T_jc| for every channel (|T| <= 1).
-  float l1 = 0.f;
+  for (int u = 0; u < TPW; ++u)
 #pragma unroll
-  for (int i = 0; i < NC; ++i) l1 += fabsf(xl[i]);
-  l1 = g_wave_sum(l1);
-  double s[NC];
-#pragma unroll
-  for (int k = 0; k < NC; ++k) s[k] = 0.0;
+    for (int k = 0; k < NC; ++k) s[u][k] = 0.0;
   // Row j of T (fp32, exact multiples of 2^-22): lane l reads channels l + 64 k, one
-  // coalesced row per element; products x_j T_jc are exact in fp64.
+  // coalesced row per element, used for the wave's TPW tokens; products are exact in fp64.
   const float* trow = gp->T + lane;
 #pragma unroll
   for (int i = 0; i < NC; ++i) {
-#pragma unroll 4
+#pragma unroll 2
     for (int jj = 0; jj < 64; ++jj) {
-      const double xd =
-          (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(xl[i]), jj));
       const float* tr = trow + (size_t)(64 * i + jj) * D;
+      double tv[NC];
 #pragma unroll
-      for (int k = 0; k < NC; ++k) s[k] = fma(xd, (double)tr[64 * k], s[k]);
-    }
-  }
-  // Every product, hence every partial sum, is a multiple of 2^(g - 22) (g the lowest set
-  // bit of the token's elements); below 2^(53 + g - 22) in magnitude they are all fp64
-  // numbers and s is exact.  The float sum l1 is within 2^-14 relative of |x|_1.
-  const double l1d = (double)l1 * (1.0 + 0x1p-14);
-  const bool exact = l1d < ldexp(1.0, 31 + min(glsb, 900));
-  float r[NC];
-  float m = 0.f;
+      for (int k = 0; k < NC; ++k) tv[k] = (double)tr[64 * k];
 #pragma unroll
-  for (int k = 0; k < NC; ++k) {
-    const int c = lane + 64 * k;
-    const double sv = s[k];
-    float h;
-    if (exact) {
-      h = (float)sv;
-    } else {
-      // fp64 sum of D exact products: |error| <= D 2^-53 sum |p| <= D 2^-53 |x|_1
-      const double bb = l1d * (D * 0x1p-52) + fabs(sv) * 0x1p-51 + 0x1p-1060;
-      const float lo = (float)(sv - bb), hi = (float)(sv + bb);
-      h = lo;
-      if (lo != hi && gp->bits[c] > 0) {
-        // (the exact accumulator holds any sum of up to 512 such products: each is below
-        // 2^46 units of its lsb, so 512 of them stay below 2^137, inside its 320 bits)
-        const int32_t* tc = gp->Tqt + (size_t)c * D;
-        h = exact_dot_q22([&](int j) { return load_elem(xrow, dtype, j); },
-                          [&](int j) { return tc[j]; }, D);
+      for (int u = 0; u < TPW; ++u) {
+        const double xd =
+            (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(xl[u][i]), jj));
+#pragma unroll
+        for (int k = 0; k < NC; ++k) s[u][k] = fma(xd, tv[k], s[u][k]);
       }
     }
-    r[k] = h * gp->inv_s[c];
-    m = fmaxf(m, gp->bits[c] > 0 ? fabsf(r[k]) : 0.f);
   }
-  const __half a16 = token_alpha(g_wave_max(m));
-  const float inv = inverse_alpha(a16);
-  const bool midrise = gp->quantizer == AATC_QUANT_MIDRISE;
-  group_wave_sync();                                 // the cleared row before the ORs
 #pragma unroll
-  for (int k = 0; k < NC; ++k) {
-    const int c = lane + 64 * k;
-    const int b = gp->bits[c], off = gp->bit_off[c];
-    if (b > 0) {
-      const uint32_t u = quantize_code(r[k], inv, b, midrise);
-      atomicOr(&row[off >> 5], u << (off & 31));
-      if ((off & 31) + b > 32) atomicOr(&row[(off >> 5) + 1], u >> (32 - (off & 31)));
+  for (int u = 0; u < TPW; ++u) {
+    if (u >= nv) break;                             // (uniform)
+    const int64_t t = t0 + u;
+    // Lowest set bit over the token's nonzero elements (4096 for a zero token), and |x|_1,
+    // which bounds sum_j |x_j T_jc| for every channel (|T| <= 1).
+    int glsb = 4096;
+    float l1 = 0.f;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const uint32_t bv = __float_as_uint(xl[u][i]) & 0x7fffffffu;
+      l1 += fabsf(xl[u][i]);
+      if (bv != 0u) {
+        const int ef = (int)(bv >> 23), m = (int)(bv & 0x7fffffu);
+        glsb = min(glsb, ef ? ef - 150 + __builtin_ctz((uint32_t)m | 0x800000u)
+                            : -149 + __builtin_ctz((uint32_t)m));
+      }
     }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) glsb = min(glsb, __shfl_xor(glsb, o, 64));
+    l1 = g_wave_sum(l1);
+    // Every product, hence every partial sum, is a multiple of 2^(g - 22); below
+    // 2^(53 + g - 22) in magnitude they are all fp64 numbers and s is exact.  The float sum
+    // l1 is within 2^-14 relative of |x|_1.
+    const double l1d = (double)l1 * (1.0 + 0x1p-14);
+    const bool exact = l1d < ldexp(1.0, 31 + min(glsb, 900));
+    float r[NC];
+    float m = 0.f;
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+      const int c = lane + 64 * k;
+      const double sv = s[u][k];
+      float h;
+      if (exact) {
+        h = (float)sv;
+      } else {
+        // fp64 sum of D exact products: |error| <= D 2^-53 sum |p| <= D 2^-53 |x|_1
+        const double bb = l1d * (D * 0x1p-52) + fabs(sv) * 0x1p-51 + 0x1p-1060;
+        const float lo = (float)(sv - bb), hi = (float)(sv + bb);
+        h = lo;
+        if (lo != hi && gp->bits[c] > 0) {
+          // (the exact accumulator holds any sum of up to 512 such products: each is below
+          // 2^46 units of its lsb, so 512 of them stay below 2^137, inside its 320 bits)
+          const int32_t* tc = gp->Tqt + (size_t)c * D;
+          const void* xr = xrow[u];
+          h = exact_dot_q22([&](int j) { return load_elem(xr, dtype, j); },
+                            [&](int j) { return tc[j]; }, D);
+        }
+      }
+      r[k] = h * gp->inv_s[c];
+      m = fmaxf(m, gp->bits[c] > 0 ? fabsf(r[k]) : 0.f);
+    }
+    const __half a16 = token_alpha(g_wave_max(m));
+    const float inv = inverse_alpha(a16);
+    const bool midrise = gp->quantizer == AATC_QUANT_MIDRISE;
+    for (int i = lane; i < rw + 1; i += 64) row[i] = 0u;
+    group_wave_sync();                               // the cleared row before the ORs
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+      const int c = lane + 64 * k;
+      const int b = gp->bits[c], off = gp->bit_off[c];
+      if (b > 0) {
+        const uint32_t q = quantize_code(r[k], inv, b, midrise);
+        atomicOr(&row[off >> 5], q << (off & 31));
+        if ((off & 31) + b > 32) atomicOr(&row[(off >> 5) + 1], q >> (32 - (off & 31)));
+      }
+    }
+    group_wave_sync();                               // every OR before the read-out
+    uint32_t* out = reinterpret_cast<uint32_t*>(codes + ((int64_t)g * cap + pos + t) * gp->record_bytes);
+    for (int i = lane; i < rw; i += 64) out[i] = row[i];
+    if (lane == 0) alpha[(int64_t)g * cap + pos + t] = __half_as_ushort(a16);
+    group_wave_sync();                               // the read-out before the next clear
   }
-  group_wave_sync();                                 // every OR before the read-out
-  uint32_t* out = reinterpret_cast<uint32_t*>(codes + ((int64_t)g * cap + pos + t) * gp->record_bytes);
-  for (int i = lane; i < rw; i += 64) out[i] = row[i];
-  if (lane == 0) alpha[(int64_t)g * cap + pos + t] = __half_as_ushort(a16);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -741,7 +762,8 @@ aatc_status launch_group_encode(const void* params, int n_groups, int gkv, const
                                 void* stream) {
   if (n_tok == 0) return AATC_OK;
   const hipStream_t st = static_cast<hipStream_t>(stream);
-  const int64_t blocks = (n_tok + kGThreads / 64 - 1) / (kGThreads / 64);
+  const int64_t per_block = (int64_t)(kGThreads / 64) * kGTokensPerWave;
+  const int64_t blocks = (n_tok + per_block - 1) / per_block;
   if (blocks > 0x7fffffff) return AATC_E_UNSUPPORTED;
   const dim3 grid((unsigned)blocks, (unsigned)n_groups);
   auto* c8 = static_cast<uint8_t*>(codes);
