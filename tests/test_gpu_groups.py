@@ -292,3 +292,26 @@ def test_full_size_llama_groups():
         ref = ora.softmax_attention(q32[j:j + 1], kh[:, blk], vh[:, blk], 1 / np.sqrt(128))
         _assert_heads_close(got[0, j:j + 1], ref, f"query head {j}")
     _log("  group 0 query heads within tolerance")
+
+
+@pytest.mark.timeout(300)
+def test_group_incremental_appends_match_bulk():
+    """Tokens appended a few at a time at increasing positions (as decode steps append them)
+    give the same records and scales as one bulk encode, and leave the other positions of
+    the cache untouched."""
+    case = GCase(2, 4, [150])
+    pk = group_device_params(case.cal["k"])
+    bulk, abulk = case.gpu_encode(pk, "k")
+    x = stored_to_torch(case.tokens(0, "k")).cuda().contiguous()
+    cap, ng = case.cap, case.ng
+    inc = torch.full((ng, cap, case.R["k"]), 0xA5, dtype=torch.uint8, device="cuda")
+    ainc = torch.full((ng, cap), 0x1234, dtype=torch.int16, device="cuda")
+    pos = 0
+    for n in (1, 2, 5, 16, 17, 1, 40, 68):
+        P.aatc_group_encode(pk, ng, 4, x[pos:pos + n], n, 8 * 128, inc, ainc, cap, pos)
+        pos += n
+    assert pos == 150
+    torch.cuda.synchronize()
+    assert torch.equal(inc[:, :150].cpu(), bulk[0, :, :150].cpu())
+    assert torch.equal(ainc[:, :150].cpu(), abulk[0, :, :150].cpu())
+    assert bool((inc[:, 150:] == 0xA5).all()) and bool((ainc[:, 150:] == 0x1234).all())
