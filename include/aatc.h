@@ -7,7 +7,8 @@
  * decode attention directly on the packed cache.
  *
  * Conventions shared by every entry point:
- *   - Head dimension d is 128 (v1); other values return AATC_E_UNSUPPORTED.
+ *   - Head dimension d is 128; other values return AATC_E_UNSUPPORTED.  The head-group
+ *     entry points (aatc_*group*, at the end) take groups of 128 gkv channels, gkv <= 4.
  *   - Channel widths are 0..16 bits (b_max <= 16; App. E allows 0 to 16 bits).
  *   - "Device" pointers are HIP device memory owned by the caller; "host" pointers are
  *     ordinary host memory.  Device buffers are 16-byte aligned unless stated
