@@ -315,3 +315,39 @@ def test_group_incremental_appends_match_bulk():
     assert torch.equal(inc[:, :150].cpu(), bulk[0, :, :150].cpu())
     assert torch.equal(ainc[:, :150].cpu(), abulk[0, :, :150].cpu())
     assert bool((inc[:, 150:] == 0xA5).all()) and bool((ainc[:, 150:] == 0x1234).all())
+
+
+@pytest.mark.timeout(300)
+def test_group_end_to_end_with_host_calibration():
+    """aatc_calibrate_group (host C++) -> aatc_group_params_pack -> encode -> decode against
+    the oracle pipeline on the oracle's own calibrations (groups of two, 256 channels)."""
+    case = GCase(2, 2, [260, 90])
+    w = case.w
+    abi = {kind: [P.aatc_calibrate_group(
+        np.concatenate([w.calib(h, kind) for h in range(2 * g, 2 * g + 2)], axis=1),
+        w.cfg["avg_bits"][0]) for g in range(case.ng)] for kind in ("k", "v")}
+    for kind in ("k", "v"):
+        assert abi[kind][0].record_bytes == case.R[kind]
+    pk, pv = group_device_params(abi["k"]), group_device_params(abi["v"])
+    kc, ka = case.gpu_encode(pk, "k")
+    vc, va = case.gpu_encode(pv, "v")
+    q = case.queries()
+    lens = torch.tensor(case.lens, dtype=torch.int32, device="cuda")
+    out = torch.empty((2, case.HQ, 128), dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.aatc_group_decode_workspace_bytes(2, case.HQ, case.H, 2, case.cap),
+                     dtype=torch.uint8, device="cuda")
+    P.aatc_group_decode_attention(pk, pv, 2, case.HQ, case.H, 2, stored_to_torch(q).cuda(), kc,
+                                  ka, vc, va, lens, case.cap, case.R["k"], case.R["v"],
+                                  1 / np.sqrt(128), out, ws)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    for b in range(2):
+        n = case.lens[b]
+        recs = {(kind, g): case.oracle_encode(b, kind, g) for kind in ("k", "v")
+                for g in range(case.ng)}
+        ref = og.group_attention(case.w.as_f32(q[b]), case.H, 2, case.cal["k"], case.cal["v"],
+                                 [recs[("k", g)][0] for g in range(case.ng)],
+                                 [recs[("k", g)][1] for g in range(case.ng)],
+                                 [recs[("v", g)][0] for g in range(case.ng)],
+                                 [recs[("v", g)][1] for g in range(case.ng)], n)
+        _assert_heads_close(got[b], ref, f"seq {b}")
