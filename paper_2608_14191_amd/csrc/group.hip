@@ -51,8 +51,8 @@ __device__ inline float g_wave_sum(float v) {
 // dwords in LDS (the row has one padding dword after the record).
 __device__ inline int record_code(const uint32_t* row, int off, int b) {
   const uint32_t w0 = row[off >> 5], w1 = row[(off >> 5) + 1];
-  const uint32_t v = (uint32_t)(((uint64_t)w1 << 32 | w0) >> (off & 31));
-  return (int)(v << (32 - b)) >> (32 - b);
+  const uint32_t v = __builtin_amdgcn_alignbit(w1, w0, (uint32_t)(off & 31));   // (w1:w0) >> off
+  return __builtin_amdgcn_sbfe((int)v, 0, b);                                   // sign-extended
 }
 
 // ---------------------------------------------------------------------------------------
