@@ -761,16 +761,15 @@ __global__ __launch_bounds__(64) void encode_token_kernel(
 }
 
 // The tokens the matrix-core kernel left with the mark kRedo.  A workgroup scans the marks
-// of kFixTokens tokens of one KV head; if any is set it copies the head's integer
-// transform into LDS (row j: Tq[j][c], rows padded by one word, so the copy and the reads
-// are free of bank conflicts) and its four waves encode the marked tokens exactly, one
-// token per wave at a time.
+// of kFixTokens tokens of one KV head and its four waves encode the marked tokens exactly,
+// one token per wave at a time, each reading the transform columns from the parameter
+// block (a few tokens per workgroup: a copy of the transform into LDS would move as many
+// bytes as the reads it saves).
 constexpr int kFixTokens = 512;
 __global__ __launch_bounds__(256) void encode_fixup_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
     int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
     int64_t cap, int64_t pos) {
-  __shared__ int32_t tq[kD][kD + 1];
   __shared__ uint16_t list[kFixTokens];
   __shared__ int n_list;
   __shared__ uint32_t rec[4][kRecStride];
@@ -795,47 +794,16 @@ __global__ __launch_bounds__(256) void encode_fixup_kernel(
   __syncthreads();
   const int cnt = n_list;
   if (cnt == 0) return;
-  {
-    // 16-byte reads, sixteen per thread in flight: entry 4 e4 + i of Tqt is (c, j) =
-    // (e4 / 32, 4 (e4 % 32) + i).
-    const int4* src = reinterpret_cast<const int4*>(hp->Tqt);
-    int4 v[16];
-#pragma unroll
-    for (int m = 0; m < 16; ++m) v[m] = src[tid + 256 * m];
-#pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      const int e4 = tid + 256 * m, c = e4 >> 5, j = 4 * (e4 & 31);
-      tq[j][c] = v[m].x;
-      tq[j + 1][c] = v[m].y;
-      tq[j + 2][c] = v[m].z;
-      tq[j + 3][c] = v[m].w;
-    }
-  }
+  const size_t esize = dtype == AATC_BF16 ? 2 : 4;
   for (int i = tid; i < 4 * kRecStride; i += 256) (&rec[0][0])[i] = 0u;
   __syncthreads();
-  const size_t esize = dtype == AATC_BF16 ? 2 : 4;
   for (int k = wave; k < cnt; k += 4) {
     const int64_t t = pos + base + list[k];
     const void* xrow = static_cast<const char*>(x) +
                        ((t - pos) * x_stride + (int64_t)head * kD) * esize;
     float xl[2], r[2];
     load_token_pair(xrow, dtype, xl);
-    // The fp64 sums of exact_r_wave, with the transform from LDS.
-    double s[2] = {0.0, 0.0}, a[2] = {0.0, 0.0};
-    auto acc = [&](float xw, int j0) {
-#pragma unroll 8
-      for (int jj = 0; jj < 64; ++jj) {
-        const double xd = (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(xw), jj));
-        const double t0 = (double)tq[j0 + jj][lane], t1 = (double)tq[j0 + jj][lane + 64];
-        s[0] = fma(xd, t0, s[0]);
-        a[0] = fma(fabs(xd), fabs(t0), a[0]);
-        s[1] = fma(xd, t1, s[1]);
-        a[1] = fma(fabs(xd), fabs(t1), a[1]);
-      }
-    };
-    acc(xl[0], 0);
-    acc(xl[1], 64);
-    exact_r_finish(hp, s, a, token_lsb(xl), xl, xrow, dtype, r);
+    exact_r_wave(hp, xl, xrow, dtype, r);
     store_token_wave(hp, r, layout, codes, alpha, cap, t, head, rec[wave]);
   }
 }
