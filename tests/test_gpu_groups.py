@@ -351,3 +351,42 @@ def test_group_end_to_end_with_host_calibration():
                                  [recs[("v", g)][0] for g in range(case.ng)],
                                  [recs[("v", g)][1] for g in range(case.ng)], n)
         _assert_heads_close(got[b], ref, f"seq {b}")
+
+
+@pytest.mark.timeout(300)
+def test_group_long_sequence_of_one_repeated_token():
+    """300000 copies of one token (1172 splits: the merge takes its split weights in two
+    passes): every score is equal, so each query head's output is its KV head's block of
+    the token's reconstruction, which the oracle gives from that one token."""
+    n = 300_000
+    case = GCase(3, 4, [1])
+    H, HQ, gkv, cap = case.H, case.HQ, 4, n + 32
+    tok_k, tok_v = case.tokens(0, "k")[:1], case.tokens(0, "v")[:1]
+    pk, pv = group_device_params(case.cal["k"]), group_device_params(case.cal["v"])
+    caches = {}
+    for kind, tok, params in (("k", tok_k, pk), ("v", tok_v, pv)):
+        x = stored_to_torch(tok).cuda().expand(n, H, 128).contiguous()
+        codes = torch.zeros((1, 1, cap, case.R[kind]), dtype=torch.uint8, device="cuda")
+        alpha = alpha_cache(1, cap, batch=1)
+        P.aatc_group_encode(params, 1, gkv, x, n, H * 128, codes[0], alpha[0], cap, 0)
+        caches[kind] = (codes, alpha)
+        del x
+    q = case.queries()[:1]
+    lens = torch.tensor([n], dtype=torch.int32, device="cuda")
+    out = torch.empty((1, HQ, 128), dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.aatc_group_decode_workspace_bytes(1, HQ, H, gkv, cap), dtype=torch.uint8,
+                     device="cuda")
+    P.aatc_group_decode_attention(pk, pv, 1, HQ, H, gkv, stored_to_torch(q).cuda(),
+                                  caches["k"][0], caches["k"][1], caches["v"][0],
+                                  caches["v"][1], lens, cap, case.R["k"], case.R["v"],
+                                  1 / np.sqrt(128), out, ws)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()[0]
+    rec, a16 = case.oracle_encode(0, "v", 0, x=tok_v)
+    from oracle import aatc as ora
+    vhat = ora.decode_tokens(rec, a16, case.cal["v"][0])[0]            # [512]
+    gq = HQ // H
+    for j in range(HQ):
+        k = j // gq
+        ref = vhat[128 * k:128 * (k + 1)]
+        assert rel_l2(got[j], ref) <= 1e-5, j
