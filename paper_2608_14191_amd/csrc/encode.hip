@@ -699,6 +699,51 @@ __global__ __launch_bounds__(kMThreads) void encode_mfma_kernel(
   }
 }
 
+// exact_r_wave (the same sums in the same order, hence the same r) with the transform
+// entries for j + 16 .. j + 31 in flight while those for j .. j + 15 are summed: four round
+// trips to the parameter block in sequence instead of eight, for more registers.  For the
+// kernels that encode a token or a few per wave, where that latency is the time.
+template <bool LEAN = false>
+__device__ inline void exact_r_wave_pipelined(const HeadParams* hp, const float (&xl)[2],
+                                              const void* xrow, int dtype, float (&r)[2]) {
+  const int lane = threadIdx.x & 63;
+  double s[2] = {0.0, 0.0}, a[2] = {0.0, 0.0};
+  const int4* tc[2] = {reinterpret_cast<const int4*>(hp->Tqt + lane * kD),
+                       reinterpret_cast<const int4*>(hp->Tqt + (lane + 64) * kD)};
+  auto load = [&](int jb, int4 (&tv)[2][4]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) tv[i][q] = tc[i][jb / 4 + q];
+  };
+  auto sum = [&](int jb, const int4 (&tv)[2][4]) {
+    const float xw = (jb < 64) ? xl[0] : xl[1];
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj) {
+      const double xd =
+          (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(xw), (jb + jj) & 63));
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int4 t4 = tv[i][jj >> 2];
+        const int ti = (jj & 3) == 0 ? t4.x : (jj & 3) == 1 ? t4.y : (jj & 3) == 2 ? t4.z : t4.w;
+        const double t = (double)ti;
+        s[i] = fma(xd, t, s[i]);
+        a[i] = fma(fabs(xd), fabs(t), a[i]);
+      }
+    }
+  };
+  int4 ta[2][4], tb[2][4];
+  load(0, ta);
+#pragma unroll 1
+  for (int jb = 0; jb < kD; jb += 32) {
+    load(jb + 16, tb);
+    sum(jb, ta);
+    if (jb + 32 < kD) load(jb + 32, ta);
+    sum(jb + 16, tb);
+  }
+  exact_r_finish<LEAN>(hp, s, a, token_lsb(xl), xl, xrow, dtype, r);
+}
+
 // Codes and scale of one token from r (lane l: channels l and l + 64, one wave) into the
 // LDS row `rec` (zero on entry, zero again on return), then into the cache.  Tile bits are
 // set and cleared with device atomics, so tokens that share a tile word may be encoded by
@@ -756,54 +801,57 @@ __global__ __launch_bounds__(64) void encode_token_kernel(
   const HeadParams* hp = head_params(params, head);
   float xl[2], r[2];
   load_token_pair(xrow, dtype, xl);
-  exact_r_wave(hp, xl, xrow, dtype, r);
+  exact_r_wave_pipelined(hp, xl, xrow, dtype, r);
   store_token_wave(hp, r, layout, codes, alpha, cap, t, head, rec);
 }
 
 // The tokens the matrix-core kernel left with the mark kRedo.  A workgroup scans the marks
-// of kFixTokens tokens of one KV head and its four waves encode the marked tokens exactly,
-// one token per wave at a time, each reading the transform columns from the parameter
-// block (a few tokens per workgroup: a copy of the transform into LDS would move as many
-// bytes as the reads it saves).
-constexpr int kFixTokens = 512;
-__global__ __launch_bounds__(256) void encode_fixup_kernel(
+// of kFixTokens tokens of one KV head (eight per thread, read together) and its four waves
+// encode the marked tokens exactly, one token per wave at a time, each reading the
+// transform columns from the parameter block (a few tokens per workgroup: a copy of the
+// transform into LDS would move as many bytes as the reads it saves).
+constexpr int kFixThreads = 256;
+constexpr int kFixWaves = kFixThreads / 64;
+constexpr int kFixTokens = 2048;
+__global__ __launch_bounds__(kFixThreads) void encode_fixup_kernel(
     const void* __restrict__ params, const void* __restrict__ x, int dtype, int64_t n_tok,
     int64_t x_stride, int layout, uint8_t* __restrict__ codes, uint16_t* __restrict__ alpha,
     int64_t cap, int64_t pos) {
   __shared__ uint16_t list[kFixTokens];
   __shared__ int n_list;
-  __shared__ uint32_t rec[4][kRecStride];
-  const int head = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ uint32_t rec[kFixWaves][kRecStride];
+  const int head = blockIdx.y, tid = threadIdx.x, wave = tid >> 6;
   const HeadParams* hp = head_params(params, head);
   const int64_t base = (int64_t)blockIdx.x * kFixTokens;
   if (tid == 0) n_list = 0;
   __syncthreads();
   {
-    // (all sixteen marks of a thread read before any is tested: one round trip)
-    const uint16_t* am = alpha + (int64_t)head * cap + pos + base;
-    uint16_t mv[kFixTokens / 256];
+    // (all marks of a thread read before any is tested, past the end clamped to the last
+    // token: one round trip)
+    const uint16_t* am = alpha + (int64_t)head * cap + pos;
+    uint16_t mv[kFixTokens / kFixThreads];
 #pragma unroll
-    for (int m = 0; m < kFixTokens / 256; ++m) {
-      const int i = tid + 256 * m;
-      mv[m] = base + i < n_tok ? am[i] : (uint16_t)0;
+    for (int m = 0; m < kFixTokens / kFixThreads; ++m)
+      mv[m] = am[min<int64_t>(base + tid + kFixThreads * m, n_tok - 1)];
+#pragma unroll
+    for (int m = 0; m < kFixTokens / kFixThreads; ++m) {
+      const int i = tid + kFixThreads * m;
+      if (mv[m] == kRedo && base + i < n_tok) list[atomicAdd(&n_list, 1)] = (uint16_t)i;
     }
-#pragma unroll
-    for (int m = 0; m < kFixTokens / 256; ++m)
-      if (mv[m] == kRedo) list[atomicAdd(&n_list, 1)] = (uint16_t)(tid + 256 * m);
   }
   __syncthreads();
   const int cnt = n_list;
   if (cnt == 0) return;
   const size_t esize = dtype == AATC_BF16 ? 2 : 4;
-  for (int i = tid; i < 4 * kRecStride; i += 256) (&rec[0][0])[i] = 0u;
+  for (int i = tid; i < kFixWaves * kRecStride; i += kFixThreads) (&rec[0][0])[i] = 0u;
   __syncthreads();
-  for (int k = wave; k < cnt; k += 4) {
+  for (int k = wave; k < cnt; k += kFixWaves) {
     const int64_t t = pos + base + list[k];
     const void* xrow = static_cast<const char*>(x) +
                        ((t - pos) * x_stride + (int64_t)head * kD) * esize;
     float xl[2], r[2];
     load_token_pair(xrow, dtype, xl);
-    exact_r_wave(hp, xl, xrow, dtype, r);
+    exact_r_wave_pipelined<true>(hp, xl, xrow, dtype, r);
     store_token_wave(hp, r, layout, codes, alpha, cap, t, head, rec[wave]);
   }
 }
@@ -842,7 +890,7 @@ aatc_status launch_encode(const void* params, int n_heads, const void* x, aatc_d
     if (hipGetLastError() != hipSuccess) return AATC_E_DEVICE;
     // The tokens whose certificate failed, exactly (stream order: after the kernel above).
     const dim3 fgrid((unsigned)((n_tok + kFixTokens - 1) / kFixTokens), (unsigned)n_heads);
-    hipLaunchKernelGGL(encode_fixup_kernel, fgrid, dim3(256), 0, (hipStream_t)stream, params, x,
+    hipLaunchKernelGGL(encode_fixup_kernel, fgrid, dim3(kFixThreads), 0, (hipStream_t)stream, params, x,
                        (int)x_dtype, n_tok, x_tok_stride, (int)layout,
                        static_cast<uint8_t*>(codes), alpha, cap, pos);
     return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
