@@ -57,12 +57,14 @@ inline const GroupParams* group_params(const void* block, int g) {
 }
 
 // Decode workspace under head groups, per call: the query weights W [batch][n_groups]
-// [heads][d], the midrise constants [batch][n_groups][heads], then the split partials
-// [batch][n_groups][n_splits][heads][d + 4] (m, l, 2 unused, o~[d]).
+// [heads][d], the midrise constants [batch][n_groups][heads], the split partials
+// [batch][n_groups][n_splits][heads][d + 4] (m, l, 2 unused, o~[d]), then for the
+// matrix-core split the weights as fp16 operands [batch][n_groups][d / 32][hi, lo][64 lanes]
+// [8] (16 head slots) and their per-head power-of-two exponents [batch][n_groups][16].
 constexpr int kGSplit = 256;                 // tokens per decode split
 
 struct GroupWs {
-  size_t w, c, partials, total;
+  size_t w, c, partials, wop, wexp, total;
   int n_splits;
 };
 
@@ -71,10 +73,13 @@ inline GroupWs group_ws_layout(int batch, int n_groups, int heads, int d, int64_
   GroupWs l;
   l.n_splits = (int)((cap + kGSplit - 1) / kGSplit);
   const size_t rows = (size_t)batch * n_groups * heads;
+  const size_t gsets = (size_t)batch * n_groups;
   l.w = 0;
   l.c = r256(rows * d * sizeof(float));
   l.partials = r256(l.c + rows * sizeof(float));
-  l.total = l.partials + rows * (size_t)l.n_splits * (d + 4) * sizeof(float);
+  l.wop = r256(l.partials + rows * (size_t)l.n_splits * (d + 4) * sizeof(float));
+  l.wexp = r256(l.wop + gsets * (size_t)(d / 32) * 2 * 64 * 16);
+  l.total = l.wexp + gsets * 16 * sizeof(int32_t);
   return l;
 }
 

@@ -10,9 +10,11 @@
 //   - group_query_kernel: per query head, the channel weights W_c = q~_c s_c 2^(1-b_c)
 //     scale log2(e) of q~ = T[block]^T q (App. B's effective query; the query of KV head k
 //     lives in block k % gkv of its group);
-//   - group_split_kernel: per (sequence, group, 256-token split) the scores of every query
-//     head of the group, an online softmax over 64-token chunks and the transformed-domain
-//     value sums, on the VALU with the records staged in LDS;
+//   - group_split_mfma_kernel: per (sequence, group, 256-token split) the scores of every
+//     query head of the group, the split's softmax and the transformed-domain value sums,
+//     on the matrix cores (fp16 operands) with the records staged in LDS; the VALU kernels
+//     group_split_wide_kernel and group_split_kernel (64-token chunks, an online softmax)
+//     take more query heads per group, wider codes, or records too long for LDS;
 //   - group_merge_kernel: per (sequence, query head) the merge of the split partials and
 //     the inverse transform o = T[block] o~.
 #include <algorithm>
@@ -211,6 +213,9 @@ struct GroupDecodeArgs {
   float* cst;
   float* part;
   float* out;
+  uint16_t* wop;                 // the weights as fp16 operands of the matrix-core split
+  int32_t* wexp;                 //   and their per-head exponents (written when wops)
+  int wops;
 };
 
 // One workgroup per (sequence, query head): W_c for the head's group channels.  Wave w
@@ -221,7 +226,7 @@ __global__ __launch_bounds__(kGThreads) void group_query_kernel(GroupDecodeArgs 
   constexpr int D = 64 * NC;
   __shared__ float qs[128];
   __shared__ float part[kGThreads / 64][D];
-  __shared__ float red[kGThreads / 64];
+  __shared__ float red[kGThreads / 64], redm[kGThreads / 64];
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
   const int wave = tid >> 6;
   const int gq = a.n_q_heads / a.n_kv_heads;
@@ -244,18 +249,54 @@ __global__ __launch_bounds__(kGThreads) void group_query_kernel(GroupDecodeArgs 
   __syncthreads();
   const bool midrise = gp->quantizer == AATC_QUANT_MIDRISE;
   const size_t rowi = ((size_t)b * a.n_groups + g) * a.heads + hl;
-  float csum = 0.f;
-  for (int c = tid; c < D; c += kGThreads) {
-    const float qt = (part[0][c] + part[1][c]) + (part[2][c] + part[3][c]);
-    const int bc = gp->bits[c];
-    const float wv = bc > 0 ? ldexpf(qt * gp->s[c] * a.scale_log2e, 1 - bc) : 0.f;
-    a.w[rowi * D + c] = wv;
-    csum += midrise ? 0.5f * wv : 0.f;
+  constexpr int CPT = (D + kGThreads - 1) / kGThreads;
+  float wvs[CPT];
+  float csum = 0.f, wmax = 0.f;
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = tid + kGThreads * i;
+    wvs[i] = 0.f;
+    if (c < D) {
+      const float qt = (part[0][c] + part[1][c]) + (part[2][c] + part[3][c]);
+      const int bc = gp->bits[c];
+      const float wv = bc > 0 ? ldexpf(qt * gp->s[c] * a.scale_log2e, 1 - bc) : 0.f;
+      a.w[rowi * D + c] = wv;
+      csum += midrise ? 0.5f * wv : 0.f;
+      wvs[i] = wv;
+      wmax = fmaxf(wmax, fabsf(wv));
+    }
   }
   csum = g_wave_sum(csum);
-  if (lane == 0) red[wave] = csum;
+  wmax = g_wave_max(wmax);
+  if (lane == 0) {
+    red[wave] = csum;
+    redm[wave] = wmax;
+  }
   __syncthreads();
   if (tid == 0) a.cst[rowi] = red[0] + red[1] + red[2] + red[3];
+  if (a.wops && hl < 16) {
+    // The matrix-core split's operands: W 2^e (largest |W| in [2^14, 2^15)) as fp16
+    // Wh + Wl, channel c of this head (slot hl) at block c / 32, lane 16 ((c % 32) / 8) + hl,
+    // element c % 8.
+    const float m = fmaxf(fmaxf(redm[0], redm[1]), fmaxf(redm[2], redm[3]));
+    int e = 0;
+    if (m > 0.f) (void)frexpf(m, &e);
+    e = m > 0.f ? 15 - e : 0;
+    const size_t gset = (size_t)b * a.n_groups + g;
+    if (tid == 0) a.wexp[gset * 16 + hl] = e;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + kGThreads * i;
+      if (c < D) {
+        const float w = ldexpf(wvs[i], e);
+        const _Float16 wh = (_Float16)w, wl = (_Float16)(w - (float)wh);
+        const int l = 16 * ((c & 31) >> 3) + hl;
+        uint16_t* o = a.wop + (gset * (D / 32) + (c >> 5)) * (2 * 64 * 8);
+        o[l * 8 + (c & 7)] = __builtin_bit_cast(uint16_t, wh);
+        o[(64 + l) * 8 + (c & 7)] = __builtin_bit_cast(uint16_t, wl);
+      }
+    }
+  }
 }
 
 // One workgroup per (sequence, group, split of kGSplit tokens).  NQ: query heads of a group
@@ -423,7 +464,7 @@ __global__ __launch_bounds__(kGThreads) void group_split_kernel(GroupDecodeArgs 
 // feeds NQ / 2 independent products), and thread = value channel.  Used when its LDS fits.
 constexpr int kGWideThreads = 512;
 template <int NC, int NQ>
-__global__ __launch_bounds__(kGWideThreads) void group_split_wide_kernel(GroupDecodeArgs a) {
+__device__ inline void group_split_wide_body(const GroupDecodeArgs& a) {
   constexpr int D = 64 * NC;
   constexpr int NT = kGWideThreads;
   constexpr int HH = NQ / 2;                        // heads scored by each half
@@ -591,6 +632,393 @@ __global__ __launch_bounds__(kGWideThreads) void group_split_wide_kernel(GroupDe
   }
 }
 
+template <int NC, int NQ>
+__global__ __launch_bounds__(kGWideThreads) void group_split_wide_kernel(GroupDecodeArgs a) {
+  group_split_wide_body<NC, NQ>(a);
+}
+
+// Loads of one staging pass: dwords i0 + u NT (u < kGStageU) of the records (the index past
+// the end clamped to the last dword), all issued before any is used.
+constexpr int kGStageU = 24;
+template <int NT>
+__device__ inline void stage_load(const uint32_t* src, int total, int i0, uint32_t (&v)[kGStageU]) {
+#pragma unroll
+  for (int u = 0; u < kGStageU; ++u) v[u] = src[min(i0 + u * NT, total - 1)];
+}
+// Their stores into LDS rows of rs dwords (token t = i / rw as the high half of
+// i ceil(2^32 / rw): exact for i < 2^32 / rw).
+template <int NT>
+__device__ inline void stage_store(uint32_t* rb, int rs, int total, int rw, int i0,
+                                   const uint32_t (&v)[kGStageU]) {
+  const uint32_t mk = rw > 1 ? (uint32_t)((0x100000000ull + (uint32_t)rw - 1u) / (uint32_t)rw) : 0u;
+#pragma unroll
+  for (int u = 0; u < kGStageU; ++u) {
+    const int i = i0 + u * NT;
+    if (i < total) {
+      const int t = rw > 1 ? (int)__umulhi((uint32_t)i, mk) : i;
+      rb[t * rs + (i - t * rw)] = v[u];
+    }
+  }
+}
+// The records of tokens 0 .. nt-1 (rw dwords each, contiguous at src) into LDS rows, one
+// round trip per pass of kGStageU dwords per thread.
+template <int NT>
+__device__ inline void stage_records(uint32_t* rb, int rs, const uint32_t* src, int nt, int rw) {
+  const int total = nt * rw;
+  for (int i0 = threadIdx.x; i0 < total; i0 += NT * kGStageU) {
+    uint32_t v[kGStageU];
+    stage_load<NT>(src, total, i0, v);
+    stage_store<NT>(rb, rs, total, rw, i0, v);
+  }
+}
+
+// The same with 16-byte loads (src 16-byte aligned, total >= 4): the whole uint4s of the
+// records, the last total % 4 dwords by single loads; kGStage4 uint4 per thread and pass.
+constexpr int kGStage4 = 6;
+template <int NT>
+__device__ inline void stage4_load(const uint32_t* src, int total, int j0, uint4 (&v)[kGStage4],
+                                   uint32_t& tail) {
+  const uint4* s4 = reinterpret_cast<const uint4*>(src);
+  const int n4 = total >> 2;
+#pragma unroll
+  for (int u = 0; u < kGStage4; ++u) v[u] = s4[min(j0 + u * NT, n4 - 1)];   // (n4 >= 1)
+  const int it = 4 * n4 + (int)threadIdx.x;
+  tail = it < total ? src[it] : 0u;
+}
+template <int NT>
+__device__ inline void stage4_store(uint32_t* rb, int rs, int total, int rw, int j0,
+                                    const uint4 (&v)[kGStage4], uint32_t tail, bool first) {
+  const uint32_t mk = rw > 1 ? (uint32_t)((0x100000000ull + (uint32_t)rw - 1u) / (uint32_t)rw) : 0u;
+  auto put = [&](int i, uint32_t x) {
+    const int t = rw > 1 ? (int)__umulhi((uint32_t)i, mk) : i;
+    rb[t * rs + (i - t * rw)] = x;
+  };
+  const int n4 = total >> 2;
+#pragma unroll
+  for (int u = 0; u < kGStage4; ++u) {
+    const int j = j0 + u * NT;
+    if (j < n4) {
+      put(4 * j, v[u].x);
+      put(4 * j + 1, v[u].y);
+      put(4 * j + 2, v[u].z);
+      put(4 * j + 3, v[u].w);
+    }
+  }
+  const int it = 4 * n4 + (int)threadIdx.x;
+  if (first && it < total) put(it, tail);
+}
+// The records into LDS rows: 16-byte loads when src is aligned, one round trip per pass.
+template <int NT>
+__device__ inline void stage_records_any(uint32_t* rb, int rs, const uint32_t* src, int nt, int rw) {
+  const int total = nt * rw;
+  if (total <= 0) return;
+  if ((reinterpret_cast<uintptr_t>(src) & 15u) == 0u && total >= 4) {
+    // (every thread takes the first pass: it also carries the tail dwords)
+    for (int j0 = threadIdx.x; j0 == (int)threadIdx.x || j0 < (total >> 2); j0 += NT * kGStage4) {
+      uint4 v[kGStage4];
+      uint32_t tail;
+      stage4_load<NT>(src, total, j0, v, tail);
+      stage4_store<NT>(rb, rs, total, rw, j0, v, tail, j0 == (int)threadIdx.x);
+    }
+  } else {
+    stage_records<NT>(rb, rs, src, nt, rw);
+  }
+}
+
+// The same split on the matrix cores (up to 16 query heads per group, codes of at most 12
+// bits, which fp16 holds exactly): eight waves, the records of all 256 tokens in LDS.
+//   - Scores: v_mfma_f32_16x16x32_f16 with A = the query weights (16 heads x 32 channels)
+//     and B = the codes of 16 tokens (32 channels x 16 tokens).  Each head's weights come
+//     scaled by a power of two (largest |W| in [2^14, 2^15)) and split into fp16 parts
+//     W' = Wh + Wl (written by group_query_kernel), both multiplied with the same codes into
+//     one fp32 sum (products exact, |W' - Wh - Wl| <= 2^-22 |W'|).
+//   - Values: A = P (16 heads x 32 tokens), P = p alpha^V scaled by a power of two (largest
+//     alpha^V of the split in [2^13, 2^14)) and split the same way, B = the codes of 16
+//     channels over those 32 tokens.  The midrise half step is 1/2 sum_t P, added once.
+// Operand layouts (lane 16 kg + n): A row n, k = 8 kg .. 8 kg + 7; B column n, the same k;
+// the 16 x 16 result row 4 kg + i, column n in element i.
+// DUAL: key and value records in LDS together, every load of the split issued at the start
+// (P then reuses the key rows); otherwise the value records replace the key records after
+// the scores.  A workgroup whose codes are wider takes the VALU body above (uniform).
+typedef _Float16 gh8 __attribute__((ext_vector_type(8)));
+typedef float gf4 __attribute__((ext_vector_type(4)));
+constexpr int kGPRow = kGSplit + 8;              // halves per head row of P (rows 4 banks
+                                                 // apart: conflict-free operand reads)
+constexpr size_t kGPBytes = (size_t)2 * 16 * kGPRow * 2;
+constexpr size_t kGMfmaLdsCap = 144 * 1024;       // dynamic LDS of the matrix-core split
+
+template <int NC>
+inline constexpr size_t group_mfma_lds(int rw_max, bool dual) {
+  const size_t rows = (size_t)kGSplit * (rw_max + 1) * 4;
+  return (size_t)(64 * NC / 32) * 2 * 64 * 16 +               // weight operands
+         (size_t)2 * 64 * NC * 4 +                              // key and value descriptors
+         (dual ? std::max(rows, kGPBytes) + rows : rows + kGPBytes);
+}
+
+template <int NC, bool DUAL>
+__global__ __launch_bounds__(kGWideThreads) void group_split_mfma_kernel(GroupDecodeArgs a) {
+  constexpr int D = 64 * NC;
+  constexpr int NT = kGWideThreads;
+  constexpr int NKB = D / 32;                       // channel blocks of the score products
+  constexpr int NCB = D / 16;                       // channel blocks of the value products
+  constexpr int W4 = NKB * 128 / NT;                // 16-byte operand loads per thread
+  static_assert(kGSplit == 256, "eight waves of 32 tokens");
+  static_assert(NKB * 128 % NT == 0, "whole operand loads");
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ float ak[kGSplit], av[kGSplit];
+  __shared__ float wred[8][16], wred2[8][16];
+  __shared__ float mh[16], lh[16], ph_sum[16], cst[16];
+  __shared__ int wexp[16];
+  __shared__ int pexp;
+  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, kg = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int len = (int)min((int64_t)max(a.seq_len[b], 0), a.cap);
+  const int s0 = split * kGSplit;
+  if (s0 >= len) return;                            // (whole workgroup, before any barrier)
+  const GroupParams* pk = group_params(a.params_k, g);
+  const GroupParams* pv = group_params(a.params_v, g);
+  if (pk->max_bits > 12 || pv->max_bits > 12) {
+    group_split_wide_body<NC, 16>(a);
+    return;
+  }
+  const int nt = min(len, s0 + kGSplit) - s0;
+  float* pbase = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits + split) * a.heads) * (D + 4);
+  const int rwk = a.rwk, rwv = a.rwv;
+  if (pk->record_bytes != 4 * rwk || pv->record_bytes != 4 * rwv || pk->d != D || pv->d != D) {
+    if (tid < a.heads) pbase[(size_t)tid * (D + 4)] = NAN;
+    return;
+  }
+  const int rs = max(rwk, rwv) + 1;                 // LDS row stride (one padding dword)
+  const size_t rows_b = (size_t)kGSplit * rs * 4;
+  gh8* wop = reinterpret_cast<gh8*>(smem);                                  // [NKB][2][64]
+  uint32_t* kdesc = reinterpret_cast<uint32_t*>(wop + NKB * 2 * 64);        // [D]: off | b << 16
+  uint32_t* vdesc = kdesc + D;
+  uint32_t* rbk = vdesc + D;                                                // [kGSplit][rs]
+  uint32_t* rbv = DUAL ? reinterpret_cast<uint32_t*>(reinterpret_cast<uint8_t*>(rbk) +
+                                                     std::max(rows_b, kGPBytes))
+                       : rbk;
+  _Float16* pl = DUAL ? reinterpret_cast<_Float16*>(rbk)                    // [2][16][kGPRow]
+                      : reinterpret_cast<_Float16*>(reinterpret_cast<uint8_t*>(rbk) + rows_b);
+  const size_t gset = (size_t)b * a.n_groups + g;
+  const size_t row0 = gset * a.heads;
+  const size_t tok0 = gset * (size_t)a.cap + s0;
+  const uint32_t* kw = reinterpret_cast<const uint32_t*>(a.k_codes + tok0 * pk->record_bytes);
+  const uint32_t* vw = reinterpret_cast<const uint32_t*>(a.v_codes + tok0 * pv->record_bytes);
+  // (1) Every load first: the weight operands, the records (the first pass of each, 16-byte
+  //     loads where the records are aligned), the scales, descriptors and constants; then
+  //     the stores.
+  auto stage_all = [&]() {
+    const uint4* wsrc = reinterpret_cast<const uint4*>(a.wop) + gset * (NKB * 128);
+    uint4 wv4[W4];
+    const int totk = nt * rwk, totv = nt * rwv;
+    const bool vec = ((reinterpret_cast<uintptr_t>(kw) | reinterpret_cast<uintptr_t>(vw)) & 15u) == 0u &&
+                     totk >= 4 && totv >= 4 && totk <= 4 * NT * kGStage4 && totv <= 4 * NT * kGStage4;
+    if (DUAL && vec) {                              // (uniform; no branch among the loads)
+      uint4 vk[kGStage4], vv[kGStage4];
+      uint32_t tk, tv;
+#pragma unroll
+      for (int i = 0; i < W4; ++i) wv4[i] = wsrc[tid + NT * i];
+      stage4_load<NT>(kw, totk, tid, vk, tk);
+      stage4_load<NT>(vw, totv, tid, vv, tv);
+#pragma unroll
+      for (int i = 0; i < W4; ++i) reinterpret_cast<uint4*>(wop)[tid + NT * i] = wv4[i];
+      stage4_store<NT>(rbk, rs, totk, rwk, tid, vk, tk, true);
+      stage4_store<NT>(rbv, rs, totv, rwv, tid, vv, tv, true);
+    } else {
+#pragma unroll
+      for (int i = 0; i < W4; ++i) wv4[i] = wsrc[tid + NT * i];
+#pragma unroll
+      for (int i = 0; i < W4; ++i) reinterpret_cast<uint4*>(wop)[tid + NT * i] = wv4[i];
+      stage_records_any<NT>(rbk, rs, kw, nt, rwk);
+      if constexpr (DUAL) stage_records_any<NT>(rbv, rs, vw, nt, rwv);
+    }
+  };
+  {
+    // (the small loads of step (1), issued before the records' and stored after them)
+    constexpr int CPT = (D + NT - 1) / NT;
+    uint32_t kbits[CPT], koff[CPT], vbits[CPT], voff[CPT];
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = min(tid + NT * i, D - 1);
+      kbits[i] = pk->bits[c];
+      koff[i] = pk->bit_off[c];
+      vbits[i] = pv->bits[c];
+      voff[i] = pv->bit_off[c];
+    }
+    const int ti = min(tid, nt - 1);
+    const uint16_t ka16 = a.k_alpha[tok0 + ti], va16 = a.v_alpha[tok0 + ti];
+    const int hi = min(tid & 15, a.heads - 1);
+    const float cst_v = a.cst[row0 + hi];
+    const int wexp_v = a.wexp[gset * 16 + hi];
+    stage_all();
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + NT * i;
+      // (a dropped channel: offset 0, width 0, whose field extract is 0)
+      if (c < D) {
+        kdesc[c] = kbits[i] ? koff[i] | (kbits[i] << 16) : 0u;
+        vdesc[c] = vbits[i] ? voff[i] | (vbits[i] << 16) : 0u;
+      }
+    }
+    if (tid < kGSplit) {
+      rbk[tid * rs + rwk] = 0u;
+      if constexpr (DUAL) rbv[tid * rs + rwv] = 0u;
+      ak[tid] = tid < nt ? __half2float(__ushort_as_half(ka16)) : 0.f;
+      av[tid] = tid < nt ? __half2float(__ushort_as_half(va16)) : 0.f;
+    }
+    if (tid < 16) {
+      cst[tid] = tid < a.heads ? cst_v : 0.f;
+      wexp[tid] = tid < a.heads ? wexp_v : 0;
+    }
+  }
+  __syncthreads();
+  if (tid < kGSplit) {
+    // the largest value scale of the split, for the exponent of P's scaling
+    const float m = g_wave_max(av[tid]);
+    if (lane == 0) wred2[wave][0] = m;
+  }
+  // (2) Scores of tokens 32 wave + 16 tb + n, heads 4 kg + i (slots past the group's heads
+  //     hold other data: their operand rows are zeroed).
+  // (no branch: a width-0 extract is 0)
+  auto code_of = [&](const uint32_t* row, uint32_t dsc) -> _Float16 {
+    return (_Float16)(float)record_code(row, (int)(dsc & 0xffffu), (int)(dsc >> 16));
+  };
+  const bool head_ok = n < a.heads;
+  gf4 zs[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  {
+    const uint32_t* krow[2] = {rbk + (32 * wave + n) * rs, rbk + (32 * wave + 16 + n) * rs};
+    const gh8 zero8 = {};
+#pragma unroll 2
+    for (int kb = 0; kb < NKB; ++kb) {
+      const gh8 whi = head_ok ? wop[(2 * kb) * 64 + lane] : zero8;
+      const gh8 wlo = head_ok ? wop[(2 * kb + 1) * 64 + lane] : zero8;
+      const int c0 = 32 * kb + 8 * kg;
+      const uint4 d0 = *reinterpret_cast<const uint4*>(kdesc + c0);
+      const uint4 d1 = *reinterpret_cast<const uint4*>(kdesc + c0 + 4);
+      const uint32_t dk[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb) {
+        gh8 cb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cb[e] = code_of(krow[tb], dk[e]);
+        zs[tb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(whi, cb, zs[tb], 0, 0, 0);
+        zs[tb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wlo, cb, zs[tb], 0, 0, 0);
+      }
+    }
+  }
+  float z[2][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int h = 4 * kg + i;
+    float m = -INFINITY;
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+      const int t = 32 * wave + 16 * tb + n;
+      z[tb][i] = t < nt ? ak[t] * (ldexpf(zs[tb][i], -wexp[h]) + cst[h]) : -INFINITY;
+      m = fmaxf(m, z[tb][i]);
+    }
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    if (n == 0) wred[wave][h] = m;
+  }
+  __syncthreads();                                  // (every key record read, maxima in)
+  if (tid < 16) {
+    float m = wred[0][tid];
+#pragma unroll
+    for (int w = 1; w < 8; ++w) m = fmaxf(m, wred[w][tid]);
+    mh[tid] = m;
+  }
+  if (tid == 0) {
+    const float m = fmaxf(fmaxf(wred2[0][0], wred2[1][0]), fmaxf(wred2[2][0], wred2[3][0]));
+    int e = 0;
+    if (m > 0.f) (void)frexpf(m, &e);
+    pexp = m > 0.f ? 14 - e : 0;                    // max alpha^V 2^pexp in [2^13, 2^14)
+  }
+  if constexpr (!DUAL) {
+    stage_records_any<NT>(rbv, rs, vw, nt, rwv);
+    if (tid < kGSplit) rbv[tid * rs + rwv] = 0u;
+  }
+  __syncthreads();
+  // (3) p = 2^(z - m), P = p alpha^V: the sums of p (the softmax denominator) and of P (the
+  //     midrise half step), and P 2^pexp as fp16 parts in [head][token] rows.
+  {
+    const int pe = pexp;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int h = 4 * kg + i;
+      float ps = 0.f, qs = 0.f;
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb) {
+        const int t = 32 * wave + 16 * tb + n;
+        const float p = t < nt ? __builtin_amdgcn_exp2f(z[tb][i] - mh[h]) : 0.f;
+        const float pv_ = p * av[t];
+        ps += p;
+        qs += pv_;
+        const float sp = ldexpf(pv_, pe);
+        const _Float16 hh = (_Float16)sp;
+        pl[h * kGPRow + t] = hh;
+        pl[(16 + h) * kGPRow + t] = (_Float16)(sp - (float)hh);
+      }
+#pragma unroll
+      for (int o = 8; o >= 1; o >>= 1) {
+        ps += __shfl_xor(ps, o, 64);
+        qs += __shfl_xor(qs, o, 64);
+      }
+      if (n == 0) {
+        wred[wave][h] = ps;
+        wred2[wave][h] = qs;
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < 16) {
+    float ps = 0.f, qs = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      ps += wred[w][tid];
+      qs += wred2[w][tid];
+    }
+    lh[tid] = ps;
+    ph_sum[tid] = qs;
+  }
+  __syncthreads();
+  // (4) Values: wave w takes channel blocks w, w + 8, ...; lane 16 kg + n ends with heads
+  //     4 kg + i of channel 16 cb + n.
+  const bool mr_v = pv->quantizer == AATC_QUANT_MIDRISE;
+  const int pe = pexp;
+  for (int cb = wave; cb < NCB; cb += 8) {
+    const int c = 16 * cb + n;
+    const uint32_t dsc = vdesc[c];
+    gf4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+    for (int tk = 0; tk < kGSplit / 32; ++tk) {
+      const int t0 = 32 * tk + 8 * kg;
+      const gh8 phi = *reinterpret_cast<const gh8*>(pl + n * kGPRow + t0);
+      const gh8 plo = *reinterpret_cast<const gh8*>(pl + (16 + n) * kGPRow + t0);
+      gh8 cv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) cv[e] = code_of(rbv + (t0 + e) * rs, dsc);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(phi, cv, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(plo, cv, acc, 0, 0, 0);
+    }
+    const int bc = (int)(dsc >> 16);
+    const float sc = bc > 0 ? ldexpf(pv->s[c], 1 - bc) : 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int h = 4 * kg + i;
+      if (h < a.heads) {
+        const float o = ldexpf(acc[i], -pe) + (mr_v ? 0.5f * ph_sum[h] : 0.f);
+        pbase[(size_t)h * (D + 4) + 4 + c] = o * sc;
+      }
+    }
+  }
+  if (tid < a.heads) {
+    pbase[(size_t)tid * (D + 4)] = mh[tid];
+    pbase[(size_t)tid * (D + 4) + 1] = lh[tid];
+  }
+}
+
 // One workgroup per (sequence, query head): merge the splits, then o = T_V[block] o~.  The
 // splits' weights 2^(m_s - M) go to LDS first; thread (sub, c) then sums channel c over one
 // NSUB-th of the splits with independent loads, and the NSUB sums meet in LDS.
@@ -710,6 +1138,21 @@ struct GroupLds {
   }
 };
 
+// Whether the matrix-core split fits (its LDS, and that of the VALU body it falls back to
+// for codes over 12 bits, with 16 head slots); *lds gets the size, and the result is true
+// when both record sets fit at once (DUAL).
+template <int NC>
+bool group_mfma_fit(int rwk, int rwv, size_t* lds) {
+  constexpr int D = 64 * NC;
+  const int rwm = std::max(rwk, rwv);
+  const size_t w16 = sizeof(float) * (size_t)D * 16 + sizeof(uint32_t) * (size_t)kGSplit * (rwm + 1) +
+                     sizeof(float) * (size_t)kGSplit * 16 + sizeof(uint32_t) * D;
+  const size_t m2 = std::max(w16, group_mfma_lds<NC>(rwm, true));
+  const size_t m1 = std::max(w16, group_mfma_lds<NC>(rwm, false));
+  *lds = m2 <= kGMfmaLdsCap ? m2 : m1 <= kGMfmaLdsCap ? m1 : 0;
+  return m2 <= kGMfmaLdsCap;
+}
+
 template <int NC, int NQ>
 aatc_status launch_split(const GroupDecodeArgs& a, int batch, int rwk, int rwv,
                          hipStream_t st) {
@@ -718,6 +1161,26 @@ aatc_status launch_split(const GroupDecodeArgs& a, int batch, int rwk, int rwv,
                           sizeof(uint32_t) * (size_t)kGSplit * (std::max(rwk, rwv) + 1) +
                           sizeof(float) * (size_t)kGSplit * NQ + sizeof(uint32_t) * D;
   const dim3 grid((unsigned)a.n_splits, (unsigned)a.n_groups, (unsigned)batch);
+  if constexpr (NQ <= 16) {
+    if (a.wops) {
+      size_t lds = 0;
+      const bool dual = group_mfma_fit<NC>(rwk, rwv, &lds);
+      if (dual) {
+        static GroupLds limit_m2;
+        if (!limit_m2.ensure((const void*)group_split_mfma_kernel<NC, true>, lds))
+          return AATC_E_DEVICE;
+        hipLaunchKernelGGL((group_split_mfma_kernel<NC, true>), grid, dim3(kGWideThreads), lds,
+                           st, a);
+      } else {
+        static GroupLds limit_m1;
+        if (!limit_m1.ensure((const void*)group_split_mfma_kernel<NC, false>, lds))
+          return AATC_E_DEVICE;
+        hipLaunchKernelGGL((group_split_mfma_kernel<NC, false>), grid, dim3(kGWideThreads), lds,
+                           st, a);
+      }
+      return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
+    }
+  }
   if (lds_wide <= 144 * 1024) {
     static GroupLds limit_wide;
     if (!limit_wide.ensure((const void*)group_split_wide_kernel<NC, NQ>, lds_wide))
@@ -740,6 +1203,9 @@ aatc_status launch_split(const GroupDecodeArgs& a, int batch, int rwk, int rwv,
 
 template <int NC>
 aatc_status launch_decode_nc(GroupDecodeArgs a, int batch, int rwk, int rwv, hipStream_t st) {
+  size_t lds_m = 0;
+  (void)group_mfma_fit<NC>(rwk, rwv, &lds_m);
+  a.wops = a.heads <= 16 && lds_m > 0 ? 1 : 0;      // the query kernel writes the operands
   hipLaunchKernelGGL((group_query_kernel<NC>), dim3((unsigned)a.n_q_heads, (unsigned)batch),
                      dim3(kGThreads), 0, st, a);
   if (hipGetLastError() != hipSuccess) return AATC_E_DEVICE;
@@ -820,6 +1286,8 @@ aatc_status launch_group_decode(const void* params_k, const void* params_v, int 
   a.w = reinterpret_cast<float*>(ws + l.w);
   a.cst = reinterpret_cast<float*>(ws + l.c);
   a.part = reinterpret_cast<float*>(ws + l.partials);
+  a.wop = reinterpret_cast<uint16_t*>(ws + l.wop);
+  a.wexp = reinterpret_cast<int32_t*>(ws + l.wexp);
   a.out = out;
   const int rwk = k_record_bytes / 4, rwv = v_record_bytes / 4;
   a.rwk = rwk;

@@ -154,6 +154,10 @@ CASES = {
     # 8 bits over 512 channels: 512-byte records, the split kernel that stages 64-token
     # chunks (the whole split's records do not fit in LDS)
     "llama_g2_8bit_records_512b": dict(cfg=2, gkv=4, lens=[300, 129], avg_bits=8.0),
+    # key codes of 12 bits (the widest the matrix-core split takes: exact in fp16)
+    "gkv2_12bit_codes": dict(cfg=2, gkv=2, lens=[200, 45], avg_bits=8.0, b_max=12),
+    # key codes of 15 bits: the matrix-core split kernel runs its VALU body instead
+    "gkv2_15bit_codes": dict(cfg=2, gkv=2, lens=[140, 33], avg_bits=10.0, b_max=16),
 }
 
 
