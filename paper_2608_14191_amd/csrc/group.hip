@@ -855,7 +855,7 @@ __global__ __launch_bounds__(kGWideThreads) void group_split_mfma_kernel(GroupDe
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int c = tid + NT * i;
-      // (a dropped channel: offset 0, width 0, whose field extract is 0)
+      // (a dropped channel: offset 0, width 0; its code is selected to 0)
       if (c < D) {
         kdesc[c] = kbits[i] ? koff[i] | (kbits[i] << 16) : 0u;
         vdesc[c] = vbits[i] ? voff[i] | (vbits[i] << 16) : 0u;
@@ -880,9 +880,12 @@ __global__ __launch_bounds__(kGWideThreads) void group_split_mfma_kernel(GroupDe
   }
   // (2) Scores of tokens 32 wave + 16 tb + n, heads 4 kg + i (slots past the group's heads
   //     hold other data: their operand rows are zeroed).
-  // (no branch: a width-0 extract is 0)
+  // (the extract is made for every channel and a dropped one, width 0, selected to 0:
+  // no branch around the LDS reads)
   auto code_of = [&](const uint32_t* row, uint32_t dsc) -> _Float16 {
-    return (_Float16)(float)record_code(row, (int)(dsc & 0xffffu), (int)(dsc >> 16));
+    const int bw = (int)(dsc >> 16);
+    const int code = record_code(row, (int)(dsc & 0xffffu), bw);
+    return (_Float16)(float)(bw ? code : 0);
   };
   const bool head_ok = n < a.heads;
   gf4 zs[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
