@@ -460,8 +460,8 @@ aatc_status aatc_group_encode(const void* dev_params, int32_t n_groups, int32_t 
  * k_codes / v_codes [batch][n_groups][cap][R] (RECORDS), k_alpha / v_alpha
  * [batch][n_groups][cap] fp16, q [batch][n_q_heads][128], out [batch][n_q_heads][128]
  * fp32.  Query heads per group (n_q_heads / n_groups) at most 32; records at most 512
- * bytes.  Three launches on `stream` (query weights, 256-token splits, merge with the
- * inverse transform); workspace of aatc_group_decode_workspace_bytes bytes, every value
+ * bytes.  Four launches on `stream` (query weights, 256-token splits, the merge of the
+ * splits, the inverse transform); workspace of aatc_group_decode_workspace_bytes bytes, every value
  * used written earlier in the same call (no zero fill needed).  Errors: AATC_E_INVALID, AATC_E_UNSUPPORTED,
  * AATC_E_WORKSPACE, AATC_E_DEVICE.
  */

@@ -15,8 +15,9 @@
 //     on the matrix cores (fp16 operands) with the records staged in LDS; the VALU kernels
 //     group_split_wide_kernel and group_split_kernel (64-token chunks, an online softmax)
 //     take more query heads per group, wider codes, or records too long for LDS;
-//   - group_merge_kernel: per (sequence, query head) the merge of the split partials and
-//     the inverse transform o = T[block] o~.
+//   - group_merge_sum_kernel, group_merge_apply_kernel: per (sequence, query head) the merge
+//     of the split partials (by 64-channel chunks) and the inverse transform o = T[block] o~
+//     (by 32-row chunks).
 #include <algorithm>
 #include <atomic>
 
@@ -216,6 +217,7 @@ struct GroupDecodeArgs {
   uint16_t* wop;                 // the weights as fp16 operands of the matrix-core split
   int32_t* wexp;                 //   and their per-head exponents (written when wops)
   int wops;
+  float* otl;                    // merged o~ per (sequence, query head)
 };
 
 // One workgroup per (sequence, query head): W_c for the head's group channels.  Wave w
@@ -1022,28 +1024,32 @@ __global__ __launch_bounds__(kGWideThreads) void group_split_mfma_kernel(GroupDe
   }
 }
 
-// One workgroup per (sequence, query head): merge the splits, then o = T_V[block] o~.  The
-// splits' weights 2^(m_s - M) go to LDS first; thread (sub, c) then sums channel c over one
-// NSUB-th of the splits with independent loads, and the NSUB sums meet in LDS.
-constexpr int kGMergeThreads = 1024;
-constexpr int kGMergeSplits = 1024;              // splits merged per pass of the weights
+// The merge in two launches, spread over (query head, channel chunk) and (query head,
+// output rows) so that every CU reads a share of the split partials and of T_V.
+// group_merge_sum_kernel: one workgroup per (sequence, query head, 64 channels of o~): the
+// splits' maximum M and weights 2^(m_s - M) (recomputed by every chunk: a few hundred
+// floats), thread (range, channel) sums one quarter of the splits with eight loads in
+// flight, and o~ = sum_s w_s o~_s / sum_s w_s l_s goes to the workspace (NaN if a split
+// reported mismatched records, 0 for an empty sequence).
+constexpr int kGMergeThreads = 256;
+constexpr int kGMergeSplits = 1024;              // splits weighted per pass
 template <int NC>
-__global__ __launch_bounds__(kGMergeThreads) void group_merge_kernel(GroupDecodeArgs a) {
+__global__ __launch_bounds__(kGMergeThreads) void group_merge_sum_kernel(GroupDecodeArgs a) {
   constexpr int D = 64 * NC;
   constexpr int NT = kGMergeThreads;
-  constexpr int NSUB = NT / D;                     // split ranges per channel (2 .. 8)
+  constexpr int NSUB = NT / 64;                    // split ranges per channel
   constexpr int NW = NT / 64;
-  __shared__ float ot[NSUB][D];
+  __shared__ float ot[NSUB][64];
   __shared__ float wsp[kGMergeSplits];
   __shared__ float red[NW];
-  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
-  const int wave = tid >> 6;
+  const int h = blockIdx.x / NC, ci = blockIdx.x % NC, b = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int gq = a.n_q_heads / a.n_kv_heads;
-  const int k = h / gq, g = k / a.gkv, kk = k % a.gkv, hl = h - g * a.heads;
-  float* out = a.out + ((int64_t)b * a.n_q_heads + h) * 128;
+  const int k = h / gq, g = k / a.gkv, hl = h - g * a.heads;
+  float* otw = a.otl + ((size_t)b * a.n_q_heads + h) * D + 64 * ci;
   const int len = (int)min((int64_t)max(a.seq_len[b], 0), a.cap);
   if (len == 0) {
-    if (tid < 128) out[tid] = 0.f;
+    if (tid < 64) otw[tid] = 0.f;
     return;
   }
   const int ns = (len + kGSplit - 1) / kGSplit;
@@ -1064,10 +1070,10 @@ __global__ __launch_bounds__(kGMergeThreads) void group_merge_kernel(GroupDecode
   float M = red[0];
   for (int w = 1; w < NW; ++w) M = (M != M || red[w] != red[w]) ? NAN : fmaxf(M, red[w]);
   if (M != M) {
-    if (tid < 128) out[tid] = NAN;
+    if (tid < 64) otw[tid] = NAN;
     return;
   }
-  const int c = tid % D, sub = tid / D;            // (sub >= NSUB: no channel)
+  const int c = tid & 63, sub = tid >> 6;
   float L = 0.f, acc = 0.f;
   for (int s0 = 0; s0 < ns; s0 += kGMergeSplits) {
     const int n = min(kGMergeSplits, ns - s0);
@@ -1084,40 +1090,66 @@ __global__ __launch_bounds__(kGMergeThreads) void group_merge_kernel(GroupDecode
     if (lane == 0) red[wave] = lsum;
     __syncthreads();
     for (int w = 0; w < NW; ++w) L += red[w];
-    if (sub < NSUB) {
-      const int lo = n * sub / NSUB, hi = n * (sub + 1) / NSUB;
-      const float* p = pb + 4 + c + (size_t)s0 * sstride;
-      float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-      int s = lo;
-      for (; s + 4 <= hi; s += 4) {
-        a0 = fmaf(wsp[s], p[(size_t)s * sstride], a0);
-        a1 = fmaf(wsp[s + 1], p[(size_t)(s + 1) * sstride], a1);
-        a2 = fmaf(wsp[s + 2], p[(size_t)(s + 2) * sstride], a2);
-        a3 = fmaf(wsp[s + 3], p[(size_t)(s + 3) * sstride], a3);
+    const int lo = n * sub / NSUB, hi = n * (sub + 1) / NSUB;
+    const float* p = pb + 4 + 64 * ci + c + (size_t)s0 * sstride;
+    float a0 = 0.f, a1 = 0.f;
+    int s = lo;
+    for (; s + 8 <= hi; s += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = p[(size_t)(s + u) * sstride];
+#pragma unroll
+      for (int u = 0; u < 8; u += 2) {
+        a0 = fmaf(wsp[s + u], v[u], a0);
+        a1 = fmaf(wsp[s + u + 1], v[u + 1], a1);
       }
-      for (; s < hi; ++s) a0 = fmaf(wsp[s], p[(size_t)s * sstride], a0);
-      acc += (a0 + a1) + (a2 + a3);
     }
+    for (; s < hi; ++s) a0 = fmaf(wsp[s], p[(size_t)s * sstride], a0);
+    acc += a0 + a1;
   }
-  if (sub < NSUB) ot[sub][c] = acc;
+  ot[sub][c] = acc;
   __syncthreads();
-  const float inv_l = L > 0.f ? 1.f / L : 0.f;
-  if (tid < D) {
+  if (tid < 64) {
     float v = 0.f;
 #pragma unroll
     for (int u = 0; u < NSUB; ++u) v += ot[u][tid];
-    ot[0][tid] = v * inv_l;
+    otw[tid] = v * (L > 0.f ? 1.f / L : 0.f);
   }
-  __syncthreads();
+}
+
+// group_merge_apply_kernel: one workgroup per (sequence, query head, 32 output rows):
+// o_j = sum_c T_V[128 kk + j][c] o~_c, thread (row, part) over D / 8 consecutive channels
+// (every load of its slice in flight at once), the eight parts met by shuffles.
+constexpr int kGApplyRows = 32;
+template <int NC>
+__global__ __launch_bounds__(256) void group_merge_apply_kernel(GroupDecodeArgs a) {
+  constexpr int D = 64 * NC;
+  constexpr int PC = D / 8;                         // channels per part (a multiple of 16)
+  const int h = blockIdx.x / (128 / kGApplyRows), jq = blockIdx.x % (128 / kGApplyRows);
+  const int b = blockIdx.y, tid = threadIdx.x;
+  const int gq = a.n_q_heads / a.n_kv_heads;
+  const int k = h / gq, g = k / a.gkv, kk = k % a.gkv;
+  const int j = kGApplyRows * jq + (tid >> 3), part = tid & 7;
   const GroupParams* pv = group_params(a.params_v, g);
-  for (int j = wave; j < 128; j += NW) {
-    const float* trow = pv->T + (size_t)(kk * 128 + j) * D;
-    float v = 0.f;
+  const float4* trow = reinterpret_cast<const float4*>(pv->T + (size_t)(kk * 128 + j) * D + part * PC);
+  const float4* ov = reinterpret_cast<const float4*>(a.otl + ((size_t)b * a.n_q_heads + h) * D + part * PC);
+  float4 tv[PC / 4], o4[PC / 4];
 #pragma unroll
-    for (int m = 0; m < NC; ++m) v = fmaf(trow[lane + 64 * m], ot[0][lane + 64 * m], v);
-    v = g_wave_sum(v);
-    if (lane == 0) out[j] = v;
+  for (int q = 0; q < PC / 4; ++q) {
+    tv[q] = trow[q];
+    o4[q] = ov[q];
   }
+  float v = 0.f;
+#pragma unroll
+  for (int q = 0; q < PC / 4; ++q) {
+    v = fmaf(tv[q].x, o4[q].x, v);
+    v = fmaf(tv[q].y, o4[q].y, v);
+    v = fmaf(tv[q].z, o4[q].z, v);
+    v = fmaf(tv[q].w, o4[q].w, v);
+  }
+#pragma unroll
+  for (int o = 4; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  if (part == 0) a.out[((int64_t)b * a.n_q_heads + h) * 128 + j] = v;
 }
 
 // The dynamic LDS limit of one kernel on the current device, raised once per device when a
@@ -1218,8 +1250,13 @@ aatc_status launch_decode_nc(GroupDecodeArgs a, int batch, int rwk, int rwv, hip
   else if (a.heads <= 16) s = launch_split<NC, 16>(a, batch, rwk, rwv, st);
   else s = launch_split<NC, 32>(a, batch, rwk, rwv, st);
   if (s != AATC_OK) return s;
-  hipLaunchKernelGGL((group_merge_kernel<NC>), dim3((unsigned)a.n_q_heads, (unsigned)batch),
-                     dim3(kGMergeThreads), 0, st, a);
+  hipLaunchKernelGGL((group_merge_sum_kernel<NC>),
+                     dim3((unsigned)(a.n_q_heads * NC), (unsigned)batch), dim3(kGMergeThreads), 0,
+                     st, a);
+  if (hipGetLastError() != hipSuccess) return AATC_E_DEVICE;
+  hipLaunchKernelGGL((group_merge_apply_kernel<NC>),
+                     dim3((unsigned)(a.n_q_heads * (128 / kGApplyRows)), (unsigned)batch),
+                     dim3(256), 0, st, a);
   return hipGetLastError() == hipSuccess ? AATC_OK : AATC_E_DEVICE;
 }
 
@@ -1291,6 +1328,7 @@ aatc_status launch_group_decode(const void* params_k, const void* params_v, int 
   a.part = reinterpret_cast<float*>(ws + l.partials);
   a.wop = reinterpret_cast<uint16_t*>(ws + l.wop);
   a.wexp = reinterpret_cast<int32_t*>(ws + l.wexp);
+  a.otl = reinterpret_cast<float*>(ws + l.ot);
   a.out = out;
   const int rwk = k_record_bytes / 4, rwv = v_record_bytes / 4;
   a.rwk = rwk;
