@@ -32,6 +32,7 @@ namespace aatc {
 namespace {
 
 constexpr int kGThreads = 256;
+constexpr int kGQThreads = 1024;                  // query kernel: sixteen waves of 8 rows
 constexpr int kGChunk = 64;                       // tokens staged per chunk (one per lane)
 
 __device__ inline void group_wave_sync() {
@@ -220,15 +221,18 @@ struct GroupDecodeArgs {
   float* otl;                    // merged o~ per (sequence, query head)
 };
 
-// One workgroup per (sequence, query head): W_c for the head's group channels.  Wave w
-// sums the query against rows 32 w .. 32 w + 31 of the head's block of T (lane l: channels
-// l + 64 m, coalesced rows), and the four partial sums meet in LDS.
+// One workgroup per (sequence, query head): W_c for the head's group channels.  Wave w of
+// sixteen sums the query against rows 8 w .. 8 w + 7 of the head's block of T (lane l:
+// channels l + 64 m, coalesced rows; every load of the wave in flight at once), and the
+// sixteen partial sums meet in LDS.
 template <int NC>
-__global__ __launch_bounds__(kGThreads) void group_query_kernel(GroupDecodeArgs a) {
+__global__ __launch_bounds__(kGQThreads) void group_query_kernel(GroupDecodeArgs a) {
   constexpr int D = 64 * NC;
+  constexpr int NW = kGQThreads / 64;
+  constexpr int RW = 128 / NW;                      // rows of the block per wave
   __shared__ float qs[128];
-  __shared__ float part[kGThreads / 64][D];
-  __shared__ float red[kGThreads / 64], redm[kGThreads / 64];
+  __shared__ float part[NW][D];
+  __shared__ float red[NW], redm[NW];
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
   const int wave = tid >> 6;
   const int gq = a.n_q_heads / a.n_kv_heads;
@@ -239,10 +243,10 @@ __global__ __launch_bounds__(kGThreads) void group_query_kernel(GroupDecodeArgs 
   float acc[NC];
 #pragma unroll
   for (int m = 0; m < NC; ++m) acc[m] = 0.f;
-  const float* trow = gp->T + (size_t)(kk * 128 + 32 * wave) * D + lane;
-#pragma unroll 8
-  for (int j = 0; j < 32; ++j) {
-    const float qj = qs[32 * wave + j];
+  const float* trow = gp->T + (size_t)(kk * 128 + RW * wave) * D + lane;
+#pragma unroll
+  for (int j = 0; j < RW; ++j) {
+    const float qj = qs[RW * wave + j];
 #pragma unroll
     for (int m = 0; m < NC; ++m) acc[m] = fmaf(qj, trow[(size_t)j * D + 64 * m], acc[m]);
   }
@@ -251,15 +255,17 @@ __global__ __launch_bounds__(kGThreads) void group_query_kernel(GroupDecodeArgs 
   __syncthreads();
   const bool midrise = gp->quantizer == AATC_QUANT_MIDRISE;
   const size_t rowi = ((size_t)b * a.n_groups + g) * a.heads + hl;
-  constexpr int CPT = (D + kGThreads - 1) / kGThreads;
+  constexpr int CPT = (D + kGQThreads - 1) / kGQThreads;
   float wvs[CPT];
   float csum = 0.f, wmax = 0.f;
 #pragma unroll
   for (int i = 0; i < CPT; ++i) {
-    const int c = tid + kGThreads * i;
+    const int c = tid + kGQThreads * i;
     wvs[i] = 0.f;
     if (c < D) {
-      const float qt = (part[0][c] + part[1][c]) + (part[2][c] + part[3][c]);
+      float qt = part[0][c];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) qt += part[w][c];
       const int bc = gp->bits[c];
       const float wv = bc > 0 ? ldexpf(qt * gp->s[c] * a.scale_log2e, 1 - bc) : 0.f;
       a.w[rowi * D + c] = wv;
@@ -275,12 +281,19 @@ __global__ __launch_bounds__(kGThreads) void group_query_kernel(GroupDecodeArgs 
     redm[wave] = wmax;
   }
   __syncthreads();
-  if (tid == 0) a.cst[rowi] = red[0] + red[1] + red[2] + red[3];
+  if (tid == 0) {
+    float cs = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) cs += red[w];
+    a.cst[rowi] = cs;
+  }
   if (a.wops && hl < 16) {
     // The matrix-core split's operands: W 2^e (largest |W| in [2^14, 2^15)) as fp16
     // Wh + Wl, channel c of this head (slot hl) at block c / 32, lane 16 ((c % 32) / 8) + hl,
     // element c % 8.
-    const float m = fmaxf(fmaxf(redm[0], redm[1]), fmaxf(redm[2], redm[3]));
+    float m = redm[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) m = fmaxf(m, redm[w]);
     int e = 0;
     if (m > 0.f) (void)frexpf(m, &e);
     e = m > 0.f ? 15 - e : 0;
@@ -288,7 +301,7 @@ __global__ __launch_bounds__(kGThreads) void group_query_kernel(GroupDecodeArgs 
     if (tid == 0) a.wexp[gset * 16 + hl] = e;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      const int c = tid + kGThreads * i;
+      const int c = tid + kGQThreads * i;
       if (c < D) {
         const float w = ldexpf(wvs[i], e);
         const _Float16 wh = (_Float16)w, wl = (_Float16)(w - (float)wh);
@@ -1242,7 +1255,7 @@ aatc_status launch_decode_nc(GroupDecodeArgs a, int batch, int rwk, int rwv, hip
   (void)group_mfma_fit<NC>(rwk, rwv, &lds_m);
   a.wops = a.heads <= 16 && lds_m > 0 ? 1 : 0;      // the query kernel writes the operands
   hipLaunchKernelGGL((group_query_kernel<NC>), dim3((unsigned)a.n_q_heads, (unsigned)batch),
-                     dim3(kGThreads), 0, st, a);
+                     dim3(kGQThreads), 0, st, a);
   if (hipGetLastError() != hipSuccess) return AATC_E_DEVICE;
   aatc_status s;
   if (a.heads <= 4) s = launch_split<NC, 4>(a, batch, rwk, rwv, st);
