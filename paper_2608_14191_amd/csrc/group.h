@@ -58,11 +58,13 @@ inline const GroupParams* group_params(const void* block, int g) {
 
 // Decode workspace under head groups, per call: the query weights W [batch][n_groups]
 // [heads][d], the midrise constants [batch][n_groups][heads], the split partials
-// [batch][n_groups][n_splits][heads][d + 4] (m, l, 2 unused, o~[d]), then for the
+// [batch][n_groups][n_splits][heads][kGPH + d] (m, l, unused to a 128-byte header, o~[d]:
+// every o~ row starts on a 128-byte line), then for the
 // matrix-core split the weights as fp16 operands [batch][n_groups][d / 32][hi, lo][64 lanes]
 // [8] (16 head slots) and their per-head power-of-two exponents [batch][n_groups][16], then
 // the merged transformed-domain outputs o~ [batch][n_groups * heads][d].
 constexpr int kGSplit = 256;                 // tokens per decode split
+constexpr int kGPH = 32;                     // header floats of a split partial row
 
 struct GroupWs {
   size_t w, c, partials, wop, wexp, ot, total;
@@ -78,7 +80,7 @@ inline GroupWs group_ws_layout(int batch, int n_groups, int heads, int d, int64_
   l.w = 0;
   l.c = r256(rows * d * sizeof(float));
   l.partials = r256(l.c + rows * sizeof(float));
-  l.wop = r256(l.partials + rows * (size_t)l.n_splits * (d + 4) * sizeof(float));
+  l.wop = r256(l.partials + rows * (size_t)l.n_splits * (d + kGPH) * sizeof(float));
   l.wexp = r256(l.wop + gsets * (size_t)(d / 32) * 2 * 64 * 16);
   l.ot = r256(l.wexp + gsets * 16 * sizeof(int32_t));
   l.total = l.ot + rows * d * sizeof(float);

@@ -334,11 +334,11 @@ __global__ __launch_bounds__(kGThreads) void group_split_kernel(GroupDecodeArgs 
   const GroupParams* pk = group_params(a.params_k, g);
   const GroupParams* pv = group_params(a.params_v, g);
   // (partial rows are [(sequence, group)][split][head])
-  float* pbase = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits + split) * a.heads) * (D + 4);
+  float* pbase = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits + split) * a.heads) * (D + kGPH);
   const int rwk = a.rwk, rwv = a.rwv;
   if (pk->record_bytes != 4 * rwk || pv->record_bytes != 4 * rwv || pk->d != D || pv->d != D) {
     // caches of another record size than the parameter blocks: NaN outputs
-    if (tid < a.heads) pbase[(size_t)tid * (D + 4)] = NAN;
+    if (tid < a.heads) pbase[(size_t)tid * (D + kGPH)] = NAN;
     return;
   }
   const int rsk = rwk + 1, rsv = rwv + 1;           // LDS row strides (one padding dword)
@@ -464,12 +464,12 @@ __global__ __launch_bounds__(kGThreads) void group_split_kernel(GroupDecodeArgs 
       const float sc = vb[i] > 0 ? ldexpf(pv->s[c], 1 - vb[i]) : 0.f;
 #pragma unroll
       for (int h = 0; h < NQ; ++h)
-        if (h < a.heads) pbase[(size_t)h * (D + 4) + 4 + c] = acc[h][i] * sc;
+        if (h < a.heads) pbase[(size_t)h * (D + kGPH) + kGPH + c] = acc[h][i] * sc;
     }
   }
   if (tid < a.heads) {
-    pbase[(size_t)tid * (D + 4)] = m_run[tid];
-    pbase[(size_t)tid * (D + 4) + 1] = l_run[tid];
+    pbase[(size_t)tid * (D + kGPH)] = m_run[tid];
+    pbase[(size_t)tid * (D + kGPH) + 1] = l_run[tid];
   }
 }
 
@@ -499,10 +499,10 @@ __device__ inline void group_split_wide_body(const GroupDecodeArgs& a) {
   const int nt = min(len, s0 + kGSplit) - s0;
   const GroupParams* pk = group_params(a.params_k, g);
   const GroupParams* pv = group_params(a.params_v, g);
-  float* pbase = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits + split) * a.heads) * (D + 4);
+  float* pbase = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits + split) * a.heads) * (D + kGPH);
   const int rwk = a.rwk, rwv = a.rwv;
   if (pk->record_bytes != 4 * rwk || pv->record_bytes != 4 * rwv || pk->d != D || pv->d != D) {
-    if (tid < a.heads) pbase[(size_t)tid * (D + 4)] = NAN;
+    if (tid < a.heads) pbase[(size_t)tid * (D + kGPH)] = NAN;
     return;
   }
   const int rs = max(rwk, rwv) + 1;                 // LDS row stride (one padding dword)
@@ -638,12 +638,12 @@ __device__ inline void group_split_wide_body(const GroupDecodeArgs& a) {
       const float sc = vb[i] > 0 ? ldexpf(pv->s[c], 1 - vb[i]) : 0.f;
 #pragma unroll
       for (int h = 0; h < NQ; ++h)
-        if (h < a.heads) pbase[(size_t)h * (D + 4) + 4 + c] = acc[h][i] * sc;
+        if (h < a.heads) pbase[(size_t)h * (D + kGPH) + kGPH + c] = acc[h][i] * sc;
     }
   }
   if (tid < a.heads) {
-    pbase[(size_t)tid * (D + 4)] = mh[tid];
-    pbase[(size_t)tid * (D + 4) + 1] = lh[tid];
+    pbase[(size_t)tid * (D + kGPH)] = mh[tid];
+    pbase[(size_t)tid * (D + kGPH) + 1] = lh[tid];
   }
 }
 
@@ -798,10 +798,10 @@ __global__ __launch_bounds__(kGWideThreads) void group_split_mfma_kernel(GroupDe
     return;
   }
   const int nt = min(len, s0 + kGSplit) - s0;
-  float* pbase = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits + split) * a.heads) * (D + 4);
+  float* pbase = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits + split) * a.heads) * (D + kGPH);
   const int rwk = a.rwk, rwv = a.rwv;
   if (pk->record_bytes != 4 * rwk || pv->record_bytes != 4 * rwv || pk->d != D || pv->d != D) {
-    if (tid < a.heads) pbase[(size_t)tid * (D + 4)] = NAN;
+    if (tid < a.heads) pbase[(size_t)tid * (D + kGPH)] = NAN;
     return;
   }
   const int rs = max(rwk, rwv) + 1;                 // LDS row stride (one padding dword)
@@ -1027,13 +1027,13 @@ __global__ __launch_bounds__(kGWideThreads) void group_split_mfma_kernel(GroupDe
       const int h = 4 * kg + i;
       if (h < a.heads) {
         const float o = ldexpf(acc[i], -pe) + (mr_v ? 0.5f * ph_sum[h] : 0.f);
-        pbase[(size_t)h * (D + 4) + 4 + c] = o * sc;
+        pbase[(size_t)h * (D + kGPH) + kGPH + c] = o * sc;
       }
     }
   }
   if (tid < a.heads) {
-    pbase[(size_t)tid * (D + 4)] = mh[tid];
-    pbase[(size_t)tid * (D + 4) + 1] = lh[tid];
+    pbase[(size_t)tid * (D + kGPH)] = mh[tid];
+    pbase[(size_t)tid * (D + kGPH) + 1] = lh[tid];
   }
 }
 
@@ -1066,8 +1066,8 @@ __global__ __launch_bounds__(kGMergeThreads) void group_merge_sum_kernel(GroupDe
     return;
   }
   const int ns = (len + kGSplit - 1) / kGSplit;
-  const float* pb = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits) * a.heads + hl) * (D + 4);
-  const size_t sstride = (size_t)a.heads * (D + 4);
+  const float* pb = a.part + ((((size_t)b * a.n_groups + g) * a.n_splits) * a.heads + hl) * (D + kGPH);
+  const size_t sstride = (size_t)a.heads * (D + kGPH);
   float mx = -INFINITY;
   for (int s = tid; s < ns; s += NT) {
     const float ms = pb[s * sstride];
@@ -1104,7 +1104,7 @@ __global__ __launch_bounds__(kGMergeThreads) void group_merge_sum_kernel(GroupDe
     __syncthreads();
     for (int w = 0; w < NW; ++w) L += red[w];
     const int lo = n * sub / NSUB, hi = n * (sub + 1) / NSUB;
-    const float* p = pb + 4 + 64 * ci + c + (size_t)s0 * sstride;
+    const float* p = pb + kGPH + 64 * ci + c + (size_t)s0 * sstride;
     float a0 = 0.f, a1 = 0.f;
     int s = lo;
     for (; s + 8 <= hi; s += 8) {
